@@ -1,0 +1,235 @@
+"""ctypes wrapper around the CPU oracle (mtref.c).
+
+TEST INFRASTRUCTURE ONLY: imported by the tests, the smoke check and the
+benchmark's CPU-baseline leg.  Needs numpy only; it never imports the GPU
+package, and the GPU package never imports it.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import subprocess
+from typing import Dict, Optional
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(HERE, "mtref.c")
+LIB = os.path.join(HERE, "libmtref.so")
+
+_f = C.POINTER(C.c_float)
+_d = C.POINTER(C.c_double)
+_i = C.POINTER(C.c_int32)
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (-O2, no fast-math, single-threaded)."""
+    if force or not os.path.exists(LIB):
+        tmp = LIB + ".tmp"
+        subprocess.check_call(
+            ["gcc", "-O2", "-std=c11", "-Wall", "-Wextra", "-fno-fast-math", "-shared", "-fPIC",
+             "-o", tmp, SRC, "-lm"]
+        )
+        os.replace(tmp, LIB)
+    return LIB
+
+
+class _Dims(C.Structure):
+    _fields_ = [("E", C.c_int32), ("H", C.c_int32), ("A", C.c_int32), ("V", C.c_int32),
+                ("layer_norm", C.c_int32), ("tied_output", C.c_int32), ("ln_eps", C.c_double)]
+
+
+_WNAMES = ["emb", "W1", "U1", "b1", "Ua", "ba", "Wa", "va", "W2", "U2", "b2",
+           "Wt_s", "Wt_y", "Wt_c", "bt", "Wo", "bo", "Wi", "bi",
+           "g1a", "be1a", "g1u", "be1u", "g2a", "be2a", "g2u", "be2u", "gt", "bet"]
+
+
+class _Weights(C.Structure):
+    _fields_ = [(n, _f) for n in _WNAMES]
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB):
+            build()
+        L = C.CDLL(LIB)
+        L.mtref_layer_norm.argtypes = [C.c_int, _d, _f, _f, C.c_double, _d]
+        L.mtref_layer_norm.restype = None
+        L.mtref_gru.argtypes = [C.c_int, C.c_int, _d, _d, _f, _f, _f, _f, _f, _f, _f, C.c_double, _d]
+        L.mtref_gru.restype = None
+        L.mtref_attention.argtypes = [C.c_int, C.c_int, C.c_int, _d, _f, _f, _f, _f, _d, _d]
+        L.mtref_attention.restype = None
+        L.mtref_log_softmax.argtypes = [C.c_int, _d, _d]
+        L.mtref_log_softmax.restype = C.c_double
+        L.mtref_precompute.argtypes = [C.POINTER(_Dims), C.POINTER(_Weights), C.c_int, C.c_int,
+                                       _f, _f, _f, _f]
+        L.mtref_precompute.restype = C.c_int
+        L.mtref_step.argtypes = [C.POINTER(_Dims), C.POINTER(_Weights), C.c_int, C.c_int, C.c_int,
+                                 _i, _i, C.c_int, _f, _f, _f, _f, _f, _f, _f, _f, _f, _f]
+        L.mtref_step.restype = C.c_int
+        L.mtref_topk.argtypes = [C.c_int, C.c_int, C.c_int, _f, _f, _i, _i, _f]
+        L.mtref_topk.restype = C.c_int
+        _lib = L
+    return _lib
+
+
+def _fp(a: Optional[np.ndarray]):
+    if a is None:
+        return None
+    assert a.dtype == np.float32 and a.flags.c_contiguous
+    return a.ctypes.data_as(_f)
+
+
+def _dp(a: np.ndarray):
+    assert a.dtype == np.float64 and a.flags.c_contiguous
+    return a.ctypes.data_as(_d)
+
+
+def _ip(a: np.ndarray):
+    assert a.dtype == np.int32 and a.flags.c_contiguous
+    return a.ctypes.data_as(_i)
+
+
+def f32(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.float32)
+
+
+def f64(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+# ---- stage functions -----------------------------------------------------------
+
+
+def layer_norm(x, gamma, beta, eps=1e-5) -> np.ndarray:
+    x = f64(x)
+    y = np.empty_like(x)
+    lib().mtref_layer_norm(x.size, _dp(x), _fp(f32(gamma)), _fp(f32(beta)), eps, _dp(y))
+    return y
+
+
+def gru(x, h, W, U, b, ln=None, eps=1e-5) -> np.ndarray:
+    """ln: None or (gamma_a, beta_a, gamma_u, beta_u), each [3H]."""
+    x, h = f64(x), f64(h)
+    W, U, b = f32(W), f32(U), f32(b)
+    H = h.size
+    assert W.shape == (x.size, 3 * H) and U.shape == (H, 3 * H) and b.shape == (3 * H,)
+    out = np.empty(H, np.float64)
+    lnp = [None] * 4 if ln is None else [f32(t) for t in ln]
+    lib().mtref_gru(x.size, H, _dp(x), _dp(h), _fp(W), _fp(U), _fp(b),
+                    *[_fp(t) for t in lnp], eps, _dp(out))
+    return out
+
+
+def attention(q, P, Cx, mask, va):
+    q, P, Cx, mask, va = f64(q), f32(P), f32(Cx), f32(mask), f32(va)
+    S, A = P.shape
+    Cd = Cx.shape[1]
+    alpha = np.empty(S, np.float64)
+    ctx = np.empty(Cd, np.float64)
+    lib().mtref_attention(S, A, Cd, _dp(q), _fp(P), _fp(Cx), _fp(mask), _fp(va), _dp(alpha), _dp(ctx))
+    return alpha, ctx
+
+
+def log_softmax(l):
+    l = f64(l)
+    out = np.empty_like(l)
+    lse = lib().mtref_log_softmax(l.size, _dp(l), _dp(out))
+    return out, lse
+
+
+# ---- model ----------------------------------------------------------------------
+
+
+class Model:
+    """Holds the fp32 weights (row-major logical [in x out]) and the dims."""
+
+    def __init__(self, E: int, H: int, A: int, V: int, weights: Dict[str, np.ndarray],
+                 layer_norm: bool = False, tied_output: bool = False, ln_eps: float = 1e-5):
+        self.E, self.H, self.A, self.V = E, H, A, V
+        self.C = 2 * H
+        self.dims = _Dims(E, H, A, V, int(layer_norm), int(tied_output), ln_eps)
+        self._keep = {}
+        shapes = {
+            "emb": (V, E), "W1": (E, 3 * H), "U1": (H, 3 * H), "b1": (3 * H,),
+            "Ua": (2 * H, A), "ba": (A,), "Wa": (H, A), "va": (A,),
+            "W2": (2 * H, 3 * H), "U2": (H, 3 * H), "b2": (3 * H,),
+            "Wt_s": (H, E), "Wt_y": (E, E), "Wt_c": (2 * H, E), "bt": (E,),
+            "Wo": (E, V), "bo": (V,), "Wi": (2 * H, H), "bi": (H,),
+        }
+        for n in ("g1a", "be1a", "g1u", "be1u", "g2a", "be2a", "g2u", "be2u"):
+            shapes[n] = (3 * H,)
+        shapes["gt"] = (E,)
+        shapes["bet"] = (E,)
+        ptrs = {}
+        for n in _WNAMES:
+            a = weights.get(n)
+            if a is None:
+                if n in ("g1a", "be1a", "g1u", "be1u", "g2a", "be2a", "g2u", "be2u", "gt", "bet") and not layer_norm:
+                    ptrs[n] = None
+                    continue
+                if n == "Wo" and tied_output:
+                    ptrs[n] = None
+                    continue
+                raise KeyError(n)
+            a = f32(a)
+            if a.shape != shapes[n]:
+                raise ValueError(f"{n}: shape {a.shape} != {shapes[n]}")
+            self._keep[n] = a
+            ptrs[n] = _fp(a)
+        self.w = _Weights(**{n: p for n, p in ptrs.items() if p is not None})
+
+    def precompute(self, ctx, mask):
+        ctx, mask = f32(ctx), f32(mask)
+        B, S, Cd = ctx.shape
+        assert Cd == self.C and mask.shape == (B, S)
+        P = np.empty((B, S, self.A), np.float32)
+        s0 = np.empty((B, self.H), np.float32)
+        rc = lib().mtref_precompute(C.byref(self.dims), C.byref(self.w), B, S, _fp(ctx), _fp(mask),
+                                    _fp(P), _fp(s0))
+        if rc != 0:
+            raise ValueError(f"mtref_precompute: {rc}")
+        return P, s0
+
+    def step(self, K, prev_tok, src_row, state_in, ctx, P, mask, want_logp=True,
+             want_alpha=False, taps=False):
+        ctx, P, mask, state_in = f32(ctx), f32(P), f32(mask), f32(state_in)
+        prev_tok = np.ascontiguousarray(prev_tok, np.int32)
+        src_row = np.ascontiguousarray(src_row, np.int32)
+        B, S, _ = ctx.shape
+        M = B * K
+        assert prev_tok.shape == (M,) and src_row.shape == (M,)
+        out = {"state": np.empty((M, self.H), np.float32)}
+        if want_logp:
+            out["logp"] = np.empty((M, self.V), np.float32)
+        if want_alpha:
+            out["alpha"] = np.empty((M, S), np.float32)
+        if taps:
+            out["s1"] = np.empty((M, self.H), np.float32)
+            out["c"] = np.empty((M, self.C), np.float32)
+            out["t"] = np.empty((M, self.E), np.float32)
+        rc = lib().mtref_step(
+            C.byref(self.dims), C.byref(self.w), B, K, S, _ip(prev_tok), _ip(src_row),
+            state_in.shape[0], _fp(state_in), _fp(ctx), _fp(P), _fp(mask), _fp(out["state"]),
+            _fp(out.get("logp")), _fp(out.get("alpha")), _fp(out.get("s1")), _fp(out.get("c")),
+            _fp(out.get("t")))
+        if rc != 0:
+            raise ValueError(f"mtref_step: {rc}")
+        return out
+
+
+def topk(K, prev_score, logp):
+    prev_score, logp = f32(prev_score), f32(logp)
+    M, V = logp.shape
+    B = M // K
+    tok = np.empty(M, np.int32)
+    bp = np.empty(M, np.int32)
+    sc = np.empty(M, np.float32)
+    rc = lib().mtref_topk(B, K, V, _fp(prev_score), _fp(logp), _ip(tok), _ip(bp), _fp(sc))
+    if rc != 0:
+        raise ValueError(f"mtref_topk: {rc}")
+    return tok, bp, sc

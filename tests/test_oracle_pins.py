@@ -1,0 +1,530 @@
+"""Pins for the CPU oracle: checks against what the mathematics and the paper fix.
+
+Each test ties one part of the oracle to something other than itself:
+library routines it must reduce to (torch.nn.GRUCell, F.layer_norm,
+log_softmax), closed forms, invariants (normalisation, masking, scale and
+permutation invariance, sentence independence), brute force on tiny inputs,
+and the attention rows the paper prints in Figure 2.
+"""
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+from oracle import mtref
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+rng0 = np.random.default_rng(1804)
+
+
+def rnd(*shape, s=1.0, rng=rng0):
+    return (rng.standard_normal(shape) * s).astype(np.float32)
+
+
+# --------------------------------------------------------------------------------------
+# GRU block: reduction to torch.nn.GRUCell (PyTorch's documented r, z, n equations with
+# the reset gate applied to the recurrent product, h' = (1 - z) n + z h)
+# --------------------------------------------------------------------------------------
+
+
+def torch_gru(x, h, W, U, b):
+    H = h.size
+    cell = torch.nn.GRUCell(x.size, H, bias=True).double()
+    with torch.no_grad():
+        cell.weight_ih.copy_(torch.from_numpy(W.astype(np.float64).T))
+        cell.weight_hh.copy_(torch.from_numpy(U.astype(np.float64).T))
+        cell.bias_ih.copy_(torch.from_numpy(b.astype(np.float64)))
+        cell.bias_hh.zero_()
+        out = cell(torch.from_numpy(x.astype(np.float64))[None], torch.from_numpy(h.astype(np.float64))[None])
+    return out[0].numpy()
+
+
+@pytest.mark.parametrize("in_dim,H", [(7, 5), (3, 9), (16, 16)])
+def test_gru_equals_torch_grucell(in_dim, H):
+    rng = np.random.default_rng(in_dim * 100 + H)
+    x, h = rnd(in_dim, rng=rng), np.tanh(rnd(H, rng=rng))
+    W, U, b = rnd(in_dim, 3 * H, s=0.7, rng=rng), rnd(H, 3 * H, s=0.7, rng=rng), rnd(3 * H, s=0.3, rng=rng)
+    got = mtref.gru(x, h, W, U, b)
+    ref = torch_gru(x, h, W, U, b)
+    assert np.max(np.abs(got - ref)) <= 1e-12
+
+
+def test_gru_closed_forms():
+    rng = np.random.default_rng(5)
+    in_dim, H = 6, 4
+    x, h = rnd(in_dim, rng=rng), np.tanh(rnd(H, rng=rng))
+    b = rnd(3 * H, rng=rng)
+    # all weights zero, b_z = 0 -> z = 1/2, hh = tanh(b_h): s = (tanh(b_h) + h) / 2
+    bz = b.copy()
+    bz[H:2 * H] = 0
+    s = mtref.gru(x, h, np.zeros((in_dim, 3 * H), np.float32), np.zeros((H, 3 * H), np.float32), bz)
+    assert np.max(np.abs(s - 0.5 * (np.tanh(bz[2 * H:].astype(np.float64)) + h))) <= 1e-15
+    # b_z = +40: the update gate keeps the old state
+    W, U = rnd(in_dim, 3 * H, s=0.3, rng=rng), rnd(H, 3 * H, s=0.3, rng=rng)
+    bc = b.copy()
+    bc[H:2 * H] = 40.0
+    assert np.max(np.abs(mtref.gru(x, h, W, U, bc) - h)) <= 1e-15
+    # b_z = -40 and U_h = 0: the state becomes tanh(x W_h + b_h)
+    bn = b.copy()
+    bn[H:2 * H] = -40.0
+    U0 = U.copy()
+    U0[:, 2 * H:] = 0
+    want = np.tanh(x.astype(np.float64) @ W[:, 2 * H:].astype(np.float64) + bn[2 * H:])
+    assert np.max(np.abs(mtref.gru(x, h, W, U0, bn) - want)) <= 1e-15
+
+
+# --------------------------------------------------------------------------------------
+# layer normalisation
+# --------------------------------------------------------------------------------------
+
+
+@pytest.mark.parametrize("n", [1, 5, 64, 1000])
+def test_layer_norm_equals_torch(n):
+    rng = np.random.default_rng(n)
+    x = rng.standard_normal(n) * 3 + 1.5
+    g, b = rnd(n, rng=rng), rnd(n, rng=rng)
+    got = mtref.layer_norm(x, g, b, 1e-5)
+    ref = F.layer_norm(torch.from_numpy(x)[None], (n,), torch.from_numpy(g.astype(np.float64)),
+                       torch.from_numpy(b.astype(np.float64)), eps=1e-5)[0].numpy()
+    assert np.max(np.abs(got - ref)) <= 1e-12
+
+
+def test_layer_norm_closed_forms():
+    n = 37
+    g, b = rnd(n), rnd(n)
+    # constant input: x - mean = 0 exactly, output = beta
+    assert np.array_equal(mtref.layer_norm(np.full(n, 2.75), g, b), b.astype(np.float64))
+    # unit gain, zero shift: mean 0 and variance var/(var + eps)
+    x = np.random.default_rng(3).standard_normal(n) * 0.01
+    y = mtref.layer_norm(x, np.ones(n, np.float32), np.zeros(n, np.float32), 1e-5)
+    var = x.var()
+    assert abs(y.mean()) <= 1e-12
+    assert abs(y.var() - var / (var + 1e-5)) <= 1e-12
+
+
+def test_ln_gru_gain_zero_gives_shifts_only():
+    """gamma = 0 on every LN instance: each normalised block equals its shift beta,
+    so the gates depend on the betas only (a check of which beta feeds which gate)."""
+    rng = np.random.default_rng(11)
+    in_dim, H = 5, 3
+    x, h = rnd(in_dim, rng=rng), np.tanh(rnd(H, rng=rng))
+    W, U, b = rnd(in_dim, 3 * H, rng=rng), rnd(H, 3 * H, rng=rng), rnd(3 * H, rng=rng)
+    ba, bu = rnd(3 * H, rng=rng).astype(np.float64), rnd(3 * H, rng=rng).astype(np.float64)
+    z0 = np.zeros(3 * H, np.float32)
+    s = mtref.gru(x, h, W, U, b, ln=(z0, ba.astype(np.float32), z0, bu.astype(np.float32)))
+    sig = lambda v: 1 / (1 + np.exp(-v))
+    r = sig(ba[:H] + bu[:H])
+    z = sig(ba[H:2 * H] + bu[H:2 * H])
+    hh = np.tanh(ba[2 * H:] + r * bu[2 * H:])
+    assert np.max(np.abs(s - ((1 - z) * hh + z * h))) <= 1e-15
+
+
+def test_ln_gru_scale_invariance():
+    """LN on each H-block of each path makes the block invariant to a positive
+    rescaling of that block's weights (exact up to eps)."""
+    rng = np.random.default_rng(12)
+    in_dim, H = 8, 6
+    x, h = rnd(in_dim, rng=rng), np.tanh(rnd(H, rng=rng))
+    W, U, b = rnd(in_dim, 3 * H, rng=rng), rnd(H, 3 * H, rng=rng), rnd(3 * H, rng=rng)
+    ln = tuple(rnd(3 * H, rng=rng) for _ in range(4))
+    base = mtref.gru(x, h, W, U, b, ln=ln, eps=1e-12)
+    for g in range(3):
+        U2 = U.copy()
+        U2[:, g * H:(g + 1) * H] *= 4.0  # powers of two: the scaled fp32 weights are exact
+        W2, b2 = W.copy(), b.copy()
+        W2[:, g * H:(g + 1) * H] *= 0.25
+        b2[g * H:(g + 1) * H] *= 0.25
+        assert np.max(np.abs(mtref.gru(x, h, W2, U2, b2, ln=ln, eps=1e-12) - base)) <= 1e-12
+    # a scaling that mixes blocks is NOT an invariance (LN must be per block)
+    U3 = U.copy()
+    U3[:, :H] *= 3.5
+    U3[:, H:] *= 1.0
+    W3 = W.copy()
+    W3[:, H] *= 5.0
+    assert np.max(np.abs(mtref.gru(x, h, W3, U3, b, ln=ln, eps=1e-12) - base)) > 1e-6
+
+
+# --------------------------------------------------------------------------------------
+# attention
+# --------------------------------------------------------------------------------------
+
+
+def attn_case(S=9, A=6, Cd=10, lens=5, seed=0):
+    rng = np.random.default_rng(seed)
+    q = rng.standard_normal(A)
+    P, Cx = rnd(S, A, rng=rng), rnd(S, Cd, rng=rng)
+    mask = (np.arange(S) < lens).astype(np.float32)
+    va = rnd(A, rng=rng)
+    return q, P, Cx, mask, va
+
+
+@pytest.mark.parametrize("L", [1, 2, 5, 9])
+def test_attention_normalised_and_masked(L):
+    q, P, Cx, mask, va = attn_case(lens=L, seed=L)
+    P[L:] = np.nan
+    Cx[L:] = np.nan
+    alpha, ctx = mtref.attention(q, P, Cx, mask, va)
+    assert abs(alpha.sum() - 1.0) <= 1e-12
+    assert np.all(alpha[L:] == 0.0) and np.all(np.isfinite(ctx))
+    assert np.all(alpha[:L] > 0)
+    if L == 1:
+        assert alpha[0] == 1.0
+        assert np.array_equal(ctx, Cx[0].astype(np.float64))
+
+
+def test_attention_zero_va_is_uniform_mean():
+    q, P, Cx, mask, va = attn_case(lens=6, seed=3)
+    alpha, ctx = mtref.attention(q, P, Cx, mask, np.zeros_like(va))
+    assert np.max(np.abs(alpha[:6] - 1 / 6)) <= 1e-15
+    assert np.max(np.abs(ctx - Cx[:6].astype(np.float64).mean(0))) <= 1e-13
+
+
+def test_attention_one_dim_reduces_to_softmax():
+    """A = 1, va = 1: the scores are tanh(P_i + q) and alpha is scipy's softmax of them."""
+    from scipy.special import softmax
+    S = 11
+    rng = np.random.default_rng(4)
+    P = rnd(S, 1, rng=rng)
+    q = np.array([0.3])
+    mask = np.ones(S, np.float32)
+    mask[[2, 7]] = 0  # not a prefix: positions 2 and 7 masked
+    Cx = rnd(S, 3, rng=rng)
+    alpha, ctx = mtref.attention(q, P, Cx, mask, np.ones(1, np.float32))
+    keep = mask != 0
+    e = np.tanh(P[keep, 0].astype(np.float64) + 0.3)
+    assert np.max(np.abs(alpha[keep] - softmax(e))) <= 1e-15
+    assert np.all(alpha[~keep] == 0)
+    assert np.max(np.abs(ctx - softmax(e) @ Cx[keep].astype(np.float64))) <= 1e-14
+
+
+def test_attention_all_masked_is_zero():
+    q, P, Cx, mask, va = attn_case(lens=0, seed=5)
+    alpha, ctx = mtref.attention(q, P, Cx, mask, va)
+    assert np.all(alpha == 0) and np.all(ctx == 0)
+
+
+def _load_fig2(name):
+    rows = [l for l in open(os.path.join(GOLD, name)) if l[0].isdigit()]
+    xs, ys, vs = zip(*[(int(a), int(b), float(c)) for a, b, c in (r.strip().split(",") for r in rows)])
+    X, Y = max(xs) + 1, max(ys) + 1
+    m = np.zeros((Y, X))
+    for x, y, v in zip(xs, ys, vs):
+        m[y, x] = v
+    return m
+
+
+@pytest.mark.parametrize("name", ["fig2_mt_to_pe_attention.csv", "fig2_src_to_pe_attention.csv"])
+def test_attention_reproduces_paper_figure2_rows(name):
+    """Figure 2 prints attention rows of a trained model to 4 decimals.
+
+    Witness: every printed row sums to 1 within the rounding bound n * 5e-5.
+    Reproduction: with A = 1 and keys chosen so that each score equals the log
+    of the printed weight, the oracle's masked softmax returns the printed row
+    (within rounding and the row's renormalisation)."""
+    m = _load_fig2(name)
+    n = m.shape[1]
+    assert np.all(np.abs(m.sum(1) - 1.0) <= n * 5e-5)
+    for row in m:
+        logs = np.log(np.maximum(row, 2.5e-5))
+        w = 2.0 * np.max(np.abs(logs - logs.mean()))
+        P = np.arctanh((logs - logs.mean()) / w).astype(np.float32)[:, None]
+        Cx = np.eye(n, dtype=np.float32)
+        alpha, ctx = mtref.attention(np.zeros(1), P, Cx, np.ones(n, np.float32), np.array([w], np.float32))
+        assert np.max(np.abs(alpha - row)) <= n * 5e-5 + 1e-4
+        assert np.max(np.abs(ctx - alpha)) == 0.0  # identity context returns alpha itself
+
+
+# --------------------------------------------------------------------------------------
+# log-softmax
+# --------------------------------------------------------------------------------------
+
+
+@pytest.mark.parametrize("n", [1, 2, 1000, 50000])
+def test_log_softmax(n):
+    l = np.random.default_rng(n).standard_normal(n) * 5
+    out, lse = mtref.log_softmax(l)
+    assert abs(np.log(np.exp(out).sum())) <= 1e-12
+    ref = torch.log_softmax(torch.from_numpy(l), 0).numpy()
+    assert np.max(np.abs(out - ref)) <= 1e-12
+    assert abs(lse - torch.logsumexp(torch.from_numpy(l), 0).item()) <= 1e-12
+
+
+# --------------------------------------------------------------------------------------
+# top-K beam selection: brute force
+# --------------------------------------------------------------------------------------
+
+
+def brute_topk(K, score, logp):
+    M, V = logp.shape
+    B = M // K
+    tok, bp, sc = [], [], []
+    for b in range(B):
+        c = []
+        for k in range(K):
+            for v in range(V):
+                c.append((-float(np.float32(score[b * K + k]) + np.float32(logp[b * K + k, v])), k * V + v))
+        c.sort()
+        for j in range(K):
+            tok.append(c[j][1] % V)
+            bp.append(c[j][1] // V)
+            sc.append(np.float32(score[b * K + bp[-1]]) + np.float32(logp[b * K + bp[-1], tok[-1]]))
+    return np.array(tok), np.array(bp), np.array(sc, np.float32)
+
+
+@pytest.mark.parametrize("K", [1, 2, 3, 4])
+@pytest.mark.parametrize("V", [4, 7, 20])
+def test_topk_brute_force_with_ties(K, V):
+    if V < K:
+        pytest.skip("K > V")
+    rng = np.random.default_rng(K * 31 + V)
+    B = 3
+    logp = rng.choice(np.array([-1.0, -2.0, -2.5, -3.0], np.float32), size=(B * K, V))
+    score = rng.choice(np.array([0.0, -0.5, -1.0], np.float32), size=B * K)
+    tok, bp, sc = mtref.topk(K, score, logp)
+    t2, b2, s2 = brute_topk(K, score, logp)
+    assert np.array_equal(tok, t2) and np.array_equal(bp, b2) and np.array_equal(sc, s2)
+
+
+def test_topk_random_v1000():
+    K, B, V = 4, 2, 1000
+    rng = np.random.default_rng(9)
+    logp = rnd(B * K, V, rng=rng)
+    score = rnd(B * K, rng=rng)
+    tok, bp, sc = mtref.topk(K, score, logp)
+    t2, b2, s2 = brute_topk(K, score, logp)
+    assert np.array_equal(tok, t2) and np.array_equal(bp, b2) and np.array_equal(sc, s2)
+
+
+def test_topk_k1_is_argmax_smallest_index():
+    logp = np.array([[0.5, 2.0, 2.0, 1.0], [3.0, -1.0, 3.0, 3.0]], np.float32)
+    tok, bp, sc = mtref.topk(1, np.zeros(2, np.float32), logp)
+    assert tok.tolist() == [1, 0] and bp.tolist() == [0, 0]
+    assert np.array_equal(tok, np.argmax(logp, axis=1))  # numpy argmax takes the first maximum
+
+
+def test_topk_bos_start_draws_from_hyp0():
+    K, V = 4, 50
+    rng = np.random.default_rng(2)
+    logp = rnd(K, V, rng=rng)
+    score = np.array([0, -np.inf, -np.inf, -np.inf], np.float32)
+    tok, bp, sc = mtref.topk(K, score, logp)
+    assert np.all(bp == 0)
+    assert len(set(tok.tolist())) == K
+    assert np.array_equal(tok, np.argsort(-logp[0], kind="stable")[:K])
+
+
+# --------------------------------------------------------------------------------------
+# whole step and precompute
+# --------------------------------------------------------------------------------------
+
+E_, H_, A_, V_ = 6, 5, 7, 23
+
+
+def tiny_model(seed=0, layer_norm=False, **over):
+    rng = np.random.default_rng(seed)
+    E, H, A, V, C = E_, H_, A_, V_, 2 * H_
+    w = dict(
+        emb=rnd(V, E, s=0.5, rng=rng), W1=rnd(E, 3 * H, s=0.5, rng=rng), U1=rnd(H, 3 * H, s=0.5, rng=rng),
+        b1=rnd(3 * H, s=0.1, rng=rng), Ua=rnd(C, A, s=0.4, rng=rng), ba=rnd(A, s=0.1, rng=rng),
+        Wa=rnd(H, A, s=0.5, rng=rng), va=rnd(A, rng=rng), W2=rnd(C, 3 * H, s=0.4, rng=rng),
+        U2=rnd(H, 3 * H, s=0.5, rng=rng), b2=rnd(3 * H, s=0.1, rng=rng), Wt_s=rnd(H, E, s=0.5, rng=rng),
+        Wt_y=rnd(E, E, s=0.5, rng=rng), Wt_c=rnd(C, E, s=0.4, rng=rng), bt=rnd(E, s=0.1, rng=rng),
+        Wo=rnd(E, V, rng=rng), bo=rnd(V, s=0.2, rng=rng), Wi=rnd(C, H, s=0.4, rng=rng), bi=rnd(H, s=0.1, rng=rng))
+    if layer_norm:
+        for n in ("g1a", "g1u", "g2a", "g2u"):
+            w[n] = (1 + rnd(3 * H, s=0.1, rng=rng)).astype(np.float32)
+        for n in ("be1a", "be1u", "be2a", "be2u"):
+            w[n] = rnd(3 * H, s=0.1, rng=rng)
+        w["gt"] = (1 + rnd(E, s=0.1, rng=rng)).astype(np.float32)
+        w["bet"] = rnd(E, s=0.1, rng=rng)
+    w.update(over)
+    return mtref.Model(E, H, A, V, w, layer_norm=layer_norm), w
+
+
+def tiny_batch(B=3, K=2, S=6, seed=1, lens=None):
+    rng = np.random.default_rng(seed)
+    C = 2 * H_
+    lens = np.array(lens if lens is not None else rng.integers(1, S + 1, size=B))
+    ctx = rnd(B, S, C, rng=rng)
+    mask = (np.arange(S)[None] < lens[:, None]).astype(np.float32)
+    M = B * K
+    tok = rng.integers(0, V_, size=M).astype(np.int32)
+    src = ((np.arange(M) // K) * K + rng.integers(0, K, size=M)).astype(np.int32)
+    state = np.tanh(rnd(M, H_, rng=rng))
+    return ctx, mask, lens, tok, src, state
+
+
+def test_precompute_matches_library_matmul_and_masked_mean():
+    model, w = tiny_model()
+    ctx, mask, lens, *_ = tiny_batch(B=4, S=5, lens=[1, 5, 3, 2])
+    ctx[mask == 0] = np.nan  # padded positions must never be read
+    P, s0 = model.precompute(ctx, mask)
+    for b, L in enumerate(lens):
+        c = ctx[b, :L].astype(np.float64)
+        assert np.max(np.abs(P[b, :L] - (c @ w["Ua"].astype(np.float64) + w["ba"]))) <= 1e-6
+        want = np.tanh(c.mean(0) @ w["Wi"].astype(np.float64) + w["bi"])
+        assert np.max(np.abs(s0[b] - want)) <= 1e-6
+        assert np.all(P[b, L:] == 0)
+    assert np.all(np.isfinite(s0))
+
+
+def test_step_reduces_to_library_pieces_when_gru2_copies_and_readout_sees_x_only():
+    """b2_z = +40 makes GRU block 2 a copy (state_out = s1 = GRUCell(x, h));
+    Wt_s = Wt_c = 0 leaves logp = log_softmax(tanh(x Wt_y + bt) Wo + bo)."""
+    H, E, C = H_, E_, 2 * H_
+    b2 = np.zeros(3 * H, np.float32)
+    b2[H:2 * H] = 40.0
+    model, w = tiny_model(seed=4, b2=b2, Wt_s=np.zeros((H, E), np.float32), Wt_c=np.zeros((C, E), np.float32))
+    ctx, mask, lens, tok, src, state = tiny_batch(seed=5)
+    P, _ = model.precompute(ctx, mask)
+    out = model.step(2, tok, src, state, ctx, P, mask, taps=True)
+    for m in range(tok.size):
+        g = torch_gru(w["emb"][tok[m]], state[src[m]], w["W1"], w["U1"], w["b1"])
+        assert np.max(np.abs(out["s1"][m] - g)) <= 1e-6
+        assert np.max(np.abs(out["state"][m] - out["s1"][m])) <= 1e-7
+        x = torch.from_numpy(w["emb"][tok[m]].astype(np.float64))
+        t = torch.tanh(x @ torch.from_numpy(w["Wt_y"].astype(np.float64)) + torch.from_numpy(w["bt"].astype(np.float64)))
+        ref = torch.log_softmax(t @ torch.from_numpy(w["Wo"].astype(np.float64)) + torch.from_numpy(w["bo"].astype(np.float64)), 0)
+        assert np.max(np.abs(out["logp"][m] - ref.numpy())) <= 2e-6
+
+
+def test_step_zero_va_gives_masked_mean_context():
+    model, w = tiny_model(seed=6, va=np.zeros(A_, np.float32))
+    ctx, mask, lens, tok, src, state = tiny_batch(seed=7)
+    P, _ = model.precompute(ctx, mask)
+    out = model.step(2, tok, src, state, ctx, P, mask, want_alpha=True, taps=True)
+    for m in range(tok.size):
+        b = m // 2
+        L = lens[b]
+        assert np.allclose(out["alpha"][m, :L], 1.0 / L, atol=1e-7, rtol=0)
+        assert np.all(out["alpha"][m, L:] == 0)
+        assert np.max(np.abs(out["c"][m] - ctx[b, :L].astype(np.float64).mean(0))) <= 1e-6
+
+
+def test_step_zero_wa_makes_attention_independent_of_state():
+    model, w = tiny_model(seed=8, Wa=np.zeros((H_, A_), np.float32))
+    ctx, mask, lens, tok, src, state = tiny_batch(seed=9)
+    P, _ = model.precompute(ctx, mask)
+    a1 = model.step(2, tok, src, state, ctx, P, mask, want_alpha=True)["alpha"]
+    a2 = model.step(2, tok, src, np.tanh(state * 3 + 1).astype(np.float32), ctx, P, mask, want_alpha=True)["alpha"]
+    assert np.array_equal(a1, a2)
+
+
+@pytest.mark.parametrize("layer_norm", [False, True])
+def test_step_invariants(layer_norm):
+    model, w = tiny_model(seed=10, layer_norm=layer_norm)
+    ctx, mask, lens, tok, src, state = tiny_batch(seed=11)
+    ctx[mask == 0] = np.nan
+    P, _ = model.precompute(ctx, mask)
+    out = model.step(2, tok, src, state, ctx, P, mask, want_alpha=True)
+    assert np.all(np.isfinite(out["state"])) and np.all(np.isfinite(out["logp"]))
+    assert np.max(np.abs(np.log(np.exp(out["logp"].astype(np.float64)).sum(1)))) <= 1e-6
+    assert np.max(np.abs(out["alpha"].sum(1) - 1)) <= 1e-6
+    for m in range(tok.size):
+        assert np.all(out["alpha"][m, lens[m // 2]:] == 0)
+    assert np.all(np.abs(out["state"]) < 1)
+
+
+def test_step_zero_output_layer_gives_uniform():
+    model, w = tiny_model(seed=12, Wo=np.zeros((E_, V_), np.float32), bo=np.zeros(V_, np.float32))
+    ctx, mask, lens, tok, src, state = tiny_batch(seed=13)
+    P, _ = model.precompute(ctx, mask)
+    out = model.step(2, tok, src, state, ctx, P, mask)
+    assert np.all(out["logp"] == np.float32(-math.log(V_)))
+
+
+def test_tied_output_equals_explicit_transpose():
+    model, w = tiny_model(seed=14)
+    w2 = dict(w)
+    w2["Wo"] = np.ascontiguousarray(w["emb"].T)
+    m_exp = mtref.Model(E_, H_, A_, V_, w2)
+    w3 = dict(w)
+    del w3["Wo"]
+    m_tied = mtref.Model(E_, H_, A_, V_, w3, tied_output=True)
+    ctx, mask, lens, tok, src, state = tiny_batch(seed=15)
+    P, _ = m_exp.precompute(ctx, mask)
+    a = m_exp.step(2, tok, src, state, ctx, P, mask)["logp"]
+    b = m_tied.step(2, tok, src, state, ctx, P, mask)["logp"]
+    assert np.array_equal(a, b)
+
+
+def test_sentence_independence():
+    model, w = tiny_model(seed=16, layer_norm=True)
+    ctx, mask, lens, tok, src, state = tiny_batch(B=3, K=2, seed=17)
+    P, _ = model.precompute(ctx, mask)
+    o1 = model.step(2, tok, src, state, ctx, P, mask, want_alpha=True)
+    ctx2, tok2, state2 = ctx.copy(), tok.copy(), state.copy()
+    ctx2[1:] = rnd(*ctx2[1:].shape)
+    tok2[2:] = (tok2[2:] + 5) % V_
+    state2[2:] = 0.3
+    P2, _ = model.precompute(ctx2, mask)
+    o2 = model.step(2, tok2, src, state2, ctx2, P2, mask, want_alpha=True)
+    for k in ("state", "logp", "alpha"):
+        assert np.array_equal(o1[k][:2], o2[k][:2])
+        assert not np.array_equal(o1[k][2:], o2[k][2:])
+
+
+def test_full_step_equals_torch_reexpression():
+    """Wiring check of the no-LN step against a float64 torch re-expression built on
+    torch.nn.GRUCell, masked softmax and log_softmax."""
+    model, w = tiny_model(seed=18)
+    ctx, mask, lens, tok, src, state = tiny_batch(seed=19)
+    P, _ = model.precompute(ctx, mask)
+    out = model.step(2, tok, src, state, ctx, P, mask, want_alpha=True)
+    T = lambda a: torch.from_numpy(np.asarray(a, np.float64))
+    for m in range(tok.size):
+        b = m // 2
+        x = w["emb"][tok[m]]
+        s1 = torch_gru(x, state[src[m]], w["W1"], w["U1"], w["b1"])
+        q = T(s1) @ T(w["Wa"])
+        e = torch.tanh(T(P[b]) + q) @ T(w["va"])
+        e = e.masked_fill(T(mask[b]) == 0, -math.inf)
+        al = torch.softmax(e, 0)
+        c = al @ T(ctx[b])
+        s = torch_gru(c.numpy(), s1, w["W2"], w["U2"], w["b2"])
+        t = torch.tanh(T(s) @ T(w["Wt_s"]) + T(x) @ T(w["Wt_y"]) + c @ T(w["Wt_c"]) + T(w["bt"]))
+        lp = torch.log_softmax(t @ T(w["Wo"]) + T(w["bo"]), 0)
+        assert np.max(np.abs(out["alpha"][m] - al.numpy())) <= 1e-6
+        assert np.max(np.abs(out["state"][m] - s)) <= 1e-6
+        assert np.max(np.abs(out["logp"][m] - lp.numpy())) <= 1e-5
+
+
+def test_beam_k1_equals_greedy_decoding():
+    model, w = tiny_model(seed=20, layer_norm=True)
+    ctx, mask, lens, *_ = tiny_batch(B=3, K=1, seed=21)
+    P, s0 = model.precompute(ctx, mask)
+    tok = np.ones(3, np.int32)
+    src = np.arange(3, dtype=np.int32)
+    st = s0
+    score = np.zeros(3, np.float32)
+    for _ in range(6):
+        out = model.step(1, tok, src, st, ctx, P, mask)
+        t, bp, sc = mtref.topk(1, score, out["logp"])
+        assert np.array_equal(t, np.argmax(out["logp"], 1))
+        assert np.all(bp == 0)
+        tok, st, score = t, out["state"], sc
+        src = np.arange(3, dtype=np.int32)
+
+
+def test_beam_permutation_invariance():
+    """Permuting the hypotheses of a sentence (with their states and scores) leaves
+    the selected (score, token, source state) multiset unchanged."""
+    model, w = tiny_model(seed=22)
+    K = 3
+    ctx, mask, lens, tok, src, state = tiny_batch(B=2, K=K, seed=23)
+    P, _ = model.precompute(ctx, mask)
+    rng = np.random.default_rng(24)
+    score = -rng.uniform(0, 3, size=2 * K).astype(np.float32)
+    out = model.step(K, tok, src, state, ctx, P, mask)
+    t1, b1, s1 = mtref.topk(K, score, out["logp"])
+    perm = np.concatenate([b * K + rng.permutation(K) for b in range(2)])
+    out2 = model.step(K, tok[perm], src[perm], state, ctx, P, mask)
+    t2, b2, s2 = mtref.topk(K, score[perm], out2["logp"])
+    for b in range(2):
+        sl = slice(b * K, (b + 1) * K)
+        a = sorted(zip(s1[sl].tolist(), t1[sl].tolist(), src[b * K + b1[sl]].tolist()))
+        c = sorted(zip(s2[sl].tolist(), t2[sl].tolist(), src[perm][b * K + b2[sl]].tolist()))
+        assert a == c
