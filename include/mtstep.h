@@ -1,0 +1,207 @@
+/*
+ * libmtstep — one batched beam-search step of a shallow attentional cGRU
+ * decoder on an AMD Instinct MI355X (gfx950), behind a plain C ABI.
+ *
+ * The calls follow the encoder/decoder interface of Marian (arXiv
+ * 1804.00344, Section 2.2): the encoder's output (context + mask, the
+ * EncoderState) is an input here; mt_precompute_ctx plays
+ * Decoder::startState (per-batch attention keys and the initial state);
+ * mt_decoder_step plays Decoder::step (next state and the log-probabilities
+ * over the target vocabulary); mt_beam_topk is the selection of the next
+ * hypotheses from the decoder state (Section 2.2, last paragraphs; batched
+ * beam search, Section 2.3).  The model is the shallow Nematus-compatible
+ * RNN of Section 1 / Table 2 ("Shallow RNN"): conditional GRU with fused
+ * gates and optional layer normalisation (Section 2.1), additive attention
+ * with a masked softmax, a deep-output readout, the output projection and a
+ * log-softmax.
+ *
+ * Model (row m = b*K + k of sentence b, all matrices stored [in x out]):
+ *   x  = emb[prev_tok[m]],        h = state_in[src_row[m]]
+ *   s1 = GRU(x, h; W1, U1, b1)    GRU(x,h): a = xW + b, u = hU, per-block LN
+ *                                 (if enabled) on a_r,a_z,a_h,u_r,u_z,u_h,
+ *                                 r = sig(a_r+u_r), z = sig(a_z+u_z),
+ *                                 hh = tanh(a_h + r*u_h), out = (1-z)hh + z h
+ *   q  = s1 Wa;  e_i = va . tanh(P[b,i] + q) for valid i;  alpha = softmax(e)
+ *   c  = sum_i alpha_i ctx[b,i]
+ *   s  = GRU(c, s1; W2, U2, b2)   -> state_out[m]
+ *   t  = tanh(LN?(s Wt_s + x Wt_y + c Wt_c + bt))
+ *   logp = log_softmax(t Wo + bo)
+ * with P[b,i] = ctx[b,i] Ua + ba and s0[b] = tanh(mean_valid(ctx[b]) Wi + bi).
+ *
+ * Conventions for every call:
+ *   - Device pointers unless stated otherwise; row-major; 16-byte aligned.
+ *   - Calls are asynchronous on the given HIP stream (a hipStream_t passed as
+ *     void*, NULL = the null stream) and never synchronise, except
+ *     mt_load_weights, mt_free, mt_device_errors and mt_profile_query.
+ *   - Every argument is validated on the host before anything is launched;
+ *     a failed call launches nothing and returns a negative mt_status, with a
+ *     message in mt_last_error().  Kernel faults surface at the caller's
+ *     next synchronisation.
+ *   - One model handle serves one stream at a time.  Callers own every
+ *     activation buffer and the workspace; the library allocates only in
+ *     mt_load_weights and never per step.
+ */
+#ifndef MTSTEP_H
+#define MTSTEP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MT_OK = 0,
+  MT_ERR_ARG = -1,       /* null/misaligned pointer, bad enum, bad flag */
+  MT_ERR_SHAPE = -2,     /* a size out of its supported range */
+  MT_ERR_DTYPE = -3,     /* unsupported dtype */
+  MT_ERR_HIP = -4,       /* a HIP runtime call failed (message says which) */
+  MT_ERR_OOM = -5,       /* device allocation failed in mt_load_weights */
+  MT_ERR_STATE = -6,     /* call order violated (e.g. top-K without a step) */
+  MT_ERR_WORKSPACE = -7  /* workspace too small */
+} mt_status;
+
+typedef enum { MT_F32 = 0, MT_BF16 = 1 } mt_dtype;
+
+/* Model shape and options.
+ *   E, H, A: multiples of 16 with 16 <= E, H <= 4096 and 16 <= A <= 4096;
+ *   C = 2H (bi-directional encoder context); 2 <= V <= 2^24.
+ *   gemm_dtype: operand type of every matrix product (accumulation is fp32).
+ *     MT_BF16 also stores the encoder context and attention keys in bf16.
+ *     Gates, layer norm, softmax, log-softmax, states and scores stay fp32.
+ *   layer_norm: 0/1 — LN on each gate block of both paths of both GRUs and
+ *     on the readout pre-activation (eps = ln_eps, biased variance).
+ *   tied_output: 0/1 — the output matrix is emb transposed (Wo ignored).
+ *   k_max: largest beam size the model will be called with, 1..16. */
+typedef struct {
+  int32_t E, H, A, V;
+  int32_t layer_norm;
+  int32_t tied_output;
+  int32_t k_max;
+  int32_t gemm_dtype;
+  float ln_eps;
+} mt_config;
+
+/* Model parameters: HOST pointers to fp32, row-major logical [in x out]
+ * (gate blocks of the [*, 3H] matrices in the order r, z, h).  Only read
+ * during mt_load_weights; the caller may free them afterwards.
+ *   emb[V,E]; W1[E,3H] U1[H,3H] b1[3H]; Ua[C,A] ba[A] Wa[H,A] va[A];
+ *   W2[C,3H] U2[H,3H] b2[3H]; Wt_s[H,E] Wt_y[E,E] Wt_c[C,E] bt[E];
+ *   Wo[E,V] bo[V]; Wi[C,H] bi[H];
+ *   layer norm (read only if layer_norm): gain/shift of the input path (a)
+ *   and recurrent path (u) of GRU 1 and 2, [3H] each; readout gt/bet [E]. */
+typedef struct {
+  const float *emb;
+  const float *W1, *U1, *b1;
+  const float *Ua, *ba, *Wa, *va;
+  const float *W2, *U2, *b2;
+  const float *Wt_s, *Wt_y, *Wt_c, *bt;
+  const float *Wo, *bo;
+  const float *Wi, *bi;
+  const float *g1a, *be1a, *g1u, *be1u, *g2a, *be2a, *g2u, *be2u, *gt, *bet;
+} mt_weights;
+
+typedef struct mt_model mt_model; /* opaque, library-owned */
+
+/* Optional per-stage outputs of mt_decoder_step, each fp32 [B*K, n] or NULL:
+ * s1 (n = H), c (n = 2H), t (n = E).  For stage-level checks. */
+typedef struct {
+  float *s1;
+  float *c;
+  float *t;
+} mt_taps;
+
+/* Copy, pack and convert the weights into library-owned device memory on
+ * the current HIP device (fused gate layouts, K-contiguous transposes,
+ * bf16 round-to-nearest-even when gemm_dtype is MT_BF16).  Synchronous.
+ * On success *out receives the handle; release it with mt_free. */
+mt_status mt_load_weights(const mt_config *cfg, const mt_weights *w, mt_model **out);
+
+/* Release a handle and its device memory (synchronises the device). */
+mt_status mt_free(mt_model *model);
+
+/* Workspace bytes that mt_precompute_ctx, mt_decoder_step and mt_beam_topk
+ * need for B sentences, beam K and padded source length S; 0 on bad input.
+ * The same workspace must be passed to a step and to the mt_beam_topk call
+ * that consumes it (it carries the fused top-K candidates between them). */
+size_t mt_workspace_bytes(const mt_model *model, int B, int K, int S);
+
+/* Decoder start state for B sentences (Section 2.2, Decoder::startState):
+ *   ctx  [B,S,2H] in gemm dtype (fp32 or bf16) — the encoder context;
+ *   mask [B,S] fp32, nonzero = valid position (any pattern; a row without a
+ *        valid position yields zero context and zero attention);
+ *   pctx_out [B,S,A] in gemm dtype — attention keys ctx Ua + ba (values at
+ *        masked positions are unspecified and never read);
+ *   s0_out [B,H] fp32 — tanh(masked mean of ctx[b] times Wi + bi).
+ * 1 <= S <= 1024; B*S <= 2^24. */
+mt_status mt_precompute_ctx(mt_model *model, int B, int S, const void *ctx, const float *mask,
+                            void *pctx_out, float *s0_out, void *ws, size_t ws_bytes,
+                            void *stream);
+
+/* One decoder step for M = B*K hypothesis rows (Section 2.2, Decoder::step):
+ *   prev_tok [M] int32 in [0,V); src_row [M] int32 in [0,n_state_rows):
+ *   row m reads h = state_in[src_row[m]] (at step 0 pass s0 with
+ *   src_row[m] = m / K; later pass the previous state_out with row_out of
+ *   mt_beam_topk).  Out-of-range indices are clamped and reported by
+ *   mt_device_errors.  state_in [n_state_rows,H] fp32;
+ *   ctx/pctx/mask as produced for mt_precompute_ctx;
+ *   state_out [M,H] fp32 (must not alias state_in);
+ *   logp_out [M,V] fp32 or NULL — materialised log-probabilities;
+ *   attn_out [M,S] fp32 or NULL — attention weights (0 at masked positions);
+ *   taps: NULL or optional stage outputs.
+ * 1 <= K <= k_max, K <= V. */
+mt_status mt_decoder_step(mt_model *model, int B, int K, int S, const int32_t *prev_tok,
+                          const int32_t *src_row, int n_state_rows, const float *state_in,
+                          const void *ctx, const void *pctx, const float *mask, float *state_out,
+                          float *logp_out, float *attn_out, const mt_taps *taps, void *ws,
+                          size_t ws_bytes, void *stream);
+
+/* Beam selection (Section 2.2: next hypotheses from the decoder state;
+ * Section 2.3: batched beam search).  For sentence b the candidates are
+ * cand(k,v) = prev_score[b*K+k] + logp[b*K+k, v], summed in fp32; the K best
+ * by (cand descending, k*V + v ascending) are written as
+ *   score_out[b*K+j] = cand, tok_out[b*K+j] = v, bp_out[b*K+j] = k,
+ *   row_out[b*K+j] = b*K + k (NULL allowed) — the next step's src_row.
+ * logp: [M,V] fp32 from any source, or NULL to use the candidates that the
+ * preceding mt_decoder_step (same B, K, workspace) left in the workspace.
+ * prev_score may alias score_out. */
+mt_status mt_beam_topk(mt_model *model, int B, int K, const float *prev_score, const float *logp,
+                       float *score_out, int32_t *tok_out, int32_t *bp_out, int32_t *row_out,
+                       void *ws, size_t ws_bytes, void *stream);
+
+/* Reads and clears the device-side error bits (synchronises the device):
+ * bit 0 = a prev_tok out of range, bit 1 = a src_row out of range. */
+mt_status mt_device_errors(mt_model *model, int32_t *flags);
+
+/* Kernel timing with HIP events recorded on the launch stream around each
+ * launch of the given kernel class (off by default; costs two event records
+ * per launch).  mt_profile_query synchronises and returns the summed
+ * duration in milliseconds and the number of timed launches since the last
+ * reset. */
+typedef enum {
+  MT_KERNEL_GEMM_GRU1 = 0,  /* x [W1|Wt_y] and h U1 */
+  MT_KERNEL_GRU_CELL = 1,   /* both GRU elementwise kernels */
+  MT_KERNEL_GEMM_S1 = 2,    /* s1 [Wa|U2] */
+  MT_KERNEL_ATTENTION = 3,
+  MT_KERNEL_GEMM_CTX = 4,   /* c [W2|Wt_c] */
+  MT_KERNEL_GEMM_READOUT = 5, /* s Wt_s */
+  MT_KERNEL_READOUT = 6,    /* sum + LN + tanh */
+  MT_KERNEL_VOCAB_GEMM = 7, /* t Wo + bo with fused LSE / top-K partials */
+  MT_KERNEL_LSE = 8,        /* row log-sum-exp merge (+ logp finalize) */
+  MT_KERNEL_TOPK = 9,       /* all top-K kernels */
+  MT_KERNEL_PRECOMPUTE = 10,
+  MT_KERNEL_COUNT = 11
+} mt_kernel_id;
+
+mt_status mt_profile_enable(mt_model *model, int on);
+mt_status mt_profile_reset(mt_model *model);
+mt_status mt_profile_query(mt_model *model, int kernel, double *total_ms, int64_t *launches);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char *mt_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,616 @@
+// libmtstep C ABI: argument validation, weight packing, workspace layout and the launch
+// sequence of one decoder step (declarations and contracts in include/mtstep.h).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "mt_internal.h"
+
+using namespace mt;
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+mt_status fail(mt_status s, const char *fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+#define HIP_TRY(expr)                                                                      \
+  do {                                                                                     \
+    hipError_t e_ = (expr);                                                                \
+    if (e_ != hipSuccess) return fail(MT_ERR_HIP, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+constexpr uint32_t kMagic = 0x4d545350u;  // "MTSP"
+constexpr int kNPad = 256;                // N padding of packed weights (>= any tile BN)
+constexpr int kKPad = 64;                 // K padding (>= any tile BK)
+
+size_t rup(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+struct Packed {
+  void *p = nullptr;
+  int N = 0, K = 0, ldb = 0;
+};
+
+struct ProfSlot {
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> pending;
+  double ms = 0.0;
+  int64_t n = 0;
+};
+
+}  // namespace
+
+struct mt_model {
+  uint32_t magic;
+  mt_config cfg;
+  int C;
+  int bf16;       // gemm dtype is bf16
+  int esize;      // bytes per GEMM operand element
+  Packed w1x, w1h, w2, w3, w4, wo, wp, ws0;  // packed [N_pad][K_pad]
+  void *emb;      // [V][E] compute dtype (row gather source)
+  float *bias1x, *bias3, *bo, *ba, *bi, *bt, *va;
+  float *ln[10];  // g1a be1a g1u be1u g2a be2a g2u be2u gt bet
+  int32_t *err;
+  std::vector<void *> allocs;
+  // call-order state for mt_beam_topk(logp = NULL)
+  int last_B = -1, last_K = -1;
+  const void *last_ws = nullptr;
+  // profiling
+  bool prof_on = false;
+  ProfSlot prof[MT_KERNEL_COUNT];
+  std::vector<hipEvent_t> ev_pool;
+};
+
+namespace {
+
+bool valid_model(const mt_model *m) { return m && m->magic == kMagic; }
+
+bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+mt_status check_cfg(const mt_config *c) {
+  if (!c) return fail(MT_ERR_ARG, "config is NULL");
+  auto dim_ok = [](int v, int lo, int hi) { return v >= lo && v <= hi && v % 16 == 0; };
+  if (!dim_ok(c->E, 16, 4096)) return fail(MT_ERR_SHAPE, "E=%d: need a multiple of 16 in [16, 4096]", c->E);
+  if (!dim_ok(c->H, 16, 4096)) return fail(MT_ERR_SHAPE, "H=%d: need a multiple of 16 in [16, 4096]", c->H);
+  if (!dim_ok(c->A, 16, 4096)) return fail(MT_ERR_SHAPE, "A=%d: need a multiple of 16 in [16, 4096]", c->A);
+  if (c->V < 2 || c->V > (1 << 24)) return fail(MT_ERR_SHAPE, "V=%d: need 2 <= V <= 2^24", c->V);
+  if (c->k_max < 1 || c->k_max > kKMax) return fail(MT_ERR_SHAPE, "k_max=%d: need 1..%d", c->k_max, kKMax);
+  if (c->k_max > c->V) return fail(MT_ERR_SHAPE, "k_max=%d exceeds V=%d", c->k_max, c->V);
+  if (c->layer_norm != 0 && c->layer_norm != 1) return fail(MT_ERR_ARG, "layer_norm must be 0 or 1");
+  if (c->tied_output != 0 && c->tied_output != 1) return fail(MT_ERR_ARG, "tied_output must be 0 or 1");
+  if (c->gemm_dtype != MT_F32 && c->gemm_dtype != MT_BF16)
+    return fail(MT_ERR_DTYPE, "gemm_dtype=%d: need MT_F32 or MT_BF16", c->gemm_dtype);
+  if (c->layer_norm && !(c->ln_eps > 0.f && std::isfinite(c->ln_eps)))
+    return fail(MT_ERR_ARG, "ln_eps must be positive and finite");
+  return MT_OK;
+}
+
+uint16_t bf16_bits(float f) {  // round to nearest even, NaN stays a quiet NaN
+  uint32_t u;
+  std::memcpy(&u, &f, 4);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+struct Seg {
+  const float *w;  // logical [K][ncols] row-major
+  int ncols;
+};
+
+// packed[n][k] = concat(segments)[k][n], zero padded to [rup(N, kNPad)][rup(K, kKPad)]
+std::vector<char> pack_host(const std::vector<Seg> &segs, int K, int esize, int *N_out, int *ldb_out) {
+  int N = 0;
+  for (auto &s : segs) N += s.ncols;
+  const int Np = (int)rup(N, kNPad), Kp = (int)rup(K, kKPad);
+  std::vector<char> buf((size_t)Np * Kp * esize, 0);
+  int n0 = 0;
+  for (auto &s : segs) {
+    for (int kb = 0; kb < K; kb += 64)
+      for (int nb = 0; nb < s.ncols; nb += 64)
+        for (int k = kb; k < std::min(K, kb + 64); ++k) {
+          const float *src = s.w + (size_t)k * s.ncols;
+          for (int n = nb; n < std::min(s.ncols, nb + 64); ++n) {
+            const size_t o = (size_t)(n0 + n) * Kp + k;
+            if (esize == 4)
+              ((float *)buf.data())[o] = src[n];
+            else
+              ((uint16_t *)buf.data())[o] = bf16_bits(src[n]);
+          }
+        }
+    n0 += s.ncols;
+  }
+  *N_out = N;
+  *ldb_out = Kp;
+  return buf;
+}
+
+mt_status dev_upload(mt_model *m, const void *host, size_t bytes, void **out) {
+  void *d = nullptr;
+  const hipError_t e = hipMalloc(&d, bytes ? bytes : 16);
+  if (e != hipSuccess) return fail(MT_ERR_OOM, "hipMalloc(%zu): %s", bytes, hipGetErrorString(e));
+  m->allocs.push_back(d);
+  if (bytes) HIP_TRY(hipMemcpy(d, host, bytes, hipMemcpyHostToDevice));
+  *out = d;
+  return MT_OK;
+}
+
+mt_status upload_packed(mt_model *m, const std::vector<Seg> &segs, int K, Packed *p) {
+  int N = 0, ldb = 0;
+  std::vector<char> buf = pack_host(segs, K, m->esize, &N, &ldb);
+  p->N = N;
+  p->K = K;
+  p->ldb = ldb;
+  return dev_upload(m, buf.data(), buf.size(), &p->p);
+}
+
+mt_status upload_vec(mt_model *m, const std::vector<float> &v, float **out) {
+  return dev_upload(m, v.data(), v.size() * sizeof(float), (void **)out);
+}
+
+std::vector<float> cat(std::initializer_list<std::pair<const float *, int>> parts) {
+  std::vector<float> v;
+  for (auto &p : parts) {
+    if (p.first)
+      v.insert(v.end(), p.first, p.first + p.second);
+    else
+      v.insert(v.end(), (size_t)p.second, 0.f);
+  }
+  return v;
+}
+
+// ---- workspace ----
+struct WsLayout {
+  size_t gx, gh, s1, g2, c, g3, g4, t, part, cand, lse, rowc, scand, total;
+  int ntiles, kc, nchunks;
+};
+
+WsLayout ws_layout(const mt_model *m, int B, int K) {
+  const mt_config &c = m->cfg;
+  const size_t M = (size_t)B * K, E = c.E, H = c.H, A = c.A, C = 2 * H;
+  WsLayout L{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += rup(bytes, 256);
+    return o;
+  };
+  L.gx = take(M * (3 * H + E) * 4);
+  L.gh = take(M * 3 * H * 4);
+  L.s1 = take(M * H * 4);
+  L.g2 = take(M * (A + 3 * H) * 4);
+  L.c = take(M * C * 4);
+  L.g3 = take(M * (3 * H + E) * 4);
+  L.g4 = take(M * E * 4);
+  L.t = take(M * E * m->esize);
+  L.ntiles = (c.V + vocab_tile_n() - 1) / vocab_tile_n();
+  L.kc = K;
+  L.part = take(M * L.ntiles * sizeof(float2));
+  L.cand = take(M * L.ntiles * L.kc * sizeof(int2));
+  L.lse = take(M * 4);
+  L.rowc = take(M * K * sizeof(int2));
+  L.nchunks = std::max(1, std::min(64, (c.V + 2047) / 2048));
+  L.scand = take(M * L.nchunks * K * sizeof(int2));
+  L.total = off;
+  return L;
+}
+
+size_t precompute_ws_bytes(const mt_model *m, int B) { return (size_t)B * 2 * m->cfg.H * 4; }
+
+// ---- profiling ----
+hipEvent_t get_event(mt_model *m) {
+  if (!m->ev_pool.empty()) {
+    hipEvent_t e = m->ev_pool.back();
+    m->ev_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+void fold_profile(mt_model *m, int k) {
+  ProfSlot &s = m->prof[k];
+  for (auto &pr : s.pending) {
+    float ms = 0.f;
+    if (hipEventSynchronize(pr.second) == hipSuccess && hipEventElapsedTime(&ms, pr.first, pr.second) == hipSuccess) {
+      s.ms += ms;
+      s.n += 1;
+    }
+    m->ev_pool.push_back(pr.first);
+    m->ev_pool.push_back(pr.second);
+  }
+  s.pending.clear();
+}
+
+struct Timed {  // records events around one launch when profiling is on
+  mt_model *m;
+  int k;
+  hipStream_t st;
+  hipEvent_t a = nullptr, b = nullptr;
+  Timed(mt_model *m_, int k_, hipStream_t st_) : m(m_), k(k_), st(st_) {
+    if (m->prof_on) {
+      a = get_event(m);
+      b = get_event(m);
+      if (a && b) hipEventRecord(a, st);
+    }
+  }
+  ~Timed() {
+    if (a && b) {
+      hipEventRecord(b, st);
+      m->prof[k].pending.emplace_back(a, b);
+      if (m->prof[k].pending.size() > 8192) fold_profile(m, k);
+    }
+  }
+};
+
+#define LAUNCH(kid, expr)                                                                   \
+  do {                                                                                      \
+    hipError_t e_;                                                                          \
+    {                                                                                       \
+      Timed tm_(model, kid, st);                                                            \
+      e_ = (expr);                                                                          \
+    }                                                                                       \
+    if (e_ != hipSuccess) return fail(MT_ERR_HIP, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+mt_status check_dev_ptr(const void *p, const char *name, size_t align = 16) {
+  if (!p) return fail(MT_ERR_ARG, "%s is NULL", name);
+  if (!aligned(p, align)) return fail(MT_ERR_ARG, "%s is not %zu-byte aligned", name, align);
+  return MT_OK;
+}
+
+#define CHECK(expr)                 \
+  do {                              \
+    mt_status s_ = (expr);          \
+    if (s_ != MT_OK) return s_;     \
+  } while (0)
+
+}  // namespace
+
+extern "C" {
+
+const char *mt_last_error(void) { return g_err; }
+
+mt_status mt_load_weights(const mt_config *cfg, const mt_weights *w, mt_model **out) {
+  g_err[0] = 0;
+  if (!out) return fail(MT_ERR_ARG, "out is NULL");
+  *out = nullptr;
+  CHECK(check_cfg(cfg));
+  if (!w) return fail(MT_ERR_ARG, "weights is NULL");
+  const mt_config &c = *cfg;
+  struct Need {
+    const float *p;
+    const char *n;
+  } need[] = {{w->emb, "emb"}, {w->W1, "W1"}, {w->U1, "U1"}, {w->b1, "b1"}, {w->Ua, "Ua"},
+              {w->ba, "ba"},   {w->Wa, "Wa"}, {w->va, "va"}, {w->W2, "W2"}, {w->U2, "U2"},
+              {w->b2, "b2"},   {w->Wt_s, "Wt_s"}, {w->Wt_y, "Wt_y"}, {w->Wt_c, "Wt_c"},
+              {w->bt, "bt"},   {w->bo, "bo"}, {w->Wi, "Wi"}, {w->bi, "bi"}};
+  for (auto &n : need)
+    if (!n.p) return fail(MT_ERR_ARG, "weight %s is NULL", n.n);
+  if (!c.tied_output && !w->Wo) return fail(MT_ERR_ARG, "weight Wo is NULL (tied_output = 0)");
+  const float *lnp[10] = {w->g1a, w->be1a, w->g1u, w->be1u, w->g2a, w->be2a, w->g2u, w->be2u, w->gt, w->bet};
+  if (c.layer_norm)
+    for (int i = 0; i < 10; ++i)
+      if (!lnp[i]) return fail(MT_ERR_ARG, "layer-norm parameter %d is NULL (layer_norm = 1)", i);
+
+  mt_model *m = new (std::nothrow) mt_model();
+  if (!m) return fail(MT_ERR_OOM, "host allocation failed");
+  m->magic = kMagic;
+  m->cfg = c;
+  m->C = 2 * c.H;
+  m->bf16 = c.gemm_dtype == MT_BF16;
+  m->esize = m->bf16 ? 2 : 4;
+  const int E = c.E, H = c.H, A = c.A, V = c.V, C = 2 * c.H;
+  mt_status s = MT_OK;
+  auto run = [&]() -> mt_status {
+    CHECK(upload_packed(m, {{w->W1, 3 * H}, {w->Wt_y, E}}, E, &m->w1x));
+    CHECK(upload_packed(m, {{w->U1, 3 * H}}, H, &m->w1h));
+    CHECK(upload_packed(m, {{w->Wa, A}, {w->U2, 3 * H}}, H, &m->w2));
+    CHECK(upload_packed(m, {{w->W2, 3 * H}, {w->Wt_c, E}}, C, &m->w3));
+    CHECK(upload_packed(m, {{w->Wt_s, E}}, H, &m->w4));
+    CHECK(upload_packed(m, {{w->Ua, A}}, C, &m->wp));
+    CHECK(upload_packed(m, {{w->Wi, H}}, C, &m->ws0));
+    if (c.tied_output) {
+      // logits = t emb^T: the packed [V][E] layout is emb itself
+      std::vector<char> buf((size_t)rup(V, kNPad) * rup(E, kKPad) * m->esize, 0);
+      const int Kp = (int)rup(E, kKPad);
+      for (int v = 0; v < V; ++v)
+        for (int e = 0; e < E; ++e) {
+          const float x = w->emb[(size_t)v * E + e];
+          if (m->esize == 4)
+            ((float *)buf.data())[(size_t)v * Kp + e] = x;
+          else
+            ((uint16_t *)buf.data())[(size_t)v * Kp + e] = bf16_bits(x);
+        }
+      m->wo.N = V;
+      m->wo.K = E;
+      m->wo.ldb = Kp;
+      CHECK(dev_upload(m, buf.data(), buf.size(), &m->wo.p));
+    } else {
+      CHECK(upload_packed(m, {{w->Wo, V}}, E, &m->wo));
+    }
+    {  // embedding rows in the GEMM operand type
+      std::vector<char> buf((size_t)V * E * m->esize);
+      for (size_t i = 0; i < (size_t)V * E; ++i) {
+        if (m->esize == 4)
+          ((float *)buf.data())[i] = w->emb[i];
+        else
+          ((uint16_t *)buf.data())[i] = bf16_bits(w->emb[i]);
+      }
+      CHECK(dev_upload(m, buf.data(), buf.size(), &m->emb));
+    }
+    CHECK(upload_vec(m, cat({{w->b1, 3 * H}, {nullptr, E}}), &m->bias1x));
+    CHECK(upload_vec(m, cat({{w->b2, 3 * H}, {nullptr, E}}), &m->bias3));
+    CHECK(upload_vec(m, cat({{w->bo, V}}), &m->bo));
+    CHECK(upload_vec(m, cat({{w->ba, A}}), &m->ba));
+    CHECK(upload_vec(m, cat({{w->bi, H}}), &m->bi));
+    CHECK(upload_vec(m, cat({{w->bt, E}}), &m->bt));
+    CHECK(upload_vec(m, cat({{w->va, A}}), &m->va));
+    for (int i = 0; i < 10; ++i) {
+      m->ln[i] = nullptr;
+      if (c.layer_norm) CHECK(upload_vec(m, cat({{lnp[i], i < 8 ? 3 * H : E}}), &m->ln[i]));
+    }
+    int32_t zero = 0;
+    CHECK(dev_upload(m, &zero, sizeof zero, (void **)&m->err));
+    return MT_OK;
+  };
+  s = run();
+  if (s != MT_OK) {
+    char keep[sizeof g_err];
+    std::memcpy(keep, g_err, sizeof keep);
+    mt_free(m);
+    std::memcpy(g_err, keep, sizeof keep);
+    return s;
+  }
+  *out = m;
+  return MT_OK;
+}
+
+mt_status mt_free(mt_model *m) {
+  if (!valid_model(m)) return fail(MT_ERR_ARG, "invalid model handle");
+  hipDeviceSynchronize();
+  for (int k = 0; k < MT_KERNEL_COUNT; ++k) {
+    for (auto &pr : m->prof[k].pending) {
+      hipEventDestroy(pr.first);
+      hipEventDestroy(pr.second);
+    }
+  }
+  for (auto e : m->ev_pool) hipEventDestroy(e);
+  for (void *p : m->allocs) hipFree(p);
+  m->magic = 0;
+  delete m;
+  return MT_OK;
+}
+
+size_t mt_workspace_bytes(const mt_model *m, int B, int K, int S) {
+  if (!valid_model(m) || B < 1 || K < 1 || K > m->cfg.k_max || S < 1 || S > 1024) return 0;
+  const WsLayout L = ws_layout(m, B, K);
+  return std::max(L.total, precompute_ws_bytes(m, B));
+}
+
+mt_status mt_precompute_ctx(mt_model *model, int B, int S, const void *ctx, const float *mask,
+                            void *pctx_out, float *s0_out, void *ws, size_t ws_bytes, void *stream) {
+  g_err[0] = 0;
+  if (!valid_model(model)) return fail(MT_ERR_ARG, "invalid model handle");
+  if (B < 1 || S < 1 || S > 1024) return fail(MT_ERR_SHAPE, "B=%d S=%d: need B >= 1, 1 <= S <= 1024", B, S);
+  if ((long long)B * S > (1 << 24)) return fail(MT_ERR_SHAPE, "B*S=%lld exceeds 2^24", (long long)B * S);
+  CHECK(check_dev_ptr(ctx, "ctx"));
+  CHECK(check_dev_ptr(mask, "mask", 4));
+  CHECK(check_dev_ptr(pctx_out, "pctx_out"));
+  CHECK(check_dev_ptr(s0_out, "s0_out"));
+  CHECK(check_dev_ptr(ws, "ws", 256));
+  const size_t need = precompute_ws_bytes(model, B);
+  if (ws_bytes < need) return fail(MT_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, need);
+  hipStream_t st = (hipStream_t)stream;
+  const mt_config &c = model->cfg;
+  const int H = c.H, A = c.A, C = model->C;
+  float *cbar = (float *)ws;
+  GemmProblem p{};
+  p.A = ctx; p.a_idx = nullptr; p.a_rows = B * S; p.lda = C; p.a_bf16 = model->bf16;
+  p.Bp = model->wp.p; p.ldb = model->wp.ldb; p.bias = model->ba;
+  p.out = pctx_out; p.ldc = A; p.out_bf16 = model->bf16;
+  p.M = B * S; p.N = A; p.K = C; p.err = nullptr; p.err_bit = 0;
+  LAUNCH(MT_KERNEL_PRECOMPUTE, launch_gemm(model->bf16, &p, 1, EPI_STORE, nullptr, st));
+  LAUNCH(MT_KERNEL_PRECOMPUTE, launch_masked_mean(B, S, C, ctx, model->bf16, mask, cbar, st));
+  GemmProblem q{};
+  q.A = cbar; q.a_rows = B; q.lda = C; q.a_bf16 = 0;
+  q.Bp = model->ws0.p; q.ldb = model->ws0.ldb; q.bias = model->bi;
+  q.out = s0_out; q.ldc = H; q.out_bf16 = 0;
+  q.M = B; q.N = H; q.K = C;
+  LAUNCH(MT_KERNEL_PRECOMPUTE, launch_gemm(model->bf16, &q, 1, EPI_TANH, nullptr, st));
+  return MT_OK;
+}
+
+mt_status mt_decoder_step(mt_model *model, int B, int K, int S, const int32_t *prev_tok,
+                          const int32_t *src_row, int n_state_rows, const float *state_in,
+                          const void *ctx, const void *pctx, const float *mask, float *state_out,
+                          float *logp_out, float *attn_out, const mt_taps *taps, void *ws,
+                          size_t ws_bytes, void *stream) {
+  g_err[0] = 0;
+  if (!valid_model(model)) return fail(MT_ERR_ARG, "invalid model handle");
+  const mt_config &c = model->cfg;
+  if (B < 1 || K < 1 || K > c.k_max || K > c.V || S < 1 || S > 1024)
+    return fail(MT_ERR_SHAPE, "B=%d K=%d S=%d: need B >= 1, 1 <= K <= k_max=%d, 1 <= S <= 1024", B, K, S, c.k_max);
+  if ((long long)B * K > (1 << 20)) return fail(MT_ERR_SHAPE, "B*K exceeds 2^20");
+  if ((long long)B * S > (1 << 24)) return fail(MT_ERR_SHAPE, "B*S exceeds 2^24");
+  if (n_state_rows < 1) return fail(MT_ERR_SHAPE, "n_state_rows=%d must be >= 1", n_state_rows);
+  CHECK(check_dev_ptr(prev_tok, "prev_tok", 4));
+  CHECK(check_dev_ptr(src_row, "src_row", 4));
+  CHECK(check_dev_ptr(state_in, "state_in"));
+  CHECK(check_dev_ptr(ctx, "ctx"));
+  CHECK(check_dev_ptr(pctx, "pctx"));
+  CHECK(check_dev_ptr(mask, "mask", 4));
+  CHECK(check_dev_ptr(state_out, "state_out"));
+  CHECK(check_dev_ptr(ws, "ws", 256));
+  if (logp_out) CHECK(check_dev_ptr(logp_out, "logp_out", 4));
+  if (attn_out) CHECK(check_dev_ptr(attn_out, "attn_out", 4));
+  if (taps) {
+    if (taps->s1) CHECK(check_dev_ptr(taps->s1, "taps->s1", 4));
+    if (taps->c) CHECK(check_dev_ptr(taps->c, "taps->c", 4));
+    if (taps->t) CHECK(check_dev_ptr(taps->t, "taps->t", 4));
+  }
+  const int M = B * K, E = c.E, H = c.H, A = c.A, V = c.V, C = model->C;
+  {
+    const char *si = (const char *)state_in, *so = (const char *)state_out;
+    if (si < so + (size_t)M * H * 4 && so < si + (size_t)n_state_rows * H * 4)
+      return fail(MT_ERR_ARG, "state_out overlaps state_in");
+  }
+  const WsLayout L = ws_layout(model, B, K);
+  if (ws_bytes < L.total) return fail(MT_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, L.total);
+  hipStream_t st = (hipStream_t)stream;
+  char *W = (char *)ws;
+  float *gx = (float *)(W + L.gx), *gh = (float *)(W + L.gh), *s1 = (float *)(W + L.s1);
+  float *g2 = (float *)(W + L.g2), *cc = (float *)(W + L.c), *g3 = (float *)(W + L.g3);
+  float *g4 = (float *)(W + L.g4);
+  void *t = W + L.t;
+  const int bf = model->bf16;
+  const float eps = c.ln_eps;
+  float *const *ln = model->ln;
+  const bool LNon = c.layer_norm != 0;
+
+  // GRU 1 products: x [W1 | Wt_y] + [b1 | 0] and h U1 (one launch, two problems)
+  GemmProblem p1[2] = {};
+  p1[0].A = model->emb; p1[0].a_idx = prev_tok; p1[0].a_rows = V; p1[0].lda = E; p1[0].a_bf16 = bf;
+  p1[0].Bp = model->w1x.p; p1[0].ldb = model->w1x.ldb; p1[0].bias = model->bias1x;
+  p1[0].out = gx; p1[0].ldc = 3 * H + E; p1[0].M = M; p1[0].N = 3 * H + E; p1[0].K = E;
+  p1[0].err = model->err; p1[0].err_bit = 0;
+  p1[1].A = state_in; p1[1].a_idx = src_row; p1[1].a_rows = n_state_rows; p1[1].lda = H; p1[1].a_bf16 = 0;
+  p1[1].Bp = model->w1h.p; p1[1].ldb = model->w1h.ldb; p1[1].bias = nullptr;
+  p1[1].out = gh; p1[1].ldc = 3 * H; p1[1].M = M; p1[1].N = 3 * H; p1[1].K = H;
+  p1[1].err = model->err; p1[1].err_bit = 1;
+  LAUNCH(MT_KERNEL_GEMM_GRU1, launch_gemm(bf, p1, 2, EPI_STORE, nullptr, st));
+  LAUNCH(MT_KERNEL_GRU_CELL,
+         launch_gru_cell(M, H, gx, 3 * H + E, gh, 3 * H, state_in, src_row, n_state_rows, model->err,
+                         LNon ? ln[0] : nullptr, ln[1], ln[2], ln[3], eps, s1, H, taps ? taps->s1 : nullptr, st));
+  // s1 [Wa | U2]: attention query and GRU 2 recurrent product
+  GemmProblem p2{};
+  p2.A = s1; p2.a_rows = M; p2.lda = H; p2.a_bf16 = 0;
+  p2.Bp = model->w2.p; p2.ldb = model->w2.ldb;
+  p2.out = g2; p2.ldc = A + 3 * H; p2.M = M; p2.N = A + 3 * H; p2.K = H;
+  LAUNCH(MT_KERNEL_GEMM_S1, launch_gemm(bf, &p2, 1, EPI_STORE, nullptr, st));
+  LAUNCH(MT_KERNEL_ATTENTION, launch_attention(B, K, S, A, C, pctx, ctx, bf, mask, g2, A + 3 * H, model->va, cc, C,
+                                               attn_out, st));
+  if (taps && taps->c) HIP_TRY(hipMemcpyAsync(taps->c, cc, (size_t)M * C * 4, hipMemcpyDeviceToDevice, st));
+  // c [W2 | Wt_c] + [b2 | 0]
+  GemmProblem p3{};
+  p3.A = cc; p3.a_rows = M; p3.lda = C; p3.a_bf16 = 0;
+  p3.Bp = model->w3.p; p3.ldb = model->w3.ldb; p3.bias = model->bias3;
+  p3.out = g3; p3.ldc = 3 * H + E; p3.M = M; p3.N = 3 * H + E; p3.K = C;
+  LAUNCH(MT_KERNEL_GEMM_CTX, launch_gemm(bf, &p3, 1, EPI_STORE, nullptr, st));
+  LAUNCH(MT_KERNEL_GRU_CELL,
+         launch_gru_cell(M, H, g3, 3 * H + E, g2 + A, A + 3 * H, s1, nullptr, M, model->err,
+                         LNon ? ln[4] : nullptr, ln[5], ln[6], ln[7], eps, state_out, H, nullptr, st));
+  // readout: s Wt_s, then tanh(LN?(s Wt_s + x Wt_y + c Wt_c + bt))
+  GemmProblem p4{};
+  p4.A = state_out; p4.a_rows = M; p4.lda = H; p4.a_bf16 = 0;
+  p4.Bp = model->w4.p; p4.ldb = model->w4.ldb;
+  p4.out = g4; p4.ldc = E; p4.M = M; p4.N = E; p4.K = H;
+  LAUNCH(MT_KERNEL_GEMM_READOUT, launch_gemm(bf, &p4, 1, EPI_STORE, nullptr, st));
+  LAUNCH(MT_KERNEL_READOUT, launch_readout(M, E, g4, E, gx + 3 * H, 3 * H + E, g3 + 3 * H, 3 * H + E, model->bt,
+                                           LNon ? ln[8] : nullptr, ln[9], eps, t, bf, taps ? taps->t : nullptr, st));
+  // vocabulary GEMM with fused log-sum-exp partials and per-tile top-K
+  GemmProblem p5{};
+  p5.A = t; p5.a_rows = M; p5.lda = E; p5.a_bf16 = bf;
+  p5.Bp = model->wo.p; p5.ldb = model->wo.ldb; p5.bias = model->bo;
+  p5.out = nullptr; p5.ldc = V; p5.M = M; p5.N = V; p5.K = E;
+  VocabOut vo{};
+  vo.part = (float2 *)(W + L.part);
+  vo.cand = (int2 *)(W + L.cand);
+  vo.kc = L.kc;
+  vo.ntiles = L.ntiles;
+  vo.logits = logp_out;
+  LAUNCH(MT_KERNEL_VOCAB_GEMM, launch_gemm(bf, &p5, 1, EPI_VOCAB, &vo, st));
+  LAUNCH(MT_KERNEL_LSE, launch_lse(M, L.ntiles, vo.part, (float *)(W + L.lse), logp_out, V, st));
+  model->last_B = B;
+  model->last_K = K;
+  model->last_ws = ws;
+  return MT_OK;
+}
+
+mt_status mt_beam_topk(mt_model *model, int B, int K, const float *prev_score, const float *logp,
+                       float *score_out, int32_t *tok_out, int32_t *bp_out, int32_t *row_out,
+                       void *ws, size_t ws_bytes, void *stream) {
+  g_err[0] = 0;
+  if (!valid_model(model)) return fail(MT_ERR_ARG, "invalid model handle");
+  const mt_config &c = model->cfg;
+  if (B < 1 || K < 1 || K > c.k_max || K > c.V) return fail(MT_ERR_SHAPE, "B=%d K=%d: need B >= 1, 1 <= K <= k_max", B, K);
+  if ((long long)B * K > (1 << 20)) return fail(MT_ERR_SHAPE, "B*K exceeds 2^20");
+  CHECK(check_dev_ptr(prev_score, "prev_score", 4));
+  CHECK(check_dev_ptr(score_out, "score_out", 4));
+  CHECK(check_dev_ptr(tok_out, "tok_out", 4));
+  CHECK(check_dev_ptr(bp_out, "bp_out", 4));
+  if (row_out) CHECK(check_dev_ptr(row_out, "row_out", 4));
+  if (logp) CHECK(check_dev_ptr(logp, "logp", 4));
+  CHECK(check_dev_ptr(ws, "ws", 256));
+  const WsLayout L = ws_layout(model, B, K);
+  if (ws_bytes < L.total) return fail(MT_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, L.total);
+  if (!logp && (model->last_B != B || model->last_K != K || model->last_ws != ws))
+    return fail(MT_ERR_STATE, "no preceding mt_decoder_step with this B, K and workspace (pass logp instead)");
+  hipStream_t st = (hipStream_t)stream;
+  char *W = (char *)ws;
+  const int M = B * K, V = c.V;
+  int2 *rowc = (int2 *)(W + L.rowc);
+  if (!logp) {
+    LAUNCH(MT_KERNEL_TOPK, launch_topk_rows(M, K, V, L.ntiles * L.kc, (const int2 *)(W + L.cand),
+                                            (const float *)(W + L.lse), prev_score, rowc, st));
+  } else {
+    int2 *sc = (int2 *)(W + L.scand);
+    LAUNCH(MT_KERNEL_TOPK, launch_topk_scan_logp(M, K, V, L.nchunks, prev_score, logp, sc, st));
+    LAUNCH(MT_KERNEL_TOPK, launch_topk_rows(M, K, V, L.nchunks * K, sc, nullptr, nullptr, rowc, st));
+  }
+  LAUNCH(MT_KERNEL_TOPK, launch_topk_sentence(B, K, V, rowc, score_out, tok_out, bp_out, row_out, st));
+  return MT_OK;
+}
+
+mt_status mt_device_errors(mt_model *model, int32_t *flags) {
+  g_err[0] = 0;
+  if (!valid_model(model)) return fail(MT_ERR_ARG, "invalid model handle");
+  if (!flags) return fail(MT_ERR_ARG, "flags is NULL");
+  HIP_TRY(hipDeviceSynchronize());
+  HIP_TRY(hipMemcpy(flags, model->err, 4, hipMemcpyDeviceToHost));
+  HIP_TRY(hipMemset(model->err, 0, 4));
+  return MT_OK;
+}
+
+mt_status mt_profile_enable(mt_model *model, int on) {
+  g_err[0] = 0;
+  if (!valid_model(model)) return fail(MT_ERR_ARG, "invalid model handle");
+  model->prof_on = on != 0;
+  return MT_OK;
+}
+
+mt_status mt_profile_reset(mt_model *model) {
+  g_err[0] = 0;
+  if (!valid_model(model)) return fail(MT_ERR_ARG, "invalid model handle");
+  for (int k = 0; k < MT_KERNEL_COUNT; ++k) {
+    fold_profile(model, k);
+    model->prof[k].ms = 0.0;
+    model->prof[k].n = 0;
+  }
+  return MT_OK;
+}
+
+mt_status mt_profile_query(mt_model *model, int kernel, double *total_ms, int64_t *launches) {
+  g_err[0] = 0;
+  if (!valid_model(model)) return fail(MT_ERR_ARG, "invalid model handle");
+  if (kernel < 0 || kernel >= MT_KERNEL_COUNT) return fail(MT_ERR_ARG, "kernel id %d out of range", kernel);
+  if (!total_ms || !launches) return fail(MT_ERR_ARG, "output pointer is NULL");
+  fold_profile(model, kernel);
+  *total_ms = model->prof[kernel].ms;
+  *launches = model->prof[kernel].n;
+  return MT_OK;
+}
+
+}  // extern "C"

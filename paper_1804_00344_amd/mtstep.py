@@ -1,0 +1,201 @@
+"""ctypes binding of libmtstep (declarations in include/mtstep.h).
+
+Argument marshalling only: every step of the decoder runs in the library's HIP
+kernels.  Device buffers are passed as torch tensors (or raw integer device
+addresses); streams as torch streams (default: torch's current stream).  The
+binding raises if the built library is missing — there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import Dict, Optional
+
+import numpy as np
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libmtstep.so")
+
+MT_OK, MT_ERR_ARG, MT_ERR_SHAPE, MT_ERR_DTYPE, MT_ERR_HIP, MT_ERR_OOM, MT_ERR_STATE, MT_ERR_WORKSPACE = (
+    0, -1, -2, -3, -4, -5, -6, -7)
+MT_F32, MT_BF16 = 0, 1
+KERNELS = ["GEMM_GRU1", "GRU_CELL", "GEMM_S1", "ATTENTION", "GEMM_CTX", "GEMM_READOUT", "READOUT",
+           "VOCAB_GEMM", "LSE", "TOPK", "PRECOMPUTE"]
+KERNEL_ID = {n: i for i, n in enumerate(KERNELS)}
+
+
+class MtError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"libmtstep status {status}: {msg}")
+        self.status = status
+
+
+class mt_config(C.Structure):
+    _fields_ = [("E", C.c_int32), ("H", C.c_int32), ("A", C.c_int32), ("V", C.c_int32),
+                ("layer_norm", C.c_int32), ("tied_output", C.c_int32), ("k_max", C.c_int32),
+                ("gemm_dtype", C.c_int32), ("ln_eps", C.c_float)]
+
+
+WEIGHT_FIELDS = ["emb", "W1", "U1", "b1", "Ua", "ba", "Wa", "va", "W2", "U2", "b2", "Wt_s", "Wt_y",
+                 "Wt_c", "bt", "Wo", "bo", "Wi", "bi", "g1a", "be1a", "g1u", "be1u", "g2a", "be2a",
+                 "g2u", "be2u", "gt", "bet"]
+
+_fp = C.POINTER(C.c_float)
+
+
+class mt_weights(C.Structure):
+    _fields_ = [(n, _fp) for n in WEIGHT_FIELDS]
+
+
+class mt_taps(C.Structure):
+    _fields_ = [("s1", C.c_void_p), ("c", C.c_void_p), ("t", C.c_void_p)]
+
+
+_lib = None
+_vp = C.c_void_p
+
+
+def lib() -> C.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
+                               "(python -m paper_1804_00344_amd.build)")
+        L = C.CDLL(LIB_PATH)
+        L.mt_last_error.restype = C.c_char_p
+        L.mt_last_error.argtypes = []
+        L.mt_load_weights.argtypes = [C.POINTER(mt_config), C.POINTER(mt_weights), C.POINTER(_vp)]
+        L.mt_free.argtypes = [_vp]
+        L.mt_workspace_bytes.argtypes = [_vp, C.c_int, C.c_int, C.c_int]
+        L.mt_workspace_bytes.restype = C.c_size_t
+        L.mt_precompute_ctx.argtypes = [_vp, C.c_int, C.c_int, _vp, _vp, _vp, _vp, _vp, C.c_size_t, _vp]
+        L.mt_decoder_step.argtypes = [_vp, C.c_int, C.c_int, C.c_int, _vp, _vp, C.c_int, _vp, _vp, _vp,
+                                      _vp, _vp, _vp, _vp, C.POINTER(mt_taps), _vp, C.c_size_t, _vp]
+        L.mt_beam_topk.argtypes = [_vp, C.c_int, C.c_int, _vp, _vp, _vp, _vp, _vp, _vp, _vp, C.c_size_t, _vp]
+        L.mt_device_errors.argtypes = [_vp, C.POINTER(C.c_int32)]
+        L.mt_profile_enable.argtypes = [_vp, C.c_int]
+        L.mt_profile_reset.argtypes = [_vp]
+        L.mt_profile_query.argtypes = [_vp, C.c_int, C.POINTER(C.c_double), C.POINTER(C.c_int64)]
+        for f in ("mt_load_weights", "mt_free", "mt_precompute_ctx", "mt_decoder_step", "mt_beam_topk",
+                  "mt_device_errors", "mt_profile_enable", "mt_profile_reset", "mt_profile_query"):
+            getattr(L, f).restype = C.c_int
+        _lib = L
+    return _lib
+
+
+def _check(rc: int):
+    if rc != MT_OK:
+        raise MtError(rc, lib().mt_last_error().decode())
+
+
+def _ptr(x) -> Optional[int]:
+    """Device address of a torch tensor (contiguous), an int, or None."""
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    if not x.is_contiguous():
+        raise ValueError("tensor must be contiguous")
+    return x.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def make_config(E, H, A, V, *, layer_norm=False, tied_output=False, k_max=16, gemm="f32", ln_eps=1e-5):
+    return mt_config(E, H, A, V, int(layer_norm), int(tied_output), k_max,
+                     MT_BF16 if gemm == "bf16" else MT_F32, ln_eps)
+
+
+class Model:
+    """Owns an mt_model handle (freed with mt_free)."""
+
+    def __init__(self, handle: int, cfg: mt_config):
+        self.handle = handle
+        self.cfg = cfg
+
+    def __del__(self):
+        if getattr(self, "handle", None):
+            try:
+                lib().mt_free(self.handle)
+            except Exception:
+                pass
+            self.handle = None
+
+
+def mt_load_weights(cfg: mt_config, weights: Dict[str, np.ndarray]) -> Model:
+    """weights: host fp32 arrays by field name (see mt_weights)."""
+    keep = {}
+    w = mt_weights()
+    for n in WEIGHT_FIELDS:
+        a = weights.get(n)
+        if a is None:
+            continue
+        a = np.ascontiguousarray(a, dtype=np.float32)
+        keep[n] = a
+        setattr(w, n, a.ctypes.data_as(_fp))
+    h = _vp()
+    _check(lib().mt_load_weights(C.byref(cfg), C.byref(w), C.byref(h)))
+    return Model(h.value, cfg)
+
+
+def mt_free(model: Model):
+    if model.handle:
+        _check(lib().mt_free(model.handle))
+        model.handle = None
+
+
+def mt_workspace_bytes(model: Model, B: int, K: int, S: int) -> int:
+    return int(lib().mt_workspace_bytes(model.handle, B, K, S))
+
+
+def mt_precompute_ctx(model: Model, B, S, ctx, mask, pctx_out, s0_out, ws, ws_bytes=None, stream=None):
+    ws_bytes = ws.numel() * ws.element_size() if ws_bytes is None else ws_bytes
+    _check(lib().mt_precompute_ctx(model.handle, B, S, _ptr(ctx), _ptr(mask), _ptr(pctx_out), _ptr(s0_out),
+                                   _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def mt_decoder_step(model: Model, B, K, S, prev_tok, src_row, n_state_rows, state_in, ctx, pctx, mask,
+                    state_out, logp_out=None, attn_out=None, taps=None, ws=None, ws_bytes=None, stream=None):
+    ws_bytes = ws.numel() * ws.element_size() if ws_bytes is None else ws_bytes
+    tp = None
+    if taps:
+        tp = mt_taps(_ptr(taps.get("s1")), _ptr(taps.get("c")), _ptr(taps.get("t")))
+    _check(lib().mt_decoder_step(model.handle, B, K, S, _ptr(prev_tok), _ptr(src_row), n_state_rows,
+                                 _ptr(state_in), _ptr(ctx), _ptr(pctx), _ptr(mask), _ptr(state_out),
+                                 _ptr(logp_out), _ptr(attn_out), C.byref(tp) if tp is not None else None,
+                                 _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def mt_beam_topk(model: Model, B, K, prev_score, logp, score_out, tok_out, bp_out, row_out=None, ws=None,
+                 ws_bytes=None, stream=None):
+    ws_bytes = ws.numel() * ws.element_size() if ws_bytes is None else ws_bytes
+    _check(lib().mt_beam_topk(model.handle, B, K, _ptr(prev_score), _ptr(logp), _ptr(score_out), _ptr(tok_out),
+                              _ptr(bp_out), _ptr(row_out), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def mt_device_errors(model: Model) -> int:
+    f = C.c_int32(0)
+    _check(lib().mt_device_errors(model.handle, C.byref(f)))
+    return int(f.value)
+
+
+def mt_profile_enable(model: Model, on: bool = True):
+    _check(lib().mt_profile_enable(model.handle, int(on)))
+
+
+def mt_profile_reset(model: Model):
+    _check(lib().mt_profile_reset(model.handle))
+
+
+def mt_profile_query(model: Model, kernel) -> tuple:
+    k = KERNEL_ID[kernel] if isinstance(kernel, str) else int(kernel)
+    ms, n = C.c_double(0), C.c_int64(0)
+    _check(lib().mt_profile_query(model.handle, k, C.byref(ms), C.byref(n)))
+    return float(ms.value), int(n.value)

@@ -1,0 +1,97 @@
+"""Device-buffer harness around the libmtstep calls (allocation and call order only).
+
+Holds a loaded model, one batch's device inputs (context, mask, attention keys,
+start state), a workspace and ping-pong state/beam buffers, and issues
+mt_precompute_ctx / mt_decoder_step / mt_beam_topk in decode order.  torch
+provides device memory and the stream; all arithmetic runs in libmtstep.
+"""
+from __future__ import annotations
+
+from typing import Dict, Optional
+
+import numpy as np
+import torch
+
+from . import mtstep as mt
+
+
+class Decoder:
+    def __init__(self, E: int, H: int, A: int, V: int, weights: Dict[str, np.ndarray], *, gemm: str = "f32",
+                 layer_norm: bool = False, tied_output: bool = False, k_max: int = 16, ln_eps: float = 1e-5,
+                 device: str = "cuda:0"):
+        self.E, self.H, self.A, self.V, self.C = E, H, A, V, 2 * H
+        self.gemm = gemm
+        self.device = torch.device(device)
+        self.cfg = mt.make_config(E, H, A, V, layer_norm=layer_norm, tied_output=tied_output, k_max=k_max,
+                                  gemm=gemm, ln_eps=ln_eps)
+        with torch.cuda.device(self.device):
+            self.model = mt.mt_load_weights(self.cfg, weights)
+        self.io_dtype = torch.bfloat16 if gemm == "bf16" else torch.float32
+
+    @classmethod
+    def from_preset(cls, p, weights, **kw):
+        return cls(p.E, p.H, p.A, p.V, weights, gemm=p.gemm, layer_norm=p.layer_norm, k_max=max(p.K, 1), **kw)
+
+    # ---- batch ------------------------------------------------------------------------
+    def set_batch(self, ctx: np.ndarray, mask: np.ndarray, K: int):
+        B, S, Cd = ctx.shape
+        assert Cd == self.C and mask.shape == (B, S)
+        d = self.device
+        self.B, self.S, self.K, self.M = B, S, K, B * K
+        self.ctx = torch.from_numpy(np.ascontiguousarray(ctx, np.float32)).to(d).to(self.io_dtype).contiguous()
+        self.mask = torch.from_numpy(np.ascontiguousarray(mask, np.float32)).to(d)
+        self.pctx = torch.empty((B, S, self.A), dtype=self.io_dtype, device=d)
+        self.s0 = torch.empty((B, self.H), dtype=torch.float32, device=d)
+        nbytes = mt.mt_workspace_bytes(self.model, B, K, S)
+        assert nbytes > 0
+        self.ws = torch.empty(nbytes, dtype=torch.uint8, device=d)
+        M = self.M
+        self.state = [torch.empty((M, self.H), dtype=torch.float32, device=d) for _ in range(2)]
+        self.tok = torch.empty(M, dtype=torch.int32, device=d)
+        self.row = torch.empty(M, dtype=torch.int32, device=d)
+        self.bp = torch.empty(M, dtype=torch.int32, device=d)
+        self.score = torch.empty(M, dtype=torch.float32, device=d)
+        self.cur = 0
+
+    def precompute(self, stream=None):
+        mt.mt_precompute_ctx(self.model, self.B, self.S, self.ctx, self.mask, self.pctx, self.s0, self.ws,
+                             stream=stream)
+
+    def step(self, prev_tok, src_row, state_in, n_state_rows: int, state_out, *, logp=None, attn=None,
+             taps=None, stream=None):
+        mt.mt_decoder_step(self.model, self.B, self.K, self.S, prev_tok, src_row, n_state_rows, state_in, self.ctx,
+                           self.pctx, self.mask, state_out, logp_out=logp, attn_out=attn, taps=taps, ws=self.ws,
+                           stream=stream)
+
+    def topk(self, prev_score, logp=None, *, score_out=None, tok_out=None, bp_out=None, row_out=None,
+             stream=None):
+        score_out = self.score if score_out is None else score_out
+        tok_out = self.tok if tok_out is None else tok_out
+        bp_out = self.bp if bp_out is None else bp_out
+        row_out = self.row if row_out is None else row_out
+        mt.mt_beam_topk(self.model, self.B, self.K, prev_score, logp, score_out, tok_out, bp_out, row_out,
+                        ws=self.ws, stream=stream)
+        return score_out, tok_out, bp_out, row_out
+
+    # ---- decode loop ------------------------------------------------------------------
+    def start(self, tok0: np.ndarray, score0: np.ndarray):
+        """Beam start: every row reads its sentence's start state (src_row = m // K)."""
+        d = self.device
+        self.tok.copy_(torch.from_numpy(np.ascontiguousarray(tok0, np.int32)).to(d))
+        self.row.copy_(torch.arange(self.M, dtype=torch.int32, device=d) // self.K)
+        self.score.copy_(torch.from_numpy(np.ascontiguousarray(score0, np.float32)).to(d))
+        self.first = True
+
+    def advance(self, *, logp=None, attn=None, stream=None):
+        """One beam-search step: decoder step on the current beam, then top-K in place."""
+        if self.first:
+            state_in, nrows = self.s0, self.B
+        else:
+            state_in, nrows = self.state[self.cur], self.M
+        out = self.state[1 - self.cur] if not self.first else self.state[self.cur]
+        self.step(self.tok, self.row, state_in, nrows, out, logp=logp, attn=attn, stream=stream)
+        self.topk(self.score, None, stream=stream)
+        if not self.first:
+            self.cur = 1 - self.cur
+        self.first = False
+        return self.state[self.cur]

@@ -1,0 +1,316 @@
+"""GPU path (libmtstep through its C ABI) against the CPU oracle on seeded inputs."""
+import math
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import mtref
+from paper_1804_00344_amd import synth
+from tests.parity_util import TOL, maxerr, oracle_model, oracle_sentences, sample_sentences, topk_gap_check
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # pragma: no cover - collected on CPU-only machines
+    pytestmark = [pytest.mark.gpu, pytest.mark.skip(reason="no GPU")]
+else:
+    from paper_1804_00344_amd.runner import Decoder
+    from paper_1804_00344_amd import mtstep as mt
+
+DEV = "cuda:0"
+
+
+def log(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def T(x, dtype=None):
+    t = torch.from_numpy(np.ascontiguousarray(x)).to(DEV)
+    return t if dtype is None else t.to(dtype)
+
+
+_cache = {}
+
+
+def setup(name, peaked=False, nan_padding=False):
+    key = (name, peaked, nan_padding)
+    if key not in _cache:
+        p = synth.PRESETS[name]
+        w = synth.make_weights(p, peaked_bias=peaked)
+        ctx, mask, lens = synth.make_source(p, nan_padding=nan_padding)
+        dec = Decoder.from_preset(p, w)
+        dec.set_batch(ctx, mask, p.K)
+        dec.precompute()
+        _cache.clear()
+        _cache[key] = (p, w, ctx, mask, lens, dec)
+    return _cache[key]
+
+
+def run_step(dec, p, tok, src, state, nrows, logp=True, attn=True, taps=True):
+    M = p.M
+    out = {"state": torch.empty((M, p.H), device=DEV)}
+    if logp:
+        out["logp"] = torch.empty((M, p.V), device=DEV)
+    if attn:
+        out["alpha"] = torch.empty((M, dec.S), device=DEV)
+    tp = None
+    if taps:
+        tp = {"s1": torch.empty((M, p.H), device=DEV), "c": torch.empty((M, p.C), device=DEV),
+              "t": torch.empty((M, p.E), device=DEV)}
+        out.update(tp)
+    dec.step(T(tok), T(src), state, nrows, out["state"], logp=out.get("logp"), attn=out.get("alpha"), taps=tp)
+    return out
+
+
+def compare_rows(p, gpu, orc, sents, tol, label):
+    K = p.K
+    errs = {}
+    for b in sents:
+        rows = slice(b * K, (b + 1) * K)
+        o = orc[b]
+        for k, tk in (("state", "state"), ("logp", "logp"), ("alpha", "alpha"), ("s1", "s1"), ("c", "c"), ("t", "t")):
+            if tk not in gpu or k not in o:
+                continue
+            g = gpu[tk][rows].float().cpu().numpy()
+            errs[k] = max(errs.get(k, 0.0), maxerr(g, o[k]))
+        if "alpha" in gpu:
+            a = gpu["alpha"][rows].cpu().numpy()
+            L = int((o["alpha"][0] != 0).sum()) if o["alpha"].size else 0
+            assert np.all(np.abs(a.sum(1) - 1.0) <= 1e-5), (label, b, a.sum(1))
+    log(f"[{label}] max errors over sentences {sents[:8]}{'...' if len(sents) > 8 else ''}: "
+        + ", ".join(f"{k}={v:.3g}" for k, v in errs.items()))
+    assert errs["state"] <= tol["state"], (label, errs)
+    if "logp" in errs:
+        assert errs["logp"] <= tol["logp"], (label, errs)
+    if "alpha" in errs:
+        assert errs["alpha"] <= tol["alpha"], (label, errs)
+    for k in ("s1", "c", "t"):
+        if k in errs:
+            assert errs[k] <= tol["tap"], (label, k, errs)
+    return errs
+
+
+def masked_alpha_zero(p, gpu_alpha, mask):
+    a = gpu_alpha.cpu().numpy().reshape(p.B, p.K, -1)
+    m = mask[:, None, :] == 0
+    assert np.all(a[np.broadcast_to(m, a.shape)] == 0.0)
+
+
+# ------------------------------------------------------------------------------------------
+# one step from a synthetic mid-decode beam: every preset
+# ------------------------------------------------------------------------------------------
+
+N_SAMPLE = {"tiny_f32": 99, "tiny_bf16_ln": 99, "nematus_f32": 4, "nematus_bf16_ln": 4,
+            "vocab85k_bf16_ln": 4, "greedy_bf16_ln": 16}
+
+
+@pytest.mark.parametrize("name", list(N_SAMPLE))
+def test_step_parity_mid_decode(name):
+    log(f"\n[step parity] preset={name}")
+    p, w, ctx, mask, lens, dec = setup(name, peaked=True)
+    tok, src, state, score = synth.mid_decode_inputs(p, salt=1)
+    gpu = run_step(dec, p, tok, src, T(state), p.M)
+    # fused top-K (candidates from the vocabulary GEMM epilogue)
+    sc, tk, bp, rw = [x.cpu().numpy() for x in dec.topk(T(score), None)]
+    # materialised top-K on the GPU's own log-probs
+    sc2, tk2, bp2, _ = [x.cpu().numpy() for x in dec.topk(T(score), gpu["logp"], score_out=torch.empty_like(dec.score),
+                                                          tok_out=torch.empty_like(dec.tok), bp_out=torch.empty_like(dec.bp),
+                                                          row_out=torch.empty_like(dec.row))]
+    torch.cuda.synchronize()
+    assert mt.mt_device_errors(dec.model) == 0
+    sents = sample_sentences(lens, N_SAMPLE[name])
+    orc = oracle_sentences(oracle_model(p, w), p.K, sents, ctx, mask, tok, src, state)
+    tol = TOL[p.gemm]
+    compare_rows(p, gpu, orc, sents, tol, name)
+    masked_alpha_zero(p, gpu["alpha"], mask)
+    dec_slots = tot = 0
+    for b in sents:
+        rows = slice(b * p.K, (b + 1) * p.K)
+        d, n = topk_gap_check(p.K, score[rows], orc[b]["logp"], sc[rows], tk[rows], bp[rows], tol["logp"])
+        dec_slots += d
+        tot += n
+        assert np.array_equal(rw[rows], b * p.K + bp[rows])
+    log(f"[{name}] top-K decided slots {dec_slots}/{tot}")
+    # the materialised path is an exact sort of the GPU's own log-probs
+    lp = gpu["logp"].cpu().numpy()
+    t3, b3, s3 = mtref.topk(p.K, score, lp)
+    assert np.array_equal(tk2, t3) and np.array_equal(bp2, b3) and np.array_equal(sc2, s3)
+    # fused and materialised selections agree (the GPU's keys are computed identically)
+    same = np.mean((tk == tk2) & (bp == bp2))
+    log(f"[{name}] fused vs materialised top-K agreement {same:.4f}")
+    assert np.array_equal(sc, sc2)
+
+
+@pytest.mark.parametrize("name", list(N_SAMPLE))
+def test_precompute_parity(name):
+    log(f"\n[precompute parity] preset={name}")
+    p, w, ctx, mask, lens, dec = setup(name, peaked=True)
+    dec.precompute()
+    P = dec.pctx.float().cpu().numpy()
+    s0 = dec.s0.cpu().numpy()
+    sents = sample_sentences(lens, N_SAMPLE[name])
+    om = oracle_model(p, w)
+    tol = 1e-4 if p.gemm == "f32" else 5e-2
+    eP = es = 0.0
+    for b in sents:
+        Po, so = om.precompute(ctx[b:b + 1], mask[b:b + 1])
+        L = int(lens[b])
+        eP = max(eP, maxerr(P[b, :L], Po[0, :L]))
+        es = max(es, maxerr(s0[b], so[0]))
+    log(f"[{name}] P err {eP:.3g}  s0 err {es:.3g}")
+    assert eP <= tol and es <= tol
+
+
+# ------------------------------------------------------------------------------------------
+# beam-search trajectories on the tiny preset: GPU and oracle run their own beams from the
+# same start; each sentence is compared until its first undecided (near-tie) selection
+# ------------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name", ["tiny_f32", "tiny_bf16_ln"])
+def test_tiny_trajectory(name):
+    log(f"\n[trajectory] preset={name}")
+    p, w, ctx, mask, lens, dec = setup(name, peaked=True)
+    tol = TOL[p.gemm]
+    om = oracle_model(p, w)
+    Po, s0o = om.precompute(ctx, mask)
+    tok0, src0, score0 = synth.start_beam(p)
+    dec.precompute()
+    dec.start(tok0, score0)
+    o_tok, o_src, o_state, o_score = tok0.copy(), src0.copy(), s0o, score0.copy()
+    alive = np.ones(p.B, bool)
+    logp = torch.empty((p.M, p.V), device=DEV)
+    compared = 0
+    for t in range(p.steps):
+        state = dec.advance(logp=logp)
+        g_score, g_tok, g_bp, g_row = [x.cpu().numpy() for x in (dec.score, dec.tok, dec.bp, dec.row)]
+        g_state = state.cpu().numpy()
+        out = om.step(p.K, o_tok, o_src, o_state, ctx, Po, mask)
+        n_tok, n_bp, n_score = mtref.topk(p.K, o_score, out["logp"])
+        for b in range(p.B):
+            if not alive[b]:
+                continue
+            rows = slice(b * p.K, (b + 1) * p.K)
+            topk_gap_check(p.K, o_score[rows], out["logp"][rows], g_score[rows], g_tok[rows], g_bp[rows],
+                           tol["logp"] * (t + 1))
+            same = np.array_equal(g_tok[rows], n_tok[rows]) and np.array_equal(g_bp[rows], n_bp[rows])
+            if not same:
+                alive[b] = False
+                log(f"[{name}] sentence {b} leaves the comparison at step {t} (near-tie)")
+                continue
+            # the new beam's states: GPU state_out rows vs oracle rows (before reordering)
+            err = maxerr(g_state[rows], out["state"][rows])
+            assert err <= tol["state"], (name, t, b, err)
+            compared += 1
+        o_tok, o_bp, o_score = n_tok, n_bp, n_score
+        o_src = ((np.arange(p.M) // p.K) * p.K + o_bp).astype(np.int32)
+        o_state = out["state"]
+    log(f"[{name}] compared {compared} sentence-steps; alive at end {alive.sum()}/{p.B}")
+    assert compared >= p.steps  # at least one sentence's worth of steps compared
+
+
+# ------------------------------------------------------------------------------------------
+# top-K on given log-probabilities: bit-exact against the oracle's full sort
+# ------------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("K,V", [(1, 16), (2, 7), (3, 1000), (5, 85000), (12, 50000), (16, 50000), (16, 16), (4, 2049)])
+def test_topk_given_logp_bit_exact(K, V):
+    log(f"\n[topk] K={K} V={V}")
+    B = 6
+    rng = np.random.default_rng(K * 1000 + V)
+    p = synth.with_sizes(synth.PRESETS["tiny_f32"], V=max(V, 16), K=K, B=B)
+    w = synth.make_weights(p)
+    dec = Decoder(p.E, p.H, p.A, p.V, w, k_max=16)
+    ctx, mask, _ = synth.make_source(p)
+    dec.set_batch(ctx, mask, K)
+    # heavy ties: values from a small set, plus some -inf scores
+    logp = rng.choice(np.array([-1.0, -2.0, -2.5, -3.0, -7.25], np.float32), size=(B * K, p.V))
+    logp[:, ::7] += rng.standard_normal((B * K, len(range(0, p.V, 7)))).astype(np.float32)
+    score = rng.choice(np.array([0.0, -0.5, -1.0], np.float32), size=B * K)
+    score[1] = -np.inf
+    g = [x.cpu().numpy() for x in dec.topk(T(score), T(logp))]
+    t, b, s = mtref.topk(K, score, logp)
+    assert np.array_equal(g[1], t) and np.array_equal(g[2], b) and np.array_equal(g[0], s)
+    assert np.array_equal(g[3], (np.arange(B * K) // K) * K + b)
+
+
+# ------------------------------------------------------------------------------------------
+# properties
+# ------------------------------------------------------------------------------------------
+
+def test_determinism_and_nan_padding():
+    log("\n[determinism / NaN padding] nematus_bf16_ln")
+    p, w, ctx, mask, lens, dec = setup("nematus_bf16_ln", peaked=True)
+    tok, src, state, score = synth.mid_decode_inputs(p, salt=2)
+    dec.precompute()
+    outs = []
+    for _ in range(3):
+        o = run_step(dec, p, tok, src, T(state), p.M, taps=False)
+        s = [x.clone() for x in dec.topk(T(score), None)]
+        torch.cuda.synchronize()
+        outs.append((o, s))
+    for o, s in outs[1:]:
+        for k in o:
+            assert torch.equal(o[k], outs[0][0][k]), k
+        for a, b in zip(s, outs[0][1]):
+            assert torch.equal(a, b)
+    # same inputs with NaN in every padded position of the context: nothing changes
+    ctx_nan = ctx.copy()
+    ctx_nan[mask == 0] = np.nan
+    dec.set_batch(ctx_nan, mask, p.K)
+    dec.precompute()
+    o = run_step(dec, p, tok, src, T(state), p.M, taps=False)
+    s = dec.topk(T(score), None)
+    torch.cuda.synchronize()
+    for k in o:
+        assert torch.equal(o[k], outs[0][0][k]), k
+    for a, b in zip(s, outs[0][1]):
+        assert torch.equal(a, b)
+    assert torch.isfinite(dec.s0).all()
+    _cache.clear()
+
+
+def test_out_of_range_indices_are_clamped_and_flagged():
+    p, w, ctx, mask, lens, dec = setup("tiny_f32")
+    tok, src, state, score = synth.mid_decode_inputs(p, salt=3)
+    assert mt.mt_device_errors(dec.model) == 0
+    bad_tok = tok.copy()
+    bad_tok[3] = p.V + 5
+    run_step(dec, p, bad_tok, src, T(state), p.M, taps=False)
+    assert mt.mt_device_errors(dec.model) == 1
+    bad_src = src.copy()
+    bad_src[0] = -2
+    run_step(dec, p, tok, bad_src, T(state), p.M, taps=False)
+    assert mt.mt_device_errors(dec.model) == 2
+    assert mt.mt_device_errors(dec.model) == 0
+
+
+def test_abi_errors_on_gpu():
+    p, w, ctx, mask, lens, dec = setup("tiny_f32")
+    tok, src, state, score = synth.mid_decode_inputs(p, salt=4)
+    st = T(state)
+    out = torch.empty((p.M, p.H), device=DEV)
+    small = torch.empty(256, dtype=torch.uint8, device=DEV)
+    with pytest.raises(mt.MtError) as e:
+        mt.mt_decoder_step(dec.model, p.B, p.K, dec.S, T(tok), T(src), p.M, st, dec.ctx, dec.pctx, dec.mask, out,
+                           ws=small)
+    assert e.value.status == mt.MT_ERR_WORKSPACE
+    with pytest.raises(mt.MtError) as e:
+        mt.mt_decoder_step(dec.model, p.B, p.K, dec.S, T(tok), T(src), p.M, st, dec.ctx, dec.pctx, dec.mask, st,
+                           ws=dec.ws)
+    assert e.value.status == mt.MT_ERR_ARG  # state_out aliases state_in
+    with pytest.raises(mt.MtError) as e:
+        mt.mt_decoder_step(dec.model, p.B, p.K + 1, dec.S, T(tok), T(src), p.M, st, dec.ctx, dec.pctx, dec.mask,
+                           out, ws=dec.ws)
+    assert e.value.status == mt.MT_ERR_SHAPE  # K > k_max
+    # top-K from the workspace with a different workspace than the step's
+    ws2 = torch.empty_like(dec.ws)
+    with pytest.raises(mt.MtError) as e:
+        mt.mt_beam_topk(dec.model, p.B, p.K, T(score), None, dec.score, dec.tok, dec.bp, dec.row, ws=ws2)
+    assert e.value.status == mt.MT_ERR_STATE
+    misaligned = dec.ws[1:]
+    with pytest.raises(mt.MtError) as e:
+        mt.mt_decoder_step(dec.model, p.B, p.K, dec.S, T(tok), T(src), p.M, st, dec.ctx, dec.pctx, dec.mask, out,
+                           ws=misaligned)
+    assert e.value.status == mt.MT_ERR_ARG
