@@ -1,0 +1,210 @@
+#!/usr/bin/env python3
+"""Throughput of the batched beam-search decoder step on one MI355X.
+
+A bench step is one pass of the whole hot path over the batch: mt_decoder_step
+(cGRU 1, attention, cGRU 2, readout, vocabulary GEMM with fused log-sum-exp and
+per-tile top-K) followed by mt_beam_topk.  Every `preset.steps` steps a new
+decode starts: mt_precompute_ctx (attention keys and start state) runs inside
+the timed region at that rate, as it would when translating batch after batch.
+Inputs are synthetic and already resident in HBM when timing starts.
+
+    python bench.py [--steps K] [--warmup W] [--preset nematus_f32]
+
+Prints one JSON line (see README of the driver contract): steps/s for the whole
+batch, the dominant kernel's roofline fraction (timed with HIP events on its
+launch stream) and the CPU oracle's rate on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "beam decoder steps/s (B×K hyp-rows/s) + % of HBM BW / bf16 MFMA peak"
+PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}
+HBM_GBS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def source_hash(path):
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+
+
+def cpu_baseline(p, w, ctx, mask, budget_s=15.0):
+    """The oracle (single-threaded C, double accumulation) on whole sentences of the same
+    workload: one precompute + decoder step + top-K per sentence, scaled to full-batch steps/s
+    with the precompute amortised over preset.steps steps."""
+    import numpy as np
+    from oracle import mtref
+    from paper_1804_00344_amd import synth
+
+    om = mtref.Model(p.E, p.H, p.A, p.V, w, layer_norm=p.layer_norm)
+    tok, src, state, score = synth.mid_decode_inputs(p, salt=11)
+    t_pre = t_step = 0.0
+    n = 0
+    t_start = time.perf_counter()
+    while n < p.B and (time.perf_counter() - t_start) < budget_s:
+        b = n
+        rows = slice(b * p.K, (b + 1) * p.K)
+        t0 = time.perf_counter()
+        P, s0 = om.precompute(ctx[b:b + 1], mask[b:b + 1])
+        t1 = time.perf_counter()
+        out = om.step(p.K, tok[rows], (src[rows] - b * p.K).astype(np.int32), state[rows], ctx[b:b + 1], P,
+                      mask[b:b + 1], want_alpha=False)
+        mtref.topk(p.K, score[rows], out["logp"])
+        t2 = time.perf_counter()
+        t_pre += t1 - t0
+        t_step += t2 - t1
+        n += 1
+    per_sentence = t_step / n + t_pre / n / p.steps
+    steps_per_s = 1.0 / (per_sentence * p.B)
+    return {
+        "value": steps_per_s,
+        "unit": "steps/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": f"{n} of {p.B} sentences ({n * p.K} hyp rows), one step each + their start-state precompute "
+                  f"amortised over {p.steps} steps; {t_pre + t_step:.1f} s of CPU; scaled linearly to the batch",
+        "hyp_rows_per_s": steps_per_s * p.M,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--preset", default="nematus_f32")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--copy-calib-mib", type=int, default=0,
+                    help="also run one device copy of this size (counter calibration under rocprofv3)")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(decoding shards by sentence with no exchange; see the design notes)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_1804_00344_amd import mtstep as mt
+    from paper_1804_00344_amd import synth
+    from paper_1804_00344_amd.runner import Decoder
+
+    p = synth.PRESETS[args.preset]
+    log(f"[bench] preset {p.name}: B={p.B} K={p.K} E={p.E} H={p.H} A={p.A} V={p.V} gemm={p.gemm} ln={p.layer_norm}")
+    w = synth.make_weights(p)
+    ctx, mask, lens = synth.make_source(p)
+    dec = Decoder.from_preset(p, w)
+    dec.set_batch(ctx, mask, p.K)
+    tok0, src0, score0 = synth.start_beam(p)
+    stream = torch.cuda.current_stream()
+
+    def run(n, first_index):
+        for i in range(first_index, first_index + n):
+            if i % p.steps == 0:
+                dec.precompute()
+                dec.start(tok0, score0)
+            dec.advance()
+
+    log("[bench] warmup")
+    run(args.warmup, 0)
+    torch.cuda.synchronize()
+    mt.mt_profile_enable(dec.model, ("VOCAB_GEMM",))
+    mt.mt_profile_reset(dec.model)
+    log(f"[bench] timing {args.steps} steps")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    run(args.steps, args.warmup)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    vocab_ms, vocab_n = mt.mt_profile_query(dec.model, "VOCAB_GEMM")
+    mt.mt_profile_enable(dec.model, ())
+    assert mt.mt_device_errors(dec.model) == 0
+
+    # per-kernel breakdown (separate pass, every class timed)
+    mt.mt_profile_enable(dec.model, mt.KERNELS)
+    mt.mt_profile_reset(dec.model)
+    run(min(args.steps, 50), args.warmup + args.steps)
+    torch.cuda.synchronize()
+    breakdown = {}
+    for k in mt.KERNELS:
+        ms, n = mt.mt_profile_query(dec.model, k)
+        if n:
+            breakdown[k.lower()] = {"us_per_step": round(1e3 * ms / min(args.steps, 50), 2), "launches": n}
+    mt.mt_profile_enable(dec.model, ())
+
+    if args.copy_calib_mib:
+        src = torch.empty(args.copy_calib_mib << 20, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+
+    steps_per_s = args.steps / elapsed
+    avg_vocab_s = vocab_ms / 1e3 / max(vocab_n, 1)
+    flops = 2.0 * p.M * p.E * p.V
+    achieved = flops / avg_vocab_s / 1e12
+    peak = PEAK_TFLOPS[p.gemm]
+    traffic = None
+    if os.path.exists(TRAFFIC_FILE):
+        tf = json.load(open(TRAFFIC_FILE))
+        ent = tf.get(p.name, {}).get("vocab_gemm")
+        src_h = source_hash(os.path.join(ROOT, "paper_1804_00344_amd", "csrc", "mt_gemm.hip"))
+        if ent and ent.get("source_hash") == src_h:
+            traffic = ent["bytes_per_launch"]
+    roofline = {
+        "kernel": "vocab_gemm (t Wo + bo, fused log-sum-exp partials + per-tile top-K)",
+        "bound": "mfma",
+        "achieved": round(achieved, 2),
+        "peak": peak,
+        "unit": "TFLOP/s",
+        "frac": round(achieved / peak, 4),
+        "traffic": traffic,
+        "avg_launch_us": round(avg_vocab_s * 1e6, 2),
+        "flops_per_launch": flops,
+        "launches_timed": vocab_n,
+    }
+    rec = {
+        "metric": METRIC,
+        "value": round(steps_per_s, 2),
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(1e3 * elapsed / args.steps, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if p.gemm == "f32" else "bf16",
+        "data": "synthetic (seeded; shapes and distributions of the preset)",
+        "config": {
+            "workload": f"{p.name}: shallow cGRU attention decoder step + beam top-K, B={p.B} sentences, beam K={p.K}, "
+                        f"E={p.E}, H={p.H}, C={p.C}, A={p.A}, V={p.V}, padded S={dec.S} (mean len {lens.mean():.1f}), "
+                        f"{p.gemm} GEMMs, layer_norm={p.layer_norm}, precompute every {p.steps} steps",
+            "B": p.B, "K": p.K, "S": dec.S, "V": p.V, "parallelism": "single GPU",
+        },
+        "hyp_rows_per_s": round(steps_per_s * p.M, 1),
+        "target_tok_per_s": round(steps_per_s * p.B, 1),
+        "roofline": roofline,
+        "kernels": breakdown,
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] cpu baseline (oracle)")
+        rec["cpu_baseline"] = cpu_baseline(p, w, ctx, mask, args.cpu_budget)
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -175,8 +175,9 @@ mt_status mt_beam_topk(mt_model *model, int B, int K, const float *prev_score, c
 mt_status mt_device_errors(mt_model *model, int32_t *flags);
 
 /* Kernel timing with HIP events recorded on the launch stream around each
- * launch of the given kernel class (off by default; costs two event records
- * per launch).  mt_profile_query synchronises and returns the summed
+ * launch of the selected kernel classes (bit k of kernel_mask selects
+ * mt_kernel_id k; 0 turns timing off, the default; each timed launch costs
+ * two event records).  mt_profile_query synchronises and returns the summed
  * duration in milliseconds and the number of timed launches since the last
  * reset. */
 typedef enum {
@@ -194,7 +195,7 @@ typedef enum {
   MT_KERNEL_COUNT = 11
 } mt_kernel_id;
 
-mt_status mt_profile_enable(mt_model *model, int on);
+mt_status mt_profile_enable(mt_model *model, uint32_t kernel_mask);
 mt_status mt_profile_reset(mt_model *model);
 mt_status mt_profile_query(mt_model *model, int kernel, double *total_ms, int64_t *launches);
 

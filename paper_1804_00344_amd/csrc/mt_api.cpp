@@ -67,7 +67,7 @@ struct mt_model {
   int last_B = -1, last_K = -1;
   const void *last_ws = nullptr;
   // profiling
-  bool prof_on = false;
+  uint32_t prof_mask = 0;
   ProfSlot prof[MT_KERNEL_COUNT];
   std::vector<hipEvent_t> ev_pool;
 };
@@ -240,7 +240,7 @@ struct Timed {  // records events around one launch when profiling is on
   hipStream_t st;
   hipEvent_t a = nullptr, b = nullptr;
   Timed(mt_model *m_, int k_, hipStream_t st_) : m(m_), k(k_), st(st_) {
-    if (m->prof_on) {
+    if (m->prof_mask & (1u << k)) {
       a = get_event(m);
       b = get_event(m);
       if (a && b) hipEventRecord(a, st);
@@ -584,10 +584,11 @@ mt_status mt_device_errors(mt_model *model, int32_t *flags) {
   return MT_OK;
 }
 
-mt_status mt_profile_enable(mt_model *model, int on) {
+mt_status mt_profile_enable(mt_model *model, uint32_t kernel_mask) {
   g_err[0] = 0;
   if (!valid_model(model)) return fail(MT_ERR_ARG, "invalid model handle");
-  model->prof_on = on != 0;
+  if (kernel_mask >> MT_KERNEL_COUNT) return fail(MT_ERR_ARG, "kernel_mask 0x%x has bits beyond the kernel ids", kernel_mask);
+  model->prof_mask = kernel_mask;
   return MT_OK;
 }
 

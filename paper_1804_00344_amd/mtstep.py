@@ -73,7 +73,7 @@ def lib() -> C.CDLL:
                                       _vp, _vp, _vp, _vp, C.POINTER(mt_taps), _vp, C.c_size_t, _vp]
         L.mt_beam_topk.argtypes = [_vp, C.c_int, C.c_int, _vp, _vp, _vp, _vp, _vp, _vp, _vp, C.c_size_t, _vp]
         L.mt_device_errors.argtypes = [_vp, C.POINTER(C.c_int32)]
-        L.mt_profile_enable.argtypes = [_vp, C.c_int]
+        L.mt_profile_enable.argtypes = [_vp, C.c_uint32]
         L.mt_profile_reset.argtypes = [_vp]
         L.mt_profile_query.argtypes = [_vp, C.c_int, C.POINTER(C.c_double), C.POINTER(C.c_int64)]
         for f in ("mt_load_weights", "mt_free", "mt_precompute_ctx", "mt_decoder_step", "mt_beam_topk",
@@ -186,8 +186,12 @@ def mt_device_errors(model: Model) -> int:
     return int(f.value)
 
 
-def mt_profile_enable(model: Model, on: bool = True):
-    _check(lib().mt_profile_enable(model.handle, int(on)))
+def mt_profile_enable(model: Model, kernels=("VOCAB_GEMM",)):
+    """Times the given kernel classes (names or ids) with HIP events; () turns timing off."""
+    mask = 0
+    for k in kernels:
+        mask |= 1 << (KERNEL_ID[k] if isinstance(k, str) else int(k))
+    _check(lib().mt_profile_enable(model.handle, mask))
 
 
 def mt_profile_reset(model: Model):

@@ -37,13 +37,11 @@ def sample_sentences(lens: np.ndarray, n: int) -> List[int]:
 
 
 def oracle_sentences(om: mtref.Model, K: int, sents: Sequence[int], ctx, mask, tok, src_row, state_in,
-                     want_logp=True, want_alpha=True, taps=True, threads: int = 8):
+                     want_logp=True, want_alpha=True, taps=True, threads: int = 8, start: bool = False):
     """Runs the oracle's precompute + one step on each sampled sentence separately.
 
-    state_in rows for sentence b are the K rows b*K..b*K+K-1 (mid-decode) or the single
-    start-state row b (n_state_rows == B, src_row = m // K)."""
-    B = ctx.shape[0]
-    start = state_in.shape[0] == B and np.all(src_row == np.arange(B * K) // K)
+    state_in rows for sentence b are the K rows b*K..b*K+K-1 (mid-decode), or with
+    start=True the oracle's own start state of the sentence (src_row = m // K)."""
 
     def one(b):
         c = ctx[b:b + 1]
