@@ -147,9 +147,10 @@ def main():
     mt.mt_profile_enable(dec.model, ())
 
     if args.copy_calib_mib:
-        src = torch.empty(args.copy_calib_mib << 20, dtype=torch.uint8, device="cuda")
+        # a plain elementwise kernel of known traffic: reads N MiB, writes N MiB
+        src = torch.ones((args.copy_calib_mib << 20) // 4, dtype=torch.float32, device="cuda")
         dst = torch.empty_like(src)
-        dst.copy_(src)
+        torch.neg(src, out=dst)
         torch.cuda.synchronize()
 
     steps_per_s = args.steps / elapsed

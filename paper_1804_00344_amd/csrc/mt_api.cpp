@@ -57,9 +57,13 @@ struct mt_model {
   int C;
   int bf16;       // gemm dtype is bf16
   int esize;      // bytes per GEMM operand element
-  Packed w1x, w1h, w2, w3, w4, wo, wp, ws0;  // packed [N_pad][K_pad]
+  Packed w1x, w1h, w2, w3, w4, wp, ws0;  // packed [N_pad][K_pad]
+  void *wo_frag;  // output matrix in MFMA fragment order (vocabulary kernel)
+  Packed wsamp;   // its first vocab_sample_size(V) columns in the GEMM layout (threshold pass)
+  float *bo_pad;  // output bias padded to a multiple of kVocabPad with -inf
+  int num_cu;
   void *emb;      // [V][E] compute dtype (row gather source)
-  float *bias1x, *bias3, *bo, *ba, *bi, *bt, *va;
+  float *bias1x, *bias3, *ba, *bi, *bt, *va;
   float *ln[10];  // g1a be1a g1u be1u g2a be2a g2u be2u gt bet
   int32_t *err;
   std::vector<void *> allocs;
@@ -93,6 +97,9 @@ mt_status check_cfg(const mt_config *c) {
     return fail(MT_ERR_DTYPE, "gemm_dtype=%d: need MT_F32 or MT_BF16", c->gemm_dtype);
   if (c->layer_norm && !(c->ln_eps > 0.f && std::isfinite(c->ln_eps)))
     return fail(MT_ERR_ARG, "ln_eps must be positive and finite");
+  if (vocab_rows_per_block(c->gemm_dtype == MT_BF16, c->E) == 0)
+    return fail(MT_ERR_SHAPE, "E=%d too large for the vocabulary kernel (E <= %d)", c->E,
+                c->gemm_dtype == MT_BF16 ? 2048 : 1024);
   return MT_OK;
 }
 
@@ -172,7 +179,7 @@ std::vector<float> cat(std::initializer_list<std::pair<const float *, int>> part
 
 // ---- workspace ----
 struct WsLayout {
-  size_t gx, gh, s1, g2, c, g3, g4, t, part, cand, lse, rowc, scand, total;
+  size_t gx, gh, s1, g2, c, g3, g4, t, sample, thr, part, cbuf, ccnt, lse, rowc, scand, total;
   int ntiles, kc, nchunks;
 };
 
@@ -194,10 +201,13 @@ WsLayout ws_layout(const mt_model *m, int B, int K) {
   L.g3 = take(M * (3 * H + E) * 4);
   L.g4 = take(M * E * 4);
   L.t = take(M * E * m->esize);
-  L.ntiles = (c.V + vocab_tile_n() - 1) / vocab_tile_n();
+  L.ntiles = vocab_chunks(m->bf16, (int)M, c.V, c.E, m->num_cu);
   L.kc = K;
+  L.sample = take(M * vocab_sample_size(c.V) * 4);
+  L.thr = take(M * 4);
   L.part = take(M * L.ntiles * sizeof(float2));
-  L.cand = take(M * L.ntiles * L.kc * sizeof(int2));
+  L.cbuf = take(M * L.ntiles * vocab_lists() * kVocabCap * sizeof(int2));
+  L.ccnt = take(M * L.ntiles * vocab_lists() * sizeof(int));
   L.lse = take(M * 4);
   L.rowc = take(M * K * sizeof(int2));
   L.nchunks = std::max(1, std::min(64, (c.V + 2047) / 2048));
@@ -312,6 +322,15 @@ mt_status mt_load_weights(const mt_config *cfg, const mt_weights *w, mt_model **
   m->C = 2 * c.H;
   m->bf16 = c.gemm_dtype == MT_BF16;
   m->esize = m->bf16 ? 2 : 4;
+  {
+    int dev = 0, ncu = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || ncu <= 0) {
+      delete m;
+      return fail(MT_ERR_HIP, "cannot query the device's compute units");
+    }
+    m->num_cu = ncu;
+  }
   const int E = c.E, H = c.H, A = c.A, V = c.V, C = 2 * c.H;
   mt_status s = MT_OK;
   auto run = [&]() -> mt_status {
@@ -322,24 +341,19 @@ mt_status mt_load_weights(const mt_config *cfg, const mt_weights *w, mt_model **
     CHECK(upload_packed(m, {{w->Wt_s, E}}, H, &m->w4));
     CHECK(upload_packed(m, {{w->Ua, A}}, C, &m->wp));
     CHECK(upload_packed(m, {{w->Wi, H}}, C, &m->ws0));
-    if (c.tied_output) {
-      // logits = t emb^T: the packed [V][E] layout is emb itself
-      std::vector<char> buf((size_t)rup(V, kNPad) * rup(E, kKPad) * m->esize, 0);
-      const int Kp = (int)rup(E, kKPad);
-      for (int v = 0; v < V; ++v)
-        for (int e = 0; e < E; ++e) {
-          const float x = w->emb[(size_t)v * E + e];
-          if (m->esize == 4)
-            ((float *)buf.data())[(size_t)v * Kp + e] = x;
-          else
-            ((uint16_t *)buf.data())[(size_t)v * Kp + e] = bf16_bits(x);
-        }
-      m->wo.N = V;
-      m->wo.K = E;
-      m->wo.ldb = Kp;
-      CHECK(dev_upload(m, buf.data(), buf.size(), &m->wo.p));
-    } else {
-      CHECK(upload_packed(m, {{w->Wo, V}}, E, &m->wo));
+    {  // output layer: Wo^T rows (or emb rows when tied) in MFMA fragment order
+      std::vector<char> buf(vocab_pack_bytes(m->bf16, V, E));
+      vocab_pack_host(m->bf16, V, E, c.tied_output ? w->emb : w->Wo, c.tied_output, buf.data());
+      CHECK(dev_upload(m, buf.data(), buf.size(), &m->wo_frag));
+      const int S = vocab_sample_size(V);
+      std::vector<float> ws((size_t)E * S, 0.f);  // [E][S]: the first S output columns
+      for (int e = 0; e < E; ++e)
+        for (int v = 0; v < S && v < V; ++v)
+          ws[(size_t)e * S + v] = c.tied_output ? w->emb[(size_t)v * E + e] : w->Wo[(size_t)e * V + v];
+      CHECK(upload_packed(m, {{ws.data(), S}}, E, &m->wsamp));
+      std::vector<float> bp((V + kVocabPad - 1) / kVocabPad * kVocabPad, -INFINITY);
+      std::copy(w->bo, w->bo + V, bp.begin());
+      CHECK(upload_vec(m, bp, &m->bo_pad));
     }
     {  // embedding rows in the GEMM operand type
       std::vector<char> buf((size_t)V * E * m->esize);
@@ -353,7 +367,6 @@ mt_status mt_load_weights(const mt_config *cfg, const mt_weights *w, mt_model **
     }
     CHECK(upload_vec(m, cat({{w->b1, 3 * H}, {nullptr, E}}), &m->bias1x));
     CHECK(upload_vec(m, cat({{w->b2, 3 * H}, {nullptr, E}}), &m->bias3));
-    CHECK(upload_vec(m, cat({{w->bo, V}}), &m->bo));
     CHECK(upload_vec(m, cat({{w->ba, A}}), &m->ba));
     CHECK(upload_vec(m, cat({{w->bi, H}}), &m->bi));
     CHECK(upload_vec(m, cat({{w->bt, E}}), &m->bt));
@@ -422,14 +435,14 @@ mt_status mt_precompute_ctx(mt_model *model, int B, int S, const void *ctx, cons
   p.Bp = model->wp.p; p.ldb = model->wp.ldb; p.bias = model->ba;
   p.out = pctx_out; p.ldc = A; p.out_bf16 = model->bf16;
   p.M = B * S; p.N = A; p.K = C; p.err = nullptr; p.err_bit = 0;
-  LAUNCH(MT_KERNEL_PRECOMPUTE, launch_gemm(model->bf16, &p, 1, EPI_STORE, nullptr, st));
+  LAUNCH(MT_KERNEL_PRECOMPUTE, launch_gemm(model->bf16, &p, 1, EPI_STORE, st));
   LAUNCH(MT_KERNEL_PRECOMPUTE, launch_masked_mean(B, S, C, ctx, model->bf16, mask, cbar, st));
   GemmProblem q{};
   q.A = cbar; q.a_rows = B; q.lda = C; q.a_bf16 = 0;
   q.Bp = model->ws0.p; q.ldb = model->ws0.ldb; q.bias = model->bi;
   q.out = s0_out; q.ldc = H; q.out_bf16 = 0;
   q.M = B; q.N = H; q.K = C;
-  LAUNCH(MT_KERNEL_PRECOMPUTE, launch_gemm(model->bf16, &q, 1, EPI_TANH, nullptr, st));
+  LAUNCH(MT_KERNEL_PRECOMPUTE, launch_gemm(model->bf16, &q, 1, EPI_TANH, st));
   return MT_OK;
 }
 
@@ -490,7 +503,7 @@ mt_status mt_decoder_step(mt_model *model, int B, int K, int S, const int32_t *p
   p1[1].Bp = model->w1h.p; p1[1].ldb = model->w1h.ldb; p1[1].bias = nullptr;
   p1[1].out = gh; p1[1].ldc = 3 * H; p1[1].M = M; p1[1].N = 3 * H; p1[1].K = H;
   p1[1].err = model->err; p1[1].err_bit = 1;
-  LAUNCH(MT_KERNEL_GEMM_GRU1, launch_gemm(bf, p1, 2, EPI_STORE, nullptr, st));
+  LAUNCH(MT_KERNEL_GEMM_GRU1, launch_gemm(bf, p1, 2, EPI_STORE, st));
   LAUNCH(MT_KERNEL_GRU_CELL,
          launch_gru_cell(M, H, gx, 3 * H + E, gh, 3 * H, state_in, src_row, n_state_rows, model->err,
                          LNon ? ln[0] : nullptr, ln[1], ln[2], ln[3], eps, s1, H, taps ? taps->s1 : nullptr, st));
@@ -499,7 +512,7 @@ mt_status mt_decoder_step(mt_model *model, int B, int K, int S, const int32_t *p
   p2.A = s1; p2.a_rows = M; p2.lda = H; p2.a_bf16 = 0;
   p2.Bp = model->w2.p; p2.ldb = model->w2.ldb;
   p2.out = g2; p2.ldc = A + 3 * H; p2.M = M; p2.N = A + 3 * H; p2.K = H;
-  LAUNCH(MT_KERNEL_GEMM_S1, launch_gemm(bf, &p2, 1, EPI_STORE, nullptr, st));
+  LAUNCH(MT_KERNEL_GEMM_S1, launch_gemm(bf, &p2, 1, EPI_STORE, st));
   LAUNCH(MT_KERNEL_ATTENTION, launch_attention(B, K, S, A, C, pctx, ctx, bf, mask, g2, A + 3 * H, model->va, cc, C,
                                                attn_out, st));
   if (taps && taps->c) HIP_TRY(hipMemcpyAsync(taps->c, cc, (size_t)M * C * 4, hipMemcpyDeviceToDevice, st));
@@ -508,7 +521,7 @@ mt_status mt_decoder_step(mt_model *model, int B, int K, int S, const int32_t *p
   p3.A = cc; p3.a_rows = M; p3.lda = C; p3.a_bf16 = 0;
   p3.Bp = model->w3.p; p3.ldb = model->w3.ldb; p3.bias = model->bias3;
   p3.out = g3; p3.ldc = 3 * H + E; p3.M = M; p3.N = 3 * H + E; p3.K = C;
-  LAUNCH(MT_KERNEL_GEMM_CTX, launch_gemm(bf, &p3, 1, EPI_STORE, nullptr, st));
+  LAUNCH(MT_KERNEL_GEMM_CTX, launch_gemm(bf, &p3, 1, EPI_STORE, st));
   LAUNCH(MT_KERNEL_GRU_CELL,
          launch_gru_cell(M, H, g3, 3 * H + E, g2 + A, A + 3 * H, s1, nullptr, M, model->err,
                          LNon ? ln[4] : nullptr, ln[5], ln[6], ln[7], eps, state_out, H, nullptr, st));
@@ -517,22 +530,26 @@ mt_status mt_decoder_step(mt_model *model, int B, int K, int S, const int32_t *p
   p4.A = state_out; p4.a_rows = M; p4.lda = H; p4.a_bf16 = 0;
   p4.Bp = model->w4.p; p4.ldb = model->w4.ldb;
   p4.out = g4; p4.ldc = E; p4.M = M; p4.N = E; p4.K = H;
-  LAUNCH(MT_KERNEL_GEMM_READOUT, launch_gemm(bf, &p4, 1, EPI_STORE, nullptr, st));
+  LAUNCH(MT_KERNEL_GEMM_READOUT, launch_gemm(bf, &p4, 1, EPI_STORE, st));
   LAUNCH(MT_KERNEL_READOUT, launch_readout(M, E, g4, E, gx + 3 * H, 3 * H + E, g3 + 3 * H, 3 * H + E, model->bt,
                                            LNon ? ln[8] : nullptr, ln[9], eps, t, bf, taps ? taps->t : nullptr, st));
-  // vocabulary GEMM with fused log-sum-exp partials and per-tile top-K
-  GemmProblem p5{};
-  p5.A = t; p5.a_rows = M; p5.lda = E; p5.a_bf16 = bf;
-  p5.Bp = model->wo.p; p5.ldb = model->wo.ldb; p5.bias = model->bo;
-  p5.out = nullptr; p5.ldc = V; p5.M = M; p5.N = V; p5.K = E;
-  VocabOut vo{};
-  vo.part = (float2 *)(W + L.part);
-  vo.cand = (int2 *)(W + L.cand);
-  vo.kc = L.kc;
-  vo.ntiles = L.ntiles;
-  vo.logits = logp_out;
-  LAUNCH(MT_KERNEL_VOCAB_GEMM, launch_gemm(bf, &p5, 1, EPI_VOCAB, &vo, st));
-  LAUNCH(MT_KERNEL_LSE, launch_lse(M, L.ntiles, vo.part, (float *)(W + L.lse), logp_out, V, st));
+  // vocabulary projection: threshold pass, then the full pass with fused log-sum-exp partials
+  // and threshold-filtered beam candidates
+  float2 *part = (float2 *)(W + L.part);
+  {
+    const int S = vocab_sample_size(V);
+    GemmProblem ps{};
+    ps.A = t; ps.a_rows = M; ps.lda = E; ps.a_bf16 = bf;
+    ps.Bp = model->wsamp.p; ps.ldb = model->wsamp.ldb; ps.bias = model->bo_pad;
+    ps.out = W + L.sample; ps.ldc = S; ps.M = M; ps.N = S; ps.K = E;
+    LAUNCH(MT_KERNEL_VOCAB_THRESHOLD, launch_gemm(bf, &ps, 1, EPI_STORE, st));
+    LAUNCH(MT_KERNEL_VOCAB_THRESHOLD, launch_vocab_threshold(M, V, K, (const float *)(W + L.sample),
+                                                             (float *)(W + L.thr), st));
+  }
+  LAUNCH(MT_KERNEL_VOCAB_GEMM, launch_vocab(bf, t, model->wo_frag, model->bo_pad, M, V, E, L.ntiles,
+                                            (const float *)(W + L.thr), part, (int2 *)(W + L.cbuf),
+                                            (int *)(W + L.ccnt), kVocabCap, logp_out, st));
+  LAUNCH(MT_KERNEL_LSE, launch_lse(M, L.ntiles, part, (float *)(W + L.lse), logp_out, V, st));
   model->last_B = B;
   model->last_K = K;
   model->last_ws = ws;
@@ -563,8 +580,9 @@ mt_status mt_beam_topk(mt_model *model, int B, int K, const float *prev_score, c
   const int M = B * K, V = c.V;
   int2 *rowc = (int2 *)(W + L.rowc);
   if (!logp) {
-    LAUNCH(MT_KERNEL_TOPK, launch_topk_rows(M, K, V, L.ntiles * L.kc, (const int2 *)(W + L.cand),
-                                            (const float *)(W + L.lse), prev_score, rowc, st));
+    LAUNCH(MT_KERNEL_TOPK, launch_vocab_rows(model->bf16, W + L.t, model->wo_frag, model->bo_pad, M, V, c.E, K,
+                                             L.ntiles, (const int2 *)(W + L.cbuf), (const int *)(W + L.ccnt),
+                                             kVocabCap, (const float *)(W + L.lse), prev_score, rowc, st));
   } else {
     int2 *sc = (int2 *)(W + L.scand);
     LAUNCH(MT_KERNEL_TOPK, launch_topk_scan_logp(M, K, V, L.nchunks, prev_score, logp, sc, st));

@@ -16,10 +16,7 @@
 // The A operand may be gathered by a row index (token -> embedding row, backpointer ->
 // state row) and converted fp32 -> bf16 while staged.
 //
-// Epilogues: plain store (fp32 or bf16), tanh store, and the vocabulary epilogue, which
-// stages the biased logit tile in LDS and emits per (row, tile): the tile max and the
-// sum of exp(logit - max) (log-sum-exp partials) and the tile's best kc logits with
-// their token ids (first level of the beam top-K).  Logits are stored only on request.
+// Epilogues: plain store (fp32 or bf16) and tanh store, with an optional bias.
 #include "mt_internal.h"
 
 namespace mt {
@@ -62,41 +59,8 @@ __device__ __forceinline__ u32x4 pack_bf16x8(const float4 &a, const float4 &b) {
   return r;
 }
 
-// Sorted (descending by `better`) list of the best KMAX (key, idx) pairs, kept in registers
-// with static indexing only.
-template <int KMAX>
-struct TopList {
-  float v[KMAX];
-  int i[KMAX];
-  __device__ __forceinline__ void init() {
-#pragma unroll
-    for (int p = 0; p < KMAX; ++p) { v[p] = -INFINITY; i[p] = 0x7fffffff; }
-  }
-  __device__ __forceinline__ void push(float x, int xi) {
-    if (!better(x, xi, v[KMAX - 1], i[KMAX - 1])) return;
-    float cv = x;
-    int ci = xi;
-#pragma unroll
-    for (int p = 0; p < KMAX; ++p) {
-      const bool sw = better(cv, ci, v[p], i[p]);
-      const float tv = sw ? v[p] : cv;
-      const int ti = sw ? i[p] : ci;
-      v[p] = sw ? cv : v[p];
-      i[p] = sw ? ci : i[p];
-      cv = tv;
-      ci = ti;
-    }
-  }
-  __device__ __forceinline__ void pop() {
-#pragma unroll
-    for (int p = 0; p + 1 < KMAX; ++p) { v[p] = v[p + 1]; i[p] = i[p + 1]; }
-    v[KMAX - 1] = -INFINITY;
-    i[KMAX - 1] = 0x7fffffff;
-  }
-};
-
-template <typename CT, int EPI, int BM, int BN, int KMAX>
-__global__ __launch_bounds__(kThreads) void gemm_kernel(Problems probs, VocabOut vo) {
+template <typename CT, int EPI, int BM, int BN>
+__global__ __launch_bounds__(kThreads) void gemm_kernel(Problems probs) {
   using C = Cfg<CT, BM, BN>;
   __shared__ __attribute__((aligned(16))) char lds[C::LDS];
 
@@ -226,7 +190,7 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(Problems probs, VocabOut
     __syncthreads();
   }
 
-  if constexpr (EPI != EPI_VOCAB) {
+  {
     // lane holds D[row = 4*(lane/16) + r][col = lane % 16] of each 16x16 block
 #pragma unroll
     for (int i = 0; i < C::FM; ++i)
@@ -247,110 +211,39 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(Problems probs, VocabOut
             ((float *)P.out)[(size_t)row * P.ldc + col] = v;
         }
       }
-  } else {
-    // ---- vocabulary epilogue ----
-    constexpr int TS = BN + 4;
-    static_assert(BM * TS * 4 <= C::LDS, "logit tile must fit the LDS ring");
-    float *T = (float *)lds;
-#pragma unroll
-    for (int i = 0; i < C::FM; ++i)
-#pragma unroll
-      for (int j = 0; j < C::FN; ++j) {
-        const int cl = wn * C::WN + j * 16 + (lane & 15);
-        const int col = n0 + cl;
-        const float bias = (col < P.N && P.bias) ? P.bias[col] : 0.f;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int rl = wm * C::WM + i * 16 + (lane >> 4) * 4 + r;
-          T[rl * TS + cl] = col < P.N ? acc[i][j][r] + bias : -INFINITY;
-        }
-      }
-    __syncthreads();
-    if (vo.logits) {
-      for (int idx = tid; idx < BM * BN; idx += kThreads) {
-        const int r = idx / BN, cc = idx % BN;
-        const int row = m0 + r, col = n0 + cc;
-        if (row < P.M && col < P.N) vo.logits[(size_t)row * P.N + col] = T[r * TS + cc];
-      }
-    }
-    constexpr int TPR = kThreads / BM;  // threads per row
-    constexpr int CPT = BN / TPR;       // columns per thread
-    const int r = tid / TPR, part = tid % TPR;
-    const float *Tr = T + r * TS + part * CPT;
-    float mx = -INFINITY;
-    for (int c = 0; c < CPT; ++c) mx = fmaxf(mx, Tr[c]);
-#pragma unroll
-    for (int o = 1; o < TPR; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
-    float se = 0.f;
-    for (int c = 0; c < CPT; ++c) se += exp_fast(Tr[c] - mx);
-#pragma unroll
-    for (int o = 1; o < TPR; o <<= 1) se += __shfl_xor(se, o, 64);
-    TopList<KMAX> L;
-    L.init();
-    const int cbase = n0 + part * CPT;
-    for (int c = 0; c < CPT; ++c) {
-      if (cbase + c < P.N) L.push(Tr[c], cbase + c);
-    }
-    const int row = m0 + r;
-    const size_t slot = (size_t)row * vo.ntiles + tn;
-    for (int j = 0; j < vo.kc; ++j) {
-      float bv = L.v[0];
-      int bi = L.i[0];
-#pragma unroll
-      for (int o = 1; o < TPR; o <<= 1) {
-        const float ov = __shfl_xor(bv, o, 64);
-        const int oi = __shfl_xor(bi, o, 64);
-        if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
-      }
-      if (L.i[0] == bi) L.pop();
-      if (part == 0 && row < P.M) vo.cand[slot * vo.kc + j] = make_int2(__float_as_int(bv), bi);
-    }
-    if (part == 0 && row < P.M) vo.part[slot] = make_float2(mx, se);
   }
 }
 
-int vocab_tile_n() { return 128; }
 
-template <typename CT, int EPI, int BM, int BN, int KMAX>
-static hipError_t go(const Problems &ps, int nprob, const VocabOut &vo, hipStream_t st) {
+
+template <typename CT, int EPI, int BM, int BN>
+static hipError_t go(const Problems &ps, int nprob, hipStream_t st) {
   int maxt = 0;
   for (int i = 0; i < nprob; ++i) {
     const int t = ((ps.p[i].M + BM - 1) / BM) * ((ps.p[i].N + BN - 1) / BN);
     maxt = t > maxt ? t : maxt;
   }
   if (maxt == 0) return hipSuccess;
-  hipLaunchKernelGGL((gemm_kernel<CT, EPI, BM, BN, KMAX>), dim3(maxt, 1, nprob), dim3(kThreads), 0, st,
-                     ps, vo);
+  hipLaunchKernelGGL((gemm_kernel<CT, EPI, BM, BN>), dim3(maxt, 1, nprob), dim3(kThreads), 0, st, ps);
   return hipGetLastError();
 }
 
 template <typename CT>
-static hipError_t dispatch(const Problems &ps, int nprob, Epilogue epi, const VocabOut *vo,
-                           hipStream_t st) {
-  VocabOut none{};
-  if (epi == EPI_VOCAB) {
-    const int kc = vo->kc;
-    if (kc <= 1) return go<CT, EPI_VOCAB, 128, 128, 1>(ps, nprob, *vo, st);
-    if (kc <= 2) return go<CT, EPI_VOCAB, 128, 128, 2>(ps, nprob, *vo, st);
-    if (kc <= 4) return go<CT, EPI_VOCAB, 128, 128, 4>(ps, nprob, *vo, st);
-    if (kc <= 8) return go<CT, EPI_VOCAB, 128, 128, 8>(ps, nprob, *vo, st);
-    return go<CT, EPI_VOCAB, 128, 128, 16>(ps, nprob, *vo, st);
-  }
+static hipError_t dispatch(const Problems &ps, int nprob, Epilogue epi, hipStream_t st) {
   // big tiles when they already fill the chip, else 64 x 64
   long t128 = 0;
   for (int i = 0; i < nprob; ++i)
     t128 += (long)((ps.p[i].M + 127) / 128) * ((ps.p[i].N + 127) / 128);
   const bool big = t128 >= 512;
   if (epi == EPI_TANH)
-    return big ? go<CT, EPI_TANH, 128, 128, 1>(ps, nprob, none, st) : go<CT, EPI_TANH, 64, 64, 1>(ps, nprob, none, st);
-  return big ? go<CT, EPI_STORE, 128, 128, 1>(ps, nprob, none, st) : go<CT, EPI_STORE, 64, 64, 1>(ps, nprob, none, st);
+    return big ? go<CT, EPI_TANH, 128, 128>(ps, nprob, st) : go<CT, EPI_TANH, 64, 64>(ps, nprob, st);
+  return big ? go<CT, EPI_STORE, 128, 128>(ps, nprob, st) : go<CT, EPI_STORE, 64, 64>(ps, nprob, st);
 }
 
-hipError_t launch_gemm(int bf16_mma, const GemmProblem *probs, int nprob, Epilogue epi,
-                       const VocabOut *vo, hipStream_t st) {
+hipError_t launch_gemm(int bf16_mma, const GemmProblem *probs, int nprob, Epilogue epi, hipStream_t st) {
   Problems ps{};
   for (int i = 0; i < nprob; ++i) ps.p[i] = probs[i];
-  return bf16_mma ? dispatch<bf16>(ps, nprob, epi, vo, st) : dispatch<float>(ps, nprob, epi, vo, st);
+  return bf16_mma ? dispatch<bf16>(ps, nprob, epi, st) : dispatch<float>(ps, nprob, epi, st);
 }
 
 }  // namespace mt

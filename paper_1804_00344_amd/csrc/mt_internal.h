@@ -74,11 +74,72 @@ __device__ __forceinline__ bool better(float ka, int ia, float kb, int ib) {
   return ka > kb || (ka == kb && ia < ib);
 }
 
+// Sorted (by `better`) list of the best KMAX (key, idx) pairs in registers, static indexing
+template <int KMAX>
+struct List {
+  float v[KMAX];
+  int i[KMAX];
+  __device__ __forceinline__ void init() {
+#pragma unroll
+    for (int p = 0; p < KMAX; ++p) { v[p] = -INFINITY; i[p] = 0x7fffffff; }
+  }
+  __device__ __forceinline__ void push(float x, int xi) {
+    if (!better(x, xi, v[KMAX - 1], i[KMAX - 1])) return;
+    float cv = x;
+    int ci = xi;
+#pragma unroll
+    for (int p = 0; p < KMAX; ++p) {
+      const bool sw = better(cv, ci, v[p], i[p]);
+      const float tv = sw ? v[p] : cv;
+      const int ti = sw ? i[p] : ci;
+      v[p] = sw ? cv : v[p];
+      i[p] = sw ? ci : i[p];
+      cv = tv;
+      ci = ti;
+    }
+  }
+  __device__ __forceinline__ void pop() {
+#pragma unroll
+    for (int p = 0; p + 1 < KMAX; ++p) { v[p] = v[p + 1]; i[p] = i[p + 1]; }
+    v[KMAX - 1] = -INFINITY;
+    i[KMAX - 1] = 0x7fffffff;
+  }
+};
+
+// Repeatedly extracts the block-wide best head of the per-thread sorted lists; the
+// winner pops its head.  Writes n results (key bits, idx) through `emit`.
+template <int KMAX, typename Emit>
+__device__ __forceinline__ void block_extract(List<KMAX> &L, int n, Emit emit) {
+  __shared__ float wv[4];
+  __shared__ int wi[4];
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  for (int r = 0; r < n; ++r) {
+    float bv = L.v[0];
+    int bi = L.i[0];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float ov = __shfl_xor(bv, o, 64);
+      const int oi = __shfl_xor(bi, o, 64);
+      if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
+    }
+    if (lane == 0) { wv[wave] = bv; wi[wave] = bi; }
+    __syncthreads();
+    bv = wv[0];
+    bi = wi[0];
+#pragma unroll
+    for (int w = 1; w < 4; ++w)
+      if (better(wv[w], wi[w], bv, bi)) { bv = wv[w]; bi = wi[w]; }
+    __syncthreads();
+    if (L.i[0] == bi && L.v[0] == bv) L.pop();
+    if (t == 0) emit(r, bv, bi);
+  }
+}
+
 // ---------------------------------------------------------------------------------------
 // launchers (host side).  All return hipSuccess or the launch error.
 // ---------------------------------------------------------------------------------------
 
-enum Epilogue { EPI_STORE = 0, EPI_TANH = 1, EPI_VOCAB = 2 };
+enum Epilogue { EPI_STORE = 0, EPI_TANH = 1 };
 
 struct GemmProblem {
   const void *A;          // activations [rows][lda] (fp32 or bf16, see a_bf16)
@@ -97,18 +158,34 @@ struct GemmProblem {
   int err_bit;
 };
 
-struct VocabOut {          // fused epilogue outputs of the vocabulary GEMM
-  float2 *part;            // [M][ntiles] (tile max, sum exp(l - max))
-  int2 *cand;              // [M][ntiles][kc] (key bits, token) best kc of the tile
-  int kc;                  // candidates kept per (row, tile)
-  int ntiles;
-  float *logits;           // [M][N] or NULL
-};
-
 // gemm dtype: 0 fp32 MFMA, 1 bf16 MFMA.  nprob = 1 or 2 (problems share one launch).
 hipError_t launch_gemm(int bf16_mma, const GemmProblem *probs, int nprob, Epilogue epi,
-                       const VocabOut *vo, hipStream_t st);
-int vocab_tile_n();  // BN of the vocabulary GEMM (columns per candidate tile)
+                       hipStream_t st);
+
+// ---- vocabulary projection with fused log-sum-exp partials and beam candidates ----
+// hypothesis rows per workgroup (0 if E is too large for the LDS-resident activations)
+int vocab_rows_per_block(int bf16_mma, int E);
+// vocabulary chunks (one workgroup per chunk and row block; per-chunk outputs)
+int vocab_chunks(int bf16_mma, int M, int V, int E, int num_cu);
+int vocab_sample_size(int V);  // vocabulary entries of the threshold pass (padded)
+int vocab_lists();             // candidate buffers per (row, chunk)
+size_t vocab_pack_bytes(int bf16_mma, int V, int E);
+// packs Wo^T rows into MFMA fragment order; src is Wo [E][V] or, if src_is_emb, emb [V][E]
+void vocab_pack_host(int bf16_mma, int V, int E, const float *src, int src_is_emb, void *out);
+// thr[m] = K-th best of sample[m][0 .. min(V, S)) minus a rounding margin, S = vocab_sample_size(V);
+// sample [M][S] holds the logits of the first S vocabulary entries (computed by launch_gemm)
+hipError_t launch_vocab_threshold(int M, int V, int K, const float *sample, float *thr, hipStream_t st);
+// part [M][n_chunks] (max, sum exp(l - max)); every logit >= thr[m] goes to cbuf
+// [M][n_chunks][lists][cap] with counts in ccnt [M][n_chunks][lists]; logits [M][V] or NULL
+hipError_t launch_vocab(int bf16_mma, const void *t, const void *wp, const float *bias_pad, int M, int V,
+                        int E, int n_chunks, const float *thr, float2 *part, int2 *cbuf, int *ccnt, int cap,
+                        float *logits, hipStream_t st);
+// row_out [M][K] (key bits, token): the K best keys prev_score + (logit - lse) of each row
+hipError_t launch_vocab_rows(int bf16_mma, const void *t, const void *wp, const float *bias_pad, int M, int V,
+                             int E, int K, int n_chunks, const int2 *cbuf, const int *ccnt, int cap,
+                             const float *lse, const float *prev_score, int2 *row_out, hipStream_t st);
+constexpr int kVocabCap = 32;  // candidate buffer entries per (row, chunk, list)
+constexpr int kVocabPad = 64;  // vocabulary rows are padded to a multiple of this
 
 hipError_t launch_gru_cell(int M, int H, const float *a, int lda, const float *u, int ldu,
                            const float *hsrc, const int32_t *hidx, int hrows, int32_t *err,

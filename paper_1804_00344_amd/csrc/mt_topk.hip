@@ -17,66 +17,6 @@ namespace mt {
 
 constexpr int kTT = 256;
 
-template <int KMAX>
-struct List {
-  float v[KMAX];
-  int i[KMAX];
-  __device__ __forceinline__ void init() {
-#pragma unroll
-    for (int p = 0; p < KMAX; ++p) { v[p] = -INFINITY; i[p] = 0x7fffffff; }
-  }
-  __device__ __forceinline__ void push(float x, int xi) {
-    if (!better(x, xi, v[KMAX - 1], i[KMAX - 1])) return;
-    float cv = x;
-    int ci = xi;
-#pragma unroll
-    for (int p = 0; p < KMAX; ++p) {
-      const bool sw = better(cv, ci, v[p], i[p]);
-      const float tv = sw ? v[p] : cv;
-      const int ti = sw ? i[p] : ci;
-      v[p] = sw ? cv : v[p];
-      i[p] = sw ? ci : i[p];
-      cv = tv;
-      ci = ti;
-    }
-  }
-  __device__ __forceinline__ void pop() {
-#pragma unroll
-    for (int p = 0; p + 1 < KMAX; ++p) { v[p] = v[p + 1]; i[p] = i[p + 1]; }
-    v[KMAX - 1] = -INFINITY;
-    i[KMAX - 1] = 0x7fffffff;
-  }
-};
-
-// Repeatedly extracts the block-wide best head of the per-thread sorted lists; the
-// winner pops its head.  Writes n results (key bits, idx) through `emit`.
-template <int KMAX, typename Emit>
-__device__ __forceinline__ void block_extract(List<KMAX> &L, int n, Emit emit) {
-  __shared__ float wv[4];
-  __shared__ int wi[4];
-  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  for (int r = 0; r < n; ++r) {
-    float bv = L.v[0];
-    int bi = L.i[0];
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      const float ov = __shfl_xor(bv, o, 64);
-      const int oi = __shfl_xor(bi, o, 64);
-      if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
-    }
-    if (lane == 0) { wv[wave] = bv; wi[wave] = bi; }
-    __syncthreads();
-    bv = wv[0];
-    bi = wi[0];
-#pragma unroll
-    for (int w = 1; w < 4; ++w)
-      if (better(wv[w], wi[w], bv, bi)) { bv = wv[w]; bi = wi[w]; }
-    __syncthreads();
-    if (L.i[0] == bi && L.v[0] == bv) L.pop();
-    if (t == 0) emit(r, bv, bi);
-  }
-}
-
 // Level 2.  cand: [M][ncand] (key or logit bits, token); lse != NULL means the values are
 // logits to turn into keys with prev_score; tokens >= V are padding and skipped.
 template <int KMAX>

@@ -1,0 +1,544 @@
+// Output layer of the decoder step: logits = t Wo + bo over the whole target vocabulary,
+// fused with the log-sum-exp partials of the log-softmax and the candidate collection of the
+// beam top-K.  Logits are never written unless requested.
+//
+// Orientation: the product is computed transposed, logits^T = Wo^T t^T, so the MFMA's A
+// operand is the weight (vocabulary rows) and its B operand the readout activations
+// (hypothesis columns).  In the 32x32 MFMA output layout a lane owns one hypothesis column
+// of each 32-column block, so the per-hypothesis running state (online log-sum-exp, candidate
+// count) lives in the lane's registers while the vocabulary streams past.
+//
+// Work split: a workgroup owns HB hypothesis rows (their activations stay resident in LDS for
+// the whole kernel) and one contiguous chunk of the vocabulary, split into 4 runs of 64-row
+// vocabulary tiles.  Each wave covers WH <= 64 hypothesis columns of one run (HB/WH waves per
+// run share its weight fragments) and streams the packed weights straight from global memory
+// (fragment order, one coalesced 16-byte load per lane per MFMA operand), prefetching D
+// k-steps ahead across tile boundaries, with no barrier in the main loop.
+//
+// Beam candidates without sorting: a row's K best logits are all >= the K-th best logit of
+// any subset of that row.  A small first pass computes the logits of the first S vocabulary
+// entries and takes their K-th best (minus a rounding margin) as the row's threshold; the main
+// pass appends every logit at or above it to a per-lane buffer (one compare per logit, a
+// store when it passes).  The row merge then selects the K best keys among the few collected
+// values; a row whose buffer overflowed is recomputed there in full, so the result is exact.
+//
+// Packed weights (built at load time): for 32-row vocabulary block vb and k-step ks of KV
+// k-values, 64 lanes x 16 bytes at ((vb * KS + ks) * 64 + lane) * 16, where lane l holds
+// Wo^T[vb*32 + l%32][ks*KV + (l/32)*KV/2 + j], j < 16/sizeof(CT).  fp32 uses the 32x32x2
+// MFMA with each 16-byte vector feeding 4 successive MFMAs (lane half g supplies k = 4g + s
+// to MFMA s); bf16 uses 32x32x16 with one vector per MFMA.
+#include "mt_internal.h"
+
+namespace mt {
+
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
+typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+
+constexpr int kVRows = 64;       // vocabulary rows per wave tile (2 MFMA blocks)
+constexpr int kLists = 8;        // candidate buffers per (hypothesis, chunk): 2 lane halves x 4 runs
+constexpr int kSampleMax = 512;  // vocabulary entries of the threshold pass
+
+template <int HB>
+struct VShape {
+  static constexpr int WH = HB >= 64 ? 64 : HB;  // hypothesis columns per wave
+  static constexpr int HBW = WH / 32;            // 32-column MFMA blocks per wave
+  static constexpr int NW = 4 * (HB / WH);       // waves per workgroup
+  static constexpr int NT = 64 * NW;             // threads per workgroup
+};
+
+template <typename CT>
+struct VCfg;
+template <>
+struct VCfg<bf16> {
+  static constexpr int KV = 16;  // k per 16-byte vector step
+};
+template <>
+struct VCfg<float> {
+  static constexpr int KV = 8;
+};
+
+struct VocabArgs {
+  const void *t;        // [M][E] activations in CT
+  const void *wp;       // packed weights (see header comment)
+  const float *bias;    // [Vpad] with -inf beyond V
+  int M, V, E, KS;      // KS = E / KV
+  int n_chunks;
+  int tiles_total;      // 64-row tiles of the processed range [0, 64 * tiles_total)
+  float2 *part;         // [M][n_chunks] (max, sum exp(l - max)); NULL in the threshold pass
+  const float *thr;     // [M] candidate threshold
+  int2 *cbuf;           // [M][n_chunks][kLists][cap] (logit bits, token)
+  int *ccnt;            // [M][n_chunks][kLists] values at or above the threshold
+  int cap;
+  float *logits;        // [M][logits_ld] or NULL
+  int logits_ld;
+};
+
+template <typename CT, int HB, int D>
+__global__ __launch_bounds__(VShape<HB>::NT) void vocab_kernel(VocabArgs a) {
+  extern __shared__ __attribute__((aligned(16))) char lds[];
+  constexpr int HBB = VShape<HB>::HBW;
+  constexpr int kVT = VShape<HB>::NT;
+  constexpr int KV = VCfg<CT>::KV;
+  constexpr int es = (int)sizeof(CT);
+  const int rowb = a.E * es + 16;  // LDS row stride of the resident activations
+
+  const int nhb = (a.M + HB - 1) / HB;
+  const int L = xcd_remap(blockIdx.x, gridDim.x);
+  const int chunk = L / nhb, hb = L % nhb;
+  if (chunk >= a.n_chunks) return;
+  const int h0 = hb * HB;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: keeps the stream scalar
+  const int run = wave & 3;                                    // vocabulary run of this wave
+  const int hc0 = (wave >> 2) * VShape<HB>::WH;               // first hypothesis column of this wave
+
+  // ---- resident activations: rows h0..h0+HB-1 (zero beyond M) ----
+  {
+    const int vecs_per_row = a.E * es / 16;
+    for (int idx = tid; idx < HB * vecs_per_row; idx += kVT) {
+      const int r = idx / vecs_per_row, c = idx % vecs_per_row;
+      v4u val = {0u, 0u, 0u, 0u};
+      if (h0 + r < a.M) val = *(const v4u *)((const char *)a.t + ((size_t)(h0 + r) * a.E) * es + c * 16);
+      *(v4u *)(lds + r * rowb + c * 16) = val;
+    }
+  }
+  __syncthreads();
+
+  // ---- this wave's contiguous run of vocabulary tiles ----
+  const int slots = a.n_chunks * 4;
+  const int slot = chunk * 4 + run;
+  const int t_begin = (int)((long)a.tiles_total * slot / slots);
+  const int t_end = (int)((long)a.tiles_total * (slot + 1) / slots);
+  const int ntile = t_end - t_begin;
+  const int total = ntile * a.KS;  // flat (tile, k-step) stream, KS % D == 0
+  const int KS = a.KS;
+  const int lrow = lane & 31, lhalf = lane >> 5;
+  const int src = run * 2 + lhalf;
+  const bool collect = a.part != nullptr;
+
+  float lm[HBB], ls[HBB], th[HBB];
+  int cnt[HBB];
+  size_t cb[HBB];  // first entry of this lane's candidate buffer, per hypothesis block
+#pragma unroll
+  for (int j = 0; j < HBB; ++j) {
+    const int h = h0 + hc0 + j * 32 + lrow;
+    lm[j] = -INFINITY;
+    ls[j] = 0.f;
+    cnt[j] = 0;
+    th[j] = (collect && h < a.M) ? a.thr[h] : INFINITY;
+    cb[j] = (((size_t)(h < a.M ? h : 0) * a.n_chunks + chunk) * kLists + src) * a.cap;
+  }
+
+  if (ntile > 0) {
+    // Weight fragments of step g of tile ti are vocabulary blocks 2*(t_begin+ti) and +1 at
+    // k-step ks.  Every prefetch is issued unconditionally (clamped to the last step) and a
+    // slot is refilled only after its MFMAs consumed it, so waits can be exact.
+    const v4u *wbase = (const v4u *)a.wp + (size_t)2 * t_begin * KS * 64 + lane;
+    int pf_k = 0, pf_n = 0;
+    const v4u *pf = wbase;
+    auto advance = [&]() {
+      if (pf_n + 1 < total) {
+        ++pf_n;
+        pf += 64;
+        if (++pf_k == KS) { pf_k = 0; pf += (size_t)KS * 64; }
+      }
+    };
+    v4u ring[D][2];
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+      ring[d][0] = pf[0];
+      ring[d][1] = pf[(size_t)KS * 64];
+      advance();
+    }
+    const v4u *bl = (const v4u *)lds + (size_t)(hc0 + lrow) * (rowb / 16) + lhalf * (KV / 2 * es / 16);
+
+    for (int ti = 0; ti < ntile; ++ti) {
+      f32x16 acc[2][HBB];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < HBB; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+      for (int ks0 = 0; ks0 < KS; ks0 += D) {
+#pragma unroll
+        for (int d = 0; d < D; ++d) {
+          const int ks = ks0 + d;
+          const v4u c0 = ring[d][0], c1 = ring[d][1];
+          v4u bfr[HBB];
+#pragma unroll
+          for (int j = 0; j < HBB; ++j) bfr[j] = bl[(size_t)j * 32 * (rowb / 16) + ks * (KV * es / 16)];
+          if constexpr (es == 2) {
+            bf16x8 a0, a1;
+            __builtin_memcpy(&a0, &c0, 16);
+            __builtin_memcpy(&a1, &c1, 16);
+#pragma unroll
+            for (int j = 0; j < HBB; ++j) {
+              bf16x8 b;
+              __builtin_memcpy(&b, &bfr[j], 16);
+              acc[0][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b, acc[0][j], 0, 0, 0);
+              acc[1][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b, acc[1][j], 0, 0, 0);
+            }
+          } else {
+            float fa0[4], fa1[4], fb[HBB][4];
+            __builtin_memcpy(fa0, &c0, 16);
+            __builtin_memcpy(fa1, &c1, 16);
+#pragma unroll
+            for (int j = 0; j < HBB; ++j) __builtin_memcpy(fb[j], &bfr[j], 16);
+#pragma unroll
+            for (int s = 0; s < 4; ++s)
+#pragma unroll
+              for (int j = 0; j < HBB; ++j) {
+                acc[0][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa0[s], fb[j][s], acc[0][j], 0, 0, 0);
+                acc[1][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa1[s], fb[j][s], acc[1][j], 0, 0, 0);
+              }
+          }
+          ring[d][0] = pf[0];
+          ring[d][1] = pf[(size_t)KS * 64];
+          advance();
+        }
+      }
+
+      // ---- epilogue of this tile: bias, online log-sum-exp, threshold-filtered candidates ----
+      // lane holds rows v = v0 + 32*i + 8*(r/4) + 4*lhalf + r%4 of hypothesis column j*32 + lrow
+      const int v0 = (t_begin + ti) * kVRows;
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float4 b4 = *(const float4 *)(a.bias + v0 + 32 * i + 8 * q + 4 * lhalf);
+#pragma unroll
+          for (int j = 0; j < HBB; ++j) {
+            acc[i][j][4 * q + 0] += b4.x; acc[i][j][4 * q + 1] += b4.y;
+            acc[i][j][4 * q + 2] += b4.z; acc[i][j][4 * q + 3] += b4.w;
+          }
+        }
+#pragma unroll
+      for (int j = 0; j < HBB; ++j) {
+        const int h = h0 + hc0 + j * 32 + lrow;
+        if (collect) {
+          float mt = -INFINITY;
+#pragma unroll
+          for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) mt = fmaxf(mt, acc[i][j][r]);
+          if (mt != -INFINITY) {  // -inf only when the whole tile is padding
+            float se = 0.f;
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+              for (int r = 0; r < 16; ++r) {
+                const float x = acc[i][j][r];
+                se += exp_fast(x - mt);
+                if (x >= th[j]) {
+                  if (cnt[j] < a.cap)
+                    a.cbuf[cb[j] + cnt[j]] = make_int2(__float_as_int(x), v0 + 32 * i + 8 * (r >> 2) + 4 * lhalf + (r & 3));
+                  ++cnt[j];
+                }
+              }
+            const float mn = fmaxf(lm[j], mt);
+            ls[j] = ls[j] * exp_fast(lm[j] - mn) + se * exp_fast(mt - mn);
+            lm[j] = mn;
+          }
+        }
+        if (a.logits && h < a.M) {
+          float *lrowp = a.logits + (size_t)h * a.logits_ld;
+#pragma unroll
+          for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              const int v = v0 + 32 * i + 8 * (r >> 2) + 4 * lhalf + (r & 3);
+              if (v < a.V && v < a.logits_ld) lrowp[v] = acc[i][j][r];
+            }
+        }
+      }
+    }
+  }  // ntile > 0
+
+  if (!collect) return;
+  // ---- candidate counts, and the 8 log-sum-exp partials of each hypothesis merged via LDS ----
+#pragma unroll
+  for (int j = 0; j < HBB; ++j) {
+    const int h = h0 + hc0 + j * 32 + lrow;
+    if (h < a.M) a.ccnt[((size_t)h * a.n_chunks + chunk) * kLists + src] = cnt[j];
+  }
+  __syncthreads();  // the resident activations are no longer read
+  float2 *lp = (float2 *)lds;  // [HB][kLists]
+#pragma unroll
+  for (int j = 0; j < HBB; ++j) lp[(hc0 + j * 32 + lrow) * kLists + src] = make_float2(lm[j], ls[j]);
+  __syncthreads();
+  for (int hl = tid; hl < HB; hl += kVT) {
+    const int h = h0 + hl;
+    if (h >= a.M) continue;
+    float m = -INFINITY;
+    for (int s = 0; s < kLists; ++s) m = fmaxf(m, lp[hl * kLists + s].x);
+    float sum = 0.f;
+    if (m != -INFINITY)
+      for (int s = 0; s < kLists; ++s) {
+        const float2 q = lp[hl * kLists + s];
+        if (q.x != -INFINITY) sum += q.y * exp_fast(q.x - m);
+      }
+    a.part[(size_t)h * a.n_chunks + chunk] = make_float2(m, sum);
+  }
+}
+
+// Threshold of each row: the K-th best of the first S logits, lowered by a margin that covers
+// fp32 rounding of the keys (two logits whose keys round equal differ by far less).
+template <int KMAX>
+__global__ __launch_bounds__(256) void vocab_threshold_kernel(int M, int S, int K, const float *__restrict__ sample,
+                                                              int ld, float *__restrict__ thr) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int m = blockIdx.x * 4 + w;
+  if (m >= M) return;  // uniform per wave
+  const float *row = sample + (size_t)m * ld;
+  List<KMAX> lst;
+  lst.init();
+  for (int v = lane; v < S; v += 64) lst.push(row[v], v);
+  float kth = -INFINITY;
+  for (int r = 0; r < K; ++r) {
+    float bv = lst.v[0];
+    int bi = lst.i[0];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float ov = __shfl_xor(bv, o, 64);
+      const int oi = __shfl_xor(bi, o, 64);
+      if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
+    }
+    if (lst.i[0] == bi && lst.v[0] == bv) lst.pop();
+    kth = bv;
+  }
+  if (lane == 0) thr[m] = kth - 1e-3f * (1.0f + fabsf(kth));
+}
+
+// Row merge of the fused path: the K best keys (score + (logit - lse)) among the row's
+// collected candidates.  If any of the row's buffers overflowed, the row's logits are
+// recomputed here from the packed weights (slow but exact).
+template <typename CT, int KMAX>
+__global__ __launch_bounds__(256) void vocab_rows_kernel(VocabArgs a, int K, const float *__restrict__ lse,
+                                                         const float *__restrict__ prev_score,
+                                                         int2 *__restrict__ row_out) {
+  constexpr int KV = VCfg<CT>::KV;
+  constexpr int epv = 16 / (int)sizeof(CT);
+  const int m = blockIdx.x, t = threadIdx.x;
+  const int nl = a.n_chunks * kLists;
+  const int *cnt = a.ccnt + (size_t)m * nl;
+  const float Lm = lse[m], sc = prev_score[m];
+  __shared__ int ovf;
+  if (t == 0) ovf = 0;
+  __syncthreads();
+  for (int l = t; l < nl; l += 256)
+    if (cnt[l] > a.cap) ovf = 1;
+  __syncthreads();
+  List<KMAX> lst;
+  lst.init();
+  if (!ovf) {
+    for (int l = t; l < nl; l += 256) {
+      const int n = cnt[l];
+      const int2 *e = a.cbuf + ((size_t)m * nl + l) * a.cap;
+      for (int q = 0; q < n; ++q) {
+        const int2 c = e[q];
+        const float lp = __int_as_float(c.x) - Lm;
+        lst.push(sc + lp, c.y);
+      }
+    }
+  } else {
+    // full recomputation of the row: lane pairs (l, l+32) of a wave share one vocabulary entry
+    const int lane = t & 63, w = t >> 6;
+    const CT *trow = (const CT *)a.t + (size_t)m * a.E;
+    const int nvb = (a.V + 31) / 32;
+    for (int vb = w; vb < nvb; vb += 4) {
+      float acc = 0.f;
+      for (int ks = 0; ks < a.KS; ++ks) {
+        const CT *wv = (const CT *)((const v4u *)a.wp + ((size_t)vb * a.KS + ks) * 64 + lane);
+        const int k0 = ks * KV + (lane >> 5) * (KV / 2);
+#pragma unroll
+        for (int j = 0; j < epv; ++j) acc += to_f32(wv[j]) * to_f32(trow[k0 + j]);
+      }
+      acc += __shfl_xor(acc, 32, 64);
+      const int v = vb * 32 + (lane & 31);
+      if (lane < 32 && v < a.V) lst.push(sc + ((acc + a.bias[v]) - Lm), v);
+    }
+  }
+  block_extract<KMAX>(lst, K, [&](int r, float v, int i) { row_out[(size_t)m * K + r] = make_int2(__float_as_int(v), i); });
+}
+
+// ---------------------------------------------------------------------------------------
+
+int vocab_rows_per_block(int bf16_mma, int E) {
+  const int es = bf16_mma ? 2 : 4;
+  const int want = bf16_mma ? 128 : 64;
+  for (int hb = want; hb >= 32; hb /= 2)
+    if ((size_t)hb * (E * es + 16) <= 160 * 1024 - 1024) return hb;
+  return 0;
+}
+
+size_t vocab_pack_bytes(int bf16_mma, int V, int E) {
+  const int Vpad = (V + kVRows - 1) / kVRows * kVRows;
+  return (size_t)Vpad * E * (bf16_mma ? 2 : 4);
+}
+
+int vocab_sample_size(int V) {
+  const int s = V < kSampleMax ? V : kSampleMax;
+  return (s + kVRows - 1) / kVRows * kVRows;
+}
+
+int vocab_lists() { return kLists; }
+
+// packed[((vb * KS + ks) * 64 + lane) * 16 bytes] from Wo^T rows (row v = column v of Wo)
+void vocab_pack_host(int bf16_mma, int V, int E, const float *src, int src_is_emb, void *out) {
+  const int KV = bf16_mma ? 16 : 8, epv = bf16_mma ? 8 : 4;
+  const int KS = E / KV;
+  const int Vpad = (V + kVRows - 1) / kVRows * kVRows;
+  for (int vb = 0; vb < Vpad / 32; ++vb)
+    for (int ks = 0; ks < KS; ++ks)
+      for (int l = 0; l < 64; ++l)
+        for (int j = 0; j < epv; ++j) {
+          const int v = vb * 32 + (l & 31);
+          const int k = ks * KV + (l >> 5) * (KV / 2) + j;
+          float x = 0.f;
+          if (v < V) x = src_is_emb ? src[(size_t)v * E + k] : src[(size_t)k * V + v];
+          const size_t o = (((size_t)vb * KS + ks) * 64 + l) * epv + j;
+          if (bf16_mma) {
+            uint32_t u;
+            __builtin_memcpy(&u, &x, 4);
+            uint16_t hbits;
+            if ((u & 0x7fffffffu) > 0x7f800000u)
+              hbits = (uint16_t)((u >> 16) | 0x40u);
+            else
+              hbits = (uint16_t)((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
+            ((uint16_t *)out)[o] = hbits;
+          } else {
+            ((float *)out)[o] = x;
+          }
+        }
+}
+
+// prefetch depth in k-steps: a bf16 k-step is 16x shorter in MFMA time than an fp32 one, so it
+// needs a deeper ring to cover the same memory latency
+static int ring_depth(int bf16_mma, int KS) {
+  if (bf16_mma && KS % 8 == 0) return 8;
+  return KS % 4 == 0 ? 4 : KS % 2 == 0 ? 2 : 1;
+}
+
+template <typename CT, int HB, int D>
+static hipError_t vgo(const VocabArgs &a, hipStream_t st) {
+  const int nhb = (a.M + HB - 1) / HB;
+  const size_t tbytes = (size_t)HB * (a.E * sizeof(CT) + 16);
+  const size_t lbytes = (size_t)HB * kLists * 8;
+  const size_t lds = tbytes > lbytes ? tbytes : lbytes;
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute((const void *)vocab_kernel<CT, HB, D>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  hipLaunchKernelGGL((vocab_kernel<CT, HB, D>), dim3(nhb * a.n_chunks), dim3(VShape<HB>::NT), lds, st, a);
+  return hipGetLastError();
+}
+
+template <typename CT, int HB>
+static hipError_t vgo_d(const VocabArgs &a, hipStream_t st) {
+  switch (ring_depth(sizeof(CT) == 2, a.KS)) {
+    case 8: return vgo<CT, HB, sizeof(CT) == 2 ? 8 : 4>(a, st);
+    case 4: return vgo<CT, HB, 4>(a, st);
+    case 2: return vgo<CT, HB, 2>(a, st);
+    default: return vgo<CT, HB, 1>(a, st);
+  }
+}
+
+static hipError_t vgo_any(int bf16_mma, const VocabArgs &a, hipStream_t st) {
+  const int HB = vocab_rows_per_block(bf16_mma, a.E);
+  if (bf16_mma) {
+    if (HB == 128) return vgo_d<bf16, 128>(a, st);
+    if (HB == 64) return vgo_d<bf16, 64>(a, st);
+    return vgo_d<bf16, 32>(a, st);
+  }
+  if (HB == 64) return vgo_d<float, 64>(a, st);
+  return vgo_d<float, 32>(a, st);
+}
+
+int vocab_chunks(int bf16_mma, int M, int V, int E, int num_cu) {
+  const int HB = vocab_rows_per_block(bf16_mma, E);
+  const int nhb = (M + HB - 1) / HB;
+  const int tiles = (V + kVRows - 1) / kVRows;
+  int n = num_cu / nhb;
+  if (n < 1) n = 1;
+  if (n * 4 > tiles) n = (tiles + 3) / 4;
+  return n;
+}
+
+static VocabArgs base_args(int bf16_mma, const void *t, const void *wp, const float *bias_pad, int M, int V,
+                           int E) {
+  VocabArgs a{};
+  a.t = t;
+  a.wp = wp;
+  a.bias = bias_pad;
+  a.M = M;
+  a.V = V;
+  a.E = E;
+  a.KS = E / (bf16_mma ? 16 : 8);
+  return a;
+}
+
+hipError_t launch_vocab_threshold(int M, int V, int K, const float *sample, float *thr, hipStream_t st) {
+  if (M == 0) return hipSuccess;
+  const int S = vocab_sample_size(V);
+  const int Sv = V < S ? V : S;  // entries >= V of the sample are padding
+#define MT_TH(N) \
+  hipLaunchKernelGGL((vocab_threshold_kernel<N>), dim3((M + 3) / 4), dim3(256), 0, st, M, Sv, K, sample, S, thr)
+  if (K <= 1) MT_TH(1);
+  else if (K <= 2) MT_TH(2);
+  else if (K <= 4) MT_TH(4);
+  else if (K <= 8) MT_TH(8);
+  else MT_TH(16);
+#undef MT_TH
+  return hipGetLastError();
+}
+
+hipError_t launch_vocab(int bf16_mma, const void *t, const void *wp, const float *bias_pad, int M, int V,
+                        int E, int n_chunks, const float *thr, float2 *part, int2 *cbuf, int *ccnt, int cap,
+                        float *logits, hipStream_t st) {
+  if (M == 0) return hipSuccess;
+  VocabArgs a = base_args(bf16_mma, t, wp, bias_pad, M, V, E);
+  a.tiles_total = (V + kVRows - 1) / kVRows;
+  a.n_chunks = n_chunks;
+  a.part = part;
+  a.thr = thr;
+  a.cbuf = cbuf;
+  a.ccnt = ccnt;
+  a.cap = cap;
+  a.logits = logits;
+  a.logits_ld = V;
+  return vgo_any(bf16_mma, a, st);
+}
+
+hipError_t launch_vocab_rows(int bf16_mma, const void *t, const void *wp, const float *bias_pad, int M, int V,
+                             int E, int K, int n_chunks, const int2 *cbuf, const int *ccnt, int cap,
+                             const float *lse, const float *prev_score, int2 *row_out, hipStream_t st) {
+  if (M == 0) return hipSuccess;
+  VocabArgs a = base_args(bf16_mma, t, wp, bias_pad, M, V, E);
+  a.n_chunks = n_chunks;
+  a.cbuf = (int2 *)cbuf;
+  a.ccnt = (int *)ccnt;
+  a.cap = cap;
+#define MT_VR(CT, N) \
+  hipLaunchKernelGGL((vocab_rows_kernel<CT, N>), dim3(M), dim3(256), 0, st, a, K, lse, prev_score, row_out)
+#define MT_VRK(CT)                 \
+  if (K <= 1) MT_VR(CT, 1);        \
+  else if (K <= 2) MT_VR(CT, 2);   \
+  else if (K <= 4) MT_VR(CT, 4);   \
+  else if (K <= 8) MT_VR(CT, 8);   \
+  else MT_VR(CT, 16);
+  if (bf16_mma) {
+    MT_VRK(bf16)
+  } else {
+    MT_VRK(float)
+  }
+#undef MT_VRK
+#undef MT_VR
+  return hipGetLastError();
+}
+
+}  // namespace mt

@@ -20,7 +20,7 @@ MT_OK, MT_ERR_ARG, MT_ERR_SHAPE, MT_ERR_DTYPE, MT_ERR_HIP, MT_ERR_OOM, MT_ERR_ST
     0, -1, -2, -3, -4, -5, -6, -7)
 MT_F32, MT_BF16 = 0, 1
 KERNELS = ["GEMM_GRU1", "GRU_CELL", "GEMM_S1", "ATTENTION", "GEMM_CTX", "GEMM_READOUT", "READOUT",
-           "VOCAB_GEMM", "LSE", "TOPK", "PRECOMPUTE"]
+           "VOCAB_GEMM", "LSE", "TOPK", "PRECOMPUTE", "VOCAB_THRESHOLD"]
 KERNEL_ID = {n: i for i, n in enumerate(KERNELS)}
 
 

@@ -314,3 +314,28 @@ def test_abi_errors_on_gpu():
         mt.mt_decoder_step(dec.model, p.B, p.K, dec.S, T(tok), T(src), p.M, st, dec.ctx, dec.pctx, dec.mask, out,
                            ws=misaligned)
     assert e.value.status == mt.MT_ERR_ARG
+
+
+def test_candidate_buffer_overflow_falls_back_exactly():
+    """A bias that makes the first vocabulary entries (the threshold sample) very unlikely puts
+    the candidate threshold far below the rest of the vocabulary, so the candidate buffers
+    overflow; the row merge must then recompute the rows and still select exactly."""
+    log("\n[overflow fallback]")
+    p = synth.with_sizes(synth.PRESETS["tiny_f32"], V=85000, K=4, B=2)
+    w = synth.make_weights(p)
+    w["bo"] = np.zeros(p.V, np.float32)
+    w["bo"][:1024] = -50.0
+    dec = Decoder.from_preset(p, w)
+    ctx, mask, lens = synth.make_source(p)
+    dec.set_batch(ctx, mask, p.K)
+    dec.precompute()
+    tok, src, state, score = synth.mid_decode_inputs(p, salt=5)
+    gpu = run_step(dec, p, tok, src, T(state), p.M, attn=False, taps=False)
+    sc, tk, bp, _ = [x.cpu().numpy() for x in dec.topk(T(score), None)]
+    lp = gpu["logp"].cpu().numpy()
+    t2, b2, s2 = mtref.topk(p.K, score, lp)
+    assert np.array_equal(tk, t2) and np.array_equal(bp, b2) and np.array_equal(sc, s2)
+    orc = oracle_sentences(oracle_model(p, w), p.K, [0, 1], ctx, mask, tok, src, state, want_alpha=False, taps=False)
+    for b in (0, 1):
+        rows = slice(b * p.K, (b + 1) * p.K)
+        assert maxerr(lp[rows], orc[b]["logp"]) <= 1e-3
