@@ -179,7 +179,7 @@ std::vector<float> cat(std::initializer_list<std::pair<const float *, int>> part
 
 // ---- workspace ----
 struct WsLayout {
-  size_t gx, gh, s1, g2, c, g3, g4, t, sample, thr, part, cbuf, ccnt, lse, rowc, scand, total;
+  size_t gx, gh, s1, g2, c, g3, g4, t, sample, thr, part, cbuf, ccnt, ovf, lse, rowc, scand, total;
   int ntiles, kc, nchunks;
 };
 
@@ -208,6 +208,7 @@ WsLayout ws_layout(const mt_model *m, int B, int K) {
   L.part = take(M * L.ntiles * sizeof(float2));
   L.cbuf = take(M * L.ntiles * vocab_lists() * kVocabCap * sizeof(int2));
   L.ccnt = take(M * L.ntiles * vocab_lists() * sizeof(int));
+  L.ovf = take(M * sizeof(int));
   L.lse = take(M * 4);
   L.rowc = take(M * K * sizeof(int2));
   L.nchunks = std::max(1, std::min(64, (c.V + 2047) / 2048));
@@ -582,7 +583,8 @@ mt_status mt_beam_topk(mt_model *model, int B, int K, const float *prev_score, c
   if (!logp) {
     LAUNCH(MT_KERNEL_TOPK, launch_vocab_rows(model->bf16, W + L.t, model->wo_frag, model->bo_pad, M, V, c.E, K,
                                              L.ntiles, (const int2 *)(W + L.cbuf), (const int *)(W + L.ccnt),
-                                             kVocabCap, (const float *)(W + L.lse), prev_score, rowc, st));
+                                             kVocabCap, (const float *)(W + L.lse), prev_score, rowc,
+                                             (int *)(W + L.ovf), st));
   } else {
     int2 *sc = (int2 *)(W + L.scand);
     LAUNCH(MT_KERNEL_TOPK, launch_topk_scan_logp(M, K, V, L.nchunks, prev_score, logp, sc, st));

@@ -135,6 +135,24 @@ __device__ __forceinline__ void block_extract(List<KMAX> &L, int n, Emit emit) {
   }
 }
 
+// Wave-level version (no barriers): the wave's best head is found with shuffles; the owning
+// lane pops it.  Every lane receives the n results in order through `emit` (lane-uniform).
+template <int KMAX, typename Emit>
+__device__ __forceinline__ void wave_extract(List<KMAX> &L, int n, Emit emit) {
+  for (int r = 0; r < n; ++r) {
+    float bv = L.v[0];
+    int bi = L.i[0];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float ov = __shfl_xor(bv, o, 64);
+      const int oi = __shfl_xor(bi, o, 64);
+      if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
+    }
+    if (L.i[0] == bi && L.v[0] == bv) L.pop();
+    emit(r, bv, bi);
+  }
+}
+
 // ---------------------------------------------------------------------------------------
 // launchers (host side).  All return hipSuccess or the launch error.
 // ---------------------------------------------------------------------------------------
@@ -183,7 +201,8 @@ hipError_t launch_vocab(int bf16_mma, const void *t, const void *wp, const float
 // row_out [M][K] (key bits, token): the K best keys prev_score + (logit - lse) of each row
 hipError_t launch_vocab_rows(int bf16_mma, const void *t, const void *wp, const float *bias_pad, int M, int V,
                              int E, int K, int n_chunks, const int2 *cbuf, const int *ccnt, int cap,
-                             const float *lse, const float *prev_score, int2 *row_out, hipStream_t st);
+                             const float *lse, const float *prev_score, int2 *row_out, int *ovf,
+                             hipStream_t st);
 constexpr int kVocabCap = 32;  // candidate buffer entries per (row, chunk, list)
 constexpr int kVocabPad = 64;  // vocabulary rows are padded to a multiple of this
 

@@ -61,25 +61,28 @@ __global__ __launch_bounds__(kTT) void topk_scan_logp_kernel(int M, int K, int V
   block_extract<KMAX>(lst, K, [&](int r, float v, int i) { o[r] = make_int2(__float_as_int(v), i); });
 }
 
-// Level 3: one workgroup per sentence; candidate (k, j) -> flat index k*V + token.
+// Level 3: one wave per sentence; candidate (k, j) -> flat index k*V + token.
 template <int KMAX>
-__global__ __launch_bounds__(kTT) void topk_sentence_kernel(int B, int K, int V,
+__global__ __launch_bounds__(256) void topk_sentence_kernel(int B, int K, int V,
                                                             const int2 *__restrict__ row_cand,
                                                             float *__restrict__ score_out,
                                                             int32_t *__restrict__ tok_out,
                                                             int32_t *__restrict__ bp_out,
                                                             int32_t *__restrict__ row_out) {
-  const int b = blockIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int b = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (b >= B) return;  // uniform per wave
   const int n = K * K;
   List<KMAX> lst;
   lst.init();
-  for (int j = threadIdx.x; j < n; j += kTT) {
+  for (int j = lane; j < n; j += 64) {
     const int k = j / K;
     const int2 e = row_cand[(size_t)(b * K + k) * K + (j % K)];
     if (e.y < 0 || e.y >= V) continue;
     lst.push(__int_as_float(e.x), k * V + e.y);
   }
-  block_extract<KMAX>(lst, K, [&](int r, float v, int i) {
+  wave_extract<KMAX>(lst, K, [&](int r, float v, int i) {
+    if (lane != 0) return;
     const int o = b * K + r;
     // a flat index beyond the K x V range only appears if fewer than K candidates exist
     const int k = i < K * V ? i / V : 0;
@@ -125,7 +128,7 @@ hipError_t launch_topk_sentence(int B, int K, int V, const int2 *row_cand, float
                                 int32_t *tok_out, int32_t *bp_out, int32_t *row_out,
                                 hipStream_t st) {
   if (B == 0) return hipSuccess;
-#define MT_TSN(N) hipLaunchKernelGGL((topk_sentence_kernel<N>), dim3(B), dim3(kTT), 0, st, B, K, V, row_cand, score_out, tok_out, bp_out, row_out)
+#define MT_TSN(N) hipLaunchKernelGGL((topk_sentence_kernel<N>), dim3((B + 3) / 4), dim3(256), 0, st, B, K, V, row_cand, score_out, tok_out, bp_out, row_out)
   MT_KSWITCH(K, MT_TSN)
 #undef MT_TSN
   return hipGetLastError();

@@ -311,42 +311,69 @@ __global__ __launch_bounds__(256) void vocab_threshold_kernel(int M, int S, int 
   if (lane == 0) thr[m] = kth - 1e-3f * (1.0f + fabsf(kth));
 }
 
-// Row merge of the fused path: the K best keys (score + (logit - lse)) among the row's
-// collected candidates.  If any of the row's buffers overflowed, the row's logits are
-// recomputed here from the packed weights (slow but exact).
-template <typename CT, int KMAX>
+// Row merge of the fused path, one wave per row: the K best keys (score + (logit - lse)) among
+// the row's collected candidates.  A row with an overflowed buffer is only flagged here and
+// recomputed by vocab_fallback_kernel.
+template <int KMAX>
 __global__ __launch_bounds__(256) void vocab_rows_kernel(VocabArgs a, int K, const float *__restrict__ lse,
                                                          const float *__restrict__ prev_score,
-                                                         int2 *__restrict__ row_out) {
-  constexpr int KV = VCfg<CT>::KV;
-  constexpr int epv = 16 / (int)sizeof(CT);
-  const int m = blockIdx.x, t = threadIdx.x;
+                                                         int2 *__restrict__ row_out, int *__restrict__ ovf) {
+  const int lane = threadIdx.x & 63;
+  const int m = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (m >= a.M) return;  // uniform per wave
   const int nl = a.n_chunks * kLists;
   const int *cnt = a.ccnt + (size_t)m * nl;
   const float Lm = lse[m], sc = prev_score[m];
-  __shared__ int ovf;
-  if (t == 0) ovf = 0;
-  __syncthreads();
-  for (int l = t; l < nl; l += 256)
-    if (cnt[l] > a.cap) ovf = 1;
-  __syncthreads();
   List<KMAX> lst;
   lst.init();
-  if (!ovf) {
-    for (int l = t; l < nl; l += 256) {
-      const int n = cnt[l];
-      const int2 *e = a.cbuf + ((size_t)m * nl + l) * a.cap;
-      for (int q = 0; q < n; ++q) {
-        const int2 c = e[q];
-        const float lp = __int_as_float(c.x) - Lm;
-        lst.push(sc + lp, c.y);
-      }
+  bool over = false;
+  for (int l = lane; l < nl; l += 64) {
+    const int n = cnt[l];
+    over |= n > a.cap;
+    const int2 *e = a.cbuf + ((size_t)m * nl + l) * a.cap;
+    const int nn = n < a.cap ? n : a.cap;
+    for (int q = 0; q < nn; ++q) {
+      const int2 c = e[q];
+      const float lp = __int_as_float(c.x) - Lm;
+      lst.push(sc + lp, c.y);
     }
-  } else {
-    // full recomputation of the row: lane pairs (l, l+32) of a wave share one vocabulary entry
-    const int lane = t & 63, w = t >> 6;
+  }
+  const bool any_over = __ballot(over) != 0ull;
+  if (lane == 0) ovf[m] = any_over ? 1 : 0;
+  wave_extract<KMAX>(lst, K, [&](int r, float v, int i) {
+    if (lane == 0) row_out[(size_t)m * K + r] = make_int2(__float_as_int(v), i);
+  });
+}
+
+// Exact recomputation of the rows flagged by vocab_rows_kernel (a buffer overflowed): the full
+// logit row from the packed weights, then the K best keys.  Workgroup x reads the flags of rows
+// [256x, 256x + 256) in parallel and processes its flagged rows one after another.
+template <typename CT, int KMAX>
+__global__ __launch_bounds__(256) void vocab_fallback_kernel(VocabArgs a, int K, const float *__restrict__ lse,
+                                                             const float *__restrict__ prev_score,
+                                                             int2 *__restrict__ row_out,
+                                                             const int *__restrict__ ovf) {
+  constexpr int KV = VCfg<CT>::KV;
+  constexpr int epv = 16 / (int)sizeof(CT);
+  __shared__ int rows[256];
+  __shared__ int nr;
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  if (t == 0) nr = 0;
+  __syncthreads();
+  {
+    const int m = blockIdx.x * 256 + t;
+    if (m < a.M && ovf[m]) rows[atomicAdd(&nr, 1)] = m;
+  }
+  __syncthreads();
+  const int n = nr;
+  for (int r = 0; r < n; ++r) {
+    const int m = rows[r];
+    const float Lm = lse[m], sc = prev_score[m];
     const CT *trow = (const CT *)a.t + (size_t)m * a.E;
     const int nvb = (a.V + 31) / 32;
+    List<KMAX> lst;
+    lst.init();
+    // lane pairs (l, l+32) of a wave share one vocabulary entry
     for (int vb = w; vb < nvb; vb += 4) {
       float acc = 0.f;
       for (int ks = 0; ks < a.KS; ++ks) {
@@ -359,8 +386,9 @@ __global__ __launch_bounds__(256) void vocab_rows_kernel(VocabArgs a, int K, con
       const int v = vb * 32 + (lane & 31);
       if (lane < 32 && v < a.V) lst.push(sc + ((acc + a.bias[v]) - Lm), v);
     }
+    block_extract<KMAX>(lst, K, [&](int q, float v, int i) { row_out[(size_t)m * K + q] = make_int2(__float_as_int(v), i); });
+    __syncthreads();
   }
-  block_extract<KMAX>(lst, K, [&](int r, float v, int i) { row_out[(size_t)m * K + r] = make_int2(__float_as_int(v), i); });
 }
 
 // ---------------------------------------------------------------------------------------
@@ -516,15 +544,22 @@ hipError_t launch_vocab(int bf16_mma, const void *t, const void *wp, const float
 
 hipError_t launch_vocab_rows(int bf16_mma, const void *t, const void *wp, const float *bias_pad, int M, int V,
                              int E, int K, int n_chunks, const int2 *cbuf, const int *ccnt, int cap,
-                             const float *lse, const float *prev_score, int2 *row_out, hipStream_t st) {
+                             const float *lse, const float *prev_score, int2 *row_out, int *ovf,
+                             hipStream_t st) {
   if (M == 0) return hipSuccess;
   VocabArgs a = base_args(bf16_mma, t, wp, bias_pad, M, V, E);
   a.n_chunks = n_chunks;
   a.cbuf = (int2 *)cbuf;
   a.ccnt = (int *)ccnt;
   a.cap = cap;
-#define MT_VR(CT, N) \
-  hipLaunchKernelGGL((vocab_rows_kernel<CT, N>), dim3(M), dim3(256), 0, st, a, K, lse, prev_score, row_out)
+  const int nfb = (M + 255) / 256;
+#define MT_VR(CT, N)                                                                                         \
+  do {                                                                                                       \
+    hipLaunchKernelGGL((vocab_rows_kernel<N>), dim3((M + 3) / 4), dim3(256), 0, st, a, K, lse, prev_score,  \
+                       row_out, ovf);                                                                        \
+    hipLaunchKernelGGL((vocab_fallback_kernel<CT, N>), dim3(nfb), dim3(256), 0, st, a, K, lse, prev_score,  \
+                       row_out, (const int *)ovf);                                                           \
+  } while (0)
 #define MT_VRK(CT)                 \
   if (K <= 1) MT_VR(CT, 1);        \
   else if (K <= 2) MT_VR(CT, 2);   \
