@@ -3,20 +3,32 @@
 //   e_i   = sum_a va[a] * tanh(P[b,i,a] + q[m,a])      (valid i only)
 //   alpha = exp(e_i - max_valid e) / sum_valid exp(...)  (exactly 0 at masked i)
 //   c[m]  = sum_valid alpha_i * Cx[b,i,:]
-// The valid positions are first compacted into an LDS list (ballot prefix sums), so neither
-// loop branches on the mask or reads a masked row.  Scores: each wave takes two valid
-// positions per iteration; its 64 lanes stream the A features of P[b,i] in coalesced 16-byte
-// granules against q and va held in registers, and reduce with cross-lane shuffles.  Softmax:
-// one wave over the compacted scores.  Context: each thread owns 16-byte column granules of
-// C and walks the valid positions four at a time, so four rows of loads are in flight.
-// Workgroup ids are remapped so that the K rows of one sentence run on one XCD and share its
-// L2 copy of P[b] and Cx[b].
+//
+// The valid positions are first compacted into an LDS list (ballot prefix sums), so no loop
+// branches on the mask or reads a masked row.
+//
+// Scores.  tanh x = 1 - 2 / (2^(x * 2/ln2) + 1), so
+//   e_i = sum_a va[a] - sum_a 2 va[a] / (2^(P[i,a] c + q[m,a] c) + 1),   c = 2/ln2.
+// The row's q is held pre-scaled by c and va pre-scaled by -2, which leaves one FMA, one
+// exp2, one add, one reciprocal and one FMA per element; sum_a va[a] is a per-row constant.
+// Each wave takes two valid positions per iteration: its 64 lanes cover the A features of
+// P[b,i] in 16-byte granules, and every granule load of both positions is issued before any
+// of them is consumed (lanes beyond A read a clamped in-range address and carry zero
+// weight, so the loop has no per-granule branch).  Cross-lane shuffles reduce the sums.
+//
+// Context.  Each thread owns 16-byte column granules of Cx and walks the valid positions
+// several at a time (eight for up to two granules per thread) with all their row loads in
+// flight.
+//
+// Workgroup ids are remapped so that the K rows of one sentence run on one XCD and share
+// its L2 copy of P[b] and Cx[b].
 #include "mt_internal.h"
 
 namespace mt {
 
 constexpr int kAT = 256;
 constexpr int kMaxS = 1024;
+constexpr float kTwoOverLn2 = 2.8853900817779268f;  // 2 / ln 2
 
 template <typename T>
 struct Gran;  // one 16-byte granule of a row, widened to fp32
@@ -38,8 +50,9 @@ struct Gran<bf16> {
   }
 };
 
-// MAXJ: granules per lane of a score row (A <= 64 * MAXJ * Gran<T>::N)
-template <typename T, int MAXJ>
+// NG: granules per lane of a score row (A <= 64 * NG * Gran<T>::N);
+// NC: granules per thread of a context row (2H <= 256 * NC * Gran<T>::N)
+template <typename T, int NG, int NC>
 __global__ __launch_bounds__(kAT) void attention_kernel(int B, int K, int S, int A, int Cd,
                                                         const T *__restrict__ P,
                                                         const T *__restrict__ Cx,
@@ -49,6 +62,7 @@ __global__ __launch_bounds__(kAT) void attention_kernel(int B, int K, int S, int
                                                         float *__restrict__ ctx_out, int ldc,
                                                         float *__restrict__ alpha_out) {
   constexpr int G = Gran<T>::N;
+  constexpr int U = NC <= 2 ? 8 : NC == 4 ? 4 : 2;  // context positions in flight per thread
   __shared__ float es[kMaxS];
   __shared__ int vidx[kMaxS];
   __shared__ float stat[2];
@@ -74,16 +88,31 @@ __global__ __launch_bounds__(kAT) void attention_kernel(int B, int K, int S, int
     if (lane == 0) nvalid = n;
   }
 
-  float qr[MAXJ][G], vr[MAXJ][G];
+  // ---- this lane's slice of q (scaled by 2/ln2) and va (scaled by -2) ----
+  float qr[NG][G], vr[NG][G];
+  int goff[NG];  // element offset of the lane's granule j in a P row (clamped)
+  float vsum = 0.f;
 #pragma unroll
-  for (int j = 0; j < MAXJ; ++j) {
+  for (int j = 0; j < NG; ++j) {
     const int g = j * 64 + lane;
+    const bool ok = g < ng;
+    goff[j] = (ok ? g : ng - 1) * G;
+    float qv[G], vv[G];
+#pragma unroll
+    for (int e = 0; e < G; e += 4) {
+      const float4 a = *(const float4 *)(q + (size_t)m * ldq + goff[j] + e);
+      const float4 w = *(const float4 *)(va + goff[j] + e);
+      qv[e] = a.x; qv[e + 1] = a.y; qv[e + 2] = a.z; qv[e + 3] = a.w;
+      vv[e] = w.x; vv[e + 1] = w.y; vv[e + 2] = w.z; vv[e + 3] = w.w;
+    }
 #pragma unroll
     for (int e = 0; e < G; ++e) {
-      qr[j][e] = g < ng ? q[(size_t)m * ldq + g * G + e] : 0.f;
-      vr[j][e] = g < ng ? va[g * G + e] : 0.f;
+      qr[j][e] = ok ? qv[e] * kTwoOverLn2 : 0.f;
+      vr[j][e] = ok ? -2.0f * vv[e] : 0.f;
+      vsum += ok ? vv[e] : 0.f;
     }
   }
+  vsum = wave_sum(vsum);
   __syncthreads();
   const int n = nvalid;
 
@@ -93,26 +122,27 @@ __global__ __launch_bounds__(kAT) void attention_kernel(int B, int K, int S, int
     const int i0 = vidx[j], i1 = two ? vidx[j + 4] : i0;
     const T *P0 = P + ((size_t)b * S + i0) * A;
     const T *P1 = P + ((size_t)b * S + i1) * A;
+    float x0[NG][G], x1[NG][G];
+#pragma unroll
+    for (int jj = 0; jj < NG; ++jj) {
+      Gran<T>::load(P0 + goff[jj], x0[jj]);
+      Gran<T>::load(P1 + goff[jj], x1[jj]);
+    }
     float acc0 = 0.f, acc1 = 0.f;
 #pragma unroll
-    for (int jj = 0; jj < MAXJ; ++jj) {
-      const int g = jj * 64 + lane;
-      if (g < ng) {
-        float x0[G], x1[G];
-        Gran<T>::load(P0 + g * G, x0);
-        Gran<T>::load(P1 + g * G, x1);
+    for (int jj = 0; jj < NG; ++jj)
 #pragma unroll
-        for (int e = 0; e < G; ++e) {
-          acc0 += vr[jj][e] * tanh_fast(x0[e] + qr[jj][e]);
-          acc1 += vr[jj][e] * tanh_fast(x1[e] + qr[jj][e]);
-        }
+      for (int e = 0; e < G; ++e) {
+        const float d0 = __builtin_amdgcn_exp2f(__builtin_fmaf(x0[jj][e], kTwoOverLn2, qr[jj][e])) + 1.0f;
+        const float d1 = __builtin_amdgcn_exp2f(__builtin_fmaf(x1[jj][e], kTwoOverLn2, qr[jj][e])) + 1.0f;
+        acc0 = __builtin_fmaf(vr[jj][e], rcp_fast(d0), acc0);
+        acc1 = __builtin_fmaf(vr[jj][e], rcp_fast(d1), acc1);
       }
-    }
     acc0 = wave_sum(acc0);
     acc1 = wave_sum(acc1);
     if (lane == 0) {
-      es[j] = acc0;
-      if (two) es[j + 4] = acc1;
+      es[j] = vsum + acc0;
+      if (two) es[j + 4] = vsum + acc1;
     }
   }
   __syncthreads();
@@ -141,53 +171,83 @@ __global__ __launch_bounds__(kAT) void attention_kernel(int B, int K, int S, int
   if (alpha_out)
     for (int j = t; j < n; j += kAT) alpha_out[(size_t)m * S + vidx[j]] = es[j];
 
-  // ---- context: granules g of the C columns, four positions per iteration ----
+  // ---- context: granules of the Cx columns, U positions in flight ----
   const int ncg = Cd / G;
   const T *Cb = Cx + (size_t)b * S * Cd;
-  for (int g = t; g < ncg; g += kAT) {
-    float c[G];
+  float c[NC][G];
+  int coff[NC];
 #pragma unroll
-    for (int e = 0; e < G; ++e) c[e] = 0.f;
-    int j = 0;
-    for (; j + 4 <= n; j += 4) {
-      float x[4][G];
+  for (int p = 0; p < NC; ++p) {
+    const int g = t + kAT * p;
+    coff[p] = (g < ncg ? g : ncg - 1) * G;
 #pragma unroll
-      for (int u = 0; u < 4; ++u) Gran<T>::load(Cb + (size_t)vidx[j + u] * Cd + g * G, x[u]);
+    for (int e = 0; e < G; ++e) c[p][e] = 0.f;
+  }
+  for (int j0 = 0; j0 < n; j0 += U) {
+    float al[U];
+    const T *rows[U];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const float al = es[j + u];
-#pragma unroll
-        for (int e = 0; e < G; ++e) c[e] += al * x[u][e];
-      }
+    for (int u = 0; u < U; ++u) {
+      const int j = j0 + u;
+      const bool ok = j < n;
+      al[u] = ok ? es[j] : 0.f;
+      rows[u] = Cb + (size_t)vidx[ok ? j : j0] * Cd;
     }
-    for (; j < n; ++j) {
-      float x[G];
-      Gran<T>::load(Cb + (size_t)vidx[j] * Cd + g * G, x);
-      const float al = es[j];
+    float x[U][NC][G];
 #pragma unroll
-      for (int e = 0; e < G; ++e) c[e] += al * x[e];
-    }
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int p = 0; p < NC; ++p) Gran<T>::load(rows[u] + coff[p], x[u][p]);
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int p = 0; p < NC; ++p)
+#pragma unroll
+        for (int e = 0; e < G; ++e) c[p][e] = __builtin_fmaf(al[u], x[u][p][e], c[p][e]);
+  }
+#pragma unroll
+  for (int p = 0; p < NC; ++p) {
+    const int g = t + kAT * p;
+    if (g >= ncg) continue;
     float *o = ctx_out + (size_t)m * ldc + g * G;
 #pragma unroll
-    for (int e = 0; e < G; e += 4) *(float4 *)(o + e) = make_float4(c[e], c[e + 1], c[e + 2], c[e + 3]);
+    for (int e = 0; e < G; e += 4) *(float4 *)(o + e) = make_float4(c[p][e], c[p][e + 1], c[p][e + 2], c[p][e + 3]);
   }
+}
+
+static int bucket(int n) { return n <= 1 ? 1 : n <= 2 ? 2 : n <= 4 ? 4 : n <= 8 ? 8 : 16; }
+
+template <typename T, int NG>
+static void attn_go_c(int nc, int B, int K, int S, int A, int Cd, const T *P, const T *Cx, const float *mask,
+                      const float *q, int ldq, const float *va, float *ctx_out, int ldc, float *alpha_out,
+                      hipStream_t st) {
+  const int M = B * K;
+#define MT_AT(NC)                                                                                    \
+  hipLaunchKernelGGL((attention_kernel<T, NG, NC>), dim3(M), dim3(kAT), 0, st, B, K, S, A, Cd, P, Cx, \
+                     mask, q, ldq, va, ctx_out, ldc, alpha_out)
+  if (nc <= 1) MT_AT(1);
+  else if (nc <= 2) MT_AT(2);
+  else if (nc <= 4) MT_AT(4);
+  else MT_AT(8);
+#undef MT_AT
 }
 
 template <typename T>
 static void attn_go(int B, int K, int S, int A, int Cd, const T *P, const T *Cx, const float *mask,
-                    const float *q, int ldq, const float *va, float *ctx_out, int ldc,
-                    float *alpha_out, hipStream_t st) {
-  const int M = B * K;
-  const int j = (A / Gran<T>::N + 63) / 64;
-#define MT_AT(N)                                                                                    \
-  hipLaunchKernelGGL((attention_kernel<T, N>), dim3(M), dim3(kAT), 0, st, B, K, S, A, Cd, P, Cx,    \
-                     mask, q, ldq, va, ctx_out, ldc, alpha_out)
-  if (j <= 1) MT_AT(1);
-  else if (j <= 2) MT_AT(2);
-  else if (j <= 4) MT_AT(4);
-  else if (j <= 8) MT_AT(8);
-  else MT_AT(16);
-#undef MT_AT
+                    const float *q, int ldq, const float *va, float *ctx_out, int ldc, float *alpha_out,
+                    hipStream_t st) {
+  constexpr int G = Gran<T>::N;
+  const int ng = bucket((A / G + 63) / 64);
+  const int nc = bucket((Cd / G + kAT - 1) / kAT);
+#define MT_AG(NG) attn_go_c<T, NG>(nc, B, K, S, A, Cd, P, Cx, mask, q, ldq, va, ctx_out, ldc, alpha_out, st)
+  switch (ng) {
+    case 1: MT_AG(1); break;
+    case 2: MT_AG(2); break;
+    case 4: MT_AG(4); break;
+    case 8: MT_AG(8); break;
+    default: MT_AG(16); break;
+  }
+#undef MT_AG
 }
 
 hipError_t launch_attention(int B, int K, int S, int A, int Cd, const void *P, const void *Cx,
