@@ -160,9 +160,11 @@ def main():
     peak = PEAK_TFLOPS[p.gemm]
     traffic = None
     if os.path.exists(TRAFFIC_FILE):
+        # HBM bytes per launch from the FETCH_SIZE / WRITE_SIZE passes, valid only while the
+        # vocabulary kernel's source is the one the counters were taken on
         tf = json.load(open(TRAFFIC_FILE))
         ent = tf.get(p.name, {}).get("vocab_gemm")
-        src_h = source_hash(os.path.join(ROOT, "paper_1804_00344_amd", "csrc", "mt_gemm.hip"))
+        src_h = source_hash(os.path.join(ROOT, "paper_1804_00344_amd", "csrc", "mt_vocab.hip"))
         if ent and ent.get("source_hash") == src_h:
             traffic = ent["bytes_per_launch"]
     roofline = {

@@ -62,7 +62,7 @@ struct mt_model {
   Packed wsamp;   // its first vocab_sample_size(V) columns in the GEMM layout (threshold pass)
   float *bo_pad;  // output bias padded to a multiple of kVocabPad with -inf
   int num_cu;
-  void *emb;      // [V][E] compute dtype (row gather source)
+  void *emb;      // [V][E] fp32 (row gather source)
   float *bias1x, *bias3, *ba, *bi, *bt, *va;
   float *ln[10];  // g1a be1a g1u be1u g2a be2a g2u be2u gt bet
   int32_t *err;
@@ -356,16 +356,9 @@ mt_status mt_load_weights(const mt_config *cfg, const mt_weights *w, mt_model **
       std::copy(w->bo, w->bo + V, bp.begin());
       CHECK(upload_vec(m, bp, &m->bo_pad));
     }
-    {  // embedding rows in the GEMM operand type
-      std::vector<char> buf((size_t)V * E * m->esize);
-      for (size_t i = 0; i < (size_t)V * E; ++i) {
-        if (m->esize == 4)
-          ((float *)buf.data())[i] = w->emb[i];
-        else
-          ((uint16_t *)buf.data())[i] = bf16_bits(w->emb[i]);
-      }
-      CHECK(dev_upload(m, buf.data(), buf.size(), &m->emb));
-    }
+    // embedding rows stay fp32 (only the gathered rows are read; a bf16 model rounds them to
+    // bf16 when they are staged as the GEMM operand, like every other fp32 activation)
+    CHECK(dev_upload(m, w->emb, (size_t)V * E * sizeof(float), &m->emb));
     CHECK(upload_vec(m, cat({{w->b1, 3 * H}, {nullptr, E}}), &m->bias1x));
     CHECK(upload_vec(m, cat({{w->b2, 3 * H}, {nullptr, E}}), &m->bias3));
     CHECK(upload_vec(m, cat({{w->ba, A}}), &m->ba));
@@ -496,7 +489,7 @@ mt_status mt_decoder_step(mt_model *model, int B, int K, int S, const int32_t *p
 
   // GRU 1 products: x [W1 | Wt_y] + [b1 | 0] and h U1 (one launch, two problems)
   GemmProblem p1[2] = {};
-  p1[0].A = model->emb; p1[0].a_idx = prev_tok; p1[0].a_rows = V; p1[0].lda = E; p1[0].a_bf16 = bf;
+  p1[0].A = model->emb; p1[0].a_idx = prev_tok; p1[0].a_rows = V; p1[0].lda = E; p1[0].a_bf16 = 0;
   p1[0].Bp = model->w1x.p; p1[0].ldb = model->w1x.ldb; p1[0].bias = model->bias1x;
   p1[0].out = gx; p1[0].ldc = 3 * H + E; p1[0].M = M; p1[0].N = 3 * H + E; p1[0].K = E;
   p1[0].err = model->err; p1[0].err_bit = 0;
@@ -581,14 +574,17 @@ mt_status mt_beam_topk(mt_model *model, int B, int K, const float *prev_score, c
   const int M = B * K, V = c.V;
   int2 *rowc = (int2 *)(W + L.rowc);
   if (!logp) {
-    LAUNCH(MT_KERNEL_TOPK, launch_vocab_rows(model->bf16, W + L.t, model->wo_frag, model->bo_pad, M, V, c.E, K,
-                                             L.ntiles, (const int2 *)(W + L.cbuf), (const int *)(W + L.ccnt),
-                                             kVocabCap, (const float *)(W + L.lse), prev_score, rowc,
-                                             (int *)(W + L.ovf), st));
+    int *ovf = (int *)(W + L.ovf);
+    LAUNCH(MT_KERNEL_TOPK, launch_row_select(M, K, V, L.ntiles * vocab_lists(), kVocabCap, (const int *)(W + L.ccnt),
+                                             (const int2 *)(W + L.cbuf), (const float *)(W + L.lse), prev_score,
+                                             rowc, ovf, st));
+    LAUNCH(MT_KERNEL_TOPK, launch_vocab_fallback(model->bf16, W + L.t, model->wo_frag, model->bo_pad, M, V, c.E, K,
+                                                 (const float *)(W + L.lse), prev_score, rowc, ovf, st));
   } else {
     int2 *sc = (int2 *)(W + L.scand);
     LAUNCH(MT_KERNEL_TOPK, launch_topk_scan_logp(M, K, V, L.nchunks, prev_score, logp, sc, st));
-    LAUNCH(MT_KERNEL_TOPK, launch_topk_rows(M, K, V, L.nchunks * K, sc, nullptr, nullptr, rowc, st));
+    LAUNCH(MT_KERNEL_TOPK, launch_row_select(M, K, V, L.nchunks, K, nullptr, sc, nullptr, nullptr, rowc,
+                                             nullptr, st));
   }
   LAUNCH(MT_KERNEL_TOPK, launch_topk_sentence(B, K, V, rowc, score_out, tok_out, bp_out, row_out, st));
   return MT_OK;

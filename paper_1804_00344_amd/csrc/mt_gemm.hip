@@ -10,11 +10,18 @@
 // Both paths read LDS identically: per 64-byte k-chunk, lane l reads 16 bytes at row
 // (l % 16), byte offset 16 * (l / 16).
 //
-// Tiles: BM x BN per 256-thread workgroup, 2 x 2 waves, each wave (BM/2) x (BN/2) as
-// 16 x 16 MFMA blocks.  K advances 128 bytes per tile through a double-buffered LDS
-// ring; the next tile's global loads are issued before the current tile's MFMAs.
+// Tiles: BM x BN (32, 64 or 128 square) per 256-thread workgroup, 2 x 2 waves, each wave
+// (BM/2) x (BN/2) as 16 x 16 MFMA blocks.  K advances 128 bytes (of the compute dtype) per
+// tile through a double-buffered LDS ring fed from two register stages: the global loads of
+// tile k+2 are issued while tile k is multiplied, and tile k+1 is written to LDS behind it,
+// so every load has two tiles of MFMA work to arrive.  Loads are unconditional straight-line
+// code and nothing is masked: a row past M reads row 0 and its output row is never stored,
+// and a vector past K reads the row's last in-range vector, which meets the zero padding of
+// the packed weights (finite x 0 adds nothing).  The fp32 -> bf16 rounding of an fp32 A
+// operand happens when a stage is written to LDS; scheduling fences keep the load, multiply
+// and store phases in that order, so no wait on the loads is forced early.
 // The A operand may be gathered by a row index (token -> embedding row, backpointer ->
-// state row) and converted fp32 -> bf16 while staged.
+// state row).  Every problem of one launch has the same A element type AT.
 //
 // Epilogues: plain store (fp32 or bf16) and tanh store, with an optional bias.
 #include "mt_internal.h"
@@ -25,9 +32,10 @@ constexpr int kRowBytes = 128;              // K bytes per LDS tile row
 constexpr int kLdsStride = kRowBytes + 16;  // padded row stride: conflict-free 16B reads
 constexpr int kThreads = 256;
 
-template <typename CT, int BM, int BN>
+template <typename CT, typename AT, int BM, int BN>
 struct Cfg {
-  static constexpr int EPV = 16 / (int)sizeof(CT);  // elements per 16-byte vector
+  static constexpr int EPV = 16 / (int)sizeof(CT);  // compute elements per 16-byte vector
+  static constexpr int AV = (int)sizeof(AT) / (int)sizeof(CT);  // 16-byte source loads per vector
   static constexpr int BK = kRowBytes / (int)sizeof(CT);
   static constexpr int WM = BM / 2, WN = BN / 2;
   static constexpr int FM = WM / 16, FN = WN / 16;
@@ -50,18 +58,32 @@ __device__ __forceinline__ T bitcast16(const u32x4 &v) {
   return r;
 }
 
-__device__ __forceinline__ u32x4 pack_bf16x8(const float4 &a, const float4 &b) {
+__device__ __forceinline__ u32x4 pack_bf16x8(const u32x4 &lo, const u32x4 &hi) {
+  float a[4], b[4];
+  __builtin_memcpy(a, &lo, 16);
+  __builtin_memcpy(b, &hi, 16);
   bf16x8 h;
-  h[0] = to_bf16(a.x); h[1] = to_bf16(a.y); h[2] = to_bf16(a.z); h[3] = to_bf16(a.w);
-  h[4] = to_bf16(b.x); h[5] = to_bf16(b.y); h[6] = to_bf16(b.z); h[7] = to_bf16(b.w);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    h[j] = to_bf16(a[j]);
+    h[4 + j] = to_bf16(b[j]);
+  }
   u32x4 r;
   __builtin_memcpy(&r, &h, 16);
   return r;
 }
 
-template <typename CT, int EPI, int BM, int BN>
+// one tile's global data in flight: raw A source vectors and B vectors
+template <int A_PER_T, int AV, int B_PER_T>
+struct Stage {
+  u32x4 a[A_PER_T][AV];
+  u32x4 b[B_PER_T];
+};
+
+template <typename CT, typename AT, int EPI, int BM, int BN>
 __global__ __launch_bounds__(kThreads) void gemm_kernel(Problems probs) {
-  using C = Cfg<CT, BM, BN>;
+  using C = Cfg<CT, AT, BM, BN>;
+  using St = Stage<C::A_PER_T, C::AV, C::B_PER_T>;
   __shared__ __attribute__((aligned(16))) char lds[C::LDS];
 
   const GemmProblem &P = probs.p[blockIdx.z];
@@ -78,26 +100,24 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(Problems probs) {
 
   // ---- per-thread global source rows (fixed across k tiles) ----
   const char *a_src[C::A_PER_T];
-  bool a_ok[C::A_PER_T];
+  bool a_row_ok[C::A_PER_T];
   int a_kv[C::A_PER_T];
-  const int a_bf16 = P.a_bf16;
-  const int a_es = (sizeof(CT) == 2 && !a_bf16) ? 4 : (int)sizeof(CT);  // source element bytes
 #pragma unroll
   for (int p = 0; p < C::A_PER_T; ++p) {
     const int v = tid + kThreads * p;
     const int r = v >> 3;
     a_kv[p] = v & 7;
     const int m = m0 + r;
-    a_ok[p] = m < P.M;
+    a_row_ok[p] = m < P.M;
     int src = m;
-    if (P.a_idx && a_ok[p]) {
+    if (P.a_idx && a_row_ok[p]) {
       src = P.a_idx[m];
       if (src < 0 || src >= P.a_rows) {
         if (P.err) atomicOr(P.err, 1 << P.err_bit);
         src = src < 0 ? 0 : P.a_rows - 1;
       }
     }
-    a_src[p] = (const char *)P.A + (size_t)(a_ok[p] ? src : 0) * P.lda * a_es;
+    a_src[p] = (const char *)P.A + (size_t)(a_row_ok[p] ? src : 0) * P.lda * sizeof(AT);
   }
   const char *b_src[C::B_PER_T];
 #pragma unroll
@@ -106,36 +126,36 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(Problems probs) {
     b_src[p] = (const char *)P.Bp + ((size_t)(n0 + (v >> 3)) * P.ldb + (v & 7) * C::EPV) * sizeof(CT);
   }
 
-  u32x4 ra[C::A_PER_T], rb[C::B_PER_T];
-  auto load_tile = [&](int kt) {
+  auto load_tile = [&](int kt, St &S) {
     const int kbase = kt * C::BK;
 #pragma unroll
     for (int p = 0; p < C::A_PER_T; ++p) {
       const int k = kbase + a_kv[p] * C::EPV;
-      if (!a_ok[p] || k >= P.K) {
-        ra[p] = u32x4{0u, 0u, 0u, 0u};
-      } else if (sizeof(CT) == 2 && !a_bf16) {
-        const float4 *s = (const float4 *)(a_src[p] + (size_t)k * 4);
-        ra[p] = pack_bf16x8(s[0], s[1]);
-      } else {
-        ra[p] = *(const u32x4 *)(a_src[p] + (size_t)k * sizeof(CT));
-      }
+      const int kc = k < P.K ? k : P.K - C::EPV;
+      const char *src = a_src[p] + (size_t)kc * sizeof(AT);
+#pragma unroll
+      for (int v = 0; v < C::AV; ++v) S.a[p][v] = *(const u32x4 *)(src + 16 * v);
     }
 #pragma unroll
-    for (int p = 0; p < C::B_PER_T; ++p) rb[p] = *(const u32x4 *)(b_src[p] + (size_t)kbase * sizeof(CT));
+    for (int p = 0; p < C::B_PER_T; ++p) S.b[p] = *(const u32x4 *)(b_src[p] + (size_t)kbase * sizeof(CT));
   };
-  auto store_tile = [&](int buf) {
+  auto store_tile = [&](int buf, const St &S) {
     char *As = lds + buf * C::STAGE;
     char *Bs = As + BM * kLdsStride;
 #pragma unroll
     for (int p = 0; p < C::A_PER_T; ++p) {
       const int v = tid + kThreads * p;
-      *(u32x4 *)(As + (v >> 3) * kLdsStride + (v & 7) * 16) = ra[p];
+      u32x4 val;
+      if constexpr (C::AV == 2)
+        val = pack_bf16x8(S.a[p][0], S.a[p][1]);
+      else
+        val = S.a[p][0];
+      *(u32x4 *)(As + (v >> 3) * kLdsStride + (v & 7) * 16) = val;
     }
 #pragma unroll
     for (int p = 0; p < C::B_PER_T; ++p) {
       const int v = tid + kThreads * p;
-      *(u32x4 *)(Bs + (v >> 3) * kLdsStride + (v & 7) * 16) = rb[p];
+      *(u32x4 *)(Bs + (v >> 3) * kLdsStride + (v & 7) * 16) = S.b[p];
     }
   };
 
@@ -145,13 +165,8 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(Problems probs) {
 #pragma unroll
     for (int j = 0; j < C::FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const int nk = (P.K + C::BK - 1) / C::BK;
-  load_tile(0);
-  store_tile(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    if (kt + 1 < nk) load_tile(kt + 1);
-    const char *As = lds + (kt & 1) * C::STAGE;
+  auto compute = [&](int buf) {
+    const char *As = lds + buf * C::STAGE;
     const char *Bs = As + BM * kLdsStride;
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
@@ -186,9 +201,35 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(Problems probs) {
               acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[i][s], fb[j][s], acc[i][j], 0, 0, 0);
       }
     }
-    if (kt + 1 < nk) store_tile((kt + 1) & 1);
+  };
+
+  // Iteration kt multiplies LDS stage kt & 1 (tile kt), loads tile kt + 2 into register
+  // stage kt & 1 and writes register stage (kt + 1) & 1 (tile kt + 1, loaded one iteration
+  // earlier) into the other LDS stage.  Tile indices clamp to the last tile, so the body is
+  // branch-free (the last two iterations re-load the last tile, an L2 hit, and the final
+  // LDS write is never read): conditional loads would make the compiler drain every
+  // outstanding load at the loop header.
+  St s0, s1;
+  const int nk = (P.K + C::BK - 1) / C::BK;
+  const int last = nk - 1;
+  auto step = [&](int kt, St &cur, St &nxt, int buf) {
+    load_tile(kt + 2 < last ? kt + 2 : last, cur);
+    __builtin_amdgcn_sched_barrier(0);
+    compute(buf);
+    __builtin_amdgcn_sched_barrier(0);
+    store_tile(buf ^ 1, nxt);
     __syncthreads();
+  };
+  load_tile(0, s0);
+  load_tile(1 < last ? 1 : last, s1);
+  store_tile(0, s0);
+  __syncthreads();
+  int kt = 0;
+  for (; kt + 1 < nk; kt += 2) {
+    step(kt, s0, s1, 0);
+    step(kt + 1, s1, s0, 1);
   }
+  if (kt < nk) step(kt, s0, s1, 0);
 
   {
     // lane holds D[row = 4*(lane/16) + r][col = lane % 16] of each 16x16 block
@@ -214,9 +255,7 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(Problems probs) {
   }
 }
 
-
-
-template <typename CT, int EPI, int BM, int BN>
+template <typename CT, typename AT, int EPI, int BM, int BN>
 static hipError_t go(const Problems &ps, int nprob, hipStream_t st) {
   int maxt = 0;
   for (int i = 0; i < nprob; ++i) {
@@ -224,26 +263,37 @@ static hipError_t go(const Problems &ps, int nprob, hipStream_t st) {
     maxt = t > maxt ? t : maxt;
   }
   if (maxt == 0) return hipSuccess;
-  hipLaunchKernelGGL((gemm_kernel<CT, EPI, BM, BN>), dim3(maxt, 1, nprob), dim3(kThreads), 0, st, ps);
+  hipLaunchKernelGGL((gemm_kernel<CT, AT, EPI, BM, BN>), dim3(maxt, 1, nprob), dim3(kThreads), 0, st, ps);
   return hipGetLastError();
 }
 
-template <typename CT>
-static hipError_t dispatch(const Problems &ps, int nprob, Epilogue epi, hipStream_t st) {
-  // big tiles when they already fill the chip, else 64 x 64
-  long t128 = 0;
-  for (int i = 0; i < nprob; ++i)
+template <typename CT, typename AT, int EPI>
+static hipError_t go_tiles(const Problems &ps, int nprob, hipStream_t st) {
+  // 128 x 128 tiles when they already fill the chip, 32 x 32 when 64 x 64 tiles would leave
+  // CUs idle, else 64 x 64
+  long t128 = 0, t64 = 0;
+  for (int i = 0; i < nprob; ++i) {
     t128 += (long)((ps.p[i].M + 127) / 128) * ((ps.p[i].N + 127) / 128);
-  const bool big = t128 >= 512;
-  if (epi == EPI_TANH)
-    return big ? go<CT, EPI_TANH, 128, 128>(ps, nprob, st) : go<CT, EPI_TANH, 64, 64>(ps, nprob, st);
-  return big ? go<CT, EPI_STORE, 128, 128>(ps, nprob, st) : go<CT, EPI_STORE, 64, 64>(ps, nprob, st);
+    t64 += (long)((ps.p[i].M + 63) / 64) * ((ps.p[i].N + 63) / 64);
+  }
+  if (t128 >= 512) return go<CT, AT, EPI, 128, 128>(ps, nprob, st);
+  if (t64 < 256) return go<CT, AT, EPI, 32, 32>(ps, nprob, st);
+  return go<CT, AT, EPI, 64, 64>(ps, nprob, st);
+}
+
+template <typename CT, typename AT>
+static hipError_t go_epi(const Problems &ps, int nprob, Epilogue epi, hipStream_t st) {
+  return epi == EPI_TANH ? go_tiles<CT, AT, EPI_TANH>(ps, nprob, st) : go_tiles<CT, AT, EPI_STORE>(ps, nprob, st);
 }
 
 hipError_t launch_gemm(int bf16_mma, const GemmProblem *probs, int nprob, Epilogue epi, hipStream_t st) {
   Problems ps{};
-  for (int i = 0; i < nprob; ++i) ps.p[i] = probs[i];
-  return bf16_mma ? dispatch<bf16>(ps, nprob, epi, st) : dispatch<float>(ps, nprob, epi, st);
+  for (int i = 0; i < nprob; ++i) {
+    ps.p[i] = probs[i];
+    if (probs[i].a_bf16 != probs[0].a_bf16 || (probs[i].a_bf16 && !bf16_mma)) return hipErrorInvalidValue;
+  }
+  if (!bf16_mma) return go_epi<float, float>(ps, nprob, epi, st);
+  return probs[0].a_bf16 ? go_epi<bf16, bf16>(ps, nprob, epi, st) : go_epi<bf16, float>(ps, nprob, epi, st);
 }
 
 }  // namespace mt

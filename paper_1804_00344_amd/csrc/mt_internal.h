@@ -135,22 +135,139 @@ __device__ __forceinline__ void block_extract(List<KMAX> &L, int n, Emit emit) {
   }
 }
 
-// Wave-level version (no barriers): the wave's best head is found with shuffles; the owning
-// lane pops it.  Every lane receives the n results in order through `emit` (lane-uniform).
-template <int KMAX, typename Emit>
-__device__ __forceinline__ void wave_extract(List<KMAX> &L, int n, Emit emit) {
-  for (int r = 0; r < n; ++r) {
-    float bv = L.v[0];
-    int bi = L.i[0];
+// ---- exact selection by bisection over order-preserving key codes ----
+// code(f) is a uint32 that orders like the float (-0 counts as +0); 0 marks "no entry".
+__device__ __forceinline__ uint32_t key_code(float f) {
+  uint32_t b = __float_as_uint(f);
+  if (b == 0x80000000u) b = 0u;
+  return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+__device__ __forceinline__ float key_from_code(uint32_t u) {
+  return __uint_as_float((u & 0x80000000u) ? (u & 0x7fffffffu) : ~u);
+}
+
+// Wave-wide counts over R register slots per lane, of which the first rs (wave-uniform) are
+// in use.  Ballots and scalar popcounts only: no cross-lane data movement.
+template <int R>
+__device__ __forceinline__ int wave_count_ge(const uint32_t (&u)[R], int rs, uint32_t t) {
+  int c = 0;
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      const float ov = __shfl_xor(bv, o, 64);
-      const int oi = __shfl_xor(bi, o, 64);
-      if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
+  for (int s = 0; s < R; ++s)
+    if (s < rs) c += __popcll(__ballot(u[s] >= t));
+  return c;
+}
+template <int R>
+__device__ __forceinline__ int wave_count_eq_le(const uint32_t (&u)[R], const int (&ix)[R], int rs, uint32_t t,
+                                                int i) {
+  int c = 0;
+#pragma unroll
+  for (int s = 0; s < R; ++s)
+    if (s < rs) c += __popcll(__ballot(u[s] == t && ix[s] <= i));
+  return c;
+}
+
+// Largest t with count(code >= t) >= K over the wave's entries (codes >= 1), given
+// count(code >= 1) >= K.  Binary search between the smallest and largest code present.
+template <int R>
+__device__ __forceinline__ uint32_t wave_kth_code(const uint32_t (&u)[R], int rs, int K) {
+  uint32_t lo = 0xffffffffu, hi = 0u;
+#pragma unroll
+  for (int s = 0; s < R; ++s)
+    if (s < rs && u[s] != 0u) {
+      lo = u[s] < lo ? u[s] : lo;
+      hi = u[s] > hi ? u[s] : hi;
     }
-    if (L.i[0] == bi && L.v[0] == bv) L.pop();
-    emit(r, bv, bi);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const uint32_t a = __shfl_xor(lo, o, 64), b = __shfl_xor(hi, o, 64);
+    lo = a < lo ? a : lo;
+    hi = b > hi ? b : hi;
   }
+  lo = __builtin_amdgcn_readfirstlane(lo);
+  hi = __builtin_amdgcn_readfirstlane(hi);
+  while (lo < hi) {  // invariant: count(>= lo) >= K, count(>= hi + 1) < K
+    const uint32_t mid = lo + (uint32_t)(((uint64_t)hi - lo + 1u) >> 1);
+    if (wave_count_ge<R>(u, rs, mid) >= K)
+      lo = mid;
+    else
+      hi = mid - 1u;
+  }
+  return lo;
+}
+
+// Exact top-K of the wave's entries (code u, index ix; u == 0 = empty slot) under the order
+// "larger key first, equal keys -> smaller index first".  Indices must be distinct.  The
+// selected entries are compacted into scratch (>= K slots, wave-private LDS); lane j < n_sel
+// (n_sel = min(K, entries)) then calls emit(rank, key, idx) for the j-th of them, with its
+// rank 0..n_sel-1 in that order.  Returns n_sel (wave-uniform).
+template <int R, typename Emit>
+__device__ __forceinline__ int wave_topk(const uint32_t (&u)[R], const int (&ix)[R], int rs, int K,
+                                         uint32_t *su, int *si, Emit emit) {
+  const int lane = threadIdx.x & 63;
+  const int n = wave_count_ge<R>(u, rs, 1u);
+  uint32_t tau = 1u;
+  int iota = 0x7fffffff;
+  if (n > K) {
+    tau = wave_kth_code<R>(u, rs, K);
+    const int gt = tau == 0xffffffffu ? 0 : wave_count_ge<R>(u, rs, tau + 1u);
+    const int need = K - gt;
+    const int eq = wave_count_eq_le<R>(u, ix, rs, tau, 0x7fffffff);
+    if (eq > need) {  // ties at the cut: keep the `need` smallest indices among them
+      int lo = 0x7fffffff, hi = (int)0x80000000;
+#pragma unroll
+      for (int s = 0; s < R; ++s)
+        if (s < rs && u[s] == tau) {
+          lo = ix[s] < lo ? ix[s] : lo;
+          hi = ix[s] > hi ? ix[s] : hi;
+        }
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) {
+        const int a = __shfl_xor(lo, o, 64), b = __shfl_xor(hi, o, 64);
+        lo = a < lo ? a : lo;
+        hi = b > hi ? b : hi;
+      }
+      lo = __builtin_amdgcn_readfirstlane(lo);
+      hi = __builtin_amdgcn_readfirstlane(hi);
+      while (lo < hi) {  // smallest i with count(code == tau, idx <= i) >= need
+        const int mid = (int)(((int64_t)lo + hi) >> 1);
+        if (wave_count_eq_le<R>(u, ix, rs, tau, mid) >= need)
+          hi = mid;
+        else
+          lo = mid + 1;
+      }
+      iota = lo;
+    }
+  }
+  // compact the selected entries into scratch
+  int base = 0;
+#pragma unroll
+  for (int s = 0; s < R; ++s) {
+    if (s >= rs) break;
+    const bool sel = u[s] != 0u && (u[s] > tau || (u[s] == tau && ix[s] <= iota));
+    const uint64_t bal = __ballot(sel);
+    const int pos = base + __popcll(bal & ((1ull << lane) - 1ull));
+    if (sel && pos < K) {  // more than K only if indices repeat, which callers exclude
+      su[pos] = u[s];
+      si[pos] = ix[s];
+    }
+    base += __popcll(bal);
+  }
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  const int ns = base < K ? base : K;
+  if (lane < ns) {
+    const uint32_t mu = su[lane];
+    const int mi = si[lane];
+    int rank = 0;
+    for (int j = 0; j < ns; ++j) {
+      const uint32_t ou = su[j];
+      const int oi = si[j];
+      rank += (ou > mu || (ou == mu && oi < mi)) ? 1 : 0;
+    }
+    emit(rank, key_from_code(mu), mi);
+  }
+  return ns;
 }
 
 // ---------------------------------------------------------------------------------------
@@ -198,11 +315,11 @@ hipError_t launch_vocab_threshold(int M, int V, int K, const float *sample, floa
 hipError_t launch_vocab(int bf16_mma, const void *t, const void *wp, const float *bias_pad, int M, int V,
                         int E, int n_chunks, const float *thr, float2 *part, int2 *cbuf, int *ccnt, int cap,
                         float *logits, hipStream_t st);
-// row_out [M][K] (key bits, token): the K best keys prev_score + (logit - lse) of each row
-hipError_t launch_vocab_rows(int bf16_mma, const void *t, const void *wp, const float *bias_pad, int M, int V,
-                             int E, int K, int n_chunks, const int2 *cbuf, const int *ccnt, int cap,
-                             const float *lse, const float *prev_score, int2 *row_out, int *ovf,
-                             hipStream_t st);
+// exact recomputation of the rows with ovf[m] != 0: row_out[m] = the K best keys
+// prev_score + (logit - lse) over the whole vocabulary
+hipError_t launch_vocab_fallback(int bf16_mma, const void *t, const void *wp, const float *bias_pad, int M,
+                                 int V, int E, int K, const float *lse, const float *prev_score, int2 *row_out,
+                                 const int *ovf, hipStream_t st);
 constexpr int kVocabCap = 32;  // candidate buffer entries per (row, chunk, list)
 constexpr int kVocabPad = 64;  // vocabulary rows are padded to a multiple of this
 
@@ -227,10 +344,13 @@ hipError_t launch_attention(int B, int K, int S, int A, int Cd, const void *P, c
 hipError_t launch_lse(int M, int ntiles, const float2 *part, float *lse, float *logits, int V,
                       hipStream_t st);
 
-// candidates are (key, idx) pairs stored as int2 {float bits, idx}
-hipError_t launch_topk_rows(int M, int K, int V, int ncand_per_row, const int2 *cand,
-                            const float *lse, const float *prev_score, int2 *row_out,
-                            hipStream_t st);
+// candidates are (value, token) pairs stored as int2 {float bits, token}.  Row selection: the K
+// best keys of each row from nl lists of up to cap candidates (cnt NULL = lists full; lse NULL
+// = values are keys, else logits keyed as prev_score + (logit - lse)); rows whose candidates do
+// not fit get ovf[m] = 1 and no output (see launch_vocab_fallback), the others ovf[m] = 0.
+hipError_t launch_row_select(int M, int K, int V, int nl, int cap, const int *cnt, const int2 *cbuf,
+                             const float *lse, const float *prev_score, int2 *row_out, int *ovf,
+                             hipStream_t st);
 hipError_t launch_topk_scan_logp(int M, int K, int V, int nchunks, const float *prev_score,
                                  const float *logp, int2 *cand_out, hipStream_t st);
 hipError_t launch_topk_sentence(int B, int K, int V, const int2 *row_cand, float *score_out,

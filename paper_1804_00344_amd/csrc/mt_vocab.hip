@@ -19,8 +19,8 @@
 // any subset of that row.  A small first pass computes the logits of the first S vocabulary
 // entries and takes their K-th best (minus a rounding margin) as the row's threshold; the main
 // pass appends every logit at or above it to a per-lane buffer (one compare per logit, a
-// store when it passes).  The row merge then selects the K best keys among the few collected
-// values; a row whose buffer overflowed is recomputed there in full, so the result is exact.
+// store when it passes).  The row selection then takes the K best keys among the collected
+// values; a row whose buffers overflowed is recomputed in full, so the result is exact.
 //
 // Packed weights (built at load time): for 32-row vocabulary block vb and k-step ks of KV
 // k-values, 64 lanes x 16 bytes at ((vb * KS + ks) * 64 + lane) * 16, where lane l holds
@@ -37,6 +37,7 @@ typedef uint32_t v4u __attribute__((ext_vector_type(4)));
 constexpr int kVRows = 64;       // vocabulary rows per wave tile (2 MFMA blocks)
 constexpr int kLists = 8;        // candidate buffers per (hypothesis, chunk): 2 lane halves x 4 runs
 constexpr int kSampleMax = 512;  // vocabulary entries of the threshold pass
+constexpr float kLog2e = 1.4426950408889634f;
 
 template <int HB>
 struct VShape {
@@ -118,7 +119,8 @@ __global__ __launch_bounds__(VShape<HB>::NT) void vocab_kernel(VocabArgs a) {
 
   float lm[HBB], ls[HBB], th[HBB];
   int cnt[HBB];
-  size_t cb[HBB];  // first entry of this lane's candidate buffer, per hypothesis block
+  uint32_t loff[HBB];  // byte offset of this lane's candidate list in cbuf, per hypothesis block
+  char *const cbase = (char *)a.cbuf;
 #pragma unroll
   for (int j = 0; j < HBB; ++j) {
     const int h = h0 + hc0 + j * 32 + lrow;
@@ -126,33 +128,57 @@ __global__ __launch_bounds__(VShape<HB>::NT) void vocab_kernel(VocabArgs a) {
     ls[j] = 0.f;
     cnt[j] = 0;
     th[j] = (collect && h < a.M) ? a.thr[h] : INFINITY;
-    cb[j] = (((size_t)(h < a.M ? h : 0) * a.n_chunks + chunk) * kLists + src) * a.cap;
+    loff[j] = (uint32_t)((((size_t)(h < a.M ? h : 0) * a.n_chunks + chunk) * kLists + src) * a.cap * sizeof(int2));
   }
+
+  // With two hypothesis groups (two waves per SIMD, same vocabulary tiles), both waves of a
+  // SIMD would reach their VALU-heavy tile epilogues at the same moments and leave the
+  // matrix core idle meanwhile.  Starting the second group about half a tile late puts one
+  // wave's epilogue under the other's MFMAs.
+  if (VShape<HB>::NW > 4 && (wave >> 2) == 1) __builtin_amdgcn_s_sleep(32);
 
   if (ntile > 0) {
     // Weight fragments of step g of tile ti are vocabulary blocks 2*(t_begin+ti) and +1 at
-    // k-step ks.  Every prefetch is issued unconditionally (clamped to the last step) and a
-    // slot is refilled only after its MFMAs consumed it, so waits can be exact.
-    const v4u *wbase = (const v4u *)a.wp + (size_t)2 * t_begin * KS * 64 + lane;
+    // k-step ks, 1 KiB (64 lanes x 16 bytes) apart per k-step.  The ring is refilled right
+    // after its slot is consumed, from a wave-uniform fragment index that advances without a
+    // branch (clamped to the last step), so the loads stay in flight across k-steps: a
+    // conditional refill would make the compiler wait for every outstanding load.
+    const v4u *wb = (const v4u *)a.wp + (size_t)2 * t_begin * KS * 64 + lane;
     int pf_k = 0, pf_n = 0;
-    const v4u *pf = wbase;
-    auto advance = [&]() {
-      if (pf_n + 1 < total) {
-        ++pf_n;
-        pf += 64;
-        if (++pf_k == KS) { pf_k = 0; pf += (size_t)KS * 64; }
-      }
+    int poff = 0;  // fragment index of the next prefetch, in 1 KiB steps from wb
+    auto fetch = [&](v4u(&slot)[2]) {
+      slot[0] = wb[(size_t)poff * 64];
+      slot[1] = wb[(size_t)(poff + KS) * 64];
+      const int more = pf_n + 1 < total ? 1 : 0;
+      const int nk = pf_k + more;
+      const int wrap = nk == KS ? 1 : 0;
+      pf_n += more;
+      pf_k = wrap ? 0 : nk;
+      poff += more + wrap * KS;
     };
     v4u ring[D][2];
 #pragma unroll
-    for (int d = 0; d < D; ++d) {
-      ring[d][0] = pf[0];
-      ring[d][1] = pf[(size_t)KS * 64];
-      advance();
-    }
+    for (int d = 0; d < D; ++d) fetch(ring[d]);
     const v4u *bl = (const v4u *)lds + (size_t)(hc0 + lrow) * (rowb / 16) + lhalf * (KV / 2 * es / 16);
 
+    // activation fragments of k-step ks (identical for every tile, so the sequence repeats
+    // with period KS).  With one wave per SIMD (fp32) the fragments of the next k-step are
+    // read before the current step's MFMAs so the LDS latency is not exposed; bf16 runs two
+    // waves per SIMD, which cover it, and has no registers to spare for the second copy.
+    constexpr bool kPrefetchLds = es == 4;
+    auto lds_frag = [&](int ks, v4u(&f)[HBB]) {
+#pragma unroll
+      for (int j = 0; j < HBB; ++j) f[j] = bl[(size_t)j * 32 * (rowb / 16) + ks * (KV * es / 16)];
+    };
+    v4u bcur[HBB], bnxt[HBB];
+    if constexpr (kPrefetchLds) lds_frag(0, bcur);
+
     for (int ti = 0; ti < ntile; ++ti) {
+      // Drain the memory counter once per tile (stores count in it too, and the previous
+      // epilogue issued a data-dependent number of them; the ring loads have long arrived).
+      // With nothing outstanding on entry, the compiler keeps exact, non-draining waits on
+      // the ring inside the k-loop.
+      __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
       f32x16 acc[2][HBB];
 #pragma unroll
       for (int i = 0; i < 2; ++i)
@@ -165,10 +191,13 @@ __global__ __launch_bounds__(VShape<HB>::NT) void vocab_kernel(VocabArgs a) {
 #pragma unroll
         for (int d = 0; d < D; ++d) {
           const int ks = ks0 + d;
+          if constexpr (kPrefetchLds) {
+            lds_frag(ks + 1 < KS ? ks + 1 : 0, bnxt);
+            __builtin_amdgcn_sched_barrier(0);  // issue the reads before this step's MFMAs
+          } else {
+            lds_frag(ks, bcur);
+          }
           const v4u c0 = ring[d][0], c1 = ring[d][1];
-          v4u bfr[HBB];
-#pragma unroll
-          for (int j = 0; j < HBB; ++j) bfr[j] = bl[(size_t)j * 32 * (rowb / 16) + ks * (KV * es / 16)];
           if constexpr (es == 2) {
             bf16x8 a0, a1;
             __builtin_memcpy(&a0, &c0, 16);
@@ -176,7 +205,7 @@ __global__ __launch_bounds__(VShape<HB>::NT) void vocab_kernel(VocabArgs a) {
 #pragma unroll
             for (int j = 0; j < HBB; ++j) {
               bf16x8 b;
-              __builtin_memcpy(&b, &bfr[j], 16);
+              __builtin_memcpy(&b, &bcur[j], 16);
               acc[0][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b, acc[0][j], 0, 0, 0);
               acc[1][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b, acc[1][j], 0, 0, 0);
             }
@@ -185,7 +214,7 @@ __global__ __launch_bounds__(VShape<HB>::NT) void vocab_kernel(VocabArgs a) {
             __builtin_memcpy(fa0, &c0, 16);
             __builtin_memcpy(fa1, &c1, 16);
 #pragma unroll
-            for (int j = 0; j < HBB; ++j) __builtin_memcpy(fb[j], &bfr[j], 16);
+            for (int j = 0; j < HBB; ++j) __builtin_memcpy(fb[j], &bcur[j], 16);
 #pragma unroll
             for (int s = 0; s < 4; ++s)
 #pragma unroll
@@ -194,9 +223,15 @@ __global__ __launch_bounds__(VShape<HB>::NT) void vocab_kernel(VocabArgs a) {
                 acc[1][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa1[s], fb[j][s], acc[1][j], 0, 0, 0);
               }
           }
-          ring[d][0] = pf[0];
-          ring[d][1] = pf[(size_t)KS * 64];
-          advance();
+          fetch(ring[d]);
+          if constexpr (kPrefetchLds) {
+#pragma unroll
+            for (int j = 0; j < HBB; ++j) bcur[j] = bnxt[j];
+          }
+          // keep each refill right behind the MFMAs that consumed its slot (left alone, the
+          // scheduler sinks all refills to the end of the unrolled body, which shortens the
+          // prefetch distance of the first slots to almost nothing)
+          __builtin_amdgcn_sched_barrier(0);
         }
       }
 
@@ -224,16 +259,17 @@ __global__ __launch_bounds__(VShape<HB>::NT) void vocab_kernel(VocabArgs a) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) mt = fmaxf(mt, acc[i][j][r]);
           if (mt != -INFINITY) {  // -inf only when the whole tile is padding
+            const float mts = mt * kLog2e;
             float se = 0.f;
 #pragma unroll
             for (int i = 0; i < 2; ++i)
 #pragma unroll
               for (int r = 0; r < 16; ++r) {
                 const float x = acc[i][j][r];
-                se += exp_fast(x - mt);
-                if (x >= th[j]) {
-                  if (cnt[j] < a.cap)
-                    a.cbuf[cb[j] + cnt[j]] = make_int2(__float_as_int(x), v0 + 32 * i + 8 * (r >> 2) + 4 * lhalf + (r & 3));
+                se += __builtin_amdgcn_exp2f(__builtin_fmaf(x, kLog2e, -mts));
+                if (x >= th[j]) {  // a slot past the list's capacity only counts (overflow)
+                  const uint32_t o = loff[j] + (uint32_t)(cnt[j] < a.cap - 1 ? cnt[j] : a.cap - 1) * 8u;
+                  *(int2 *)(cbase + o) = make_int2(__float_as_int(x), v0 + 32 * i + 8 * (r >> 2) + 4 * lhalf + (r & 3));
                   ++cnt[j];
                 }
               }
@@ -283,70 +319,29 @@ __global__ __launch_bounds__(VShape<HB>::NT) void vocab_kernel(VocabArgs a) {
   }
 }
 
-// Threshold of each row: the K-th best of the first S logits, lowered by a margin that covers
-// fp32 rounding of the keys (two logits whose keys round equal differ by far less).
-template <int KMAX>
+// Threshold of each row: the K-th best of the first S logits (exact, by bisection over
+// order-preserving codes), lowered by a margin that covers the rounding difference between
+// this pass's logits and the main pass's (the two sum the same products in different orders).
+template <int R>
 __global__ __launch_bounds__(256) void vocab_threshold_kernel(int M, int S, int K, const float *__restrict__ sample,
                                                               int ld, float *__restrict__ thr) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int m = blockIdx.x * 4 + w;
   if (m >= M) return;  // uniform per wave
   const float *row = sample + (size_t)m * ld;
-  List<KMAX> lst;
-  lst.init();
-  for (int v = lane; v < S; v += 64) lst.push(row[v], v);
-  float kth = -INFINITY;
-  for (int r = 0; r < K; ++r) {
-    float bv = lst.v[0];
-    int bi = lst.i[0];
+  uint32_t u[R];
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      const float ov = __shfl_xor(bv, o, 64);
-      const int oi = __shfl_xor(bi, o, 64);
-      if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
-    }
-    if (lst.i[0] == bi && lst.v[0] == bv) lst.pop();
-    kth = bv;
+  for (int s = 0; s < R; ++s) {
+    const int v = s * 64 + lane;
+    u[s] = v < S ? key_code(row[v]) : 0u;
   }
+  float kth = -INFINITY;
+  if (wave_count_ge<R>(u, R, 1u) >= K) kth = key_from_code(wave_kth_code<R>(u, R, K));
   if (lane == 0) thr[m] = kth - 1e-3f * (1.0f + fabsf(kth));
 }
 
-// Row merge of the fused path, one wave per row: the K best keys (score + (logit - lse)) among
-// the row's collected candidates.  A row with an overflowed buffer is only flagged here and
-// recomputed by vocab_fallback_kernel.
-template <int KMAX>
-__global__ __launch_bounds__(256) void vocab_rows_kernel(VocabArgs a, int K, const float *__restrict__ lse,
-                                                         const float *__restrict__ prev_score,
-                                                         int2 *__restrict__ row_out, int *__restrict__ ovf) {
-  const int lane = threadIdx.x & 63;
-  const int m = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (m >= a.M) return;  // uniform per wave
-  const int nl = a.n_chunks * kLists;
-  const int *cnt = a.ccnt + (size_t)m * nl;
-  const float Lm = lse[m], sc = prev_score[m];
-  List<KMAX> lst;
-  lst.init();
-  bool over = false;
-  for (int l = lane; l < nl; l += 64) {
-    const int n = cnt[l];
-    over |= n > a.cap;
-    const int2 *e = a.cbuf + ((size_t)m * nl + l) * a.cap;
-    const int nn = n < a.cap ? n : a.cap;
-    for (int q = 0; q < nn; ++q) {
-      const int2 c = e[q];
-      const float lp = __int_as_float(c.x) - Lm;
-      lst.push(sc + lp, c.y);
-    }
-  }
-  const bool any_over = __ballot(over) != 0ull;
-  if (lane == 0) ovf[m] = any_over ? 1 : 0;
-  wave_extract<KMAX>(lst, K, [&](int r, float v, int i) {
-    if (lane == 0) row_out[(size_t)m * K + r] = make_int2(__float_as_int(v), i);
-  });
-}
-
-// Exact recomputation of the rows flagged by vocab_rows_kernel (a buffer overflowed): the full
-// logit row from the packed weights, then the K best keys.  Workgroup x reads the flags of rows
+// Exact recomputation of the rows flagged by the row selection (their candidates did not fit):
+// the full logit row from the packed weights, then the K best keys.  Workgroup x reads the flags of rows
 // [256x, 256x + 256) in parallel and processes its flagged rows one after another.
 template <typename CT, int KMAX>
 __global__ __launch_bounds__(256) void vocab_fallback_kernel(VocabArgs a, int K, const float *__restrict__ lse,
@@ -514,14 +509,8 @@ hipError_t launch_vocab_threshold(int M, int V, int K, const float *sample, floa
   if (M == 0) return hipSuccess;
   const int S = vocab_sample_size(V);
   const int Sv = V < S ? V : S;  // entries >= V of the sample are padding
-#define MT_TH(N) \
-  hipLaunchKernelGGL((vocab_threshold_kernel<N>), dim3((M + 3) / 4), dim3(256), 0, st, M, Sv, K, sample, S, thr)
-  if (K <= 1) MT_TH(1);
-  else if (K <= 2) MT_TH(2);
-  else if (K <= 4) MT_TH(4);
-  else if (K <= 8) MT_TH(8);
-  else MT_TH(16);
-#undef MT_TH
+hipLaunchKernelGGL((vocab_threshold_kernel<kSampleMax / 64>), dim3((M + 3) / 4), dim3(256), 0, st, M, Sv, K, sample,
+                     S, thr);
   return hipGetLastError();
 }
 
@@ -542,37 +531,28 @@ hipError_t launch_vocab(int bf16_mma, const void *t, const void *wp, const float
   return vgo_any(bf16_mma, a, st);
 }
 
-hipError_t launch_vocab_rows(int bf16_mma, const void *t, const void *wp, const float *bias_pad, int M, int V,
-                             int E, int K, int n_chunks, const int2 *cbuf, const int *ccnt, int cap,
-                             const float *lse, const float *prev_score, int2 *row_out, int *ovf,
-                             hipStream_t st) {
+hipError_t launch_vocab_fallback(int bf16_mma, const void *t, const void *wp, const float *bias_pad, int M,
+                                 int V, int E, int K, const float *lse, const float *prev_score, int2 *row_out,
+                                 const int *ovf, hipStream_t st) {
   if (M == 0) return hipSuccess;
   VocabArgs a = base_args(bf16_mma, t, wp, bias_pad, M, V, E);
-  a.n_chunks = n_chunks;
-  a.cbuf = (int2 *)cbuf;
-  a.ccnt = (int *)ccnt;
-  a.cap = cap;
   const int nfb = (M + 255) / 256;
-#define MT_VR(CT, N)                                                                                         \
-  do {                                                                                                       \
-    hipLaunchKernelGGL((vocab_rows_kernel<N>), dim3((M + 3) / 4), dim3(256), 0, st, a, K, lse, prev_score,  \
-                       row_out, ovf);                                                                        \
-    hipLaunchKernelGGL((vocab_fallback_kernel<CT, N>), dim3(nfb), dim3(256), 0, st, a, K, lse, prev_score,  \
-                       row_out, (const int *)ovf);                                                           \
-  } while (0)
-#define MT_VRK(CT)                 \
-  if (K <= 1) MT_VR(CT, 1);        \
-  else if (K <= 2) MT_VR(CT, 2);   \
-  else if (K <= 4) MT_VR(CT, 4);   \
-  else if (K <= 8) MT_VR(CT, 8);   \
-  else MT_VR(CT, 16);
+#define MT_VF(CT, N)                                                                                          \
+  hipLaunchKernelGGL((vocab_fallback_kernel<CT, N>), dim3(nfb), dim3(256), 0, st, a, K, lse, prev_score, \
+                     row_out, ovf)
+#define MT_VFK(CT)                 \
+  if (K <= 1) MT_VF(CT, 1);        \
+  else if (K <= 2) MT_VF(CT, 2);   \
+  else if (K <= 4) MT_VF(CT, 4);   \
+  else if (K <= 8) MT_VF(CT, 8);   \
+  else MT_VF(CT, 16);
   if (bf16_mma) {
-    MT_VRK(bf16)
+    MT_VFK(bf16)
   } else {
-    MT_VRK(float)
+    MT_VFK(float)
   }
-#undef MT_VRK
-#undef MT_VR
+#undef MT_VFK
+#undef MT_VF
   return hipGetLastError();
 }
 
