@@ -114,7 +114,9 @@ typedef struct {
 
 /* Copy, pack and convert the weights into library-owned device memory on
  * the current HIP device (fused gate layouts, K-contiguous transposes,
- * bf16 round-to-nearest-even when gemm_dtype is MT_BF16).  Synchronous.
+ * bf16 round-to-nearest-even when gemm_dtype is MT_BF16), and compute the
+ * token-side table emb [W1 | Wt_y] + [b1 | 0] ([V, 3H+E] fp32, V(3H+E)*4
+ * bytes of device memory) that the step gathers rows from.  Synchronous.
  * On success *out receives the handle; release it with mt_free. */
 mt_status mt_load_weights(const mt_config *cfg, const mt_weights *w, mt_model **out);
 
@@ -181,7 +183,7 @@ mt_status mt_device_errors(mt_model *model, int32_t *flags);
  * duration in milliseconds and the number of timed launches since the last
  * reset. */
 typedef enum {
-  MT_KERNEL_GEMM_GRU1 = 0,  /* x [W1|Wt_y] and h U1 */
+  MT_KERNEL_GEMM_GRU1 = 0,  /* h U1 (the token side is a precomputed table) */
   MT_KERNEL_GRU_CELL = 1,   /* both GRU elementwise kernels */
   MT_KERNEL_GEMM_S1 = 2,    /* s1 [Wa|U2] */
   MT_KERNEL_ATTENTION = 3,

@@ -61,8 +61,10 @@ struct mt_model {
   void *wo_frag;  // output matrix in MFMA fragment order (vocabulary kernel)
   Packed wsamp;   // its first vocab_sample_size(V) columns in the GEMM layout (threshold pass)
   float *bo_pad;  // output bias padded to a multiple of kVocabPad with -inf
+  int logit_bounded;  // every logit provably in [-40, 40] (see mt_load_weights)
   int num_cu;
-  void *emb;      // [V][E] fp32 (row gather source)
+  void *emb;      // [V][E] fp32
+  float *embx;    // [V][3H+E] fp32: emb [W1 | Wt_y] + [b1 | 0], the token side of GRU 1 and the readout
   float *bias1x, *bias3, *ba, *bi, *bt, *va;
   float *ln[10];  // g1a be1a g1u be1u g2a be2a g2u be2u gt bet
   int32_t *err;
@@ -148,7 +150,7 @@ mt_status dev_upload(mt_model *m, const void *host, size_t bytes, void **out) {
   const hipError_t e = hipMalloc(&d, bytes ? bytes : 16);
   if (e != hipSuccess) return fail(MT_ERR_OOM, "hipMalloc(%zu): %s", bytes, hipGetErrorString(e));
   m->allocs.push_back(d);
-  if (bytes) HIP_TRY(hipMemcpy(d, host, bytes, hipMemcpyHostToDevice));
+  if (bytes && host) HIP_TRY(hipMemcpy(d, host, bytes, hipMemcpyHostToDevice));
   *out = d;
   return MT_OK;
 }
@@ -179,7 +181,7 @@ std::vector<float> cat(std::initializer_list<std::pair<const float *, int>> part
 
 // ---- workspace ----
 struct WsLayout {
-  size_t gx, gh, s1, g2, c, g3, g4, t, sample, thr, part, cbuf, ccnt, ovf, lse, rowc, scand, total;
+  size_t gh, s1, g2, c, g3, g4, t, sample, thr, part, cbuf, ccnt, ovf, lse, rowc, scand, total;
   int ntiles, kc, nchunks;
 };
 
@@ -193,7 +195,6 @@ WsLayout ws_layout(const mt_model *m, int B, int K) {
     off += rup(bytes, 256);
     return o;
   };
-  L.gx = take(M * (3 * H + E) * 4);
   L.gh = take(M * 3 * H * 4);
   L.s1 = take(M * H * 4);
   L.g2 = take(M * (A + 3 * H) * 4);
@@ -355,9 +356,41 @@ mt_status mt_load_weights(const mt_config *cfg, const mt_weights *w, mt_model **
       std::vector<float> bp((V + kVocabPad - 1) / kVocabPad * kVocabPad, -INFINITY);
       std::copy(w->bo, w->bo + V, bp.begin());
       CHECK(upload_vec(m, bp, &m->bo_pad));
+      // The readout activations are tanh outputs (|t_e| <= 1, also after bf16 rounding), so
+      // |logit_v| <= sqrt(E) |Wo[:, v]|_2 + |bo_v| (Cauchy-Schwarz; the weights as the kernel
+      // sees them, i.e. bf16-rounded for a bf16 model, plus a relative slack for rounding).
+      // When that bound is at most 40 the vocabulary kernel sums exp(logit) with no running
+      // maximum: no term can overflow (e^40 * V is far below the fp32 range) or underflow.
+      std::vector<double> ss(V, 0.0);
+      auto as_kernel_sees = [&](float x) {
+        if (m->bf16) {
+          const uint32_t hb = (uint32_t)bf16_bits(x) << 16;
+          std::memcpy(&x, &hb, 4);
+        }
+        return (double)x;
+      };
+      if (c.tied_output) {
+        for (int v = 0; v < V; ++v)
+          for (int e = 0; e < E; ++e) {
+            const double x = as_kernel_sees(w->emb[(size_t)v * E + e]);
+            ss[v] += x * x;
+          }
+      } else {
+        for (int e = 0; e < E; ++e)
+          for (int v = 0; v < V; ++v) {
+            const double x = as_kernel_sees(w->Wo[(size_t)e * V + v]);
+            ss[v] += x * x;
+          }
+      }
+      double bound = 0.0;
+      for (int v = 0; v < V; ++v) {
+        const double bv = std::sqrt((double)E * ss[v]) * 1.01 + std::fabs((double)w->bo[v]);
+        if (!(bv <= bound)) bound = bv;  // NaN propagates as "unbounded"
+      }
+      m->logit_bounded = bound <= 40.0 ? 1 : 0;
     }
-    // embedding rows stay fp32 (only the gathered rows are read; a bf16 model rounds them to
-    // bf16 when they are staged as the GEMM operand, like every other fp32 activation)
+    // embedding rows stay fp32 (a bf16 model rounds them to bf16 when they are staged as the
+    // GEMM operand, like every other fp32 activation)
     CHECK(dev_upload(m, w->emb, (size_t)V * E * sizeof(float), &m->emb));
     CHECK(upload_vec(m, cat({{w->b1, 3 * H}, {nullptr, E}}), &m->bias1x));
     CHECK(upload_vec(m, cat({{w->b2, 3 * H}, {nullptr, E}}), &m->bias3));
@@ -371,6 +404,19 @@ mt_status mt_load_weights(const mt_config *cfg, const mt_weights *w, mt_model **
     }
     int32_t zero = 0;
     CHECK(dev_upload(m, &zero, sizeof zero, (void **)&m->err));
+    {
+      // The token side of GRU 1 and of the readout, x [W1 | Wt_y] + [b1 | 0], depends only on
+      // the token: it is computed once here for the whole vocabulary (same products, same
+      // operand rounding as a per-step product) and the step gathers rows of it.
+      CHECK(dev_upload(m, nullptr, (size_t)V * (3 * H + E) * sizeof(float), (void **)&m->embx));
+      GemmProblem p{};
+      p.A = m->emb; p.a_rows = V; p.lda = E; p.a_bf16 = 0;
+      p.Bp = m->w1x.p; p.ldb = m->w1x.ldb; p.bias = m->bias1x;
+      p.out = m->embx; p.ldc = 3 * H + E; p.out_bf16 = 0;
+      p.M = V; p.N = 3 * H + E; p.K = E;
+      HIP_TRY(launch_gemm(m->bf16, &p, 1, EPI_STORE, nullptr));
+      HIP_TRY(hipDeviceSynchronize());
+    }
     return MT_OK;
   };
   s = run();
@@ -478,7 +524,7 @@ mt_status mt_decoder_step(mt_model *model, int B, int K, int S, const int32_t *p
   if (ws_bytes < L.total) return fail(MT_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, L.total);
   hipStream_t st = (hipStream_t)stream;
   char *W = (char *)ws;
-  float *gx = (float *)(W + L.gx), *gh = (float *)(W + L.gh), *s1 = (float *)(W + L.s1);
+  float *gh = (float *)(W + L.gh), *s1 = (float *)(W + L.s1);
   float *g2 = (float *)(W + L.g2), *cc = (float *)(W + L.c), *g3 = (float *)(W + L.g3);
   float *g4 = (float *)(W + L.g4);
   void *t = W + L.t;
@@ -487,20 +533,18 @@ mt_status mt_decoder_step(mt_model *model, int B, int K, int S, const int32_t *p
   float *const *ln = model->ln;
   const bool LNon = c.layer_norm != 0;
 
-  // GRU 1 products: x [W1 | Wt_y] + [b1 | 0] and h U1 (one launch, two problems)
-  GemmProblem p1[2] = {};
-  p1[0].A = model->emb; p1[0].a_idx = prev_tok; p1[0].a_rows = V; p1[0].lda = E; p1[0].a_bf16 = 0;
-  p1[0].Bp = model->w1x.p; p1[0].ldb = model->w1x.ldb; p1[0].bias = model->bias1x;
-  p1[0].out = gx; p1[0].ldc = 3 * H + E; p1[0].M = M; p1[0].N = 3 * H + E; p1[0].K = E;
-  p1[0].err = model->err; p1[0].err_bit = 0;
-  p1[1].A = state_in; p1[1].a_idx = src_row; p1[1].a_rows = n_state_rows; p1[1].lda = H; p1[1].a_bf16 = 0;
-  p1[1].Bp = model->w1h.p; p1[1].ldb = model->w1h.ldb; p1[1].bias = nullptr;
-  p1[1].out = gh; p1[1].ldc = 3 * H; p1[1].M = M; p1[1].N = 3 * H; p1[1].K = H;
-  p1[1].err = model->err; p1[1].err_bit = 1;
-  LAUNCH(MT_KERNEL_GEMM_GRU1, launch_gemm(bf, p1, 2, EPI_STORE, st));
+  // GRU 1: h U1 (the gathered previous state), then the cell with the token side gathered
+  // from the precomputed x [W1 | Wt_y] + [b1 | 0] table
+  GemmProblem p1{};
+  p1.A = state_in; p1.a_idx = src_row; p1.a_rows = n_state_rows; p1.lda = H; p1.a_bf16 = 0;
+  p1.Bp = model->w1h.p; p1.ldb = model->w1h.ldb; p1.bias = nullptr;
+  p1.out = gh; p1.ldc = 3 * H; p1.M = M; p1.N = 3 * H; p1.K = H;
+  p1.err = model->err; p1.err_bit = 1;
+  LAUNCH(MT_KERNEL_GEMM_GRU1, launch_gemm(bf, &p1, 1, EPI_STORE, st));
   LAUNCH(MT_KERNEL_GRU_CELL,
-         launch_gru_cell(M, H, gx, 3 * H + E, gh, 3 * H, state_in, src_row, n_state_rows, model->err,
-                         LNon ? ln[0] : nullptr, ln[1], ln[2], ln[3], eps, s1, H, taps ? taps->s1 : nullptr, st));
+         launch_gru_cell(M, H, model->embx, 3 * H + E, prev_tok, V, gh, 3 * H, state_in, src_row, n_state_rows,
+                         model->err, LNon ? ln[0] : nullptr, ln[1], ln[2], ln[3], eps, s1, H,
+                         taps ? taps->s1 : nullptr, st));
   // s1 [Wa | U2]: attention query and GRU 2 recurrent product
   GemmProblem p2{};
   p2.A = s1; p2.a_rows = M; p2.lda = H; p2.a_bf16 = 0;
@@ -517,7 +561,7 @@ mt_status mt_decoder_step(mt_model *model, int B, int K, int S, const int32_t *p
   p3.out = g3; p3.ldc = 3 * H + E; p3.M = M; p3.N = 3 * H + E; p3.K = C;
   LAUNCH(MT_KERNEL_GEMM_CTX, launch_gemm(bf, &p3, 1, EPI_STORE, st));
   LAUNCH(MT_KERNEL_GRU_CELL,
-         launch_gru_cell(M, H, g3, 3 * H + E, g2 + A, A + 3 * H, s1, nullptr, M, model->err,
+         launch_gru_cell(M, H, g3, 3 * H + E, nullptr, M, g2 + A, A + 3 * H, s1, nullptr, M, model->err,
                          LNon ? ln[4] : nullptr, ln[5], ln[6], ln[7], eps, state_out, H, nullptr, st));
   // readout: s Wt_s, then tanh(LN?(s Wt_s + x Wt_y + c Wt_c + bt))
   GemmProblem p4{};
@@ -525,7 +569,8 @@ mt_status mt_decoder_step(mt_model *model, int B, int K, int S, const int32_t *p
   p4.Bp = model->w4.p; p4.ldb = model->w4.ldb;
   p4.out = g4; p4.ldc = E; p4.M = M; p4.N = E; p4.K = H;
   LAUNCH(MT_KERNEL_GEMM_READOUT, launch_gemm(bf, &p4, 1, EPI_STORE, st));
-  LAUNCH(MT_KERNEL_READOUT, launch_readout(M, E, g4, E, gx + 3 * H, 3 * H + E, g3 + 3 * H, 3 * H + E, model->bt,
+  LAUNCH(MT_KERNEL_READOUT, launch_readout(M, E, g4, E, model->embx + 3 * H, 3 * H + E, prev_tok, V, g3 + 3 * H,
+                                           3 * H + E, model->bt,
                                            LNon ? ln[8] : nullptr, ln[9], eps, t, bf, taps ? taps->t : nullptr, st));
   // vocabulary projection: threshold pass, then the full pass with fused log-sum-exp partials
   // and threshold-filtered beam candidates
@@ -542,7 +587,7 @@ mt_status mt_decoder_step(mt_model *model, int B, int K, int S, const int32_t *p
   }
   LAUNCH(MT_KERNEL_VOCAB_GEMM, launch_vocab(bf, t, model->wo_frag, model->bo_pad, M, V, E, L.ntiles,
                                             (const float *)(W + L.thr), part, (int2 *)(W + L.cbuf),
-                                            (int *)(W + L.ccnt), kVocabCap, logp_out, st));
+                                            (int *)(W + L.ccnt), kVocabCap, logp_out, model->logit_bounded, st));
   LAUNCH(MT_KERNEL_LSE, launch_lse(M, L.ntiles, part, (float *)(W + L.lse), logp_out, V, st));
   model->last_B = B;
   model->last_K = K;

@@ -310,11 +310,13 @@ void vocab_pack_host(int bf16_mma, int V, int E, const float *src, int src_is_em
 // thr[m] = K-th best of sample[m][0 .. min(V, S)) minus a rounding margin, S = vocab_sample_size(V);
 // sample [M][S] holds the logits of the first S vocabulary entries (computed by launch_gemm)
 hipError_t launch_vocab_threshold(int M, int V, int K, const float *sample, float *thr, hipStream_t st);
-// part [M][n_chunks] (max, sum exp(l - max)); every logit >= thr[m] goes to cbuf
-// [M][n_chunks][lists][cap] with counts in ccnt [M][n_chunks][lists]; logits [M][V] or NULL
+// part [M][n_chunks] (reference m, sum exp(l - m)); every logit >= thr[m] goes to cbuf
+// [M][n_chunks][lists][cap] with counts in ccnt [M][n_chunks][lists] (a count above cap marks
+// an overflowed list); logits [M][V] or NULL.  fixed_ref: the caller has proven every logit
+// lies in [-40, 40], so the reference is 0 and no running maximum is kept.
 hipError_t launch_vocab(int bf16_mma, const void *t, const void *wp, const float *bias_pad, int M, int V,
                         int E, int n_chunks, const float *thr, float2 *part, int2 *cbuf, int *ccnt, int cap,
-                        float *logits, hipStream_t st);
+                        float *logits, int fixed_ref, hipStream_t st);
 // exact recomputation of the rows with ovf[m] != 0: row_out[m] = the K best keys
 // prev_score + (logit - lse) over the whole vocabulary
 hipError_t launch_vocab_fallback(int bf16_mma, const void *t, const void *wp, const float *bias_pad, int M,
@@ -323,13 +325,15 @@ hipError_t launch_vocab_fallback(int bf16_mma, const void *t, const void *wp, co
 constexpr int kVocabCap = 32;  // candidate buffer entries per (row, chunk, list)
 constexpr int kVocabPad = 64;  // vocabulary rows are padded to a multiple of this
 
-hipError_t launch_gru_cell(int M, int H, const float *a, int lda, const float *u, int ldu,
-                           const float *hsrc, const int32_t *hidx, int hrows, int32_t *err,
-                           const float *ga, const float *ba, const float *gu, const float *bu,
+// GRU cell for M rows; a row m = aidx[m] (if given), previous state row hidx[m] (if given);
+// out-of-range indices are clamped and flagged in err (bit 0: aidx, bit 1: hidx)
+hipError_t launch_gru_cell(int M, int H, const float *a, int lda, const int32_t *aidx, int arows,
+                           const float *u, int ldu, const float *hsrc, const int32_t *hidx, int hrows,
+                           int32_t *err, const float *ga, const float *ba, const float *gu, const float *bu,
                            float eps, float *out, int ldo, float *tap, hipStream_t st);
 
-hipError_t launch_readout(int M, int E, const float *p1, int ld1, const float *p2, int ld2,
-                          const float *p3, int ld3, const float *bt, const float *g,
+hipError_t launch_readout(int M, int E, const float *p1, int ld1, const float *p2, int ld2, const int32_t *idx2,
+                          int rows2, const float *p3, int ld3, const float *bt, const float *g,
                           const float *be, float eps, void *t_out, int t_bf16, float *tap,
                           hipStream_t st);
 

@@ -3,9 +3,13 @@
 // mean of the encoder context (start state), and the log-sum-exp merge of the
 // vocabulary partials (optionally turning stored logits into log-probabilities).
 //
-// One 256-thread workgroup per row; each thread keeps its NPT elements per block in
-// registers.  Layer-norm statistics are two-pass (mean, then mean squared deviation)
-// over register-resident values: wave shuffles, then 4 partials through LDS.
+// GRU cell and readout: one 256-thread workgroup per row; thread t holds 16-byte granules
+// 4t + 1024p of each H-block in registers, and every operand (products, previous state,
+// layer-norm gains and shifts) is loaded up front so the row costs one memory round trip.
+// Layer-norm statistics are taken in one pass over shifted values d = x - x_0 (x_0 = the
+// block's first element): mean = x_0 + sum(d)/n and var = sum(d^2)/n - (sum(d)/n)^2, which
+// keeps the cancellation of the one-pass formula small; all blocks' sums are reduced
+// together (wave shuffles, then 4 partials through LDS).
 #include "mt_internal.h"
 
 namespace mt {
@@ -28,12 +32,29 @@ __device__ __forceinline__ void block_sum(float (&v)[NV], float (*red)[NV]) {
   __syncthreads();
 }
 
+__device__ __forceinline__ float4 ld4(const float *p) { return *(const float4 *)p; }
+__device__ __forceinline__ void st4(float *p, float a, float b, float c, float d) {
+  *(float4 *)p = make_float4(a, b, c, d);
+}
+
+__device__ __forceinline__ int clamp_row(const int32_t *idx, int m, int rows, int32_t *err, int bit) {
+  int r = idx[m];
+  if (r < 0 || r >= rows) {
+    if (threadIdx.x == 0 && err) atomicOr(err, 1 << bit);
+    r = r < 0 ? 0 : rows - 1;
+  }
+  return r;
+}
+
 // GRU cell (reset applied to the recurrent product, z gates the previous state):
 //   r = sig(a_r + u_r), z = sig(a_z + u_z), hh = tanh(a_h + r u_h), out = (1-z) hh + z h
 // a and u hold the three H-blocks (r, z, h) of the input and recurrent products; with
-// layer norm each of the six blocks is normalised on its own before the gates.
-template <int NPT, bool LN>
+// layer norm each of the six blocks is normalised on its own before the gates.  Row m
+// reads a from row aidx[m] (if given; error bit 0 on a clamp) and the previous state from
+// row hidx[m] (if given; error bit 1).  G = 16-byte granules per thread per block.
+template <int G, bool LN>
 __global__ __launch_bounds__(kT) void gru_cell_kernel(int M, int H, const float *__restrict__ a, int lda,
+                                                      const int32_t *__restrict__ aidx, int arows,
                                                       const float *__restrict__ u, int ldu,
                                                       const float *__restrict__ hsrc,
                                                       const int32_t *__restrict__ hidx, int hrows,
@@ -43,124 +64,157 @@ __global__ __launch_bounds__(kT) void gru_cell_kernel(int M, int H, const float 
                                                       const float *__restrict__ bu, float eps,
                                                       float *__restrict__ out, int ldo,
                                                       float *__restrict__ tap) {
-  __shared__ float red[4][6];
+  __shared__ float red[4][12];
   const int m = blockIdx.x;
   const int t = threadIdx.x;
-  int hr = m;
-  if (hidx) {
-    hr = hidx[m];
-    if (hr < 0 || hr >= hrows) {
-      if (t == 0 && err) atomicOr(err, 2);
-      hr = hr < 0 ? 0 : hrows - 1;
-    }
-  }
-  const float *ar = a + (size_t)m * lda;
-  const float *ur = u + (size_t)m * ldu;
+  const int ar = aidx ? clamp_row(aidx, m, arows, err, 0) : m;
+  const int hr = hidx ? clamp_row(hidx, m, hrows, err, 1) : m;
+  const float *arow = a + (size_t)ar * lda;
+  const float *urow = u + (size_t)m * ldu;
   const float *hp = hsrc + (size_t)hr * H;
-  float x[6][NPT], h[NPT];
+  float x[6][G][4], h[G][4];
+  float lg[6][G][4], lb[6][G][4];
 #pragma unroll
-  for (int p = 0; p < NPT; ++p) {
-    const int j = t + kT * p;
-    const bool ok = j < H;
+  for (int p = 0; p < G; ++p) {
+    const int j = 4 * t + 4 * kT * p;
+    const int jc = j < H ? j : 0;  // lanes past H read element 0 and take no part
 #pragma unroll
     for (int g = 0; g < 3; ++g) {
-      x[g][p] = ok ? ar[g * H + j] : 0.f;
-      x[3 + g][p] = ok ? ur[g * H + j] : 0.f;
+      const float4 va = ld4(arow + g * H + jc), vu = ld4(urow + g * H + jc);
+      x[g][p][0] = va.x; x[g][p][1] = va.y; x[g][p][2] = va.z; x[g][p][3] = va.w;
+      x[3 + g][p][0] = vu.x; x[3 + g][p][1] = vu.y; x[3 + g][p][2] = vu.z; x[3 + g][p][3] = vu.w;
+      if (LN) {
+        const float4 g0 = ld4(ga + g * H + jc), b0 = ld4(ba + g * H + jc);
+        const float4 g1 = ld4(gu + g * H + jc), b1 = ld4(bu + g * H + jc);
+        lg[g][p][0] = g0.x; lg[g][p][1] = g0.y; lg[g][p][2] = g0.z; lg[g][p][3] = g0.w;
+        lb[g][p][0] = b0.x; lb[g][p][1] = b0.y; lb[g][p][2] = b0.z; lb[g][p][3] = b0.w;
+        lg[3 + g][p][0] = g1.x; lg[3 + g][p][1] = g1.y; lg[3 + g][p][2] = g1.z; lg[3 + g][p][3] = g1.w;
+        lb[3 + g][p][0] = b1.x; lb[3 + g][p][1] = b1.y; lb[3 + g][p][2] = b1.z; lb[3 + g][p][3] = b1.w;
+      }
     }
-    h[p] = ok ? hp[j] : 0.f;
+    const float4 vh = ld4(hp + jc);
+    h[p][0] = vh.x; h[p][1] = vh.y; h[p][2] = vh.z; h[p][3] = vh.w;
   }
   if (LN) {
-    float s[6];
+    float sh[6];
 #pragma unroll
-    for (int g = 0; g < 6; ++g) {
-      s[g] = 0.f;
-#pragma unroll
-      for (int p = 0; p < NPT; ++p) s[g] += x[g][p];
+    for (int g = 0; g < 3; ++g) {
+      sh[g] = arow[g * H];
+      sh[3 + g] = urow[g * H];
     }
-    block_sum<6>(s, red);
-    float mean[6], d[6];
+    float st[12];
 #pragma unroll
     for (int g = 0; g < 6; ++g) {
-      mean[g] = s[g] / (float)H;
-      d[g] = 0.f;
+      float s1 = 0.f, s2 = 0.f;
 #pragma unroll
-      for (int p = 0; p < NPT; ++p) {
-        const int j = t + kT * p;
-        const float e = j < H ? x[g][p] - mean[g] : 0.f;
-        d[g] += e * e;
+      for (int p = 0; p < G; ++p) {
+        if (4 * t + 4 * kT * p >= H) continue;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float d = x[g][p][e] - sh[g];
+          s1 += d;
+          s2 += d * d;
+        }
       }
+      st[2 * g] = s1;
+      st[2 * g + 1] = s2;
     }
-    block_sum<6>(d, red);
+    block_sum<12>(st, red);
+    const float invn = 1.0f / (float)H;
 #pragma unroll
     for (int g = 0; g < 6; ++g) {
-      const float inv = 1.0f / sqrtf(d[g] / (float)H + eps);
-      const float *gg = g < 3 ? ga + g * H : gu + (g - 3) * H;
-      const float *bb = g < 3 ? ba + g * H : bu + (g - 3) * H;
+      const float md = st[2 * g] * invn;
+      const float var = fmaxf(st[2 * g + 1] * invn - md * md, 0.f);
+      const float mean = sh[g] + md;
+      const float inv = 1.0f / sqrtf(var + eps);
 #pragma unroll
-      for (int p = 0; p < NPT; ++p) {
-        const int j = t + kT * p;
-        if (j < H) x[g][p] = gg[j] * (x[g][p] - mean[g]) * inv + bb[j];
-      }
+      for (int p = 0; p < G; ++p)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[g][p][e] = lg[g][p][e] * (x[g][p][e] - mean) * inv + lb[g][p][e];
     }
   }
   float *o = out + (size_t)m * ldo;
 #pragma unroll
-  for (int p = 0; p < NPT; ++p) {
-    const int j = t + kT * p;
+  for (int p = 0; p < G; ++p) {
+    const int j = 4 * t + 4 * kT * p;
     if (j >= H) continue;
-    const float r = sigmoid_fast(x[0][p] + x[3][p]);
-    const float z = sigmoid_fast(x[1][p] + x[4][p]);
-    const float hh = tanh_fast(x[2][p] + r * x[5][p]);
-    const float v = (1.0f - z) * hh + z * h[p];
-    o[j] = v;
-    if (tap) tap[(size_t)m * H + j] = v;
+    float v[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float r = sigmoid_fast(x[0][p][e] + x[3][p][e]);
+      const float z = sigmoid_fast(x[1][p][e] + x[4][p][e]);
+      const float hh = tanh_fast(x[2][p][e] + r * x[5][p][e]);
+      v[e] = (1.0f - z) * hh + z * h[p][e];
+    }
+    st4(o + j, v[0], v[1], v[2], v[3]);
+    if (tap) st4(tap + (size_t)m * H + j, v[0], v[1], v[2], v[3]);
   }
 }
 
-// t = tanh(LN?(p1 + p2 + p3 + bt)), written in the vocabulary GEMM's operand type
-template <int NPT, bool LN, typename TO>
+// t = tanh(LN?(p1 + p2 + p3 + bt)), written in the vocabulary GEMM's operand type; row m
+// reads p2 from row idx2[m] (if given, clamped)
+template <int G, bool LN, typename TO>
 __global__ __launch_bounds__(kT) void readout_kernel(int M, int E, const float *__restrict__ p1, int ld1,
                                                      const float *__restrict__ p2, int ld2,
+                                                     const int32_t *__restrict__ idx2, int rows2,
                                                      const float *__restrict__ p3, int ld3,
                                                      const float *__restrict__ bt,
                                                      const float *__restrict__ g,
                                                      const float *__restrict__ be, float eps,
                                                      TO *__restrict__ tout, float *__restrict__ tap) {
-  __shared__ float red[4][1];
+  __shared__ float red[4][2];
   const int m = blockIdx.x, t = threadIdx.x;
-  float x[NPT];
-  float s[1] = {0.f};
+  const int r2 = idx2 ? clamp_row(idx2, m, rows2, nullptr, 0) : m;
+  const float *q1 = p1 + (size_t)m * ld1, *q2 = p2 + (size_t)r2 * ld2, *q3 = p3 + (size_t)m * ld3;
+  float x[G][4], lg[G][4], lb[G][4];
 #pragma unroll
-  for (int p = 0; p < NPT; ++p) {
-    const int j = t + kT * p;
-    x[p] = j < E ? p1[(size_t)m * ld1 + j] + p2[(size_t)m * ld2 + j] + p3[(size_t)m * ld3 + j] + bt[j] : 0.f;
-    s[0] += x[p];
+  for (int p = 0; p < G; ++p) {
+    const int j = 4 * t + 4 * kT * p;
+    const int jc = j < E ? j : 0;
+    const float4 a = ld4(q1 + jc), b = ld4(q2 + jc), c = ld4(q3 + jc), d = ld4(bt + jc);
+    x[p][0] = a.x + b.x + c.x + d.x;
+    x[p][1] = a.y + b.y + c.y + d.y;
+    x[p][2] = a.z + b.z + c.z + d.z;
+    x[p][3] = a.w + b.w + c.w + d.w;
+    if (LN) {
+      const float4 g0 = ld4(g + jc), b0 = ld4(be + jc);
+      lg[p][0] = g0.x; lg[p][1] = g0.y; lg[p][2] = g0.z; lg[p][3] = g0.w;
+      lb[p][0] = b0.x; lb[p][1] = b0.y; lb[p][2] = b0.z; lb[p][3] = b0.w;
+    }
   }
   if (LN) {
-    block_sum<1>(s, red);
-    const float mean = s[0] / (float)E;
-    float d[1] = {0.f};
+    const float sh = q1[0] + q2[0] + q3[0] + bt[0];
+    float st[2] = {0.f, 0.f};
 #pragma unroll
-    for (int p = 0; p < NPT; ++p) {
-      const int j = t + kT * p;
-      const float e = j < E ? x[p] - mean : 0.f;
-      d[0] += e * e;
-    }
-    block_sum<1>(d, red);
-    const float inv = 1.0f / sqrtf(d[0] / (float)E + eps);
+    for (int p = 0; p < G; ++p) {
+      if (4 * t + 4 * kT * p >= E) continue;
 #pragma unroll
-    for (int p = 0; p < NPT; ++p) {
-      const int j = t + kT * p;
-      if (j < E) x[p] = g[j] * (x[p] - mean) * inv + be[j];
+      for (int e = 0; e < 4; ++e) {
+        const float d = x[p][e] - sh;
+        st[0] += d;
+        st[1] += d * d;
+      }
     }
+    block_sum<2>(st, red);
+    const float md = st[0] / (float)E;
+    const float var = fmaxf(st[1] / (float)E - md * md, 0.f);
+    const float mean = sh + md;
+    const float inv = 1.0f / sqrtf(var + eps);
+#pragma unroll
+    for (int p = 0; p < G; ++p)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) x[p][e] = lg[p][e] * (x[p][e] - mean) * inv + lb[p][e];
   }
 #pragma unroll
-  for (int p = 0; p < NPT; ++p) {
-    const int j = t + kT * p;
+  for (int p = 0; p < G; ++p) {
+    const int j = 4 * t + 4 * kT * p;
     if (j >= E) continue;
-    const float v = tanh_fast(x[p]);
-    Store<TO>::put(tout + (size_t)m * E + j, v);
-    if (tap) tap[(size_t)m * E + j] = v;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float v = tanh_fast(x[p][e]);
+      Store<TO>::put(tout + (size_t)m * E + j + e, v);
+      if (tap) tap[(size_t)m * E + j + e] = v;
+    }
   }
 }
 
@@ -213,66 +267,64 @@ __global__ __launch_bounds__(kT) void lse_kernel(int M, int ntiles, const float2
 
 // ---------------------------------------------------------------------------------------
 
-static int npt_for(int n) {
-  const int q = (n + kT - 1) / kT;
-  return q <= 1 ? 1 : q <= 2 ? 2 : q <= 4 ? 4 : q <= 8 ? 8 : 16;
+static int gran_for(int n) {  // 16-byte granules per thread for an n-wide row
+  const int q = (n / 4 + kT - 1) / kT;
+  return q <= 1 ? 1 : q <= 2 ? 2 : 4;
 }
 
-hipError_t launch_gru_cell(int M, int H, const float *a, int lda, const float *u, int ldu,
-                           const float *hsrc, const int32_t *hidx, int hrows, int32_t *err,
-                           const float *ga, const float *ba, const float *gu, const float *bu,
+hipError_t launch_gru_cell(int M, int H, const float *a, int lda, const int32_t *aidx, int arows,
+                           const float *u, int ldu, const float *hsrc, const int32_t *hidx, int hrows,
+                           int32_t *err, const float *ga, const float *ba, const float *gu, const float *bu,
                            float eps, float *out, int ldo, float *tap, hipStream_t st) {
   if (M == 0) return hipSuccess;
   const bool ln = ga != nullptr;
-#define MT_GRU(N)                                                                                       \
-  if (ln)                                                                                               \
-    hipLaunchKernelGGL((gru_cell_kernel<N, true>), dim3(M), dim3(kT), 0, st, M, H, a, lda, u, ldu,      \
-                       hsrc, hidx, hrows, err, ga, ba, gu, bu, eps, out, ldo, tap);                     \
-  else                                                                                                  \
-    hipLaunchKernelGGL((gru_cell_kernel<N, false>), dim3(M), dim3(kT), 0, st, M, H, a, lda, u, ldu,     \
-                       hsrc, hidx, hrows, err, ga, ba, gu, bu, eps, out, ldo, tap);
-  switch (npt_for(H)) {
+#define MT_GRU(N)                                                                                        \
+  if (ln)                                                                                                \
+    hipLaunchKernelGGL((gru_cell_kernel<N, true>), dim3(M), dim3(kT), 0, st, M, H, a, lda, aidx, arows, \
+                       u, ldu, hsrc, hidx, hrows, err, ga, ba, gu, bu, eps, out, ldo, tap);              \
+  else                                                                                                   \
+    hipLaunchKernelGGL((gru_cell_kernel<N, false>), dim3(M), dim3(kT), 0, st, M, H, a, lda, aidx, arows,\
+                       u, ldu, hsrc, hidx, hrows, err, ga, ba, gu, bu, eps, out, ldo, tap);
+  switch (gran_for(H)) {
     case 1: MT_GRU(1) break;
     case 2: MT_GRU(2) break;
-    case 4: MT_GRU(4) break;
-    case 8: MT_GRU(8) break;
-    default: MT_GRU(16) break;
+    default: MT_GRU(4) break;
   }
 #undef MT_GRU
   return hipGetLastError();
 }
 
 template <typename TO>
-static void readout_go(int npt, bool ln, int M, int E, const float *p1, int ld1, const float *p2,
-                       int ld2, const float *p3, int ld3, const float *bt, const float *g,
-                       const float *be, float eps, TO *t, float *tap, hipStream_t st) {
+static void readout_go(int gr, bool ln, int M, int E, const float *p1, int ld1, const float *p2, int ld2,
+                       const int32_t *idx2, int rows2, const float *p3, int ld3, const float *bt,
+                       const float *g, const float *be, float eps, TO *t, float *tap, hipStream_t st) {
 #define MT_RO(N)                                                                                      \
   if (ln)                                                                                             \
     hipLaunchKernelGGL((readout_kernel<N, true, TO>), dim3(M), dim3(kT), 0, st, M, E, p1, ld1, p2,    \
-                       ld2, p3, ld3, bt, g, be, eps, t, tap);                                         \
+                       ld2, idx2, rows2, p3, ld3, bt, g, be, eps, t, tap);                            \
   else                                                                                                \
     hipLaunchKernelGGL((readout_kernel<N, false, TO>), dim3(M), dim3(kT), 0, st, M, E, p1, ld1, p2,   \
-                       ld2, p3, ld3, bt, g, be, eps, t, tap);
-  switch (npt) {
+                       ld2, idx2, rows2, p3, ld3, bt, g, be, eps, t, tap);
+  switch (gr) {
     case 1: MT_RO(1) break;
     case 2: MT_RO(2) break;
-    case 4: MT_RO(4) break;
-    case 8: MT_RO(8) break;
-    default: MT_RO(16) break;
+    default: MT_RO(4) break;
   }
 #undef MT_RO
 }
 
-hipError_t launch_readout(int M, int E, const float *p1, int ld1, const float *p2, int ld2,
-                          const float *p3, int ld3, const float *bt, const float *g,
+hipError_t launch_readout(int M, int E, const float *p1, int ld1, const float *p2, int ld2, const int32_t *idx2,
+                          int rows2, const float *p3, int ld3, const float *bt, const float *g,
                           const float *be, float eps, void *t_out, int t_bf16, float *tap,
                           hipStream_t st) {
   if (M == 0) return hipSuccess;
   const bool ln = g != nullptr;
   if (t_bf16)
-    readout_go<bf16>(npt_for(E), ln, M, E, p1, ld1, p2, ld2, p3, ld3, bt, g, be, eps, (bf16 *)t_out, tap, st);
+    readout_go<bf16>(gran_for(E), ln, M, E, p1, ld1, p2, ld2, idx2, rows2, p3, ld3, bt, g, be, eps, (bf16 *)t_out,
+                     tap, st);
   else
-    readout_go<float>(npt_for(E), ln, M, E, p1, ld1, p2, ld2, p3, ld3, bt, g, be, eps, (float *)t_out, tap, st);
+    readout_go<float>(gran_for(E), ln, M, E, p1, ld1, p2, ld2, idx2, rows2, p3, ld3, bt, g, be, eps, (float *)t_out,
+                      tap, st);
   return hipGetLastError();
 }
 

@@ -39,9 +39,13 @@ constexpr int kLists = 8;        // candidate buffers per (hypothesis, chunk): 2
 constexpr int kSampleMax = 512;  // vocabulary entries of the threshold pass
 constexpr float kLog2e = 1.4426950408889634f;
 
-template <int HB>
+// Hypothesis columns per wave: fp32 64 (two 32-column MFMA blocks); bf16 all HB columns, so
+// each 16-byte weight fragment a lane loads feeds 2 x HB/32 MFMAs.  At bf16 rates a fragment
+// feeding only 2 x 2 MFMAs (and loaded again by a second wave for the other columns) keeps
+// the texture-address path busy enough to cap the matrix cores near half their rate.
+template <typename CT, int HB>
 struct VShape {
-  static constexpr int WH = HB >= 64 ? 64 : HB;  // hypothesis columns per wave
+  static constexpr int WH = sizeof(CT) == 2 ? HB : (HB >= 64 ? 64 : HB);  // columns per wave
   static constexpr int HBW = WH / 32;            // 32-column MFMA blocks per wave
   static constexpr int NW = 4 * (HB / WH);       // waves per workgroup
   static constexpr int NT = 64 * NW;             // threads per workgroup
@@ -72,13 +76,19 @@ struct VocabArgs {
   int cap;
   float *logits;        // [M][logits_ld] or NULL
   int logits_ld;
+  int fixed_ref;        // logits proven bounded: log-sum-exp without a running maximum
 };
 
-template <typename CT, int HB, int D>
-__global__ __launch_bounds__(VShape<HB>::NT) void vocab_kernel(VocabArgs a) {
+// FIX: the logits are bounded (|logit| <= 40, checked at load time), so the log-sum-exp is
+// accumulated as sum exp(logit) directly: no tile maximum, no rescaling, and every partial
+// carries the reference 0.
+// LOG: the logits are also written (parity mode); a separate instance so that the timed
+// path carries none of that path's registers.
+template <typename CT, int HB, int D, bool FIX, bool LOG>
+__global__ __launch_bounds__((VShape<CT, HB>::NT)) void vocab_kernel(VocabArgs a) {
   extern __shared__ __attribute__((aligned(16))) char lds[];
-  constexpr int HBB = VShape<HB>::HBW;
-  constexpr int kVT = VShape<HB>::NT;
+  constexpr int HBB = VShape<CT, HB>::HBW;
+  constexpr int kVT = VShape<CT, HB>::NT;
   constexpr int KV = VCfg<CT>::KV;
   constexpr int es = (int)sizeof(CT);
   const int rowb = a.E * es + 16;  // LDS row stride of the resident activations
@@ -91,7 +101,7 @@ __global__ __launch_bounds__(VShape<HB>::NT) void vocab_kernel(VocabArgs a) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: keeps the stream scalar
   const int run = wave & 3;                                    // vocabulary run of this wave
-  const int hc0 = (wave >> 2) * VShape<HB>::WH;               // first hypothesis column of this wave
+  const int hc0 = (wave >> 2) * VShape<CT, HB>::WH;               // first hypothesis column of this wave
 
   // ---- resident activations: rows h0..h0+HB-1 (zero beyond M) ----
   {
@@ -118,24 +128,24 @@ __global__ __launch_bounds__(VShape<HB>::NT) void vocab_kernel(VocabArgs a) {
   const bool collect = a.part != nullptr;
 
   float lm[HBB], ls[HBB], th[HBB];
-  int cnt[HBB];
-  uint32_t loff[HBB];  // byte offset of this lane's candidate list in cbuf, per hypothesis block
+  uint32_t loff[HBB];  // byte offset of this lane's next candidate slot in cbuf, per hypothesis block
+  uint32_t lend[HBB];  // offset of the list's last slot (writes past capacity stay there)
   char *const cbase = (char *)a.cbuf;
 #pragma unroll
   for (int j = 0; j < HBB; ++j) {
     const int h = h0 + hc0 + j * 32 + lrow;
-    lm[j] = -INFINITY;
+    lm[j] = FIX ? 0.f : -INFINITY;
     ls[j] = 0.f;
-    cnt[j] = 0;
     th[j] = (collect && h < a.M) ? a.thr[h] : INFINITY;
     loff[j] = (uint32_t)((((size_t)(h < a.M ? h : 0) * a.n_chunks + chunk) * kLists + src) * a.cap * sizeof(int2));
+    lend[j] = loff[j] + (uint32_t)(a.cap - 1) * 8u;
   }
 
   // With two hypothesis groups (two waves per SIMD, same vocabulary tiles), both waves of a
   // SIMD would reach their VALU-heavy tile epilogues at the same moments and leave the
   // matrix core idle meanwhile.  Starting the second group about half a tile late puts one
   // wave's epilogue under the other's MFMAs.
-  if (VShape<HB>::NW > 4 && (wave >> 2) == 1) __builtin_amdgcn_s_sleep(32);
+  if (VShape<CT, HB>::NW > 4 && (wave >> 2) == 1) __builtin_amdgcn_s_sleep(32);
 
   if (ntile > 0) {
     // Weight fragments of step g of tile ti are vocabulary blocks 2*(t_begin+ti) and +1 at
@@ -253,32 +263,49 @@ __global__ __launch_bounds__(VShape<HB>::NT) void vocab_kernel(VocabArgs a) {
       for (int j = 0; j < HBB; ++j) {
         const int h = h0 + hc0 + j * 32 + lrow;
         if (collect) {
-          float mt = -INFINITY;
-#pragma unroll
-          for (int i = 0; i < 2; ++i)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) mt = fmaxf(mt, acc[i][j][r]);
-          if (mt != -INFINITY) {  // -inf only when the whole tile is padding
-            const float mts = mt * kLog2e;
+          // candidate capture: store the (logit, token) pair at the lane's next slot and
+          // advance; the offset sticks at the list's last slot, and a list that reaches it is
+          // reported as overflowed (its row is recomputed exactly)
+          auto capture = [&](float x, int i, int r) {
+            *(int2 *)(cbase + loff[j]) = make_int2(__float_as_int(x), v0 + 32 * i + 8 * (r >> 2) + 4 * lhalf + (r & 3));
+            const uint32_t nx = loff[j] + 8u;
+            loff[j] = nx < lend[j] ? nx : lend[j];
+          };
+          if constexpr (FIX) {
             float se = 0.f;
 #pragma unroll
             for (int i = 0; i < 2; ++i)
 #pragma unroll
               for (int r = 0; r < 16; ++r) {
                 const float x = acc[i][j][r];
-                se += __builtin_amdgcn_exp2f(__builtin_fmaf(x, kLog2e, -mts));
-                if (x >= th[j]) {  // a slot past the list's capacity only counts (overflow)
-                  const uint32_t o = loff[j] + (uint32_t)(cnt[j] < a.cap - 1 ? cnt[j] : a.cap - 1) * 8u;
-                  *(int2 *)(cbase + o) = make_int2(__float_as_int(x), v0 + 32 * i + 8 * (r >> 2) + 4 * lhalf + (r & 3));
-                  ++cnt[j];
-                }
+                se += __builtin_amdgcn_exp2f(x * kLog2e);
+                if (x >= th[j]) capture(x, i, r);
               }
-            const float mn = fmaxf(lm[j], mt);
-            ls[j] = ls[j] * exp_fast(lm[j] - mn) + se * exp_fast(mt - mn);
-            lm[j] = mn;
+            ls[j] += se;
+          } else {
+            float mt = -INFINITY;
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+              for (int r = 0; r < 16; ++r) mt = fmaxf(mt, acc[i][j][r]);
+            if (mt != -INFINITY) {  // -inf only when the whole tile is padding
+              const float mts = mt * kLog2e;
+              float se = 0.f;
+#pragma unroll
+              for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                  const float x = acc[i][j][r];
+                  se += __builtin_amdgcn_exp2f(__builtin_fmaf(x, kLog2e, -mts));
+                  if (x >= th[j]) capture(x, i, r);
+                }
+              const float mn = fmaxf(lm[j], mt);
+              ls[j] = ls[j] * exp_fast(lm[j] - mn) + se * exp_fast(mt - mn);
+              lm[j] = mn;
+            }
           }
         }
-        if (a.logits && h < a.M) {
+        if (LOG && h < a.M) {
           float *lrowp = a.logits + (size_t)h * a.logits_ld;
 #pragma unroll
           for (int i = 0; i < 2; ++i)
@@ -297,7 +324,11 @@ __global__ __launch_bounds__(VShape<HB>::NT) void vocab_kernel(VocabArgs a) {
 #pragma unroll
   for (int j = 0; j < HBB; ++j) {
     const int h = h0 + hc0 + j * 32 + lrow;
-    if (h < a.M) a.ccnt[((size_t)h * a.n_chunks + chunk) * kLists + src] = cnt[j];
+    if (h < a.M) {
+      const uint32_t lstart = lend[j] - (uint32_t)(a.cap - 1) * 8u;
+      const int n = (int)((loff[j] - lstart) / 8u);
+      a.ccnt[((size_t)h * a.n_chunks + chunk) * kLists + src] = n >= a.cap - 1 ? a.cap + 1 : n;
+    }
   }
   __syncthreads();  // the resident activations are no longer read
   float2 *lp = (float2 *)lds;  // [HB][kLists]
@@ -444,7 +475,7 @@ static int ring_depth(int bf16_mma, int KS) {
   return KS % 4 == 0 ? 4 : KS % 2 == 0 ? 2 : 1;
 }
 
-template <typename CT, int HB, int D>
+template <typename CT, int HB, int D, bool FIX, bool LOG>
 static hipError_t vgo(const VocabArgs &a, hipStream_t st) {
   const int nhb = (a.M + HB - 1) / HB;
   const size_t tbytes = (size_t)HB * (a.E * sizeof(CT) + 16);
@@ -452,22 +483,30 @@ static hipError_t vgo(const VocabArgs &a, hipStream_t st) {
   const size_t lds = tbytes > lbytes ? tbytes : lbytes;
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void *)vocab_kernel<CT, HB, D>,
+    hipError_t e = hipFuncSetAttribute((const void *)vocab_kernel<CT, HB, D, FIX, LOG>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  hipLaunchKernelGGL((vocab_kernel<CT, HB, D>), dim3(nhb * a.n_chunks), dim3(VShape<HB>::NT), lds, st, a);
+  hipLaunchKernelGGL((vocab_kernel<CT, HB, D, FIX, LOG>), dim3(nhb * a.n_chunks), dim3(VShape<CT, HB>::NT), lds,
+                     st, a);
   return hipGetLastError();
+}
+
+template <typename CT, int HB, int D>
+static hipError_t vgo_f(const VocabArgs &a, hipStream_t st) {
+  if (a.logits) return a.fixed_ref ? vgo<CT, HB, D, true, true>(a, st) : vgo<CT, HB, D, false, true>(a, st);
+  return a.fixed_ref ? vgo<CT, HB, D, true, false>(a, st) : vgo<CT, HB, D, false, false>(a, st);
 }
 
 template <typename CT, int HB>
 static hipError_t vgo_d(const VocabArgs &a, hipStream_t st) {
   switch (ring_depth(sizeof(CT) == 2, a.KS)) {
-    case 8: return vgo<CT, HB, sizeof(CT) == 2 ? 8 : 4>(a, st);
-    case 4: return vgo<CT, HB, 4>(a, st);
-    case 2: return vgo<CT, HB, 2>(a, st);
-    default: return vgo<CT, HB, 1>(a, st);
+    // a wave covering 128 columns holds 128 accumulators: a 4-step ring keeps it in registers
+    case 8: return vgo_f<CT, HB, (sizeof(CT) == 2 && HB < 128) ? 8 : 4>(a, st);
+    case 4: return vgo_f<CT, HB, 4>(a, st);
+    case 2: return vgo_f<CT, HB, 2>(a, st);
+    default: return vgo_f<CT, HB, 1>(a, st);
   }
 }
 
@@ -516,7 +555,7 @@ hipLaunchKernelGGL((vocab_threshold_kernel<kSampleMax / 64>), dim3((M + 3) / 4),
 
 hipError_t launch_vocab(int bf16_mma, const void *t, const void *wp, const float *bias_pad, int M, int V,
                         int E, int n_chunks, const float *thr, float2 *part, int2 *cbuf, int *ccnt, int cap,
-                        float *logits, hipStream_t st) {
+                        float *logits, int fixed_ref, hipStream_t st) {
   if (M == 0) return hipSuccess;
   VocabArgs a = base_args(bf16_mma, t, wp, bias_pad, M, V, E);
   a.tiles_total = (V + kVRows - 1) / kVRows;
@@ -528,6 +567,7 @@ hipError_t launch_vocab(int bf16_mma, const void *t, const void *wp, const float
   a.cap = cap;
   a.logits = logits;
   a.logits_ld = V;
+  a.fixed_ref = fixed_ref;
   return vgo_any(bf16_mma, a, st);
 }
 

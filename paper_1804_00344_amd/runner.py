@@ -75,11 +75,22 @@ class Decoder:
 
     # ---- decode loop ------------------------------------------------------------------
     def start(self, tok0: np.ndarray, score0: np.ndarray):
-        """Beam start: every row reads its sentence's start state (src_row = m // K)."""
+        """Beam start: every row reads its sentence's start state (src_row = m // K).
+
+        The start beam is staged on the device once per (tok0, score0) pair; later starts
+        are device-to-device copies on the stream, so a new decode does not synchronise."""
         d = self.device
-        self.tok.copy_(torch.from_numpy(np.ascontiguousarray(tok0, np.int32)).to(d))
-        self.row.copy_(torch.arange(self.M, dtype=torch.int32, device=d) // self.K)
-        self.score.copy_(torch.from_numpy(np.ascontiguousarray(score0, np.float32)).to(d))
+        tok0 = np.ascontiguousarray(tok0, np.int32)
+        score0 = np.ascontiguousarray(score0, np.float32)
+        key = (self.M, tok0.tobytes(), score0.tobytes())
+        if getattr(self, "_start_key", None) != key:
+            self._start_tok = torch.from_numpy(tok0).to(d)
+            self._start_score = torch.from_numpy(score0).to(d)
+            self._start_row = torch.arange(self.M, dtype=torch.int32, device=d) // self.K
+            self._start_key = key
+        self.tok.copy_(self._start_tok)
+        self.row.copy_(self._start_row)
+        self.score.copy_(self._start_score)
         self.first = True
 
     def advance(self, *, logp=None, attn=None, stream=None):
