@@ -307,7 +307,8 @@ int vocab_lists();             // candidate buffers per (row, chunk)
 size_t vocab_pack_bytes(int bf16_mma, int V, int E);
 // packs Wo^T rows into MFMA fragment order; src is Wo [E][V] or, if src_is_emb, emb [V][E]
 void vocab_pack_host(int bf16_mma, int V, int E, const float *src, int src_is_emb, void *out);
-// thr[m] = K-th best of sample[m][0 .. min(V, S)) minus a rounding margin, S = vocab_sample_size(V);
+// thr[m] = a value reached by K of sample[m][0 .. min(V, S)) (the K-th largest of 64 lane maxima),
+// minus a rounding margin, S = vocab_sample_size(V);
 // sample [M][S] holds the logits of the first S vocabulary entries (computed by launch_gemm)
 hipError_t launch_vocab_threshold(int M, int V, int K, const float *sample, float *thr, hipStream_t st);
 // part [M][n_chunks] (reference m, sum exp(l - m)); every logit >= thr[m] goes to cbuf

@@ -26,8 +26,9 @@ constexpr int kSlots = kRowCap / 256;  // register slots per lane when a wave ta
 // (value bits, token), with fill counts cnt [M][nl] (NULL: every list holds cap entries).
 // lse != NULL: values are logits, turned into keys prev_score + (logit - lse); else values
 // are keys.  Tokens outside [0, V) are padding.  A row whose candidates do not fit (a list
-// count above cap, or more than kRowCap in total) is flagged in ovf[m] (if given) and left
-// for the exact recomputation; other rows get ovf[m] = 0 and their K best in row_out.
+// count above cap, or more than kRowCap in total), or, with fill counts, a row with fewer
+// than K candidates (its threshold was above its K-th best), is flagged in ovf[m] (if given)
+// and left for the exact recomputation; other rows get ovf[m] = 0 and their K best in row_out.
 template <int KMAX>
 __global__ __launch_bounds__(kTT) void row_select_kernel(int M, int K, int V, int nl, int cap,
                                                          const int *__restrict__ cnt,
@@ -74,7 +75,7 @@ __global__ __launch_bounds__(kTT) void row_select_kernel(int M, int K, int V, in
     off += v < w ? wtot[v] : 0;
     N += wtot[v];
   }
-  if (any_over || N > kRowCap) {
+  if (any_over || N > kRowCap || (cr && N < K)) {
     if (t == 0 && ovf) ovf[m] = 1;
     return;
   }

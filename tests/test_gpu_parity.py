@@ -141,6 +141,24 @@ def test_step_parity_mid_decode(name):
     same = np.mean((tk == tk2) & (bp == bp2))
     log(f"[{name}] fused vs materialised top-K agreement {same:.4f}")
     assert np.array_equal(sc, sc2)
+    # the production configuration: no log-probs, attention or taps written (the vocabulary
+    # pass then runs its candidates-only kernel)
+    run_step(dec, p, tok, src, T(state), p.M, logp=False, attn=False, taps=False)
+    sc4, tk4, bp4, rw4 = [x.cpu().numpy() for x in dec.topk(T(score), None, score_out=torch.empty_like(dec.score),
+                                                            tok_out=torch.empty_like(dec.tok),
+                                                            bp_out=torch.empty_like(dec.bp),
+                                                            row_out=torch.empty_like(dec.row))]
+    torch.cuda.synchronize()
+    assert mt.mt_device_errors(dec.model) == 0
+    dec_slots = 0
+    for b in sents:
+        rows = slice(b * p.K, (b + 1) * p.K)
+        d, _ = topk_gap_check(p.K, score[rows], orc[b]["logp"], sc4[rows], tk4[rows], bp4[rows], tol["logp"])
+        dec_slots += d
+        assert np.array_equal(rw4[rows], b * p.K + bp4[rows])
+    assert np.all(np.abs(sc4.astype(np.float64) - sc.astype(np.float64)) <= 2 * tol["logp"])
+    same = np.mean((tk4 == tk) & (bp4 == bp))
+    log(f"[{name}] candidates-only pass: decided slots {dec_slots}/{tot}, agreement with the logits pass {same:.4f}")
 
 
 @pytest.mark.parametrize("name", list(N_SAMPLE))
