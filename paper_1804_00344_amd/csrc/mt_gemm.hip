@@ -6,12 +6,16 @@
 //    of one row; lane group g = lane/16 owns k = 4g..4g+3 of each 16-k chunk and feeds
 //    them to 4 successive MFMAs (A and B use the same k assignment, so the sum is the
 //    plain dot product).
-//  * bf16 operands: v_mfma_f32_16x16x32_bf16, one 16-byte vector (8 k) per lane per MFMA.
-// Both paths read LDS identically: per 64-byte k-chunk, lane l reads 16 bytes at row
+//  * bf16 operands, wave tiles of 32 x 32 or more: v_mfma_f32_32x32x16_bf16, whose rate
+//    is twice that of the 16 x 16 x 32 form on this chip.  Per 32-byte k-step lane l reads
+//    16 bytes (8 k) at row (l % 32), byte offset 16 * (l / 32).
+//  * bf16 operands, 16 x 16 wave tiles: v_mfma_f32_16x16x32_bf16, one 16-byte vector (8 k)
+//    per lane per MFMA.
+// The 16 x 16 forms read LDS identically: per 64-byte k-chunk, lane l reads 16 bytes at row
 // (l % 16), byte offset 16 * (l / 16).
 //
-// Tiles: BM x BN (32, 64 or 128 square) per 256-thread workgroup, 2 x 2 waves, each wave
-// (BM/2) x (BN/2) as 16 x 16 MFMA blocks.  K advances 128 bytes (of the compute dtype) per
+// Tiles: BM x BN (32 x 32 up to 128 x 128) per 256-thread workgroup, 2 x 2 waves, each wave
+// (BM/2) x (BN/2) as 16 x 16 or 32 x 32 MFMA blocks.  K advances 128 bytes (of the compute dtype) per
 // tile through a double-buffered LDS ring fed from two register stages: the global loads of
 // tile k+2 are issued while tile k is multiplied, and tile k+1 is written to LDS behind it,
 // so every load has two tiles of MFMA work to arrive.  Loads are unconditional straight-line
@@ -39,6 +43,9 @@ struct Cfg {
   static constexpr int BK = kRowBytes / (int)sizeof(CT);
   static constexpr int WM = BM / 2, WN = BN / 2;
   static constexpr int FM = WM / 16, FN = WN / 16;
+  // bf16 with wave tiles that are whole 32 x 32 blocks: the 32 x 32 x 16 MFMA
+  static constexpr bool M32 = sizeof(CT) == 2 && WM % 32 == 0 && WN % 32 == 0;
+  static constexpr int FM32 = WM / 32, FN32 = WN / 32;
   static constexpr int A_PER_T = BM * 8 / kThreads;  // 16B vectors per thread per tile
   static constexpr int B_PER_T = BN * 8 / kThreads;
   static constexpr int STAGE = (BM + BN) * kLdsStride;
@@ -50,6 +57,7 @@ struct Problems {
 };
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
 
 template <typename T>
 __device__ __forceinline__ T bitcast16(const u32x4 &v) {
@@ -159,15 +167,44 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(Problems probs) {
     }
   };
 
-  f32x4 acc[C::FM][C::FN];
+  f32x4 acc[C::M32 ? 1 : C::FM][C::M32 ? 1 : C::FN];
+  f32x16 acc32[C::M32 ? C::FM32 : 1][C::M32 ? C::FN32 : 1];
+  if constexpr (C::M32) {
 #pragma unroll
-  for (int i = 0; i < C::FM; ++i)
+    for (int i = 0; i < C::FM32; ++i)
 #pragma unroll
-    for (int j = 0; j < C::FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int j = 0; j < C::FN32; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc32[i][j][r] = 0.f;
+  } else {
+#pragma unroll
+    for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+      for (int j = 0; j < C::FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
 
   auto compute = [&](int buf) {
     const char *As = lds + buf * C::STAGE;
     const char *Bs = As + BM * kLdsStride;
+    if constexpr (C::M32) {
+#pragma unroll
+      for (int s = 0; s < kRowBytes / 32; ++s) {
+        u32x4 af[C::FM32], bfv[C::FN32];
+#pragma unroll
+        for (int i = 0; i < C::FM32; ++i)
+          af[i] = *(const u32x4 *)(As + (wm * C::WM + i * 32 + (lane & 31)) * kLdsStride + s * 32 + (lane >> 5) * 16);
+#pragma unroll
+        for (int j = 0; j < C::FN32; ++j)
+          bfv[j] = *(const u32x4 *)(Bs + (wn * C::WN + j * 32 + (lane & 31)) * kLdsStride + s * 32 + (lane >> 5) * 16);
+#pragma unroll
+        for (int i = 0; i < C::FM32; ++i)
+#pragma unroll
+          for (int j = 0; j < C::FN32; ++j)
+            acc32[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bitcast16<bf16x8>(af[i]), bitcast16<bf16x8>(bfv[j]),
+                                                                  acc32[i][j], 0, 0, 0);
+      }
+      return;
+    }
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
       u32x4 af[C::FM], bfv[C::FN];
@@ -231,7 +268,28 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(Problems probs) {
   }
   if (kt < nk) step(kt, s0, s1, 0);
 
-  {
+  if constexpr (C::M32) {
+    // lane holds D[row = 8*(r/4) + 4*(lane/32) + r%4][col = lane % 32] of each 32x32 block
+#pragma unroll
+    for (int i = 0; i < C::FM32; ++i)
+#pragma unroll
+      for (int j = 0; j < C::FN32; ++j) {
+        const int col = n0 + wn * C::WN + j * 32 + (lane & 31);
+        if (col >= P.N) continue;
+        const float bias = P.bias ? P.bias[col] : 0.f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = m0 + wm * C::WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+          if (row >= P.M) continue;
+          float v = acc32[i][j][r] + bias;
+          if (EPI == EPI_TANH) v = tanh_fast(v);
+          if (P.out_bf16)
+            ((bf16 *)P.out)[(size_t)row * P.ldc + col] = to_bf16(v);
+          else
+            ((float *)P.out)[(size_t)row * P.ldc + col] = v;
+        }
+      }
+  } else {
     // lane holds D[row = 4*(lane/16) + r][col = lane % 16] of each 16x16 block
 #pragma unroll
     for (int i = 0; i < C::FM; ++i)
@@ -270,13 +328,16 @@ static hipError_t go(const Problems &ps, int nprob, hipStream_t st) {
 template <typename CT, typename AT, int EPI>
 static hipError_t go_tiles(const Problems &ps, int nprob, hipStream_t st) {
   // 128 x 128 tiles when they already fill the chip, 32 x 32 when 64 x 64 tiles would leave
-  // CUs idle, else 64 x 64
-  long t128 = 0, t64 = 0;
+  // CUs idle, else 64 x 64; bf16 takes 64 x 128 (32 x 64 per wave, 32 x 32 x 16 MFMAs) when
+  // that fills the chip
+  long t128 = 0, t64 = 0, t64x128 = 0;
   for (int i = 0; i < nprob; ++i) {
     t128 += (long)((ps.p[i].M + 127) / 128) * ((ps.p[i].N + 127) / 128);
     t64 += (long)((ps.p[i].M + 63) / 64) * ((ps.p[i].N + 63) / 64);
+    t64x128 += (long)((ps.p[i].M + 63) / 64) * ((ps.p[i].N + 127) / 128);
   }
   if (t128 >= 512) return go<CT, AT, EPI, 128, 128>(ps, nprob, st);
+  if (sizeof(CT) == 2 && t64x128 >= 256) return go<CT, AT, EPI, 64, 128>(ps, nprob, st);
   if (t64 < 256) return go<CT, AT, EPI, 32, 32>(ps, nprob, st);
   return go<CT, AT, EPI, 64, 64>(ps, nprob, st);
 }

@@ -39,13 +39,11 @@ constexpr int kLists = 8;        // candidate buffers per (hypothesis, chunk): 2
 constexpr int kSampleMax = 2048;  // vocabulary entries of the threshold pass
 constexpr float kLog2e = 1.4426950408889634f;
 
-// Hypothesis columns per wave: fp32 64 (two 32-column MFMA blocks); bf16 all HB columns, so
-// each 16-byte weight fragment a lane loads feeds 2 x HB/32 MFMAs.  At bf16 rates a fragment
-// feeding only 2 x 2 MFMAs (and loaded again by a second wave for the other columns) keeps
-// the texture-address path busy enough to cap the matrix cores near half their rate.
+// Hypothesis columns per wave: at most 64 (two 32-column MFMA blocks); a workgroup of HB
+// columns runs HB/64 waves per vocabulary run on the same tiles.
 template <typename CT, int HB>
 struct VShape {
-  static constexpr int WH = sizeof(CT) == 2 ? HB : (HB >= 64 ? 64 : HB);  // columns per wave
+  static constexpr int WH = HB >= 64 ? 64 : HB;  // columns per wave
   static constexpr int HBW = WH / 32;            // 32-column MFMA blocks per wave
   static constexpr int NW = 4 * (HB / WH);       // waves per workgroup
   static constexpr int NT = 64 * NW;             // threads per workgroup
@@ -350,259 +348,6 @@ __global__ __launch_bounds__((VShape<CT, HB>::NT)) void vocab_kernel(VocabArgs a
   }
 }
 
-// bf16 main pass for a compile-time depth (KS k-steps of 16, E = 16 KS) with bounded logits.
-//
-// Each wave owns a 64 x 128 tile (2 vocabulary blocks x all 4 hypothesis blocks of the
-// workgroup), so a 16-byte weight fragment feeds 4 MFMAs and an activation fragment 2.  The
-// k-loop of a tile is fully unrolled: every LDS offset and weight offset is a constant, and
-// the ring refill needs no index arithmetic.  Two accumulator sets alternate between tiles:
-// while the MFMAs of tile t run, the same instruction stream works through tile t-1's values
-// (NV per k-step): exp-sum for the log-sum-exp and a per-lane bit mask of the values above the
-// candidate threshold.  The bias enters as the C operand of the first k-step.  Candidates are
-// extracted after the tile from the mask: the lane's 16 values of a half block go to a small
-// LDS scratch and only the set bits are read back and stored.
-template <int KS, int D>
-__global__ __launch_bounds__(256) void vocab_bf16_kernel(VocabArgs a) {
-  extern __shared__ __attribute__((aligned(16))) char lds[];
-  constexpr int HB = 128;
-  constexpr int E = KS * 16;
-  constexpr int rowb = E * 2 + 16;  // LDS row stride of the resident activations
-  constexpr int NV = 128 / KS;      // epilogue values of the previous tile per k-step
-  constexpr int kXs = 80;           // scratch bytes per lane (16 floats, 16-byte aligned, conflict-free)
-  static_assert(128 % KS == 0 && KS % D == 0 && KS % 2 == 0, "tile shape");
-
-  const int nhb = (a.M + HB - 1) / HB;
-  const int L = xcd_remap(blockIdx.x, gridDim.x);
-  const int chunk = L / nhb, hb = L % nhb;
-  if (chunk >= a.n_chunks) return;
-  const int h0 = hb * HB;
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int run = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int lrow = lane & 31, lhalf = lane >> 5;
-  const int src = run * 2 + lhalf;
-
-  {
-    // 16 loads in flight per thread (rows clamped, zeroed on store), so the fill costs two
-    // memory round trips rather than one per vector
-    constexpr int vpr = E * 2 / 16;
-    constexpr int per = HB * vpr / 256;
-    constexpr int BATCH = per < 16 ? per : 16;
-    static_assert(per % BATCH == 0, "fill batches");
-    for (int b0 = 0; b0 < per; b0 += BATCH) {
-      v4u v[BATCH];
-#pragma unroll
-      for (int u = 0; u < BATCH; ++u) {
-        const int idx = tid + (b0 + u) * 256;
-        const int r = idx / vpr, c = idx % vpr;
-        const int hr = h0 + r < a.M ? h0 + r : a.M - 1;
-        v[u] = *(const v4u *)((const char *)a.t + ((size_t)hr * E) * 2 + c * 16);
-      }
-#pragma unroll
-      for (int u = 0; u < BATCH; ++u) {
-        const int idx = tid + (b0 + u) * 256;
-        const int r = idx / vpr, c = idx % vpr;
-        *(v4u *)(lds + r * rowb + c * 16) = h0 + r < a.M ? v[u] : v4u{0u, 0u, 0u, 0u};
-      }
-    }
-  }
-  __syncthreads();
-
-  const int slots = a.n_chunks * 4;
-  const int slot = chunk * 4 + run;
-  const int t_begin = (int)((long)a.tiles_total * slot / slots);
-  const int t_end = (int)((long)a.tiles_total * (slot + 1) / slots);
-  char *const xs = lds + HB * rowb + run * 64 * kXs + lane * kXs;
-
-  float th[4], ls[4];
-  uint32_t loff[4], lend[4];
-  char *const cbase = (char *)a.cbuf;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int h = h0 + j * 32 + lrow;
-    th[j] = h < a.M ? a.thr[h] : INFINITY;
-    ls[j] = 0.f;
-    loff[j] = (uint32_t)((((size_t)(h < a.M ? h : 0) * a.n_chunks + chunk) * kLists + src) * a.cap * sizeof(int2));
-    lend[j] = loff[j] + (uint32_t)(a.cap - 1) * 8u;
-  }
-
-  if (t_end > t_begin) {
-    // Buffer addressing: the resource and the per-lane byte offset are fixed, and each
-    // fragment's offset is a scalar (tile base + constant), so the unrolled loop carries no
-    // per-fetch vector addresses.  Reads past the buffer's end return zero.
-    const __amdgpu_buffer_rsrc_t wrs =
-        __builtin_amdgcn_make_buffer_rsrc((void *)a.wp, 0, a.tiles_total * kVRows * E * 2, 0x00020000);
-    const __amdgpu_buffer_rsrc_t brs =
-        __builtin_amdgcn_make_buffer_rsrc((void *)a.bias, 0, a.tiles_total * kVRows * 4, 0x00020000);
-    const int wvo = lane * 16, bvo = lhalf * 16;
-    const v4u *bl = (const v4u *)(lds + lrow * rowb + lhalf * 16);
-    v4u ring[D][2];
-    v4u bq[2][4];
-    f32x16 bias[2];
-    f32x16 accA[2][4], accB[2][4];
-    float se[4];
-    uint32_t msk[4];
-
-    auto fetch = [&](int T, int ks, v4u(&r)[2]) {
-      const int so = (2 * T * KS + ks) * 1024;
-      r[0] = __builtin_amdgcn_raw_buffer_load_b128(wrs, wvo, so, 0);
-      r[1] = __builtin_amdgcn_raw_buffer_load_b128(wrs, wvo, so + KS * 1024, 0);
-    };
-    auto load_bias = [&](int T) {
-      const int so = T * kVRows * 4;
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const v4u v = __builtin_amdgcn_raw_buffer_load_b128(brs, bvo, so + (32 * i + 8 * q) * 4, 0);
-          bias[i][4 * q + 0] = __uint_as_float(v.x); bias[i][4 * q + 1] = __uint_as_float(v.y);
-          bias[i][4 * q + 2] = __uint_as_float(v.z); bias[i][4 * q + 3] = __uint_as_float(v.w);
-        }
-    };
-    auto lds_frags = [&](int ks, v4u(&f)[4]) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) f[j] = bl[(j * 32 * rowb + ks * 32) / 16];
-    };
-    // one value of the previous tile: exp-sum and the threshold mask (bit set when x > th)
-    auto epi_value = [&](const f32x16(&prev)[2][4], int n) {
-      const int j = n >> 5, i = (n >> 4) & 1, r = n & 15;
-      // read the accumulator register here: otherwise the compiler copies the whole previous
-      // tile (128 registers) out of the accumulator file at the tile boundary
-      float x;
-      asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(x) : "a"(prev[i][j][r]));
-      se[j] += __builtin_amdgcn_exp2f(x * kLog2e);
-      msk[j] = __builtin_amdgcn_alignbit(msk[j], __float_as_uint(th[j] - x), 31);
-    };
-
-    // tile T into cur while finishing the values of prev
-    auto ktile = [&](int T, f32x16(&cur)[2][4], const f32x16(&prev)[2][4]) {
-      const int Tn = T + 1 < t_end ? T + 1 : T;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) { se[j] = 0.f; msk[j] = 0u; }
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        lds_frags(ks + 1 < KS ? ks + 1 : 0, bq[(ks + 1) & 1]);
-        bf16x8 a0, a1;
-        __builtin_memcpy(&a0, &ring[ks % D][0], 16);
-        __builtin_memcpy(&a1, &ring[ks % D][1], 16);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          bf16x8 b;
-          __builtin_memcpy(&b, &bq[ks & 1][j], 16);
-          cur[0][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b, ks == 0 ? bias[0] : cur[0][j], 0, 0, 0);
-          cur[1][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b, ks == 0 ? bias[1] : cur[1][j], 0, 0, 0);
-        }
-        if (ks + D < KS) fetch(T, ks + D, ring[ks % D]);
-        else fetch(Tn, ks + D - KS, ring[ks % D]);
-        if (ks == 0) load_bias(Tn);
-#pragma unroll
-        for (int u = 0; u < NV; ++u) epi_value(prev, ks * NV + u);
-        // The epilogue values are pure arithmetic: left alone, instruction selection places
-        // them next to their use after the tile, not under this k-step's MFMAs.  Passing the
-        // running sums through an empty volatile statement fixes them here.
-        {
-          const int j = (ks * NV) >> 5;
-          asm volatile("" : "+v"(se[j]), "+v"(msk[j]));
-        }
-        // keep each k-step's work together: hoisting the previous tile's accumulator reads
-        // (or sinking the refills) would cost registers or prefetch distance
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    };
-    auto epi_all = [&](const f32x16(&prev)[2][4]) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) { se[j] = 0.f; msk[j] = 0u; }
-#pragma unroll
-      for (int n = 0; n < 128; ++n) {
-        epi_value(prev, n);
-        if ((n & 7) == 7) __builtin_amdgcn_sched_barrier(0);  // bounded live range of the reads
-      }
-    };
-    // add the tile's exp-sums and store its candidates (mask bit 31 - (16 i + r) is value (i, r))
-    auto fin = [&](int T, const f32x16(&prev)[2][4]) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) ls[j] += se[j];
-      // 4 * lhalf recomputed here (a volatile lane-id read cannot be merged with the copy made
-      // before the loop): kept live across the tile loop, it is spilled, and the reload waits for
-      // every outstanding load, the ring prefetches included
-      int lid;
-      asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(lid));
-      const int tok0 = T * kVRows + ((lid >> 3) & 4);
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-          uint32_t mh = (msk[j] >> (16 - 16 * i)) & 0xffffu;
-          if (__any(mh != 0u)) {
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-              *(float4 *)(xs + 16 * q) =
-                  make_float4(prev[i][j][4 * q], prev[i][j][4 * q + 1], prev[i][j][4 * q + 2], prev[i][j][4 * q + 3]);
-            while (mh != 0u) {
-              const int bp = 31 - __builtin_clz(mh);
-              mh &= ~(1u << bp);
-              const int r = 15 - bp;
-              const float x = *(const float *)(xs + 4 * r);
-              *(int2 *)(cbase + loff[j]) = make_int2(__float_as_int(x), tok0 + 32 * i + 8 * (r >> 2) + (r & 3));
-              const uint32_t nx = loff[j] + 8u;
-              loff[j] = nx < lend[j] ? nx : lend[j];
-            }
-          }
-        }
-    };
-
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) accB[i][j][r] = -INFINITY;
-#pragma unroll
-    for (int d = 0; d < D; ++d) fetch(t_begin, d, ring[d]);
-    load_bias(t_begin);
-    lds_frags(0, bq[0]);
-
-    int T = t_begin;
-    for (;;) {
-      ktile(T, accA, accB);
-      if (T > t_begin) fin(T - 1, accB);
-      if (++T == t_end) {
-        epi_all(accA);
-        fin(T - 1, accA);
-        break;
-      }
-      ktile(T, accB, accA);
-      fin(T - 1, accA);
-      if (++T == t_end) {
-        epi_all(accB);
-        fin(T - 1, accB);
-        break;
-      }
-    }
-  }
-
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int h = h0 + j * 32 + lrow;
-    if (h < a.M) {
-      const uint32_t lstart = lend[j] - (uint32_t)(a.cap - 1) * 8u;
-      const int n = (int)((loff[j] - lstart) / 8u);
-      a.ccnt[((size_t)h * a.n_chunks + chunk) * kLists + src] = n >= a.cap - 1 ? a.cap + 1 : n;
-    }
-  }
-  __syncthreads();  // the resident activations are no longer read
-  float2 *lp = (float2 *)lds;  // [HB][kLists]
-#pragma unroll
-  for (int j = 0; j < 4; ++j) lp[(j * 32 + lrow) * kLists + src] = make_float2(0.f, ls[j]);
-  __syncthreads();
-  for (int hl = tid; hl < HB; hl += 256) {
-    const int h = h0 + hl;
-    if (h >= a.M) continue;
-    float sum = 0.f;
-    for (int s = 0; s < kLists; ++s) sum += lp[hl * kLists + s].y;
-    a.part[(size_t)h * a.n_chunks + chunk] = make_float2(0.f, sum);
-  }
-}
-
 // Threshold of each row: a value with at least K of the first S logits at or above it, lowered
 // by a margin that covers the rounding difference between this pass's logits and the main
 // pass's (the two sum the same products in different orders).  The row's K best are all at or
@@ -766,36 +511,15 @@ static hipError_t vgo_f(const VocabArgs &a, hipStream_t st) {
 template <typename CT, int HB>
 static hipError_t vgo_d(const VocabArgs &a, hipStream_t st) {
   switch (ring_depth(sizeof(CT) == 2, a.KS)) {
-    // a wave covering 128 columns holds 128 accumulators: a 4-step ring keeps it in registers
-    case 8: return vgo_f<CT, HB, (sizeof(CT) == 2 && HB < 128) ? 8 : 4>(a, st);
+    case 8: return vgo_f<CT, HB, 8>(a, st);
     case 4: return vgo_f<CT, HB, 4>(a, st);
     case 2: return vgo_f<CT, HB, 2>(a, st);
     default: return vgo_f<CT, HB, 1>(a, st);
   }
 }
 
-template <int KS, int D>
-static hipError_t vgo_b16(const VocabArgs &a, hipStream_t st) {
-  const int nhb = (a.M + 127) / 128;
-  const size_t lds = (size_t)128 * (KS * 32 + 16) + 4 * 64 * 80;
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void *)vocab_bf16_kernel<KS, D>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
-  hipLaunchKernelGGL((vocab_bf16_kernel<KS, D>), dim3(nhb * a.n_chunks), dim3(256), lds, st, a);
-  return hipGetLastError();
-}
-
 static hipError_t vgo_any(int bf16_mma, const VocabArgs &a, hipStream_t st) {
   const int HB = vocab_rows_per_block(bf16_mma, a.E);
-  // bounded logits, main pass, no logits written: the interleaved bf16 kernel
-#ifndef MT_B16_RING
-#define MT_B16_RING 4
-#endif
-  if (bf16_mma && HB == 128 && a.fixed_ref && a.part && !a.logits && a.E == 512) return vgo_b16<32, MT_B16_RING>(a, st);
   if (bf16_mma) {
     if (HB == 128) return vgo_d<bf16, 128>(a, st);
     if (HB == 64) return vgo_d<bf16, 64>(a, st);
