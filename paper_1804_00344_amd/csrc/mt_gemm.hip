@@ -9,6 +9,9 @@
 //  * bf16 operands, wave tiles of 32 x 32 or more: v_mfma_f32_32x32x16_bf16, whose rate
 //    is twice that of the 16 x 16 x 32 form on this chip.  Per 32-byte k-step lane l reads
 //    16 bytes (8 k) at row (l % 32), byte offset 16 * (l / 32).
+//  * fp32 operands, wave tiles of 32 x 64 or more: v_mfma_f32_32x32x2f32 with the same reads,
+//    each 16-byte vector feeding 4 successive MFMAs (lane half g supplies k = 4g + e to
+//    MFMA e).
 //  * bf16 operands, 16 x 16 wave tiles: v_mfma_f32_16x16x32_bf16, one 16-byte vector (8 k)
 //    per lane per MFMA.
 // The 16 x 16 forms read LDS identically: per 64-byte k-chunk, lane l reads 16 bytes at row
@@ -43,8 +46,9 @@ struct Cfg {
   static constexpr int BK = kRowBytes / (int)sizeof(CT);
   static constexpr int WM = BM / 2, WN = BN / 2;
   static constexpr int FM = WM / 16, FN = WN / 16;
-  // bf16 with wave tiles that are whole 32 x 32 blocks: the 32 x 32 x 16 MFMA
-  static constexpr bool M32 = sizeof(CT) == 2 && WM % 32 == 0 && WN % 32 == 0;
+  // wave tiles of whole 32 x 32 blocks: the 32 x 32 MFMA (bf16 32x32x16; fp32 32x32x2 when
+  // the wave has at least two blocks, so that successive MFMAs alternate accumulators)
+  static constexpr bool M32 = WM % 32 == 0 && (sizeof(CT) == 2 ? WN % 32 == 0 : WN % 64 == 0);
   static constexpr int FM32 = WM / 32, FN32 = WN / 32;
   static constexpr int A_PER_T = BM * 8 / kThreads;  // 16B vectors per thread per tile
   static constexpr int B_PER_T = BN * 8 / kThreads;
@@ -196,12 +200,29 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(Problems probs) {
 #pragma unroll
         for (int j = 0; j < C::FN32; ++j)
           bfv[j] = *(const u32x4 *)(Bs + (wn * C::WN + j * 32 + (lane & 31)) * kLdsStride + s * 32 + (lane >> 5) * 16);
+        if constexpr (sizeof(CT) == 2) {
 #pragma unroll
-        for (int i = 0; i < C::FM32; ++i)
+          for (int i = 0; i < C::FM32; ++i)
 #pragma unroll
-          for (int j = 0; j < C::FN32; ++j)
-            acc32[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bitcast16<bf16x8>(af[i]), bitcast16<bf16x8>(bfv[j]),
-                                                                  acc32[i][j], 0, 0, 0);
+            for (int j = 0; j < C::FN32; ++j)
+              acc32[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bitcast16<bf16x8>(af[i]),
+                                                                    bitcast16<bf16x8>(bfv[j]), acc32[i][j], 0, 0, 0);
+        } else {
+          // fp32: the 32-byte step is 8 k; element e of a lane's vector feeds MFMA e, lane half
+          // g supplying k = 4g + e (the same assignment on both operands)
+          float fa[C::FM32][4], fb[C::FN32][4];
+#pragma unroll
+          for (int i = 0; i < C::FM32; ++i) __builtin_memcpy(fa[i], &af[i], 16);
+#pragma unroll
+          for (int j = 0; j < C::FN32; ++j) __builtin_memcpy(fb[j], &bfv[j], 16);
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+#pragma unroll
+            for (int i = 0; i < C::FM32; ++i)
+#pragma unroll
+              for (int j = 0; j < C::FN32; ++j)
+                acc32[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[i][e], fb[j][e], acc32[i][j], 0, 0, 0);
+        }
       }
       return;
     }
@@ -329,7 +350,8 @@ template <typename CT, typename AT, int EPI>
 static hipError_t go_tiles(const Problems &ps, int nprob, hipStream_t st) {
   // 128 x 128 tiles when they already fill the chip, 32 x 32 when 64 x 64 tiles would leave
   // CUs idle, else 64 x 64; bf16 takes 64 x 128 (32 x 64 per wave, 32 x 32 x 16 MFMAs) when
-  // that fills the chip
+  // that fills the chip.  (fp32 stays on 64 x 64: at these shapes the time follows the
+  // number of tiles per CU, and 64 x 128 tiles divide worse over 256 CUs.)
   long t128 = 0, t64 = 0, t64x128 = 0;
   for (int i = 0; i < nprob; ++i) {
     t128 += (long)((ps.p[i].M + 127) / 128) * ((ps.p[i].N + 127) / 128);

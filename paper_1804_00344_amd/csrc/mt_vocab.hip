@@ -82,7 +82,10 @@ struct VocabArgs {
 // carries the reference 0.
 // LOG: the logits are also written (parity mode); a separate instance so that the timed
 // path carries none of that path's registers.
-template <typename CT, int HB, int D, bool FIX, bool LOG>
+// KSC > 0: the depth is the compile-time KSC k-steps (E = KSC * KV); each tile's k-loop is
+// then unrolled and the weights are read with buffer loads at a scalar offset (tile base +
+// constant), so a refill costs one scalar add instead of the flat-stream index update.
+template <typename CT, int HB, int D, bool FIX, bool LOG, int KSC>
 __global__ __launch_bounds__((VShape<CT, HB>::NT)) void vocab_kernel(VocabArgs a) {
   extern __shared__ __attribute__((aligned(16))) char lds[];
   constexpr int HBB = VShape<CT, HB>::HBW;
@@ -165,8 +168,22 @@ __global__ __launch_bounds__((VShape<CT, HB>::NT)) void vocab_kernel(VocabArgs a
       poff += more + wrap * KS;
     };
     v4u ring[D][2];
+    // buffer view of the packed weights (KSC > 0): fixed per-lane offset, scalar fragment
+    // offsets; reads past the end return zero
+    const __amdgpu_buffer_rsrc_t wrs =
+        __builtin_amdgcn_make_buffer_rsrc((void *)a.wp, 0, a.tiles_total * kVRows * a.E * es, 0x00020000);
+    const int wvo = lane * 16;
+    if constexpr (KSC > 0) {
 #pragma unroll
-    for (int d = 0; d < D; ++d) fetch(ring[d]);
+      for (int d = 0; d < D; ++d) {
+        const int so = (2 * t_begin * KSC + d) * 1024;
+        ring[d][0] = __builtin_amdgcn_raw_buffer_load_b128(wrs, wvo, so, 0);
+        ring[d][1] = __builtin_amdgcn_raw_buffer_load_b128(wrs, wvo, so + KSC * 1024, 0);
+      }
+    } else {
+#pragma unroll
+      for (int d = 0; d < D; ++d) fetch(ring[d]);
+    }
     const v4u *bl = (const v4u *)lds + (size_t)(hc0 + lrow) * (rowb / 16) + lhalf * (KV / 2 * es / 16);
 
     // activation fragments of k-step ks (identical for every tile, so the sequence repeats
@@ -195,51 +212,66 @@ __global__ __launch_bounds__((VShape<CT, HB>::NT)) void vocab_kernel(VocabArgs a
 #pragma unroll
           for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-      for (int ks0 = 0; ks0 < KS; ks0 += D) {
+      // one k-step: MFMAs on ring slot `slot`, then its refill (refill(slot) issues the loads)
+      auto kstep = [&](int ks, v4u(&slot)[2], auto refill) {
+        if constexpr (kPrefetchLds) {
+          lds_frag(ks + 1 < KS ? ks + 1 : 0, bnxt);
+          __builtin_amdgcn_sched_barrier(0);  // issue the reads before this step's MFMAs
+        } else {
+          lds_frag(ks, bcur);
+        }
+        const v4u c0 = slot[0], c1 = slot[1];
+        if constexpr (es == 2) {
+          bf16x8 a0, a1;
+          __builtin_memcpy(&a0, &c0, 16);
+          __builtin_memcpy(&a1, &c1, 16);
 #pragma unroll
-        for (int d = 0; d < D; ++d) {
-          const int ks = ks0 + d;
-          if constexpr (kPrefetchLds) {
-            lds_frag(ks + 1 < KS ? ks + 1 : 0, bnxt);
-            __builtin_amdgcn_sched_barrier(0);  // issue the reads before this step's MFMAs
-          } else {
-            lds_frag(ks, bcur);
+          for (int j = 0; j < HBB; ++j) {
+            bf16x8 b;
+            __builtin_memcpy(&b, &bcur[j], 16);
+            acc[0][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b, acc[0][j], 0, 0, 0);
+            acc[1][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b, acc[1][j], 0, 0, 0);
           }
-          const v4u c0 = ring[d][0], c1 = ring[d][1];
-          if constexpr (es == 2) {
-            bf16x8 a0, a1;
-            __builtin_memcpy(&a0, &c0, 16);
-            __builtin_memcpy(&a1, &c1, 16);
+        } else {
+          float fa0[4], fa1[4], fb[HBB][4];
+          __builtin_memcpy(fa0, &c0, 16);
+          __builtin_memcpy(fa1, &c1, 16);
+#pragma unroll
+          for (int j = 0; j < HBB; ++j) __builtin_memcpy(fb[j], &bcur[j], 16);
+#pragma unroll
+          for (int s = 0; s < 4; ++s)
 #pragma unroll
             for (int j = 0; j < HBB; ++j) {
-              bf16x8 b;
-              __builtin_memcpy(&b, &bcur[j], 16);
-              acc[0][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b, acc[0][j], 0, 0, 0);
-              acc[1][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b, acc[1][j], 0, 0, 0);
+              acc[0][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa0[s], fb[j][s], acc[0][j], 0, 0, 0);
+              acc[1][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa1[s], fb[j][s], acc[1][j], 0, 0, 0);
             }
-          } else {
-            float fa0[4], fa1[4], fb[HBB][4];
-            __builtin_memcpy(fa0, &c0, 16);
-            __builtin_memcpy(fa1, &c1, 16);
+        }
+        refill(slot);
+        if constexpr (kPrefetchLds) {
 #pragma unroll
-            for (int j = 0; j < HBB; ++j) __builtin_memcpy(fb[j], &bcur[j], 16);
+          for (int j = 0; j < HBB; ++j) bcur[j] = bnxt[j];
+        }
+        // keep each refill right behind the MFMAs that consumed its slot (left alone, the
+        // scheduler sinks all refills to the end of the unrolled body, which shortens the
+        // prefetch distance of the first slots to almost nothing)
+        __builtin_amdgcn_sched_barrier(0);
+      };
+      if constexpr (KSC > 0) {
+        // byte offsets of this tile's and the next tile's first fragment (the last tile
+        // prefetches itself again, in bounds)
+        const int tb = 2 * (t_begin + ti) * KSC * 1024;
+        const int tn = ti + 1 < ntile ? tb + 2 * KSC * 1024 : tb;
 #pragma unroll
-            for (int s = 0; s < 4; ++s)
+        for (int ks = 0; ks < KSC; ++ks)
+          kstep(ks, ring[ks % D], [&](v4u(&r)[2]) {
+            const int so = ks + D < KSC ? tb + (ks + D) * 1024 : tn + (ks + D - KSC) * 1024;
+            r[0] = __builtin_amdgcn_raw_buffer_load_b128(wrs, wvo, so, 0);
+            r[1] = __builtin_amdgcn_raw_buffer_load_b128(wrs, wvo, so + KSC * 1024, 0);
+          });
+      } else {
+        for (int ks0 = 0; ks0 < KS; ks0 += D) {
 #pragma unroll
-              for (int j = 0; j < HBB; ++j) {
-                acc[0][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa0[s], fb[j][s], acc[0][j], 0, 0, 0);
-                acc[1][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa1[s], fb[j][s], acc[1][j], 0, 0, 0);
-              }
-          }
-          fetch(ring[d]);
-          if constexpr (kPrefetchLds) {
-#pragma unroll
-            for (int j = 0; j < HBB; ++j) bcur[j] = bnxt[j];
-          }
-          // keep each refill right behind the MFMAs that consumed its slot (left alone, the
-          // scheduler sinks all refills to the end of the unrolled body, which shortens the
-          // prefetch distance of the first slots to almost nothing)
-          __builtin_amdgcn_sched_barrier(0);
+          for (int d = 0; d < D; ++d) kstep(ks0 + d, ring[d], fetch);
         }
       }
 
@@ -484,7 +516,7 @@ static int ring_depth(int bf16_mma, int KS) {
   return KS % 4 == 0 ? 4 : KS % 2 == 0 ? 2 : 1;
 }
 
-template <typename CT, int HB, int D, bool FIX, bool LOG>
+template <typename CT, int HB, int D, bool FIX, bool LOG, int KSC>
 static hipError_t vgo(const VocabArgs &a, hipStream_t st) {
   const int nhb = (a.M + HB - 1) / HB;
   const size_t tbytes = (size_t)HB * (a.E * sizeof(CT) + 16);
@@ -492,20 +524,27 @@ static hipError_t vgo(const VocabArgs &a, hipStream_t st) {
   const size_t lds = tbytes > lbytes ? tbytes : lbytes;
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void *)vocab_kernel<CT, HB, D, FIX, LOG>,
+    hipError_t e = hipFuncSetAttribute((const void *)vocab_kernel<CT, HB, D, FIX, LOG, KSC>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  hipLaunchKernelGGL((vocab_kernel<CT, HB, D, FIX, LOG>), dim3(nhb * a.n_chunks), dim3(VShape<CT, HB>::NT), lds,
+  hipLaunchKernelGGL((vocab_kernel<CT, HB, D, FIX, LOG, KSC>), dim3(nhb * a.n_chunks), dim3(VShape<CT, HB>::NT), lds,
                      st, a);
   return hipGetLastError();
 }
 
+template <typename CT, int HB, int D, int KSC>
+static hipError_t vgo_k(const VocabArgs &a, hipStream_t st) {
+  if (a.logits) return a.fixed_ref ? vgo<CT, HB, D, true, true, KSC>(a, st) : vgo<CT, HB, D, false, true, KSC>(a, st);
+  return a.fixed_ref ? vgo<CT, HB, D, true, false, KSC>(a, st) : vgo<CT, HB, D, false, false, KSC>(a, st);
+}
+
+// bf16 at E = 512 (32 k-steps) takes the unrolled form
 template <typename CT, int HB, int D>
 static hipError_t vgo_f(const VocabArgs &a, hipStream_t st) {
-  if (a.logits) return a.fixed_ref ? vgo<CT, HB, D, true, true>(a, st) : vgo<CT, HB, D, false, true>(a, st);
-  return a.fixed_ref ? vgo<CT, HB, D, true, false>(a, st) : vgo<CT, HB, D, false, false>(a, st);
+  if (sizeof(CT) == 2 && a.KS == 32 && 32 % D == 0) return vgo_k<CT, HB, D, 32>(a, st);
+  return vgo_k<CT, HB, D, 0>(a, st);
 }
 
 template <typename CT, int HB>
