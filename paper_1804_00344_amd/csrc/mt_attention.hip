@@ -11,10 +11,11 @@
 //   e_i = sum_a va[a] - sum_a 2 va[a] / (2^(P[i,a] c + q[m,a] c) + 1),   c = 2/ln2.
 // The row's q is held pre-scaled by c and va pre-scaled by -2, which leaves one FMA, one
 // exp2, one add, one reciprocal and one FMA per element; sum_a va[a] is a per-row constant.
-// Each wave takes two valid positions per iteration: its 64 lanes cover the A features of
-// P[b,i] in 16-byte granules, and every granule load of both positions is issued before any
-// of them is consumed (lanes beyond A read a clamped in-range address and carry zero
-// weight, so the loop has no per-granule branch).  Cross-lane shuffles reduce the sums.
+// Each wave walks every fourth valid position: its 64 lanes cover the A features of P[b,i]
+// in 16-byte granules, and the rows pass through a two-deep ring of raw granules, so the
+// loads of the next row are in flight while the current one is scored (lanes beyond A read a
+// clamped in-range address and carry zero weight, so the loop has no per-granule branch).
+// Cross-lane shuffles reduce the sums.
 //
 // Context.  Each thread owns 16-byte column granules of Cx and walks the valid positions
 // several at a time (eight for up to two granules per thread) with all their row loads in
@@ -35,6 +36,10 @@ struct Gran;  // one 16-byte granule of a row, widened to fp32
 template <>
 struct Gran<float> {
   static constexpr int N = 4;
+  template <typename V>
+  __device__ __forceinline__ static void unpack(const V &v, float (&x)[4]) {
+    __builtin_memcpy(x, &v, 16);
+  }
   __device__ __forceinline__ static void load(const float *p, float (&x)[4]) {
     const float4 v = *(const float4 *)p;
     x[0] = v.x; x[1] = v.y; x[2] = v.z; x[3] = v.w;
@@ -43,6 +48,13 @@ struct Gran<float> {
 template <>
 struct Gran<bf16> {
   static constexpr int N = 8;
+  template <typename V>
+  __device__ __forceinline__ static void unpack(const V &v, float (&x)[8]) {
+    bf16x8 h;
+    __builtin_memcpy(&h, &v, 16);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) x[j] = (float)h[j];
+  }
   __device__ __forceinline__ static void load(const bf16 *p, float (&x)[8]) {
     const bf16x8 v = *(const bf16x8 *)p;
 #pragma unroll
@@ -116,36 +128,71 @@ __global__ __launch_bounds__(kAT) void attention_kernel(int B, int K, int S, int
   __syncthreads();
   const int n = nvalid;
 
-  // ---- scores, two positions per wave iteration ----
-  for (int j = wave; j < n; j += 8) {
-    const bool two = j + 4 < n;
-    const int i0 = vidx[j], i1 = two ? vidx[j + 4] : i0;
-    const T *P0 = P + ((size_t)b * S + i0) * A;
-    const T *P1 = P + ((size_t)b * S + i1) * A;
-    float x0[NG][G], x1[NG][G];
+  // ---- scores: wave w takes positions w, w + 4, w + 8, ... through a two-deep ring of
+  // raw P rows, so the next row's loads are in flight while the current one is scored ----
+  typedef uint32_t v4u32 __attribute__((ext_vector_type(4)));
+  auto load_raw = [&](int jp, v4u32(&r)[NG]) {
+    const int i = vidx[jp < n ? jp : 0];  // past the end: an in-range row, never scored
+    const char *row = (const char *)(P + ((size_t)b * S + i) * A);
+#pragma unroll
+    for (int jj = 0; jj < NG; ++jj) r[jj] = *(const v4u32 *)(row + (size_t)goff[jj] * sizeof(T));
+  };
+  auto score_raw = [&](const v4u32(&r)[NG]) {
+    float acc = 0.f;
 #pragma unroll
     for (int jj = 0; jj < NG; ++jj) {
-      Gran<T>::load(P0 + goff[jj], x0[jj]);
-      Gran<T>::load(P1 + goff[jj], x1[jj]);
-    }
-    float acc0 = 0.f, acc1 = 0.f;
-#pragma unroll
-    for (int jj = 0; jj < NG; ++jj)
+      float x[G];
+      Gran<T>::unpack(r[jj], x);
 #pragma unroll
       for (int e = 0; e < G; ++e) {
-        const float d0 = __builtin_amdgcn_exp2f(__builtin_fmaf(x0[jj][e], kTwoOverLn2, qr[jj][e])) + 1.0f;
-        const float d1 = __builtin_amdgcn_exp2f(__builtin_fmaf(x1[jj][e], kTwoOverLn2, qr[jj][e])) + 1.0f;
-        acc0 = __builtin_fmaf(vr[jj][e], rcp_fast(d0), acc0);
-        acc1 = __builtin_fmaf(vr[jj][e], rcp_fast(d1), acc1);
+        const float d = __builtin_amdgcn_exp2f(__builtin_fmaf(x[e], kTwoOverLn2, qr[jj][e])) + 1.0f;
+        acc = __builtin_fmaf(vr[jj][e], rcp_fast(d), acc);
       }
-    acc0 = wave_sum(acc0);
-    acc1 = wave_sum(acc1);
-    if (lane == 0) {
-      es[j] = vsum + acc0;
-      if (two) es[j + 4] = vsum + acc1;
+    }
+    return wave_sum(acc);
+  };
+  if (wave < n) {  // wave-uniform
+    v4u32 ra[NG], rb[NG];
+    load_raw(wave, ra);
+    load_raw(wave + 4, rb);
+    int j = wave;
+    for (;;) {
+      const float s0 = score_raw(ra);
+      if (lane == 0) es[j] = vsum + s0;
+      load_raw(j + 8, ra);
+      j += 4;
+      if (j >= n) break;
+      const float s1 = score_raw(rb);
+      if (lane == 0) es[j] = vsum + s1;
+      load_raw(j + 8, rb);
+      j += 4;
+      if (j >= n) break;
     }
   }
   __syncthreads();
+
+  // ---- the first U context rows are loaded now: they do not depend on the weights, so
+  // their latency runs under the softmax ----
+  const int ncg = Cd / G;
+  const T *Cb = Cx + (size_t)b * S * Cd;
+  float c[NC][G];
+  int coff[NC];
+#pragma unroll
+  for (int p = 0; p < NC; ++p) {
+    const int g = t + kAT * p;
+    coff[p] = (g < ncg ? g : ncg - 1) * G;
+#pragma unroll
+    for (int e = 0; e < G; ++e) c[p][e] = 0.f;
+  }
+  float x[U][NC][G];
+  if (n > 0) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const T *row = Cb + (size_t)vidx[u < n ? u : 0] * Cd;
+#pragma unroll
+      for (int p = 0; p < NC; ++p) Gran<T>::load(row + coff[p], x[u][p]);
+    }
+  }
 
   // ---- masked softmax over the compacted scores (wave 0) ----
   if (wave == 0) {
@@ -172,17 +219,6 @@ __global__ __launch_bounds__(kAT) void attention_kernel(int B, int K, int S, int
     for (int j = t; j < n; j += kAT) alpha_out[(size_t)m * S + vidx[j]] = es[j];
 
   // ---- context: granules of the Cx columns, U positions in flight ----
-  const int ncg = Cd / G;
-  const T *Cb = Cx + (size_t)b * S * Cd;
-  float c[NC][G];
-  int coff[NC];
-#pragma unroll
-  for (int p = 0; p < NC; ++p) {
-    const int g = t + kAT * p;
-    coff[p] = (g < ncg ? g : ncg - 1) * G;
-#pragma unroll
-    for (int e = 0; e < G; ++e) c[p][e] = 0.f;
-  }
   for (int j0 = 0; j0 < n; j0 += U) {
     float al[U];
     const T *rows[U];
@@ -193,11 +229,12 @@ __global__ __launch_bounds__(kAT) void attention_kernel(int B, int K, int S, int
       al[u] = ok ? es[j] : 0.f;
       rows[u] = Cb + (size_t)vidx[ok ? j : j0] * Cd;
     }
-    float x[U][NC][G];
+    if (j0 > 0) {
 #pragma unroll
-    for (int u = 0; u < U; ++u)
+      for (int u = 0; u < U; ++u)
 #pragma unroll
-      for (int p = 0; p < NC; ++p) Gran<T>::load(rows[u] + coff[p], x[u][p]);
+        for (int p = 0; p < NC; ++p) Gran<T>::load(rows[u] + coff[p], x[u][p]);
+    }
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
