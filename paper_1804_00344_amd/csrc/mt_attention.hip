@@ -17,9 +17,10 @@
 // clamped in-range address and carry zero weight, so the loop has no per-granule branch).
 // Cross-lane shuffles reduce the sums.
 //
-// Context.  Each thread owns 16-byte column granules of Cx and walks the valid positions
-// several at a time (eight for up to two granules per thread) with all their row loads in
-// flight.
+// Context.  Each thread owns 16-byte column granules of Cx and walks the valid positions in
+// groups (eight positions for up to two granules per thread), with the next group's row
+// loads in flight while the current group is accumulated; the first two groups are loaded
+// before the softmax.
 //
 // Workgroup ids are remapped so that the K rows of one sentence run on one XCD and share
 // its L2 copy of P[b] and Cx[b].
@@ -171,8 +172,8 @@ __global__ __launch_bounds__(kAT) void attention_kernel(int B, int K, int S, int
   }
   __syncthreads();
 
-  // ---- the first U context rows are loaded now: they do not depend on the weights, so
-  // their latency runs under the softmax ----
+  // ---- the first context rows are loaded now: they do not depend on the weights, so their
+  // latency runs under the softmax ----
   const int ncg = Cd / G;
   const T *Cb = Cx + (size_t)b * S * Cd;
   float c[NC][G];
@@ -184,14 +185,21 @@ __global__ __launch_bounds__(kAT) void attention_kernel(int B, int K, int S, int
 #pragma unroll
     for (int e = 0; e < G; ++e) c[p][e] = 0.f;
   }
-  float x[U][NC][G];
-  if (n > 0) {
+  // raw 16-byte granules of U context rows (a group); two groups in flight
+  typedef uint32_t v4c __attribute__((ext_vector_type(4)));
+  auto load_group = [&](int j0, v4c(&r)[U][NC]) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const T *row = Cb + (size_t)vidx[u < n ? u : 0] * Cd;
+      const int j = j0 + u;
+      const char *row = (const char *)(Cb + (size_t)vidx[j < n ? j : 0] * Cd);  // past the end: weight 0
 #pragma unroll
-      for (int p = 0; p < NC; ++p) Gran<T>::load(row + coff[p], x[u][p]);
+      for (int p = 0; p < NC; ++p) r[u][p] = *(const v4c *)(row + (size_t)coff[p] * sizeof(T));
     }
+  };
+  v4c ga[U][NC], gb[U][NC];
+  if (n > 0) {
+    load_group(0, ga);
+    load_group(U, gb);
   }
 
   // ---- masked softmax over the compacted scores (wave 0) ----
@@ -218,29 +226,29 @@ __global__ __launch_bounds__(kAT) void attention_kernel(int B, int K, int S, int
   if (alpha_out)
     for (int j = t; j < n; j += kAT) alpha_out[(size_t)m * S + vidx[j]] = es[j];
 
-  // ---- context: granules of the Cx columns, U positions in flight ----
-  for (int j0 = 0; j0 < n; j0 += U) {
-    float al[U];
-    const T *rows[U];
+  // ---- context: the groups of U positions pass through the two-deep ring ----
+  auto accumulate = [&](int j0, const v4c(&r)[U][NC]) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int j = j0 + u;
-      const bool ok = j < n;
-      al[u] = ok ? es[j] : 0.f;
-      rows[u] = Cb + (size_t)vidx[ok ? j : j0] * Cd;
+      const float al = j < n ? es[j] : 0.f;
+#pragma unroll
+      for (int p = 0; p < NC; ++p) {
+        float x[G];
+        Gran<T>::unpack(r[u][p], x);
+#pragma unroll
+        for (int e = 0; e < G; ++e) c[p][e] = __builtin_fmaf(al, x[e], c[p][e]);
+      }
     }
-    if (j0 > 0) {
-#pragma unroll
-      for (int u = 0; u < U; ++u)
-#pragma unroll
-        for (int p = 0; p < NC; ++p) Gran<T>::load(rows[u] + coff[p], x[u][p]);
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-#pragma unroll
-      for (int p = 0; p < NC; ++p)
-#pragma unroll
-        for (int e = 0; e < G; ++e) c[p][e] = __builtin_fmaf(al[u], x[u][p][e], c[p][e]);
+  };
+  for (int j0 = 0; j0 < n;) {
+    accumulate(j0, ga);
+    load_group(j0 + 2 * U, ga);
+    j0 += U;
+    if (j0 >= n) break;
+    accumulate(j0, gb);
+    load_group(j0 + 2 * U, gb);
+    j0 += U;
   }
 #pragma unroll
   for (int p = 0; p < NC; ++p) {
