@@ -191,8 +191,8 @@ typedef enum {
   MT_KERNEL_GEMM_READOUT = 5, /* s Wt_s */
   MT_KERNEL_READOUT = 6,    /* sum + LN + tanh */
   MT_KERNEL_VOCAB_GEMM = 7, /* t Wo + bo with fused LSE partials and beam candidates */
-  MT_KERNEL_LSE = 8,        /* row log-sum-exp merge (+ logp finalize) */
-  MT_KERNEL_TOPK = 9,       /* all top-K kernels */
+  MT_KERNEL_LSE = 8,        /* logits -> log-probabilities (only when logp_out is given) */
+  MT_KERNEL_TOPK = 9,       /* all top-K kernels (row log-sum-exp merge included) */
   MT_KERNEL_PRECOMPUTE = 10,
   MT_KERNEL_VOCAB_THRESHOLD = 11, /* logits of the first vocabulary entries -> candidate threshold */
   MT_KERNEL_COUNT = 12

@@ -181,7 +181,7 @@ std::vector<float> cat(std::initializer_list<std::pair<const float *, int>> part
 
 // ---- workspace ----
 struct WsLayout {
-  size_t gh, s1, g2, c, g3, g4, t, sample, thr, part, cbuf, ccnt, ovf, lse, rowc, scand, total;
+  size_t gh, s1, g2, c, g3, g4, t, sample, thr, part, cbuf, ccnt, lse, rowc, scand, scnt, total;
   int ntiles, kc, nchunks;
 };
 
@@ -209,11 +209,11 @@ WsLayout ws_layout(const mt_model *m, int B, int K) {
   L.part = take(M * L.ntiles * sizeof(float2));
   L.cbuf = take(M * L.ntiles * vocab_lists() * kVocabCap * sizeof(int2));
   L.ccnt = take(M * L.ntiles * vocab_lists() * sizeof(int));
-  L.ovf = take(M * sizeof(int));
   L.lse = take(M * 4);
   L.rowc = take(M * K * sizeof(int2));
   L.nchunks = std::max(1, std::min(64, (c.V + 2047) / 2048));
   L.scand = take(M * L.nchunks * K * sizeof(int2));
+  L.scnt = take((size_t)B * sizeof(int));
   L.total = off;
   return L;
 }
@@ -583,12 +583,14 @@ mt_status mt_decoder_step(mt_model *model, int B, int K, int S, const int32_t *p
     ps.out = W + L.sample; ps.ldc = S; ps.M = M; ps.N = S; ps.K = E;
     LAUNCH(MT_KERNEL_VOCAB_THRESHOLD, launch_gemm(bf, &ps, 1, EPI_STORE, st));
     LAUNCH(MT_KERNEL_VOCAB_THRESHOLD, launch_vocab_threshold(M, V, K, (const float *)(W + L.sample),
-                                                             (float *)(W + L.thr), st));
+                                                             (float *)(W + L.thr), (int *)(W + L.scnt), B, st));
   }
   LAUNCH(MT_KERNEL_VOCAB_GEMM, launch_vocab(bf, t, model->wo_frag, model->bo_pad, M, V, E, L.ntiles,
                                             (const float *)(W + L.thr), part, (int2 *)(W + L.cbuf),
                                             (int *)(W + L.ccnt), kVocabCap, logp_out, model->logit_bounded, st));
-  LAUNCH(MT_KERNEL_LSE, launch_lse(M, L.ntiles, part, (float *)(W + L.lse), logp_out, V, st));
+  // the row log-sum-exp is merged by the beam selection itself; this pass only turns the
+  // written logits into log-probabilities
+  if (logp_out) LAUNCH(MT_KERNEL_LSE, launch_lse(M, L.ntiles, part, (float *)(W + L.lse), logp_out, V, st));
   model->last_B = B;
   model->last_K = K;
   model->last_ws = ws;
@@ -618,20 +620,26 @@ mt_status mt_beam_topk(mt_model *model, int B, int K, const float *prev_score, c
   char *W = (char *)ws;
   const int M = B * K, V = c.V;
   int2 *rowc = (int2 *)(W + L.rowc);
+  RowSelect rs{};
+  rs.B = B; rs.K = K; rs.V = V;
+  rs.prev_score = prev_score;
+  rs.row_cand = rowc;
+  rs.scnt = (int *)(W + L.scnt);
+  rs.score_out = score_out; rs.tok_out = tok_out; rs.bp_out = bp_out; rs.row_out = row_out;
   if (!logp) {
-    int *ovf = (int *)(W + L.ovf);
-    LAUNCH(MT_KERNEL_TOPK, launch_row_select(M, K, V, L.ntiles * vocab_lists(), kVocabCap, (const int *)(W + L.ccnt),
-                                             (const int2 *)(W + L.cbuf), (const float *)(W + L.lse), prev_score,
-                                             rowc, ovf, st));
-    LAUNCH(MT_KERNEL_TOPK, launch_vocab_fallback(model->bf16, W + L.t, model->wo_frag, model->bo_pad, M, V, c.E, K,
-                                                 (const float *)(W + L.lse), prev_score, rowc, ovf, st));
+    rs.nl = L.ntiles * vocab_lists(); rs.cap = kVocabCap;
+    rs.cnt = (const int *)(W + L.ccnt); rs.cbuf = (const int2 *)(W + L.cbuf);
+    rs.part = (const float2 *)(W + L.part); rs.ntiles = L.ntiles;
+    rs.vv.t = W + L.t; rs.vv.wp = model->wo_frag; rs.vv.bias = model->bo_pad;
+    rs.vv.V = V; rs.vv.E = c.E; rs.vv.KS = c.E / (model->bf16 ? 16 : 8);
+    rs.bf16_mma = model->bf16;
+    LAUNCH(MT_KERNEL_TOPK, launch_row_select(rs, st));
   } else {
     int2 *sc = (int2 *)(W + L.scand);
-    LAUNCH(MT_KERNEL_TOPK, launch_topk_scan_logp(M, K, V, L.nchunks, prev_score, logp, sc, st));
-    LAUNCH(MT_KERNEL_TOPK, launch_row_select(M, K, V, L.nchunks, K, nullptr, sc, nullptr, nullptr, rowc,
-                                             nullptr, st));
+    LAUNCH(MT_KERNEL_TOPK, launch_topk_scan_logp(M, K, V, L.nchunks, prev_score, logp, sc, rs.scnt, B, st));
+    rs.nl = L.nchunks; rs.cap = K; rs.cbuf = sc;
+    LAUNCH(MT_KERNEL_TOPK, launch_row_select(rs, st));
   }
-  LAUNCH(MT_KERNEL_TOPK, launch_topk_sentence(B, K, V, rowc, score_out, tok_out, bp_out, row_out, st));
   return MT_OK;
 }
 

@@ -270,6 +270,72 @@ __device__ __forceinline__ int wave_topk(const uint32_t (&u)[R], const int (&ix)
   return ns;
 }
 
+// ---- row-level pieces shared by the log-sum-exp pass and the beam selection ----
+
+// Log-sum-exp of one row from its per-chunk partials (m_c, s_c), s_c = sum of exp(logit - m_c)
+// over chunk c: L = M + ln sum_c s_c exp(m_c - M), M = max_c m_c.  Called by a whole
+// 256-thread workgroup (every thread gets L) with a fixed order of operations, so every
+// caller obtains the same bits from the same partials.
+__device__ __forceinline__ float block_row_lse(const float2 *pr, int ntiles) {
+  __shared__ float wmx[4], wsm[4];
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  float mx = -INFINITY;
+  for (int i = t; i < ntiles; i += 256) mx = fmaxf(mx, pr[i].x);
+  mx = wave_max(mx);
+  if (lane == 0) wmx[w] = mx;
+  __syncthreads();
+  mx = fmaxf(fmaxf(wmx[0], wmx[1]), fmaxf(wmx[2], wmx[3]));
+  float s = 0.f;
+  for (int i = t; i < ntiles; i += 256) {
+    const float2 q = pr[i];
+    s += q.y * exp_fast(q.x - mx);
+  }
+  s = wave_sum(s);
+  if (lane == 0) wsm[w] = s;
+  __syncthreads();
+  s = wsm[0] + wsm[1] + wsm[2] + wsm[3];
+  __syncthreads();  // the scratch may be reused by the caller's next call
+  return mx + __builtin_amdgcn_logf(s) * 0.6931471805599453f;
+}
+
+// The output projection as the exact recomputation reads it: packed Wo^T in MFMA fragment
+// order (32-row vocabulary block vb, k-step ks of KV = 32 / sizeof(CT) k-values: 64 lanes x 16
+// bytes at ((vb * KS + ks) * 64 + lane) * 16, lane l holding row vb*32 + l%32 and k-values
+// ks*KV + (l/32)*KV/2 + j), the padded bias, and the readout activations t [M][E].
+struct VocabView {
+  const void *t;
+  const void *wp;
+  const float *bias;
+  int V, E, KS;
+};
+
+// Exact K best keys prev + (logit - L) of row m over the whole vocabulary, recomputed from the
+// weights by a 256-thread workgroup; emit(rank, key, token) for ranks 0..K-1.
+template <typename CT, int KMAX, typename Emit>
+__device__ __forceinline__ void row_recompute(const VocabView &vv, int m, int K, float L, float prev, Emit emit) {
+  constexpr int epv = 16 / (int)sizeof(CT);  // k-values per lane vector
+  constexpr int KV = 2 * epv;
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const CT *trow = (const CT *)vv.t + (size_t)m * vv.E;
+  const int nvb = (vv.V + 31) / 32;
+  List<KMAX> lst;
+  lst.init();
+  // lane pairs (l, l+32) of a wave share one vocabulary entry
+  for (int vb = w; vb < nvb; vb += 4) {
+    float acc = 0.f;
+    for (int ks = 0; ks < vv.KS; ++ks) {
+      const CT *wv = (const CT *)((const char *)vv.wp + (((size_t)vb * vv.KS + ks) * 64 + lane) * 16);
+      const int k0 = ks * KV + (lane >> 5) * epv;
+#pragma unroll
+      for (int j = 0; j < epv; ++j) acc += to_f32(wv[j]) * to_f32(trow[k0 + j]);
+    }
+    acc += __shfl_xor(acc, 32, 64);
+    const int v = vb * 32 + (lane & 31);
+    if (lane < 32 && v < vv.V) lst.push(prev + ((acc + vv.bias[v]) - L), v);
+  }
+  block_extract<KMAX>(lst, K, emit);
+}
+
 // ---------------------------------------------------------------------------------------
 // launchers (host side).  All return hipSuccess or the launch error.
 // ---------------------------------------------------------------------------------------
@@ -310,7 +376,9 @@ void vocab_pack_host(int bf16_mma, int V, int E, const float *src, int src_is_em
 // thr[m] = a value reached by K of sample[m][0 .. min(V, S)) (the K-th largest of 64 lane maxima),
 // minus a rounding margin, S = vocab_sample_size(V);
 // sample [M][S] holds the logits of the first S vocabulary entries (computed by launch_gemm)
-hipError_t launch_vocab_threshold(int M, int V, int K, const float *sample, float *thr, hipStream_t st);
+// Block 0 also clears the B sentence arrival counters scnt of the following beam selection.
+hipError_t launch_vocab_threshold(int M, int V, int K, const float *sample, float *thr, int *scnt, int B,
+                                  hipStream_t st);
 // part [M][n_chunks] (reference m, sum exp(l - m)); every logit >= thr[m] goes to cbuf
 // [M][n_chunks][lists][cap] with counts in ccnt [M][n_chunks][lists] (a count above cap marks
 // an overflowed list); logits [M][V] or NULL.  fixed_ref: the caller has proven every logit
@@ -318,11 +386,6 @@ hipError_t launch_vocab_threshold(int M, int V, int K, const float *sample, floa
 hipError_t launch_vocab(int bf16_mma, const void *t, const void *wp, const float *bias_pad, int M, int V,
                         int E, int n_chunks, const float *thr, float2 *part, int2 *cbuf, int *ccnt, int cap,
                         float *logits, int fixed_ref, hipStream_t st);
-// exact recomputation of the rows with ovf[m] != 0: row_out[m] = the K best keys
-// prev_score + (logit - lse) over the whole vocabulary
-hipError_t launch_vocab_fallback(int bf16_mma, const void *t, const void *wp, const float *bias_pad, int M,
-                                 int V, int E, int K, const float *lse, const float *prev_score, int2 *row_out,
-                                 const int *ovf, hipStream_t st);
 constexpr int kVocabCap = 32;  // candidate buffer entries per (row, chunk, list)
 constexpr int kVocabPad = 64;  // vocabulary rows are padded to a multiple of this
 
@@ -349,17 +412,34 @@ hipError_t launch_attention(int B, int K, int S, int A, int Cd, const void *P, c
 hipError_t launch_lse(int M, int ntiles, const float2 *part, float *lse, float *logits, int V,
                       hipStream_t st);
 
-// candidates are (value, token) pairs stored as int2 {float bits, token}.  Row selection: the K
-// best keys of each row from nl lists of up to cap candidates (cnt NULL = lists full; lse NULL
-// = values are keys, else logits keyed as prev_score + (logit - lse)); rows whose candidates do
-// not fit get ovf[m] = 1 and no output (see launch_vocab_fallback), the others ovf[m] = 0.
-hipError_t launch_row_select(int M, int K, int V, int nl, int cap, const int *cnt, const int2 *cbuf,
-                             const float *lse, const float *prev_score, int2 *row_out, int *ovf,
-                             hipStream_t st);
+// Beam selection, one workgroup per row m = b*K + k.  Candidates are (value, token) pairs stored
+// as int2 {float bits, token} in nl lists of up to cap entries per row: cbuf [M][nl][cap] with
+// fill counts cnt [M][nl] (NULL: every list holds cap entries).
+//  * part != NULL (candidates from the vocabulary pass): values are logits; the row's
+//    log-sum-exp is merged from part [M][ntiles] and keys are prev_score + (logit - lse).  A
+//    row whose candidates do not fit (a list count above cap, more than the row can stage,
+//    or fewer than K) is recomputed exactly from vv (bf16_mma gives its compute dtype).
+//  * part == NULL: values are keys (the logp path).
+// The row's K best go to row_cand [M][K].  The last row of sentence b to finish (counted in
+// scnt[b], which must be 0 before the first use and is left at 0) merges the sentence's K x K
+// row results into score/tok/bp/row_out [B][K].
+struct RowSelect {
+  int B, K, V, nl, cap;
+  const int *cnt;
+  const int2 *cbuf;
+  const float2 *part;
+  int ntiles;
+  const float *prev_score;
+  VocabView vv;
+  int bf16_mma;
+  int2 *row_cand;
+  int *scnt;
+  float *score_out;
+  int32_t *tok_out, *bp_out, *row_out;
+};
+hipError_t launch_row_select(const RowSelect &a, hipStream_t st);
+// Block (0, 0) also clears the B sentence arrival counters scnt.
 hipError_t launch_topk_scan_logp(int M, int K, int V, int nchunks, const float *prev_score,
-                                 const float *logp, int2 *cand_out, hipStream_t st);
-hipError_t launch_topk_sentence(int B, int K, int V, const int2 *row_cand, float *score_out,
-                                int32_t *tok_out, int32_t *bp_out, int32_t *row_out,
-                                hipStream_t st);
+                                 const float *logp, int2 *cand_out, int *scnt, int B, hipStream_t st);
 
 }  // namespace mt

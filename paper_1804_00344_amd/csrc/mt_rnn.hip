@@ -241,23 +241,8 @@ __global__ __launch_bounds__(kT) void masked_mean_kernel(int B, int S, int Cd, c
 __global__ __launch_bounds__(kT) void lse_kernel(int M, int ntiles, const float2 *__restrict__ part,
                                                  float *__restrict__ lse, float *__restrict__ logits,
                                                  int V) {
-  __shared__ float red[4][1];
   const int m = blockIdx.x, t = threadIdx.x;
-  const float2 *pr = part + (size_t)m * ntiles;
-  float mx = -INFINITY;
-  for (int i = t; i < ntiles; i += kT) mx = fmaxf(mx, pr[i].x);
-  mx = wave_max(mx);
-  __shared__ float wmx[4];
-  if ((t & 63) == 0) wmx[t >> 6] = mx;
-  __syncthreads();
-  mx = fmaxf(fmaxf(wmx[0], wmx[1]), fmaxf(wmx[2], wmx[3]));
-  float s[1] = {0.f};
-  for (int i = t; i < ntiles; i += kT) {
-    const float2 q = pr[i];
-    s[0] += q.y * exp_fast(q.x - mx);
-  }
-  block_sum<1>(s, red);
-  const float L = mx + __builtin_amdgcn_logf(s[0]) * 0.6931471805599453f;
+  const float L = block_row_lse(part + (size_t)m * ntiles, ntiles);
   if (t == 0) lse[m] = L;
   if (logits) {
     float *row = logits + (size_t)m * V;

@@ -8,7 +8,8 @@
 //      vocabulary kernel into per-(row, chunk, lane) lists; or, for a materialised logp, the
 //      K best keys of each chunk of the row (topk_scan_logp);
 //   2. per row (row_select): the K best keys among the row's candidates;
-//   3. per sentence (topk_sentence): the K best of the K rows' K candidates.
+//   3. per sentence (by the last of its rows to finish row selection): the K best of the K
+//      rows' K candidates.
 // Levels 2 and 3 select exactly by bisection over order-preserving integer codes of the
 // keys (wave_topk): every count is a ballot plus a scalar popcount, ties at the cut are
 // resolved by a second bisection over the indices, and the K survivors are ranked by
@@ -16,173 +17,35 @@
 // chain longer than one min/max reduction.
 #include "mt_internal.h"
 
+#include <type_traits>
+
 namespace mt {
 
 constexpr int kTT = 256;
 constexpr int kRowCap = 4096;          // candidates one row can stage in LDS
 constexpr int kSlots = kRowCap / 256;  // register slots per lane when a wave takes a quarter
 
-// Level 2.  Row m's candidates sit in nl lists of up to cap entries: cbuf [M][nl][cap] of
-// (value bits, token), with fill counts cnt [M][nl] (NULL: every list holds cap entries).
-// lse != NULL: values are logits, turned into keys prev_score + (logit - lse); else values
-// are keys.  Tokens outside [0, V) are padding.  A row whose candidates do not fit (a list
-// count above cap, or more than kRowCap in total), or, with fill counts, a row with fewer
-// than K candidates (its threshold was above its K-th best), is flagged in ovf[m] (if given)
-// and left for the exact recomputation; other rows get ovf[m] = 0 and their K best in row_out.
-template <int KMAX>
-__global__ __launch_bounds__(kTT) void row_select_kernel(int M, int K, int V, int nl, int cap,
-                                                         const int *__restrict__ cnt,
-                                                         const int2 *__restrict__ cbuf,
-                                                         const float *__restrict__ lse,
-                                                         const float *__restrict__ prev_score,
-                                                         int2 *__restrict__ row_out, int *__restrict__ ovf) {
-  __shared__ uint32_t su[kRowCap];
-  __shared__ int si[kRowCap];
-  __shared__ int wtot[4];
-  __shared__ uint32_t qu[4][KMAX];
-  __shared__ int qi[4][KMAX];
-  __shared__ int qn[4];
-  const int m = blockIdx.x, t = threadIdx.x, lane = t & 63, w = t >> 6;
-  const float L = lse ? lse[m] : 0.f;
-  const float sc = lse ? prev_score[m] : 0.f;
-  int2 *out = row_out + (size_t)m * K;
-  if (lse && sc == -INFINITY) {  // every key of the row is -inf: the K smallest tokens win
-    if (t < K) out[t] = make_int2(__float_as_int(-INFINITY), t);
-    if (t == 0 && ovf) ovf[m] = 0;
-    return;
-  }
-  const int *cr = cnt ? cnt + (size_t)m * nl : nullptr;
-
-  // ---- list fill counts and the block-wide offsets of this thread's entries ----
-  int mine = 0;
-  bool over = false;
-  for (int l = t; l < nl; l += kTT) {
-    const int c = cr ? cr[l] : cap;
-    over |= c > cap;
-    mine += c < cap ? c : cap;
-  }
-  int incl = mine;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(incl, o, 64);
-    if (lane >= o) incl += y;
-  }
-  if (lane == 63) wtot[w] = incl;
-  const bool any_over = __syncthreads_or(over);
-  int off = incl - mine, N = 0;
-#pragma unroll
-  for (int v = 0; v < 4; ++v) {
-    off += v < w ? wtot[v] : 0;
-    N += wtot[v];
-  }
-  if (any_over || N > kRowCap || (cr && N < K)) {
-    if (t == 0 && ovf) ovf[m] = 1;
-    return;
-  }
-  if (t == 0 && ovf) ovf[m] = 0;
-
-  // ---- stage the candidates as (key code, token) in LDS ----
-  for (int l = t; l < nl; l += kTT) {
-    int c = cr ? cr[l] : cap;
-    c = c < cap ? c : cap;
-    const int2 *e = cbuf + ((size_t)m * nl + l) * cap;
-    for (int q0 = 0; q0 < c; q0 += 8) {
-      int2 v[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) v[u] = q0 + u < c ? e[q0 + u] : make_int2(0, -1);
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        if (q0 + u >= c) continue;
-        const int tok = v[u].y;
-        uint32_t code = 0u;
-        if (tok >= 0 && tok < V) {
-          float key = __int_as_float(v[u].x);
-          if (lse) {
-            const float lp = key - L;
-            key = sc + lp;
-          }
-          code = key_code(key);
-        }
-        su[off + q0 + u] = code;
-        si[off + q0 + u] = tok;
-      }
-    }
-    off += c;
-  }
-  __syncthreads();
-
-  // ---- each wave selects the K best of one quarter ----
-  {
-    const int per = (N + 3) / 4;
-    const int s0 = w * per, s1 = s0 + per < N ? s0 + per : N;
-    const int nw = s1 > s0 ? s1 - s0 : 0;
-    const int rs = (nw + 63) / 64;
-    uint32_t u[kSlots];
-    int ix[kSlots];
-#pragma unroll
-    for (int s = 0; s < kSlots; ++s) {
-      const int j = s0 + s * 64 + lane;
-      const bool ok = s < rs && j < s1;
-      u[s] = ok ? su[j] : 0u;
-      ix[s] = ok ? si[j] : 0x7fffffff;
-    }
-    const int ns = wave_topk<kSlots>(u, ix, rs, K, qu[w], qi[w], [](int, float, int) {});
-    if (lane == 0) qn[w] = ns;
-  }
-  __syncthreads();
-
-  // ---- wave 0 merges the four selections ----
-  if (w == 0) {
-    int base = 0, src = -1, r = 0;
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      if (src < 0 && lane < base + qn[v]) {
-        src = v;
-        r = lane - base;
-      }
-      base += qn[v];
-    }
-    uint32_t u[1] = {src >= 0 ? qu[src][r] : 0u};
-    int ix[1] = {src >= 0 ? qi[src][r] : 0x7fffffff};
-    const int ns = wave_topk<1>(u, ix, 1, K, su, si, [&](int rank, float key, int tok) {
-      out[rank] = make_int2(__float_as_int(key), tok);
-    });
-    if (lane >= ns && lane < K) out[lane] = make_int2(__float_as_int(-INFINITY), 0x7fffffff);
-  }
+// Row results cross workgroups (and XCDs, whose L2 caches are not coherent with each other)
+// on their way to the sentence merge.  They are written and read with device-scope atomic
+// accesses, which are coherent without the full L2 write-back a device-scope release fence
+// costs; each writer waits for its stores to complete before its workgroup is counted in.
+__device__ __forceinline__ void put_row(int2 *p, float key, int tok) {
+  const unsigned long long v = (unsigned long long)(uint32_t)__float_as_int(key) |
+                               ((unsigned long long)(uint32_t)tok << 32);
+  __hip_atomic_store((unsigned long long *)p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ int2 get_row(const int2 *p) {
+  const unsigned long long v =
+      __hip_atomic_load((const unsigned long long *)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return make_int2((int)(uint32_t)v, (int)(uint32_t)(v >> 32));
 }
 
-// Level 1 for a materialised logp: the best K keys score + logp[v] of one chunk of a row.
+// Level 3 for one sentence, by one wave: the K best of the K x K row results
+// (row_cand [M][K] of (key bits, token)); candidate (k, j) has flat index k*V + token.
 template <int KMAX>
-__global__ __launch_bounds__(kTT) void topk_scan_logp_kernel(int M, int K, int V, int chunk,
-                                                             const float *__restrict__ prev_score,
-                                                             const float *__restrict__ logp,
-                                                             int2 *__restrict__ cand_out) {
-  const int m = blockIdx.y, ch = blockIdx.x, nch = gridDim.x;
-  const float sc = prev_score[m];
-  const float *row = logp + (size_t)m * V;
-  const int v0 = ch * chunk, v1 = min(V, v0 + chunk);
-  List<KMAX> lst;
-  lst.init();
-  for (int v = v0 + threadIdx.x; v < v1; v += kTT) lst.push(sc + row[v], v);
-  int2 *o = cand_out + ((size_t)m * nch + ch) * K;
-  block_extract<KMAX>(lst, K, [&](int r, float v, int i) { o[r] = make_int2(__float_as_int(v), i); });
-}
-
-// Level 3: one wave per sentence over the K x K row candidates (row_cand [M][K] of
-// (key bits, token)); candidate (k, j) has flat index k*V + token.
-template <int KMAX>
-__global__ __launch_bounds__(256) void topk_sentence_kernel(int B, int K, int V,
-                                                            const int2 *__restrict__ row_cand,
-                                                            float *__restrict__ score_out,
-                                                            int32_t *__restrict__ tok_out,
-                                                            int32_t *__restrict__ bp_out,
-                                                            int32_t *__restrict__ row_out) {
+__device__ __forceinline__ void sentence_merge(const RowSelect &a, int b, uint32_t *su, int *si) {
   constexpr int R = (KMAX * KMAX + 63) / 64;
-  __shared__ uint32_t su[4][KMAX];
-  __shared__ int si[4][KMAX];
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int b = blockIdx.x * 4 + w;
-  if (b >= B) return;  // uniform per wave
+  const int lane = threadIdx.x & 63, K = a.K, V = a.V;
   const int n = K * K;
   uint32_t u[R];
   int ix[R];
@@ -193,27 +56,189 @@ __global__ __launch_bounds__(256) void topk_sentence_kernel(int B, int K, int V,
     ix[s] = 0x7fffffff;
     if (j < n) {
       const int k = j / K;
-      const int2 e = row_cand[(size_t)(b * K + k) * K + (j - k * K)];
+      const int2 e = get_row(a.row_cand + (size_t)(b * K + k) * K + (j - k * K));
       if (e.y >= 0 && e.y < V) {
         u[s] = key_code(__int_as_float(e.x));
         ix[s] = k * V + e.y;
       }
     }
   }
-  const int ns = wave_topk<R>(u, ix, (n + 63) / 64, K, su[w], si[w], [&](int rank, float key, int i) {
+  const int ns = wave_topk<R>(u, ix, (n + 63) / 64, K, su, si, [&](int rank, float key, int i) {
     const int o = b * K + rank;
-    score_out[o] = key;
-    tok_out[o] = i % V;
-    bp_out[o] = i / V;
-    if (row_out) row_out[o] = b * K + i / V;
+    a.score_out[o] = key;
+    a.tok_out[o] = i % V;
+    a.bp_out[o] = i / V;
+    if (a.row_out) a.row_out[o] = b * K + i / V;
   });
   if (lane >= ns && lane < K) {  // fewer than K candidates: dead slots continue hypothesis 0
     const int o = b * K + lane;
-    score_out[o] = -INFINITY;
-    tok_out[o] = 0;
-    bp_out[o] = 0;
-    if (row_out) row_out[o] = b * K;
+    a.score_out[o] = -INFINITY;
+    a.tok_out[o] = 0;
+    a.bp_out[o] = 0;
+    if (a.row_out) a.row_out[o] = b * K;
   }
+}
+
+// Levels 2 and 3: one workgroup per row (see RowSelect).  A row's K best are staged as (key
+// code, token) in LDS, four waves each select from a quarter and wave 0 merges the quarters.
+// Every workgroup then counts itself in for its sentence; the last of the sentence's K rows
+// merges them.
+template <int KMAX, typename CT>
+__global__ __launch_bounds__(kTT) void row_select_kernel(RowSelect a) {
+  __shared__ uint32_t su[kRowCap];
+  __shared__ int si[kRowCap];
+  __shared__ int wtot[4];
+  __shared__ uint32_t qu[4][KMAX];
+  __shared__ int qi[4][KMAX];
+  __shared__ int qn[4];
+  __shared__ int last;
+  const int m = blockIdx.x, t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int K = a.K, V = a.V, nl = a.nl, cap = a.cap;
+  const int b = m / K;
+  const bool fused = a.part != nullptr;
+  const float L = fused ? block_row_lse(a.part + (size_t)m * a.ntiles, a.ntiles) : 0.f;
+  const float sc = fused ? a.prev_score[m] : 0.f;
+  int2 *out = a.row_cand + (size_t)m * K;
+  auto emit_row = [&](int rank, float key, int tok) { put_row(out + rank, key, tok); };
+
+  if (fused && sc == -INFINITY) {  // every key of the row is -inf: the K smallest tokens win
+    if (t < K) put_row(out + t, -INFINITY, t);
+  } else {
+    const int *cr = a.cnt ? a.cnt + (size_t)m * nl : nullptr;
+
+    // ---- list fill counts and the block-wide offsets of this thread's entries ----
+    int mine = 0;
+    bool over = false;
+    for (int l = t; l < nl; l += kTT) {
+      const int c = cr ? cr[l] : cap;
+      over |= c > cap;
+      mine += c < cap ? c : cap;
+    }
+    int incl = mine;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(incl, o, 64);
+      if (lane >= o) incl += y;
+    }
+    if (lane == 63) wtot[w] = incl;
+    const bool any_over = __syncthreads_or(over);
+    int off = incl - mine, N = 0;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      off += v < w ? wtot[v] : 0;
+      N += wtot[v];
+    }
+    if (any_over || N > kRowCap || (cr && N < K)) {
+      // the candidates do not fit (or fall short of K): exact recomputation of the row
+      if (fused) row_recompute<CT, KMAX>(a.vv, m, K, L, sc, emit_row);
+    } else {
+      // ---- stage the candidates as (key code, token) in LDS ----
+      for (int l = t; l < nl; l += kTT) {
+        int c = cr ? cr[l] : cap;
+        c = c < cap ? c : cap;
+        const int2 *e = a.cbuf + ((size_t)m * nl + l) * cap;
+        for (int q0 = 0; q0 < c; q0 += 8) {
+          int2 v[8];
+#pragma unroll
+          for (int u = 0; u < 8; ++u) v[u] = q0 + u < c ? e[q0 + u] : make_int2(0, -1);
+#pragma unroll
+          for (int u = 0; u < 8; ++u) {
+            if (q0 + u >= c) continue;
+            const int tok = v[u].y;
+            uint32_t code = 0u;
+            if (tok >= 0 && tok < V) {
+              float key = __int_as_float(v[u].x);
+              if (fused) {
+                const float lp = key - L;
+                key = sc + lp;
+              }
+              code = key_code(key);
+            }
+            su[off + q0 + u] = code;
+            si[off + q0 + u] = tok;
+          }
+        }
+        off += c;
+      }
+      __syncthreads();
+
+      // ---- each wave selects the K best of one quarter (register slots sized to the
+      // quarter: the bisection's cost grows with the slot count) ----
+      {
+        const int per = (N + 3) / 4;
+        const int s0 = w * per, s1 = s0 + per < N ? s0 + per : N;
+        const int nw = s1 > s0 ? s1 - s0 : 0;
+        const int rs = (nw + 63) / 64;
+        auto quarter = [&](auto slots) {
+          constexpr int R = decltype(slots)::value;
+          uint32_t u[R];
+          int ix[R];
+#pragma unroll
+          for (int s = 0; s < R; ++s) {
+            const int j = s0 + s * 64 + lane;
+            const bool ok = s < rs && j < s1;
+            u[s] = ok ? su[j] : 0u;
+            ix[s] = ok ? si[j] : 0x7fffffff;
+          }
+          return wave_topk<R>(u, ix, rs, K, qu[w], qi[w], [](int, float, int) {});
+        };
+        int ns;
+        if (rs <= 2)
+          ns = quarter(std::integral_constant<int, 2>());
+        else if (rs <= 4)
+          ns = quarter(std::integral_constant<int, 4>());
+        else
+          ns = quarter(std::integral_constant<int, kSlots>());
+        if (lane == 0) qn[w] = ns;
+      }
+      __syncthreads();
+
+      // ---- wave 0 merges the four selections ----
+      if (w == 0) {
+        int base = 0, src = -1, r = 0;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          if (src < 0 && lane < base + qn[v]) {
+            src = v;
+            r = lane - base;
+          }
+          base += qn[v];
+        }
+        uint32_t u[1] = {src >= 0 ? qu[src][r] : 0u};
+        int ix[1] = {src >= 0 ? qi[src][r] : 0x7fffffff};
+        const int ns = wave_topk<1>(u, ix, 1, K, su, si, emit_row);
+        if (lane >= ns && lane < K) put_row(out + lane, -INFINITY, 0x7fffffff);
+      }
+    }
+  }
+
+  // ---- the last row of the sentence to finish merges the sentence ----
+  __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): this thread's row stores have completed
+  __syncthreads();
+  if (t == 0) last = __hip_atomic_fetch_add(a.scnt + b, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == K - 1;
+  __syncthreads();
+  if (!last) return;
+  if (w == 0) sentence_merge<KMAX>(a, b, qu[0], qi[0]);
+  if (t == 0) __hip_atomic_store(a.scnt + b, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Level 1 for a materialised logp: the best K keys score + logp[v] of one chunk of a row.
+template <int KMAX>
+__global__ __launch_bounds__(kTT) void topk_scan_logp_kernel(int M, int K, int V, int chunk,
+                                                             const float *__restrict__ prev_score,
+                                                             const float *__restrict__ logp,
+                                                             int2 *__restrict__ cand_out, int *scnt, int B) {
+  const int m = blockIdx.y, ch = blockIdx.x, nch = gridDim.x;
+  if (m == 0 && ch == 0)
+    for (int i = threadIdx.x; i < B; i += kTT) __hip_atomic_store(scnt + i, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const float sc = prev_score[m];
+  const float *row = logp + (size_t)m * V;
+  const int v0 = ch * chunk, v1 = min(V, v0 + chunk);
+  List<KMAX> lst;
+  lst.init();
+  for (int v = v0 + threadIdx.x; v < v1; v += kTT) lst.push(sc + row[v], v);
+  int2 *o = cand_out + ((size_t)m * nch + ch) * K;
+  block_extract<KMAX>(lst, K, [&](int r, float v, int i) { o[r] = make_int2(__float_as_int(v), i); });
 }
 
 static int kbucket(int K) { return K <= 1 ? 1 : K <= 2 ? 2 : K <= 4 ? 4 : K <= 8 ? 8 : 16; }
@@ -227,34 +252,26 @@ static int kbucket(int K) { return K <= 1 ? 1 : K <= 2 ? 2 : K <= 4 ? 4 : K <= 8
     default: CALL(16); break; \
   }
 
-hipError_t launch_row_select(int M, int K, int V, int nl, int cap, const int *cnt, const int2 *cbuf,
-                             const float *lse, const float *prev_score, int2 *row_out, int *ovf,
-                             hipStream_t st) {
+hipError_t launch_row_select(const RowSelect &a, hipStream_t st) {
+  const int M = a.B * a.K;
   if (M == 0) return hipSuccess;
-#define MT_RS(N) \
-  hipLaunchKernelGGL((row_select_kernel<N>), dim3(M), dim3(kTT), 0, st, M, K, V, nl, cap, cnt, cbuf, lse, prev_score, row_out, ovf)
-  MT_KSWITCH(K, MT_RS)
+#define MT_RS(N)                                                                          \
+  if (a.bf16_mma)                                                                         \
+    hipLaunchKernelGGL((row_select_kernel<N, bf16>), dim3(M), dim3(kTT), 0, st, a);       \
+  else                                                                                    \
+    hipLaunchKernelGGL((row_select_kernel<N, float>), dim3(M), dim3(kTT), 0, st, a);
+  MT_KSWITCH(a.K, MT_RS)
 #undef MT_RS
   return hipGetLastError();
 }
 
 hipError_t launch_topk_scan_logp(int M, int K, int V, int nchunks, const float *prev_score,
-                                 const float *logp, int2 *cand_out, hipStream_t st) {
+                                 const float *logp, int2 *cand_out, int *scnt, int B, hipStream_t st) {
   if (M == 0) return hipSuccess;
   const int chunk = (V + nchunks - 1) / nchunks;
-#define MT_TS(N) hipLaunchKernelGGL((topk_scan_logp_kernel<N>), dim3(nchunks, M), dim3(kTT), 0, st, M, K, V, chunk, prev_score, logp, cand_out)
+#define MT_TS(N) hipLaunchKernelGGL((topk_scan_logp_kernel<N>), dim3(nchunks, M), dim3(kTT), 0, st, M, K, V, chunk, prev_score, logp, cand_out, scnt, B)
   MT_KSWITCH(K, MT_TS)
 #undef MT_TS
-  return hipGetLastError();
-}
-
-hipError_t launch_topk_sentence(int B, int K, int V, const int2 *row_cand, float *score_out,
-                                int32_t *tok_out, int32_t *bp_out, int32_t *row_out,
-                                hipStream_t st) {
-  if (B == 0) return hipSuccess;
-#define MT_TSN(N) hipLaunchKernelGGL((topk_sentence_kernel<N>), dim3((B + 3) / 4), dim3(256), 0, st, B, K, V, row_cand, score_out, tok_out, bp_out, row_out)
-  MT_KSWITCH(K, MT_TSN)
-#undef MT_TSN
   return hipGetLastError();
 }
 

@@ -390,8 +390,10 @@ __global__ __launch_bounds__((VShape<CT, HB>::NT)) void vocab_kernel(VocabArgs a
 // share a lane, at a small fraction of the cost.
 template <int R>
 __global__ __launch_bounds__(256) void vocab_threshold_kernel(int M, int S, int K, const float *__restrict__ sample,
-                                                              int ld, float *__restrict__ thr) {
+                                                              int ld, float *__restrict__ thr, int *scnt, int B) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  if (blockIdx.x == 0)
+    for (int i = threadIdx.x; i < B; i += 256) __hip_atomic_store(scnt + i, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   const int m = blockIdx.x * 4 + w;
   if (m >= M) return;  // uniform per wave
   const float *row = sample + (size_t)m * ld;
@@ -410,52 +412,6 @@ __global__ __launch_bounds__(256) void vocab_threshold_kernel(int M, int S, int 
   float kth = -INFINITY;
   if (wave_count_ge<1>(um, 1, 1u) >= K) kth = key_from_code(wave_kth_code<1>(um, 1, K));
   if (lane == 0) thr[m] = kth - 1e-3f * (1.0f + fabsf(kth));
-}
-
-// Exact recomputation of the rows flagged by the row selection (their candidates did not fit):
-// the full logit row from the packed weights, then the K best keys.  Workgroup x reads the flags of rows
-// [256x, 256x + 256) in parallel and processes its flagged rows one after another.
-template <typename CT, int KMAX>
-__global__ __launch_bounds__(256) void vocab_fallback_kernel(VocabArgs a, int K, const float *__restrict__ lse,
-                                                             const float *__restrict__ prev_score,
-                                                             int2 *__restrict__ row_out,
-                                                             const int *__restrict__ ovf) {
-  constexpr int KV = VCfg<CT>::KV;
-  constexpr int epv = 16 / (int)sizeof(CT);
-  __shared__ int rows[256];
-  __shared__ int nr;
-  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
-  if (t == 0) nr = 0;
-  __syncthreads();
-  {
-    const int m = blockIdx.x * 256 + t;
-    if (m < a.M && ovf[m]) rows[atomicAdd(&nr, 1)] = m;
-  }
-  __syncthreads();
-  const int n = nr;
-  for (int r = 0; r < n; ++r) {
-    const int m = rows[r];
-    const float Lm = lse[m], sc = prev_score[m];
-    const CT *trow = (const CT *)a.t + (size_t)m * a.E;
-    const int nvb = (a.V + 31) / 32;
-    List<KMAX> lst;
-    lst.init();
-    // lane pairs (l, l+32) of a wave share one vocabulary entry
-    for (int vb = w; vb < nvb; vb += 4) {
-      float acc = 0.f;
-      for (int ks = 0; ks < a.KS; ++ks) {
-        const CT *wv = (const CT *)((const v4u *)a.wp + ((size_t)vb * a.KS + ks) * 64 + lane);
-        const int k0 = ks * KV + (lane >> 5) * (KV / 2);
-#pragma unroll
-        for (int j = 0; j < epv; ++j) acc += to_f32(wv[j]) * to_f32(trow[k0 + j]);
-      }
-      acc += __shfl_xor(acc, 32, 64);
-      const int v = vb * 32 + (lane & 31);
-      if (lane < 32 && v < a.V) lst.push(sc + ((acc + a.bias[v]) - Lm), v);
-    }
-    block_extract<KMAX>(lst, K, [&](int q, float v, int i) { row_out[(size_t)m * K + q] = make_int2(__float_as_int(v), i); });
-    __syncthreads();
-  }
 }
 
 // ---------------------------------------------------------------------------------------
@@ -591,12 +547,13 @@ static VocabArgs base_args(int bf16_mma, const void *t, const void *wp, const fl
   return a;
 }
 
-hipError_t launch_vocab_threshold(int M, int V, int K, const float *sample, float *thr, hipStream_t st) {
+hipError_t launch_vocab_threshold(int M, int V, int K, const float *sample, float *thr, int *scnt, int B,
+                                  hipStream_t st) {
   if (M == 0) return hipSuccess;
   const int S = vocab_sample_size(V);
   const int Sv = V < S ? V : S;  // entries >= V of the sample are padding
   hipLaunchKernelGGL((vocab_threshold_kernel<kSampleMax / 64>), dim3((M + 3) / 4), dim3(256), 0, st, M, Sv, K,
-                     sample, S, thr);
+                     sample, S, thr, scnt, B);
   return hipGetLastError();
 }
 
@@ -616,31 +573,6 @@ hipError_t launch_vocab(int bf16_mma, const void *t, const void *wp, const float
   a.logits_ld = V;
   a.fixed_ref = fixed_ref;
   return vgo_any(bf16_mma, a, st);
-}
-
-hipError_t launch_vocab_fallback(int bf16_mma, const void *t, const void *wp, const float *bias_pad, int M,
-                                 int V, int E, int K, const float *lse, const float *prev_score, int2 *row_out,
-                                 const int *ovf, hipStream_t st) {
-  if (M == 0) return hipSuccess;
-  VocabArgs a = base_args(bf16_mma, t, wp, bias_pad, M, V, E);
-  const int nfb = (M + 255) / 256;
-#define MT_VF(CT, N)                                                                                          \
-  hipLaunchKernelGGL((vocab_fallback_kernel<CT, N>), dim3(nfb), dim3(256), 0, st, a, K, lse, prev_score, \
-                     row_out, ovf)
-#define MT_VFK(CT)                 \
-  if (K <= 1) MT_VF(CT, 1);        \
-  else if (K <= 2) MT_VF(CT, 2);   \
-  else if (K <= 4) MT_VF(CT, 4);   \
-  else if (K <= 8) MT_VF(CT, 8);   \
-  else MT_VF(CT, 16);
-  if (bf16_mma) {
-    MT_VFK(bf16)
-  } else {
-    MT_VFK(float)
-  }
-#undef MT_VFK
-#undef MT_VF
-  return hipGetLastError();
 }
 
 }  // namespace mt

@@ -335,14 +335,16 @@ def test_abi_errors_on_gpu():
 
 
 def test_candidate_buffer_overflow_falls_back_exactly():
-    """A bias that makes the first vocabulary entries (the threshold sample) very unlikely puts
-    the candidate threshold far below the rest of the vocabulary, so the candidate buffers
-    overflow; the row merge must then recompute the rows and still select exactly."""
+    """A bias that makes the first vocabulary entries (the threshold sample, 2048 entries) very
+    unlikely puts the candidate threshold far below the rest of the vocabulary, so the
+    candidate buffers overflow; the row selection must then recompute the rows and still
+    select exactly.  The recomputation sums each logit in another order than the matrix
+    cores, so its scores match the materialised path to rounding, and its tokens exactly."""
     log("\n[overflow fallback]")
     p = synth.with_sizes(synth.PRESETS["tiny_f32"], V=85000, K=4, B=2)
     w = synth.make_weights(p)
     w["bo"] = np.zeros(p.V, np.float32)
-    w["bo"][:1024] = -50.0
+    w["bo"][:2048] = -50.0
     dec = Decoder.from_preset(p, w)
     ctx, mask, lens = synth.make_source(p)
     dec.set_batch(ctx, mask, p.K)
@@ -352,7 +354,8 @@ def test_candidate_buffer_overflow_falls_back_exactly():
     sc, tk, bp, _ = [x.cpu().numpy() for x in dec.topk(T(score), None)]
     lp = gpu["logp"].cpu().numpy()
     t2, b2, s2 = mtref.topk(p.K, score, lp)
-    assert np.array_equal(tk, t2) and np.array_equal(bp, b2) and np.array_equal(sc, s2)
+    assert np.array_equal(tk, t2) and np.array_equal(bp, b2)
+    assert np.all(np.abs(sc.astype(np.float64) - s2) <= 1e-5 * (1.0 + np.abs(s2)))
     orc = oracle_sentences(oracle_model(p, w), p.K, [0, 1], ctx, mask, tok, src, state, want_alpha=False, taps=False)
     for b in (0, 1):
         rows = slice(b * p.K, (b + 1) * p.K)
