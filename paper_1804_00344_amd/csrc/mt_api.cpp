@@ -181,7 +181,7 @@ std::vector<float> cat(std::initializer_list<std::pair<const float *, int>> part
 
 // ---- workspace ----
 struct WsLayout {
-  size_t gh, s1, g2, c, g3, g4, t, sample, thr, part, cbuf, ccnt, lse, rowc, scand, scnt, total;
+  size_t gh, s1, g2, c, g3, g4, t, sample, thr, part, cbuf, ccnt, lse, rowc, scand, scnt, s1h, ch, sth, total;
   int ntiles, kc, nchunks;
 };
 
@@ -214,6 +214,11 @@ WsLayout ws_layout(const mt_model *m, int B, int K) {
   L.nchunks = std::max(1, std::min(64, (c.V + 2047) / 2048));
   L.scand = take(M * L.nchunks * K * sizeof(int2));
   L.scnt = take((size_t)B * sizeof(int));
+  // bf16 copies of s1, the context and the new state: the A operands of the bf16 products
+  const size_t h16 = m->bf16 ? 2 : 0;
+  L.s1h = take(M * H * h16);
+  L.ch = take(M * C * h16);
+  L.sth = take(M * H * h16);
   L.total = off;
   return L;
 }
@@ -544,28 +549,32 @@ mt_status mt_decoder_step(mt_model *model, int B, int K, int S, const int32_t *p
   LAUNCH(MT_KERNEL_GRU_CELL,
          launch_gru_cell(M, H, model->embx, 3 * H + E, prev_tok, V, gh, 3 * H, state_in, src_row, n_state_rows,
                          model->err, LNon ? ln[0] : nullptr, ln[1], ln[2], ln[3], eps, s1, H,
-                         taps ? taps->s1 : nullptr, st));
-  // s1 [Wa | U2]: attention query and GRU 2 recurrent product
+                         bf ? (bf16 *)(W + L.s1h) : nullptr, taps ? taps->s1 : nullptr, st));
+  // s1 [Wa | U2]: attention query and GRU 2 recurrent product (bf16 models read the bf16 copy
+  // of s1, which holds exactly the values the product would round s1 to)
   GemmProblem p2{};
-  p2.A = s1; p2.a_rows = M; p2.lda = H; p2.a_bf16 = 0;
+  p2.A = bf ? (const void *)(W + L.s1h) : (const void *)s1; p2.a_rows = M; p2.lda = H; p2.a_bf16 = bf;
   p2.Bp = model->w2.p; p2.ldb = model->w2.ldb;
   p2.out = g2; p2.ldc = A + 3 * H; p2.M = M; p2.N = A + 3 * H; p2.K = H;
   LAUNCH(MT_KERNEL_GEMM_S1, launch_gemm(bf, &p2, 1, EPI_STORE, st));
-  LAUNCH(MT_KERNEL_ATTENTION, launch_attention(B, K, S, A, C, pctx, ctx, bf, mask, g2, A + 3 * H, model->va, cc, C,
-                                               attn_out, st));
+  // bf16 models need the context only in bf16 (fp32 too when it is tapped)
+  float *cc32 = (!bf || (taps && taps->c)) ? cc : nullptr;
+  LAUNCH(MT_KERNEL_ATTENTION, launch_attention(B, K, S, A, C, pctx, ctx, bf, mask, g2, A + 3 * H, model->va, cc32, C,
+                                               bf ? (bf16 *)(W + L.ch) : nullptr, attn_out, st));
   if (taps && taps->c) HIP_TRY(hipMemcpyAsync(taps->c, cc, (size_t)M * C * 4, hipMemcpyDeviceToDevice, st));
   // c [W2 | Wt_c] + [b2 | 0]
   GemmProblem p3{};
-  p3.A = cc; p3.a_rows = M; p3.lda = C; p3.a_bf16 = 0;
+  p3.A = bf ? (const void *)(W + L.ch) : (const void *)cc; p3.a_rows = M; p3.lda = C; p3.a_bf16 = bf;
   p3.Bp = model->w3.p; p3.ldb = model->w3.ldb; p3.bias = model->bias3;
   p3.out = g3; p3.ldc = 3 * H + E; p3.M = M; p3.N = 3 * H + E; p3.K = C;
   LAUNCH(MT_KERNEL_GEMM_CTX, launch_gemm(bf, &p3, 1, EPI_STORE, st));
   LAUNCH(MT_KERNEL_GRU_CELL,
          launch_gru_cell(M, H, g3, 3 * H + E, nullptr, M, g2 + A, A + 3 * H, s1, nullptr, M, model->err,
-                         LNon ? ln[4] : nullptr, ln[5], ln[6], ln[7], eps, state_out, H, nullptr, st));
+                         LNon ? ln[4] : nullptr, ln[5], ln[6], ln[7], eps, state_out, H,
+                         bf ? (bf16 *)(W + L.sth) : nullptr, nullptr, st));
   // readout: s Wt_s, then tanh(LN?(s Wt_s + x Wt_y + c Wt_c + bt))
   GemmProblem p4{};
-  p4.A = state_out; p4.a_rows = M; p4.lda = H; p4.a_bf16 = 0;
+  p4.A = bf ? (const void *)(W + L.sth) : (const void *)state_out; p4.a_rows = M; p4.lda = H; p4.a_bf16 = bf;
   p4.Bp = model->w4.p; p4.ldb = model->w4.ldb;
   p4.out = g4; p4.ldc = E; p4.M = M; p4.N = E; p4.K = H;
   LAUNCH(MT_KERNEL_GEMM_READOUT, launch_gemm(bf, &p4, 1, EPI_STORE, st));

@@ -390,11 +390,12 @@ constexpr int kVocabCap = 32;  // candidate buffer entries per (row, chunk, list
 constexpr int kVocabPad = 64;  // vocabulary rows are padded to a multiple of this
 
 // GRU cell for M rows; a row m = aidx[m] (if given), previous state row hidx[m] (if given);
-// out-of-range indices are clamped and flagged in err (bit 0: aidx, bit 1: hidx)
+// out-of-range indices are clamped and flagged in err (bit 0: aidx, bit 1: hidx); out16 (if
+// given) receives a bf16 copy [M][H] of the new state
 hipError_t launch_gru_cell(int M, int H, const float *a, int lda, const int32_t *aidx, int arows,
                            const float *u, int ldu, const float *hsrc, const int32_t *hidx, int hrows,
                            int32_t *err, const float *ga, const float *ba, const float *gu, const float *bu,
-                           float eps, float *out, int ldo, float *tap, hipStream_t st);
+                           float eps, float *out, int ldo, bf16 *out16, float *tap, hipStream_t st);
 
 hipError_t launch_readout(int M, int E, const float *p1, int ld1, const float *p2, int ld2, const int32_t *idx2,
                           int rows2, const float *p3, int ld3, const float *bt, const float *g,
@@ -404,9 +405,10 @@ hipError_t launch_readout(int M, int E, const float *p1, int ld1, const float *p
 hipError_t launch_masked_mean(int B, int S, int Cd, const void *ctx, int ctx_bf16,
                               const float *mask, float *out, hipStream_t st);
 
+// context rows go to ctx_out [M][ldc] fp32 and/or ctx16 [M][Cd] bf16 (either may be NULL)
 hipError_t launch_attention(int B, int K, int S, int A, int Cd, const void *P, const void *Cx,
                             int bf16_io, const float *mask, const float *q, int ldq,
-                            const float *va, float *ctx_out, int ldc, float *alpha_out,
+                            const float *va, float *ctx_out, int ldc, bf16 *ctx16, float *alpha_out,
                             hipStream_t st);
 
 hipError_t launch_lse(int M, int ntiles, const float2 *part, float *lse, float *logits, int V,

@@ -63,6 +63,7 @@ __global__ __launch_bounds__(kT) void gru_cell_kernel(int M, int H, const float 
                                                       const float *__restrict__ gu,
                                                       const float *__restrict__ bu, float eps,
                                                       float *__restrict__ out, int ldo,
+                                                      bf16 *__restrict__ out16,
                                                       float *__restrict__ tap) {
   __shared__ float red[4][12];
   const int m = blockIdx.x;
@@ -147,6 +148,12 @@ __global__ __launch_bounds__(kT) void gru_cell_kernel(int M, int H, const float 
       v[e] = (1.0f - z) * hh + z * h[p][e];
     }
     st4(o + j, v[0], v[1], v[2], v[3]);
+    if (out16) {  // bf16 copy for a following bf16 product (same rounding as its operand staging)
+      bf16 h4[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) h4[e] = to_bf16(v[e]);
+      __builtin_memcpy(out16 + (size_t)m * H + j, h4, sizeof(h4));
+    }
     if (tap) st4(tap + (size_t)m * H + j, v[0], v[1], v[2], v[3]);
   }
 }
@@ -260,16 +267,16 @@ static int gran_for(int n) {  // 16-byte granules per thread for an n-wide row
 hipError_t launch_gru_cell(int M, int H, const float *a, int lda, const int32_t *aidx, int arows,
                            const float *u, int ldu, const float *hsrc, const int32_t *hidx, int hrows,
                            int32_t *err, const float *ga, const float *ba, const float *gu, const float *bu,
-                           float eps, float *out, int ldo, float *tap, hipStream_t st) {
+                           float eps, float *out, int ldo, bf16 *out16, float *tap, hipStream_t st) {
   if (M == 0) return hipSuccess;
   const bool ln = ga != nullptr;
 #define MT_GRU(N)                                                                                        \
   if (ln)                                                                                                \
     hipLaunchKernelGGL((gru_cell_kernel<N, true>), dim3(M), dim3(kT), 0, st, M, H, a, lda, aidx, arows, \
-                       u, ldu, hsrc, hidx, hrows, err, ga, ba, gu, bu, eps, out, ldo, tap);              \
+                       u, ldu, hsrc, hidx, hrows, err, ga, ba, gu, bu, eps, out, ldo, out16, tap);              \
   else                                                                                                   \
     hipLaunchKernelGGL((gru_cell_kernel<N, false>), dim3(M), dim3(kT), 0, st, M, H, a, lda, aidx, arows,\
-                       u, ldu, hsrc, hidx, hrows, err, ga, ba, gu, bu, eps, out, ldo, tap);
+                       u, ldu, hsrc, hidx, hrows, err, ga, ba, gu, bu, eps, out, ldo, out16, tap);
   switch (gran_for(H)) {
     case 1: MT_GRU(1) break;
     case 2: MT_GRU(2) break;
