@@ -34,7 +34,8 @@ mt_status fail(mt_status s, const char *fmt, ...) {
 
 constexpr uint32_t kMagic = 0x4d545350u;  // "MTSP"
 constexpr int kNPad = 256;                // N padding of packed weights (>= any tile BN)
-constexpr int kKPad = 64;                 // K padding (>= any tile BK)
+constexpr int kKPad = 64;                 // K padding of fp32 weights (>= any tile BK)
+constexpr int kKPadFrag = 128;            // K padding of bf16 weights (one LDS stage)
 
 size_t rup(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -118,11 +119,15 @@ struct Seg {
   int ncols;
 };
 
-// packed[n][k] = concat(segments)[k][n], zero padded to [rup(N, kNPad)][rup(K, kKPad)]
+// fp32: packed[n][k] = concat(segments)[k][n], zero padded to [rup(N, kNPad)][rup(K, kKPad)].
+// bf16: the same matrix (K padded to kKPadFrag) in the MFMA fragment order of the bf16 GEMM:
+// 16 bytes for lane l of 32-column block nb and 16-k step ks at ((nb * KSp + ks) * 64 + l) * 16,
+// holding columns nb * 32 + l % 32 and k = ks * 16 + (l / 32) * 8 + 0..7 (KSp = K_pad / 16).
 std::vector<char> pack_host(const std::vector<Seg> &segs, int K, int esize, int *N_out, int *ldb_out) {
   int N = 0;
   for (auto &s : segs) N += s.ncols;
-  const int Np = (int)rup(N, kNPad), Kp = (int)rup(K, kKPad);
+  const int Np = (int)rup(N, kNPad), Kp = (int)rup(K, esize == 2 ? kKPadFrag : kKPad);
+  const int KSp = Kp / 16;
   std::vector<char> buf((size_t)Np * Kp * esize, 0);
   int n0 = 0;
   for (auto &s : segs) {
@@ -131,11 +136,14 @@ std::vector<char> pack_host(const std::vector<Seg> &segs, int K, int esize, int 
         for (int k = kb; k < std::min(K, kb + 64); ++k) {
           const float *src = s.w + (size_t)k * s.ncols;
           for (int n = nb; n < std::min(s.ncols, nb + 64); ++n) {
-            const size_t o = (size_t)(n0 + n) * Kp + k;
-            if (esize == 4)
-              ((float *)buf.data())[o] = src[n];
-            else
+            const int nn = n0 + n;
+            if (esize == 4) {
+              ((float *)buf.data())[(size_t)nn * Kp + k] = src[n];
+            } else {
+              const int lane = (nn & 31) + 32 * ((k & 15) >> 3);
+              const size_t o = ((((size_t)(nn >> 5) * KSp + (k >> 4)) * 64 + lane) * 8) + (k & 7);
               ((uint16_t *)buf.data())[o] = bf16_bits(src[n]);
+            }
           }
         }
     n0 += s.ncols;

@@ -348,8 +348,8 @@ struct GemmProblem {
   int a_rows;             // rows available in A (for the gather clamp)
   int lda;                // elements
   int a_bf16;             // A element type: 0 fp32, 1 bf16
-  const void *Bp;         // packed weights [N_pad][ldb], K contiguous, compute dtype
-  int ldb;                // = K_pad
+  const void *Bp;         // packed weights: fp32 [N_pad][ldb] K contiguous; bf16 MFMA fragment order
+  int ldb;                // = K_pad (a multiple of 128 for bf16)
   const float *bias;      // [N] or NULL
   void *out;              // [M][ldc] (fp32, or bf16 if out_bf16)
   int ldc;
