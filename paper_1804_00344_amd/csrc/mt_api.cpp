@@ -34,7 +34,7 @@ mt_status fail(mt_status s, const char *fmt, ...) {
 
 constexpr uint32_t kMagic = 0x4d545350u;  // "MTSP"
 constexpr int kNPad = 256;                // N padding of packed weights (>= any tile BN)
-constexpr int kKPad = 64;                 // K padding of fp32 weights (>= any tile BK)
+constexpr int kKPad = 64;                 // K padding of fp32 weights (a multiple of 4 k-steps)
 constexpr int kKPadFrag = 128;            // K padding of bf16 weights (one LDS stage)
 
 size_t rup(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -119,10 +119,11 @@ struct Seg {
   int ncols;
 };
 
-// fp32: packed[n][k] = concat(segments)[k][n], zero padded to [rup(N, kNPad)][rup(K, kKPad)].
-// bf16: the same matrix (K padded to kKPadFrag) in the MFMA fragment order of the bf16 GEMM:
-// 16 bytes for lane l of 32-column block nb and 16-k step ks at ((nb * KSp + ks) * 64 + l) * 16,
-// holding columns nb * 32 + l % 32 and k = ks * 16 + (l / 32) * 8 + 0..7 (KSp = K_pad / 16).
+// W = concat(segments) [K][N], zero padded to [rup(K, kKPad or kKPadFrag)][rup(N, kNPad)], in the
+// MFMA fragment order of the GEMM kernels (KSp = K_pad / 16), 16 bytes per lane l of each
+// (column block nb, 16-k step ks) at ((nb * KSp + ks) * 64 + l) * 16:
+//  fp32: 16-column blocks; lane l holds column nb * 16 + l % 16, k = ks * 16 + (l / 16) * 4 + 0..3;
+//  bf16: 32-column blocks; lane l holds column nb * 32 + l % 32, k = ks * 16 + (l / 32) * 8 + 0..7.
 std::vector<char> pack_host(const std::vector<Seg> &segs, int K, int esize, int *N_out, int *ldb_out) {
   int N = 0;
   for (auto &s : segs) N += s.ncols;
@@ -138,7 +139,9 @@ std::vector<char> pack_host(const std::vector<Seg> &segs, int K, int esize, int 
           for (int n = nb; n < std::min(s.ncols, nb + 64); ++n) {
             const int nn = n0 + n;
             if (esize == 4) {
-              ((float *)buf.data())[(size_t)nn * Kp + k] = src[n];
+              const int lane = (nn & 15) + 16 * ((k & 15) >> 2);
+              const size_t o = ((((size_t)(nn >> 4) * KSp + (k >> 4)) * 64 + lane) * 4) + (k & 3);
+              ((float *)buf.data())[o] = src[n];
             } else {
               const int lane = (nn & 31) + 32 * ((k & 15) >> 3);
               const size_t o = ((((size_t)(nn >> 5) * KSp + (k >> 4)) * 64 + lane) * 8) + (k & 7);

@@ -557,6 +557,209 @@ static hipError_t go_wd(const Problems &ps, int nprob, hipStream_t st) {
   return t64 >= 256 ? go_wd_mb<AT, EPI, 2>(ps, nprob, st) : go_wd_mb<AT, EPI, 1>(ps, nprob, st);
 }
 
+// ---------------------------------------------------------------------------------------
+// fp32 operands: one wave per (16 TA) x (16 TB) output tile, both operands straight from global
+// memory (at fp32 rates the MFMAs need only a few bytes per cycle, so no LDS staging).
+//
+// v_mfma_f32_16x16x4_f32 takes one fp32 per lane per operand: A lane l holds row l % 16 and k
+// (l / 16), B lane l holds column l % 16 and k (l / 16).  A 16-byte vector per lane holds the k
+// quadruple 4 (l / 16) + e, e < 4, of one 16-k step and feeds MFMA e, so the four MFMAs of a step
+// cover its 16 k once (the same assignment on both operands).  The weights are packed at load
+// time in that order: for 16-column block nb and 16-k step ks, 64 lanes x 16 bytes at
+// ((nb * KSp + ks) * 64 + lane) * 16, lane l holding W[ks * 16 + (l / 16) * 4 + e][nb * 16 + l % 16]
+// (KSp = K_pad / 16).  The activation vector of lane l is A[row][ks * 16 + (l / 16) * 4 ..], one
+// 16-byte load.  Both come through a register ring refilled D steps ahead.
+//
+// Tiles are sized per launch so that the wave count fits the chip's 1024 SIMDs (go_f32): at these
+// shapes the time is set by the SIMD with the most work.
+template <int TA, int TB, int EPI, int D, int U>
+__global__ __launch_bounds__(256) void gemm_f32_kernel(Problems probs) {
+  const GemmProblem &P = probs.p[blockIdx.z];
+  const int M = pin_s(P.M), N = pin_s(P.N), K = pin_s(P.K), lda = pin_s(P.lda), ldc = pin_s(P.ldc);
+  const int KSp = pin_s(P.ldb) / 16;
+  const int tilesM = (M + 16 * TA - 1) / (16 * TA);
+  const int tilesN = (N + 16 * TB - 1) / (16 * TB);
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int tile = xcd_remap(blockIdx.x, gridDim.x) * 4 + wave;  // four tiles per workgroup
+  if (tile >= tilesM * tilesN) return;
+  const int tm = tile % tilesM, tn = tile / tilesM;  // neighbours share a weight panel
+  const int m0 = tm * 16 * TA, n0 = tn * 16 * TB;
+  const int lr = lane & 15, lk = (lane >> 4) * 4;
+
+  // activation rows of this lane (gathered, clamped; rows past M read row 0, never stored), as
+  // byte offsets into a buffer view of A
+  const __amdgpu_buffer_rsrc_t ars =
+      __builtin_amdgcn_make_buffer_rsrc((void *)P.A, 0, P.a_rows * lda * 4, 0x00020000);
+  int a_off[TA];
+#pragma unroll
+  for (int i = 0; i < TA; ++i) {
+    const int m = m0 + 16 * i + lr;
+    int src = m < M ? m : 0;
+    if (P.a_idx && m < M) {
+      src = P.a_idx[m];
+      if (src < 0 || src >= P.a_rows) {
+        if (P.err) atomicOr(P.err, 1 << P.err_bit);
+        src = src < 0 ? 0 : P.a_rows - 1;
+      }
+    }
+    a_off[i] = src * lda * 4;
+  }
+  const __amdgpu_buffer_rsrc_t wrs =
+      __builtin_amdgcn_make_buffer_rsrc((void *)P.Bp, 0, tilesN * TB * KSp * 1024, 0x00020000);
+  const int wvo = lane * 16;
+  const int wb0 = (n0 >> 4) * KSp * 1024;
+  const int kslast = KSp - 1;
+
+  struct Slot {
+    u32x4 a[TA], b[TB];
+  };
+  Slot ring[D];
+  auto fetch = [&](int ks, Slot &r) {
+    const int kc = ks < kslast ? ks : kslast;  // clamped: in bounds, never used
+    int k = kc * 16 + lk;
+    k = k < K ? k : K - 4;  // past K: the row's last vector (it meets zero weights)
+#pragma unroll
+    for (int i = 0; i < TA; ++i) r.a[i] = __builtin_amdgcn_raw_buffer_load_b128(ars, a_off[i] + k * 4, 0, 0);
+#pragma unroll
+    for (int j = 0; j < TB; ++j) r.b[j] = __builtin_amdgcn_raw_buffer_load_b128(wrs, wvo, wb0 + (j * KSp + kc) * 1024, 0);
+  };
+#pragma unroll
+  for (int d = 0; d < D; ++d) fetch(d, ring[d]);
+
+  f32x4 acc[TA][TB];
+#pragma unroll
+  for (int i = 0; i < TA; ++i)
+#pragma unroll
+    for (int j = 0; j < TB; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // the ring index of step ks is ks % D; the loop advances U steps per iteration (KSp % U == 0,
+  // U a multiple of D).  The compiler drains the memory counter at the loop header, so the
+  // longer the body, the rarer the drain.
+  for (int ks0 = 0; ks0 < KSp; ks0 += U) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int d = u % D;
+      float fa[TA][4], fb[TB][4];
+#pragma unroll
+      for (int i = 0; i < TA; ++i) __builtin_memcpy(fa[i], &ring[d].a[i], 16);
+#pragma unroll
+      for (int j = 0; j < TB; ++j) __builtin_memcpy(fb[j], &ring[d].b[j], 16);
+      // element e of every vector feeds MFMA e; the TA x TB accumulators alternate between
+      // dependent MFMAs
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+#pragma unroll
+        for (int i = 0; i < TA; ++i)
+#pragma unroll
+          for (int j = 0; j < TB; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[i][e], fb[j][e], acc[i][j], 0, 0, 0);
+      // the refill of a slot goes behind the MFMAs that read it (hoisted above them, its loads
+      // would need fresh registers and a wait for every load in flight)
+      __builtin_amdgcn_sched_barrier(0);
+      fetch(ks0 + u + D, ring[d]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+
+  // ---- epilogue: lane holds D[row = 4 * (lane / 16) + r][col = lane % 16] of each 16x16 block;
+  // the bias values are loaded before any store and waited for once ----
+  const int obf = pin_s(P.out_bf16);
+  const float *const biasp = pin_s(P.bias);
+  char *const outp = (char *)pin_s(P.out);
+  float bias[TB];
+#pragma unroll
+  for (int j = 0; j < TB; ++j) {
+    const int col = n0 + 16 * j + lr;
+    bias[j] = biasp ? ((const __attribute__((address_space(1))) float *)biasp)[col < N ? col : N - 1] : 0.f;
+  }
+  __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
+  auto epilogue = [&](auto bf) {
+#pragma unroll
+    for (int j = 0; j < TB; ++j) {
+      const int col = n0 + 16 * j + lr;
+      if (col >= N) continue;
+#pragma unroll
+      for (int i = 0; i < TA; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int row = m0 + 16 * i + (lane >> 4) * 4 + r;
+          if (row >= M) continue;
+          float v = acc[i][j][r] + bias[j];
+          if (EPI == EPI_TANH) v = tanh_fast(v);
+          if constexpr (decltype(bf)::value)
+            ((__attribute__((address_space(1))) bf16 *)outp)[(size_t)row * ldc + col] = to_bf16(v);
+          else
+            ((__attribute__((address_space(1))) float *)outp)[(size_t)row * ldc + col] = v;
+        }
+    }
+  };
+  if (obf)
+    epilogue(std::integral_constant<bool, true>{});
+  else
+    epilogue(std::integral_constant<bool, false>{});
+}
+
+template <int TA, int TB, int EPI>
+static hipError_t go_f32_t(const Problems &ps, int nprob, hipStream_t st) {
+  int maxw = 0;
+  bool deep = TA + TB <= 4;  // ring depth in 16-k steps: 8 for small tiles when it divides the steps
+  bool long16 = true;        // 16 steps per loop iteration
+  for (int i = 0; i < nprob; ++i) {
+    const int w = ((ps.p[i].M + 16 * TA - 1) / (16 * TA)) * ((ps.p[i].N + 16 * TB - 1) / (16 * TB));
+    maxw = w > maxw ? w : maxw;
+    deep = deep && (ps.p[i].ldb / 16) % 8 == 0;
+    long16 = long16 && (ps.p[i].ldb / 16) % 16 == 0;
+  }
+  if (maxw == 0) return hipSuccess;
+  const dim3 grid((maxw + 3) / 4, 1, nprob);
+  if constexpr (TA + TB <= 4) {
+    if (deep && long16) hipLaunchKernelGGL((gemm_f32_kernel<TA, TB, EPI, 8, 16>), grid, dim3(256), 0, st, ps);
+    else if (deep) hipLaunchKernelGGL((gemm_f32_kernel<TA, TB, EPI, 8, 8>), grid, dim3(256), 0, st, ps);
+    else hipLaunchKernelGGL((gemm_f32_kernel<TA, TB, EPI, 4, 4>), grid, dim3(256), 0, st, ps);
+  } else {
+    if (long16) hipLaunchKernelGGL((gemm_f32_kernel<TA, TB, EPI, 4, 16>), grid, dim3(256), 0, st, ps);
+    else hipLaunchKernelGGL((gemm_f32_kernel<TA, TB, EPI, 4, 4>), grid, dim3(256), 0, st, ps);
+  }
+  return hipGetLastError();
+}
+
+// Tile choice: the fewest rounds of waves over the chip's SIMDs, each round costing the tile's
+// MFMA count (TA x TB blocks), among a few shapes with enough accumulators per wave to keep the
+// matrix core busy.
+template <int EPI>
+static hipError_t go_f32(const Problems &ps, int nprob, hipStream_t st) {
+  for (int i = 0; i < nprob; ++i) {
+    const GemmProblem &p = ps.p[i];
+    if (p.ldb % 64 != 0 || p.K > p.ldb || p.K % 4 != 0 || p.lda % 4 != 0) return hipErrorInvalidValue;
+  }
+  static const int shapes[][2] = {{3, 3}, {3, 4}, {3, 5}, {3, 2}, {2, 4}, {4, 4}, {2, 2}, {1, 2}};
+  constexpr int kSimds = 1024;
+  long best = -1;
+  int bi = 0;
+  for (int s = 0; s < 8; ++s) {
+    long w = 0;
+    for (int i = 0; i < nprob; ++i)
+      w += (long)((ps.p[i].M + 16 * shapes[s][0] - 1) / (16 * shapes[s][0])) *
+           ((ps.p[i].N + 16 * shapes[s][1] - 1) / (16 * shapes[s][1]));
+    const long cost = ((w + kSimds - 1) / kSimds) * shapes[s][0] * shapes[s][1];
+    if (best < 0 || cost < best) {
+      best = cost;
+      bi = s;
+    }
+  }
+  switch (bi) {
+    case 0: return go_f32_t<3, 3, EPI>(ps, nprob, st);
+    case 1: return go_f32_t<3, 4, EPI>(ps, nprob, st);
+    case 2: return go_f32_t<3, 5, EPI>(ps, nprob, st);
+    case 3: return go_f32_t<3, 2, EPI>(ps, nprob, st);
+    case 4: return go_f32_t<2, 4, EPI>(ps, nprob, st);
+    case 5: return go_f32_t<4, 4, EPI>(ps, nprob, st);
+    case 6: return go_f32_t<2, 2, EPI>(ps, nprob, st);
+    default: return go_f32_t<1, 2, EPI>(ps, nprob, st);
+  }
+}
+
 template <typename CT, typename AT, int EPI, int BM, int BN>
 static hipError_t go(const Problems &ps, int nprob, hipStream_t st) {
   int maxt = 0;
@@ -595,7 +798,7 @@ hipError_t launch_gemm(int bf16_mma, const GemmProblem *probs, int nprob, Epilog
     ps.p[i] = probs[i];
     if (probs[i].a_bf16 != probs[0].a_bf16 || (probs[i].a_bf16 && !bf16_mma)) return hipErrorInvalidValue;
   }
-  if (!bf16_mma) return go_epi<float, float>(ps, nprob, epi, st);
+  if (!bf16_mma) return epi == EPI_TANH ? go_f32<EPI_TANH>(ps, nprob, st) : go_f32<EPI_STORE>(ps, nprob, st);
   if (probs[0].a_bf16)
     return epi == EPI_TANH ? go_wd<bf16, EPI_TANH>(ps, nprob, st) : go_wd<bf16, EPI_STORE>(ps, nprob, st);
   return epi == EPI_TANH ? go_wd<float, EPI_TANH>(ps, nprob, st) : go_wd<float, EPI_STORE>(ps, nprob, st);
