@@ -36,12 +36,17 @@ constexpr uint32_t kMagic = 0x4d545350u;  // "MTSP"
 constexpr int kNPad = 256;                // N padding of packed weights (>= any tile BN)
 constexpr int kKPad = 64;                 // K padding of fp32 weights (a multiple of 4 k-steps)
 constexpr int kKPadFrag = 128;            // K padding of bf16 weights (one LDS stage)
+// Row counts the products are expected to run at, for the choice of the fp32 fragment form
+// (64 sentences x beam 12, their 5000 or so source positions, the sentences): a model serves
+// any batch, only the speed of other row counts may differ.
+constexpr long kRefRows = 768, kRefCtxRows = 4096, kRefSentences = 64;
 
 size_t rup(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 struct Packed {
   void *p = nullptr;
   int N = 0, K = 0, ldb = 0;
+  int blk = 16;  // fp32: column block width of the fragment order (16 or 32)
 };
 
 struct ProfSlot {
@@ -120,15 +125,15 @@ struct Seg {
 };
 
 // W = concat(segments) [K][N], zero padded to [rup(K, kKPad or kKPadFrag)][rup(N, kNPad)], in the
-// MFMA fragment order of the GEMM kernels (KSp = K_pad / 16), 16 bytes per lane l of each
-// (column block nb, 16-k step ks) at ((nb * KSp + ks) * 64 + l) * 16:
-//  fp32: 16-column blocks; lane l holds column nb * 16 + l % 16, k = ks * 16 + (l / 16) * 4 + 0..3;
-//  bf16: 32-column blocks; lane l holds column nb * 32 + l % 32, k = ks * 16 + (l / 32) * 8 + 0..7.
-std::vector<char> pack_host(const std::vector<Seg> &segs, int K, int esize, int *N_out, int *ldb_out) {
+// MFMA fragment order of the GEMM kernels: 16 bytes per lane l of each (column block nb, k-step
+// ks) at ((nb * KS + ks) * 64 + l) * 16, KS = K_pad / (k per step):
+//  fp32, 16-column blocks, 16-k steps: lane l holds column nb*16 + l%16, k = ks*16 + (l/16)*4 + 0..3;
+//  fp32, 32-column blocks, 8-k steps:  lane l holds column nb*32 + l%32, k = ks*8 + (l/32)*4 + 0..3;
+//  bf16, 32-column blocks, 16-k steps: lane l holds column nb*32 + l%32, k = ks*16 + (l/32)*8 + 0..7.
+std::vector<char> pack_host(const std::vector<Seg> &segs, int K, int esize, int blk, int *N_out, int *ldb_out) {
   int N = 0;
   for (auto &s : segs) N += s.ncols;
   const int Np = (int)rup(N, kNPad), Kp = (int)rup(K, esize == 2 ? kKPadFrag : kKPad);
-  const int KSp = Kp / 16;
   std::vector<char> buf((size_t)Np * Kp * esize, 0);
   int n0 = 0;
   for (auto &s : segs) {
@@ -138,13 +143,17 @@ std::vector<char> pack_host(const std::vector<Seg> &segs, int K, int esize, int 
           const float *src = s.w + (size_t)k * s.ncols;
           for (int n = nb; n < std::min(s.ncols, nb + 64); ++n) {
             const int nn = n0 + n;
-            if (esize == 4) {
+            if (esize == 4 && blk == 32) {
+              const int lane = (nn & 31) + 32 * ((k & 7) >> 2);
+              const size_t o = ((((size_t)(nn >> 5) * (Kp / 8) + (k >> 3)) * 64 + lane) * 4) + (k & 3);
+              ((float *)buf.data())[o] = src[n];
+            } else if (esize == 4) {
               const int lane = (nn & 15) + 16 * ((k & 15) >> 2);
-              const size_t o = ((((size_t)(nn >> 4) * KSp + (k >> 4)) * 64 + lane) * 4) + (k & 3);
+              const size_t o = ((((size_t)(nn >> 4) * (Kp / 16) + (k >> 4)) * 64 + lane) * 4) + (k & 3);
               ((float *)buf.data())[o] = src[n];
             } else {
               const int lane = (nn & 31) + 32 * ((k & 15) >> 3);
-              const size_t o = ((((size_t)(nn >> 5) * KSp + (k >> 4)) * 64 + lane) * 8) + (k & 7);
+              const size_t o = ((((size_t)(nn >> 5) * (Kp / 16) + (k >> 4)) * 64 + lane) * 8) + (k & 7);
               ((uint16_t *)buf.data())[o] = bf16_bits(src[n]);
             }
           }
@@ -166,12 +175,18 @@ mt_status dev_upload(mt_model *m, const void *host, size_t bytes, void **out) {
   return MT_OK;
 }
 
-mt_status upload_packed(mt_model *m, const std::vector<Seg> &segs, int K, Packed *p) {
-  int N = 0, ldb = 0;
-  std::vector<char> buf = pack_host(segs, K, m->esize, &N, &ldb);
+// rows: the row count the product is expected to run at (it picks the fp32 fragment form; any
+// row count computes the same product)
+mt_status upload_packed(mt_model *m, const std::vector<Seg> &segs, int K, long rows, Packed *p) {
+  int N = 0;
+  for (auto &s : segs) N += s.ncols;
+  const int blk = m->esize == 4 ? gemm_f32_weight_block(rows, N, K) : 32;
+  int ldb = 0;
+  std::vector<char> buf = pack_host(segs, K, m->esize, blk, &N, &ldb);
   p->N = N;
   p->K = K;
   p->ldb = ldb;
+  p->blk = blk;
   return dev_upload(m, buf.data(), buf.size(), &p->p);
 }
 
@@ -352,13 +367,13 @@ mt_status mt_load_weights(const mt_config *cfg, const mt_weights *w, mt_model **
   const int E = c.E, H = c.H, A = c.A, V = c.V, C = 2 * c.H;
   mt_status s = MT_OK;
   auto run = [&]() -> mt_status {
-    CHECK(upload_packed(m, {{w->W1, 3 * H}, {w->Wt_y, E}}, E, &m->w1x));
-    CHECK(upload_packed(m, {{w->U1, 3 * H}}, H, &m->w1h));
-    CHECK(upload_packed(m, {{w->Wa, A}, {w->U2, 3 * H}}, H, &m->w2));
-    CHECK(upload_packed(m, {{w->W2, 3 * H}, {w->Wt_c, E}}, C, &m->w3));
-    CHECK(upload_packed(m, {{w->Wt_s, E}}, H, &m->w4));
-    CHECK(upload_packed(m, {{w->Ua, A}}, C, &m->wp));
-    CHECK(upload_packed(m, {{w->Wi, H}}, C, &m->ws0));
+    CHECK(upload_packed(m, {{w->W1, 3 * H}, {w->Wt_y, E}}, E, V, &m->w1x));
+    CHECK(upload_packed(m, {{w->U1, 3 * H}}, H, kRefRows, &m->w1h));
+    CHECK(upload_packed(m, {{w->Wa, A}, {w->U2, 3 * H}}, H, kRefRows, &m->w2));
+    CHECK(upload_packed(m, {{w->W2, 3 * H}, {w->Wt_c, E}}, C, kRefRows, &m->w3));
+    CHECK(upload_packed(m, {{w->Wt_s, E}}, H, kRefRows, &m->w4));
+    CHECK(upload_packed(m, {{w->Ua, A}}, C, kRefCtxRows, &m->wp));
+    CHECK(upload_packed(m, {{w->Wi, H}}, C, kRefSentences, &m->ws0));
     {  // output layer: Wo^T rows (or emb rows when tied) in MFMA fragment order
       std::vector<char> buf(vocab_pack_bytes(m->bf16, V, E));
       vocab_pack_host(m->bf16, V, E, c.tied_output ? w->emb : w->Wo, c.tied_output, buf.data());
@@ -368,7 +383,7 @@ mt_status mt_load_weights(const mt_config *cfg, const mt_weights *w, mt_model **
       for (int e = 0; e < E; ++e)
         for (int v = 0; v < S && v < V; ++v)
           ws[(size_t)e * S + v] = c.tied_output ? w->emb[(size_t)v * E + e] : w->Wo[(size_t)e * V + v];
-      CHECK(upload_packed(m, {{ws.data(), S}}, E, &m->wsamp));
+      CHECK(upload_packed(m, {{ws.data(), S}}, E, kRefRows, &m->wsamp));
       std::vector<float> bp((V + kVocabPad - 1) / kVocabPad * kVocabPad, -INFINITY);
       std::copy(w->bo, w->bo + V, bp.begin());
       CHECK(upload_vec(m, bp, &m->bo_pad));
@@ -427,7 +442,7 @@ mt_status mt_load_weights(const mt_config *cfg, const mt_weights *w, mt_model **
       CHECK(dev_upload(m, nullptr, (size_t)V * (3 * H + E) * sizeof(float), (void **)&m->embx));
       GemmProblem p{};
       p.A = m->emb; p.a_rows = V; p.lda = E; p.a_bf16 = 0;
-      p.Bp = m->w1x.p; p.ldb = m->w1x.ldb; p.bias = m->bias1x;
+      p.Bp = m->w1x.p; p.ldb = m->w1x.ldb; p.wblk = m->w1x.blk; p.bias = m->bias1x;
       p.out = m->embx; p.ldc = 3 * H + E; p.out_bf16 = 0;
       p.M = V; p.N = 3 * H + E; p.K = E;
       HIP_TRY(launch_gemm(m->bf16, &p, 1, EPI_STORE, nullptr));
@@ -488,14 +503,14 @@ mt_status mt_precompute_ctx(mt_model *model, int B, int S, const void *ctx, cons
   float *cbar = (float *)ws;
   GemmProblem p{};
   p.A = ctx; p.a_idx = nullptr; p.a_rows = B * S; p.lda = C; p.a_bf16 = model->bf16;
-  p.Bp = model->wp.p; p.ldb = model->wp.ldb; p.bias = model->ba;
+  p.Bp = model->wp.p; p.ldb = model->wp.ldb; p.wblk = model->wp.blk; p.bias = model->ba;
   p.out = pctx_out; p.ldc = A; p.out_bf16 = model->bf16;
   p.M = B * S; p.N = A; p.K = C; p.err = nullptr; p.err_bit = 0;
   LAUNCH(MT_KERNEL_PRECOMPUTE, launch_gemm(model->bf16, &p, 1, EPI_STORE, st));
   LAUNCH(MT_KERNEL_PRECOMPUTE, launch_masked_mean(B, S, C, ctx, model->bf16, mask, cbar, st));
   GemmProblem q{};
   q.A = cbar; q.a_rows = B; q.lda = C; q.a_bf16 = 0;
-  q.Bp = model->ws0.p; q.ldb = model->ws0.ldb; q.bias = model->bi;
+  q.Bp = model->ws0.p; q.ldb = model->ws0.ldb; q.wblk = model->ws0.blk; q.bias = model->bi;
   q.out = s0_out; q.ldc = H; q.out_bf16 = 0;
   q.M = B; q.N = H; q.K = C;
   LAUNCH(MT_KERNEL_PRECOMPUTE, launch_gemm(model->bf16, &q, 1, EPI_TANH, st));
@@ -553,7 +568,7 @@ mt_status mt_decoder_step(mt_model *model, int B, int K, int S, const int32_t *p
   // from the precomputed x [W1 | Wt_y] + [b1 | 0] table
   GemmProblem p1{};
   p1.A = state_in; p1.a_idx = src_row; p1.a_rows = n_state_rows; p1.lda = H; p1.a_bf16 = 0;
-  p1.Bp = model->w1h.p; p1.ldb = model->w1h.ldb; p1.bias = nullptr;
+  p1.Bp = model->w1h.p; p1.ldb = model->w1h.ldb; p1.wblk = model->w1h.blk; p1.bias = nullptr;
   p1.out = gh; p1.ldc = 3 * H; p1.M = M; p1.N = 3 * H; p1.K = H;
   p1.err = model->err; p1.err_bit = 1;
   LAUNCH(MT_KERNEL_GEMM_GRU1, launch_gemm(bf, &p1, 1, EPI_STORE, st));
@@ -565,7 +580,7 @@ mt_status mt_decoder_step(mt_model *model, int B, int K, int S, const int32_t *p
   // of s1, which holds exactly the values the product would round s1 to)
   GemmProblem p2{};
   p2.A = bf ? (const void *)(W + L.s1h) : (const void *)s1; p2.a_rows = M; p2.lda = H; p2.a_bf16 = bf;
-  p2.Bp = model->w2.p; p2.ldb = model->w2.ldb;
+  p2.Bp = model->w2.p; p2.ldb = model->w2.ldb; p2.wblk = model->w2.blk;
   p2.out = g2; p2.ldc = A + 3 * H; p2.M = M; p2.N = A + 3 * H; p2.K = H;
   LAUNCH(MT_KERNEL_GEMM_S1, launch_gemm(bf, &p2, 1, EPI_STORE, st));
   // bf16 models need the context only in bf16 (fp32 too when it is tapped)
@@ -576,7 +591,7 @@ mt_status mt_decoder_step(mt_model *model, int B, int K, int S, const int32_t *p
   // c [W2 | Wt_c] + [b2 | 0]
   GemmProblem p3{};
   p3.A = bf ? (const void *)(W + L.ch) : (const void *)cc; p3.a_rows = M; p3.lda = C; p3.a_bf16 = bf;
-  p3.Bp = model->w3.p; p3.ldb = model->w3.ldb; p3.bias = model->bias3;
+  p3.Bp = model->w3.p; p3.ldb = model->w3.ldb; p3.wblk = model->w3.blk; p3.bias = model->bias3;
   p3.out = g3; p3.ldc = 3 * H + E; p3.M = M; p3.N = 3 * H + E; p3.K = C;
   LAUNCH(MT_KERNEL_GEMM_CTX, launch_gemm(bf, &p3, 1, EPI_STORE, st));
   LAUNCH(MT_KERNEL_GRU_CELL,
@@ -586,7 +601,7 @@ mt_status mt_decoder_step(mt_model *model, int B, int K, int S, const int32_t *p
   // readout: s Wt_s, then tanh(LN?(s Wt_s + x Wt_y + c Wt_c + bt))
   GemmProblem p4{};
   p4.A = bf ? (const void *)(W + L.sth) : (const void *)state_out; p4.a_rows = M; p4.lda = H; p4.a_bf16 = bf;
-  p4.Bp = model->w4.p; p4.ldb = model->w4.ldb;
+  p4.Bp = model->w4.p; p4.ldb = model->w4.ldb; p4.wblk = model->w4.blk;
   p4.out = g4; p4.ldc = E; p4.M = M; p4.N = E; p4.K = H;
   LAUNCH(MT_KERNEL_GEMM_READOUT, launch_gemm(bf, &p4, 1, EPI_STORE, st));
   LAUNCH(MT_KERNEL_READOUT, launch_readout(M, E, g4, E, model->embx + 3 * H, 3 * H + E, prev_tok, V, g3 + 3 * H,
@@ -599,7 +614,7 @@ mt_status mt_decoder_step(mt_model *model, int B, int K, int S, const int32_t *p
     const int S = vocab_sample_size(V);
     GemmProblem ps{};
     ps.A = t; ps.a_rows = M; ps.lda = E; ps.a_bf16 = bf;
-    ps.Bp = model->wsamp.p; ps.ldb = model->wsamp.ldb; ps.bias = model->bo_pad;
+    ps.Bp = model->wsamp.p; ps.ldb = model->wsamp.ldb; ps.wblk = model->wsamp.blk; ps.bias = model->bo_pad;
     ps.out = W + L.sample; ps.ldc = S; ps.M = M; ps.N = S; ps.K = E;
     LAUNCH(MT_KERNEL_VOCAB_THRESHOLD, launch_gemm(bf, &ps, 1, EPI_STORE, st));
     LAUNCH(MT_KERNEL_VOCAB_THRESHOLD, launch_vocab_threshold(M, V, K, (const float *)(W + L.sample),

@@ -275,30 +275,43 @@ static hipError_t go_wd(const Problems &ps, int nprob, hipStream_t st) {
 }
 
 // ---------------------------------------------------------------------------------------
-// fp32 operands: (16 TA) x (16 TB) output tiles, each computed by S waves of one workgroup that
+// fp32 operands: (BLK TA) x (BLK TB) output tiles, each computed by S waves of one workgroup that
 // split its k-steps and add their partial sums through LDS; both operands straight from global
 // memory (at fp32 rates the MFMAs need only a few bytes per cycle, so no LDS staging).
 //
-// v_mfma_f32_16x16x4_f32 takes one fp32 per lane per operand: A lane l holds row l % 16 and k
-// (l / 16), B lane l holds column l % 16 and k (l / 16).  A 16-byte vector per lane holds the k
-// quadruple 4 (l / 16) + e, e < 4, of one 16-k step and feeds MFMA e, so the four MFMAs of a step
-// cover its 16 k once (the same assignment on both operands).  The weights are packed in that
-// order: for 16-column block nb and 16-k step ks, 64 lanes x 16 bytes at
-// ((nb * KSp + ks) * 64 + lane) * 16, lane l holding W[ks * 16 + (l / 16) * 4 + e][nb * 16 + l % 16]
-// (KSp = K_pad / 16).  The activation vector of lane l is A[row][ks * 16 + (l / 16) * 4 ..], one
-// 16-byte load.  Both come through a register ring refilled D steps ahead.
+// BLK = 16: v_mfma_f32_16x16x4_f32 takes one fp32 per lane per operand, A lane l holding row
+// l % 16 and k (l / 16), B lane l column l % 16 and k (l / 16).  A 16-byte vector per lane holds
+// the k quadruple 4 (l / 16) + e, e < 4, of one 16-k step and feeds MFMA e, so the four MFMAs of
+// a step cover its 16 k once (the same assignment on both operands).
+// BLK = 32: v_mfma_f32_32x32x2f32, A lane l holding row l % 32 and k (l / 32); a 16-byte vector
+// holds k = 4 (l / 32) + e of one 8-k step, again feeding MFMA e.  This form sustains a higher
+// fraction of the matrix core's rate (86% against 74% in pure-MFMA loops, about 5% more in this
+// kernel), at the price of coarser tiles.
+// The weights are packed in the order of their form (mt_load_weights picks it per matrix): for
+// BLK-column block nb and step ks, 64 lanes x 16 bytes at ((nb * KS + ks) * 64 + lane) * 16
+// (KS = K_pad / (256 / BLK)).  The activation vector of lane l is A[row][step k0 + its k
+// quadruple], one 16-byte load.  Both come through a register ring refilled D steps ahead.
 //
 // Tile shape and split are chosen per launch (go_f32) so that the waves spread evenly over the
 // chip's 1024 SIMDs: at these shapes the time is set by the SIMD with the most work.
-template <int TA, int TB, int S, int EPI, int D, int U>
+template <int BLK>
+struct F32Form {
+  static constexpr int KSTEP = 256 / BLK;   // k per step (one 16-byte vector per lane)
+  static constexpr int NACC = BLK * BLK / 64;  // accumulator registers per lane per block
+  static constexpr int HALF = 64 / BLK;     // lane groups of the k quadruples
+};
+
+template <int BLK, int TA, int TB, int S, int EPI, int D, int U>
 __global__ __launch_bounds__(256) void gemm_f32_kernel(Problems probs) {
+  using F = F32Form<BLK>;
+  typedef __attribute__((__vector_size__(F::NACC * sizeof(float)))) float accv;
   constexpr int TPB = 4 / S;  // tiles per workgroup (four waves)
-  __shared__ __attribute__((aligned(16))) float red[S > 1 ? TPB * (S - 1) * TA * TB * 4 * 64 : 1];
+  __shared__ __attribute__((aligned(16))) float red[S > 1 ? TPB * (S - 1) * TA * TB * F::NACC * 64 : 1];
   const GemmProblem &P = probs.p[blockIdx.z];
   const int M = pin_s(P.M), N = pin_s(P.N), K = pin_s(P.K), lda = pin_s(P.lda), ldc = pin_s(P.ldc);
-  const int KSp = pin_s(P.ldb) / 16;
-  const int tilesM = (M + 16 * TA - 1) / (16 * TA);
-  const int tilesN = (N + 16 * TB - 1) / (16 * TB);
+  const int KSp = pin_s(P.ldb) / F::KSTEP;
+  const int tilesM = (M + BLK * TA - 1) / (BLK * TA);
+  const int tilesN = (N + BLK * TB - 1) / (BLK * TB);
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int part = wave % S, slot_t = wave / S;
@@ -307,8 +320,8 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(Problems probs) {
   const bool live = tile < tilesM * tilesN;
   const int tl = live ? tile : 0;
   const int tm = tl % tilesM, tn = tl / tilesM;  // neighbours share a weight panel
-  const int m0 = tm * 16 * TA, n0 = tn * 16 * TB;
-  const int lr = lane & 15, lk = (lane >> 4) * 4;
+  const int m0 = tm * BLK * TA, n0 = tn * BLK * TB;
+  const int lr = lane & (BLK - 1), lk = (lane / BLK) * 4;
   const int ks_begin = part * (KSp / S), ks_end = ks_begin + KSp / S;
 
   // activation rows of this lane (gathered, clamped; rows past M read row 0, never stored), as
@@ -318,7 +331,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(Problems probs) {
   int a_off[TA];
 #pragma unroll
   for (int i = 0; i < TA; ++i) {
-    const int m = m0 + 16 * i + lr;
+    const int m = m0 + BLK * i + lr;
     int src = m < M ? m : 0;
     if (live && P.a_idx && m < M) {
       src = P.a_idx[m];
@@ -329,13 +342,13 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(Problems probs) {
     }
     a_off[i] = src * lda * 4;
   }
-  // the view covers the 16-column blocks that exist (the packing pads N further, to N_pad, but a
+  // the view covers the column blocks that exist (the packing pads N further, to N_pad, but a
   // tile may reach past even that): fragments of blocks beyond N read as zero and their
   // columns are never stored
   const __amdgpu_buffer_rsrc_t wrs =
-      __builtin_amdgcn_make_buffer_rsrc((void *)P.Bp, 0, (N + 15) / 16 * KSp * 1024, 0x00020000);
+      __builtin_amdgcn_make_buffer_rsrc((void *)P.Bp, 0, (N + BLK - 1) / BLK * KSp * 1024, 0x00020000);
   const int wvo = lane * 16;
-  const int wb0 = (n0 >> 4) * KSp * 1024;
+  const int wb0 = (n0 / BLK) * KSp * 1024;
   const int kslast = ks_end - 1;
 
   struct Slot {
@@ -344,7 +357,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(Problems probs) {
   Slot ring[D];
   auto fetch = [&](int ks, Slot &r) {
     const int kc = ks < kslast ? ks : kslast;  // clamped: in bounds, never used
-    int k = kc * 16 + lk;
+    int k = kc * F::KSTEP + lk;
     k = k < K ? k : K - 4;  // past K: the row's last vector (it meets zero weights)
 #pragma unroll
     for (int i = 0; i < TA; ++i) r.a[i] = __builtin_amdgcn_raw_buffer_load_b128(ars, a_off[i] + k * 4, 0, 0);
@@ -354,11 +367,13 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(Problems probs) {
 #pragma unroll
   for (int d = 0; d < D; ++d) fetch(ks_begin + d, ring[d]);
 
-  f32x4 acc[TA][TB];
+  accv acc[TA][TB];
 #pragma unroll
   for (int i = 0; i < TA; ++i)
 #pragma unroll
-    for (int j = 0; j < TB; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < TB; ++j)
+#pragma unroll
+      for (int r = 0; r < F::NACC; ++r) acc[i][j][r] = 0.f;
 
   // the ring index of step ks is (ks - ks_begin) % D; the loop advances U steps per iteration
   // ((KSp / S) % U == 0, U a multiple of D).  The compiler drains the memory counter at the loop
@@ -379,8 +394,12 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(Problems probs) {
 #pragma unroll
         for (int i = 0; i < TA; ++i)
 #pragma unroll
-          for (int j = 0; j < TB; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[i][e], fb[j][e], acc[i][j], 0, 0, 0);
+          for (int j = 0; j < TB; ++j) {
+            if constexpr (BLK == 16)
+              acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[i][e], fb[j][e], acc[i][j], 0, 0, 0);
+            else
+              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[i][e], fb[j][e], acc[i][j], 0, 0, 0);
+          }
       // the refill of a slot goes behind the MFMAs that read it (hoisted above them, its loads
       // would need fresh registers and a wait for every load in flight)
       __builtin_amdgcn_sched_barrier(0);
@@ -391,52 +410,54 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(Problems probs) {
 
   // ---- the split's partial sums: parts 1.. write theirs, part 0 adds them in part order ----
   if constexpr (S > 1) {
-    float *mine = red + (size_t)((slot_t * (S - 1) + (part > 0 ? part - 1 : 0)) * TA * TB * 4) * 64;
+    constexpr int PER = TA * TB * F::NACC;
     if (part > 0) {
+      float *mine = red + (size_t)((slot_t * (S - 1) + part - 1) * PER) * 64;
 #pragma unroll
       for (int i = 0; i < TA; ++i)
 #pragma unroll
         for (int j = 0; j < TB; ++j)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) mine[((i * TB + j) * 4 + r) * 64 + lane] = acc[i][j][r];
+          for (int r = 0; r < F::NACC; ++r) mine[((i * TB + j) * F::NACC + r) * 64 + lane] = acc[i][j][r];
     }
     __syncthreads();
     if (part > 0) return;
 #pragma unroll
     for (int q = 1; q < S; ++q) {
-      const float *o = red + (size_t)((slot_t * (S - 1) + q - 1) * TA * TB * 4) * 64;
+      const float *o = red + (size_t)((slot_t * (S - 1) + q - 1) * PER) * 64;
 #pragma unroll
       for (int i = 0; i < TA; ++i)
 #pragma unroll
         for (int j = 0; j < TB; ++j)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) acc[i][j][r] += o[((i * TB + j) * 4 + r) * 64 + lane];
+          for (int r = 0; r < F::NACC; ++r) acc[i][j][r] += o[((i * TB + j) * F::NACC + r) * 64 + lane];
     }
   }
   if (!live) return;
 
-  // ---- epilogue: lane holds D[row = 4 * (lane / 16) + r][col = lane % 16] of each 16x16 block;
-  // the bias values are loaded before any store and waited for once ----
+  // ---- epilogue: lane holds D[row][col = lane % BLK] of each block, row = 4 * (lane / 16) + r
+  // (BLK 16) or 8 * (r / 4) + 4 * (lane / 32) + r % 4 (BLK 32); the bias values are loaded before
+  // any store and waited for once ----
   const int obf = pin_s(P.out_bf16);
   const float *const biasp = pin_s(P.bias);
   char *const outp = (char *)pin_s(P.out);
   float bias[TB];
 #pragma unroll
   for (int j = 0; j < TB; ++j) {
-    const int col = n0 + 16 * j + lr;
+    const int col = n0 + BLK * j + lr;
     bias[j] = biasp ? ((const __attribute__((address_space(1))) float *)biasp)[col < N ? col : N - 1] : 0.f;
   }
   __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
   auto epilogue = [&](auto bf) {
 #pragma unroll
     for (int j = 0; j < TB; ++j) {
-      const int col = n0 + 16 * j + lr;
+      const int col = n0 + BLK * j + lr;
       if (col >= N) continue;
 #pragma unroll
       for (int i = 0; i < TA; ++i)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int row = m0 + 16 * i + (lane >> 4) * 4 + r;
+        for (int r = 0; r < F::NACC; ++r) {
+          const int row = m0 + BLK * i + (BLK == 16 ? (lane >> 4) * 4 + r : 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3));
           if (row >= M) continue;
           float v = acc[i][j][r] + bias[j];
           if (EPI == EPI_TANH) v = tanh_fast(v);
@@ -453,15 +474,15 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(Problems probs) {
     epilogue(std::integral_constant<bool, false>{});
 }
 
-template <int TA, int TB, int S, int EPI>
+template <int BLK, int TA, int TB, int S, int EPI>
 static hipError_t go_f32_t(const Problems &ps, int nprob, hipStream_t st) {
   int maxw = 0;
-  bool deep = TA + TB <= 4;  // ring depth in 16-k steps: 8 for small tiles when it divides the steps
+  bool deep = TA + TB <= 4;  // ring depth in steps: 8 for small tiles when it divides the steps
   bool long16 = true;        // 16 steps per loop iteration
   for (int i = 0; i < nprob; ++i) {
-    const int w = ((ps.p[i].M + 16 * TA - 1) / (16 * TA)) * ((ps.p[i].N + 16 * TB - 1) / (16 * TB));
+    const int w = ((ps.p[i].M + BLK * TA - 1) / (BLK * TA)) * ((ps.p[i].N + BLK * TB - 1) / (BLK * TB));
     maxw = w > maxw ? w : maxw;
-    const int steps = ps.p[i].ldb / 16 / S;
+    const int steps = ps.p[i].ldb / F32Form<BLK>::KSTEP / S;
     deep = deep && steps % 8 == 0;
     long16 = long16 && steps % 16 == 0;
   }
@@ -469,66 +490,102 @@ static hipError_t go_f32_t(const Problems &ps, int nprob, hipStream_t st) {
   constexpr int TPB = 4 / S;
   const dim3 grid((maxw + TPB - 1) / TPB, 1, nprob);
   if constexpr (TA + TB <= 4) {
-    if (deep && long16) hipLaunchKernelGGL((gemm_f32_kernel<TA, TB, S, EPI, 8, 16>), grid, dim3(256), 0, st, ps);
-    else if (deep) hipLaunchKernelGGL((gemm_f32_kernel<TA, TB, S, EPI, 8, 8>), grid, dim3(256), 0, st, ps);
-    else hipLaunchKernelGGL((gemm_f32_kernel<TA, TB, S, EPI, 4, 4>), grid, dim3(256), 0, st, ps);
+    if (deep && long16) hipLaunchKernelGGL((gemm_f32_kernel<BLK, TA, TB, S, EPI, 8, 16>), grid, dim3(256), 0, st, ps);
+    else if (deep) hipLaunchKernelGGL((gemm_f32_kernel<BLK, TA, TB, S, EPI, 8, 8>), grid, dim3(256), 0, st, ps);
+    else hipLaunchKernelGGL((gemm_f32_kernel<BLK, TA, TB, S, EPI, 4, 4>), grid, dim3(256), 0, st, ps);
   } else {
-    if (long16) hipLaunchKernelGGL((gemm_f32_kernel<TA, TB, S, EPI, 4, 16>), grid, dim3(256), 0, st, ps);
-    else hipLaunchKernelGGL((gemm_f32_kernel<TA, TB, S, EPI, 4, 4>), grid, dim3(256), 0, st, ps);
+    if (long16) hipLaunchKernelGGL((gemm_f32_kernel<BLK, TA, TB, S, EPI, 4, 16>), grid, dim3(256), 0, st, ps);
+    else hipLaunchKernelGGL((gemm_f32_kernel<BLK, TA, TB, S, EPI, 4, 4>), grid, dim3(256), 0, st, ps);
   }
   return hipGetLastError();
 }
 
-// Tile choice: per shape (TA x TB blocks, k split S) the SIMD with the most work receives
-// ceil(waves / 1024) waves of TA * TB / S block-steps each.  Measured at the decoder's shapes:
-// a k split costs a little more than the same work unsplit (its partial sums and the second
-// ring fill), fewer than 6 accumulators leave dependent MFMAs too close together, and between
-// equal costs the shape with more waves hides latency better.  A split needs at least 4
-// k-steps per part.
-template <int EPI>
-static hipError_t go_f32(const Problems &ps, int nprob, hipStream_t st) {
-  int minsteps = 1 << 30;
-  for (int i = 0; i < nprob; ++i) {
-    const GemmProblem &p = ps.p[i];
-    if (p.ldb % 64 != 0 || p.K > p.ldb || p.K % 4 != 0 || p.lda % 4 != 0) return hipErrorInvalidValue;
-    minsteps = p.ldb / 16 < minsteps ? p.ldb / 16 : minsteps;
-  }
-  struct Shape {
-    int ta, tb, s;
-  };
-  static const Shape shapes[] = {{3, 3, 1}, {3, 4, 1}, {3, 5, 1}, {3, 2, 1}, {2, 4, 1}, {1, 2, 1},
-                                 {3, 3, 2}, {3, 4, 2}, {3, 5, 2}, {3, 2, 2}, {1, 2, 4}};
-  constexpr int kSimds = 1024, kShapes = sizeof(shapes) / sizeof(shapes[0]);
+// Tile shapes per form: TA x TB blocks of BLK x BLK, k split S.
+struct F32Shape {
+  int ta, tb, s;
+};
+static const F32Shape kShapes16[] = {{3, 3, 1}, {3, 4, 1}, {3, 5, 1}, {3, 2, 1}, {2, 4, 1}, {1, 2, 1},
+                                     {3, 3, 2}, {3, 4, 2}, {3, 5, 2}, {3, 2, 2}, {1, 2, 4}};
+static const F32Shape kShapes32[] = {{1, 3, 1}, {2, 2, 1}, {1, 4, 1}, {2, 3, 1}, {1, 2, 1}, {1, 2, 2}};
+
+// Cost of the best shape of a form for (rows, columns, k-steps): the SIMD with the most work
+// receives ceil(waves / 1024) waves of TA * TB / S block-steps each, counted in 16x16x4 MFMA
+// time (a 32 x 32 block-step is four 16 x 16 ones at the 32x32x2 form's better rate: 0.95 of
+// their time in this kernel at the decoder's shapes).  Also measured there: a k split costs a little more than the same
+// work unsplit (its partial sums and the second ring fill), fewer than 6 accumulators leave
+// dependent 16x16x4 MFMAs too close together, and between equal costs the shape with more
+// waves hides latency better.  A split needs at least 4 steps per part.
+static double f32_best(int blk, const long *rows, const long *cols, int nprob, int steps, int *which) {
+  const F32Shape *sh = blk == 16 ? kShapes16 : kShapes32;
+  const int n = blk == 16 ? (int)(sizeof(kShapes16) / sizeof(kShapes16[0])) : (int)(sizeof(kShapes32) / sizeof(kShapes32[0]));
   double best = -1.0;
   long best_w = 0;
-  int bi = 0;
-  for (int s = 0; s < kShapes; ++s) {
-    const Shape &h = shapes[s];
-    if (minsteps / h.s < 4 || minsteps % (4 * h.s) != 0) continue;
+  *which = 0;
+  for (int s = 0; s < n; ++s) {
+    const F32Shape &h = sh[s];
+    if (steps / h.s < 4 || steps % (4 * h.s) != 0) continue;
     long w = 0;
-    for (int i = 0; i < nprob; ++i)
-      w += (long)((ps.p[i].M + 16 * h.ta - 1) / (16 * h.ta)) * ((ps.p[i].N + 16 * h.tb - 1) / (16 * h.tb));
+    for (int i = 0; i < nprob; ++i) w += ((rows[i] + blk * h.ta - 1) / (blk * h.ta)) * ((cols[i] + blk * h.tb - 1) / (blk * h.tb));
     w *= h.s;
-    const long per = (w + kSimds - 1) / kSimds;
-    const double cost = (double)per * h.ta * h.tb / h.s * (h.s > 1 ? 1.05 : 1.0) / (h.ta * h.tb >= 6 ? 1.0 : 0.6);
+    const long per = (w + 1023) / 1024;
+    double cost = (double)per * h.ta * h.tb / h.s * (h.s > 1 ? 1.05 : 1.0);
+    if (blk == 16) cost /= h.ta * h.tb >= 6 ? 1.0 : 0.6;
+    else cost *= 4 * 0.95;
     if (best < 0 || cost < best - 1e-9 || (cost < best + 1e-9 && w > best_w)) {
       best = cost;
       best_w = w;
-      bi = s;
+      *which = s;
+    }
+  }
+  return best;
+}
+
+int gemm_f32_weight_block(long rows, long N, long K) {
+  const long kp = (K + 63) / 64 * 64;
+  int w16, w32;
+  const double c16 = f32_best(16, &rows, &N, 1, (int)(kp / 16), &w16);
+  const double c32 = f32_best(32, &rows, &N, 1, (int)(kp / 8), &w32);
+  return (c32 >= 0 && c32 < c16) ? 32 : 16;
+}
+
+template <int EPI>
+static hipError_t go_f32(const Problems &ps, int nprob, hipStream_t st) {
+  const int blk = ps.p[0].wblk == 32 ? 32 : 16;
+  int minsteps = 1 << 30;
+  long rows[2], cols[2];
+  for (int i = 0; i < nprob; ++i) {
+    const GemmProblem &p = ps.p[i];
+    if (p.ldb % 64 != 0 || p.K > p.ldb || p.K % 4 != 0 || p.lda % 4 != 0) return hipErrorInvalidValue;
+    if ((p.wblk == 32 ? 32 : 16) != blk) return hipErrorInvalidValue;
+    const int steps = p.ldb / F32Form<16>::KSTEP * (blk == 32 ? 2 : 1);
+    minsteps = steps < minsteps ? steps : minsteps;
+    rows[i] = p.M;
+    cols[i] = p.N;
+  }
+  int bi = 0;
+  if (f32_best(blk, rows, cols, nprob, minsteps, &bi) < 0) return hipErrorInvalidValue;
+  if (blk == 32) {
+    switch (bi) {
+      case 0: return go_f32_t<32, 1, 3, 1, EPI>(ps, nprob, st);
+      case 1: return go_f32_t<32, 2, 2, 1, EPI>(ps, nprob, st);
+      case 2: return go_f32_t<32, 1, 4, 1, EPI>(ps, nprob, st);
+      case 3: return go_f32_t<32, 2, 3, 1, EPI>(ps, nprob, st);
+      case 4: return go_f32_t<32, 1, 2, 1, EPI>(ps, nprob, st);
+      default: return go_f32_t<32, 1, 2, 2, EPI>(ps, nprob, st);
     }
   }
   switch (bi) {
-    case 0: return go_f32_t<3, 3, 1, EPI>(ps, nprob, st);
-    case 1: return go_f32_t<3, 4, 1, EPI>(ps, nprob, st);
-    case 2: return go_f32_t<3, 5, 1, EPI>(ps, nprob, st);
-    case 3: return go_f32_t<3, 2, 1, EPI>(ps, nprob, st);
-    case 4: return go_f32_t<2, 4, 1, EPI>(ps, nprob, st);
-    case 5: return go_f32_t<1, 2, 1, EPI>(ps, nprob, st);
-    case 6: return go_f32_t<3, 3, 2, EPI>(ps, nprob, st);
-    case 7: return go_f32_t<3, 4, 2, EPI>(ps, nprob, st);
-    case 8: return go_f32_t<3, 5, 2, EPI>(ps, nprob, st);
-    case 9: return go_f32_t<3, 2, 2, EPI>(ps, nprob, st);
-    default: return go_f32_t<1, 2, 4, EPI>(ps, nprob, st);
+    case 0: return go_f32_t<16, 3, 3, 1, EPI>(ps, nprob, st);
+    case 1: return go_f32_t<16, 3, 4, 1, EPI>(ps, nprob, st);
+    case 2: return go_f32_t<16, 3, 5, 1, EPI>(ps, nprob, st);
+    case 3: return go_f32_t<16, 3, 2, 1, EPI>(ps, nprob, st);
+    case 4: return go_f32_t<16, 2, 4, 1, EPI>(ps, nprob, st);
+    case 5: return go_f32_t<16, 1, 2, 1, EPI>(ps, nprob, st);
+    case 6: return go_f32_t<16, 3, 3, 2, EPI>(ps, nprob, st);
+    case 7: return go_f32_t<16, 3, 4, 2, EPI>(ps, nprob, st);
+    case 8: return go_f32_t<16, 3, 5, 2, EPI>(ps, nprob, st);
+    case 9: return go_f32_t<16, 3, 2, 2, EPI>(ps, nprob, st);
+    default: return go_f32_t<16, 1, 2, 4, EPI>(ps, nprob, st);
   }
 }
 

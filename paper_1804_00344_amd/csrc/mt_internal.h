@@ -357,11 +357,15 @@ struct GemmProblem {
   int M, N, K;
   int32_t *err;           // device error word (bit err_bit set on a clamped gather)
   int err_bit;
+  int wblk;               // fp32 weights: column block width of their packing (16 or 32)
 };
 
 // gemm dtype: 0 fp32 MFMA, 1 bf16 MFMA.  nprob = 1 or 2 (problems share one launch).
 hipError_t launch_gemm(int bf16_mma, const GemmProblem *probs, int nprob, Epilogue epi,
                        hipStream_t st);
+// fp32 weight packing for an [K][N] product expected at about `rows` rows: 16 (16x16x4 form) or
+// 32 (32x32x2 form), whichever the tile choice expects to run faster
+int gemm_f32_weight_block(long rows, long N, long K);
 
 // ---- vocabulary projection with fused log-sum-exp partials and beam candidates ----
 // hypothesis rows per workgroup (0 if E is too large for the LDS-resident activations)
