@@ -276,7 +276,31 @@ __device__ __forceinline__ int wave_topk(const uint32_t (&u)[R], const int (&ix)
 // over chunk c: L = M + ln sum_c s_c exp(m_c - M), M = max_c m_c.  Called by a whole
 // 256-thread workgroup (every thread gets L) with a fixed order of operations, so every
 // caller obtains the same bits from the same partials.
+// The same reduction when each thread holds at most one partial (thread t holds partial t,
+// has = t < ntiles): the identical operations in the identical order, so the same bits.
+__device__ __forceinline__ float block_row_lse_one(float2 q, bool has) {
+  __shared__ float wmx1[4], wsm1[4];
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  float mx = -INFINITY;
+  if (has) mx = fmaxf(mx, q.x);
+  mx = wave_max(mx);
+  if (lane == 0) wmx1[w] = mx;
+  __syncthreads();
+  mx = fmaxf(fmaxf(wmx1[0], wmx1[1]), fmaxf(wmx1[2], wmx1[3]));
+  float s = 0.f;
+  if (has) s += q.y * exp_fast(q.x - mx);
+  s = wave_sum(s);
+  if (lane == 0) wsm1[w] = s;
+  __syncthreads();
+  s = wsm1[0] + wsm1[1] + wsm1[2] + wsm1[3];
+  __syncthreads();  // the scratch may be reused by the caller's next call
+  return mx + __builtin_amdgcn_logf(s) * 0.6931471805599453f;
+}
 __device__ __forceinline__ float block_row_lse(const float2 *pr, int ntiles) {
+  if (ntiles <= 256) {
+    const bool has = (int)threadIdx.x < ntiles;
+    return block_row_lse_one(has ? pr[threadIdx.x] : make_float2(0.f, 0.f), has);
+  }
   __shared__ float wmx[4], wsm[4];
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   float mx = -INFINITY;
@@ -384,7 +408,7 @@ void vocab_pack_host(int bf16_mma, int V, int E, const float *src, int src_is_em
 hipError_t launch_vocab_threshold(int M, int V, int K, const float *sample, float *thr, int *scnt, int B,
                                   hipStream_t st);
 // part [M][n_chunks] (reference m, sum exp(l - m)); every logit >= thr[m] goes to cbuf
-// [M][n_chunks][lists][cap] with counts in ccnt [M][n_chunks][lists] (a count above cap marks
+// [M][cap][n_chunks * lists] (entry-major per row) with counts in ccnt [M][n_chunks][lists] (a count above cap marks
 // an overflowed list); logits [M][V] or NULL.  fixed_ref: the caller has proven every logit
 // lies in [-40, 40], so the reference is 0 and no running maximum is kept.
 hipError_t launch_vocab(int bf16_mma, const void *t, const void *wp, const float *bias_pad, int M, int V,
@@ -419,8 +443,9 @@ hipError_t launch_lse(int M, int ntiles, const float2 *part, float *lse, float *
                       hipStream_t st);
 
 // Beam selection, one workgroup per row m = b*K + k.  Candidates are (value, token) pairs stored
-// as int2 {float bits, token} in nl lists of up to cap entries per row: cbuf [M][nl][cap] with
-// fill counts cnt [M][nl] (NULL: every list holds cap entries).
+// as int2 {float bits, token} in nl lists of up to cap entries per row: cbuf [M][cap][nl]
+// (entry q of every list of a row contiguous) with fill counts cnt [M][nl] (NULL: every list
+// holds cap entries).
 //  * part != NULL (candidates from the vocabulary pass): values are logits; the row's
 //    log-sum-exp is merged from part [M][ntiles] and keys are prev_score + (logit - lse).  A
 //    row whose candidates do not fit (a list count above cap, more than the row can stage,

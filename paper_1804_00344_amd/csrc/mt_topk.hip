@@ -24,6 +24,7 @@ namespace mt {
 constexpr int kTT = 256;
 constexpr int kRowCap = 4096;          // candidates one row can stage in LDS
 constexpr int kSlots = kRowCap / 256;  // register slots per lane when a wave takes a quarter
+constexpr int kSpec = 4;               // list entries requested with the counts
 
 // Row results cross workgroups (and XCDs, whose L2 caches are not coherent with each other)
 // on their way to the sentence merge.  They are written and read with device-scope atomic
@@ -40,38 +41,51 @@ __device__ __forceinline__ int2 get_row(const int2 *p) {
   return make_int2((int)(uint32_t)v, (int)(uint32_t)(v >> 32));
 }
 
-// Level 3 for one sentence, by one wave: the K best of the K x K row results
-// (row_cand [M][K] of (key bits, token)); candidate (k, j) has flat index k*V + token.
-template <int KMAX>
+// Level 3 for one sentence, by the whole workgroup: the K best of the K x K row results
+// (row_cand [M][K] of (key bits, token)); candidate (k, j) has flat index k*V + token.  Every
+// candidate counts the candidates that beat it (larger key code, or equal code and smaller
+// index); entries without a token get distinct indices above every real one, so the counts
+// are a permutation of 0..K*K-1 and the K candidates with counts below K write themselves to
+// their rank.  Entries without a token that rank below K are dead slots (fewer than K real
+// candidates): they continue hypothesis 0 with score -inf.
 __device__ __forceinline__ void sentence_merge(const RowSelect &a, int b, uint32_t *su, int *si) {
-  constexpr int R = (KMAX * KMAX + 63) / 64;
-  const int lane = threadIdx.x & 63, K = a.K, V = a.V;
-  const int n = K * K;
-  uint32_t u[R];
-  int ix[R];
-#pragma unroll
-  for (int s = 0; s < R; ++s) {
-    const int j = s * 64 + lane;
-    u[s] = 0u;
-    ix[s] = 0x7fffffff;
-    if (j < n) {
-      const int k = j / K;
-      const int2 e = get_row(a.row_cand + (size_t)(b * K + k) * K + (j - k * K));
-      if (e.y >= 0 && e.y < V) {
-        u[s] = key_code(__int_as_float(e.x));
-        ix[s] = k * V + e.y;
-      }
-    }
+  const int t = threadIdx.x, K = a.K, V = a.V;
+  const int n = K * K;  // <= 256: K <= 16
+  const int n4 = (n + 3) / 4;
+  if (t < n) {
+    const int k = t / K;
+    const int2 e = get_row(a.row_cand + (size_t)(b * K + k) * K + (t - k * K));
+    const bool real = e.y >= 0 && e.y < V;
+    su[t] = real ? key_code(__int_as_float(e.x)) : 0u;
+    si[t] = real ? k * V + e.y : K * V + t;
+  } else if (t < 4 * n4) {  // padding to whole 16-byte groups: beats nothing
+    su[t] = 0u;
+    si[t] = 0x7fffffff;
   }
-  const int ns = wave_topk<R>(u, ix, (n + 63) / 64, K, su, si, [&](int rank, float key, int i) {
-    const int o = b * K + rank;
-    a.score_out[o] = key;
-    a.tok_out[o] = i % V;
-    a.bp_out[o] = i / V;
-    if (a.row_out) a.row_out[o] = b * K + i / V;
-  });
-  if (lane >= ns && lane < K) {  // fewer than K candidates: dead slots continue hypothesis 0
-    const int o = b * K + lane;
+  __syncthreads();
+  if (t >= n) return;
+  const uint32_t mu = su[t];
+  const int mi = si[t];
+  // the candidates are read four at a time, four groups per iteration (16-byte LDS reads, issued
+  // together: read one by one, every iteration waited out the LDS latency)
+  const uint4 *su4 = (const uint4 *)su;
+  const int4 *si4 = (const int4 *)si;
+  auto beats = [&](uint32_t ou, int oi) { return (ou > mu || (ou == mu && oi < mi)) ? 1 : 0; };
+  int rank = 0;
+#pragma unroll 4
+  for (int j = 0; j < n4; ++j) {
+    const uint4 u = su4[j];
+    const int4 x = si4[j];
+    rank += beats(u.x, x.x) + beats(u.y, x.y) + beats(u.z, x.z) + beats(u.w, x.w);
+  }
+  if (rank >= K) return;
+  const int o = b * K + rank;
+  if (mu != 0u) {
+    a.score_out[o] = key_from_code(mu);
+    a.tok_out[o] = mi % V;
+    a.bp_out[o] = mi / V;
+    if (a.row_out) a.row_out[o] = b * K + mi / V;
+  } else {
     a.score_out[o] = -INFINITY;
     a.tok_out[o] = 0;
     a.bp_out[o] = 0;
@@ -85,8 +99,8 @@ __device__ __forceinline__ void sentence_merge(const RowSelect &a, int b, uint32
 // merges them.
 template <int KMAX, typename CT>
 __global__ __launch_bounds__(kTT) void row_select_kernel(RowSelect a) {
-  __shared__ uint32_t su[kRowCap];
-  __shared__ int si[kRowCap];
+  __shared__ __attribute__((aligned(16))) uint32_t su[kRowCap];
+  __shared__ __attribute__((aligned(16))) int si[kRowCap];
   __shared__ int wtot[4];
   __shared__ uint32_t qu[4][KMAX];
   __shared__ int qi[4][KMAX];
@@ -96,7 +110,33 @@ __global__ __launch_bounds__(kTT) void row_select_kernel(RowSelect a) {
   const int K = a.K, V = a.V, nl = a.nl, cap = a.cap;
   const int b = m / K;
   const bool fused = a.part != nullptr;
-  const float L = fused ? block_row_lse(a.part + (size_t)m * a.ntiles, a.ntiles) : 0.f;
+  const int *cr = a.cnt ? a.cnt + (size_t)m * nl : nullptr;
+
+  // ---- one round trip for the usual shape (at most one partial and two lists per thread):
+  // the row's log-sum-exp partial, its list fill counts and the first kSpec entries of this
+  // thread's lists are all requested before any of them is needed (lists hold about one entry
+  // each; entries past a list's count are loaded and ignored) ----
+  const bool pre = nl <= 2 * kTT && (!fused || a.ntiles <= kTT);  // uniform
+  const bool has_p = fused && t < a.ntiles;
+  float2 pq = make_float2(0.f, 0.f);
+  int pc[2] = {0, 0};
+  int2 pe[2][kSpec];
+  if (pre) {
+    if (has_p) pq = a.part[(size_t)m * a.ntiles + t];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int l = t + j * kTT;
+      if (l < nl) {
+        pc[j] = cr ? cr[l] : cap;
+        const int2 *e = a.cbuf + (size_t)m * cap * nl + l;  // entry q at e[q * nl]
+#pragma unroll
+        for (int q = 0; q < kSpec; ++q) pe[j][q] = q < cap ? e[(size_t)q * nl] : make_int2(0, -1);
+      }
+    }
+  }
+  const float L = !fused ? 0.f
+                  : pre  ? block_row_lse_one(pq, has_p)
+                         : block_row_lse(a.part + (size_t)m * a.ntiles, a.ntiles);
   const float sc = fused ? a.prev_score[m] : 0.f;
   int2 *out = a.row_cand + (size_t)m * K;
   auto emit_row = [&](int rank, float key, int tok) { put_row(out + rank, key, tok); };
@@ -104,15 +144,22 @@ __global__ __launch_bounds__(kTT) void row_select_kernel(RowSelect a) {
   if (fused && sc == -INFINITY) {  // every key of the row is -inf: the K smallest tokens win
     if (t < K) put_row(out + t, -INFINITY, t);
   } else {
-    const int *cr = a.cnt ? a.cnt + (size_t)m * nl : nullptr;
-
     // ---- list fill counts and the block-wide offsets of this thread's entries ----
     int mine = 0;
     bool over = false;
-    for (int l = t; l < nl; l += kTT) {
-      const int c = cr ? cr[l] : cap;
-      over |= c > cap;
-      mine += c < cap ? c : cap;
+    if (pre) {
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        if (t + j * kTT < nl) {
+          over |= pc[j] > cap;
+          mine += pc[j] < cap ? pc[j] : cap;
+        }
+    } else {
+      for (int l = t; l < nl; l += kTT) {
+        const int c = cr ? cr[l] : cap;
+        over |= c > cap;
+        mine += c < cap ? c : cap;
+      }
     }
     int incl = mine;
 #pragma unroll
@@ -133,32 +180,41 @@ __global__ __launch_bounds__(kTT) void row_select_kernel(RowSelect a) {
       if (fused) row_recompute<CT, KMAX>(a.vv, m, K, L, sc, emit_row);
     } else {
       // ---- stage the candidates as (key code, token) in LDS ----
-      for (int l = t; l < nl; l += kTT) {
-        int c = cr ? cr[l] : cap;
-        c = c < cap ? c : cap;
-        const int2 *e = a.cbuf + ((size_t)m * nl + l) * cap;
-        for (int q0 = 0; q0 < c; q0 += 8) {
-          int2 v[8];
-#pragma unroll
-          for (int u = 0; u < 8; ++u) v[u] = q0 + u < c ? e[q0 + u] : make_int2(0, -1);
-#pragma unroll
-          for (int u = 0; u < 8; ++u) {
-            if (q0 + u >= c) continue;
-            const int tok = v[u].y;
-            uint32_t code = 0u;
-            if (tok >= 0 && tok < V) {
-              float key = __int_as_float(v[u].x);
-              if (fused) {
-                const float lp = key - L;
-                key = sc + lp;
-              }
-              code = key_code(key);
-            }
-            su[off + q0 + u] = code;
-            si[off + q0 + u] = tok;
+      auto stage = [&](int pos, int2 v) {
+        const int tok = v.y;
+        uint32_t code = 0u;
+        if (tok >= 0 && tok < V) {
+          float key = __int_as_float(v.x);
+          if (fused) {
+            const float lp = key - L;
+            key = sc + lp;
           }
+          code = key_code(key);
         }
-        off += c;
+        su[pos] = code;
+        si[pos] = tok;
+      };
+      if (pre) {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const int l = t + j * kTT;
+          if (l >= nl) continue;
+          const int c = pc[j] < cap ? pc[j] : cap;
+          const int2 *e = a.cbuf + (size_t)m * cap * nl + l;
+#pragma unroll
+          for (int q = 0; q < kSpec; ++q)
+            if (q < c) stage(off + q, pe[j][q]);
+          for (int q = kSpec; q < c; ++q) stage(off + q, e[(size_t)q * nl]);  // long lists (rare)
+          off += c;
+        }
+      } else {
+        for (int l = t; l < nl; l += kTT) {
+          int c = cr ? cr[l] : cap;
+          c = c < cap ? c : cap;
+          const int2 *e = a.cbuf + (size_t)m * cap * nl + l;
+          for (int q = 0; q < c; ++q) stage(off + q, e[(size_t)q * nl]);
+          off += c;
+        }
       }
       __syncthreads();
 
@@ -218,7 +274,7 @@ __global__ __launch_bounds__(kTT) void row_select_kernel(RowSelect a) {
   if (t == 0) last = __hip_atomic_fetch_add(a.scnt + b, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == K - 1;
   __syncthreads();
   if (!last) return;
-  if (w == 0) sentence_merge<KMAX>(a, b, qu[0], qi[0]);
+  sentence_merge(a, b, su, si);
   if (t == 0) __hip_atomic_store(a.scnt + b, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
@@ -237,8 +293,8 @@ __global__ __launch_bounds__(kTT) void topk_scan_logp_kernel(int M, int K, int V
   List<KMAX> lst;
   lst.init();
   for (int v = v0 + threadIdx.x; v < v1; v += kTT) lst.push(sc + row[v], v);
-  int2 *o = cand_out + ((size_t)m * nch + ch) * K;
-  block_extract<KMAX>(lst, K, [&](int r, float v, int i) { o[r] = make_int2(__float_as_int(v), i); });
+  int2 *o = cand_out + (size_t)m * K * nch + ch;  // entry r at o[r * nch] (entry-major per row)
+  block_extract<KMAX>(lst, K, [&](int r, float v, int i) { o[(size_t)r * nch] = make_int2(__float_as_int(v), i); });
 }
 
 static int kbucket(int K) { return K <= 1 ? 1 : K <= 2 ? 2 : K <= 4 ? 4 : K <= 8 ? 8 : 16; }

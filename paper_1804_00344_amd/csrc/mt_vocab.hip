@@ -69,7 +69,7 @@ struct VocabArgs {
   int tiles_total;      // 64-row tiles of the processed range [0, 64 * tiles_total)
   float2 *part;         // [M][n_chunks] (max, sum exp(l - max)); NULL in the threshold pass
   const float *thr;     // [M] candidate threshold
-  int2 *cbuf;           // [M][n_chunks][kLists][cap] (logit bits, token)
+  int2 *cbuf;           // [M][cap][n_chunks][kLists] (logit bits, token): entry-major per row
   int *ccnt;            // [M][n_chunks][kLists] values at or above the threshold
   int cap;
   float *logits;        // [M][logits_ld] or NULL
@@ -129,6 +129,11 @@ __global__ __launch_bounds__((VShape<CT, HB>::NT)) void vocab_kernel(VocabArgs a
   const bool collect = a.part != nullptr;
 
   float lm[HBB], ls[HBB], th[HBB];
+  // A row's lists are stored entry-major (entry q of all its lists contiguous), so that the
+  // selection reads the first entries of every list of a row with coalesced loads; successive
+  // entries of one list are nlr * 8 bytes apart.
+  const int nlr = a.n_chunks * kLists;
+  const uint32_t lstep = (uint32_t)nlr * 8u;
   uint32_t loff[HBB];  // byte offset of this lane's next candidate slot in cbuf, per hypothesis block
   uint32_t lend[HBB];  // offset of the list's last slot (writes past capacity stay there)
   char *const cbase = (char *)a.cbuf;
@@ -138,8 +143,8 @@ __global__ __launch_bounds__((VShape<CT, HB>::NT)) void vocab_kernel(VocabArgs a
     lm[j] = FIX ? 0.f : -INFINITY;
     ls[j] = 0.f;
     th[j] = (collect && h < a.M) ? a.thr[h] : INFINITY;
-    loff[j] = (uint32_t)((((size_t)(h < a.M ? h : 0) * a.n_chunks + chunk) * kLists + src) * a.cap * sizeof(int2));
-    lend[j] = loff[j] + (uint32_t)(a.cap - 1) * 8u;
+    loff[j] = (uint32_t)(((size_t)(h < a.M ? h : 0) * a.cap * nlr + chunk * kLists + src) * sizeof(int2));
+    lend[j] = loff[j] + (uint32_t)(a.cap - 1) * lstep;
   }
 
   // With two hypothesis groups (two waves per SIMD, same vocabulary tiles), both waves of a
@@ -298,7 +303,7 @@ __global__ __launch_bounds__((VShape<CT, HB>::NT)) void vocab_kernel(VocabArgs a
           // reported as overflowed (its row is recomputed exactly)
           auto capture = [&](float x, int i, int r) {
             *(int2 *)(cbase + loff[j]) = make_int2(__float_as_int(x), v0 + 32 * i + 8 * (r >> 2) + 4 * lhalf + (r & 3));
-            const uint32_t nx = loff[j] + 8u;
+            const uint32_t nx = loff[j] + lstep;
             loff[j] = nx < lend[j] ? nx : lend[j];
           };
           if constexpr (FIX) {
@@ -355,8 +360,8 @@ __global__ __launch_bounds__((VShape<CT, HB>::NT)) void vocab_kernel(VocabArgs a
   for (int j = 0; j < HBB; ++j) {
     const int h = h0 + hc0 + j * 32 + lrow;
     if (h < a.M) {
-      const uint32_t lstart = lend[j] - (uint32_t)(a.cap - 1) * 8u;
-      const int n = (int)((loff[j] - lstart) / 8u);
+      const uint32_t lstart = lend[j] - (uint32_t)(a.cap - 1) * lstep;
+      const int n = (int)((loff[j] - lstart) / lstep);
       a.ccnt[((size_t)h * a.n_chunks + chunk) * kLists + src] = n >= a.cap - 1 ? a.cap + 1 : n;
     }
   }
