@@ -1,4 +1,5 @@
 """GPU path (libmtstep through its C ABI) against the CPU oracle on seeded inputs."""
+import dataclasses
 import math
 import sys
 
@@ -104,6 +105,37 @@ def masked_alpha_zero(p, gpu_alpha, mask):
 
 N_SAMPLE = {"tiny_f32": 99, "tiny_bf16_ln": 99, "nematus_f32": 4, "nematus_bf16_ln": 4,
             "vocab85k_bf16_ln": 4, "greedy_bf16_ln": 16}
+
+
+# Nematus fp32 dimensions at other batch shapes: the fp32 products then run on the tile shapes
+# and k-splits that 64 x 12 rows never pick (3x2, 3x3 and 3x5 blocks split over two waves, 2x4
+# blocks, 32-wide 1x2 tiles with and without a split), and on row counts that are not a multiple
+# of any tile (296).
+BATCH_SHAPES = [(16, 12), (37, 8), (80, 8)]
+
+
+@pytest.mark.parametrize("B,K", BATCH_SHAPES)
+def test_step_parity_other_batch_shapes(B, K):
+    p = dataclasses.replace(synth.PRESETS["nematus_f32"], name=f"nematus_f32_B{B}_K{K}", B=B, K=K)
+    log(f"\n[step parity] {p.name} (M={p.M})")
+    w = synth.make_weights(p, peaked_bias=True)
+    ctx, mask, lens = synth.make_source(p)
+    dec = Decoder.from_preset(p, w)
+    dec.set_batch(ctx, mask, p.K)
+    dec.precompute()
+    tok, src, state, score = synth.mid_decode_inputs(p, salt=3)
+    gpu = run_step(dec, p, tok, src, T(state), p.M)
+    sc, tk, bp, rw = [x.cpu().numpy() for x in dec.topk(T(score), None)]
+    torch.cuda.synchronize()
+    assert mt.mt_device_errors(dec.model) == 0
+    sents = sample_sentences(lens, 3)
+    orc = oracle_sentences(oracle_model(p, w), p.K, sents, ctx, mask, tok, src, state)
+    tol = TOL[p.gemm]
+    compare_rows(p, gpu, orc, sents, tol, p.name)
+    for b in sents:
+        rows = slice(b * p.K, (b + 1) * p.K)
+        topk_gap_check(p.K, score[rows], orc[b]["logp"], sc[rows], tk[rows], bp[rows], tol["logp"])
+        assert np.array_equal(rw[rows], b * p.K + bp[rows])
 
 
 @pytest.mark.parametrize("name", list(N_SAMPLE))
