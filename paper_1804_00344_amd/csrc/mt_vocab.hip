@@ -10,7 +10,7 @@
 //
 // Work split: a workgroup owns HB hypothesis rows (their activations stay resident in LDS for
 // the whole kernel) and one contiguous chunk of the vocabulary, split into 4 runs of 64-row
-// vocabulary tiles.  Each wave covers WH <= 64 hypothesis columns of one run (HB/WH waves per
+// vocabulary tiles (cut at 32-row boundaries, so a run may end with one 32-row tile).  Each wave covers WH <= 64 hypothesis columns of one run (HB/WH waves per
 // run share its weight fragments) and streams the packed weights straight from global memory
 // (fragment order, one coalesced 16-byte load per lane per MFMA operand), prefetching D
 // k-steps ahead across tile boundaries, with no barrier in the main loop.
@@ -28,6 +28,8 @@
 // MFMA with each 16-byte vector feeding 4 successive MFMAs (lane half g supplies k = 4g + s
 // to MFMA s); bf16 uses 32x32x16 with one vector per MFMA.
 #include "mt_internal.h"
+
+#include <type_traits>
 
 namespace mt {
 
@@ -66,7 +68,7 @@ struct VocabArgs {
   const float *bias;    // [Vpad] with -inf beyond V
   int M, V, E, KS;      // KS = E / KV
   int n_chunks;
-  int tiles_total;      // 64-row tiles of the processed range [0, 64 * tiles_total)
+  int tiles_total;      // 64-row tiles of the packed weights (the packed extent)
   float2 *part;         // [M][n_chunks] (max, sum exp(l - max)); NULL in the threshold pass
   const float *thr;     // [M] candidate threshold
   int2 *cbuf;           // [M][cap][n_chunks][kLists] (logit bits, token): entry-major per row
@@ -117,11 +119,16 @@ __global__ __launch_bounds__((VShape<CT, HB>::NT)) void vocab_kernel(VocabArgs a
   __syncthreads();
 
   // ---- this wave's contiguous run of vocabulary tiles ----
+  // Runs are cut at 32-row block boundaries (half a tile), which evens out the work of the
+  // busiest wave: a run is a sequence of two-block tiles, then one single-block tile when its
+  // block count is odd.
   const int slots = a.n_chunks * 4;
   const int slot = chunk * 4 + run;
-  const int t_begin = (int)((long)a.tiles_total * slot / slots);
-  const int t_end = (int)((long)a.tiles_total * (slot + 1) / slots);
-  const int ntile = t_end - t_begin;
+  const int nblk = (a.V + 31) / 32;
+  const int b_begin = (int)((long)nblk * slot / slots);
+  const int b_end = (int)((long)nblk * (slot + 1) / slots);
+  const int npair = (b_end - b_begin) >> 1;
+  const int ntile = npair + ((b_end - b_begin) & 1);
   const int total = ntile * a.KS;  // flat (tile, k-step) stream, KS % D == 0
   const int KS = a.KS;
   const int lrow = lane & 31, lhalf = lane >> 5;
@@ -154,22 +161,24 @@ __global__ __launch_bounds__((VShape<CT, HB>::NT)) void vocab_kernel(VocabArgs a
   if (VShape<CT, HB>::NW > 4 && (wave >> 2) == 1) __builtin_amdgcn_s_sleep(32);
 
   if (ntile > 0) {
-    // Weight fragments of step g of tile ti are vocabulary blocks 2*(t_begin+ti) and +1 at
+    // Weight fragments of step g of tile ti are vocabulary blocks b_begin+2*ti and +1 at
     // k-step ks, 1 KiB (64 lanes x 16 bytes) apart per k-step.  The ring is refilled right
     // after its slot is consumed, from a wave-uniform fragment index that advances without a
     // branch (clamped to the last step), so the loads stay in flight across k-steps: a
     // conditional refill would make the compiler wait for every outstanding load.
-    const v4u *wb = (const v4u *)a.wp + (size_t)2 * t_begin * KS * 64 + lane;
-    int pf_k = 0, pf_n = 0;
+    const v4u *wb = (const v4u *)a.wp + (size_t)b_begin * KS * 64 + lane;
+    int pf_k = 0, pf_n = 0, pf_t = 0;
     int poff = 0;  // fragment index of the next prefetch, in 1 KiB steps from wb
     auto fetch = [&](v4u(&slot)[2]) {
       slot[0] = wb[(size_t)poff * 64];
-      slot[1] = wb[(size_t)(poff + KS) * 64];
+      // a single-block tile reads its one block twice (the next block may lie past the end)
+      slot[1] = wb[(size_t)(poff + (pf_t < npair ? KS : 0)) * 64];
       const int more = pf_n + 1 < total ? 1 : 0;
       const int nk = pf_k + more;
       const int wrap = nk == KS ? 1 : 0;
       pf_n += more;
       pf_k = wrap ? 0 : nk;
+      pf_t += wrap;
       poff += more + wrap * KS;
     };
     v4u ring[D][2];
@@ -181,7 +190,7 @@ __global__ __launch_bounds__((VShape<CT, HB>::NT)) void vocab_kernel(VocabArgs a
     if constexpr (KSC > 0) {
 #pragma unroll
       for (int d = 0; d < D; ++d) {
-        const int so = (2 * t_begin * KSC + d) * 1024;
+        const int so = (b_begin * KSC + d) * 1024;
         ring[d][0] = __builtin_amdgcn_raw_buffer_load_b128(wrs, wvo, so, 0);
         ring[d][1] = __builtin_amdgcn_raw_buffer_load_b128(wrs, wvo, so + KSC * 1024, 0);
       }
@@ -203,7 +212,9 @@ __global__ __launch_bounds__((VShape<CT, HB>::NT)) void vocab_kernel(VocabArgs a
     v4u bcur[HBB], bnxt[HBB];
     if constexpr (kPrefetchLds) lds_frag(0, bcur);
 
-    for (int ti = 0; ti < ntile; ++ti) {
+    // one tile of NB (2 or 1) 32-row blocks
+    auto do_tile = [&](auto nbc, int ti) {
+      constexpr int NB = decltype(nbc)::value;
       // Drain the memory counter once per tile (stores count in it too, and the previous
       // epilogue issued a data-dependent number of them; the ring loads have long arrived).
       // With nothing outstanding on entry, the compiler keeps exact, non-draining waits on
@@ -235,7 +246,7 @@ __global__ __launch_bounds__((VShape<CT, HB>::NT)) void vocab_kernel(VocabArgs a
             bf16x8 b;
             __builtin_memcpy(&b, &bcur[j], 16);
             acc[0][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b, acc[0][j], 0, 0, 0);
-            acc[1][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b, acc[1][j], 0, 0, 0);
+            if constexpr (NB == 2) acc[1][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b, acc[1][j], 0, 0, 0);
           }
         } else {
           float fa0[4], fa1[4], fb[HBB][4];
@@ -248,7 +259,7 @@ __global__ __launch_bounds__((VShape<CT, HB>::NT)) void vocab_kernel(VocabArgs a
 #pragma unroll
             for (int j = 0; j < HBB; ++j) {
               acc[0][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa0[s], fb[j][s], acc[0][j], 0, 0, 0);
-              acc[1][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa1[s], fb[j][s], acc[1][j], 0, 0, 0);
+              if constexpr (NB == 2) acc[1][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa1[s], fb[j][s], acc[1][j], 0, 0, 0);
             }
         }
         refill(slot);
@@ -263,8 +274,9 @@ __global__ __launch_bounds__((VShape<CT, HB>::NT)) void vocab_kernel(VocabArgs a
       };
       if constexpr (KSC > 0) {
         // byte offsets of this tile's and the next tile's first fragment (the last tile
-        // prefetches itself again, in bounds)
-        const int tb = 2 * (t_begin + ti) * KSC * 1024;
+        // prefetches itself again, in bounds; a single block's second fragment reads the
+        // following block, or zero past the end)
+        const int tb = (b_begin + 2 * ti) * KSC * 1024;
         const int tn = ti + 1 < ntile ? tb + 2 * KSC * 1024 : tb;
 #pragma unroll
         for (int ks = 0; ks < KSC; ++ks)
@@ -282,9 +294,9 @@ __global__ __launch_bounds__((VShape<CT, HB>::NT)) void vocab_kernel(VocabArgs a
 
       // ---- epilogue of this tile: bias, online log-sum-exp, threshold-filtered candidates ----
       // lane holds rows v = v0 + 32*i + 8*(r/4) + 4*lhalf + r%4 of hypothesis column j*32 + lrow
-      const int v0 = (t_begin + ti) * kVRows;
+      const int v0 = (b_begin + 2 * ti) * 32;
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < NB; ++i)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const float4 b4 = *(const float4 *)(a.bias + v0 + 32 * i + 8 * q + 4 * lhalf);
@@ -309,7 +321,7 @@ __global__ __launch_bounds__((VShape<CT, HB>::NT)) void vocab_kernel(VocabArgs a
           if constexpr (FIX) {
             float se = 0.f;
 #pragma unroll
-            for (int i = 0; i < 2; ++i)
+            for (int i = 0; i < NB; ++i)
 #pragma unroll
               for (int r = 0; r < 16; ++r) {
                 const float x = acc[i][j][r];
@@ -320,14 +332,14 @@ __global__ __launch_bounds__((VShape<CT, HB>::NT)) void vocab_kernel(VocabArgs a
           } else {
             float mt = -INFINITY;
 #pragma unroll
-            for (int i = 0; i < 2; ++i)
+            for (int i = 0; i < NB; ++i)
 #pragma unroll
               for (int r = 0; r < 16; ++r) mt = fmaxf(mt, acc[i][j][r]);
             if (mt != -INFINITY) {  // -inf only when the whole tile is padding
               const float mts = mt * kLog2e;
               float se = 0.f;
 #pragma unroll
-              for (int i = 0; i < 2; ++i)
+              for (int i = 0; i < NB; ++i)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                   const float x = acc[i][j][r];
@@ -343,7 +355,7 @@ __global__ __launch_bounds__((VShape<CT, HB>::NT)) void vocab_kernel(VocabArgs a
         if (LOG && h < a.M) {
           float *lrowp = a.logits + (size_t)h * a.logits_ld;
 #pragma unroll
-          for (int i = 0; i < 2; ++i)
+          for (int i = 0; i < NB; ++i)
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
               const int v = v0 + 32 * i + 8 * (r >> 2) + 4 * lhalf + (r & 3);
@@ -351,7 +363,9 @@ __global__ __launch_bounds__((VShape<CT, HB>::NT)) void vocab_kernel(VocabArgs a
             }
         }
       }
-    }
+    };
+    for (int ti = 0; ti < npair; ++ti) do_tile(std::integral_constant<int, 2>{}, ti);
+    if (ntile > npair) do_tile(std::integral_constant<int, 1>{}, npair);
   }  // ntile > 0
 
   if (!collect) return;
