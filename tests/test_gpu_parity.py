@@ -138,6 +138,32 @@ def test_step_parity_other_batch_shapes(B, K):
         assert np.array_equal(rw[rows], b * p.K + bp[rows])
 
 
+# V = 1056 is 33 vocabulary blocks of 32 rows: the runs of the vocabulary pass are one or two
+# blocks long, so most of them end with a single-block tile, the last one at the end of the range
+@pytest.mark.parametrize("name", ["tiny_f32", "tiny_bf16_ln"])
+def test_step_parity_single_block_vocab_tiles(name):
+    p = dataclasses.replace(synth.PRESETS[name], name=f"{name}_V1056", V=1056)
+    log(f"\n[step parity] {p.name} (M={p.M})")
+    w = synth.make_weights(p, peaked_bias=True)
+    ctx, mask, lens = synth.make_source(p)
+    dec = Decoder.from_preset(p, w)
+    dec.set_batch(ctx, mask, p.K)
+    dec.precompute()
+    tok, src, state, score = synth.mid_decode_inputs(p, salt=4)
+    gpu = run_step(dec, p, tok, src, T(state), p.M)
+    sc, tk, bp, rw = [x.cpu().numpy() for x in dec.topk(T(score), None)]
+    torch.cuda.synchronize()
+    assert mt.mt_device_errors(dec.model) == 0
+    sents = sample_sentences(lens, 3)
+    orc = oracle_sentences(oracle_model(p, w), p.K, sents, ctx, mask, tok, src, state)
+    tol = TOL[p.gemm]
+    compare_rows(p, gpu, orc, sents, tol, p.name)
+    for b in sents:
+        rows = slice(b * p.K, (b + 1) * p.K)
+        topk_gap_check(p.K, score[rows], orc[b]["logp"], sc[rows], tk[rows], bp[rows], tol["logp"])
+        assert np.array_equal(rw[rows], b * p.K + bp[rows])
+
+
 @pytest.mark.parametrize("name", list(N_SAMPLE))
 def test_step_parity_mid_decode(name):
     log(f"\n[step parity] preset={name}")
