@@ -133,8 +133,9 @@ size_t mt_workspace_bytes(const mt_model *model, int B, int K, int S);
  *   ctx  [B,S,2H] in gemm dtype (fp32 or bf16) — the encoder context;
  *   mask [B,S] fp32, nonzero = valid position (any pattern; a row without a
  *        valid position yields zero context and zero attention);
- *   pctx_out [B,S,A] in gemm dtype — attention keys ctx Ua + ba (values at
- *        masked positions are unspecified and never read);
+ *   pctx_out [B,S,A] in gemm dtype — attention keys ctx Ua + ba, computed and
+ *        written at valid positions only (masked rows are left as they were and
+ *        never read);
  *   s0_out [B,H] fp32 — tanh(masked mean of ctx[b] times Wi + bi).
  * 1 <= S <= 1024; B*S <= 2^24. */
 mt_status mt_precompute_ctx(mt_model *model, int B, int S, const void *ctx, const float *mask,

@@ -249,7 +249,11 @@ WsLayout ws_layout(const mt_model *m, int B, int K) {
   return L;
 }
 
-size_t precompute_ws_bytes(const mt_model *m, int B) { return (size_t)B * 2 * m->cfg.H * 4; }
+// precompute workspace: masked means [B][2H] fp32, the valid-row list [B*S] and its count
+static size_t rup256(size_t x) { return (x + 255) / 256 * 256; }
+size_t precompute_ws_bytes(const mt_model *m, int B, int S) {
+  return rup256((size_t)B * 2 * m->cfg.H * 4) + rup256((size_t)B * S * 4) + 256;
+}
 
 // ---- profiling ----
 hipEvent_t get_event(mt_model *m) {
@@ -481,7 +485,7 @@ mt_status mt_free(mt_model *m) {
 size_t mt_workspace_bytes(const mt_model *m, int B, int K, int S) {
   if (!valid_model(m) || B < 1 || K < 1 || K > m->cfg.k_max || S < 1 || S > 1024) return 0;
   const WsLayout L = ws_layout(m, B, K);
-  return std::max(L.total, precompute_ws_bytes(m, B));
+  return std::max(L.total, precompute_ws_bytes(m, B, S));
 }
 
 mt_status mt_precompute_ctx(mt_model *model, int B, int S, const void *ctx, const float *mask,
@@ -495,18 +499,23 @@ mt_status mt_precompute_ctx(mt_model *model, int B, int S, const void *ctx, cons
   CHECK(check_dev_ptr(pctx_out, "pctx_out"));
   CHECK(check_dev_ptr(s0_out, "s0_out"));
   CHECK(check_dev_ptr(ws, "ws", 256));
-  const size_t need = precompute_ws_bytes(model, B);
+  const size_t need = precompute_ws_bytes(model, B, S);
   if (ws_bytes < need) return fail(MT_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, need);
   hipStream_t st = (hipStream_t)stream;
   const mt_config &c = model->cfg;
   const int H = c.H, A = c.A, C = model->C;
   float *cbar = (float *)ws;
+  int32_t *vrows = (int32_t *)((char *)ws + rup256((size_t)B * C * 4));
+  int *nvalid = (int *)((char *)vrows + rup256((size_t)B * S * 4));
+  // keys only at valid positions (the others are never read): the product gathers the valid
+  // context rows, counted on the device, and stores each key row at its own position
+  LAUNCH(MT_KERNEL_PRECOMPUTE, launch_valid_rows(B * S, mask, vrows, nvalid, st));
   GemmProblem p{};
-  p.A = ctx; p.a_idx = nullptr; p.a_rows = B * S; p.lda = C; p.a_bf16 = model->bf16;
+  p.A = ctx; p.a_idx = vrows; p.a_rows = B * S; p.lda = C; p.a_bf16 = model->bf16;
   p.Bp = model->wp.p; p.ldb = model->wp.ldb; p.wblk = model->wp.blk; p.bias = model->ba;
   p.out = pctx_out; p.ldc = A; p.out_bf16 = model->bf16;
-  p.M = B * S; p.N = A; p.K = C; p.err = nullptr; p.err_bit = 0;
-  LAUNCH(MT_KERNEL_PRECOMPUTE, launch_gemm(model->bf16, &p, 1, EPI_STORE, st));
+  p.M = B * S; p.N = A; p.K = C; p.err = nullptr; p.err_bit = 0; p.m_dev = nvalid;
+  LAUNCH(MT_KERNEL_PRECOMPUTE, launch_gemm(model->bf16, &p, 1, EPI_SCATTER, st));
   LAUNCH(MT_KERNEL_PRECOMPUTE, launch_masked_mean(B, S, C, ctx, model->bf16, mask, cbar, st));
   GemmProblem q{};
   q.A = cbar; q.a_rows = B; q.lda = C; q.a_bf16 = 0;

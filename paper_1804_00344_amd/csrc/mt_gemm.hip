@@ -86,6 +86,14 @@ __global__ __launch_bounds__(kWdThreads) void gemm_wd_kernel(Problems probs) {
   if (tile >= tilesM * tilesN) return;
   const int tm = tile % tilesM, tn = tile / tilesM;  // neighbours share a weight panel
   const int m0 = tm * kWdRows, n0 = tn * kWdCols;
+  // rows counted on the device, when given, bound the rows read and stored
+  const int *const mdp = pin_s(P.m_dev);
+  int Mv = M;
+  if (mdp) {
+    const int md = *(const __attribute__((address_space(1))) int *)mdp;
+    Mv = md < M ? md : M;
+  }
+  if (m0 >= Mv) return;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
@@ -95,8 +103,8 @@ __global__ __launch_bounds__(kWdThreads) void gemm_wd_kernel(Problems probs) {
 #pragma unroll
   for (int p = 0; p < RP; ++p) {
     const int m = m0 + (tid >> 4) + 8 * p;
-    int src = m < M ? m : 0;  // rows past M read row 0 and are never stored
-    if (P.a_idx && m < M) {
+    int src = m < Mv ? m : 0;  // rows past the count read row 0 and are never stored
+    if (P.a_idx && m < Mv) {
       src = P.a_idx[m];
       if (src < 0 || src >= P.a_rows) {
         if (P.err) atomicOr(P.err, 1 << P.err_bit);
@@ -220,6 +228,20 @@ __global__ __launch_bounds__(kWdThreads) void gemm_wd_kernel(Problems probs) {
     const int col = n0 + wave * 64 + j * 32 + (lane & 31);
     bias[j] = biasp ? ((const __attribute__((address_space(1))) float *)biasp)[col < N ? col : N - 1] : 0.f;
   }
+  // EPI_SCATTER: the output row of each stored row is its (clamped) gather row
+  int orow[EPI == EPI_SCATTER ? MB : 1][16];
+  if constexpr (EPI == EPI_SCATTER) {
+    const int32_t *const aix = pin_s(P.a_idx);
+    const int arows = pin_s(P.a_rows);
+#pragma unroll
+    for (int i = 0; i < MB; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = m0 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        const int g = row < Mv ? ((const __attribute__((address_space(1))) int32_t *)aix)[row] : 0;
+        orow[i][r] = g < 0 ? 0 : g >= arows ? arows - 1 : g;
+      }
+  }
   __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
   auto epilogue = [&](auto bf) {
 #pragma unroll
@@ -231,13 +253,15 @@ __global__ __launch_bounds__(kWdThreads) void gemm_wd_kernel(Problems probs) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int row = m0 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-          if (row >= M) continue;
+          if (row >= Mv) continue;
           float v = acc[i][j][r] + bias[j];
           if (EPI == EPI_TANH) v = tanh_fast(v);
+          int orw = row;
+          if constexpr (EPI == EPI_SCATTER) orw = orow[i][r];
           if constexpr (decltype(bf)::value)
-            ((__attribute__((address_space(1))) bf16 *)outp)[(size_t)row * ldc + col] = to_bf16(v);
+            ((__attribute__((address_space(1))) bf16 *)outp)[(size_t)orw * ldc + col] = to_bf16(v);
           else
-            ((__attribute__((address_space(1))) float *)outp)[(size_t)row * ldc + col] = v;
+            ((__attribute__((address_space(1))) float *)outp)[(size_t)orw * ldc + col] = v;
         }
     }
   };
@@ -316,11 +340,23 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(Problems probs) {
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int part = wave % S, slot_t = wave / S;
   const int tile = xcd_remap(blockIdx.x, gridDim.x) * TPB + slot_t;
+  // rows counted on the device, when given, bound the rows read and stored
+  const int *const mdp = pin_s(P.m_dev);
+  int Mv = M;
+  if (mdp) {
+    const int md = *(const __attribute__((address_space(1))) int *)mdp;
+    Mv = md < M ? md : M;
+  }
   // a wave without a tile still takes part in the workgroup's barrier below
-  const bool live = tile < tilesM * tilesN;
-  const int tl = live ? tile : 0;
+  const bool has_tile = tile < tilesM * tilesN;
+  const int tl = has_tile ? tile : 0;
   const int tm = tl % tilesM, tn = tl / tilesM;  // neighbours share a weight panel
   const int m0 = tm * BLK * TA, n0 = tn * BLK * TB;
+  const bool live = has_tile && m0 < Mv;
+  // without a split there is no barrier, so a wave without a tile (or whose rows all lie past
+  // the device count) ends here; with one it computes a stand-in tile for the barrier's sake
+  if constexpr (S == 1)
+    if (!live) return;
   const int lr = lane & (BLK - 1), lk = (lane / BLK) * 4;
   const int ks_begin = part * (KSp / S), ks_end = ks_begin + KSp / S;
 
@@ -332,8 +368,8 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(Problems probs) {
 #pragma unroll
   for (int i = 0; i < TA; ++i) {
     const int m = m0 + BLK * i + lr;
-    int src = m < M ? m : 0;
-    if (live && P.a_idx && m < M) {
+    int src = m < Mv ? m : 0;
+    if (live && P.a_idx && m < Mv) {
       src = P.a_idx[m];
       if (src < 0 || src >= P.a_rows) {
         if (P.err) atomicOr(P.err, 1 << P.err_bit);
@@ -447,6 +483,23 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(Problems probs) {
     const int col = n0 + BLK * j + lr;
     bias[j] = biasp ? ((const __attribute__((address_space(1))) float *)biasp)[col < N ? col : N - 1] : 0.f;
   }
+  auto row_of = [&](int i, int r) {
+    return m0 + BLK * i + (BLK == 16 ? (lane >> 4) * 4 + r : 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3));
+  };
+  // EPI_SCATTER: the output row of each stored row is its (clamped) gather row
+  int orow[EPI == EPI_SCATTER ? TA : 1][EPI == EPI_SCATTER ? F::NACC : 1];
+  if constexpr (EPI == EPI_SCATTER) {
+    const int32_t *const aix = pin_s(P.a_idx);
+    const int arows = pin_s(P.a_rows);
+#pragma unroll
+    for (int i = 0; i < TA; ++i)
+#pragma unroll
+      for (int r = 0; r < F::NACC; ++r) {
+        const int row = row_of(i, r);
+        const int g = row < Mv ? ((const __attribute__((address_space(1))) int32_t *)aix)[row] : 0;
+        orow[i][r] = g < 0 ? 0 : g >= arows ? arows - 1 : g;
+      }
+  }
   __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
   auto epilogue = [&](auto bf) {
 #pragma unroll
@@ -457,14 +510,16 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(Problems probs) {
       for (int i = 0; i < TA; ++i)
 #pragma unroll
         for (int r = 0; r < F::NACC; ++r) {
-          const int row = m0 + BLK * i + (BLK == 16 ? (lane >> 4) * 4 + r : 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3));
-          if (row >= M) continue;
+          const int row = row_of(i, r);
+          if (row >= Mv) continue;
           float v = acc[i][j][r] + bias[j];
           if (EPI == EPI_TANH) v = tanh_fast(v);
+          int orw = row;
+          if constexpr (EPI == EPI_SCATTER) orw = orow[i][r];
           if constexpr (decltype(bf)::value)
-            ((__attribute__((address_space(1))) bf16 *)outp)[(size_t)row * ldc + col] = to_bf16(v);
+            ((__attribute__((address_space(1))) bf16 *)outp)[(size_t)orw * ldc + col] = to_bf16(v);
           else
-            ((__attribute__((address_space(1))) float *)outp)[(size_t)row * ldc + col] = v;
+            ((__attribute__((address_space(1))) float *)outp)[(size_t)orw * ldc + col] = v;
         }
     }
   };
@@ -594,8 +649,14 @@ hipError_t launch_gemm(int bf16_mma, const GemmProblem *probs, int nprob, Epilog
   for (int i = 0; i < nprob; ++i) {
     ps.p[i] = probs[i];
     if (probs[i].a_bf16 != probs[0].a_bf16 || (probs[i].a_bf16 && !bf16_mma)) return hipErrorInvalidValue;
+    if (epi == EPI_SCATTER && !probs[i].a_idx) return hipErrorInvalidValue;
   }
-  if (!bf16_mma) return epi == EPI_TANH ? go_f32<EPI_TANH>(ps, nprob, st) : go_f32<EPI_STORE>(ps, nprob, st);
+  if (!bf16_mma) {
+    if (epi == EPI_SCATTER) return go_f32<EPI_SCATTER>(ps, nprob, st);
+    return epi == EPI_TANH ? go_f32<EPI_TANH>(ps, nprob, st) : go_f32<EPI_STORE>(ps, nprob, st);
+  }
+  if (epi == EPI_SCATTER)  // the keys precompute: bf16 context rows
+    return probs[0].a_bf16 ? go_wd<bf16, EPI_SCATTER>(ps, nprob, st) : hipErrorInvalidValue;
   if (probs[0].a_bf16)
     return epi == EPI_TANH ? go_wd<bf16, EPI_TANH>(ps, nprob, st) : go_wd<bf16, EPI_STORE>(ps, nprob, st);
   return epi == EPI_TANH ? go_wd<float, EPI_TANH>(ps, nprob, st) : go_wd<float, EPI_STORE>(ps, nprob, st);

@@ -364,7 +364,8 @@ __device__ __forceinline__ void row_recompute(const VocabView &vv, int m, int K,
 // launchers (host side).  All return hipSuccess or the launch error.
 // ---------------------------------------------------------------------------------------
 
-enum Epilogue { EPI_STORE = 0, EPI_TANH = 1 };
+// EPI_SCATTER: row m is stored at output row a_idx[m] (the rows it was gathered from)
+enum Epilogue { EPI_STORE = 0, EPI_TANH = 1, EPI_SCATTER = 2 };
 
 struct GemmProblem {
   const void *A;          // activations [rows][lda] (fp32 or bf16, see a_bf16)
@@ -382,6 +383,8 @@ struct GemmProblem {
   int32_t *err;           // device error word (bit err_bit set on a clamped gather)
   int err_bit;
   int wblk;               // fp32 weights: column block width of their packing (16 or 32)
+  const int *m_dev;       // optional: row count on the device (<= M); later rows are neither
+                          // read nor stored, and tiles that start past it return at once
 };
 
 // gemm dtype: 0 fp32 MFMA, 1 bf16 MFMA.  nprob = 1 or 2 (problems share one launch).
@@ -432,6 +435,8 @@ hipError_t launch_readout(int M, int E, const float *p1, int ld1, const float *p
 
 hipError_t launch_masked_mean(int B, int S, int Cd, const void *ctx, int ctx_bf16,
                               const float *mask, float *out, hipStream_t st);
+// rows of a [n] 0/1 mask that are valid (nonzero), in increasing order: idx[0..*count)
+hipError_t launch_valid_rows(int n, const float *mask, int32_t *idx, int *count, hipStream_t st);
 
 // context rows go to ctx_out [M][ldc] fp32 and/or ctx16 [M][Cd] bf16 (either may be NULL)
 hipError_t launch_attention(int B, int K, int S, int A, int Cd, const void *P, const void *Cx,

@@ -243,6 +243,36 @@ __global__ __launch_bounds__(kT) void masked_mean_kernel(int B, int S, int Cd, c
   out[(size_t)b * Cd + c] = n ? acc / (float)n : 0.f;
 }
 
+// Valid rows of a 0/1 mask in increasing order, by one workgroup: per 1024-entry chunk, wave
+// ballots give each valid entry its rank within its wave and the wave totals (through LDS)
+// its wave's offset.
+__global__ __launch_bounds__(1024) void valid_rows_kernel(int n, const float *__restrict__ mask,
+                                                         int32_t *__restrict__ idx, int *__restrict__ count) {
+  __shared__ int wsum[16];
+  __shared__ int base;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  if (t == 0) base = 0;
+  __syncthreads();
+  for (int c0 = 0; c0 < n; c0 += 1024) {
+    const int i = c0 + t;
+    const bool ok = i < n && mask[i] != 0.f;
+    const unsigned long long bal = __ballot(ok);
+    if (lane == 0) wsum[wave] = __popcll(bal);
+    __syncthreads();
+    int off = base;
+    for (int w = 0; w < wave; ++w) off += wsum[w];
+    if (ok) idx[off + __popcll(bal & ((1ull << lane) - 1ull))] = i;
+    __syncthreads();
+    if (t == 0) {
+      int s = 0;
+      for (int w = 0; w < 16; ++w) s += wsum[w];
+      base += s;
+    }
+    __syncthreads();
+  }
+  if (t == 0) *count = base;
+}
+
 // LSE over the (max, sum exp) partials of one row: L = M + log(sum_t s_t exp(m_t - M)).
 // With `logits`, the row's stored logits become logits - L in place.
 __global__ __launch_bounds__(kT) void lse_kernel(int M, int ntiles, const float2 *__restrict__ part,
@@ -328,6 +358,11 @@ hipError_t launch_masked_mean(int B, int S, int Cd, const void *ctx, int ctx_bf1
     hipLaunchKernelGGL(masked_mean_kernel<bf16>, grid, dim3(kT), 0, st, B, S, Cd, (const bf16 *)ctx, mask, out);
   else
     hipLaunchKernelGGL(masked_mean_kernel<float>, grid, dim3(kT), 0, st, B, S, Cd, (const float *)ctx, mask, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_valid_rows(int n, const float *mask, int32_t *idx, int *count, hipStream_t st) {
+  hipLaunchKernelGGL(valid_rows_kernel, dim3(1), dim3(1024), 0, st, n, mask, idx, count);
   return hipGetLastError();
 }
 
