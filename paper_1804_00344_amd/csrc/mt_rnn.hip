@@ -233,12 +233,16 @@ __global__ __launch_bounds__(kT) void masked_mean_kernel(int B, int S, int Cd, c
   const int b = blockIdx.y;
   const int c = blockIdx.x * kT + threadIdx.x;
   if (c >= Cd) return;
+  // no branch on the mask: every row is loaded (in bounds) and masked rows are selected away,
+  // so the loads of successive positions overlap
   float acc = 0.f;
   int n = 0;
+#pragma unroll 8
   for (int i = 0; i < S; ++i) {
-    if (mask[(size_t)b * S + i] == 0.f) continue;
-    acc += to_f32(ctx[((size_t)b * S + i) * Cd + c]);
-    ++n;
+    const bool ok = mask[(size_t)b * S + i] != 0.f;
+    const float x = to_f32(ctx[((size_t)b * S + i) * Cd + c]);
+    acc += ok ? x : 0.f;
+    n += ok ? 1 : 0;
   }
   out[(size_t)b * Cd + c] = n ? acc / (float)n : 0.f;
 }
