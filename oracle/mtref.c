@@ -77,6 +77,26 @@ void mtref_gru(int in_dim, int H, const double *x, const double *h,
   free(u);
 }
 
+/* Transition block (Section 3.1.1: the deep-transition decoder cell stacks eight GRU
+ * blocks per step, attention between the first and the second).  Blocks past the second
+ * receive no external input, so their input path reduces to its bias; with layer
+ * normalisation only the recurrent product's H-blocks are normalised (the input path has
+ * no product to normalise).  Reading of the paper, which names the blocks only. */
+void mtref_gru_transition(int H, const double *h, const float *U, const float *b,
+                          const float *ln_gu, const float *ln_bu, double eps, double *out) {
+  double *u = (double *)malloc(sizeof(double) * 3 * H);
+  vec_mat(H, 3 * H, 3 * H, h, U, NULL, u);
+  if (ln_gu)
+    for (int g = 0; g < 3; ++g) mtref_layer_norm(H, u + g * H, ln_gu + g * H, ln_bu + g * H, eps, u + g * H);
+  for (int j = 0; j < H; ++j) {
+    double r = sigmoid((double)b[j] + u[j]);
+    double z = sigmoid((double)b[H + j] + u[H + j]);
+    double hh = tanh((double)b[2 * H + j] + r * u[2 * H + j]);
+    out[j] = (1.0 - z) * hh + z * h[j];
+  }
+  free(u);
+}
+
 /* Additive (Bahdanau) attention with a masked softmax (Section 2.1 "attention
  * mechanisms"; Section 2.2: the encoder context and its mask live in the
  * EncoderState).  The maximum is taken over valid positions only; masked
@@ -174,7 +194,8 @@ int mtref_step(const mtref_dims *d, const mtref_weights *w, int B, int K, int S,
                float *state_out, float *logp_out, float *alpha_out,
                float *s1_out, float *c_out, float *t_out) {
   if (!d || !w || B < 0 || K < 1 || S < 1 || !prev_tok || !src_row || !state_in || !ctx ||
-      !P || !mask || !state_out)
+      !P || !mask || !state_out || d->transitions < 0 ||
+      (d->transitions > 0 && (!w->Ut || !w->btr || (d->layer_norm && (!w->gtu || !w->betu)))))
     return -1;
   const int E = d->E, H = d->H, C = 2 * d->H, A = d->A, V = d->V;
   const int M = B * K;
@@ -222,7 +243,15 @@ int mtref_step(const mtref_dims *d, const mtref_weights *w, int B, int K, int S,
     /* GRU block 2: input = attention context, state = s1 */
     mtref_gru(C, H, c, s1, w->W2, w->U2, w->b2, ln ? w->g2a : NULL, ln ? w->be2a : NULL,
               ln ? w->g2u : NULL, ln ? w->be2u : NULL, d->ln_eps, s);
-    round_store(H, s, state_out + (size_t)m * H, s);
+    round_store(H, s, f, s);
+    /* deep transition: recurrent-only blocks, each output stored in fp32 */
+    for (int j = 0; j < d->transitions; ++j) {
+      mtref_gru_transition(H, s, w->Ut + (size_t)j * H * 3 * H, w->btr + (size_t)j * 3 * H,
+                           ln ? w->gtu + (size_t)j * 3 * H : NULL, ln ? w->betu + (size_t)j * 3 * H : NULL,
+                           d->ln_eps, s1);
+      round_store(H, s1, f, s);
+    }
+    memcpy(state_out + (size_t)m * H, f, sizeof(float) * H);
 
     /* deep-output readout: tanh of the sum of three projections to E */
     vec_mat(H, E, E, s, w->Wt_s, w->bt, t);

@@ -26,6 +26,7 @@ typedef struct {
   int32_t layer_norm;   /* 1: LN on every gate block of both paths and the readout */
   int32_t tied_output;  /* 1: output matrix is emb transposed */
   double ln_eps;
+  int32_t transitions;  /* recurrent-only GRU blocks after GRU 2 (deep transition); 0: shallow */
 } mtref_dims;
 
 typedef struct {
@@ -38,6 +39,9 @@ typedef struct {
   const float *Wi, *bi;             /* [C,H], [H] */
   /* layer norm (only read if layer_norm): gain/shift per path, [3H] each; readout [E] */
   const float *g1a, *be1a, *g1u, *be1u, *g2a, *be2a, *g2u, *be2u, *gt, *bet;
+  /* transition blocks j < transitions, stacked: Ut [T][H,3H], btr [T][3H]; layer norm of
+   * their recurrent products (only read if layer_norm): gtu, betu [T][3H] */
+  const float *Ut, *btr, *gtu, *betu;
 } mtref_weights;
 
 /* status: 0 ok, -1 bad argument, -2 index out of range */
@@ -57,6 +61,14 @@ void mtref_gru(int in_dim, int H, const double *x, const double *h,
                const float *W, const float *U, const float *b,
                const float *ln_ga, const float *ln_ba, const float *ln_gu, const float *ln_bu,
                double eps, double *out);
+
+/* One transition block of a deep-transition decoder cell: a GRU block with no
+ * external input, so its input path is the bias alone:
+ *   u = h U, (optionally LN on each H-block of u),
+ *   r = sig(b_r + u_r), z = sig(b_z + u_z), hh = tanh(b_h + r * u_h),
+ *   out = (1 - z) * hh + z * h. */
+void mtref_gru_transition(int H, const double *h, const float *U, const float *b,
+                          const float *ln_gu, const float *ln_bu, double eps, double *out);
 
 /* Additive attention over S positions of one sentence for one query q[A]:
  *   e_i = sum_a va[a] tanh(P[i,a] + q[a]) for valid i (mask[i] != 0),
@@ -81,6 +93,7 @@ int mtref_precompute(const mtref_dims *d, const mtref_weights *w, int B, int S,
 /* One decoder step for M = B*K hypothesis rows (row m belongs to sentence m / K):
  *   x = emb[prev_tok[m]], h = state_in[src_row[m]]  (src_row < n_state_rows),
  *   s1 = GRU1(x, h), q = s1 Wa, (alpha, c) = attention(q), s = GRU2(c, s1),
+ *   then s = transition_j(s) for j < transitions (deep transition),
  *   t = tanh(LN?(s Wt_s + x Wt_y + c Wt_c + bt)), logits = t Wo + bo,
  *   logp = log_softmax(logits).
  * Optional outputs (may be NULL): logp [M,V], alpha [M,S], s1/c/t taps. */

@@ -36,12 +36,15 @@ def build(force: bool = True) -> str:
 
 class _Dims(C.Structure):
     _fields_ = [("E", C.c_int32), ("H", C.c_int32), ("A", C.c_int32), ("V", C.c_int32),
-                ("layer_norm", C.c_int32), ("tied_output", C.c_int32), ("ln_eps", C.c_double)]
+                ("layer_norm", C.c_int32), ("tied_output", C.c_int32), ("ln_eps", C.c_double),
+                ("transitions", C.c_int32)]
 
 
 _WNAMES = ["emb", "W1", "U1", "b1", "Ua", "ba", "Wa", "va", "W2", "U2", "b2",
            "Wt_s", "Wt_y", "Wt_c", "bt", "Wo", "bo", "Wi", "bi",
-           "g1a", "be1a", "g1u", "be1u", "g2a", "be2a", "g2u", "be2u", "gt", "bet"]
+           "g1a", "be1a", "g1u", "be1u", "g2a", "be2a", "g2u", "be2u", "gt", "bet",
+           "Ut", "btr", "gtu", "betu"]
+_LN_NAMES = ("g1a", "be1a", "g1u", "be1u", "g2a", "be2a", "g2u", "be2u", "gt", "bet")
 
 
 class _Weights(C.Structure):
@@ -61,6 +64,8 @@ def lib():
         L.mtref_layer_norm.restype = None
         L.mtref_gru.argtypes = [C.c_int, C.c_int, _d, _d, _f, _f, _f, _f, _f, _f, _f, C.c_double, _d]
         L.mtref_gru.restype = None
+        L.mtref_gru_transition.argtypes = [C.c_int, _d, _f, _f, _f, _f, C.c_double, _d]
+        L.mtref_gru_transition.restype = None
         L.mtref_attention.argtypes = [C.c_int, C.c_int, C.c_int, _d, _f, _f, _f, _f, _d, _d]
         L.mtref_attention.restype = None
         L.mtref_log_softmax.argtypes = [C.c_int, _d, _d]
@@ -125,6 +130,18 @@ def gru(x, h, W, U, b, ln=None, eps=1e-5) -> np.ndarray:
     return out
 
 
+def gru_transition(h, U, b, ln=None, eps=1e-5) -> np.ndarray:
+    """Transition block (no external input); ln: None or (gamma_u, beta_u), each [3H]."""
+    h = f64(h)
+    U, b = f32(U), f32(b)
+    H = h.size
+    assert U.shape == (H, 3 * H) and b.shape == (3 * H,)
+    out = np.empty(H, np.float64)
+    lnp = [None] * 2 if ln is None else [f32(t) for t in ln]
+    lib().mtref_gru_transition(H, _dp(h), _fp(U), _fp(b), *[_fp(t) for t in lnp], eps, _dp(out))
+    return out
+
+
 def attention(q, P, Cx, mask, va):
     q, P, Cx, mask, va = f64(q), f32(P), f32(Cx), f32(mask), f32(va)
     S, A = P.shape
@@ -149,10 +166,12 @@ class Model:
     """Holds the fp32 weights (row-major logical [in x out]) and the dims."""
 
     def __init__(self, E: int, H: int, A: int, V: int, weights: Dict[str, np.ndarray],
-                 layer_norm: bool = False, tied_output: bool = False, ln_eps: float = 1e-5):
+                 layer_norm: bool = False, tied_output: bool = False, ln_eps: float = 1e-5,
+                 transitions: int = 0):
         self.E, self.H, self.A, self.V = E, H, A, V
         self.C = 2 * H
-        self.dims = _Dims(E, H, A, V, int(layer_norm), int(tied_output), ln_eps)
+        self.T = transitions
+        self.dims = _Dims(E, H, A, V, int(layer_norm), int(tied_output), ln_eps, transitions)
         self._keep = {}
         shapes = {
             "emb": (V, E), "W1": (E, 3 * H), "U1": (H, 3 * H), "b1": (3 * H,),
@@ -165,11 +184,18 @@ class Model:
             shapes[n] = (3 * H,)
         shapes["gt"] = (E,)
         shapes["bet"] = (E,)
+        T = transitions
+        shapes.update({"Ut": (T, H, 3 * H), "btr": (T, 3 * H), "gtu": (T, 3 * H), "betu": (T, 3 * H)})
         ptrs = {}
         for n in _WNAMES:
             a = weights.get(n)
+            if n in ("Ut", "btr", "gtu", "betu") and T == 0:
+                a = None  # a shallow model reads no transition weights
             if a is None:
-                if n in ("g1a", "be1a", "g1u", "be1u", "g2a", "be2a", "g2u", "be2u", "gt", "bet") and not layer_norm:
+                if n in _LN_NAMES and not layer_norm:
+                    ptrs[n] = None
+                    continue
+                if n in ("Ut", "btr", "gtu", "betu") and (T == 0 or (n in ("gtu", "betu") and not layer_norm)):
                     ptrs[n] = None
                     continue
                 if n == "Wo" and tied_output:

@@ -528,3 +528,128 @@ def test_beam_permutation_invariance():
         a = sorted(zip(s1[sl].tolist(), t1[sl].tolist(), src[b * K + b1[sl]].tolist()))
         c = sorted(zip(s2[sl].tolist(), t2[sl].tolist(), src[perm][b * K + b2[sl]].tolist()))
         assert a == c
+
+
+# --------------------------------------------------------------------------------------
+# deep transition (Section 3.1.1: eight GRU blocks per decoder step, attention between
+# the first and the second; the blocks past the second have no external input)
+# --------------------------------------------------------------------------------------
+
+
+def torch_transition(h, U, b):
+    """A transition block is a GRU block whose input is zero: torch.nn.GRUCell with a
+    zero input and bias_ih = b (the input path reduces to its bias)."""
+    H = h.size
+    cell = torch.nn.GRUCell(1, H, bias=True).double()
+    with torch.no_grad():
+        cell.weight_ih.fill_(0.37)  # multiplies the zero input: must not matter
+        cell.weight_hh.copy_(torch.from_numpy(U.astype(np.float64).T))
+        cell.bias_ih.copy_(torch.from_numpy(b.astype(np.float64)))
+        cell.bias_hh.zero_()
+        out = cell(torch.zeros(1, 1, dtype=torch.float64), torch.from_numpy(h.astype(np.float64))[None])
+    return out[0].numpy()
+
+
+@pytest.mark.parametrize("H", [1, 5, 16])
+def test_transition_equals_torch_grucell_with_zero_input(H):
+    rng = np.random.default_rng(300 + H)
+    h = np.tanh(rnd(H, rng=rng))
+    U, b = rnd(H, 3 * H, s=0.7, rng=rng), rnd(3 * H, s=0.5, rng=rng)
+    assert np.max(np.abs(mtref.gru_transition(h, U, b) - torch_transition(h, U, b))) <= 1e-12
+
+
+def test_transition_closed_forms():
+    rng = np.random.default_rng(31)
+    H = 6
+    h = np.tanh(rnd(H, rng=rng))
+    b = rnd(3 * H, rng=rng)
+    sig = lambda v: 1.0 / (1.0 + np.exp(-v.astype(np.float64)))
+    # U = 0: s = (1 - sig(b_z)) tanh(b_h) + sig(b_z) h
+    z = sig(b[H:2 * H])
+    want = (1 - z) * np.tanh(b[2 * H:].astype(np.float64)) + z * h
+    assert np.max(np.abs(mtref.gru_transition(h, np.zeros((H, 3 * H), np.float32), b) - want)) <= 1e-15
+    # b_z = +40: the block copies its state whatever U is
+    b2 = b.copy()
+    b2[H:2 * H] = 40.0
+    got = mtref.gru_transition(h, rnd(H, 3 * H, rng=rng), b2)
+    assert np.max(np.abs(got - h)) <= 1e-15
+
+
+def test_ln_transition_zero_weights_gives_shift_gates():
+    """u = 0 normalises to its shift beta: r = sig(b_r + beta_r), z = sig(b_z + beta_z),
+    hh = tanh(b_h + r beta_h) (the bias stays outside the normalisation)."""
+    rng = np.random.default_rng(32)
+    H = 5
+    h = np.tanh(rnd(H, rng=rng))
+    b, g, be = rnd(3 * H, rng=rng), 1 + rnd(3 * H, s=0.2, rng=rng), rnd(3 * H, s=0.5, rng=rng)
+    got = mtref.gru_transition(h, np.zeros((H, 3 * H), np.float32), b, ln=(g, be))
+    sig = lambda v: 1.0 / (1.0 + np.exp(-v))
+    b64, be64 = b.astype(np.float64), be.astype(np.float64)
+    r = sig(b64[:H] + be64[:H])
+    z = sig(b64[H:2 * H] + be64[H:2 * H])
+    want = (1 - z) * np.tanh(b64[2 * H:] + r * be64[2 * H:]) + z * h
+    assert np.max(np.abs(got - want)) <= 1e-15
+
+
+def test_ln_transition_scale_invariance():
+    """With layer norm only on the recurrent product, scaling U leaves the block unchanged
+    (a normalisation that took the bias inside would not be)."""
+    rng = np.random.default_rng(33)
+    H = 16
+    h = np.tanh(rnd(H, rng=rng))
+    U, b = rnd(H, 3 * H, rng=rng), rnd(3 * H, s=0.5, rng=rng)
+    g, be = 1 + rnd(3 * H, s=0.1, rng=rng), rnd(3 * H, s=0.1, rng=rng)
+    a = mtref.gru_transition(h, U, b, ln=(g, be), eps=1e-12)
+    c = mtref.gru_transition(h, (U * 8).astype(np.float32), b, ln=(g, be), eps=1e-12)
+    assert np.max(np.abs(a - c)) <= 1e-9
+
+
+def deep_model(T, seed=40, layer_norm=False, **over):
+    rng = np.random.default_rng(seed + 1000)
+    H = H_
+    extra = dict(Ut=rnd(T, H, 3 * H, s=0.5, rng=rng), btr=rnd(T, 3 * H, s=0.3, rng=rng))
+    if layer_norm:
+        extra["gtu"] = (1 + rnd(T, 3 * H, s=0.1, rng=rng)).astype(np.float32)
+        extra["betu"] = rnd(T, 3 * H, s=0.1, rng=rng)
+    extra.update(over)
+    _, w = tiny_model(seed=seed, layer_norm=layer_norm)
+    w.update(extra)
+    return mtref.Model(E_, H_, A_, V_, w, layer_norm=layer_norm, transitions=T), w
+
+
+@pytest.mark.parametrize("layer_norm", [False, True])
+def test_deep_step_with_copying_transitions_equals_shallow(layer_norm):
+    T, H = 3, H_
+    btr = np.zeros((T, 3 * H), np.float32)
+    btr[:, H:2 * H] = 40.0  # z = 1: every transition block copies its state
+    deep, w = deep_model(T, seed=41, layer_norm=layer_norm, btr=btr)
+    shallow = mtref.Model(E_, H_, A_, V_, w, layer_norm=layer_norm)
+    ctx, mask, lens, tok, src, state = tiny_batch(seed=42)
+    P, _ = shallow.precompute(ctx, mask)
+    a = deep.step(2, tok, src, state, ctx, P, mask)
+    b = shallow.step(2, tok, src, state, ctx, P, mask)
+    assert np.array_equal(a["state"], b["state"]) and np.array_equal(a["logp"], b["logp"])
+
+
+def test_deep_step_equals_torch_reexpression():
+    """The transition blocks run after GRU block 2 in order, and the readout and the new
+    state take the last block's output: the shallow step's state carried through
+    torch.nn.GRUCell(0, .) T times, then tanh(s Wt_s + x Wt_y + c Wt_c + bt), log_softmax."""
+    T = 2
+    deep, w = deep_model(T, seed=43)
+    shallow = mtref.Model(E_, H_, A_, V_, w)
+    ctx, mask, lens, tok, src, state = tiny_batch(seed=44)
+    P, _ = shallow.precompute(ctx, mask)
+    a = deep.step(2, tok, src, state, ctx, P, mask, taps=True)
+    b = shallow.step(2, tok, src, state, ctx, P, mask, taps=True)
+    Tt = lambda v: torch.from_numpy(np.asarray(v, np.float64))
+    for m in range(tok.size):
+        s = b["state"][m].astype(np.float64)
+        for j in range(T):
+            s = torch_transition(s, w["Ut"][j], w["btr"][j])
+        assert np.max(np.abs(a["state"][m] - s)) <= 1e-6
+        t = torch.tanh(Tt(s) @ Tt(w["Wt_s"]) + Tt(w["emb"][tok[m]]) @ Tt(w["Wt_y"]) + Tt(b["c"][m]) @ Tt(w["Wt_c"])
+                       + Tt(w["bt"]))
+        assert np.max(np.abs(a["t"][m] - t.numpy())) <= 1e-6
+        lp = torch.log_softmax(t @ Tt(w["Wo"]) + Tt(w["bo"]), 0)
+        assert np.max(np.abs(a["logp"][m] - lp.numpy())) <= 1e-5
