@@ -49,7 +49,7 @@ def cpu_baseline(p, w, ctx, mask, budget_s=15.0):
     from oracle import mtref
     from paper_1804_00344_amd import synth
 
-    om = mtref.Model(p.E, p.H, p.A, p.V, w, layer_norm=p.layer_norm)
+    om = mtref.Model(p.E, p.H, p.A, p.V, w, layer_norm=p.layer_norm, transitions=p.transitions)
     tok, src, state, score = synth.mid_decode_inputs(p, salt=11)
     t_pre = t_step = 0.0
     n = 0
@@ -104,6 +104,7 @@ def main():
     from paper_1804_00344_amd.runner import Decoder
 
     p = synth.PRESETS[args.preset]
+    cell = (f"deep-transition cGRU ({2 + p.transitions} GRU blocks)" if p.transitions else "shallow cGRU")
     log(f"[bench] preset {p.name}: B={p.B} K={p.K} E={p.E} H={p.H} A={p.A} V={p.V} gemm={p.gemm} ln={p.layer_norm}")
     w = synth.make_weights(p)
     ctx, mask, lens = synth.make_source(p)
@@ -193,7 +194,7 @@ def main():
         "dtype": "f32" if p.gemm == "f32" else "bf16",
         "data": "synthetic (seeded; shapes and distributions of the preset)",
         "config": {
-            "workload": f"{p.name}: shallow cGRU attention decoder step + beam top-K, B={p.B} sentences, beam K={p.K}, "
+            "workload": f"{p.name}: {cell} attention decoder step + beam top-K, B={p.B} sentences, beam K={p.K}, "
                         f"E={p.E}, H={p.H}, C={p.C}, A={p.A}, V={p.V}, padded S={dec.S} (mean len {lens.mean():.1f}), "
                         f"{p.gemm} GEMMs, layer_norm={p.layer_norm}, precompute every {p.steps} steps",
             "B": p.B, "K": p.K, "S": dec.S, "V": p.V, "parallelism": "single GPU",

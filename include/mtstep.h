@@ -73,7 +73,13 @@ typedef enum { MT_F32 = 0, MT_BF16 = 1 } mt_dtype;
  *   layer_norm: 0/1 — LN on each gate block of both paths of both GRUs and
  *     on the readout pre-activation (eps = ln_eps, biased variance).
  *   tied_output: 0/1 — the output matrix is emb transposed (Wo ignored).
- *   k_max: largest beam size the model will be called with, 1..16. */
+ *   k_max: largest beam size the model will be called with, 1..16.
+ *   dec_transitions: 0..16 — recurrent-only GRU blocks after GRU 2 (the
+ *     deep-transition decoder cell of Section 3.1.1: eight blocks in all,
+ *     attention between the first and the second, is 6); 0 is the shallow
+ *     cGRU.  Such a block has no external input (its input path is its bias
+ *     alone); with layer_norm its recurrent product is normalised per gate
+ *     block.  The new state and the readout take the last block's output. */
 typedef struct {
   int32_t E, H, A, V;
   int32_t layer_norm;
@@ -81,6 +87,7 @@ typedef struct {
   int32_t k_max;
   int32_t gemm_dtype;
   float ln_eps;
+  int32_t dec_transitions;
 } mt_config;
 
 /* Model parameters: HOST pointers to fp32, row-major logical [in x out]
@@ -90,7 +97,9 @@ typedef struct {
  *   W2[C,3H] U2[H,3H] b2[3H]; Wt_s[H,E] Wt_y[E,E] Wt_c[C,E] bt[E];
  *   Wo[E,V] bo[V]; Wi[C,H] bi[H];
  *   layer norm (read only if layer_norm): gain/shift of the input path (a)
- *   and recurrent path (u) of GRU 1 and 2, [3H] each; readout gt/bet [E]. */
+ *   and recurrent path (u) of GRU 1 and 2, [3H] each; readout gt/bet [E];
+ *   transition blocks (read only if dec_transitions = T > 0), stacked by
+ *   block: Ut[T,H,3H] btr[T,3H], and with layer_norm gtu/betu[T,3H]. */
 typedef struct {
   const float *emb;
   const float *W1, *U1, *b1;
@@ -100,6 +109,7 @@ typedef struct {
   const float *Wo, *bo;
   const float *Wi, *bi;
   const float *g1a, *be1a, *g1u, *be1u, *g2a, *be2a, *g2u, *be2u, *gt, *bet;
+  const float *Ut, *btr, *gtu, *betu;
 } mt_weights;
 
 typedef struct mt_model mt_model; /* opaque, library-owned */
@@ -196,7 +206,8 @@ typedef enum {
   MT_KERNEL_TOPK = 9,       /* all top-K kernels (row log-sum-exp merge included) */
   MT_KERNEL_PRECOMPUTE = 10,
   MT_KERNEL_VOCAB_THRESHOLD = 11, /* logits of the first vocabulary entries -> candidate threshold */
-  MT_KERNEL_COUNT = 12
+  MT_KERNEL_GEMM_TRANSITION = 12, /* s Ut_j of the transition blocks (dec_transitions > 0) */
+  MT_KERNEL_COUNT = 13
 } mt_kernel_id;
 
 mt_status mt_profile_enable(mt_model *model, uint32_t kernel_mask);

@@ -40,6 +40,7 @@ constexpr int kKPadFrag = 128;            // K padding of bf16 weights (one LDS 
 // (64 sentences x beam 12, their 5000 or so source positions, the sentences): a model serves
 // any batch, only the speed of other row counts may differ.
 constexpr long kRefRows = 768, kRefCtxRows = 4096, kRefSentences = 64;
+constexpr int kMaxTransitions = 16;  // recurrent-only GRU blocks after GRU 2
 
 size_t rup(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -73,6 +74,9 @@ struct mt_model {
   float *embx;    // [V][3H+E] fp32: emb [W1 | Wt_y] + [b1 | 0], the token side of GRU 1 and the readout
   float *bias1x, *bias3, *ba, *bi, *bt, *va;
   float *ln[10];  // g1a be1a g1u be1u g2a be2a g2u be2u gt bet
+  std::vector<Packed> wtr;        // transition blocks' recurrent matrices
+  float *btr = nullptr;           // [T][3H] their biases
+  float *gtu = nullptr, *betu = nullptr;  // [T][3H] layer norm of their recurrent products
   int32_t *err;
   std::vector<void *> allocs;
   // call-order state for mt_beam_topk(logp = NULL)
@@ -103,6 +107,8 @@ mt_status check_cfg(const mt_config *c) {
   if (c->tied_output != 0 && c->tied_output != 1) return fail(MT_ERR_ARG, "tied_output must be 0 or 1");
   if (c->gemm_dtype != MT_F32 && c->gemm_dtype != MT_BF16)
     return fail(MT_ERR_DTYPE, "gemm_dtype=%d: need MT_F32 or MT_BF16", c->gemm_dtype);
+  if (c->dec_transitions < 0 || c->dec_transitions > kMaxTransitions)
+    return fail(MT_ERR_SHAPE, "dec_transitions=%d: need 0..%d", c->dec_transitions, kMaxTransitions);
   if (c->layer_norm && !(c->ln_eps > 0.f && std::isfinite(c->ln_eps)))
     return fail(MT_ERR_ARG, "ln_eps must be positive and finite");
   if (vocab_rows_per_block(c->gemm_dtype == MT_BF16, c->E) == 0)
@@ -207,7 +213,7 @@ std::vector<float> cat(std::initializer_list<std::pair<const float *, int>> part
 
 // ---- workspace ----
 struct WsLayout {
-  size_t gh, s1, g2, c, g3, g4, t, sample, thr, part, cbuf, ccnt, lse, rowc, scand, scnt, s1h, ch, sth, total;
+  size_t gh, s1, g2, c, g3, g4, t, sample, thr, part, cbuf, ccnt, lse, rowc, scand, scnt, s1h, ch, sth, sx, total;
   int ntiles, kc, nchunks;
 };
 
@@ -245,6 +251,8 @@ WsLayout ws_layout(const mt_model *m, int B, int K) {
   L.s1h = take(M * H * h16);
   L.ch = take(M * C * h16);
   L.sth = take(M * H * h16);
+  // transition blocks alternate between state_out and this buffer
+  L.sx = take(c.dec_transitions > 0 ? M * H * 4 : 0);
   L.total = off;
   return L;
 }
@@ -351,6 +359,11 @@ mt_status mt_load_weights(const mt_config *cfg, const mt_weights *w, mt_model **
   if (c.layer_norm)
     for (int i = 0; i < 10; ++i)
       if (!lnp[i]) return fail(MT_ERR_ARG, "layer-norm parameter %d is NULL (layer_norm = 1)", i);
+  if (c.dec_transitions > 0) {
+    if (!w->Ut || !w->btr) return fail(MT_ERR_ARG, "Ut or btr is NULL (dec_transitions = %d)", c.dec_transitions);
+    if (c.layer_norm && (!w->gtu || !w->betu))
+      return fail(MT_ERR_ARG, "gtu or betu is NULL (dec_transitions > 0, layer_norm = 1)");
+  }
 
   mt_model *m = new (std::nothrow) mt_model();
   if (!m) return fail(MT_ERR_OOM, "host allocation failed");
@@ -436,6 +449,17 @@ mt_status mt_load_weights(const mt_config *cfg, const mt_weights *w, mt_model **
     for (int i = 0; i < 10; ++i) {
       m->ln[i] = nullptr;
       if (c.layer_norm) CHECK(upload_vec(m, cat({{lnp[i], i < 8 ? 3 * H : E}}), &m->ln[i]));
+    }
+    const int T = c.dec_transitions;
+    m->wtr.resize(T);
+    for (int j = 0; j < T; ++j)
+      CHECK(upload_packed(m, {{w->Ut + (size_t)j * H * 3 * H, 3 * H}}, H, kRefRows, &m->wtr[j]));
+    if (T > 0) {
+      CHECK(upload_vec(m, cat({{w->btr, T * 3 * H}}), &m->btr));
+      if (c.layer_norm) {
+        CHECK(upload_vec(m, cat({{w->gtu, T * 3 * H}}), &m->gtu));
+        CHECK(upload_vec(m, cat({{w->betu, T * 3 * H}}), &m->betu));
+      }
     }
     int32_t zero = 0;
     CHECK(dev_upload(m, &zero, sizeof zero, (void **)&m->err));
@@ -603,10 +627,28 @@ mt_status mt_decoder_step(mt_model *model, int B, int K, int S, const int32_t *p
   p3.Bp = model->w3.p; p3.ldb = model->w3.ldb; p3.wblk = model->w3.blk; p3.bias = model->bias3;
   p3.out = g3; p3.ldc = 3 * H + E; p3.M = M; p3.N = 3 * H + E; p3.K = C;
   LAUNCH(MT_KERNEL_GEMM_CTX, launch_gemm(bf, &p3, 1, EPI_STORE, st));
+  // GRU 2, then the transition blocks of a deep-transition cell (recurrent product s Ut_j,
+  // then the cell with the bias row as its input path), alternating between state_out and a
+  // workspace buffer so that the last block writes state_out
+  const int T = c.dec_transitions;
+  float *sx = (float *)(W + L.sx);
+  auto dest = [&](int i) { return ((T - i) % 2 == 0) ? state_out : sx; };  // output of block i (0: GRU 2)
   LAUNCH(MT_KERNEL_GRU_CELL,
          launch_gru_cell(M, H, g3, 3 * H + E, nullptr, M, g2 + A, A + 3 * H, s1, nullptr, M, model->err,
-                         LNon ? ln[4] : nullptr, ln[5], ln[6], ln[7], eps, state_out, H,
+                         LNon ? ln[4] : nullptr, ln[5], ln[6], ln[7], eps, dest(0), H,
                          bf ? (bf16 *)(W + L.sth) : nullptr, nullptr, st));
+  for (int j = 0; j < T; ++j) {
+    GemmProblem pt{};
+    pt.A = bf ? (const void *)(W + L.sth) : (const void *)dest(j); pt.a_rows = M; pt.lda = H; pt.a_bf16 = bf;
+    pt.Bp = model->wtr[j].p; pt.ldb = model->wtr[j].ldb; pt.wblk = model->wtr[j].blk;
+    pt.out = gh; pt.ldc = 3 * H; pt.M = M; pt.N = 3 * H; pt.K = H;
+    LAUNCH(MT_KERNEL_GEMM_TRANSITION, launch_gemm(bf, &pt, 1, EPI_STORE, st));
+    const size_t o = (size_t)j * 3 * H;
+    LAUNCH(MT_KERNEL_GRU_CELL,
+           launch_gru_cell(M, H, model->btr + o, 0, nullptr, 1, gh, 3 * H, dest(j), nullptr, M, model->err,
+                           nullptr, nullptr, LNon ? model->gtu + o : nullptr, LNon ? model->betu + o : nullptr,
+                           eps, dest(j + 1), H, bf ? (bf16 *)(W + L.sth) : nullptr, nullptr, st));
+  }
   // readout: s Wt_s, then tanh(LN?(s Wt_s + x Wt_y + c Wt_c + bt))
   GemmProblem p4{};
   p4.A = bf ? (const void *)(W + L.sth) : (const void *)state_out; p4.a_rows = M; p4.lda = H; p4.a_bf16 = bf;

@@ -422,7 +422,9 @@ constexpr int kVocabPad = 64;  // vocabulary rows are padded to a multiple of th
 
 // GRU cell for M rows; a row m = aidx[m] (if given), previous state row hidx[m] (if given);
 // out-of-range indices are clamped and flagged in err (bit 0: aidx, bit 1: hidx); out16 (if
-// given) receives a bf16 copy [M][H] of the new state
+// given) receives a bf16 copy [M][H] of the new state.  Layer norm: ga..bu all given, both
+// paths; ga = ba = NULL with gu, bu given, the recurrent path only (a transition block, whose
+// input path is its bias row, passed as a with lda = 0)
 hipError_t launch_gru_cell(int M, int H, const float *a, int lda, const int32_t *aidx, int arows,
                            const float *u, int ldu, const float *hsrc, const int32_t *hidx, int hrows,
                            int32_t *err, const float *ga, const float *ba, const float *gu, const float *bu,

@@ -52,7 +52,9 @@ __device__ __forceinline__ int clamp_row(const int32_t *idx, int m, int rows, in
 // layer norm each of the six blocks is normalised on its own before the gates.  Row m
 // reads a from row aidx[m] (if given; error bit 0 on a clamp) and the previous state from
 // row hidx[m] (if given; error bit 1).  G = 16-byte granules per thread per block.
-template <int G, bool LN>
+// LNM: 0 no layer norm; 1 on all six blocks; 2 on the recurrent blocks only (a transition
+// block of a deep-transition cell: a is its bias row, read with lda = 0).
+template <int G, int LNM>
 __global__ __launch_bounds__(kT) void gru_cell_kernel(int M, int H, const float *__restrict__ a, int lda,
                                                       const int32_t *__restrict__ aidx, int arows,
                                                       const float *__restrict__ u, int ldu,
@@ -65,6 +67,8 @@ __global__ __launch_bounds__(kT) void gru_cell_kernel(int M, int H, const float 
                                                       float *__restrict__ out, int ldo,
                                                       bf16 *__restrict__ out16,
                                                       float *__restrict__ tap) {
+  constexpr bool LN = LNM != 0;
+  constexpr int G0 = LNM == 2 ? 3 : 0;  // first normalised block
   __shared__ float red[4][12];
   const int m = blockIdx.x;
   const int t = threadIdx.x;
@@ -84,11 +88,13 @@ __global__ __launch_bounds__(kT) void gru_cell_kernel(int M, int H, const float 
       const float4 va = ld4(arow + g * H + jc), vu = ld4(urow + g * H + jc);
       x[g][p][0] = va.x; x[g][p][1] = va.y; x[g][p][2] = va.z; x[g][p][3] = va.w;
       x[3 + g][p][0] = vu.x; x[3 + g][p][1] = vu.y; x[3 + g][p][2] = vu.z; x[3 + g][p][3] = vu.w;
-      if (LN) {
+      if (LNM == 1) {
         const float4 g0 = ld4(ga + g * H + jc), b0 = ld4(ba + g * H + jc);
-        const float4 g1 = ld4(gu + g * H + jc), b1 = ld4(bu + g * H + jc);
         lg[g][p][0] = g0.x; lg[g][p][1] = g0.y; lg[g][p][2] = g0.z; lg[g][p][3] = g0.w;
         lb[g][p][0] = b0.x; lb[g][p][1] = b0.y; lb[g][p][2] = b0.z; lb[g][p][3] = b0.w;
+      }
+      if (LN) {
+        const float4 g1 = ld4(gu + g * H + jc), b1 = ld4(bu + g * H + jc);
         lg[3 + g][p][0] = g1.x; lg[3 + g][p][1] = g1.y; lg[3 + g][p][2] = g1.z; lg[3 + g][p][3] = g1.w;
         lb[3 + g][p][0] = b1.x; lb[3 + g][p][1] = b1.y; lb[3 + g][p][2] = b1.z; lb[3 + g][p][3] = b1.w;
       }
@@ -123,7 +129,7 @@ __global__ __launch_bounds__(kT) void gru_cell_kernel(int M, int H, const float 
     block_sum<12>(st, red);
     const float invn = 1.0f / (float)H;
 #pragma unroll
-    for (int g = 0; g < 6; ++g) {
+    for (int g = G0; g < 6; ++g) {
       const float md = st[2 * g] * invn;
       const float var = fmaxf(st[2 * g + 1] * invn - md * md, 0.f);
       const float mean = sh[g] + md;
@@ -303,20 +309,25 @@ hipError_t launch_gru_cell(int M, int H, const float *a, int lda, const int32_t 
                            int32_t *err, const float *ga, const float *ba, const float *gu, const float *bu,
                            float eps, float *out, int ldo, bf16 *out16, float *tap, hipStream_t st) {
   if (M == 0) return hipSuccess;
-  const bool ln = ga != nullptr;
-#define MT_GRU(N)                                                                                        \
-  if (ln)                                                                                                \
-    hipLaunchKernelGGL((gru_cell_kernel<N, true>), dim3(M), dim3(kT), 0, st, M, H, a, lda, aidx, arows, \
-                       u, ldu, hsrc, hidx, hrows, err, ga, ba, gu, bu, eps, out, ldo, out16, tap);              \
-  else                                                                                                   \
-    hipLaunchKernelGGL((gru_cell_kernel<N, false>), dim3(M), dim3(kT), 0, st, M, H, a, lda, aidx, arows,\
-                       u, ldu, hsrc, hidx, hrows, err, ga, ba, gu, bu, eps, out, ldo, out16, tap);
+  // layer norm on both paths (ga given), on the recurrent path only (gu alone), or none
+  const int lnm = ga ? 1 : gu ? 2 : 0;
+#define MT_GRU_L(N, L)                                                                                  \
+  hipLaunchKernelGGL((gru_cell_kernel<N, L>), dim3(M), dim3(kT), 0, st, M, H, a, lda, aidx, arows, u,  \
+                     ldu, hsrc, hidx, hrows, err, ga, ba, gu, bu, eps, out, ldo, out16, tap)
+#define MT_GRU(N)              \
+  if (lnm == 1)                \
+    MT_GRU_L(N, 1);            \
+  else if (lnm == 2)           \
+    MT_GRU_L(N, 2);            \
+  else                         \
+    MT_GRU_L(N, 0);
   switch (gran_for(H)) {
     case 1: MT_GRU(1) break;
     case 2: MT_GRU(2) break;
     default: MT_GRU(4) break;
   }
 #undef MT_GRU
+#undef MT_GRU_L
   return hipGetLastError();
 }
 

@@ -20,7 +20,7 @@ MT_OK, MT_ERR_ARG, MT_ERR_SHAPE, MT_ERR_DTYPE, MT_ERR_HIP, MT_ERR_OOM, MT_ERR_ST
     0, -1, -2, -3, -4, -5, -6, -7)
 MT_F32, MT_BF16 = 0, 1
 KERNELS = ["GEMM_GRU1", "GRU_CELL", "GEMM_S1", "ATTENTION", "GEMM_CTX", "GEMM_READOUT", "READOUT",
-           "VOCAB_GEMM", "LSE", "TOPK", "PRECOMPUTE", "VOCAB_THRESHOLD"]
+           "VOCAB_GEMM", "LSE", "TOPK", "PRECOMPUTE", "VOCAB_THRESHOLD", "GEMM_TRANSITION"]
 KERNEL_ID = {n: i for i, n in enumerate(KERNELS)}
 
 
@@ -33,12 +33,12 @@ class MtError(RuntimeError):
 class mt_config(C.Structure):
     _fields_ = [("E", C.c_int32), ("H", C.c_int32), ("A", C.c_int32), ("V", C.c_int32),
                 ("layer_norm", C.c_int32), ("tied_output", C.c_int32), ("k_max", C.c_int32),
-                ("gemm_dtype", C.c_int32), ("ln_eps", C.c_float)]
+                ("gemm_dtype", C.c_int32), ("ln_eps", C.c_float), ("dec_transitions", C.c_int32)]
 
 
 WEIGHT_FIELDS = ["emb", "W1", "U1", "b1", "Ua", "ba", "Wa", "va", "W2", "U2", "b2", "Wt_s", "Wt_y",
                  "Wt_c", "bt", "Wo", "bo", "Wi", "bi", "g1a", "be1a", "g1u", "be1u", "g2a", "be2a",
-                 "g2u", "be2u", "gt", "bet"]
+                 "g2u", "be2u", "gt", "bet", "Ut", "btr", "gtu", "betu"]
 
 _fp = C.POINTER(C.c_float)
 
@@ -108,9 +108,10 @@ def _stream(stream) -> Optional[int]:
     return stream.cuda_stream
 
 
-def make_config(E, H, A, V, *, layer_norm=False, tied_output=False, k_max=16, gemm="f32", ln_eps=1e-5):
+def make_config(E, H, A, V, *, layer_norm=False, tied_output=False, k_max=16, gemm="f32", ln_eps=1e-5,
+                transitions=0):
     return mt_config(E, H, A, V, int(layer_norm), int(tied_output), k_max,
-                     MT_BF16 if gemm == "bf16" else MT_F32, ln_eps)
+                     MT_BF16 if gemm == "bf16" else MT_F32, ln_eps, transitions)
 
 
 class Model:

@@ -18,19 +18,20 @@ from . import mtstep as mt
 class Decoder:
     def __init__(self, E: int, H: int, A: int, V: int, weights: Dict[str, np.ndarray], *, gemm: str = "f32",
                  layer_norm: bool = False, tied_output: bool = False, k_max: int = 16, ln_eps: float = 1e-5,
-                 device: str = "cuda:0"):
+                 transitions: int = 0, device: str = "cuda:0"):
         self.E, self.H, self.A, self.V, self.C = E, H, A, V, 2 * H
         self.gemm = gemm
         self.device = torch.device(device)
         self.cfg = mt.make_config(E, H, A, V, layer_norm=layer_norm, tied_output=tied_output, k_max=k_max,
-                                  gemm=gemm, ln_eps=ln_eps)
+                                  gemm=gemm, ln_eps=ln_eps, transitions=transitions)
         with torch.cuda.device(self.device):
             self.model = mt.mt_load_weights(self.cfg, weights)
         self.io_dtype = torch.bfloat16 if gemm == "bf16" else torch.float32
 
     @classmethod
     def from_preset(cls, p, weights, **kw):
-        return cls(p.E, p.H, p.A, p.V, weights, gemm=p.gemm, layer_norm=p.layer_norm, k_max=max(p.K, 1), **kw)
+        return cls(p.E, p.H, p.A, p.V, weights, gemm=p.gemm, layer_norm=p.layer_norm, k_max=max(p.K, 1),
+                   transitions=p.transitions, **kw)
 
     # ---- batch ------------------------------------------------------------------------
     def set_batch(self, ctx: np.ndarray, mask: np.ndarray, K: int):

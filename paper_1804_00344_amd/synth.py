@@ -54,6 +54,7 @@ class Preset:
     layer_norm: bool
     steps: int
     start: str             # "bos" or "zipf"
+    transitions: int = 0   # recurrent-only GRU blocks after GRU 2 (deep-transition cell)
 
     @property
     def C(self) -> int:
@@ -75,6 +76,11 @@ PRESETS: Dict[str, Preset] = {
         # tiny dimensions with layer norm and bf16 GEMMs at B=64, K=12: the
         # second reading of "same shapes as config 1" for the bf16+LN preset
         Preset("tiny_bf16_ln", 5, 32, 64, 64, 1000, 64, 12, "uniform", 5, 10, "bf16", True, 50, "zipf"),
+        # deep-transition decoder cell (Section 3.1.1): eight GRU blocks per step, attention
+        # between the first and the second, layer norm; Nematus sizes, and tiny ones
+        Preset("deep_bf16_ln", 6, 512, 1024, 2048, 50000, 64, 12, "lognormal", 25, 80, "bf16", True, 50, "zipf", 6),
+        Preset("deep_f32_ln", 7, 512, 1024, 2048, 50000, 64, 12, "lognormal", 25, 80, "f32", True, 50, "zipf", 6),
+        Preset("tiny_deep_f32_ln", 8, 32, 64, 64, 1000, 8, 4, "uniform", 5, 10, "f32", True, 20, "zipf", 6),
     ]
 }
 
@@ -116,7 +122,8 @@ WEIGHT_NAMES = (
 )
 LN_NAMES = ("g1a", "be1a", "g1u", "be1u", "g2a", "be2a", "g2u", "be2u", "gt", "bet")
 # tensors that are GEMM operands (rounded to bf16 for bf16 presets)
-GEMM_OPERANDS = ("emb", "W1", "U1", "Ua", "Wa", "W2", "U2", "Wt_s", "Wt_y", "Wt_c", "Wo", "Wi")
+GEMM_OPERANDS = ("emb", "W1", "U1", "Ua", "Wa", "W2", "U2", "Wt_s", "Wt_y", "Wt_c", "Wo", "Wi", "Ut")
+TRANSITION_NAMES = ("Ut", "btr", "gtu", "betu")  # stacked over the transition blocks
 
 
 def make_weights(p: Preset, peaked_bias: bool = False) -> Dict[str, np.ndarray]:
@@ -155,9 +162,19 @@ def make_weights(p: Preset, peaked_bias: bool = False) -> Dict[str, np.ndarray]:
             w["be" + path] = rng_for(p, "be" + path).normal(0, 0.05, 3 * H).astype(np.float32)
         w["gt"] = (1.0 + rng_for(p, "gt").normal(0, 0.05, E)).astype(np.float32)
         w["bet"] = rng_for(p, "bet").normal(0, 0.05, E).astype(np.float32)
+    if p.transitions:
+        T = p.transitions
+        w["Ut"] = np.stack([_gate_matrix(p, f"Ut{j}", H) for j in range(T)])
+        w["btr"] = np.zeros((T, 3 * H), np.float32)
+        if p.layer_norm:
+            w["gtu"] = np.stack([(1.0 + rng_for(p, f"gtu{j}").normal(0, 0.05, 3 * H)).astype(np.float32)
+                                 for j in range(T)])
+            w["betu"] = np.stack([rng_for(p, f"betu{j}").normal(0, 0.05, 3 * H).astype(np.float32)
+                                  for j in range(T)])
     if p.gemm == "bf16":
         for k in GEMM_OPERANDS:
-            w[k] = round_bf16(w[k])
+            if k in w:
+                w[k] = round_bf16(w[k])
     return w
 
 

@@ -19,7 +19,7 @@ TOL = {
 
 
 def oracle_model(p: synth.Preset, w: Dict[str, np.ndarray]) -> mtref.Model:
-    return mtref.Model(p.E, p.H, p.A, p.V, w, layer_norm=p.layer_norm)
+    return mtref.Model(p.E, p.H, p.A, p.V, w, layer_norm=p.layer_norm, transitions=p.transitions)
 
 
 def sample_sentences(lens: np.ndarray, n: int) -> List[int]:

@@ -104,7 +104,9 @@ def masked_alpha_zero(p, gpu_alpha, mask):
 # ------------------------------------------------------------------------------------------
 
 N_SAMPLE = {"tiny_f32": 99, "tiny_bf16_ln": 99, "nematus_f32": 4, "nematus_bf16_ln": 4,
-            "vocab85k_bf16_ln": 4, "greedy_bf16_ln": 16}
+            "vocab85k_bf16_ln": 4, "greedy_bf16_ln": 16,
+            # deep-transition cell: six recurrent-only GRU blocks after GRU 2
+            "tiny_deep_f32_ln": 99, "deep_f32_ln": 3, "deep_bf16_ln": 3}
 
 
 # Nematus fp32 dimensions at other batch shapes: the fp32 products then run on the tile shapes
