@@ -59,6 +59,8 @@ def _load_status(cfg, weights):
     (dict(k_max=17), mt.MT_ERR_SHAPE),
     (dict(k_max=0), mt.MT_ERR_SHAPE),
     (dict(V=8, k_max=9), mt.MT_ERR_SHAPE),
+    (dict(transitions=-1), mt.MT_ERR_SHAPE),
+    (dict(transitions=17), mt.MT_ERR_SHAPE),
 ])
 def test_load_weights_rejects_bad_config(kw, status):
     p = synth.PRESETS["tiny_f32"]
@@ -88,6 +90,13 @@ def test_load_weights_rejects_missing_tensors():
     # layer norm on but its parameters absent
     rc, _ = _load_status(_cfg(layer_norm=True), w)
     assert rc == mt.MT_ERR_ARG
+    # transition blocks requested but their weights absent (or, with layer norm, their gains)
+    rc, _ = _load_status(_cfg(transitions=2), w)
+    assert rc == mt.MT_ERR_ARG and "Ut" in mt.lib().mt_last_error().decode()
+    wd = synth.make_weights(synth.PRESETS["tiny_deep_f32_ln"])
+    del wd["gtu"]
+    rc, _ = _load_status(_cfg(layer_norm=True, transitions=6), wd)
+    assert rc == mt.MT_ERR_ARG and "gtu" in mt.lib().mt_last_error().decode()
     # NULL config / weights / out
     L = mt.lib()
     h = C.c_void_p()

@@ -246,7 +246,7 @@ def test_precompute_parity(name):
 # same start; each sentence is compared until its first undecided (near-tie) selection
 # ------------------------------------------------------------------------------------------
 
-@pytest.mark.parametrize("name", ["tiny_f32", "tiny_bf16_ln"])
+@pytest.mark.parametrize("name", ["tiny_f32", "tiny_bf16_ln", "tiny_deep_f32_ln"])
 def test_tiny_trajectory(name):
     log(f"\n[trajectory] preset={name}")
     p, w, ctx, mask, lens, dec = setup(name, peaked=True)
