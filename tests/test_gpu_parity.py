@@ -246,9 +246,13 @@ def test_precompute_parity(name):
 # same start; each sentence is compared until its first undecided (near-tie) selection
 # ------------------------------------------------------------------------------------------
 
-@pytest.mark.parametrize("name", ["tiny_f32", "tiny_bf16_ln", "tiny_deep_f32_ln"])
-def test_tiny_trajectory(name):
-    log(f"\n[trajectory] preset={name}")
+# anchor=True: every step the oracle continues from the GPU's beam (state, tokens, backpointers,
+# scores), so each step is compared from identical inputs.  The deep-transition preset needs it:
+# with random weights its eight GRU blocks per step amplify a state difference from step to step,
+# so two free-running trajectories drift apart whatever the arithmetic.
+@pytest.mark.parametrize("name,anchor", [("tiny_f32", False), ("tiny_bf16_ln", False), ("tiny_deep_f32_ln", True)])
+def test_tiny_trajectory(name, anchor):
+    log(f"\n[trajectory] preset={name} anchor={anchor}")
     p, w, ctx, mask, lens, dec = setup(name, peaked=True)
     tol = TOL[p.gemm]
     om = oracle_model(p, w)
@@ -260,6 +264,7 @@ def test_tiny_trajectory(name):
     alive = np.ones(p.B, bool)
     logp = torch.empty((p.M, p.V), device=DEV)
     compared = 0
+    worst = []
     for t in range(p.steps):
         state = dec.advance(logp=logp)
         g_score, g_tok, g_bp, g_row = [x.cpu().numpy() for x in (dec.score, dec.tok, dec.bp, dec.row)]
@@ -281,12 +286,18 @@ def test_tiny_trajectory(name):
             # side continues from its own previous state, so after t + 1 steps the per-step
             # bound is accumulated t + 1 times (as for the scores above)
             err = maxerr(g_state[rows], out["state"][rows])
-            assert err <= tol["state"] * (t + 1), (name, t, b, err)
+            assert err <= tol["state"] * (1 if anchor else t + 1), (name, t, b, err)
+            worst.append(err)
             compared += 1
-        o_tok, o_bp, o_score = n_tok, n_bp, n_score
+        if anchor:
+            o_tok, o_bp, o_score = g_tok.copy(), g_bp.copy(), g_score.copy()
+            o_state = g_state.copy()
+        else:
+            o_tok, o_bp, o_score = n_tok, n_bp, n_score
+            o_state = out["state"]
         o_src = ((np.arange(p.M) // p.K) * p.K + o_bp).astype(np.int32)
-        o_state = out["state"]
-    log(f"[{name}] compared {compared} sentence-steps; alive at end {alive.sum()}/{p.B}")
+    log(f"[{name}] compared {compared} sentence-steps; alive at end {alive.sum()}/{p.B}; "
+        f"largest state error {max(worst) if worst else 0:.3g}")
     assert compared >= p.steps  # at least one sentence's worth of steps compared
 
 
