@@ -248,6 +248,18 @@ class Model:
         return out
 
 
+def ensemble_logp(logps, weights) -> np.ndarray:
+    """Ensemble of models decoding the same beams (Section 2.3, ensembling as a meta-algorithm
+    of batched beam search): the members' log-probabilities combined before one beam
+    selection, out[m, v] = sum_i weights[i] * logp_i[m, v], summed in double in member order
+    and stored in fp32.  The members' own states stay separate."""
+    assert len(logps) == len(weights) and len(logps) >= 1
+    acc = np.zeros(np.shape(logps[0]), np.float64)
+    for lp, w in zip(logps, weights):
+        acc += float(np.float32(w)) * f32(lp).astype(np.float64)
+    return acc.astype(np.float32)
+
+
 def topk(K, prev_score, logp):
     prev_score, logp = f32(prev_score), f32(logp)
     M, V = logp.shape

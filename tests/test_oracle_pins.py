@@ -653,3 +653,46 @@ def test_deep_step_equals_torch_reexpression():
         assert np.max(np.abs(a["t"][m] - t.numpy())) <= 1e-6
         lp = torch.log_softmax(t @ Tt(w["Wo"]) + Tt(w["bo"]), 0)
         assert np.max(np.abs(a["logp"][m] - lp.numpy())) <= 1e-5
+
+
+# --------------------------------------------------------------------------------------
+# ensembles (Section 2.3): the members' log-probabilities combined before one selection
+# --------------------------------------------------------------------------------------
+
+
+def test_ensemble_of_one_member_is_the_member():
+    lp = rnd(6, 11)
+    assert np.array_equal(mtref.ensemble_logp([lp], [1.0]), lp)
+
+
+def test_ensemble_of_identical_members_with_unit_weights_is_the_member():
+    lp = np.log(np.random.default_rng(50).dirichlet(np.ones(13), size=4)).astype(np.float32)
+    out = mtref.ensemble_logp([lp, lp, lp, lp], [0.25] * 4)
+    assert np.max(np.abs(out - lp)) == 0.0
+
+
+def test_ensemble_is_the_weighted_sum_with_torch():
+    rng = np.random.default_rng(51)
+    lps = [rnd(5, 9, rng=rng) for _ in range(3)]
+    w = [0.5, 0.3, 0.2]
+    ref = sum(torch.from_numpy(l.astype(np.float64)) * float(np.float32(x)) for l, x in zip(lps, w))
+    assert np.max(np.abs(mtref.ensemble_logp(lps, w) - ref.numpy())) <= 1e-6
+
+
+def test_ensemble_beam_of_two_copies_equals_single_model_beam():
+    """An ensemble of two copies of one model (weights 1/2, 1/2) selects exactly the single
+    model's beam at every step (the step of each member is the same)."""
+    model, w = tiny_model(seed=52)
+    ctx, mask, lens, tok, src, state = tiny_batch(seed=53)
+    P, _ = model.precompute(ctx, mask)
+    score = np.zeros(tok.size, np.float32)
+    for _ in range(4):
+        out = model.step(2, tok, src, state, ctx, P, mask)
+        ens = mtref.ensemble_logp([out["logp"], out["logp"]], [0.5, 0.5])
+        a = mtref.topk(2, score, out["logp"])
+        b = mtref.topk(2, score, ens)
+        for x, y in zip(a, b):
+            assert np.array_equal(x, y)
+        tok, bp, score = a
+        src = ((np.arange(tok.size) // 2) * 2 + bp).astype(np.int32)
+        state = out["state"]
