@@ -17,6 +17,7 @@ launch stream) and the CPU oracle's rate on a bounded sample.
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import hashlib
 import json
 import math
@@ -41,15 +42,19 @@ def source_hash(path):
     return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
 
 
-def cpu_baseline(p, w, ctx, mask, budget_s=15.0):
+def cpu_baseline(members, ctx, mask, budget_s=15.0):
     """The oracle (single-threaded C, double accumulation) on whole sentences of the same
-    workload: one precompute + decoder step + top-K per sentence, scaled to full-batch steps/s
-    with the precompute amortised over preset.steps steps."""
+    workload: one precompute + decoder step per member, their combination (ensembles) and
+    one top-K per sentence, scaled to full-batch steps/s with the precompute amortised over
+    preset.steps steps.  members: [(preset, weights)], the first one's shapes."""
     import numpy as np
     from oracle import mtref
     from paper_1804_00344_amd import synth
 
-    om = mtref.Model(p.E, p.H, p.A, p.V, w, layer_norm=p.layer_norm, transitions=p.transitions)
+    p = members[0][0]
+    oms = [mtref.Model(q.E, q.H, q.A, q.V, wq, layer_norm=q.layer_norm, transitions=q.transitions)
+           for q, wq in members]
+    ew = [1.0 / len(oms)] * len(oms)
     tok, src, state, score = synth.mid_decode_inputs(p, salt=11)
     t_pre = t_step = 0.0
     n = 0
@@ -58,11 +63,12 @@ def cpu_baseline(p, w, ctx, mask, budget_s=15.0):
         b = n
         rows = slice(b * p.K, (b + 1) * p.K)
         t0 = time.perf_counter()
-        P, s0 = om.precompute(ctx[b:b + 1], mask[b:b + 1])
+        Ps = [om.precompute(ctx[b:b + 1], mask[b:b + 1])[0] for om in oms]
         t1 = time.perf_counter()
-        out = om.step(p.K, tok[rows], (src[rows] - b * p.K).astype(np.int32), state[rows], ctx[b:b + 1], P,
-                      mask[b:b + 1], want_alpha=False)
-        mtref.topk(p.K, score[rows], out["logp"])
+        lps = [om.step(p.K, tok[rows], (src[rows] - b * p.K).astype(np.int32), state[rows], ctx[b:b + 1], P,
+                       mask[b:b + 1], want_alpha=False)["logp"] for om, P in zip(oms, Ps)]
+        lp = lps[0] if len(lps) == 1 else mtref.ensemble_logp(lps, ew)
+        mtref.topk(p.K, score[rows], lp)
         t2 = time.perf_counter()
         t_pre += t1 - t0
         t_step += t2 - t1
@@ -87,6 +93,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--preset", default="nematus_f32")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--ensemble", type=int, default=1,
+                    help="members decoding one beam (seeded weights per member, equal weights)")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="also run one device copy of this size (counter calibration under rocprofv3)")
@@ -112,13 +120,27 @@ def main():
     dec.set_batch(ctx, mask, p.K)
     tok0, src0, score0 = synth.start_beam(p)
     stream = torch.cuda.current_stream()
+    NE = args.ensemble
+    drive = dec
+    members = [(p, w)]
+    if NE > 1:
+        from paper_1804_00344_amd.runner import Ensemble
+        decs = [dec]
+        for i in range(1, NE):
+            pi = dataclasses.replace(p, name=f"{p.name}_m{i}", index=p.index + 100 * i)
+            wi = synth.make_weights(pi)
+            members.append((pi, wi))
+            decs.append(Decoder.from_preset(pi, wi))
+        drive = Ensemble(decs, [1.0 / NE] * NE)
+        drive.set_batch(ctx, mask, p.K)
+        cell = f"ensemble of {NE} {cell}"
 
     def run(n, first_index):
         for i in range(first_index, first_index + n):
             if i % p.steps == 0:
-                dec.precompute()
-                dec.start(tok0, score0)
-            dec.advance()
+                drive.precompute()
+                drive.start(tok0, score0)
+            drive.advance()
 
     log("[bench] warmup")
     run(args.warmup, 0)
@@ -197,7 +219,7 @@ def main():
             "workload": f"{p.name}: {cell} attention decoder step + beam top-K, B={p.B} sentences, beam K={p.K}, "
                         f"E={p.E}, H={p.H}, C={p.C}, A={p.A}, V={p.V}, padded S={dec.S} (mean len {lens.mean():.1f}), "
                         f"{p.gemm} GEMMs, layer_norm={p.layer_norm}, precompute every {p.steps} steps",
-            "B": p.B, "K": p.K, "S": dec.S, "V": p.V, "parallelism": "single GPU",
+            "B": p.B, "K": p.K, "S": dec.S, "V": p.V, "members": NE, "parallelism": "single GPU",
         },
         "hyp_rows_per_s": round(steps_per_s * p.M, 1),
         "target_tok_per_s": round(steps_per_s * p.B, 1),
@@ -206,7 +228,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         log("[bench] cpu baseline (oracle)")
-        rec["cpu_baseline"] = cpu_baseline(p, w, ctx, mask, args.cpu_budget)
+        rec["cpu_baseline"] = cpu_baseline(members, ctx, mask, args.cpu_budget)
     print(json.dumps(rec), flush=True)
 
 

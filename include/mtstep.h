@@ -185,6 +185,18 @@ mt_status mt_beam_topk(mt_model *model, int B, int K, const float *prev_score, c
 
 /* Reads and clears the device-side error bits (synchronises the device):
  * bit 0 = a prev_tok out of range, bit 1 = a src_row out of range. */
+/* Ensemble of n models decoding the same beams (Section 2.3: ensembling of models as a
+ * meta-algorithm of batched beam search).  Each member runs its own mt_decoder_step on the
+ * shared tokens and state rows (its own states) with logp_out given; this call combines
+ * their log-probabilities for one mt_beam_topk (pass out as its logp):
+ *   out[m, v] = sum_i weights[i] * logp[i][m, v],  m < M = B*K, v < V,
+ * members summed in order, fp32.  logp: HOST array of n device pointers to fp32 [M, V]
+ * (16-byte aligned); weights: HOST array of n finite floats; out: device fp32 [M, V],
+ * may be one of the inputs.  model: any member (V = its vocabulary; profiling slot
+ * MT_KERNEL_ENSEMBLE).  1 <= n <= 8.  Asynchronous on the stream. */
+mt_status mt_ensemble_logp(mt_model *model, int n, const float *const *logp, const float *weights, int M,
+                           float *out, void *stream);
+
 mt_status mt_device_errors(mt_model *model, int32_t *flags);
 
 /* Kernel timing with HIP events recorded on the launch stream around each
@@ -207,7 +219,8 @@ typedef enum {
   MT_KERNEL_PRECOMPUTE = 10,
   MT_KERNEL_VOCAB_THRESHOLD = 11, /* logits of the first vocabulary entries -> candidate threshold */
   MT_KERNEL_GEMM_TRANSITION = 12, /* s Ut_j of the transition blocks (dec_transitions > 0) */
-  MT_KERNEL_COUNT = 13
+  MT_KERNEL_ENSEMBLE = 13,  /* mt_ensemble_logp */
+  MT_KERNEL_COUNT = 14
 } mt_kernel_id;
 
 mt_status mt_profile_enable(mt_model *model, uint32_t kernel_mask);

@@ -243,7 +243,14 @@ WsLayout ws_layout(const mt_model *m, int B, int K) {
   L.ccnt = take(M * L.ntiles * vocab_lists() * sizeof(int));
   L.lse = take(M * 4);
   L.rowc = take(M * K * sizeof(int2));
-  L.nchunks = std::max(1, std::min(64, (c.V + 2047) / 2048));
+  // chunks of a materialised row for the first selection level: about 3072 workgroups in all
+  // (each then runs K block-wide extraction rounds over its per-thread lists, so fewer,
+  // longer chunks cost less), at least 256 entries (one per thread) each
+  {
+    const long want = (3072 + (long)M - 1) / (long)M;
+    const long most = std::max(1L, std::min(64L, (long)c.V / 256));
+    L.nchunks = (int)std::max(1L, std::min(want, most));
+  }
   L.scand = take(M * L.nchunks * K * sizeof(int2));
   L.scnt = take((size_t)B * sizeof(int));
   // bf16 copies of s1, the context and the new state: the A operands of the bf16 products
@@ -726,6 +733,25 @@ mt_status mt_beam_topk(mt_model *model, int B, int K, const float *prev_score, c
     rs.nl = L.nchunks; rs.cap = K; rs.cbuf = sc;
     LAUNCH(MT_KERNEL_TOPK, launch_row_select(rs, st));
   }
+  return MT_OK;
+}
+
+mt_status mt_ensemble_logp(mt_model *model, int n, const float *const *logp, const float *weights, int M,
+                           float *out, void *stream) {
+  g_err[0] = 0;
+  if (!valid_model(model)) return fail(MT_ERR_ARG, "invalid model handle");
+  if (n < 1 || n > kMaxEnsemble) return fail(MT_ERR_SHAPE, "n=%d: need 1..%d members", n, kMaxEnsemble);
+  if (M < 1 || M > (1 << 20)) return fail(MT_ERR_SHAPE, "M=%d: need 1 <= M <= 2^20", M);
+  if (!logp || !weights) return fail(MT_ERR_ARG, "logp or weights is NULL");
+  for (int i = 0; i < n; ++i) {
+    char name[32];
+    std::snprintf(name, sizeof name, "logp[%d]", i);
+    CHECK(check_dev_ptr(logp[i], name));
+    if (!std::isfinite(weights[i])) return fail(MT_ERR_ARG, "weights[%d] is not finite", i);
+  }
+  CHECK(check_dev_ptr(out, "out"));
+  hipStream_t st = (hipStream_t)stream;
+  LAUNCH(MT_KERNEL_ENSEMBLE, launch_ensemble(n, logp, weights, (long long)M * model->cfg.V, out, model->num_cu, st));
   return MT_OK;
 }
 

@@ -446,6 +446,12 @@ hipError_t launch_attention(int B, int K, int S, int A, int Cd, const void *P, c
                             const float *va, float *ctx_out, int ldc, bf16 *ctx16, float *alpha_out,
                             hipStream_t st);
 
+// ensemble combination out[i] = sum_j w[j] * in[j][i] over count elements (16-byte aligned
+// buffers; out may be one of the inputs); 1 <= n <= kMaxEnsemble
+constexpr int kMaxEnsemble = 8;
+hipError_t launch_ensemble(int n, const float *const *in, const float *w, long long count, float *out,
+                           int num_cu, hipStream_t st);
+
 hipError_t launch_lse(int M, int ntiles, const float2 *part, float *lse, float *logits, int V,
                       hipStream_t st);
 

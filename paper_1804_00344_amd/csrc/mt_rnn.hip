@@ -292,8 +292,19 @@ __global__ __launch_bounds__(kT) void lse_kernel(int M, int ntiles, const float2
   const float L = block_row_lse(part + (size_t)m * ntiles, ntiles);
   if (t == 0) lse[m] = L;
   if (logits) {
+    // 16-byte accesses over the aligned middle of the row, single elements at its ends
     float *row = logits + (size_t)m * V;
-    for (int v = t; v < V; v += kT) row[v] = row[v] - L;
+    const int mis = (int)(((uintptr_t)row & 15) / 4);  // floats past a 16-byte boundary
+    const int head = ((4 - mis) & 3) < V ? ((4 - mis) & 3) : V;
+    const int n4 = (V - head) / 4;
+    if (t < head) row[t] = row[t] - L;
+    float4 *r4 = (float4 *)(row + head);
+    for (int i = t; i < n4; i += kT) {
+      float4 x = r4[i];
+      x.x -= L; x.y -= L; x.z -= L; x.w -= L;
+      r4[i] = x;
+    }
+    for (int v = head + 4 * n4 + t; v < V; v += kT) row[v] = row[v] - L;
   }
 }
 

@@ -107,3 +107,47 @@ class Decoder:
             self.cur = 1 - self.cur
         self.first = False
         return self.state[self.cur]
+
+
+class Ensemble:
+    """Members decoding one beam (ensembling, a meta-algorithm of batched beam search): every
+    member runs its step on the shared beam with its own states and materialised
+    log-probabilities, mt_ensemble_logp combines them, and the first member's selection
+    extends the beam that all members read next."""
+
+    def __init__(self, members, weights):
+        assert len(members) == len(weights) >= 1
+        self.members, self.weights = list(members), [float(x) for x in weights]
+        self.lead = self.members[0]
+
+    def set_batch(self, ctx: np.ndarray, mask: np.ndarray, K: int):
+        for d in self.members:
+            d.set_batch(ctx, mask, K)
+        lead = self.lead
+        self.logp = [torch.empty((lead.M, lead.V), dtype=torch.float32, device=lead.device) for _ in self.members]
+        self.comb = torch.empty((lead.M, lead.V), dtype=torch.float32, device=lead.device)
+
+    def precompute(self, stream=None):
+        for d in self.members:
+            d.precompute(stream=stream)
+
+    def start(self, tok0: np.ndarray, score0: np.ndarray):
+        for d in self.members:
+            d.start(tok0, score0)
+
+    def advance(self, stream=None):
+        lead = self.lead
+        for d, lp in zip(self.members, self.logp):
+            if d.first:
+                state_in, nrows = d.s0, d.B
+            else:
+                state_in, nrows = d.state[d.cur], d.M
+            out = d.state[1 - d.cur] if not d.first else d.state[d.cur]
+            d.step(lead.tok, lead.row, state_in, nrows, out, logp=lp, stream=stream)
+        mt.mt_ensemble_logp(lead.model, self.logp, self.weights, lead.M, self.comb, stream=stream)
+        lead.topk(lead.score, self.comb, stream=stream)
+        for d in self.members:
+            if not d.first:
+                d.cur = 1 - d.cur
+            d.first = False
+        return [d.state[d.cur] for d in self.members]

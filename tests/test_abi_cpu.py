@@ -113,6 +113,7 @@ def test_calls_reject_invalid_handles():
                              0, None) == mt.MT_ERR_ARG
     assert L.mt_beam_topk(None, 1, 1, None, None, None, None, None, None, None, 0, None) == mt.MT_ERR_ARG
     assert L.mt_device_errors(None, None) == mt.MT_ERR_ARG
+    assert L.mt_ensemble_logp(None, 2, None, None, 1, None, None) == mt.MT_ERR_ARG
     assert L.mt_profile_enable(None, 1) == mt.MT_ERR_ARG
     # a pointer to garbage that is not a handle is rejected by its magic word
     junk = (C.c_uint32 * 64)()

@@ -433,3 +433,53 @@ def test_candidate_buffer_overflow_falls_back_exactly():
     for b in (0, 1):
         rows = slice(b * p.K, (b + 1) * p.K)
         assert maxerr(lp[rows], orc[b]["logp"]) <= 1e-3
+
+
+# ------------------------------------------------------------------------------------------
+# ensembles: two members (different seeded weights) decode the same beam, each with its own
+# states; their log-probabilities are combined on the GPU and one selection extends the beam
+# ------------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name,weights", [("tiny_f32", (0.6, 0.4)), ("nematus_f32", (0.5, 0.5)),
+                                          ("nematus_bf16_ln", (0.7, 0.3))])
+def test_ensemble_step_parity(name, weights):
+    base = synth.PRESETS[name]
+    members = [base, dataclasses.replace(base, name=f"{name}_m2", index=base.index + 100)]
+    log(f"\n[ensemble] {name} weights={weights}")
+    ctx, mask, lens = synth.make_source(base)
+    tok, src, state, score = synth.mid_decode_inputs(base, salt=5)
+    decs, ws, logps = [], [], []
+    for p in members:
+        w = synth.make_weights(p, peaked_bias=True)
+        dec = Decoder.from_preset(p, w)
+        dec.set_batch(ctx, mask, p.K)
+        dec.precompute()
+        gpu = run_step(dec, p, tok, src, T(state), p.M, attn=False, taps=False)
+        decs.append(dec)
+        ws.append(w)
+        logps.append(gpu["logp"])
+    out = torch.empty_like(logps[0])
+    mt.mt_ensemble_logp(decs[0].model, logps, weights, base.M, out)
+    sc, tk, bp, rw = [x.cpu().numpy() for x in decs[0].topk(T(score), out)]
+    torch.cuda.synchronize()
+    for d in decs:
+        assert mt.mt_device_errors(d.model) == 0
+    sents = sample_sentences(lens, N_SAMPLE[name])
+    orcs = [oracle_sentences(oracle_model(p, w), base.K, sents, ctx, mask, tok, src, state, want_alpha=False,
+                             taps=False) for p, w in zip(members, ws)]
+    tol = TOL[base.gemm]
+    g = out.cpu().numpy()
+    worst = 0.0
+    for b in sents:
+        rows = slice(b * base.K, (b + 1) * base.K)
+        ens = mtref.ensemble_logp([o[b]["logp"] for o in orcs], weights)
+        worst = max(worst, maxerr(g[rows], ens))
+        topk_gap_check(base.K, score[rows], ens, sc[rows], tk[rows], bp[rows], tol["logp"])
+        assert np.array_equal(rw[rows], b * base.K + bp[rows])
+    log(f"[ensemble] {name}: combined logp max error {worst:.3g}")
+    assert worst <= tol["logp"]
+    # the combination alone, aliased in place, against the GPU members' own sum
+    ref = sum(float(np.float32(x)) * l.double() for l, x in zip(logps, weights))
+    mt.mt_ensemble_logp(decs[0].model, logps, weights, base.M, logps[0])
+    torch.cuda.synchronize()
+    assert torch.max(torch.abs(logps[0].double() - ref)).item() <= 1e-4
