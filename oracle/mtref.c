@@ -304,7 +304,7 @@ static int cand_cmp(const void *pa, const void *pb) {
  * its scores in. */
 int mtref_topk(int B, int K, int V, const float *prev_score, const float *logp,
                int32_t *tok_out, int32_t *bp_out, float *score_out) {
-  if (B < 0 || K < 1 || V < K || !prev_score || !logp || !tok_out || !bp_out || !score_out)
+  if (B < 0 || K < 1 || V < 1 || !prev_score || !logp || !tok_out || !bp_out || !score_out)
     return -1;
   size_t n = (size_t)K * V;
   cand_t *cs = (cand_t *)malloc(sizeof(cand_t) * n);

@@ -271,3 +271,95 @@ def topk(K, prev_score, logp):
     if rc != 0:
         raise ValueError(f"mtref_topk: {rc}")
     return tok, bp, sc
+
+
+# ---- translation bookkeeping (finished hypotheses, beam shrink, n-best) ----------
+
+
+def beam_finish(K, t, eos, alpha, tok, bp, row, score, beam, final=False):
+    """One step of beam bookkeeping after the selection of step t (Section 2.3 batched beam
+    search; Section 3.1.3 decodes to an n-best list of as many hypotheses as the beam).
+
+    Per sentence b, `beam[b]` = K minus the hypotheses it has finished.  Of its ranked
+    selection results (rank order, as the selection returns them) the first beam[b] with a
+    finite score are its new hypotheses; those whose token is eos (every one if `final`)
+    finish, with the normalised score score / (t + 1) ** alpha, and the beam shrinks by one
+    for each.  The others move, in rank order, to the leading slots; the remaining slots are
+    dead (score -inf, token eos, parent 0, state row b*K) and never extend.
+
+    Returns (tok, bp, row, score, beam, finished) with finished a list of
+    (b, score, normalised score, step, parent slot, token) in finishing order."""
+    tok, bp, row = [np.array(a, np.int32) for a in (tok, bp, row)]
+    score = np.array(score, np.float32)
+    beam = np.array(beam, np.int32)
+    B = beam.size
+    fin = []
+    o_tok, o_bp, o_row, o_score = tok.copy(), bp.copy(), row.copy(), score.copy()
+    for b in range(B):
+        keep = []
+        nf = 0
+        for r in range(int(beam[b])):
+            m = b * K + r
+            if not np.isfinite(score[m]):
+                continue
+            if final or tok[m] == eos:
+                norm = float(score[m]) / float(t + 1) ** float(alpha)
+                fin.append((b, float(score[m]), norm, t, int(bp[m]), int(tok[m])))
+                nf += 1
+            else:
+                keep.append(m)
+        for i in range(K):
+            d = b * K + i
+            if i < len(keep):
+                s = keep[i]
+                o_tok[d], o_bp[d], o_row[d], o_score[d] = tok[s], bp[s], row[s], score[s]
+            else:
+                o_tok[d], o_bp[d], o_row[d], o_score[d] = eos, 0, b * K, -np.inf
+        beam[b] -= nf
+    return o_tok, o_bp, o_row, o_score, beam, fin
+
+
+def backtrack(K, hist_tok, hist_bp, b, step, parent, token):
+    """Token sequence of a finished hypothesis: its own token at `step`, then its ancestors
+    through the recorded (compacted) beams of the earlier steps."""
+    seq = [int(token)]
+    p = int(parent)
+    for s in range(step - 1, -1, -1):
+        seq.append(int(hist_tok[s][b * K + p]))
+        p = int(hist_bp[s][b * K + p])
+    return seq[::-1]
+
+
+def translate(model, K, ctx, mask, tok0, score0, max_steps, eos, alpha):
+    """Batched beam search to finished translations: the oracle's step and selection with
+    the bookkeeping above; every hypothesis still alive at the last step finishes there.
+    Returns per sentence the n-best list [(normalised score, score, tokens)] sorted by
+    normalised score (descending; equal ones keep finishing order)."""
+    ctx, mask = f32(ctx), f32(mask)
+    B = ctx.shape[0]
+    M = B * K
+    P, s0 = model.precompute(ctx, mask)
+    tok = np.ascontiguousarray(tok0, np.int32)
+    score = np.ascontiguousarray(score0, np.float32)
+    row = (np.arange(M) // K).astype(np.int32)
+    state, nrows = s0, B
+    beam = np.full(B, K, np.int32)
+    hist_tok, hist_bp, fins = [], [], []
+    for t in range(max_steps):
+        out = model.step(K, tok, row, state, ctx, P, mask)
+        ntok, nbp, nsc = topk(K, score, out["logp"])
+        nrow = ((np.arange(M) // K) * K + nbp).astype(np.int32)
+        tok, bp, row, score, beam, fin = beam_finish(K, t, eos, alpha, ntok, nbp, nrow, nsc, beam,
+                                                     final=(t == max_steps - 1))
+        hist_tok.append(tok.copy())
+        hist_bp.append(bp.copy())
+        fins += fin
+        state, nrows = out["state"], M
+        if not beam.any():
+            break
+    nbest = [[] for _ in range(B)]
+    for (b, sc, norm, step, parent, token) in fins:
+        nbest[b].append((norm, sc, backtrack(K, hist_tok, hist_bp, b, step, parent, token)))
+    for b in range(B):
+        nbest[b].sort(key=lambda e: -e[0])  # stable: equal scores keep finishing order
+    return nbest

@@ -696,3 +696,77 @@ def test_ensemble_beam_of_two_copies_equals_single_model_beam():
         tok, bp, score = a
         src = ((np.arange(tok.size) // 2) * 2 + bp).astype(np.int32)
         state = out["state"]
+
+
+# --------------------------------------------------------------------------------------
+# translation bookkeeping: finished hypotheses on EOS, beam shrink, length-normalised n-best
+# --------------------------------------------------------------------------------------
+
+
+def test_translate_equals_exhaustive_search_when_the_beam_holds_everything():
+    """V = 3 (EOS = 0) and K = 16 over 3 steps: the beam never has to drop a hypothesis
+    (1 + 2 + 12 = 15 <= 16 sequences), so the n-best list must be every sequence that ends
+    in EOS or reaches the last step, each scored path by path with one-row steps (the same
+    fp32 additions of the step's log-probabilities), sorted by score / length ** alpha."""
+    V, K, T, eos, alpha = 3, 16, 3, 0, 0.6
+    rng = np.random.default_rng(60)
+    E, H, A = E_, H_, A_
+    C = 2 * H
+    w = dict(
+        emb=rnd(V, E, s=0.5, rng=rng), W1=rnd(E, 3 * H, s=0.5, rng=rng), U1=rnd(H, 3 * H, s=0.5, rng=rng),
+        b1=rnd(3 * H, s=0.1, rng=rng), Ua=rnd(C, A, s=0.4, rng=rng), ba=rnd(A, s=0.1, rng=rng),
+        Wa=rnd(H, A, s=0.5, rng=rng), va=rnd(A, rng=rng), W2=rnd(C, 3 * H, s=0.4, rng=rng),
+        U2=rnd(H, 3 * H, s=0.5, rng=rng), b2=rnd(3 * H, s=0.1, rng=rng), Wt_s=rnd(H, E, s=0.5, rng=rng),
+        Wt_y=rnd(E, E, s=0.5, rng=rng), Wt_c=rnd(C, E, s=0.4, rng=rng), bt=rnd(E, s=0.1, rng=rng),
+        Wo=rnd(E, V, s=2.0, rng=rng), bo=rnd(V, s=0.5, rng=rng), Wi=rnd(C, H, s=0.4, rng=rng), bi=rnd(H, s=0.1, rng=rng))
+    model = mtref.Model(E, H, A, V, w)
+    B = 2
+    ctx = rnd(B, 4, C, rng=rng)
+    mask = np.ones((B, 4), np.float32)
+    mask[1, 3] = 0
+    tok0 = np.full(B * K, 1, np.int32)
+    score0 = np.full(B * K, -np.inf, np.float32)
+    score0[::K] = 0.0
+    nbest = mtref.translate(model, K, ctx, mask, tok0, score0, T, eos, alpha)
+    P, s0 = model.precompute(ctx, mask)
+    for b in range(B):
+        want = []
+
+        def walk(prefix, tok, state, sc):
+            out = model.step(1, np.array([tok], np.int32), np.array([0], np.int32), state[None], ctx[b:b + 1],
+                             P[b:b + 1], mask[b:b + 1])
+            for v in range(V):
+                s = np.float32(sc + out["logp"][0, v])
+                seq = prefix + [v]
+                if v == eos or len(seq) == T:
+                    want.append((float(s) / float(len(seq)) ** alpha, float(s), seq))
+                else:
+                    walk(seq, v, out["state"][0], s)
+
+        walk([], 1, s0[b], np.float32(0.0))
+        assert len(want) == 15 and len(nbest[b]) == 15
+        key = lambda e: (-e[0], e[2])
+        got, ref = sorted(nbest[b], key=key), sorted(want, key=key)
+        for g, r in zip(got, ref):
+            assert g[2] == r[2] and g[1] == r[1] and abs(g[0] - r[0]) <= 1e-6 * max(1.0, abs(r[0]))
+
+
+def test_beam_finish_compacts_in_rank_order_and_shrinks_the_beam():
+    K, eos = 5, 7
+    tok = np.array([3, 7, 4, 7, 9, 1, 2, 7, 5, 6], np.int32)
+    bp = np.array([0, 1, 2, 3, 4, 4, 3, 2, 1, 0], np.int32)
+    row = (np.arange(10) // K * K + bp).astype(np.int32)
+    score = np.array([-1, -2, -3, -4, -5, -1, -2, -3, -np.inf, -np.inf], np.float32)
+    beam = np.array([4, 5], np.int32)  # sentence 0 had finished one hypothesis before
+    t_, b_, r_, s_, beam2, fin = mtref.beam_finish(K, 2, eos, 1.0, tok, bp, row, score, beam)
+    # sentence 0: ranks 0..3 are hypotheses; ranks 1 and 3 end in EOS; rank 4 is beyond the beam
+    assert [f[:2] for f in fin[:2]] == [(0, -2.0), (0, -4.0)] and fin[0][2] == -2.0 / 3
+    assert list(t_[:5]) == [3, 4, eos, eos, eos] and list(b_[:5]) == [0, 2, 0, 0, 0]
+    assert list(r_[:5]) == [0, 2, 0, 0, 0] and list(s_[:2]) == [-1, -3] and np.all(np.isinf(s_[2:5]))
+    # sentence 1: ranks 3, 4 have no finite score (fewer candidates than the beam); rank 2 is EOS
+    assert [f[0] for f in fin[2:]] == [1] and fin[2][3] == 2 and fin[2][4] == 2
+    assert list(t_[5:7]) == [1, 2] and list(r_[5:7]) == [9, 8] and np.all(np.isinf(s_[7:]))
+    assert list(beam2) == [2, 4]
+    # final step: every hypothesis finishes
+    *_, beam3, fin3 = mtref.beam_finish(K, 2, eos, 1.0, tok, bp, row, score, beam, final=True)
+    assert list(beam3) == [0, 2] and len(fin3) == 7
