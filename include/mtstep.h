@@ -197,6 +197,28 @@ mt_status mt_beam_topk(mt_model *model, int B, int K, const float *prev_score, c
 mt_status mt_ensemble_logp(mt_model *model, int n, const float *const *logp, const float *weights, int M,
                            float *out, void *stream);
 
+/* Translation bookkeeping after mt_beam_topk of step `step` (batched beam search decoding
+ * to an n-best list as large as the beam, Sections 2.3 and 3.1.3).  Per sentence b:
+ *   beam[b] (device int32 [B], in/out): K minus the hypotheses b has finished (start: K);
+ *   of b's K ranked results (tok, bp, row, score [B*K] as mt_beam_topk wrote them) the
+ *   first beam[b] with a finite score are its new hypotheses.  Those whose token is eos
+ *   (every one when final != 0) finish: entry fin_count[b] (+ rank among them) of b's list
+ *   receives fin_score = score, fin_norm = score / (step+1)^alpha, fin_step = step,
+ *   fin_parent = bp (slot in the previous beam), fin_tok = token; beam[b] shrinks by one
+ *   each and fin_count[b] (device int32 [B], start 0) grows.  The other new hypotheses
+ *   move, in rank order, to slots 0.. of tok/bp/row/score (in place); the remaining slots
+ *   become dead (score -inf, token eos, bp 0, row b*K) and never extend.
+ *   hist_tok, hist_bp (device int32 [B*K]) receive this step's compacted tok and bp, the
+ *   record a caller backtracks through (finished entry -> fin_parent -> hist_* of the
+ *   previous steps).
+ *   fin_score, fin_norm [B*K] fp32, fin_step, fin_parent, fin_tok [B*K] int32: b's list at
+ *   b*K..b*K+K-1 (at most K entries ever).
+ * 1 <= K <= k_max, 0 <= eos < V, alpha finite.  Asynchronous on the stream. */
+mt_status mt_beam_finish(mt_model *model, int B, int K, int step, int32_t eos, float alpha, int final_step,
+                         int32_t *tok, int32_t *bp, int32_t *row, float *score, int32_t *beam,
+                         int32_t *fin_count, int32_t *hist_tok, int32_t *hist_bp, float *fin_score,
+                         float *fin_norm, int32_t *fin_step, int32_t *fin_parent, int32_t *fin_tok, void *stream);
+
 mt_status mt_device_errors(mt_model *model, int32_t *flags);
 
 /* Kernel timing with HIP events recorded on the launch stream around each
@@ -220,7 +242,8 @@ typedef enum {
   MT_KERNEL_VOCAB_THRESHOLD = 11, /* logits of the first vocabulary entries -> candidate threshold */
   MT_KERNEL_GEMM_TRANSITION = 12, /* s Ut_j of the transition blocks (dec_transitions > 0) */
   MT_KERNEL_ENSEMBLE = 13,  /* mt_ensemble_logp */
-  MT_KERNEL_COUNT = 14
+  MT_KERNEL_BEAM_FINISH = 14, /* mt_beam_finish */
+  MT_KERNEL_COUNT = 15
 } mt_kernel_id;
 
 mt_status mt_profile_enable(mt_model *model, uint32_t kernel_mask);

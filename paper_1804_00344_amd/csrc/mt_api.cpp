@@ -755,6 +755,35 @@ mt_status mt_ensemble_logp(mt_model *model, int n, const float *const *logp, con
   return MT_OK;
 }
 
+mt_status mt_beam_finish(mt_model *model, int B, int K, int step, int32_t eos, float alpha, int final_step,
+                         int32_t *tok, int32_t *bp, int32_t *row, float *score, int32_t *beam,
+                         int32_t *fin_count, int32_t *hist_tok, int32_t *hist_bp, float *fin_score,
+                         float *fin_norm, int32_t *fin_step, int32_t *fin_parent, int32_t *fin_tok, void *stream) {
+  g_err[0] = 0;
+  if (!valid_model(model)) return fail(MT_ERR_ARG, "invalid model handle");
+  const mt_config &c = model->cfg;
+  if (B < 1 || K < 1 || K > c.k_max || K > c.V) return fail(MT_ERR_SHAPE, "B=%d K=%d: need B >= 1, 1 <= K <= k_max", B, K);
+  if ((long long)B * K > (1 << 20)) return fail(MT_ERR_SHAPE, "B*K exceeds 2^20");
+  if (step < 0) return fail(MT_ERR_ARG, "step=%d must be >= 0", step);
+  if (eos < 0 || eos >= c.V) return fail(MT_ERR_ARG, "eos=%d outside [0, V)", eos);
+  if (!std::isfinite(alpha)) return fail(MT_ERR_ARG, "alpha is not finite");
+  struct {
+    const void *p;
+    const char *n;
+  } ptrs[] = {{tok, "tok"}, {bp, "bp"}, {row, "row"}, {score, "score"}, {beam, "beam"}, {fin_count, "fin_count"},
+              {hist_tok, "hist_tok"}, {hist_bp, "hist_bp"}, {fin_score, "fin_score"}, {fin_norm, "fin_norm"},
+              {fin_step, "fin_step"}, {fin_parent, "fin_parent"}, {fin_tok, "fin_tok"}};
+  for (auto &q : ptrs) CHECK(check_dev_ptr(q.p, q.n, 4));
+  hipStream_t st = (hipStream_t)stream;
+  BeamFinish a{};
+  a.K = K; a.step = step; a.eos = eos; a.final = final_step != 0; a.alpha = alpha;
+  a.tok = tok; a.bp = bp; a.row = row; a.score = score; a.beam = beam; a.fin_count = fin_count;
+  a.hist_tok = hist_tok; a.hist_bp = hist_bp; a.fin_score = fin_score; a.fin_norm = fin_norm;
+  a.fin_step = fin_step; a.fin_parent = fin_parent; a.fin_tok = fin_tok;
+  LAUNCH(MT_KERNEL_BEAM_FINISH, launch_beam_finish(a, B, st));
+  return MT_OK;
+}
+
 mt_status mt_device_errors(mt_model *model, int32_t *flags) {
   g_err[0] = 0;
   if (!valid_model(model)) return fail(MT_ERR_ARG, "invalid model handle");

@@ -446,6 +446,19 @@ hipError_t launch_attention(int B, int K, int S, int A, int Cd, const void *P, c
                             const float *va, float *ctx_out, int ldc, bf16 *ctx16, float *alpha_out,
                             hipStream_t st);
 
+// translation bookkeeping for B sentences of K ranked results each (see mt_beam_finish)
+struct BeamFinish {
+  int K, step, eos, final;
+  float alpha;
+  int32_t *tok, *bp, *row;
+  float *score;
+  int32_t *beam, *fin_count;
+  int32_t *hist_tok, *hist_bp;  // this step's [M] record
+  float *fin_score, *fin_norm;  // [B][K]
+  int32_t *fin_step, *fin_parent, *fin_tok;
+};
+hipError_t launch_beam_finish(const BeamFinish &a, int B, hipStream_t st);
+
 // ensemble combination out[i] = sum_j w[j] * in[j][i] over count elements (16-byte aligned
 // buffers; out may be one of the inputs); 1 <= n <= kMaxEnsemble
 constexpr int kMaxEnsemble = 8;

@@ -20,7 +20,8 @@ MT_OK, MT_ERR_ARG, MT_ERR_SHAPE, MT_ERR_DTYPE, MT_ERR_HIP, MT_ERR_OOM, MT_ERR_ST
     0, -1, -2, -3, -4, -5, -6, -7)
 MT_F32, MT_BF16 = 0, 1
 KERNELS = ["GEMM_GRU1", "GRU_CELL", "GEMM_S1", "ATTENTION", "GEMM_CTX", "GEMM_READOUT", "READOUT",
-           "VOCAB_GEMM", "LSE", "TOPK", "PRECOMPUTE", "VOCAB_THRESHOLD", "GEMM_TRANSITION", "ENSEMBLE"]
+           "VOCAB_GEMM", "LSE", "TOPK", "PRECOMPUTE", "VOCAB_THRESHOLD", "GEMM_TRANSITION", "ENSEMBLE",
+           "BEAM_FINISH"]
 KERNEL_ID = {n: i for i, n in enumerate(KERNELS)}
 
 
@@ -74,11 +75,12 @@ def lib() -> C.CDLL:
         L.mt_beam_topk.argtypes = [_vp, C.c_int, C.c_int, _vp, _vp, _vp, _vp, _vp, _vp, _vp, C.c_size_t, _vp]
         L.mt_device_errors.argtypes = [_vp, C.POINTER(C.c_int32)]
         L.mt_ensemble_logp.argtypes = [_vp, C.c_int, C.POINTER(_vp), C.POINTER(C.c_float), C.c_int, _vp, _vp]
+        L.mt_beam_finish.argtypes = [_vp, C.c_int, C.c_int, C.c_int, C.c_int32, C.c_float, C.c_int] + [_vp] * 14
         L.mt_profile_enable.argtypes = [_vp, C.c_uint32]
         L.mt_profile_reset.argtypes = [_vp]
         L.mt_profile_query.argtypes = [_vp, C.c_int, C.POINTER(C.c_double), C.POINTER(C.c_int64)]
         for f in ("mt_load_weights", "mt_free", "mt_precompute_ctx", "mt_decoder_step", "mt_beam_topk",
-                  "mt_ensemble_logp",
+                  "mt_ensemble_logp", "mt_beam_finish",
                   "mt_device_errors", "mt_profile_enable", "mt_profile_reset", "mt_profile_query"):
             getattr(L, f).restype = C.c_int
         _lib = L
@@ -154,6 +156,14 @@ def mt_ensemble_logp(model: Model, logps, weights, M: int, out, stream=None):
     ptrs = (_vp * n)(*[_ptr(x) for x in logps])
     w = (C.c_float * n)(*[float(x) for x in weights])
     _check(lib().mt_ensemble_logp(model.handle, n, ptrs, w, M, _ptr(out), _stream(stream)))
+
+
+def mt_beam_finish(model: Model, B, K, step, eos, alpha, final, tok, bp, row, score, beam, fin_count, hist_tok,
+                   hist_bp, fin_score, fin_norm, fin_step, fin_parent, fin_tok, stream=None):
+    _check(lib().mt_beam_finish(model.handle, B, K, step, eos, alpha, int(bool(final)),
+                                *[_ptr(x) for x in (tok, bp, row, score, beam, fin_count, hist_tok, hist_bp,
+                                                    fin_score, fin_norm, fin_step, fin_parent, fin_tok)],
+                                _stream(stream)))
 
 
 def mt_free(model: Model):

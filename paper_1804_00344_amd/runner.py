@@ -109,6 +109,55 @@ class Decoder:
         return self.state[self.cur]
 
 
+def backtrack(K, hist_tok, hist_bp, b, step, parent, token):
+    """Token sequence of a finished hypothesis through the recorded beams (host arrays)."""
+    seq = [int(token)]
+    p = int(parent)
+    for s in range(step - 1, -1, -1):
+        seq.append(int(hist_tok[s, b * K + p]))
+        p = int(hist_bp[s, b * K + p])
+    return seq[::-1]
+
+
+def translate(dec: "Decoder", tok0, score0, max_steps: int, eos: int, alpha: float, check_every: int = 4,
+              stream=None):
+    """Batched beam search to finished translations: steps, selections and the device-side
+    bookkeeping (mt_beam_finish) until every sentence has finished its K hypotheses or
+    max_steps is reached (the last step finishes every live one).  The host looks at the
+    beams every `check_every` steps (one synchronisation) to stop early.  Returns
+    (n-best lists per sentence [(normalised score, score, tokens)], steps run)."""
+    d, B, K, M = dec.device, dec.B, dec.K, dec.M
+    dec.precompute(stream=stream)
+    dec.start(tok0, score0)
+    beam = torch.full((B,), K, dtype=torch.int32, device=d)
+    fcount = torch.zeros(B, dtype=torch.int32, device=d)
+    hist_tok = torch.empty((max_steps, M), dtype=torch.int32, device=d)
+    hist_bp = torch.empty((max_steps, M), dtype=torch.int32, device=d)
+    fs = torch.empty(M, dtype=torch.float32, device=d)
+    fn = torch.empty(M, dtype=torch.float32, device=d)
+    fst, fpa, fto = [torch.empty(M, dtype=torch.int32, device=d) for _ in range(3)]
+    steps = 0
+    for t in range(max_steps):
+        dec.advance(stream=stream)
+        mt.mt_beam_finish(dec.model, B, K, t, eos, alpha, t == max_steps - 1, dec.tok, dec.bp, dec.row, dec.score,
+                          beam, fcount, hist_tok[t], hist_bp[t], fs, fn, fst, fpa, fto, stream=stream)
+        steps = t + 1
+        if (t + 1) % check_every == 0 and int(beam.sum().item()) == 0:
+            break
+    ht, hb = hist_tok[:steps].cpu().numpy(), hist_bp[:steps].cpu().numpy()
+    fc = fcount.cpu().numpy()
+    fs, fn, fst, fpa, fto = [x.cpu().numpy() for x in (fs, fn, fst, fpa, fto)]
+    nbest = []
+    for b in range(B):
+        lst = []
+        for j in range(int(fc[b])):
+            f = b * K + j
+            lst.append((float(fn[f]), float(fs[f]), backtrack(K, ht, hb, b, int(fst[f]), int(fpa[f]), int(fto[f]))))
+        lst.sort(key=lambda e: -e[0])
+        nbest.append(lst)
+    return nbest, steps
+
+
 class Ensemble:
     """Members decoding one beam (ensembling, a meta-algorithm of batched beam search): every
     member runs its step on the shared beam with its own states and materialised

@@ -483,3 +483,73 @@ def test_ensemble_step_parity(name, weights):
     mt.mt_ensemble_logp(decs[0].model, logps, weights, base.M, logps[0])
     torch.cuda.synchronize()
     assert torch.max(torch.abs(logps[0].double() - ref)).item() <= 1e-4
+
+
+# ------------------------------------------------------------------------------------------
+# translation bookkeeping (mt_beam_finish) and whole translations
+# ------------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("B,K,final", [(5, 4, False), (7, 12, False), (3, 16, True), (4, 1, False)])
+def test_beam_finish_bit_exact(B, K, final):
+    """Random ranked beams (some EOS tokens, some -inf scores, beams already shrunk) through
+    the C ABI against the oracle's bookkeeping: every output equal (the normalised score to
+    a few ulps: the kernel raises to the power in fp32)."""
+    p = synth.PRESETS["tiny_f32"]
+    dec = Decoder(p.E, p.H, p.A, p.V, synth.make_weights(p), k_max=16)
+    rng = np.random.default_rng(100 + B * K)
+    M, eos, step, alpha = B * K, 7, 3, 0.6
+    tok = rng.integers(0, 10, M).astype(np.int32)
+    tok[rng.random(M) < 0.3] = eos
+    bp = rng.integers(0, K, M).astype(np.int32)
+    row = ((np.arange(M) // K) * K + bp).astype(np.int32)
+    score = np.sort(-rng.random((B, K)) * 5, axis=1)[:, ::-1].reshape(-1).astype(np.float32)
+    score[rng.random(M) < 0.15] = -np.inf
+    beam = rng.integers(0, K + 1, B).astype(np.int32)
+    fcount = (K - beam).astype(np.int32)
+    o_tok, o_bp, o_row, o_score, o_beam, fin = mtref.beam_finish(K, step, eos, alpha, tok, bp, row, score, beam,
+                                                                 final=final)
+    g = {n: T(a) for n, a in dict(tok=tok, bp=bp, row=row, score=score, beam=beam, fc=fcount).items()}
+    ht, hb = torch.empty(M, dtype=torch.int32, device=DEV), torch.empty(M, dtype=torch.int32, device=DEV)
+    fs, fn = torch.full((M,), 9.0, device=DEV), torch.full((M,), 9.0, device=DEV)
+    fst, fpa, fto = [torch.full((M,), -5, dtype=torch.int32, device=DEV) for _ in range(3)]
+    mt.mt_beam_finish(dec.model, B, K, step, eos, alpha, final, g["tok"], g["bp"], g["row"], g["score"], g["beam"],
+                      g["fc"], ht, hb, fs, fn, fst, fpa, fto)
+    torch.cuda.synchronize()
+    c = lambda x: x.cpu().numpy()
+    assert np.array_equal(c(g["tok"]), o_tok) and np.array_equal(c(g["bp"]), o_bp)
+    assert np.array_equal(c(g["row"]), o_row) and np.array_equal(c(g["score"]), o_score)
+    assert np.array_equal(c(g["beam"]), o_beam) and np.array_equal(c(ht), o_tok) and np.array_equal(c(hb), o_bp)
+    assert np.array_equal(c(g["fc"]), fcount + (beam - o_beam))
+    seen = np.zeros(B, np.int32)
+    for (b, sc, norm, st, par, tk) in fin:
+        f = b * K + fcount[b] + seen[b]
+        seen[b] += 1
+        assert c(fs)[f] == np.float32(sc) and c(fst)[f] == st and c(fpa)[f] == par and c(fto)[f] == tk
+        assert abs(c(fn)[f] - norm) <= 4e-7 * max(1.0, abs(norm))
+
+
+# (tiny_f32, 0): every hypothesis ends in EOS within 3 steps; (tiny_f32, 3) and
+# (tiny_deep_f32_ln, 1): some end in EOS mid-decode, the rest are finished at the last step
+@pytest.mark.parametrize("name,eos", [("tiny_f32", 0), ("tiny_f32", 3), ("tiny_deep_f32_ln", 1)])
+def test_translate_nbest_parity(name, eos):
+    """Whole translations to n-best lists on the GPU (steps, selections, bookkeeping, host
+    backtracking) against the oracle's translation loop on the same seeded inputs."""
+    from paper_1804_00344_amd.runner import translate
+    p, w, ctx, mask, lens, dec = setup(name, peaked=True)
+    # EOS among the most probable tokens under the peaked output prior, so that hypotheses
+    # finish at different steps and the beams shrink mid-decode
+    alpha, steps = 0.6, 12
+    tok0, _, score0 = synth.start_beam(p)
+    nb, ran = translate(dec, tok0, score0, steps, eos, alpha)
+    om = oracle_model(p, w)
+    ref = mtref.translate(om, p.K, ctx, mask, tok0, score0, steps, eos, alpha)
+    n_eos = 0
+    for b in range(p.B):
+        assert len(nb[b]) == len(ref[b]) == p.K, (b, len(nb[b]), len(ref[b]))
+        for g, r in zip(nb[b], ref[b]):
+            assert g[2] == r[2], (b, g, r)
+            assert abs(g[1] - r[1]) <= TOL[p.gemm]["logp"] * len(r[2])
+            n_eos += r[2][-1] == eos
+    lens_ = sorted({len(r[2]) for b in range(p.B) for r in ref[b]})
+    log(f"[translate] {name}: {p.B} sentences, {ran} steps, {n_eos} of {p.B * p.K} hypotheses end in EOS, "
+        f"lengths {lens_}")
