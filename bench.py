@@ -95,6 +95,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--ensemble", type=int, default=1,
                     help="members decoding one beam (seeded weights per member, equal weights)")
+    ap.add_argument("--translate", type=int, default=0,
+                    help="time whole translations of the batch to n-best lists (this many steps at most; "
+                         "EOS = token 0, length normalisation alpha 0.6) instead of a fixed step count")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="also run one device copy of this size (counter calibration under rocprofv3)")
@@ -135,12 +138,25 @@ def main():
         drive.set_batch(ctx, mask, p.K)
         cell = f"ensemble of {NE} {cell}"
 
+    tr = {"translations": 0, "steps": 0}
+
     def run(n, first_index):
+        """n steps (or, translating, whole translations until at least n steps); returns the steps run"""
+        if args.translate:
+            from paper_1804_00344_amd.runner import translate
+            done = 0
+            while done < n:
+                _, ran = translate(dec, tok0, score0, args.translate, 0, 0.6)
+                done += ran
+                tr["translations"] += 1
+                tr["steps"] += ran
+            return done
         for i in range(first_index, first_index + n):
             if i % p.steps == 0:
                 drive.precompute()
                 drive.start(tok0, score0)
             drive.advance()
+        return n
 
     log("[bench] warmup")
     run(args.warmup, 0)
@@ -150,7 +166,8 @@ def main():
     log(f"[bench] timing {args.steps} steps")
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    run(args.steps, args.warmup)
+    tr.update(translations=0, steps=0)
+    timed_steps = run(args.steps, args.warmup)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     vocab_ms, vocab_n = mt.mt_profile_query(dec.model, "VOCAB_GEMM")
@@ -160,13 +177,13 @@ def main():
     # per-kernel breakdown (separate pass, every class timed)
     mt.mt_profile_enable(dec.model, mt.KERNELS)
     mt.mt_profile_reset(dec.model)
-    run(min(args.steps, 50), args.warmup + args.steps)
+    bsteps = run(min(args.steps, 50), args.warmup + args.steps)
     torch.cuda.synchronize()
     breakdown = {}
     for k in mt.KERNELS:
         ms, n = mt.mt_profile_query(dec.model, k)
         if n:
-            breakdown[k.lower()] = {"us_per_step": round(1e3 * ms / min(args.steps, 50), 2), "launches": n}
+            breakdown[k.lower()] = {"us_per_step": round(1e3 * ms / bsteps, 2), "launches": n}
     mt.mt_profile_enable(dec.model, ())
 
     if args.copy_calib_mib:
@@ -176,7 +193,7 @@ def main():
         torch.neg(src, out=dst)
         torch.cuda.synchronize()
 
-    steps_per_s = args.steps / elapsed
+    steps_per_s = timed_steps / elapsed
     avg_vocab_s = vocab_ms / 1e3 / max(vocab_n, 1)
     flops = 2.0 * p.M * p.E * p.V
     achieved = flops / avg_vocab_s / 1e12
@@ -207,9 +224,9 @@ def main():
         "value": round(steps_per_s, 2),
         "unit": "steps/s",
         "n_gpus": 1,
-        "steps": args.steps,
+        "steps": timed_steps,
         "warmup": args.warmup,
-        "ms_per_step": round(1e3 * elapsed / args.steps, 4),
+        "ms_per_step": round(1e3 * elapsed / timed_steps, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -226,6 +243,14 @@ def main():
         "roofline": roofline,
         "kernels": breakdown,
     }
+    if args.translate:
+        rec["translate"] = {
+            "what": "whole translations of the batch to n-best lists of K (steps, selections, bookkeeping, "
+                    "an early-exit check every 4 steps, host backtracking), EOS = token 0, alpha = 0.6",
+            "max_steps": args.translate, "translations": tr["translations"],
+            "mean_steps": round(tr["steps"] / max(tr["translations"], 1), 2),
+            "sentences_per_s": round(tr["translations"] * p.B / elapsed, 1),
+        }
     if not args.no_cpu_baseline:
         log("[bench] cpu baseline (oracle)")
         rec["cpu_baseline"] = cpu_baseline(members, ctx, mask, args.cpu_budget)

@@ -147,14 +147,23 @@ def translate(dec: "Decoder", tok0, score0, max_steps: int, eos: int, alpha: flo
     ht, hb = hist_tok[:steps].cpu().numpy(), hist_bp[:steps].cpu().numpy()
     fc = fcount.cpu().numpy()
     fs, fn, fst, fpa, fto = [x.cpu().numpy() for x in (fs, fn, fst, fpa, fto)]
-    nbest = []
-    for b in range(B):
-        lst = []
-        for j in range(int(fc[b])):
-            f = b * K + j
-            lst.append((float(fn[f]), float(fs[f]), backtrack(K, ht, hb, b, int(fst[f]), int(fpa[f]), int(fto[f]))))
-        lst.sort(key=lambda e: -e[0])
-        nbest.append(lst)
+    # every finished hypothesis at once: walk the recorded beams back one step at a time
+    sel = np.concatenate([b * K + np.arange(int(fc[b])) for b in range(B)]).astype(np.int64)
+    fb = sel // K
+    step_of, parent = fst[sel].astype(np.int64), fpa[sel].astype(np.int64)
+    seqs = np.full((sel.size, max(steps, 1)), -1, np.int64)
+    seqs[np.arange(sel.size), step_of] = fto[sel]
+    for s in range(steps - 2, -1, -1):
+        act = step_of > s
+        idx = fb[act] * K + parent[act]
+        seqs[act, s] = ht[s, idx]
+        parent[act] = hb[s, idx]
+    nbest = [[] for _ in range(B)]
+    for e in range(sel.size):
+        f = sel[e]
+        nbest[fb[e]].append((float(fn[f]), float(fs[f]), seqs[e, :step_of[e] + 1].tolist()))
+    for lst in nbest:
+        lst.sort(key=lambda x: -x[0])
     return nbest, steps
 
 
