@@ -285,6 +285,45 @@ int mtref_step(const mtref_dims *d, const mtref_weights *w, int B, int K, int S,
   return 0;
 }
 
+/* Encoder::build for the shallow model (Section 2.2; bi-directional RNN encoder, Section
+ * 3.1.1): a forward and a backward GRU block over the source embeddings, their states side by
+ * side.  A padded position carries each direction's state over (reading of the paper, which
+ * does not spell out the padding). */
+int mtref_encode(int E, int H, int Vs, int B, int S, const int32_t *src_tok, const float *mask,
+                 const float *semb, const float *Wf, const float *Uf, const float *bf,
+                 const float *Wb, const float *Ub, const float *bb, float *ctx_out) {
+  if (E < 1 || H < 1 || Vs < 1 || B < 0 || S < 1 || !src_tok || !mask || !semb || !Wf || !Uf || !bf ||
+      !Wb || !Ub || !bb || !ctx_out)
+    return -1;
+  for (long i = 0; i < (long)B * S; ++i)
+    if (src_tok[i] < 0 || src_tok[i] >= Vs) return -2;
+  const int C = 2 * H;
+  double *x = (double *)malloc(sizeof(double) * E);
+  double *h = (double *)malloc(sizeof(double) * H);
+  double *hn = (double *)malloc(sizeof(double) * H);
+  for (int b = 0; b < B; ++b) {
+    for (int dir = 0; dir < 2; ++dir) {
+      for (int j = 0; j < H; ++j) h[j] = 0.0;
+      for (int n = 0; n < S; ++n) {
+        const int i = dir == 0 ? n : S - 1 - n;
+        float *out = ctx_out + ((size_t)b * S + i) * C + (size_t)dir * H;
+        if (mask[(size_t)b * S + i] != 0.f) {
+          to_double(E, semb + (size_t)src_tok[(size_t)b * S + i] * E, x);
+          mtref_gru(E, H, x, h, dir == 0 ? Wf : Wb, dir == 0 ? Uf : Ub, dir == 0 ? bf : bb, NULL, NULL, NULL,
+                    NULL, 0.0, hn);
+          round_store(H, hn, out, h);
+        } else {
+          for (int j = 0; j < H; ++j) out[j] = (float)h[j];
+        }
+      }
+    }
+  }
+  free(x);
+  free(h);
+  free(hn);
+  return 0;
+}
+
 typedef struct {
   float key;
   int32_t idx; /* k*V + v */

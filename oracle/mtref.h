@@ -103,6 +103,16 @@ int mtref_step(const mtref_dims *d, const mtref_weights *w, int B, int K, int S,
                float *state_out, float *logp_out, float *alpha_out,
                float *s1_out, float *c_out, float *t_out);
 
+/* Encoder::build for the shallow model (Section 2.2; the Nematus-compatible encoder is a
+ * bi-directional RNN, Section 3.1.1): ctx[b,i,:] = [f_i ; g_i] (C = 2H) with
+ *   f_i = GRU(x_i, f_{i-1}; Wf, Uf, bf),  i = 0..S-1,  f_{-1} = 0,
+ *   g_i = GRU(x_i, g_{i+1}; Wb, Ub, bb),  i = S-1..0,  g_S = 0,
+ *   x_i = semb[src_tok[b,i]]; at a padded position (mask 0) a direction keeps its state
+ *   (f_i = f_{i-1}, g_i = g_{i+1}).  No layer norm.  Every state stored in fp32. */
+int mtref_encode(int E, int H, int Vs, int B, int S, const int32_t *src_tok, const float *mask,
+                 const float *semb, const float *Wf, const float *Uf, const float *bf,
+                 const float *Wb, const float *Ub, const float *bb, float *ctx_out);
+
 /* Beam selection: for each sentence b, candidates cand(k,v) = score[b*K+k] +
  * logp[b*K+k, v] evaluated in fp32; the K best by (cand descending, flat
  * index k*V+v ascending) give score_out, tok_out = v, bp_out = k. */

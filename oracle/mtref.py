@@ -76,6 +76,8 @@ def lib():
         L.mtref_step.argtypes = [C.POINTER(_Dims), C.POINTER(_Weights), C.c_int, C.c_int, C.c_int,
                                  _i, _i, C.c_int, _f, _f, _f, _f, _f, _f, _f, _f, _f, _f]
         L.mtref_step.restype = C.c_int
+        L.mtref_encode.argtypes = [C.c_int, C.c_int, C.c_int, C.c_int, C.c_int, _i, _f, _f, _f, _f, _f, _f, _f, _f, _f]
+        L.mtref_encode.restype = C.c_int
         L.mtref_topk.argtypes = [C.c_int, C.c_int, C.c_int, _f, _f, _i, _i, _f]
         L.mtref_topk.restype = C.c_int
         _lib = L
@@ -258,6 +260,22 @@ def ensemble_logp(logps, weights) -> np.ndarray:
     for lp, w in zip(logps, weights):
         acc += float(np.float32(w)) * f32(lp).astype(np.float64)
     return acc.astype(np.float32)
+
+
+def encode(src_tok, mask, semb, Wf, Uf, bf, Wb, Ub, bb) -> np.ndarray:
+    """Bi-directional GRU encoder: ctx [B, S, 2H] fp32 (see mtref_encode)."""
+    src_tok = np.ascontiguousarray(src_tok, np.int32)
+    mask = f32(mask)
+    semb, Wf, Uf, bf, Wb, Ub, bb = [f32(a) for a in (semb, Wf, Uf, bf, Wb, Ub, bb)]
+    B, S = src_tok.shape
+    Vs, E = semb.shape
+    H = Uf.shape[0]
+    out = np.empty((B, S, 2 * H), np.float32)
+    rc = lib().mtref_encode(E, H, Vs, B, S, _ip(src_tok), _fp(mask), _fp(semb), _fp(Wf), _fp(Uf), _fp(bf),
+                            _fp(Wb), _fp(Ub), _fp(bb), _fp(out))
+    if rc != 0:
+        raise ValueError(f"mtref_encode: {rc}")
+    return out
 
 
 def topk(K, prev_score, logp):

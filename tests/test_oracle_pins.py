@@ -770,3 +770,66 @@ def test_beam_finish_compacts_in_rank_order_and_shrinks_the_beam():
     # final step: every hypothesis finishes
     *_, beam3, fin3 = mtref.beam_finish(K, 2, eos, 1.0, tok, bp, row, score, beam, final=True)
     assert list(beam3) == [0, 2] and len(fin3) == 7
+
+
+# --------------------------------------------------------------------------------------
+# encoder (Encoder::build): bi-directional GRU over the source embeddings
+# --------------------------------------------------------------------------------------
+
+
+def enc_weights(E, H, Vs, seed):
+    rng = np.random.default_rng(seed)
+    return dict(semb=rnd(Vs, E, s=0.5, rng=rng), Wf=rnd(E, 3 * H, s=0.5, rng=rng), Uf=rnd(H, 3 * H, s=0.5, rng=rng),
+                bf=rnd(3 * H, s=0.2, rng=rng), Wb=rnd(E, 3 * H, s=0.5, rng=rng), Ub=rnd(H, 3 * H, s=0.5, rng=rng),
+                bb=rnd(3 * H, s=0.2, rng=rng))
+
+
+def enc(tok, mask, w):
+    return mtref.encode(tok, mask, w["semb"], w["Wf"], w["Uf"], w["bf"], w["Wb"], w["Ub"], w["bb"])
+
+
+def test_encoder_equals_torch_bidirectional_gru():
+    """Unpadded sentences: torch.nn.GRU(bidirectional=True) with the same reset-after-product
+    cell (bias_ih = b, bias_hh = 0) gives the same context rows."""
+    E, H, Vs, B, S = 6, 5, 11, 3, 7
+    w = enc_weights(E, H, Vs, 70)
+    tok = np.random.default_rng(71).integers(0, Vs, (B, S)).astype(np.int32)
+    got = enc(tok, np.ones((B, S), np.float32), w)
+    gru = torch.nn.GRU(E, H, batch_first=True, bidirectional=True).double()
+    with torch.no_grad():
+        for sfx, d in (("", "f"), ("_reverse", "b")):
+            getattr(gru, "weight_ih_l0" + sfx).copy_(torch.from_numpy(w["W" + d].astype(np.float64).T))
+            getattr(gru, "weight_hh_l0" + sfx).copy_(torch.from_numpy(w["U" + d].astype(np.float64).T))
+            getattr(gru, "bias_ih_l0" + sfx).copy_(torch.from_numpy(w["b" + d].astype(np.float64)))
+            getattr(gru, "bias_hh_l0" + sfx).zero_()
+        ref, _ = gru(torch.from_numpy(w["semb"][tok].astype(np.float64)))
+    assert np.max(np.abs(got - ref.numpy())) <= 2e-6
+
+
+def test_encoder_padding_leaves_valid_rows_unchanged():
+    """A sentence padded past its length encodes its valid positions exactly as unpadded
+    (the backward direction starts from a zero state at its last valid position)."""
+    E, H, Vs = 6, 5, 11
+    w = enc_weights(E, H, Vs, 72)
+    rng = np.random.default_rng(73)
+    L, S = 4, 9
+    tok = rng.integers(0, Vs, (1, S)).astype(np.int32)
+    mask = (np.arange(S) < L).astype(np.float32)[None]
+    a = enc(tok, mask, w)
+    b = enc(tok[:, :L], np.ones((1, L), np.float32), w)
+    assert np.array_equal(a[:, :L], b)
+    # padded positions carry the forward state of the last valid position and the zero
+    # backward state
+    assert np.array_equal(a[0, L:, :H], np.repeat(b[0, L - 1:, :H], S - L, 0))
+    assert np.all(a[0, L:, H:] == 0)
+
+
+def test_encoder_reversal_swaps_directions():
+    E, H, Vs, S = 6, 5, 11, 6
+    w = enc_weights(E, H, Vs, 74)
+    tok = np.random.default_rng(75).integers(0, Vs, (2, S)).astype(np.int32)
+    one = np.ones((2, S), np.float32)
+    a = enc(tok, one, w)
+    sw = dict(w, Wf=w["Wb"], Uf=w["Ub"], bf=w["bb"], Wb=w["Wf"], Ub=w["Uf"], bb=w["bf"])
+    b = enc(tok[:, ::-1].copy(), one, sw)
+    assert np.array_equal(a[:, :, :H], b[:, ::-1, H:]) and np.array_equal(a[:, :, H:], b[:, ::-1, :H])
