@@ -88,6 +88,7 @@ typedef struct {
   int32_t gemm_dtype;
   float ln_eps;
   int32_t dec_transitions;
+  int32_t src_V;  /* source vocabulary of the encoder (mt_encode); 0: no encoder */
 } mt_config;
 
 /* Model parameters: HOST pointers to fp32, row-major logical [in x out]
@@ -99,7 +100,9 @@ typedef struct {
  *   layer norm (read only if layer_norm): gain/shift of the input path (a)
  *   and recurrent path (u) of GRU 1 and 2, [3H] each; readout gt/bet [E];
  *   transition blocks (read only if dec_transitions = T > 0), stacked by
- *   block: Ut[T,H,3H] btr[T,3H], and with layer_norm gtu/betu[T,3H]. */
+ *   block: Ut[T,H,3H] btr[T,3H], and with layer_norm gtu/betu[T,3H];
+ *   encoder (read only if src_V > 0): semb[src_V,E], forward Wef[E,3H]
+ *   Uef[H,3H] bef[3H], backward Web[E,3H] Ueb[H,3H] beb[3H]. */
 typedef struct {
   const float *emb;
   const float *W1, *U1, *b1;
@@ -110,6 +113,7 @@ typedef struct {
   const float *Wi, *bi;
   const float *g1a, *be1a, *g1u, *be1u, *g2a, *be2a, *g2u, *be2u, *gt, *bet;
   const float *Ut, *btr, *gtu, *betu;
+  const float *semb, *Wef, *Uef, *bef, *Web, *Ueb, *beb;
 } mt_weights;
 
 typedef struct mt_model mt_model; /* opaque, library-owned */
@@ -138,6 +142,23 @@ mt_status mt_free(mt_model *model);
  * The same workspace must be passed to a step and to the mt_beam_topk call
  * that consumes it (it carries the fused top-K candidates between them). */
 size_t mt_workspace_bytes(const mt_model *model, int B, int K, int S);
+
+/* Workspace bytes of mt_encode for B sentences of padded length S (0 on bad input or
+ * when the model has no encoder). */
+size_t mt_encode_workspace_bytes(const mt_model *model, int B, int S);
+
+/* Encoder::build of the shallow model (Section 2.2; bi-directional RNN encoder):
+ *   ctx_out [B,S,2H] in gemm dtype: ctx[b,i] = [f_i ; g_i], f the forward GRU over
+ *   positions 0..S-1 and g the backward one over S-1..0 (zero initial states) on the
+ *   source embeddings semb[src_tok[b,i]]; at a masked position each direction carries its
+ *   state over (no layer norm).  Ready for mt_precompute_ctx and mt_decoder_step.
+ *   src_tok [B,S] int32 in [0, src_V) (clamped, reported by mt_device_errors);
+ *   mask [B,S] fp32 as for mt_precompute_ctx.  bf16 models keep the states in fp32 in the
+ *   workspace and write their bf16 rounding (also the recurrent products' operand).
+ * 1 <= S <= 1024; B*S <= 2^24.  One product for the input side of every position, then
+ * one recurrent product and two cells per position: 3S launches. */
+mt_status mt_encode(mt_model *model, int B, int S, const int32_t *src_tok, const float *mask, void *ctx_out,
+                    void *ws, size_t ws_bytes, void *stream);
 
 /* Decoder start state for B sentences (Section 2.2, Decoder::startState):
  *   ctx  [B,S,2H] in gemm dtype (fp32 or bf16) — the encoder context;
@@ -243,7 +264,8 @@ typedef enum {
   MT_KERNEL_GEMM_TRANSITION = 12, /* s Ut_j of the transition blocks (dec_transitions > 0) */
   MT_KERNEL_ENSEMBLE = 13,  /* mt_ensemble_logp */
   MT_KERNEL_BEAM_FINISH = 14, /* mt_beam_finish */
-  MT_KERNEL_COUNT = 15
+  MT_KERNEL_ENCODE = 15,    /* every kernel of mt_encode */
+  MT_KERNEL_COUNT = 16
 } mt_kernel_id;
 
 mt_status mt_profile_enable(mt_model *model, uint32_t kernel_mask);

@@ -74,6 +74,9 @@ struct mt_model {
   float *embx;    // [V][3H+E] fp32: emb [W1 | Wt_y] + [b1 | 0], the token side of GRU 1 and the readout
   float *bias1x, *bias3, *ba, *bi, *bt, *va;
   float *ln[10];  // g1a be1a g1u be1u g2a be2a g2u be2u gt bet
+  Packed wenc_x, wenc_f, wenc_b;  // encoder: [Wef | Web], Uef, Ueb
+  float *bias_enc = nullptr;      // [bef | beb]
+  float *semb = nullptr;          // [src_V][E] fp32 source embeddings
   std::vector<Packed> wtr;        // transition blocks' recurrent matrices
   float *btr = nullptr;           // [T][3H] their biases
   float *gtu = nullptr, *betu = nullptr;  // [T][3H] layer norm of their recurrent products
@@ -107,6 +110,7 @@ mt_status check_cfg(const mt_config *c) {
   if (c->tied_output != 0 && c->tied_output != 1) return fail(MT_ERR_ARG, "tied_output must be 0 or 1");
   if (c->gemm_dtype != MT_F32 && c->gemm_dtype != MT_BF16)
     return fail(MT_ERR_DTYPE, "gemm_dtype=%d: need MT_F32 or MT_BF16", c->gemm_dtype);
+  if (c->src_V < 0 || c->src_V > (1 << 24)) return fail(MT_ERR_SHAPE, "src_V=%d: need 0 <= src_V <= 2^24", c->src_V);
   if (c->dec_transitions < 0 || c->dec_transitions > kMaxTransitions)
     return fail(MT_ERR_SHAPE, "dec_transitions=%d: need 0..%d", c->dec_transitions, kMaxTransitions);
   if (c->layer_norm && !(c->ln_eps > 0.f && std::isfinite(c->ln_eps)))
@@ -366,6 +370,12 @@ mt_status mt_load_weights(const mt_config *cfg, const mt_weights *w, mt_model **
   if (c.layer_norm)
     for (int i = 0; i < 10; ++i)
       if (!lnp[i]) return fail(MT_ERR_ARG, "layer-norm parameter %d is NULL (layer_norm = 1)", i);
+  if (c.src_V > 0) {
+    const float *ew[] = {w->semb, w->Wef, w->Uef, w->bef, w->Web, w->Ueb, w->beb};
+    const char *en[] = {"semb", "Wef", "Uef", "bef", "Web", "Ueb", "beb"};
+    for (int i = 0; i < 7; ++i)
+      if (!ew[i]) return fail(MT_ERR_ARG, "encoder weight %s is NULL (src_V = %d)", en[i], c.src_V);
+  }
   if (c.dec_transitions > 0) {
     if (!w->Ut || !w->btr) return fail(MT_ERR_ARG, "Ut or btr is NULL (dec_transitions = %d)", c.dec_transitions);
     if (c.layer_norm && (!w->gtu || !w->betu))
@@ -457,6 +467,13 @@ mt_status mt_load_weights(const mt_config *cfg, const mt_weights *w, mt_model **
       m->ln[i] = nullptr;
       if (c.layer_norm) CHECK(upload_vec(m, cat({{lnp[i], i < 8 ? 3 * H : E}}), &m->ln[i]));
     }
+    if (c.src_V > 0) {
+      CHECK(upload_packed(m, {{w->Wef, 3 * H}, {w->Web, 3 * H}}, E, kRefCtxRows, &m->wenc_x));
+      CHECK(upload_packed(m, {{w->Uef, 3 * H}}, H, kRefSentences, &m->wenc_f));
+      CHECK(upload_packed(m, {{w->Ueb, 3 * H}}, H, kRefSentences, &m->wenc_b));
+      CHECK(upload_vec(m, cat({{w->bef, 3 * H}, {w->beb, 3 * H}}), &m->bias_enc));
+      CHECK(dev_upload(m, w->semb, (size_t)c.src_V * E * sizeof(float), (void **)&m->semb));
+    }
     const int T = c.dec_transitions;
     m->wtr.resize(T);
     for (int j = 0; j < T; ++j)
@@ -517,6 +534,105 @@ size_t mt_workspace_bytes(const mt_model *m, int B, int K, int S) {
   if (!valid_model(m) || B < 1 || K < 1 || K > m->cfg.k_max || S < 1 || S > 1024) return 0;
   const WsLayout L = ws_layout(m, B, K);
   return std::max(L.total, precompute_ws_bytes(m, B, S));
+}
+
+// encoder workspace: input products [B*S][6H], recurrent products of both directions and a
+// zero block [B][3H] each, fp32 states [2 directions][2][B][H] (bf16 models)
+struct EncLayout {
+  size_t xe, uf, ub, uz, st, total;
+};
+static EncLayout enc_layout(const mt_model *m, int B, int S) {
+  const size_t H = m->cfg.H;
+  EncLayout L{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += rup256(bytes);
+    return o;
+  };
+  L.xe = take((size_t)B * S * 6 * H * 4);
+  L.uf = take((size_t)B * 3 * H * 4);
+  L.ub = take((size_t)B * 3 * H * 4);
+  L.uz = take((size_t)B * 3 * H * 4);
+  L.st = take(m->bf16 ? (size_t)4 * B * H * 4 : 0);
+  L.total = off;
+  return L;
+}
+
+size_t mt_encode_workspace_bytes(const mt_model *m, int B, int S) {
+  if (!valid_model(m) || m->cfg.src_V <= 0 || B < 1 || S < 1 || S > 1024 || (long long)B * S > (1 << 24)) return 0;
+  return enc_layout(m, B, S).total;
+}
+
+mt_status mt_encode(mt_model *model, int B, int S, const int32_t *src_tok, const float *mask, void *ctx_out,
+                    void *ws, size_t ws_bytes, void *stream) {
+  g_err[0] = 0;
+  if (!valid_model(model)) return fail(MT_ERR_ARG, "invalid model handle");
+  if (model->cfg.src_V <= 0) return fail(MT_ERR_STATE, "the model has no encoder (src_V = 0)");
+  if (B < 1 || S < 1 || S > 1024) return fail(MT_ERR_SHAPE, "B=%d S=%d: need B >= 1, 1 <= S <= 1024", B, S);
+  if ((long long)B * S > (1 << 24)) return fail(MT_ERR_SHAPE, "B*S exceeds 2^24");
+  CHECK(check_dev_ptr(src_tok, "src_tok", 4));
+  CHECK(check_dev_ptr(mask, "mask", 4));
+  CHECK(check_dev_ptr(ctx_out, "ctx_out"));
+  CHECK(check_dev_ptr(ws, "ws", 256));
+  const EncLayout L = enc_layout(model, B, S);
+  if (ws_bytes < L.total) return fail(MT_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, L.total);
+  hipStream_t st = (hipStream_t)stream;
+  const int H = model->cfg.H, E = model->cfg.E, C = 2 * H, bf = model->bf16;
+  char *W = (char *)ws;
+  float *xe = (float *)(W + L.xe), *uf = (float *)(W + L.uf), *ub = (float *)(W + L.ub), *uz = (float *)(W + L.uz);
+  float *sst = (float *)(W + L.st);  // bf16 models: [dir][parity][B][H]
+  const long ldc = (long)S * C;      // row stride of one sentence's positions in ctx_out
+  // input side of every position and both directions: semb[src_tok] [Wef | Web] + [bef | beb]
+  GemmProblem px{};
+  px.A = model->semb; px.a_idx = src_tok; px.a_rows = model->cfg.src_V; px.lda = E; px.a_bf16 = 0;
+  px.Bp = model->wenc_x.p; px.ldb = model->wenc_x.ldb; px.wblk = model->wenc_x.blk; px.bias = model->bias_enc;
+  px.out = xe; px.ldc = 6 * H; px.M = B * S; px.N = 6 * H; px.K = E; px.err = model->err; px.err_bit = 3;
+  LAUNCH(MT_KERNEL_ENCODE, launch_gemm(bf, &px, 1, EPI_STORE, st));
+  LAUNCH(MT_KERNEL_ENCODE, launch_fill_zero(uz, (long long)B * 3 * H, st));
+  float *c32 = bf ? nullptr : (float *)ctx_out;
+  bf16 *c16 = bf ? (bf16 *)ctx_out : nullptr;
+  for (int n = 0; n < S; ++n) {
+    const int pos[2] = {n, S - 1 - n};       // forward, backward position of this pass
+    const int prv[2] = {n - 1, S - n};       // the position each direction comes from
+    // recurrent products of both directions from the previous states (zero at n = 0)
+    if (n > 0) {
+      GemmProblem pr[2]{};
+      for (int d = 0; d < 2; ++d) {
+        const size_t o = (size_t)prv[d] * C + (size_t)d * H;
+        pr[d].A = bf ? (const void *)(c16 + o) : (const void *)(c32 + o);
+        pr[d].a_rows = B; pr[d].lda = (int)ldc; pr[d].a_bf16 = bf;
+        const Packed &U = d == 0 ? model->wenc_f : model->wenc_b;
+        pr[d].Bp = U.p; pr[d].ldb = U.ldb; pr[d].wblk = U.blk;
+        pr[d].out = d == 0 ? uf : ub; pr[d].ldc = 3 * H; pr[d].M = B; pr[d].N = 3 * H; pr[d].K = H;
+      }
+      LAUNCH(MT_KERNEL_ENCODE, launch_gemm(bf, pr, 2, EPI_STORE, st));
+    }
+    for (int d = 0; d < 2; ++d) {
+      const float *u = n > 0 ? (d == 0 ? uf : ub) : uz;
+      const size_t oc = (size_t)pos[d] * C + (size_t)d * H, op = (size_t)prv[d] * C + (size_t)d * H;
+      const float *hsrc;
+      int ldh;
+      float *out;
+      int ldo;
+      if (bf) {
+        hsrc = n > 0 ? sst + ((size_t)(2 * d + ((n - 1) & 1)) * B) * H : nullptr;
+        ldh = H;
+        out = sst + ((size_t)(2 * d + (n & 1)) * B) * H;
+        ldo = H;
+      } else {
+        hsrc = n > 0 ? c32 + op : nullptr;
+        ldh = (int)ldc;
+        out = c32 + oc;
+        ldo = (int)ldc;
+      }
+      LAUNCH(MT_KERNEL_ENCODE,
+             launch_gru_cell_ex(B, H, xe + (size_t)pos[d] * 6 * H + (size_t)d * 3 * H, S * 6 * H, nullptr, B, u,
+                                3 * H, hsrc, ldh, nullptr, B, model->err, nullptr, nullptr, nullptr, nullptr, 0.f,
+                                out, ldo, bf ? c16 + oc : nullptr, (int)ldc, nullptr, mask + pos[d], S, st));
+    }
+  }
+  return MT_OK;
 }
 
 mt_status mt_precompute_ctx(mt_model *model, int B, int S, const void *ctx, const float *mask,

@@ -66,7 +66,8 @@ __global__ __launch_bounds__(kT) void gru_cell_kernel(int M, int H, const float 
                                                       const float *__restrict__ bu, float eps,
                                                       float *__restrict__ out, int ldo,
                                                       bf16 *__restrict__ out16,
-                                                      float *__restrict__ tap) {
+                                                      float *__restrict__ tap, int ldh, int ld16,
+                                                      const float *__restrict__ keep, int keep_ld) {
   constexpr bool LN = LNM != 0;
   constexpr int G0 = LNM == 2 ? 3 : 0;  // first normalised block
   __shared__ float red[4][12];
@@ -76,7 +77,9 @@ __global__ __launch_bounds__(kT) void gru_cell_kernel(int M, int H, const float 
   const int hr = hidx ? clamp_row(hidx, m, hrows, err, 1) : m;
   const float *arow = a + (size_t)ar * lda;
   const float *urow = u + (size_t)m * ldu;
-  const float *hp = hsrc + (size_t)hr * H;
+  const float *hp = hsrc ? hsrc + (size_t)hr * ldh : nullptr;  // no previous state: zero
+  // keep (if given): a row whose keep value is 0 carries its previous state over
+  const bool upd = keep == nullptr || keep[(size_t)m * keep_ld] != 0.f;
   float x[6][G][4], h[G][4];
   float lg[6][G][4], lb[6][G][4];
 #pragma unroll
@@ -99,7 +102,7 @@ __global__ __launch_bounds__(kT) void gru_cell_kernel(int M, int H, const float 
         lb[3 + g][p][0] = b1.x; lb[3 + g][p][1] = b1.y; lb[3 + g][p][2] = b1.z; lb[3 + g][p][3] = b1.w;
       }
     }
-    const float4 vh = ld4(hp + jc);
+    const float4 vh = hp ? ld4(hp + jc) : make_float4(0.f, 0.f, 0.f, 0.f);
     h[p][0] = vh.x; h[p][1] = vh.y; h[p][2] = vh.z; h[p][3] = vh.w;
   }
   if (LN) {
@@ -151,14 +154,14 @@ __global__ __launch_bounds__(kT) void gru_cell_kernel(int M, int H, const float 
       const float r = sigmoid_fast(x[0][p][e] + x[3][p][e]);
       const float z = sigmoid_fast(x[1][p][e] + x[4][p][e]);
       const float hh = tanh_fast(x[2][p][e] + r * x[5][p][e]);
-      v[e] = (1.0f - z) * hh + z * h[p][e];
+      v[e] = upd ? (1.0f - z) * hh + z * h[p][e] : h[p][e];
     }
     st4(o + j, v[0], v[1], v[2], v[3]);
     if (out16) {  // bf16 copy for a following bf16 product (same rounding as its operand staging)
       bf16 h4[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) h4[e] = to_bf16(v[e]);
-      __builtin_memcpy(out16 + (size_t)m * H + j, h4, sizeof(h4));
+      __builtin_memcpy(out16 + (size_t)m * ld16 + j, h4, sizeof(h4));
     }
     if (tap) st4(tap + (size_t)m * H + j, v[0], v[1], v[2], v[3]);
   }
@@ -319,12 +322,22 @@ hipError_t launch_gru_cell(int M, int H, const float *a, int lda, const int32_t 
                            const float *u, int ldu, const float *hsrc, const int32_t *hidx, int hrows,
                            int32_t *err, const float *ga, const float *ba, const float *gu, const float *bu,
                            float eps, float *out, int ldo, bf16 *out16, float *tap, hipStream_t st) {
+  return launch_gru_cell_ex(M, H, a, lda, aidx, arows, u, ldu, hsrc, H, hidx, hrows, err, ga, ba, gu, bu, eps, out,
+                            ldo, out16, H, tap, nullptr, 0, st);
+}
+
+hipError_t launch_gru_cell_ex(int M, int H, const float *a, int lda, const int32_t *aidx, int arows,
+                              const float *u, int ldu, const float *hsrc, int ldh, const int32_t *hidx, int hrows,
+                              int32_t *err, const float *ga, const float *ba, const float *gu, const float *bu,
+                              float eps, float *out, int ldo, bf16 *out16, int ld16, float *tap,
+                              const float *keep, int keep_ld, hipStream_t st) {
   if (M == 0) return hipSuccess;
   // layer norm on both paths (ga given), on the recurrent path only (gu alone), or none
   const int lnm = ga ? 1 : gu ? 2 : 0;
 #define MT_GRU_L(N, L)                                                                                  \
   hipLaunchKernelGGL((gru_cell_kernel<N, L>), dim3(M), dim3(kT), 0, st, M, H, a, lda, aidx, arows, u,  \
-                     ldu, hsrc, hidx, hrows, err, ga, ba, gu, bu, eps, out, ldo, out16, tap)
+                     ldu, hsrc, hidx, hrows, err, ga, ba, gu, bu, eps, out, ldo, out16, tap, ldh, ld16,    \
+                     keep, keep_ld)
 #define MT_GRU(N)              \
   if (lnm == 1)                \
     MT_GRU_L(N, 1);            \
@@ -384,6 +397,18 @@ hipError_t launch_masked_mean(int B, int S, int Cd, const void *ctx, int ctx_bf1
     hipLaunchKernelGGL(masked_mean_kernel<bf16>, grid, dim3(kT), 0, st, B, S, Cd, (const bf16 *)ctx, mask, out);
   else
     hipLaunchKernelGGL(masked_mean_kernel<float>, grid, dim3(kT), 0, st, B, S, Cd, (const float *)ctx, mask, out);
+  return hipGetLastError();
+}
+
+__global__ __launch_bounds__(256) void fill_zero_kernel(float *__restrict__ p, long long n) {
+  for (long long i = (long long)blockIdx.x * 256 + threadIdx.x; i < n; i += (long long)gridDim.x * 256) p[i] = 0.f;
+}
+
+hipError_t launch_fill_zero(float *p, long long n, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  long long blocks = (n + 255) / 256;
+  if (blocks > 1024) blocks = 1024;
+  hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)blocks), dim3(256), 0, st, p, n);
   return hipGetLastError();
 }
 

@@ -21,7 +21,7 @@ MT_OK, MT_ERR_ARG, MT_ERR_SHAPE, MT_ERR_DTYPE, MT_ERR_HIP, MT_ERR_OOM, MT_ERR_ST
 MT_F32, MT_BF16 = 0, 1
 KERNELS = ["GEMM_GRU1", "GRU_CELL", "GEMM_S1", "ATTENTION", "GEMM_CTX", "GEMM_READOUT", "READOUT",
            "VOCAB_GEMM", "LSE", "TOPK", "PRECOMPUTE", "VOCAB_THRESHOLD", "GEMM_TRANSITION", "ENSEMBLE",
-           "BEAM_FINISH"]
+           "BEAM_FINISH", "ENCODE"]
 KERNEL_ID = {n: i for i, n in enumerate(KERNELS)}
 
 
@@ -34,12 +34,14 @@ class MtError(RuntimeError):
 class mt_config(C.Structure):
     _fields_ = [("E", C.c_int32), ("H", C.c_int32), ("A", C.c_int32), ("V", C.c_int32),
                 ("layer_norm", C.c_int32), ("tied_output", C.c_int32), ("k_max", C.c_int32),
-                ("gemm_dtype", C.c_int32), ("ln_eps", C.c_float), ("dec_transitions", C.c_int32)]
+                ("gemm_dtype", C.c_int32), ("ln_eps", C.c_float), ("dec_transitions", C.c_int32),
+                ("src_V", C.c_int32)]
 
 
 WEIGHT_FIELDS = ["emb", "W1", "U1", "b1", "Ua", "ba", "Wa", "va", "W2", "U2", "b2", "Wt_s", "Wt_y",
                  "Wt_c", "bt", "Wo", "bo", "Wi", "bi", "g1a", "be1a", "g1u", "be1u", "g2a", "be2a",
-                 "g2u", "be2u", "gt", "bet", "Ut", "btr", "gtu", "betu"]
+                 "g2u", "be2u", "gt", "bet", "Ut", "btr", "gtu", "betu",
+                 "semb", "Wef", "Uef", "bef", "Web", "Ueb", "beb"]
 
 _fp = C.POINTER(C.c_float)
 
@@ -75,12 +77,15 @@ def lib() -> C.CDLL:
         L.mt_beam_topk.argtypes = [_vp, C.c_int, C.c_int, _vp, _vp, _vp, _vp, _vp, _vp, _vp, C.c_size_t, _vp]
         L.mt_device_errors.argtypes = [_vp, C.POINTER(C.c_int32)]
         L.mt_ensemble_logp.argtypes = [_vp, C.c_int, C.POINTER(_vp), C.POINTER(C.c_float), C.c_int, _vp, _vp]
+        L.mt_encode_workspace_bytes.argtypes = [_vp, C.c_int, C.c_int]
+        L.mt_encode_workspace_bytes.restype = C.c_size_t
+        L.mt_encode.argtypes = [_vp, C.c_int, C.c_int, _vp, _vp, _vp, _vp, C.c_size_t, _vp]
         L.mt_beam_finish.argtypes = [_vp, C.c_int, C.c_int, C.c_int, C.c_int32, C.c_float, C.c_int] + [_vp] * 14
         L.mt_profile_enable.argtypes = [_vp, C.c_uint32]
         L.mt_profile_reset.argtypes = [_vp]
         L.mt_profile_query.argtypes = [_vp, C.c_int, C.POINTER(C.c_double), C.POINTER(C.c_int64)]
         for f in ("mt_load_weights", "mt_free", "mt_precompute_ctx", "mt_decoder_step", "mt_beam_topk",
-                  "mt_ensemble_logp", "mt_beam_finish",
+                  "mt_ensemble_logp", "mt_beam_finish", "mt_encode",
                   "mt_device_errors", "mt_profile_enable", "mt_profile_reset", "mt_profile_query"):
             getattr(L, f).restype = C.c_int
         _lib = L
@@ -113,9 +118,9 @@ def _stream(stream) -> Optional[int]:
 
 
 def make_config(E, H, A, V, *, layer_norm=False, tied_output=False, k_max=16, gemm="f32", ln_eps=1e-5,
-                transitions=0):
+                transitions=0, src_V=0):
     return mt_config(E, H, A, V, int(layer_norm), int(tied_output), k_max,
-                     MT_BF16 if gemm == "bf16" else MT_F32, ln_eps, transitions)
+                     MT_BF16 if gemm == "bf16" else MT_F32, ln_eps, transitions, src_V)
 
 
 class Model:
@@ -164,6 +169,16 @@ def mt_beam_finish(model: Model, B, K, step, eos, alpha, final, tok, bp, row, sc
                                 *[_ptr(x) for x in (tok, bp, row, score, beam, fin_count, hist_tok, hist_bp,
                                                     fin_score, fin_norm, fin_step, fin_parent, fin_tok)],
                                 _stream(stream)))
+
+
+def mt_encode_workspace_bytes(model: Model, B: int, S: int) -> int:
+    return int(lib().mt_encode_workspace_bytes(model.handle, B, S))
+
+
+def mt_encode(model: Model, B, S, src_tok, mask, ctx_out, ws, ws_bytes=None, stream=None):
+    ws_bytes = ws.numel() * ws.element_size() if ws_bytes is None else ws_bytes
+    _check(lib().mt_encode(model.handle, B, S, _ptr(src_tok), _ptr(mask), _ptr(ctx_out), _ptr(ws), ws_bytes,
+                           _stream(stream)))
 
 
 def mt_free(model: Model):

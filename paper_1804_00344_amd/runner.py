@@ -18,12 +18,12 @@ from . import mtstep as mt
 class Decoder:
     def __init__(self, E: int, H: int, A: int, V: int, weights: Dict[str, np.ndarray], *, gemm: str = "f32",
                  layer_norm: bool = False, tied_output: bool = False, k_max: int = 16, ln_eps: float = 1e-5,
-                 transitions: int = 0, device: str = "cuda:0"):
+                 transitions: int = 0, src_V: int = 0, device: str = "cuda:0"):
         self.E, self.H, self.A, self.V, self.C = E, H, A, V, 2 * H
         self.gemm = gemm
         self.device = torch.device(device)
         self.cfg = mt.make_config(E, H, A, V, layer_norm=layer_norm, tied_output=tied_output, k_max=k_max,
-                                  gemm=gemm, ln_eps=ln_eps, transitions=transitions)
+                                  gemm=gemm, ln_eps=ln_eps, transitions=transitions, src_V=src_V)
         with torch.cuda.device(self.device):
             self.model = mt.mt_load_weights(self.cfg, weights)
         self.io_dtype = torch.bfloat16 if gemm == "bf16" else torch.float32
@@ -53,6 +53,32 @@ class Decoder:
         self.bp = torch.empty(M, dtype=torch.int32, device=d)
         self.score = torch.empty(M, dtype=torch.float32, device=d)
         self.cur = 0
+
+    def set_source(self, src_tok: np.ndarray, mask: np.ndarray, K: int, stream=None):
+        """Batch from source tokens: the context comes from the model's encoder (mt_encode)."""
+        B, S = src_tok.shape
+        self.set_batch(np.zeros((1, 1, self.C), np.float32), np.ones((1, 1), np.float32), K)  # buffers of the right kind
+        d = self.device
+        self.B, self.S, self.K, self.M = B, S, K, B * K
+        self.src_tok = torch.from_numpy(np.ascontiguousarray(src_tok, np.int32)).to(d)
+        self.mask = torch.from_numpy(np.ascontiguousarray(mask, np.float32)).to(d)
+        self.ctx = torch.empty((B, S, self.C), dtype=self.io_dtype, device=d)
+        self.pctx = torch.empty((B, S, self.A), dtype=self.io_dtype, device=d)
+        self.s0 = torch.empty((B, self.H), dtype=torch.float32, device=d)
+        nbytes = mt.mt_workspace_bytes(self.model, B, K, S)
+        self.ws = torch.empty(nbytes, dtype=torch.uint8, device=d)
+        self.ews = torch.empty(mt.mt_encode_workspace_bytes(self.model, B, S), dtype=torch.uint8, device=d)
+        M = self.M
+        self.state = [torch.empty((M, self.H), dtype=torch.float32, device=d) for _ in range(2)]
+        self.tok = torch.empty(M, dtype=torch.int32, device=d)
+        self.row = torch.empty(M, dtype=torch.int32, device=d)
+        self.bp = torch.empty(M, dtype=torch.int32, device=d)
+        self.score = torch.empty(M, dtype=torch.float32, device=d)
+        self.cur = 0
+        self.encode(stream=stream)
+
+    def encode(self, stream=None):
+        mt.mt_encode(self.model, self.B, self.S, self.src_tok, self.mask, self.ctx, self.ews, stream=stream)
 
     def precompute(self, stream=None):
         mt.mt_precompute_ctx(self.model, self.B, self.S, self.ctx, self.mask, self.pctx, self.s0, self.ws,
@@ -184,6 +210,32 @@ class Ensemble:
         lead = self.lead
         self.logp = [torch.empty((lead.M, lead.V), dtype=torch.float32, device=lead.device) for _ in self.members]
         self.comb = torch.empty((lead.M, lead.V), dtype=torch.float32, device=lead.device)
+
+    def set_source(self, src_tok: np.ndarray, mask: np.ndarray, K: int, stream=None):
+        """Batch from source tokens: the context comes from the model's encoder (mt_encode)."""
+        B, S = src_tok.shape
+        self.set_batch(np.zeros((1, 1, self.C), np.float32), np.ones((1, 1), np.float32), K)  # buffers of the right kind
+        d = self.device
+        self.B, self.S, self.K, self.M = B, S, K, B * K
+        self.src_tok = torch.from_numpy(np.ascontiguousarray(src_tok, np.int32)).to(d)
+        self.mask = torch.from_numpy(np.ascontiguousarray(mask, np.float32)).to(d)
+        self.ctx = torch.empty((B, S, self.C), dtype=self.io_dtype, device=d)
+        self.pctx = torch.empty((B, S, self.A), dtype=self.io_dtype, device=d)
+        self.s0 = torch.empty((B, self.H), dtype=torch.float32, device=d)
+        nbytes = mt.mt_workspace_bytes(self.model, B, K, S)
+        self.ws = torch.empty(nbytes, dtype=torch.uint8, device=d)
+        self.ews = torch.empty(mt.mt_encode_workspace_bytes(self.model, B, S), dtype=torch.uint8, device=d)
+        M = self.M
+        self.state = [torch.empty((M, self.H), dtype=torch.float32, device=d) for _ in range(2)]
+        self.tok = torch.empty(M, dtype=torch.int32, device=d)
+        self.row = torch.empty(M, dtype=torch.int32, device=d)
+        self.bp = torch.empty(M, dtype=torch.int32, device=d)
+        self.score = torch.empty(M, dtype=torch.float32, device=d)
+        self.cur = 0
+        self.encode(stream=stream)
+
+    def encode(self, stream=None):
+        mt.mt_encode(self.model, self.B, self.S, self.src_tok, self.mask, self.ctx, self.ews, stream=stream)
 
     def precompute(self, stream=None):
         for d in self.members:

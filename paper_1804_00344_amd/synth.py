@@ -246,5 +246,33 @@ def mid_decode_inputs(p: Preset, salt: int = 0):
     return tok, src_row, state, score.reshape(M).astype(np.float32)
 
 
+ENCODER_NAMES = ("semb", "Wef", "Uef", "bef", "Web", "Ueb", "beb")
+
+
+def make_encoder_weights(p: Preset, src_V: int) -> Dict[str, np.ndarray]:
+    """Bi-directional GRU encoder over a source vocabulary of src_V: embeddings N(0, 0.1),
+    gate matrices Glorot-uniform per gate block, zero biases (bf16 presets round the product
+    operands to bf16)."""
+    E, H = p.E, p.H
+    w = {"semb": rng_for(p, "semb").normal(0.0, 0.1, size=(src_V, E)).astype(np.float32),
+         "Wef": _gate_matrix(p, "Wef", E), "Uef": _gate_matrix(p, "Uef", H), "bef": np.zeros(3 * H, np.float32),
+         "Web": _gate_matrix(p, "Web", E), "Ueb": _gate_matrix(p, "Ueb", H), "beb": np.zeros(3 * H, np.float32)}
+    if p.gemm == "bf16":
+        for k in ("semb", "Wef", "Uef", "Web", "Ueb"):
+            w[k] = round_bf16(w[k])
+    return w
+
+
+def source_tokens(p: Preset, src_V: int, lens: np.ndarray, S: int) -> np.ndarray:
+    """Source token ids [B, S]: Zipf(1.1) over src_V at valid positions, 0 at padding."""
+    rng = rng_for(p, "src_tok")
+    r = np.arange(1, src_V + 1, dtype=np.float64)
+    cdf = np.cumsum(r ** -1.1)
+    cdf /= cdf[-1]
+    tok = np.searchsorted(cdf, rng.random((len(lens), S))).astype(np.int32)
+    tok[np.arange(S)[None, :] >= np.asarray(lens)[:, None]] = 0
+    return np.minimum(tok, src_V - 1).astype(np.int32)
+
+
 def with_sizes(p: Preset, **kw) -> Preset:
     return dataclasses.replace(p, **kw)

@@ -553,3 +553,42 @@ def test_translate_nbest_parity(name, eos):
     lens_ = sorted({len(r[2]) for b in range(p.B) for r in ref[b]})
     log(f"[translate] {name}: {p.B} sentences, {ran} steps, {n_eos} of {p.B * p.K} hypotheses end in EOS, "
         f"lengths {lens_}")
+
+
+# ------------------------------------------------------------------------------------------
+# encoder (mt_encode): bi-directional GRU over source tokens, then the decoder step on its
+# context
+# ------------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name,src_V,n_sent", [("tiny_f32", 1000, 99), ("tiny_bf16_ln", 1000, 6),
+                                                ("nematus_f32", 30000, 3), ("nematus_bf16_ln", 30000, 3)])
+def test_encoder_parity(name, src_V, n_sent):
+    p = synth.PRESETS[name]
+    log(f"\n[encoder] {name} src_V={src_V}")
+    w = synth.make_weights(p, peaked_bias=True)
+    ew = synth.make_encoder_weights(p, src_V)
+    _, mask, lens = synth.make_source(p)
+    S = mask.shape[1]
+    src = synth.source_tokens(p, src_V, lens, S)
+    dec = Decoder(p.E, p.H, p.A, p.V, {**w, **ew}, gemm=p.gemm, layer_norm=p.layer_norm, k_max=max(p.K, 1),
+                  src_V=src_V)
+    dec.set_source(src, mask, p.K)
+    dec.precompute()
+    ctx_gpu = dec.ctx.float().cpu().numpy()
+    assert mt.mt_device_errors(dec.model) == 0
+    sents = sample_sentences(lens, n_sent)
+    tol = TOL[p.gemm]["state"]
+    worst = 0.0
+    for b in sents:
+        ref = mtref.encode(src[b:b + 1], mask[b:b + 1], *[ew[k] for k in synth.ENCODER_NAMES])
+        L = int(lens[b])
+        worst = max(worst, maxerr(ctx_gpu[b, :L], ref[0, :L]))
+    log(f"[encoder] {name}: context max error {worst:.3g} over sentences {sents[:6]}")
+    assert worst <= tol
+    if name == "tiny_f32":
+        # the step on the encoded context against the oracle's encoder + step
+        ctx_o = mtref.encode(src, mask, *[ew[k] for k in synth.ENCODER_NAMES])
+        tok, srow, state, score = synth.mid_decode_inputs(p, salt=6)
+        gpu = run_step(dec, p, tok, srow, T(state), p.M)
+        orc = oracle_sentences(oracle_model(p, w), p.K, sents, ctx_o, mask, tok, srow, state)
+        compare_rows(p, gpu, orc, sents, TOL[p.gemm], name + "_encoded")
