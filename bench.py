@@ -95,6 +95,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--ensemble", type=int, default=1,
                     help="members decoding one beam (seeded weights per member, equal weights)")
+    ap.add_argument("--encode", type=int, default=0,
+                    help="also time the encoder (mt_encode) over the batch with a source vocabulary of this size")
     ap.add_argument("--translate", type=int, default=0,
                     help="time whole translations of the batch to n-best lists (this many steps at most; "
                          "EOS = token 0, length normalisation alpha 0.6) instead of a fixed step count")
@@ -243,6 +245,29 @@ def main():
         "roofline": roofline,
         "kernels": breakdown,
     }
+    if args.encode:
+        # encoder of the same shapes over Zipf source tokens with the batch's lengths
+        ew = synth.make_encoder_weights(p, args.encode)
+        encd = Decoder(p.E, p.H, p.A, p.V, {**w, **ew}, gemm=p.gemm, layer_norm=p.layer_norm, k_max=max(p.K, 1),
+                       src_V=args.encode)
+        src = synth.source_tokens(p, args.encode, lens, dec.S)
+        encd.set_source(src, mask, p.K)
+        for _ in range(3):
+            encd.encode()
+        torch.cuda.synchronize()
+        reps = 20
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            encd.encode()
+        torch.cuda.synchronize()
+        e_s = (time.perf_counter() - t0) / reps
+        rec["encode"] = {
+            "what": "mt_encode of the batch: bi-directional GRU over the padded source (one input product, then "
+                    "per position the recurrent products of both directions and two cells)",
+            "src_V": args.encode, "padded_S": int(dec.S), "ms_per_batch": round(1e3 * e_s, 3),
+            "src_tokens_per_s": round(float(lens.sum()) / e_s, 1),
+            "per_decoder_step_us_at_precompute_interval": round(1e6 * e_s / p.steps, 2),
+        }
     if args.translate:
         rec["translate"] = {
             "what": "whole translations of the batch to n-best lists of K (steps, selections, bookkeeping, "
