@@ -186,18 +186,47 @@ int mtref_precompute(const mtref_dims *d, const mtref_weights *w, int B, int S,
   return 0;
 }
 
+/* Attention keys of a second source (dual-source models): P2 = ctx2 Ua2 + ba2 at valid
+ * positions, 0 elsewhere. */
+int mtref_keys2(const mtref_dims *d, const mtref_weights *w, int B, int S, const float *ctx, const float *mask,
+                float *P_out) {
+  if (!d || !w || !w->Ua2 || !w->ba2 || B < 0 || S < 1 || !ctx || !mask || !P_out) return -1;
+  const int C = 2 * d->H, A = d->A;
+  double *row = (double *)malloc(sizeof(double) * C);
+  double *tmp = (double *)malloc(sizeof(double) * A);
+  for (long i = 0; i < (long)B * S; ++i) {
+    float *Pr = P_out + (size_t)i * A;
+    if (mask[i] == 0.0f) {
+      for (int a = 0; a < A; ++a) Pr[a] = 0.0f;
+      continue;
+    }
+    to_double(C, ctx + (size_t)i * C, row);
+    vec_mat(C, A, A, row, w->Ua2, w->ba2, tmp);
+    round_store(A, tmp, Pr, NULL);
+  }
+  free(row);
+  free(tmp);
+  return 0;
+}
+
 /* Decoder::step for one batch of hypotheses (Section 2.2: consumes the target
- * part of the batch and produces the logits and the next state). */
-int mtref_step(const mtref_dims *d, const mtref_weights *w, int B, int K, int S,
-               const int32_t *prev_tok, const int32_t *src_row, int n_state_rows,
-               const float *state_in, const float *ctx, const float *P, const float *mask,
-               float *state_out, float *logp_out, float *alpha_out,
-               float *s1_out, float *c_out, float *t_out) {
+ * part of the batch and produces the logits and the next state).  With a second
+ * source (S2 > 0; dual-attention models of the post-editing systems in Section 3.2)
+ * the intermediate state s1 also queries the second source through its own attention,
+ * and GRU block 2 and the readout take the two contexts side by side. */
+static int step_impl(const mtref_dims *d, const mtref_weights *w, int B, int K, int S,
+                     const int32_t *prev_tok, const int32_t *src_row, int n_state_rows,
+                     const float *state_in, const float *ctx, const float *P, const float *mask,
+                     int S2, const float *ctx2, const float *P2, const float *mask2,
+                     float *state_out, float *logp_out, float *alpha_out,
+                     float *s1_out, float *c_out, float *t_out) {
   if (!d || !w || B < 0 || K < 1 || S < 1 || !prev_tok || !src_row || !state_in || !ctx ||
       !P || !mask || !state_out || d->transitions < 0 ||
-      (d->transitions > 0 && (!w->Ut || !w->btr || (d->layer_norm && (!w->gtu || !w->betu)))))
+      (d->transitions > 0 && (!w->Ut || !w->btr || (d->layer_norm && (!w->gtu || !w->betu)))) ||
+      (S2 > 0 && (!ctx2 || !P2 || !mask2 || !w->Wa2 || !w->va2)))
     return -1;
-  const int E = d->E, H = d->H, C = 2 * d->H, A = d->A, V = d->V;
+  const int E = d->E, H = d->H, C1 = 2 * d->H, A = d->A, V = d->V;
+  const int C = S2 > 0 ? 2 * C1 : C1;  /* width of the context fed to GRU 2 and the readout */
   const int M = B * K;
   for (int m = 0; m < M; ++m) {
     if (prev_tok[m] < 0 || prev_tok[m] >= V) return -2;
@@ -208,7 +237,7 @@ int mtref_step(const mtref_dims *d, const mtref_weights *w, int B, int K, int S,
   double *h = (double *)malloc(sizeof(double) * H);
   double *s1 = (double *)malloc(sizeof(double) * H);
   double *q = (double *)malloc(sizeof(double) * A);
-  double *al = (double *)malloc(sizeof(double) * S);
+  double *al = (double *)malloc(sizeof(double) * (S > S2 ? S : S2));
   double *c = (double *)malloc(sizeof(double) * C);
   double *s = (double *)malloc(sizeof(double) * H);
   double *t = (double *)malloc(sizeof(double) * E);
@@ -233,12 +262,18 @@ int mtref_step(const mtref_dims *d, const mtref_weights *w, int B, int K, int S,
     /* attention query from the intermediate state */
     vec_mat(H, A, A, s1, w->Wa, NULL, q);
     round_store(A, q, f, q);
-    mtref_attention(S, A, C, q, P + (size_t)b * S * A, ctx + (size_t)b * S * C,
+    mtref_attention(S, A, C1, q, P + (size_t)b * S * A, ctx + (size_t)b * S * C1,
                     mask + (size_t)b * S, w->va, al, c);
-    round_store(C, c, f, c);
-    if (c_out) memcpy(c_out + (size_t)m * C, f, sizeof(float) * C);
     if (alpha_out)
       for (int i = 0; i < S; ++i) alpha_out[(size_t)m * S + i] = (float)al[i];
+    if (S2 > 0) {  /* the second source: its own query projection, keys and va */
+      vec_mat(H, A, A, s1, w->Wa2, NULL, q);
+      round_store(A, q, f, q);
+      mtref_attention(S2, A, C1, q, P2 + (size_t)b * S2 * A, ctx2 + (size_t)b * S2 * C1,
+                      mask2 + (size_t)b * S2, w->va2, al, c + C1);
+    }
+    round_store(C, c, f, c);
+    if (c_out) memcpy(c_out + (size_t)m * C, f, sizeof(float) * C);
 
     /* GRU block 2: input = attention context, state = s1 */
     mtref_gru(C, H, c, s1, w->W2, w->U2, w->b2, ln ? w->g2a : NULL, ln ? w->be2a : NULL,
@@ -283,6 +318,26 @@ int mtref_step(const mtref_dims *d, const mtref_weights *w, int B, int K, int S,
   free(x); free(h); free(s1); free(q); free(al); free(c); free(s); free(t); free(part);
   free(l); free(f);
   return 0;
+}
+
+int mtref_step(const mtref_dims *d, const mtref_weights *w, int B, int K, int S,
+               const int32_t *prev_tok, const int32_t *src_row, int n_state_rows,
+               const float *state_in, const float *ctx, const float *P, const float *mask,
+               float *state_out, float *logp_out, float *alpha_out,
+               float *s1_out, float *c_out, float *t_out) {
+  return step_impl(d, w, B, K, S, prev_tok, src_row, n_state_rows, state_in, ctx, P, mask, 0, NULL, NULL, NULL,
+                   state_out, logp_out, alpha_out, s1_out, c_out, t_out);
+}
+
+int mtref_step_dual(const mtref_dims *d, const mtref_weights *w, int B, int K, int S,
+                    const int32_t *prev_tok, const int32_t *src_row, int n_state_rows,
+                    const float *state_in, const float *ctx, const float *P, const float *mask,
+                    int S2, const float *ctx2, const float *P2, const float *mask2,
+                    float *state_out, float *logp_out, float *alpha_out,
+                    float *s1_out, float *c_out, float *t_out) {
+  if (S2 < 1) return -1;
+  return step_impl(d, w, B, K, S, prev_tok, src_row, n_state_rows, state_in, ctx, P, mask, S2, ctx2, P2, mask2,
+                   state_out, logp_out, alpha_out, s1_out, c_out, t_out);
 }
 
 /* Encoder::build for the shallow model (Section 2.2; bi-directional RNN encoder, Section

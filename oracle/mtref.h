@@ -42,6 +42,9 @@ typedef struct {
   /* transition blocks j < transitions, stacked: Ut [T][H,3H], btr [T][3H]; layer norm of
    * their recurrent products (only read if layer_norm): gtu, betu [T][3H] */
   const float *Ut, *btr, *gtu, *betu;
+  /* second source (dual-source models): Ua2 [C,A], ba2 [A], Wa2 [H,A], va2 [A]; W2 and
+   * Wt_c then have 2C rows (the two contexts side by side) */
+  const float *Ua2, *ba2, *Wa2, *va2;
 } mtref_weights;
 
 /* status: 0 ok, -1 bad argument, -2 index out of range */
@@ -112,6 +115,20 @@ int mtref_step(const mtref_dims *d, const mtref_weights *w, int B, int K, int S,
 int mtref_encode(int E, int H, int Vs, int B, int S, const int32_t *src_tok, const float *mask,
                  const float *semb, const float *Wf, const float *Uf, const float *bf,
                  const float *Wb, const float *Ub, const float *bb, float *ctx_out);
+
+/* Attention keys of the second source: P2 = ctx2 Ua2 + ba2 at valid positions, 0 elsewhere. */
+int mtref_keys2(const mtref_dims *d, const mtref_weights *w, int B, int S, const float *ctx, const float *mask,
+                float *P_out);
+
+/* The step of a dual-source model: as mtref_step, and s1 also queries the second source
+ * (S2 positions, ctx2 [B,S2,C], keys P2, mask2) through q2 = s1 Wa2 and va2; GRU 2 and the
+ * readout take c = [c1 ; c2] (2C wide; the c tap is [M, 2C]); alpha is the first source's. */
+int mtref_step_dual(const mtref_dims *d, const mtref_weights *w, int B, int K, int S,
+                    const int32_t *prev_tok, const int32_t *src_row, int n_state_rows,
+                    const float *state_in, const float *ctx, const float *P, const float *mask,
+                    int S2, const float *ctx2, const float *P2, const float *mask2,
+                    float *state_out, float *logp_out, float *alpha_out,
+                    float *s1_out, float *c_out, float *t_out);
 
 /* Beam selection: for each sentence b, candidates cand(k,v) = score[b*K+k] +
  * logp[b*K+k, v] evaluated in fp32; the K best by (cand descending, flat

@@ -43,7 +43,7 @@ class _Dims(C.Structure):
 _WNAMES = ["emb", "W1", "U1", "b1", "Ua", "ba", "Wa", "va", "W2", "U2", "b2",
            "Wt_s", "Wt_y", "Wt_c", "bt", "Wo", "bo", "Wi", "bi",
            "g1a", "be1a", "g1u", "be1u", "g2a", "be2a", "g2u", "be2u", "gt", "bet",
-           "Ut", "btr", "gtu", "betu"]
+           "Ut", "btr", "gtu", "betu", "Ua2", "ba2", "Wa2", "va2"]
 _LN_NAMES = ("g1a", "be1a", "g1u", "be1u", "g2a", "be2a", "g2u", "be2u", "gt", "bet")
 
 
@@ -76,6 +76,11 @@ def lib():
         L.mtref_step.argtypes = [C.POINTER(_Dims), C.POINTER(_Weights), C.c_int, C.c_int, C.c_int,
                                  _i, _i, C.c_int, _f, _f, _f, _f, _f, _f, _f, _f, _f, _f]
         L.mtref_step.restype = C.c_int
+        L.mtref_keys2.argtypes = [C.POINTER(_Dims), C.POINTER(_Weights), C.c_int, C.c_int, _f, _f, _f]
+        L.mtref_keys2.restype = C.c_int
+        L.mtref_step_dual.argtypes = [C.POINTER(_Dims), C.POINTER(_Weights), C.c_int, C.c_int, C.c_int,
+                                      _i, _i, C.c_int, _f, _f, _f, _f, C.c_int, _f, _f, _f, _f, _f, _f, _f, _f, _f]
+        L.mtref_step_dual.restype = C.c_int
         L.mtref_encode.argtypes = [C.c_int, C.c_int, C.c_int, C.c_int, C.c_int, _i, _f, _f, _f, _f, _f, _f, _f, _f, _f]
         L.mtref_encode.restype = C.c_int
         L.mtref_topk.argtypes = [C.c_int, C.c_int, C.c_int, _f, _f, _i, _i, _f]
@@ -169,10 +174,12 @@ class Model:
 
     def __init__(self, E: int, H: int, A: int, V: int, weights: Dict[str, np.ndarray],
                  layer_norm: bool = False, tied_output: bool = False, ln_eps: float = 1e-5,
-                 transitions: int = 0):
+                 transitions: int = 0, dual_source: bool = False):
         self.E, self.H, self.A, self.V = E, H, A, V
         self.C = 2 * H
         self.T = transitions
+        self.dual = bool(dual_source)
+        self.Cc = (2 if self.dual else 1) * 2 * H  # width of the context fed to GRU 2 and the readout
         self.dims = _Dims(E, H, A, V, int(layer_norm), int(tied_output), ln_eps, transitions)
         self._keep = {}
         shapes = {
@@ -188,16 +195,24 @@ class Model:
         shapes["bet"] = (E,)
         T = transitions
         shapes.update({"Ut": (T, H, 3 * H), "btr": (T, 3 * H), "gtu": (T, 3 * H), "betu": (T, 3 * H)})
+        shapes.update({"Ua2": (2 * H, A), "ba2": (A,), "Wa2": (H, A), "va2": (A,)})
+        shapes["W2"] = (self.Cc, 3 * H)
+        shapes["Wt_c"] = (self.Cc, E)
         ptrs = {}
         for n in _WNAMES:
             a = weights.get(n)
             if n in ("Ut", "btr", "gtu", "betu") and T == 0:
                 a = None  # a shallow model reads no transition weights
+            if n in ("Ua2", "ba2", "Wa2", "va2") and not self.dual:
+                a = None
             if a is None:
                 if n in _LN_NAMES and not layer_norm:
                     ptrs[n] = None
                     continue
                 if n in ("Ut", "btr", "gtu", "betu") and (T == 0 or (n in ("gtu", "betu") and not layer_norm)):
+                    ptrs[n] = None
+                    continue
+                if n in ("Ua2", "ba2", "Wa2", "va2") and not self.dual:
                     ptrs[n] = None
                     continue
                 if n == "Wo" and tied_output:
@@ -223,8 +238,17 @@ class Model:
             raise ValueError(f"mtref_precompute: {rc}")
         return P, s0
 
+    def keys2(self, ctx2, mask2):
+        ctx2, mask2 = f32(ctx2), f32(mask2)
+        B, S, _ = ctx2.shape
+        P2 = np.empty((B, S, self.A), np.float32)
+        rc = lib().mtref_keys2(C.byref(self.dims), C.byref(self.w), B, S, _fp(ctx2), _fp(mask2), _fp(P2))
+        if rc != 0:
+            raise ValueError(f"mtref_keys2: {rc}")
+        return P2
+
     def step(self, K, prev_tok, src_row, state_in, ctx, P, mask, want_logp=True,
-             want_alpha=False, taps=False):
+             want_alpha=False, taps=False, src2=None):
         ctx, P, mask, state_in = f32(ctx), f32(P), f32(mask), f32(state_in)
         prev_tok = np.ascontiguousarray(prev_tok, np.int32)
         src_row = np.ascontiguousarray(src_row, np.int32)
@@ -238,13 +262,20 @@ class Model:
             out["alpha"] = np.empty((M, S), np.float32)
         if taps:
             out["s1"] = np.empty((M, self.H), np.float32)
-            out["c"] = np.empty((M, self.C), np.float32)
+            out["c"] = np.empty((M, self.Cc), np.float32)
             out["t"] = np.empty((M, self.E), np.float32)
-        rc = lib().mtref_step(
-            C.byref(self.dims), C.byref(self.w), B, K, S, _ip(prev_tok), _ip(src_row),
-            state_in.shape[0], _fp(state_in), _fp(ctx), _fp(P), _fp(mask), _fp(out["state"]),
-            _fp(out.get("logp")), _fp(out.get("alpha")), _fp(out.get("s1")), _fp(out.get("c")),
-            _fp(out.get("t")))
+        tail = (_fp(out["state"]), _fp(out.get("logp")), _fp(out.get("alpha")), _fp(out.get("s1")),
+                _fp(out.get("c")), _fp(out.get("t")))
+        if self.dual:
+            ctx2, P2, mask2 = (f32(a) for a in src2)
+            rc = lib().mtref_step_dual(
+                C.byref(self.dims), C.byref(self.w), B, K, S, _ip(prev_tok), _ip(src_row),
+                state_in.shape[0], _fp(state_in), _fp(ctx), _fp(P), _fp(mask), ctx2.shape[1], _fp(ctx2), _fp(P2),
+                _fp(mask2), *tail)
+        else:
+            rc = lib().mtref_step(
+                C.byref(self.dims), C.byref(self.w), B, K, S, _ip(prev_tok), _ip(src_row),
+                state_in.shape[0], _fp(state_in), _fp(ctx), _fp(P), _fp(mask), *tail)
         if rc != 0:
             raise ValueError(f"mtref_step: {rc}")
         return out

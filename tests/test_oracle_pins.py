@@ -833,3 +833,85 @@ def test_encoder_reversal_swaps_directions():
     sw = dict(w, Wf=w["Wb"], Uf=w["Ub"], bf=w["bb"], Wb=w["Wf"], Ub=w["Uf"], bb=w["bf"])
     b = enc(tok[:, ::-1].copy(), one, sw)
     assert np.array_equal(a[:, :, :H], b[:, ::-1, H:]) and np.array_equal(a[:, :, H:], b[:, ::-1, :H])
+
+
+# --------------------------------------------------------------------------------------
+# dual-source step (two encoders; the decoder attends to both)
+# --------------------------------------------------------------------------------------
+
+
+def dual_model(seed=80, **over):
+    rng = np.random.default_rng(seed + 500)
+    H, E, A = H_, E_, A_
+    C = 2 * H
+    _, w = tiny_model(seed=seed)
+    w.update(Ua2=rnd(C, A, s=0.4, rng=rng), ba2=rnd(A, s=0.1, rng=rng), Wa2=rnd(H, A, s=0.5, rng=rng),
+             va2=rnd(A, rng=rng), W2=rnd(2 * C, 3 * H, s=0.4, rng=rng), Wt_c=rnd(2 * C, E, s=0.4, rng=rng))
+    w.update(over)
+    return mtref.Model(E, H, A, V_, w, dual_source=True), w
+
+
+def second_source(B, S2=5, seed=81):
+    rng = np.random.default_rng(seed)
+    lens2 = rng.integers(1, S2 + 1, size=B)
+    ctx2 = rnd(B, S2, 2 * H_, rng=rng)
+    mask2 = (np.arange(S2)[None] < lens2[:, None]).astype(np.float32)
+    return ctx2, mask2, lens2
+
+
+def test_dual_step_with_silent_second_context_equals_single_source():
+    """Zero rows for the second context in W2 and Wt_c: the dual step must give the
+    single-source step exactly (the second attention then feeds nothing)."""
+    H, E = H_, E_
+    C = 2 * H
+    _, w1 = tiny_model(seed=82)
+    dual, wd = dual_model(seed=82, W2=np.concatenate([w1["W2"], np.zeros((C, 3 * H), np.float32)]),
+                          Wt_c=np.concatenate([w1["Wt_c"], np.zeros((C, E), np.float32)]))
+    single = mtref.Model(E, H, A_, V_, w1)
+    ctx, mask, lens, tok, src, state = tiny_batch(seed=83)
+    ctx2, mask2, _ = second_source(ctx.shape[0])
+    P, _ = single.precompute(ctx, mask)
+    P2 = dual.keys2(ctx2, mask2)
+    a = dual.step(2, tok, src, state, ctx, P, mask, src2=(ctx2, P2, mask2))
+    b = single.step(2, tok, src, state, ctx, P, mask)
+    assert np.array_equal(a["state"], b["state"]) and np.array_equal(a["logp"], b["logp"])
+
+
+def test_dual_zero_va2_gives_masked_mean_of_second_source():
+    dual, w = dual_model(seed=84, va2=np.zeros(A_, np.float32))
+    ctx, mask, lens, tok, src, state = tiny_batch(seed=85)
+    ctx2, mask2, lens2 = second_source(ctx.shape[0], seed=86)
+    P, _ = dual.precompute(ctx, mask)
+    out = dual.step(2, tok, src, state, ctx, P, mask, taps=True, src2=(ctx2, dual.keys2(ctx2, mask2), mask2))
+    C = 2 * H_
+    for m in range(tok.size):
+        b = m // 2
+        want = ctx2[b, :lens2[b]].astype(np.float64).mean(0)
+        assert np.max(np.abs(out["c"][m, C:] - want)) <= 1e-6
+
+
+def test_dual_step_equals_torch_reexpression():
+    dual, w = dual_model(seed=87)
+    ctx, mask, lens, tok, src, state = tiny_batch(seed=88)
+    ctx2, mask2, _ = second_source(ctx.shape[0], seed=89)
+    P, _ = dual.precompute(ctx, mask)
+    P2 = dual.keys2(ctx2, mask2)
+    out = dual.step(2, tok, src, state, ctx, P, mask, src2=(ctx2, P2, mask2))
+    Tt = lambda v: torch.from_numpy(np.asarray(v, np.float64))
+
+    def att(q, Pb, Cb, mb, va):
+        e = torch.tanh(Tt(Pb) + q) @ Tt(va)
+        return torch.softmax(e.masked_fill(Tt(mb) == 0, -math.inf), 0) @ Tt(Cb)
+
+    for m in range(tok.size):
+        b = m // 2
+        x = w["emb"][tok[m]]
+        s1 = torch_gru(x, state[src[m]], w["W1"], w["U1"], w["b1"])
+        c1 = att(Tt(s1) @ Tt(w["Wa"]), P[b], ctx[b], mask[b], w["va"])
+        c2 = att(Tt(s1) @ Tt(w["Wa2"]), (Tt(ctx2[b]) @ Tt(w["Ua2"]) + Tt(w["ba2"])).numpy(), ctx2[b], mask2[b], w["va2"])
+        c = torch.cat([c1, c2])
+        s = torch_gru(c.numpy(), s1, w["W2"], w["U2"], w["b2"])
+        t = torch.tanh(Tt(s) @ Tt(w["Wt_s"]) + Tt(x) @ Tt(w["Wt_y"]) + c @ Tt(w["Wt_c"]) + Tt(w["bt"]))
+        lp = torch.log_softmax(t @ Tt(w["Wo"]) + Tt(w["bo"]), 0)
+        assert np.max(np.abs(out["state"][m] - s)) <= 1e-6
+        assert np.max(np.abs(out["logp"][m] - lp.numpy())) <= 1e-5
