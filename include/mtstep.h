@@ -89,6 +89,7 @@ typedef struct {
   float ln_eps;
   int32_t dec_transitions;
   int32_t src_V;  /* source vocabulary of the encoder (mt_encode); 0: no encoder */
+  int32_t dual_source;  /* 1: a second source with its own attention (mt_decoder_step_dual) */
 } mt_config;
 
 /* Model parameters: HOST pointers to fp32, row-major logical [in x out]
@@ -102,7 +103,9 @@ typedef struct {
  *   transition blocks (read only if dec_transitions = T > 0), stacked by
  *   block: Ut[T,H,3H] btr[T,3H], and with layer_norm gtu/betu[T,3H];
  *   encoder (read only if src_V > 0): semb[src_V,E], forward Wef[E,3H]
- *   Uef[H,3H] bef[3H], backward Web[E,3H] Ueb[H,3H] beb[3H]. */
+ *   Uef[H,3H] bef[3H], backward Web[E,3H] Ueb[H,3H] beb[3H];
+ *   second source (read only if dual_source): Ua2[C,A] ba2[A] Wa2[H,A] va2[A],
+ *   and W2 [2C,3H], Wt_c [2C,E] then take the two contexts side by side. */
 typedef struct {
   const float *emb;
   const float *W1, *U1, *b1;
@@ -114,12 +117,14 @@ typedef struct {
   const float *g1a, *be1a, *g1u, *be1u, *g2a, *be2a, *g2u, *be2u, *gt, *bet;
   const float *Ut, *btr, *gtu, *betu;
   const float *semb, *Wef, *Uef, *bef, *Web, *Ueb, *beb;
+  const float *Ua2, *ba2, *Wa2, *va2;
 } mt_weights;
 
 typedef struct mt_model mt_model; /* opaque, library-owned */
 
 /* Optional per-stage outputs of mt_decoder_step, each fp32 [B*K, n] or NULL:
- * s1 (n = H), c (n = 2H), t (n = E).  For stage-level checks. */
+ * s1 (n = H), c (n = 2H; 4H for dual-source models, both contexts), t (n = E).  For
+ * stage-level checks. */
 typedef struct {
   float *s1;
   float *c;
@@ -190,6 +195,23 @@ mt_status mt_decoder_step(mt_model *model, int B, int K, int S, const int32_t *p
                           const void *ctx, const void *pctx, const float *mask, float *state_out,
                           float *logp_out, float *attn_out, const mt_taps *taps, void *ws,
                           size_t ws_bytes, void *stream);
+
+/* Dual-source models (the dual-attention post-editing models of Section 3.2: two encoders,
+ * a decoder attending to both).  mt_precompute_keys2: the second source's attention keys
+ * pctx2_out [B,S2,A] = ctx2 Ua2 + ba2 at its valid positions (ctx2 [B,S2,2H] and mask2
+ * [B,S2] as for mt_precompute_ctx; workspace as mt_precompute_ctx needs for S2).
+ * mt_decoder_step_dual: mt_decoder_step plus the second source: s1 also queries it (q2 =
+ * s1 Wa2, va2, masked softmax over its S2 positions), and GRU 2 and the readout take the
+ * two contexts side by side.  attn_out holds the first source's weights.  The start state
+ * comes from the first source (mt_precompute_ctx).  mt_decoder_step on a dual-source
+ * model (and these calls on another) return MT_ERR_STATE. */
+mt_status mt_precompute_keys2(mt_model *model, int B, int S2, const void *ctx2, const float *mask2,
+                              void *pctx2_out, void *ws, size_t ws_bytes, void *stream);
+mt_status mt_decoder_step_dual(mt_model *model, int B, int K, int S, const int32_t *prev_tok,
+                               const int32_t *src_row, int n_state_rows, const float *state_in,
+                               const void *ctx, const void *pctx, const float *mask, int S2, const void *ctx2,
+                               const void *pctx2, const float *mask2, float *state_out, float *logp_out,
+                               float *attn_out, const mt_taps *taps, void *ws, size_t ws_bytes, void *stream);
 
 /* Beam selection (Section 2.2: next hypotheses from the decoder state;
  * Section 2.3: batched beam search).  For sentence b the candidates are

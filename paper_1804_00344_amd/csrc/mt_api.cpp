@@ -74,6 +74,8 @@ struct mt_model {
   float *embx;    // [V][3H+E] fp32: emb [W1 | Wt_y] + [b1 | 0], the token side of GRU 1 and the readout
   float *bias1x, *bias3, *ba, *bi, *bt, *va;
   float *ln[10];  // g1a be1a g1u be1u g2a be2a g2u be2u gt bet
+  Packed wp2;                     // dual-source models: second source's key projection Ua2
+  float *ba2 = nullptr, *va2 = nullptr;
   Packed wenc_x, wenc_f, wenc_b;  // encoder: [Wef | Web], Uef, Ueb
   float *bias_enc = nullptr;      // [bef | beb]
   float *semb = nullptr;          // [src_V][E] fp32 source embeddings
@@ -110,6 +112,7 @@ mt_status check_cfg(const mt_config *c) {
   if (c->tied_output != 0 && c->tied_output != 1) return fail(MT_ERR_ARG, "tied_output must be 0 or 1");
   if (c->gemm_dtype != MT_F32 && c->gemm_dtype != MT_BF16)
     return fail(MT_ERR_DTYPE, "gemm_dtype=%d: need MT_F32 or MT_BF16", c->gemm_dtype);
+  if (c->dual_source != 0 && c->dual_source != 1) return fail(MT_ERR_ARG, "dual_source must be 0 or 1");
   if (c->src_V < 0 || c->src_V > (1 << 24)) return fail(MT_ERR_SHAPE, "src_V=%d: need 0 <= src_V <= 2^24", c->src_V);
   if (c->dec_transitions < 0 || c->dec_transitions > kMaxTransitions)
     return fail(MT_ERR_SHAPE, "dec_transitions=%d: need 0..%d", c->dec_transitions, kMaxTransitions);
@@ -233,8 +236,9 @@ WsLayout ws_layout(const mt_model *m, int B, int K) {
   };
   L.gh = take(M * 3 * H * 4);
   L.s1 = take(M * H * 4);
-  L.g2 = take(M * (A + 3 * H) * 4);
-  L.c = take(M * C * 4);
+  const size_t nsrc = m->cfg.dual_source ? 2 : 1;  // attention queries / contexts per row
+  L.g2 = take(M * (nsrc * A + 3 * H) * 4);
+  L.c = take(M * nsrc * C * 4);
   L.g3 = take(M * (3 * H + E) * 4);
   L.g4 = take(M * E * 4);
   L.t = take(M * E * m->esize);
@@ -260,7 +264,7 @@ WsLayout ws_layout(const mt_model *m, int B, int K) {
   // bf16 copies of s1, the context and the new state: the A operands of the bf16 products
   const size_t h16 = m->bf16 ? 2 : 0;
   L.s1h = take(M * H * h16);
-  L.ch = take(M * C * h16);
+  L.ch = take(M * nsrc * C * h16);
   L.sth = take(M * H * h16);
   // transition blocks alternate between state_out and this buffer
   L.sx = take(c.dec_transitions > 0 ? M * H * 4 : 0);
@@ -370,6 +374,12 @@ mt_status mt_load_weights(const mt_config *cfg, const mt_weights *w, mt_model **
   if (c.layer_norm)
     for (int i = 0; i < 10; ++i)
       if (!lnp[i]) return fail(MT_ERR_ARG, "layer-norm parameter %d is NULL (layer_norm = 1)", i);
+  if (c.dual_source) {
+    const float *dw[] = {w->Ua2, w->ba2, w->Wa2, w->va2};
+    const char *dn[] = {"Ua2", "ba2", "Wa2", "va2"};
+    for (int i = 0; i < 4; ++i)
+      if (!dw[i]) return fail(MT_ERR_ARG, "second-source weight %s is NULL (dual_source = 1)", dn[i]);
+  }
   if (c.src_V > 0) {
     const float *ew[] = {w->semb, w->Wef, w->Uef, w->bef, w->Web, w->Ueb, w->beb};
     const char *en[] = {"semb", "Wef", "Uef", "bef", "Web", "Ueb", "beb"};
@@ -403,8 +413,17 @@ mt_status mt_load_weights(const mt_config *cfg, const mt_weights *w, mt_model **
   auto run = [&]() -> mt_status {
     CHECK(upload_packed(m, {{w->W1, 3 * H}, {w->Wt_y, E}}, E, V, &m->w1x));
     CHECK(upload_packed(m, {{w->U1, 3 * H}}, H, kRefRows, &m->w1h));
-    CHECK(upload_packed(m, {{w->Wa, A}, {w->U2, 3 * H}}, H, kRefRows, &m->w2));
-    CHECK(upload_packed(m, {{w->W2, 3 * H}, {w->Wt_c, E}}, C, kRefRows, &m->w3));
+    // dual-source models: s1 [Wa | Wa2 | U2], and the context product takes [c1 ; c2] (2C rows)
+    if (c.dual_source)
+      CHECK(upload_packed(m, {{w->Wa, A}, {w->Wa2, A}, {w->U2, 3 * H}}, H, kRefRows, &m->w2));
+    else
+      CHECK(upload_packed(m, {{w->Wa, A}, {w->U2, 3 * H}}, H, kRefRows, &m->w2));
+    CHECK(upload_packed(m, {{w->W2, 3 * H}, {w->Wt_c, E}}, c.dual_source ? 2 * C : C, kRefRows, &m->w3));
+    if (c.dual_source) {
+      CHECK(upload_packed(m, {{w->Ua2, A}}, C, kRefCtxRows, &m->wp2));
+      CHECK(upload_vec(m, cat({{w->ba2, A}}), &m->ba2));
+      CHECK(upload_vec(m, cat({{w->va2, A}}), &m->va2));
+    }
     CHECK(upload_packed(m, {{w->Wt_s, E}}, H, kRefRows, &m->w4));
     CHECK(upload_packed(m, {{w->Ua, A}}, C, kRefCtxRows, &m->wp));
     CHECK(upload_packed(m, {{w->Wi, H}}, C, kRefSentences, &m->ws0));
@@ -673,13 +692,12 @@ mt_status mt_precompute_ctx(mt_model *model, int B, int S, const void *ctx, cons
   return MT_OK;
 }
 
-mt_status mt_decoder_step(mt_model *model, int B, int K, int S, const int32_t *prev_tok,
-                          const int32_t *src_row, int n_state_rows, const float *state_in,
-                          const void *ctx, const void *pctx, const float *mask, float *state_out,
-                          float *logp_out, float *attn_out, const mt_taps *taps, void *ws,
-                          size_t ws_bytes, void *stream) {
-  g_err[0] = 0;
-  if (!valid_model(model)) return fail(MT_ERR_ARG, "invalid model handle");
+// The step, with an optional second source (S2 > 0: dual-source models)
+static mt_status decoder_step_impl(mt_model *model, int B, int K, int S, const int32_t *prev_tok,
+                                   const int32_t *src_row, int n_state_rows, const float *state_in,
+                                   const void *ctx, const void *pctx, const float *mask, int S2, const void *ctx2,
+                                   const void *pctx2, const float *mask2, float *state_out, float *logp_out,
+                                   float *attn_out, const mt_taps *taps, void *ws, size_t ws_bytes, void *stream) {
   const mt_config &c = model->cfg;
   if (B < 1 || K < 1 || K > c.k_max || K > c.V || S < 1 || S > 1024)
     return fail(MT_ERR_SHAPE, "B=%d K=%d S=%d: need B >= 1, 1 <= K <= k_max=%d, 1 <= S <= 1024", B, K, S, c.k_max);
@@ -702,6 +720,8 @@ mt_status mt_decoder_step(mt_model *model, int B, int K, int S, const int32_t *p
     if (taps->t) CHECK(check_dev_ptr(taps->t, "taps->t", 4));
   }
   const int M = B * K, E = c.E, H = c.H, A = c.A, V = c.V, C = model->C;
+  const int nsrc = S2 > 0 ? 2 : 1;
+  const int Cc = nsrc * C, ldg2 = nsrc * A + 3 * H;  // context width, s1-product width
   {
     const char *si = (const char *)state_in, *so = (const char *)state_out;
     if (si < so + (size_t)M * H * 4 && so < si + (size_t)n_state_rows * H * 4)
@@ -737,18 +757,24 @@ mt_status mt_decoder_step(mt_model *model, int B, int K, int S, const int32_t *p
   GemmProblem p2{};
   p2.A = bf ? (const void *)(W + L.s1h) : (const void *)s1; p2.a_rows = M; p2.lda = H; p2.a_bf16 = bf;
   p2.Bp = model->w2.p; p2.ldb = model->w2.ldb; p2.wblk = model->w2.blk;
-  p2.out = g2; p2.ldc = A + 3 * H; p2.M = M; p2.N = A + 3 * H; p2.K = H;
+  p2.out = g2; p2.ldc = ldg2; p2.M = M; p2.N = ldg2; p2.K = H;
   LAUNCH(MT_KERNEL_GEMM_S1, launch_gemm(bf, &p2, 1, EPI_STORE, st));
-  // bf16 models need the context only in bf16 (fp32 too when it is tapped)
+  // bf16 models need the context only in bf16 (fp32 too when it is tapped); a second source's
+  // context goes to the right half of the [M][2C] rows
   float *cc32 = (!bf || (taps && taps->c)) ? cc : nullptr;
-  LAUNCH(MT_KERNEL_ATTENTION, launch_attention(B, K, S, A, C, pctx, ctx, bf, mask, g2, A + 3 * H, model->va, cc32, C,
-                                               bf ? (bf16 *)(W + L.ch) : nullptr, attn_out, st));
-  if (taps && taps->c) HIP_TRY(hipMemcpyAsync(taps->c, cc, (size_t)M * C * 4, hipMemcpyDeviceToDevice, st));
+  bf16 *ch = bf ? (bf16 *)(W + L.ch) : nullptr;
+  LAUNCH(MT_KERNEL_ATTENTION, launch_attention(B, K, S, A, C, pctx, ctx, bf, mask, g2, ldg2, model->va, cc32, Cc,
+                                               ch, Cc, attn_out, st));
+  if (S2 > 0)
+    LAUNCH(MT_KERNEL_ATTENTION, launch_attention(B, K, S2, A, C, pctx2, ctx2, bf, mask2, g2 + A, ldg2, model->va2,
+                                                 cc32 ? cc32 + C : nullptr, Cc, ch ? ch + C : nullptr, Cc, nullptr,
+                                                 st));
+  if (taps && taps->c) HIP_TRY(hipMemcpyAsync(taps->c, cc, (size_t)M * Cc * 4, hipMemcpyDeviceToDevice, st));
   // c [W2 | Wt_c] + [b2 | 0]
   GemmProblem p3{};
-  p3.A = bf ? (const void *)(W + L.ch) : (const void *)cc; p3.a_rows = M; p3.lda = C; p3.a_bf16 = bf;
+  p3.A = bf ? (const void *)ch : (const void *)cc; p3.a_rows = M; p3.lda = Cc; p3.a_bf16 = bf;
   p3.Bp = model->w3.p; p3.ldb = model->w3.ldb; p3.wblk = model->w3.blk; p3.bias = model->bias3;
-  p3.out = g3; p3.ldc = 3 * H + E; p3.M = M; p3.N = 3 * H + E; p3.K = C;
+  p3.out = g3; p3.ldc = 3 * H + E; p3.M = M; p3.N = 3 * H + E; p3.K = Cc;
   LAUNCH(MT_KERNEL_GEMM_CTX, launch_gemm(bf, &p3, 1, EPI_STORE, st));
   // GRU 2, then the transition blocks of a deep-transition cell (recurrent product s Ut_j,
   // then the cell with the bias row as its input path), alternating between state_out and a
@@ -757,7 +783,7 @@ mt_status mt_decoder_step(mt_model *model, int B, int K, int S, const int32_t *p
   float *sx = (float *)(W + L.sx);
   auto dest = [&](int i) { return ((T - i) % 2 == 0) ? state_out : sx; };  // output of block i (0: GRU 2)
   LAUNCH(MT_KERNEL_GRU_CELL,
-         launch_gru_cell(M, H, g3, 3 * H + E, nullptr, M, g2 + A, A + 3 * H, s1, nullptr, M, model->err,
+         launch_gru_cell(M, H, g3, 3 * H + E, nullptr, M, g2 + nsrc * A, ldg2, s1, nullptr, M, model->err,
                          LNon ? ln[4] : nullptr, ln[5], ln[6], ln[7], eps, dest(0), H,
                          bf ? (bf16 *)(W + L.sth) : nullptr, nullptr, st));
   for (int j = 0; j < T; ++j) {
@@ -803,6 +829,62 @@ mt_status mt_decoder_step(mt_model *model, int B, int K, int S, const int32_t *p
   model->last_B = B;
   model->last_K = K;
   model->last_ws = ws;
+  return MT_OK;
+}
+
+mt_status mt_decoder_step(mt_model *model, int B, int K, int S, const int32_t *prev_tok,
+                          const int32_t *src_row, int n_state_rows, const float *state_in,
+                          const void *ctx, const void *pctx, const float *mask, float *state_out,
+                          float *logp_out, float *attn_out, const mt_taps *taps, void *ws,
+                          size_t ws_bytes, void *stream) {
+  g_err[0] = 0;
+  if (!valid_model(model)) return fail(MT_ERR_ARG, "invalid model handle");
+  if (model->cfg.dual_source) return fail(MT_ERR_STATE, "dual-source model: use mt_decoder_step_dual");
+  return decoder_step_impl(model, B, K, S, prev_tok, src_row, n_state_rows, state_in, ctx, pctx, mask, 0, nullptr,
+                           nullptr, nullptr, state_out, logp_out, attn_out, taps, ws, ws_bytes, stream);
+}
+
+mt_status mt_decoder_step_dual(mt_model *model, int B, int K, int S, const int32_t *prev_tok,
+                               const int32_t *src_row, int n_state_rows, const float *state_in,
+                               const void *ctx, const void *pctx, const float *mask, int S2, const void *ctx2,
+                               const void *pctx2, const float *mask2, float *state_out, float *logp_out,
+                               float *attn_out, const mt_taps *taps, void *ws, size_t ws_bytes, void *stream) {
+  g_err[0] = 0;
+  if (!valid_model(model)) return fail(MT_ERR_ARG, "invalid model handle");
+  if (!model->cfg.dual_source) return fail(MT_ERR_STATE, "not a dual-source model (dual_source = 0)");
+  if (S2 < 1 || S2 > 1024) return fail(MT_ERR_SHAPE, "S2=%d: need 1 <= S2 <= 1024", S2);
+  if ((long long)B * S2 > (1 << 24)) return fail(MT_ERR_SHAPE, "B*S2 exceeds 2^24");
+  CHECK(check_dev_ptr(ctx2, "ctx2"));
+  CHECK(check_dev_ptr(pctx2, "pctx2"));
+  CHECK(check_dev_ptr(mask2, "mask2", 4));
+  return decoder_step_impl(model, B, K, S, prev_tok, src_row, n_state_rows, state_in, ctx, pctx, mask, S2, ctx2,
+                           pctx2, mask2, state_out, logp_out, attn_out, taps, ws, ws_bytes, stream);
+}
+
+mt_status mt_precompute_keys2(mt_model *model, int B, int S2, const void *ctx2, const float *mask2,
+                              void *pctx2_out, void *ws, size_t ws_bytes, void *stream) {
+  g_err[0] = 0;
+  if (!valid_model(model)) return fail(MT_ERR_ARG, "invalid model handle");
+  if (!model->cfg.dual_source) return fail(MT_ERR_STATE, "not a dual-source model (dual_source = 0)");
+  if (B < 1 || S2 < 1 || S2 > 1024) return fail(MT_ERR_SHAPE, "B=%d S2=%d: need B >= 1, 1 <= S2 <= 1024", B, S2);
+  if ((long long)B * S2 > (1 << 24)) return fail(MT_ERR_SHAPE, "B*S2 exceeds 2^24");
+  CHECK(check_dev_ptr(ctx2, "ctx2"));
+  CHECK(check_dev_ptr(mask2, "mask2", 4));
+  CHECK(check_dev_ptr(pctx2_out, "pctx2_out"));
+  CHECK(check_dev_ptr(ws, "ws", 256));
+  const size_t need = precompute_ws_bytes(model, B, S2);
+  if (ws_bytes < need) return fail(MT_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, need);
+  hipStream_t st = (hipStream_t)stream;
+  const int A = model->cfg.A, C = model->C;
+  int32_t *vrows = (int32_t *)((char *)ws + rup256((size_t)B * C * 4));
+  int *nvalid = (int *)((char *)vrows + rup256((size_t)B * S2 * 4));
+  LAUNCH(MT_KERNEL_PRECOMPUTE, launch_valid_rows(B * S2, mask2, vrows, nvalid, st));
+  GemmProblem p{};
+  p.A = ctx2; p.a_idx = vrows; p.a_rows = B * S2; p.lda = C; p.a_bf16 = model->bf16;
+  p.Bp = model->wp2.p; p.ldb = model->wp2.ldb; p.wblk = model->wp2.blk; p.bias = model->ba2;
+  p.out = pctx2_out; p.ldc = A; p.out_bf16 = model->bf16;
+  p.M = B * S2; p.N = A; p.K = C; p.m_dev = nvalid;
+  LAUNCH(MT_KERNEL_PRECOMPUTE, launch_gemm(model->bf16, &p, 1, EPI_SCATTER, st));
   return MT_OK;
 }
 

@@ -73,7 +73,7 @@ __global__ __launch_bounds__(kAT) void attention_kernel(int B, int K, int S, int
                                                         const float *__restrict__ q, int ldq,
                                                         const float *__restrict__ va,
                                                         float *__restrict__ ctx_out, int ldc,
-                                                        bf16 *__restrict__ ctx16,
+                                                        bf16 *__restrict__ ctx16, int ld16,
                                                         float *__restrict__ alpha_out) {
   constexpr int G = Gran<T>::N;
   constexpr int U = NC <= 2 ? 8 : NC == 4 ? 4 : 2;  // context positions in flight per thread
@@ -264,7 +264,7 @@ __global__ __launch_bounds__(kAT) void attention_kernel(int B, int K, int S, int
       bf16 h[G];
 #pragma unroll
       for (int e = 0; e < G; ++e) h[e] = to_bf16(c[p][e]);
-      __builtin_memcpy(ctx16 + (size_t)m * Cd + g * G, h, sizeof(h));
+      __builtin_memcpy(ctx16 + (size_t)m * ld16 + g * G, h, sizeof(h));
     }
   }
 }
@@ -274,11 +274,11 @@ static int bucket(int n) { return n <= 1 ? 1 : n <= 2 ? 2 : n <= 4 ? 4 : n <= 8 
 template <typename T, int NG>
 static void attn_go_c(int nc, int B, int K, int S, int A, int Cd, const T *P, const T *Cx, const float *mask,
                       const float *q, int ldq, const float *va, float *ctx_out, int ldc, bf16 *ctx16,
-                      float *alpha_out, hipStream_t st) {
+                      int ld16, float *alpha_out, hipStream_t st) {
   const int M = B * K;
 #define MT_AT(NC)                                                                                    \
   hipLaunchKernelGGL((attention_kernel<T, NG, NC>), dim3(M), dim3(kAT), 0, st, B, K, S, A, Cd, P, Cx, \
-                     mask, q, ldq, va, ctx_out, ldc, ctx16, alpha_out)
+                     mask, q, ldq, va, ctx_out, ldc, ctx16, ld16, alpha_out)
   if (nc <= 1) MT_AT(1);
   else if (nc <= 2) MT_AT(2);
   else if (nc <= 4) MT_AT(4);
@@ -289,11 +289,11 @@ static void attn_go_c(int nc, int B, int K, int S, int A, int Cd, const T *P, co
 template <typename T>
 static void attn_go(int B, int K, int S, int A, int Cd, const T *P, const T *Cx, const float *mask,
                     const float *q, int ldq, const float *va, float *ctx_out, int ldc, bf16 *ctx16,
-                    float *alpha_out, hipStream_t st) {
+                    int ld16, float *alpha_out, hipStream_t st) {
   constexpr int G = Gran<T>::N;
   const int ng = bucket((A / G + 63) / 64);
   const int nc = bucket((Cd / G + kAT - 1) / kAT);
-#define MT_AG(NG) attn_go_c<T, NG>(nc, B, K, S, A, Cd, P, Cx, mask, q, ldq, va, ctx_out, ldc, ctx16, alpha_out, st)
+#define MT_AG(NG) attn_go_c<T, NG>(nc, B, K, S, A, Cd, P, Cx, mask, q, ldq, va, ctx_out, ldc, ctx16, ld16, alpha_out, st)
   switch (ng) {
     case 1: MT_AG(1); break;
     case 2: MT_AG(2); break;
@@ -306,15 +306,15 @@ static void attn_go(int B, int K, int S, int A, int Cd, const T *P, const T *Cx,
 
 hipError_t launch_attention(int B, int K, int S, int A, int Cd, const void *P, const void *Cx,
                             int bf16_io, const float *mask, const float *q, int ldq,
-                            const float *va, float *ctx_out, int ldc, bf16 *ctx16, float *alpha_out,
+                            const float *va, float *ctx_out, int ldc, bf16 *ctx16, int ld16, float *alpha_out,
                             hipStream_t st) {
   if (B * K == 0) return hipSuccess;
   if (bf16_io)
     attn_go<bf16>(B, K, S, A, Cd, (const bf16 *)P, (const bf16 *)Cx, mask, q, ldq, va, ctx_out, ldc, ctx16,
-                  alpha_out, st);
+                  ld16, alpha_out, st);
   else
     attn_go<float>(B, K, S, A, Cd, (const float *)P, (const float *)Cx, mask, q, ldq, va, ctx_out, ldc, ctx16,
-                   alpha_out, st);
+                   ld16, alpha_out, st);
   return hipGetLastError();
 }
 

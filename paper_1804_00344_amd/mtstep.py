@@ -35,13 +35,13 @@ class mt_config(C.Structure):
     _fields_ = [("E", C.c_int32), ("H", C.c_int32), ("A", C.c_int32), ("V", C.c_int32),
                 ("layer_norm", C.c_int32), ("tied_output", C.c_int32), ("k_max", C.c_int32),
                 ("gemm_dtype", C.c_int32), ("ln_eps", C.c_float), ("dec_transitions", C.c_int32),
-                ("src_V", C.c_int32)]
+                ("src_V", C.c_int32), ("dual_source", C.c_int32)]
 
 
 WEIGHT_FIELDS = ["emb", "W1", "U1", "b1", "Ua", "ba", "Wa", "va", "W2", "U2", "b2", "Wt_s", "Wt_y",
                  "Wt_c", "bt", "Wo", "bo", "Wi", "bi", "g1a", "be1a", "g1u", "be1u", "g2a", "be2a",
                  "g2u", "be2u", "gt", "bet", "Ut", "btr", "gtu", "betu",
-                 "semb", "Wef", "Uef", "bef", "Web", "Ueb", "beb"]
+                 "semb", "Wef", "Uef", "bef", "Web", "Ueb", "beb", "Ua2", "ba2", "Wa2", "va2"]
 
 _fp = C.POINTER(C.c_float)
 
@@ -77,6 +77,10 @@ def lib() -> C.CDLL:
         L.mt_beam_topk.argtypes = [_vp, C.c_int, C.c_int, _vp, _vp, _vp, _vp, _vp, _vp, _vp, C.c_size_t, _vp]
         L.mt_device_errors.argtypes = [_vp, C.POINTER(C.c_int32)]
         L.mt_ensemble_logp.argtypes = [_vp, C.c_int, C.POINTER(_vp), C.POINTER(C.c_float), C.c_int, _vp, _vp]
+        L.mt_precompute_keys2.argtypes = [_vp, C.c_int, C.c_int, _vp, _vp, _vp, _vp, C.c_size_t, _vp]
+        L.mt_decoder_step_dual.argtypes = [_vp, C.c_int, C.c_int, C.c_int, _vp, _vp, C.c_int, _vp, _vp, _vp, _vp,
+                                           C.c_int, _vp, _vp, _vp, _vp, _vp, _vp, C.POINTER(mt_taps), _vp,
+                                           C.c_size_t, _vp]
         L.mt_encode_workspace_bytes.argtypes = [_vp, C.c_int, C.c_int]
         L.mt_encode_workspace_bytes.restype = C.c_size_t
         L.mt_encode.argtypes = [_vp, C.c_int, C.c_int, _vp, _vp, _vp, _vp, C.c_size_t, _vp]
@@ -85,7 +89,7 @@ def lib() -> C.CDLL:
         L.mt_profile_reset.argtypes = [_vp]
         L.mt_profile_query.argtypes = [_vp, C.c_int, C.POINTER(C.c_double), C.POINTER(C.c_int64)]
         for f in ("mt_load_weights", "mt_free", "mt_precompute_ctx", "mt_decoder_step", "mt_beam_topk",
-                  "mt_ensemble_logp", "mt_beam_finish", "mt_encode",
+                  "mt_ensemble_logp", "mt_beam_finish", "mt_encode", "mt_precompute_keys2", "mt_decoder_step_dual",
                   "mt_device_errors", "mt_profile_enable", "mt_profile_reset", "mt_profile_query"):
             getattr(L, f).restype = C.c_int
         _lib = L
@@ -118,9 +122,9 @@ def _stream(stream) -> Optional[int]:
 
 
 def make_config(E, H, A, V, *, layer_norm=False, tied_output=False, k_max=16, gemm="f32", ln_eps=1e-5,
-                transitions=0, src_V=0):
+                transitions=0, src_V=0, dual_source=False):
     return mt_config(E, H, A, V, int(layer_norm), int(tied_output), k_max,
-                     MT_BF16 if gemm == "bf16" else MT_F32, ln_eps, transitions, src_V)
+                     MT_BF16 if gemm == "bf16" else MT_F32, ln_eps, transitions, src_V, int(dual_source))
 
 
 class Model:
@@ -207,6 +211,25 @@ def mt_decoder_step(model: Model, B, K, S, prev_tok, src_row, n_state_rows, stat
                                  _ptr(state_in), _ptr(ctx), _ptr(pctx), _ptr(mask), _ptr(state_out),
                                  _ptr(logp_out), _ptr(attn_out), C.byref(tp) if tp is not None else None,
                                  _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def mt_decoder_step_dual(model: Model, B, K, S, prev_tok, src_row, n_state_rows, state_in, ctx, pctx, mask, S2,
+                         ctx2, pctx2, mask2, state_out, logp_out=None, attn_out=None, taps=None, ws=None,
+                         ws_bytes=None, stream=None):
+    ws_bytes = ws.numel() * ws.element_size() if ws_bytes is None else ws_bytes
+    tp = None
+    if taps:
+        tp = mt_taps(_ptr(taps.get("s1")), _ptr(taps.get("c")), _ptr(taps.get("t")))
+    _check(lib().mt_decoder_step_dual(model.handle, B, K, S, _ptr(prev_tok), _ptr(src_row), n_state_rows,
+                                      _ptr(state_in), _ptr(ctx), _ptr(pctx), _ptr(mask), S2, _ptr(ctx2), _ptr(pctx2),
+                                      _ptr(mask2), _ptr(state_out), _ptr(logp_out), _ptr(attn_out),
+                                      C.byref(tp) if tp is not None else None, _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def mt_precompute_keys2(model: Model, B, S2, ctx2, mask2, pctx2_out, ws, ws_bytes=None, stream=None):
+    ws_bytes = ws.numel() * ws.element_size() if ws_bytes is None else ws_bytes
+    _check(lib().mt_precompute_keys2(model.handle, B, S2, _ptr(ctx2), _ptr(mask2), _ptr(pctx2_out), _ptr(ws),
+                                     ws_bytes, _stream(stream)))
 
 
 def mt_beam_topk(model: Model, B, K, prev_score, logp, score_out, tok_out, bp_out, row_out=None, ws=None,

@@ -18,12 +18,15 @@ from . import mtstep as mt
 class Decoder:
     def __init__(self, E: int, H: int, A: int, V: int, weights: Dict[str, np.ndarray], *, gemm: str = "f32",
                  layer_norm: bool = False, tied_output: bool = False, k_max: int = 16, ln_eps: float = 1e-5,
-                 transitions: int = 0, src_V: int = 0, device: str = "cuda:0"):
+                 transitions: int = 0, src_V: int = 0, dual_source: bool = False, device: str = "cuda:0"):
         self.E, self.H, self.A, self.V, self.C = E, H, A, V, 2 * H
         self.gemm = gemm
         self.device = torch.device(device)
         self.cfg = mt.make_config(E, H, A, V, layer_norm=layer_norm, tied_output=tied_output, k_max=k_max,
-                                  gemm=gemm, ln_eps=ln_eps, transitions=transitions, src_V=src_V)
+                                  gemm=gemm, ln_eps=ln_eps, transitions=transitions, src_V=src_V,
+                                  dual_source=dual_source)
+        self.dual = bool(dual_source)
+        self.S2 = 0
         with torch.cuda.device(self.device):
             self.model = mt.mt_load_weights(self.cfg, weights)
         self.io_dtype = torch.bfloat16 if gemm == "bf16" else torch.float32
@@ -80,12 +83,33 @@ class Decoder:
     def encode(self, stream=None):
         mt.mt_encode(self.model, self.B, self.S, self.src_tok, self.mask, self.ctx, self.ews, stream=stream)
 
+    def set_second_source(self, ctx2: np.ndarray, mask2: np.ndarray):
+        """The second source of a dual-source model (after set_batch / set_source)."""
+        B, S2, Cd = ctx2.shape
+        assert self.dual and B == self.B and Cd == self.C and mask2.shape == (B, S2)
+        d = self.device
+        self.S2 = S2
+        self.ctx2 = torch.from_numpy(np.ascontiguousarray(ctx2, np.float32)).to(d).to(self.io_dtype).contiguous()
+        self.mask2 = torch.from_numpy(np.ascontiguousarray(mask2, np.float32)).to(d)
+        self.pctx2 = torch.empty((B, S2, self.A), dtype=self.io_dtype, device=d)
+        need = mt.mt_workspace_bytes(self.model, B, self.K, S2)
+        if need > self.ws.numel():
+            self.ws = torch.empty(need, dtype=torch.uint8, device=d)
+
     def precompute(self, stream=None):
         mt.mt_precompute_ctx(self.model, self.B, self.S, self.ctx, self.mask, self.pctx, self.s0, self.ws,
                              stream=stream)
+        if self.dual:
+            mt.mt_precompute_keys2(self.model, self.B, self.S2, self.ctx2, self.mask2, self.pctx2, self.ws,
+                                   stream=stream)
 
     def step(self, prev_tok, src_row, state_in, n_state_rows: int, state_out, *, logp=None, attn=None,
              taps=None, stream=None):
+        if self.dual:
+            mt.mt_decoder_step_dual(self.model, self.B, self.K, self.S, prev_tok, src_row, n_state_rows, state_in,
+                                    self.ctx, self.pctx, self.mask, self.S2, self.ctx2, self.pctx2, self.mask2,
+                                    state_out, logp_out=logp, attn_out=attn, taps=taps, ws=self.ws, stream=stream)
+            return
         mt.mt_decoder_step(self.model, self.B, self.K, self.S, prev_tok, src_row, n_state_rows, state_in, self.ctx,
                            self.pctx, self.mask, state_out, logp_out=logp, attn_out=attn, taps=taps, ws=self.ws,
                            stream=stream)

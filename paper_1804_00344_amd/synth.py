@@ -246,6 +246,29 @@ def mid_decode_inputs(p: Preset, salt: int = 0):
     return tok, src_row, state, score.reshape(M).astype(np.float32)
 
 
+DUAL_NAMES = ("Ua2", "ba2", "Wa2", "va2")
+
+
+def make_dual_weights(p: Preset) -> Dict[str, np.ndarray]:
+    """A second source's attention (Ua2, ba2, Wa2, va2) and the 2C-row W2 and Wt_c that take
+    the two contexts side by side; Glorot-uniform like the single-source ones."""
+    H, C, A, E = p.H, p.C, p.A, p.E
+    w = {"Ua2": glorot(rng_for(p, "Ua2"), C, A, (C, A)), "ba2": np.zeros(A, np.float32),
+         "Wa2": glorot(rng_for(p, "Wa2"), H, A, (H, A)), "va2": glorot(rng_for(p, "va2"), A, 1, (A,)),
+         "W2": _gate_matrix(p, "W2dual", 2 * C), "Wt_c": glorot(rng_for(p, "Wt_cdual"), 2 * C, E, (2 * C, E))}
+    if p.gemm == "bf16":
+        for k in ("Ua2", "Wa2", "W2", "Wt_c"):
+            w[k] = round_bf16(w[k])
+    return w
+
+
+def make_source2(p: Preset):
+    """A second source's encoder output stand-in (ctx2 [B,S2,C], mask2, lens2): lengths and
+    values drawn like the first source's, from their own streams."""
+    q = dataclasses.replace(p, index=p.index + 1000)
+    return make_source(q)
+
+
 ENCODER_NAMES = ("semb", "Wef", "Uef", "bef", "Web", "Ueb", "beb")
 
 

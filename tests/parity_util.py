@@ -18,8 +18,8 @@ TOL = {
 }
 
 
-def oracle_model(p: synth.Preset, w: Dict[str, np.ndarray]) -> mtref.Model:
-    return mtref.Model(p.E, p.H, p.A, p.V, w, layer_norm=p.layer_norm, transitions=p.transitions)
+def oracle_model(p: synth.Preset, w: Dict[str, np.ndarray], dual: bool = False) -> mtref.Model:
+    return mtref.Model(p.E, p.H, p.A, p.V, w, layer_norm=p.layer_norm, transitions=p.transitions, dual_source=dual)
 
 
 def sample_sentences(lens: np.ndarray, n: int) -> List[int]:
@@ -37,7 +37,8 @@ def sample_sentences(lens: np.ndarray, n: int) -> List[int]:
 
 
 def oracle_sentences(om: mtref.Model, K: int, sents: Sequence[int], ctx, mask, tok, src_row, state_in,
-                     want_logp=True, want_alpha=True, taps=True, threads: int = 8, start: bool = False):
+                     want_logp=True, want_alpha=True, taps=True, threads: int = 8, start: bool = False,
+                     src2=None):
     """Runs the oracle's precompute + one step on each sampled sentence separately.
 
     state_in rows for sentence b are the K rows b*K..b*K+K-1 (mid-decode), or with
@@ -54,7 +55,11 @@ def oracle_sentences(om: mtref.Model, K: int, sents: Sequence[int], ctx, mask, t
         else:
             st = state_in[rows]
             sr = (src_row[rows] - b * K).astype(np.int32)
-        out = om.step(K, tok[rows], sr, st, c, P, m, want_logp=want_logp, want_alpha=want_alpha, taps=taps)
+        s2 = None
+        if src2 is not None:  # dual-source models: (ctx2, mask2) of the batch
+            c2, m2 = src2[0][b:b + 1], src2[1][b:b + 1]
+            s2 = (c2, om.keys2(c2, m2), m2)
+        out = om.step(K, tok[rows], sr, st, c, P, m, want_logp=want_logp, want_alpha=want_alpha, taps=taps, src2=s2)
         out["P"], out["s0"] = P, s0
         return b, out
 

@@ -592,3 +592,40 @@ def test_encoder_parity(name, src_V, n_sent):
         gpu = run_step(dec, p, tok, srow, T(state), p.M)
         orc = oracle_sentences(oracle_model(p, w), p.K, sents, ctx_o, mask, tok, srow, state)
         compare_rows(p, gpu, orc, sents, TOL[p.gemm], name + "_encoded")
+
+
+# ------------------------------------------------------------------------------------------
+# dual-source steps: a second source with its own attention; GRU 2 and the readout take both
+# contexts
+# ------------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name,n_sent", [("tiny_f32", 99), ("tiny_bf16_ln", 6), ("nematus_f32", 3),
+                                         ("nematus_bf16_ln", 3)])
+def test_dual_source_step_parity(name, n_sent):
+    p = synth.PRESETS[name]
+    log(f"\n[dual] {name}")
+    w = {**synth.make_weights(p, peaked_bias=True), **synth.make_dual_weights(p)}
+    ctx, mask, lens = synth.make_source(p)
+    ctx2, mask2, _ = synth.make_source2(p)
+    dec = Decoder(p.E, p.H, p.A, p.V, w, gemm=p.gemm, layer_norm=p.layer_norm, k_max=max(p.K, 1), dual_source=True)
+    dec.set_batch(ctx, mask, p.K)
+    dec.set_second_source(ctx2, mask2)
+    dec.precompute()
+    tok, src, state, score = synth.mid_decode_inputs(p, salt=7)
+    gpu = run_step(dec, p, tok, src, T(state), p.M, taps=False)
+    sc, tk, bp, rw = [x.cpu().numpy() for x in dec.topk(T(score), None)]
+    torch.cuda.synchronize()
+    assert mt.mt_device_errors(dec.model) == 0
+    sents = sample_sentences(lens, n_sent)
+    orc = oracle_sentences(oracle_model(p, w, dual=True), p.K, sents, ctx, mask, tok, src, state, taps=False,
+                           src2=(ctx2, mask2))
+    tol = TOL[p.gemm]
+    compare_rows(p, gpu, orc, sents, tol, name + "_dual")
+    for b in sents:
+        rows = slice(b * p.K, (b + 1) * p.K)
+        topk_gap_check(p.K, score[rows], orc[b]["logp"], sc[rows], tk[rows], bp[rows], tol["logp"])
+        assert np.array_equal(rw[rows], b * p.K + bp[rows])
+    # a shallow call on a dual-source model is refused
+    with pytest.raises(mt.MtError):
+        mt.mt_decoder_step(dec.model, p.B, p.K, dec.S, T(tok), T(src), p.M, T(state), dec.ctx, dec.pctx, dec.mask,
+                           torch.empty((p.M, p.H), device=DEV), ws=dec.ws)
