@@ -42,7 +42,7 @@ def source_hash(path):
     return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
 
 
-def cpu_baseline(members, ctx, mask, budget_s=15.0):
+def cpu_baseline(members, ctx, mask, budget_s=15.0, src2=None):
     """The oracle (single-threaded C, double accumulation) on whole sentences of the same
     workload: one precompute + decoder step per member, their combination (ensembles) and
     one top-K per sentence, scaled to full-batch steps/s with the precompute amortised over
@@ -52,8 +52,8 @@ def cpu_baseline(members, ctx, mask, budget_s=15.0):
     from paper_1804_00344_amd import synth
 
     p = members[0][0]
-    oms = [mtref.Model(q.E, q.H, q.A, q.V, wq, layer_norm=q.layer_norm, transitions=q.transitions)
-           for q, wq in members]
+    oms = [mtref.Model(q.E, q.H, q.A, q.V, wq, layer_norm=q.layer_norm, transitions=q.transitions,
+                       dual_source=src2 is not None) for q, wq in members]
     ew = [1.0 / len(oms)] * len(oms)
     tok, src, state, score = synth.mid_decode_inputs(p, salt=11)
     t_pre = t_step = 0.0
@@ -64,9 +64,13 @@ def cpu_baseline(members, ctx, mask, budget_s=15.0):
         rows = slice(b * p.K, (b + 1) * p.K)
         t0 = time.perf_counter()
         Ps = [om.precompute(ctx[b:b + 1], mask[b:b + 1])[0] for om in oms]
+        s2 = None
+        if src2 is not None:
+            c2, m2 = src2[0][b:b + 1], src2[1][b:b + 1]
+            s2 = (c2, oms[0].keys2(c2, m2), m2)
         t1 = time.perf_counter()
         lps = [om.step(p.K, tok[rows], (src[rows] - b * p.K).astype(np.int32), state[rows], ctx[b:b + 1], P,
-                       mask[b:b + 1], want_alpha=False)["logp"] for om, P in zip(oms, Ps)]
+                       mask[b:b + 1], want_alpha=False, src2=s2)["logp"] for om, P in zip(oms, Ps)]
         lp = lps[0] if len(lps) == 1 else mtref.ensemble_logp(lps, ew)
         mtref.topk(p.K, score[rows], lp)
         t2 = time.perf_counter()
@@ -95,6 +99,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--ensemble", type=int, default=1,
                     help="members decoding one beam (seeded weights per member, equal weights)")
+    ap.add_argument("--dual", action="store_true",
+                    help="dual-source model: a second source (seeded like the first) with its own attention")
     ap.add_argument("--encode", type=int, default=0,
                     help="also time the encoder (mt_encode) over the batch with a source vocabulary of this size")
     ap.add_argument("--translate", type=int, default=0,
@@ -121,8 +127,17 @@ def main():
     log(f"[bench] preset {p.name}: B={p.B} K={p.K} E={p.E} H={p.H} A={p.A} V={p.V} gemm={p.gemm} ln={p.layer_norm}")
     w = synth.make_weights(p)
     ctx, mask, lens = synth.make_source(p)
-    dec = Decoder.from_preset(p, w)
-    dec.set_batch(ctx, mask, p.K)
+    if args.dual:
+        w = {**w, **synth.make_dual_weights(p)}
+        dec = Decoder(p.E, p.H, p.A, p.V, w, gemm=p.gemm, layer_norm=p.layer_norm, k_max=max(p.K, 1),
+                      transitions=p.transitions, dual_source=True)
+        dec.set_batch(ctx, mask, p.K)
+        ctx2, mask2, lens2 = synth.make_source2(p)
+        dec.set_second_source(ctx2, mask2)
+        cell = f"dual-source {cell}"
+    else:
+        dec = Decoder.from_preset(p, w)
+        dec.set_batch(ctx, mask, p.K)
     tok0, src0, score0 = synth.start_beam(p)
     stream = torch.cuda.current_stream()
     NE = args.ensemble
@@ -278,7 +293,8 @@ def main():
         }
     if not args.no_cpu_baseline:
         log("[bench] cpu baseline (oracle)")
-        rec["cpu_baseline"] = cpu_baseline(members, ctx, mask, args.cpu_budget)
+        rec["cpu_baseline"] = cpu_baseline(members, ctx, mask, args.cpu_budget,
+                                           src2=(ctx2, mask2) if args.dual else None)
     print(json.dumps(rec), flush=True)
 
 
