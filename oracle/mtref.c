@@ -347,8 +347,18 @@ int mtref_step_dual(const mtref_dims *d, const mtref_weights *w, int B, int K, i
 int mtref_encode(int E, int H, int Vs, int B, int S, const int32_t *src_tok, const float *mask,
                  const float *semb, const float *Wf, const float *Uf, const float *bf,
                  const float *Wb, const float *Ub, const float *bb, float *ctx_out) {
+  return mtref_encode_deep(E, H, Vs, B, S, src_tok, mask, semb, Wf, Uf, bf, Wb, Ub, bb, 0, NULL, NULL, NULL, NULL,
+                           ctx_out);
+}
+
+/* Deep-transition encoder cell (Section 3.1.1, four GRU blocks per encoder cell): the input
+ * block, then T blocks without external input, each output stored in fp32. */
+int mtref_encode_deep(int E, int H, int Vs, int B, int S, const int32_t *src_tok, const float *mask,
+                      const float *semb, const float *Wf, const float *Uf, const float *bf,
+                      const float *Wb, const float *Ub, const float *bb, int T, const float *Utf,
+                      const float *btf, const float *Utb, const float *btb, float *ctx_out) {
   if (E < 1 || H < 1 || Vs < 1 || B < 0 || S < 1 || !src_tok || !mask || !semb || !Wf || !Uf || !bf ||
-      !Wb || !Ub || !bb || !ctx_out)
+      !Wb || !Ub || !bb || !ctx_out || T < 0 || (T > 0 && (!Utf || !btf || !Utb || !btb)))
     return -1;
   for (long i = 0; i < (long)B * S; ++i)
     if (src_tok[i] < 0 || src_tok[i] >= Vs) return -2;
@@ -367,6 +377,12 @@ int mtref_encode(int E, int H, int Vs, int B, int S, const int32_t *src_tok, con
           mtref_gru(E, H, x, h, dir == 0 ? Wf : Wb, dir == 0 ? Uf : Ub, dir == 0 ? bf : bb, NULL, NULL, NULL,
                     NULL, 0.0, hn);
           round_store(H, hn, out, h);
+          for (int j = 0; j < T; ++j) {
+            const float *U = (dir == 0 ? Utf : Utb) + (size_t)j * H * 3 * H;
+            const float *bt = (dir == 0 ? btf : btb) + (size_t)j * 3 * H;
+            mtref_gru_transition(H, h, U, bt, NULL, NULL, 0.0, hn);
+            round_store(H, hn, out, h);
+          }
         } else {
           for (int j = 0; j < H; ++j) out[j] = (float)h[j];
         }

@@ -116,6 +116,15 @@ int mtref_encode(int E, int H, int Vs, int B, int S, const int32_t *src_tok, con
                  const float *semb, const float *Wf, const float *Uf, const float *bf,
                  const float *Wb, const float *Ub, const float *bb, float *ctx_out);
 
+/* The same with a deep-transition cell per direction (Section 3.1.1: the deep model's encoder
+ * cell has four GRU blocks): after the input block, T recurrent-only transition blocks
+ * (mtref_gru_transition, no layer norm) with stacked Utf/btf (forward) and Utb/btb
+ * (backward), [T,H,3H] and [T,3H]; a padded position carries the state over all blocks. */
+int mtref_encode_deep(int E, int H, int Vs, int B, int S, const int32_t *src_tok, const float *mask,
+                      const float *semb, const float *Wf, const float *Uf, const float *bf,
+                      const float *Wb, const float *Ub, const float *bb, int T, const float *Utf,
+                      const float *btf, const float *Utb, const float *btb, float *ctx_out);
+
 /* Attention keys of the second source: P2 = ctx2 Ua2 + ba2 at valid positions, 0 elsewhere. */
 int mtref_keys2(const mtref_dims *d, const mtref_weights *w, int B, int S, const float *ctx, const float *mask,
                 float *P_out);

@@ -915,3 +915,30 @@ def test_dual_step_equals_torch_reexpression():
         lp = torch.log_softmax(t @ Tt(w["Wo"]) + Tt(w["bo"]), 0)
         assert np.max(np.abs(out["state"][m] - s)) <= 1e-6
         assert np.max(np.abs(out["logp"][m] - lp.numpy())) <= 1e-5
+
+
+def test_deep_encoder_copying_transitions_equal_shallow_and_torch_per_block():
+    """Transition blocks that copy their state (b_z = +40) leave the shallow encoder's
+    context; general ones equal torch's GRU cell with a zero input applied per position
+    after the input block (one direction, unpadded)."""
+    E, H, Vs, B, S, T = 6, 5, 11, 2, 5, 3
+    w = enc_weights(E, H, Vs, 76)
+    rng = np.random.default_rng(77)
+    tok = rng.integers(0, Vs, (B, S)).astype(np.int32)
+    mask = np.ones((B, S), np.float32)
+    mask[1, 3:] = 0
+    copy_b = np.zeros((T, 3 * H), np.float32)
+    copy_b[:, H:2 * H] = 40.0
+    Ut = rnd(T, H, 3 * H, rng=rng)
+    a = mtref.encode(tok, mask, *[w[k] for k in ("semb", "Wf", "Uf", "bf", "Wb", "Ub", "bb")],
+                     transitions=(Ut, copy_b, Ut, copy_b))
+    assert np.array_equal(a, enc(tok, mask, w))
+    bt = rnd(T, 3 * H, s=0.3, rng=rng)
+    got = mtref.encode(tok[:1], mask[:1], *[w[k] for k in ("semb", "Wf", "Uf", "bf", "Wb", "Ub", "bb")],
+                       transitions=(Ut, bt, Ut, bt))
+    h = np.zeros(H)
+    for i in range(S):
+        h = torch_gru(w["semb"][tok[0, i]], h, w["Wf"], w["Uf"], w["bf"])
+        for j in range(T):
+            h = torch_transition(h, Ut[j], bt[j])
+        assert np.max(np.abs(got[0, i, :H] - h)) <= 1e-6
