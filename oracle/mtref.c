@@ -348,18 +348,23 @@ int mtref_encode(int E, int H, int Vs, int B, int S, const int32_t *src_tok, con
                  const float *semb, const float *Wf, const float *Uf, const float *bf,
                  const float *Wb, const float *Ub, const float *bb, float *ctx_out) {
   return mtref_encode_deep(E, H, Vs, B, S, src_tok, mask, semb, Wf, Uf, bf, Wb, Ub, bb, 0, NULL, NULL, NULL, NULL,
-                           ctx_out);
+                           NULL, NULL, NULL, NULL, NULL, NULL, 0.0, ctx_out);
 }
 
-/* Deep-transition encoder cell (Section 3.1.1, four GRU blocks per encoder cell): the input
- * block, then T blocks without external input, each output stored in fp32. */
+/* Deep-transition encoder cell (Section 3.1.1: four GRU blocks per encoder cell, layer
+ * normalisation inside the blocks): the input block, then T blocks without external input,
+ * each output stored in fp32. */
 int mtref_encode_deep(int E, int H, int Vs, int B, int S, const int32_t *src_tok, const float *mask,
                       const float *semb, const float *Wf, const float *Uf, const float *bf,
                       const float *Wb, const float *Ub, const float *bb, int T, const float *Utf,
-                      const float *btf, const float *Utb, const float *btb, float *ctx_out) {
+                      const float *btf, const float *Utb, const float *btb, const float *lna_g,
+                      const float *lna_b, const float *lnu_g, const float *lnu_b, const float *lnt_g,
+                      const float *lnt_b, double eps, float *ctx_out) {
   if (E < 1 || H < 1 || Vs < 1 || B < 0 || S < 1 || !src_tok || !mask || !semb || !Wf || !Uf || !bf ||
       !Wb || !Ub || !bb || !ctx_out || T < 0 || (T > 0 && (!Utf || !btf || !Utb || !btb)))
     return -1;
+  const int ln = lna_g != NULL;
+  if (ln && (!lna_b || !lnu_g || !lnu_b || (T > 0 && (!lnt_g || !lnt_b)))) return -1;
   for (long i = 0; i < (long)B * S; ++i)
     if (src_tok[i] < 0 || src_tok[i] >= Vs) return -2;
   const int C = 2 * H;
@@ -374,13 +379,16 @@ int mtref_encode_deep(int E, int H, int Vs, int B, int S, const int32_t *src_tok
         float *out = ctx_out + ((size_t)b * S + i) * C + (size_t)dir * H;
         if (mask[(size_t)b * S + i] != 0.f) {
           to_double(E, semb + (size_t)src_tok[(size_t)b * S + i] * E, x);
-          mtref_gru(E, H, x, h, dir == 0 ? Wf : Wb, dir == 0 ? Uf : Ub, dir == 0 ? bf : bb, NULL, NULL, NULL,
-                    NULL, 0.0, hn);
+          const size_t lo = (size_t)dir * 3 * H;
+          mtref_gru(E, H, x, h, dir == 0 ? Wf : Wb, dir == 0 ? Uf : Ub, dir == 0 ? bf : bb,
+                    ln ? lna_g + lo : NULL, ln ? lna_b + lo : NULL, ln ? lnu_g + lo : NULL, ln ? lnu_b + lo : NULL,
+                    eps, hn);
           round_store(H, hn, out, h);
           for (int j = 0; j < T; ++j) {
             const float *U = (dir == 0 ? Utf : Utb) + (size_t)j * H * 3 * H;
             const float *bt = (dir == 0 ? btf : btb) + (size_t)j * 3 * H;
-            mtref_gru_transition(H, h, U, bt, NULL, NULL, 0.0, hn);
+            const size_t to = ((size_t)dir * T + j) * 3 * H;
+            mtref_gru_transition(H, h, U, bt, ln ? lnt_g + to : NULL, ln ? lnt_b + to : NULL, eps, hn);
             round_store(H, hn, out, h);
           }
         } else {

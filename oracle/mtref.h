@@ -117,13 +117,19 @@ int mtref_encode(int E, int H, int Vs, int B, int S, const int32_t *src_tok, con
                  const float *Wb, const float *Ub, const float *bb, float *ctx_out);
 
 /* The same with a deep-transition cell per direction (Section 3.1.1: the deep model's encoder
- * cell has four GRU blocks): after the input block, T recurrent-only transition blocks
- * (mtref_gru_transition, no layer norm) with stacked Utf/btf (forward) and Utb/btb
- * (backward), [T,H,3H] and [T,3H]; a padded position carries the state over all blocks. */
+ * cell has four GRU blocks, with layer normalisation inside them): after the input block, T
+ * recurrent-only transition blocks (mtref_gru_transition) with stacked Utf/btf (forward) and
+ * Utb/btb (backward), [T,H,3H] and [T,3H]; a padded position carries the state over all
+ * blocks.  Layer norm (lna_g NULL: none): the input block normalises both paths with
+ * lna_g/lna_b (input path) and lnu_g/lnu_b (recurrent path), [2,3H] each, forward then
+ * backward; transition block j of direction d normalises its recurrent path with
+ * lnt_g/lnt_b[d][j], [2,T,3H]. */
 int mtref_encode_deep(int E, int H, int Vs, int B, int S, const int32_t *src_tok, const float *mask,
                       const float *semb, const float *Wf, const float *Uf, const float *bf,
                       const float *Wb, const float *Ub, const float *bb, int T, const float *Utf,
-                      const float *btf, const float *Utb, const float *btb, float *ctx_out);
+                      const float *btf, const float *Utb, const float *btb, const float *lna_g,
+                      const float *lna_b, const float *lnu_g, const float *lnu_b, const float *lnt_g,
+                      const float *lnt_b, double eps, float *ctx_out);
 
 /* Attention keys of the second source: P2 = ctx2 Ua2 + ba2 at valid positions, 0 elsewhere. */
 int mtref_keys2(const mtref_dims *d, const mtref_weights *w, int B, int S, const float *ctx, const float *mask,

@@ -84,7 +84,8 @@ def lib():
         L.mtref_encode.argtypes = [C.c_int, C.c_int, C.c_int, C.c_int, C.c_int, _i, _f, _f, _f, _f, _f, _f, _f, _f, _f]
         L.mtref_encode.restype = C.c_int
         L.mtref_encode_deep.argtypes = [C.c_int, C.c_int, C.c_int, C.c_int, C.c_int, _i, _f, _f, _f, _f, _f, _f,
-                                        _f, _f, C.c_int, _f, _f, _f, _f, _f]
+                                        _f, _f, C.c_int, _f, _f, _f, _f, _f, _f, _f, _f, _f, _f,
+                                        C.c_double, _f]
         L.mtref_encode_deep.restype = C.c_int
         L.mtref_topk.argtypes = [C.c_int, C.c_int, C.c_int, _f, _f, _i, _i, _f]
         L.mtref_topk.restype = C.c_int
@@ -296,9 +297,11 @@ def ensemble_logp(logps, weights) -> np.ndarray:
     return acc.astype(np.float32)
 
 
-def encode(src_tok, mask, semb, Wf, Uf, bf, Wb, Ub, bb, transitions=None) -> np.ndarray:
+def encode(src_tok, mask, semb, Wf, Uf, bf, Wb, Ub, bb, transitions=None, ln=None, eps=1e-5) -> np.ndarray:
     """Bi-directional GRU encoder: ctx [B, S, 2H] fp32 (see mtref_encode); transitions:
-    None or (Utf, btf, Utb, btb) stacked [T,H,3H] / [T,3H] (deep-transition cell)."""
+    None or (Utf, btf, Utb, btb) stacked [T,H,3H] / [T,3H] (deep-transition cell); ln: None or
+    (ga, ba, gu, bu) [2,3H] and, with transitions, (gt, bt) [2,T,3H] appended (see
+    mtref_encode_deep)."""
     src_tok = np.ascontiguousarray(src_tok, np.int32)
     mask = f32(mask)
     semb, Wf, Uf, bf, Wb, Ub, bb = [f32(a) for a in (semb, Wf, Uf, bf, Wb, Ub, bb)]
@@ -306,11 +309,18 @@ def encode(src_tok, mask, semb, Wf, Uf, bf, Wb, Ub, bb, transitions=None) -> np.
     Vs, E = semb.shape
     H = Uf.shape[0]
     out = np.empty((B, S, 2 * H), np.float32)
-    if transitions is not None:
-        Utf, btf, Utb, btb = [f32(a) for a in transitions]
+    if transitions is not None or ln is not None:
+        if transitions is not None:
+            Utf, btf, Utb, btb = [f32(a) for a in transitions]
+            T = Utf.shape[0]
+        else:
+            Utf = btf = Utb = btb = None
+            T = 0
+        lnp = [None] * 6 if ln is None else [f32(a) for a in ln] + [None] * (6 - len(ln))
+        assert ln is None or len(ln) == (6 if T else 4)
         rc = lib().mtref_encode_deep(E, H, Vs, B, S, _ip(src_tok), _fp(mask), _fp(semb), _fp(Wf), _fp(Uf), _fp(bf),
-                                     _fp(Wb), _fp(Ub), _fp(bb), Utf.shape[0], _fp(Utf), _fp(btf), _fp(Utb), _fp(btb),
-                                     _fp(out))
+                                     _fp(Wb), _fp(Ub), _fp(bb), T, _fp(Utf), _fp(btf), _fp(Utb), _fp(btb),
+                                     *[_fp(a) for a in lnp], eps, _fp(out))
         if rc != 0:
             raise ValueError(f"mtref_encode_deep: {rc}")
         return out

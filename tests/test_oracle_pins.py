@@ -942,3 +942,90 @@ def test_deep_encoder_copying_transitions_equal_shallow_and_torch_per_block():
         for j in range(T):
             h = torch_transition(h, Ut[j], bt[j])
         assert np.max(np.abs(got[0, i, :H] - h)) <= 1e-6
+
+
+def enc_ln_params(H, T, seed, g=None):
+    """(ga, ba, gu, bu) [2,3H] and, for T > 0, (gt, bt) [2,T,3H]; gains ~1 + N(0, 0.2) unless g."""
+    rng = np.random.default_rng(seed)
+    gain = (lambda *s: np.full(s, g, np.float32)) if g is not None else (lambda *s: 1 + rnd(*s, s=0.2, rng=rng))
+    p = [gain(2, 3 * H), rnd(2, 3 * H, s=0.3, rng=rng), gain(2, 3 * H), rnd(2, 3 * H, s=0.3, rng=rng)]
+    if T:
+        p += [gain(2, T, 3 * H), rnd(2, T, 3 * H, s=0.3, rng=rng)]
+    return tuple(p)
+
+
+def enc_deep(tok, mask, w, trans=None, ln=None, eps=1e-5):
+    return mtref.encode(tok, mask, *[w[k] for k in ("semb", "Wf", "Uf", "bf", "Wb", "Ub", "bb")],
+                        transitions=trans, ln=ln, eps=eps)
+
+
+def test_ln_encoder_zero_gains_give_closed_form():
+    """With every layer-norm gain 0 each normalised path is its shift alone, so the gates are
+    constants: r = s(ba_r + bu_r), z = s(ba_z + bu_z), n = tanh(ba_n + r bu_n) for the input
+    block, and with the transition bias b_t added in place of ba for a transition block.  A
+    block then maps h to (1 - z) n + z h; from the zero state the forward direction's state
+    after the input block of position i (0-based, unpadded) follows that recursion."""
+    E, H, Vs, S, T = 6, 5, 11, 5, 2
+    w = enc_weights(E, H, Vs, 78)
+    rng = np.random.default_rng(79)
+    tok = rng.integers(0, Vs, (1, S)).astype(np.int32)
+    Ut = rnd(T, H, 3 * H, rng=rng)
+    btf, btb = rnd(T, 3 * H, s=0.3, rng=rng), rnd(T, 3 * H, s=0.3, rng=rng)
+    ga, ba, gu, bu, gt, bt = enc_ln_params(H, T, 80, g=0.0)
+    got = enc_deep(tok, np.ones((1, S), np.float32), w, (Ut, btf, Ut, btb), (ga, ba, gu, bu, gt, bt))
+    sig = lambda v: 1 / (1 + np.exp(-v))
+
+    def block(h, a, u):
+        r = sig(a[:H] + u[:H])
+        z = sig(a[H:2 * H] + u[H:2 * H])
+        n = np.tanh(a[2 * H:] + r * u[2 * H:])
+        return (1 - z) * n + z * h
+
+    for d, order, bt_d in ((0, range(S), btf), (1, range(S - 1, -1, -1), btb)):
+        h = np.zeros(H)
+        for i in order:
+            h = block(h, ba[d].astype(np.float64), bu[d].astype(np.float64))
+            for j in range(T):
+                h = block(h, bt_d[j].astype(np.float64), bt[d, j].astype(np.float64))
+            assert np.max(np.abs(got[0, i, d * H:(d + 1) * H] - h)) <= 1e-6
+
+
+def test_ln_encoder_scale_invariance_and_direction_reversal():
+    """Layer norm on both paths of the input block and on the transition blocks' recurrent
+    path: scaling Wf, bf, Wb, bb by 3 and Uf, Ub, Utf, Utb by 0.5 leaves the context
+    unchanged (with a variance epsilon of 1e-12, which the scaling would otherwise see
+    where a state is still small); reversing a sentence with every per-direction
+    parameter swapped (layer-norm ones included) swaps the halves exactly."""
+    E, H, Vs, S, T = 6, 5, 11, 6, 3
+    w = enc_weights(E, H, Vs, 81)
+    rng = np.random.default_rng(82)
+    tok = rng.integers(0, Vs, (2, S)).astype(np.int32)
+    one = np.ones((2, S), np.float32)
+    Utf, Utb = rnd(T, H, 3 * H, rng=rng), rnd(T, H, 3 * H, rng=rng)
+    btf, btb = rnd(T, 3 * H, s=0.3, rng=rng), rnd(T, 3 * H, s=0.3, rng=rng)
+    ln = enc_ln_params(H, T, 83)
+    a = enc_deep(tok, one, w, (Utf, btf, Utb, btb), ln, eps=1e-12)
+    ws = dict(w, Wf=w["Wf"] * 3, bf=w["bf"] * 3, Wb=w["Wb"] * 3, bb=w["bb"] * 3, Uf=w["Uf"] * 0.5, Ub=w["Ub"] * 0.5)
+    b = enc_deep(tok, one, ws, (Utf * 0.5, btf, Utb * 0.5, btb), ln, eps=1e-12)
+    assert np.max(np.abs(a - b)) <= 1e-5
+    # without layer norm the same scaling changes the context (the pin above has teeth)
+    assert np.max(np.abs(enc_deep(tok, one, w, (Utf, btf, Utb, btb)) - enc_deep(tok, one, ws, (Utf * 0.5, btf,
+                                                                                                 Utb * 0.5, btb)))) > 1e-2
+    sw = dict(w, Wf=w["Wb"], Uf=w["Ub"], bf=w["bb"], Wb=w["Wf"], Ub=w["Uf"], bb=w["bf"])
+    lsw = tuple(np.ascontiguousarray(x[::-1]) for x in ln)
+    c = enc_deep(tok[:, ::-1].copy(), one, sw, (Utb, btb, Utf, btf), lsw, eps=1e-12)
+    assert np.array_equal(a[:, :, :H], c[:, ::-1, H:]) and np.array_equal(a[:, :, H:], c[:, ::-1, :H])
+
+
+def test_ln_deep_encoder_padding_leaves_valid_rows_unchanged():
+    E, H, Vs, T = 6, 5, 11, 3
+    w = enc_weights(E, H, Vs, 84)
+    rng = np.random.default_rng(85)
+    L, S = 3, 8
+    tok = rng.integers(0, Vs, (1, S)).astype(np.int32)
+    Ut, bt = rnd(T, H, 3 * H, rng=rng), rnd(T, 3 * H, s=0.3, rng=rng)
+    ln = enc_ln_params(H, T, 86)
+    a = enc_deep(tok, (np.arange(S) < L).astype(np.float32)[None], w, (Ut, bt, Ut, bt), ln)
+    b = enc_deep(tok[:, :L], np.ones((1, L), np.float32), w, (Ut, bt, Ut, bt), ln)
+    assert np.array_equal(a[:, :L], b)
+    assert np.array_equal(a[0, L:, :H], np.repeat(b[0, L - 1:, :H], S - L, 0)) and np.all(a[0, L:, H:] == 0)
