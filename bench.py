@@ -103,6 +103,11 @@ def main():
                     help="dual-source model: a second source (seeded like the first) with its own attention")
     ap.add_argument("--encode", type=int, default=0,
                     help="also time the encoder (mt_encode) over the batch with a source vocabulary of this size")
+    ap.add_argument("--enc-transitions", type=int, default=0,
+                    help="with --encode: recurrent-only GRU blocks after each direction's input block "
+                         "(the deep model's four-block encoder cell: 3)")
+    ap.add_argument("--enc-layer-norm", action="store_true",
+                    help="with --encode: layer norm inside the encoder's GRU blocks")
     ap.add_argument("--translate", type=int, default=0,
                     help="time whole translations of the batch to n-best lists (this many steps at most; "
                          "EOS = token 0, length normalisation alpha 0.6) instead of a fixed step count")
@@ -262,9 +267,11 @@ def main():
     }
     if args.encode:
         # encoder of the same shapes over Zipf source tokens with the batch's lengths
-        ew = synth.make_encoder_weights(p, args.encode)
+        ew = synth.make_encoder_weights(p, args.encode, transitions=args.enc_transitions,
+                                        layer_norm=args.enc_layer_norm)
         encd = Decoder(p.E, p.H, p.A, p.V, {**w, **ew}, gemm=p.gemm, layer_norm=p.layer_norm, k_max=max(p.K, 1),
-                       src_V=args.encode)
+                       src_V=args.encode, enc_transitions=args.enc_transitions,
+                       enc_layer_norm=args.enc_layer_norm)
         src = synth.source_tokens(p, args.encode, lens, dec.S)
         encd.set_source(src, mask, p.K)
         for _ in range(3):
@@ -278,8 +285,9 @@ def main():
         e_s = (time.perf_counter() - t0) / reps
         rec["encode"] = {
             "what": "mt_encode of the batch: bi-directional GRU over the padded source (one input product, then "
-                    "per position the recurrent products of both directions and two cells)",
-            "src_V": args.encode, "padded_S": int(dec.S), "ms_per_batch": round(1e3 * e_s, 3),
+                    "per position the recurrent products of both directions and two cells, then per "
+                    "transition block one more product and two more cells)",
+            "src_V": args.encode, "enc_transitions": args.enc_transitions, "enc_layer_norm": args.enc_layer_norm, "padded_S": int(dec.S), "ms_per_batch": round(1e3 * e_s, 3),
             "src_tokens_per_s": round(float(lens.sum()) / e_s, 1),
             "per_decoder_step_us_at_precompute_interval": round(1e6 * e_s / p.steps, 2),
         }

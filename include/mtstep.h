@@ -90,6 +90,12 @@ typedef struct {
   int32_t dec_transitions;
   int32_t src_V;  /* source vocabulary of the encoder (mt_encode); 0: no encoder */
   int32_t dual_source;  /* 1: a second source with its own attention (mt_decoder_step_dual) */
+  int32_t enc_transitions; /* 0..16: recurrent-only GRU blocks after the input block of each
+                            * encoder direction (the deep-transition encoder cell of Section
+                            * 3.1.1 has four blocks in all: 3); needs src_V > 0. */
+  int32_t enc_layer_norm;  /* 0/1: layer norm inside the encoder's GRU blocks (eps = ln_eps):
+                            * per gate block on both paths of each direction's input block and
+                            * on the recurrent path of each transition block; needs src_V > 0 */
 } mt_config;
 
 /* Model parameters: HOST pointers to fp32, row-major logical [in x out]
@@ -105,7 +111,12 @@ typedef struct {
  *   encoder (read only if src_V > 0): semb[src_V,E], forward Wef[E,3H]
  *   Uef[H,3H] bef[3H], backward Web[E,3H] Ueb[H,3H] beb[3H];
  *   second source (read only if dual_source): Ua2[C,A] ba2[A] Wa2[H,A] va2[A],
- *   and W2 [2C,3H], Wt_c [2C,E] then take the two contexts side by side. */
+ *   and W2 [2C,3H], Wt_c [2C,E] then take the two contexts side by side;
+ *   encoder transition blocks (read only if enc_transitions = T > 0), stacked
+ *   by block: forward Utef[T,H,3H] btef[T,3H], backward Uteb[T,H,3H] bteb[T,3H];
+ *   encoder layer norm (read only if enc_layer_norm), forward then backward: gain/shift
+ *   of the input blocks' input path gea/bea[2,3H] and recurrent path geu/beu[2,3H], and of
+ *   the transition blocks' recurrent path gteu/beteu[2,T,3H]. */
 typedef struct {
   const float *emb;
   const float *W1, *U1, *b1;
@@ -118,6 +129,8 @@ typedef struct {
   const float *Ut, *btr, *gtu, *betu;
   const float *semb, *Wef, *Uef, *bef, *Web, *Ueb, *beb;
   const float *Ua2, *ba2, *Wa2, *va2;
+  const float *Utef, *btef, *Uteb, *bteb;
+  const float *gea, *bea, *geu, *beu, *gteu, *beteu;
 } mt_weights;
 
 typedef struct mt_model mt_model; /* opaque, library-owned */

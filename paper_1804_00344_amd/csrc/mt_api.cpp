@@ -79,6 +79,11 @@ struct mt_model {
   Packed wenc_x, wenc_f, wenc_b;  // encoder: [Wef | Web], Uef, Ueb
   float *bias_enc = nullptr;      // [bef | beb]
   float *semb = nullptr;          // [src_V][E] fp32 source embeddings
+  std::vector<Packed> wenc_tf, wenc_tb;  // encoder transition blocks, per block and direction
+  float *bias_tenc = nullptr;            // [block][direction][3H]
+  // encoder layer norm: input-block gains/shifts of both paths [direction][3H] (gea, bea,
+  // geu, beu), transition blocks' recurrent-path gains/shifts [direction][block][3H]
+  float *ln_enc[6] = {nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
   std::vector<Packed> wtr;        // transition blocks' recurrent matrices
   float *btr = nullptr;           // [T][3H] their biases
   float *gtu = nullptr, *betu = nullptr;  // [T][3H] layer norm of their recurrent products
@@ -116,7 +121,13 @@ mt_status check_cfg(const mt_config *c) {
   if (c->src_V < 0 || c->src_V > (1 << 24)) return fail(MT_ERR_SHAPE, "src_V=%d: need 0 <= src_V <= 2^24", c->src_V);
   if (c->dec_transitions < 0 || c->dec_transitions > kMaxTransitions)
     return fail(MT_ERR_SHAPE, "dec_transitions=%d: need 0..%d", c->dec_transitions, kMaxTransitions);
-  if (c->layer_norm && !(c->ln_eps > 0.f && std::isfinite(c->ln_eps)))
+  if (c->enc_transitions < 0 || c->enc_transitions > kMaxTransitions)
+    return fail(MT_ERR_SHAPE, "enc_transitions=%d: need 0..%d", c->enc_transitions, kMaxTransitions);
+  if (c->enc_transitions > 0 && c->src_V <= 0)
+    return fail(MT_ERR_ARG, "enc_transitions=%d needs an encoder (src_V > 0)", c->enc_transitions);
+  if (c->enc_layer_norm != 0 && c->enc_layer_norm != 1) return fail(MT_ERR_ARG, "enc_layer_norm must be 0 or 1");
+  if (c->enc_layer_norm && c->src_V <= 0) return fail(MT_ERR_ARG, "enc_layer_norm needs an encoder (src_V > 0)");
+  if ((c->layer_norm || c->enc_layer_norm) && !(c->ln_eps > 0.f && std::isfinite(c->ln_eps)))
     return fail(MT_ERR_ARG, "ln_eps must be positive and finite");
   if (vocab_rows_per_block(c->gemm_dtype == MT_BF16, c->E) == 0)
     return fail(MT_ERR_SHAPE, "E=%d too large for the vocabulary kernel (E <= %d)", c->E,
@@ -385,6 +396,12 @@ mt_status mt_load_weights(const mt_config *cfg, const mt_weights *w, mt_model **
     const char *en[] = {"semb", "Wef", "Uef", "bef", "Web", "Ueb", "beb"};
     for (int i = 0; i < 7; ++i)
       if (!ew[i]) return fail(MT_ERR_ARG, "encoder weight %s is NULL (src_V = %d)", en[i], c.src_V);
+    if (c.enc_transitions > 0 && (!w->Utef || !w->btef || !w->Uteb || !w->bteb))
+      return fail(MT_ERR_ARG, "Utef, btef, Uteb or bteb is NULL (enc_transitions = %d)", c.enc_transitions);
+    if (c.enc_layer_norm && (!w->gea || !w->bea || !w->geu || !w->beu))
+      return fail(MT_ERR_ARG, "gea, bea, geu or beu is NULL (enc_layer_norm = 1)");
+    if (c.enc_layer_norm && c.enc_transitions > 0 && (!w->gteu || !w->beteu))
+      return fail(MT_ERR_ARG, "gteu or beteu is NULL (enc_layer_norm = 1, enc_transitions > 0)");
   }
   if (c.dec_transitions > 0) {
     if (!w->Ut || !w->btr) return fail(MT_ERR_ARG, "Ut or btr is NULL (dec_transitions = %d)", c.dec_transitions);
@@ -492,6 +509,26 @@ mt_status mt_load_weights(const mt_config *cfg, const mt_weights *w, mt_model **
       CHECK(upload_packed(m, {{w->Ueb, 3 * H}}, H, kRefSentences, &m->wenc_b));
       CHECK(upload_vec(m, cat({{w->bef, 3 * H}, {w->beb, 3 * H}}), &m->bias_enc));
       CHECK(dev_upload(m, w->semb, (size_t)c.src_V * E * sizeof(float), (void **)&m->semb));
+      const int Te = c.enc_transitions;
+      m->wenc_tf.resize(Te);
+      m->wenc_tb.resize(Te);
+      std::vector<float> bte;
+      for (int j = 0; j < Te; ++j) {
+        const size_t o = (size_t)j * H * 3 * H;
+        CHECK(upload_packed(m, {{w->Utef + o, 3 * H}}, H, kRefSentences, &m->wenc_tf[j]));
+        CHECK(upload_packed(m, {{w->Uteb + o, 3 * H}}, H, kRefSentences, &m->wenc_tb[j]));
+        bte.insert(bte.end(), w->btef + (size_t)j * 3 * H, w->btef + (size_t)(j + 1) * 3 * H);
+        bte.insert(bte.end(), w->bteb + (size_t)j * 3 * H, w->bteb + (size_t)(j + 1) * 3 * H);
+      }
+      if (Te > 0) CHECK(upload_vec(m, bte, &m->bias_tenc));
+      if (c.enc_layer_norm) {
+        const float *src[4] = {w->gea, w->bea, w->geu, w->beu};
+        for (int i = 0; i < 4; ++i) CHECK(upload_vec(m, cat({{src[i], 6 * H}}), &m->ln_enc[i]));
+        if (Te > 0) {
+          CHECK(upload_vec(m, cat({{w->gteu, 2 * Te * 3 * H}}), &m->ln_enc[4]));
+          CHECK(upload_vec(m, cat({{w->beteu, 2 * Te * 3 * H}}), &m->ln_enc[5]));
+        }
+      }
     }
     const int T = c.dec_transitions;
     m->wtr.resize(T);
@@ -556,9 +593,10 @@ size_t mt_workspace_bytes(const mt_model *m, int B, int K, int S) {
 }
 
 // encoder workspace: input products [B*S][6H], recurrent products of both directions and a
-// zero block [B][3H] each, fp32 states [2 directions][2][B][H] (bf16 models)
+// zero block [B][3H] each, fp32 states [2 directions][2][B][H] (bf16 models), intermediate
+// states of the transition blocks [2 directions][B][H]
 struct EncLayout {
-  size_t xe, uf, ub, uz, st, total;
+  size_t xe, uf, ub, uz, st, tx, total;
 };
 static EncLayout enc_layout(const mt_model *m, int B, int S) {
   const size_t H = m->cfg.H;
@@ -574,6 +612,7 @@ static EncLayout enc_layout(const mt_model *m, int B, int S) {
   L.ub = take((size_t)B * 3 * H * 4);
   L.uz = take((size_t)B * 3 * H * 4);
   L.st = take(m->bf16 ? (size_t)4 * B * H * 4 : 0);
+  L.tx = take(m->cfg.enc_transitions > 0 ? (size_t)2 * B * H * 4 : 0);
   L.total = off;
   return L;
 }
@@ -611,9 +650,25 @@ mt_status mt_encode(mt_model *model, int B, int S, const int32_t *src_tok, const
   LAUNCH(MT_KERNEL_ENCODE, launch_fill_zero(uz, (long long)B * 3 * H, st));
   float *c32 = bf ? nullptr : (float *)ctx_out;
   bf16 *c16 = bf ? (bf16 *)ctx_out : nullptr;
+  const int Te = model->cfg.enc_transitions;
+  float *tx = (float *)(W + L.tx);  // intermediate transition states [dir][B][H]
+  float *const *eln = model->cfg.enc_layer_norm ? model->ln_enc : nullptr;
+  const float eps = model->cfg.ln_eps;
   for (int n = 0; n < S; ++n) {
     const int pos[2] = {n, S - 1 - n};       // forward, backward position of this pass
     const int prv[2] = {n - 1, S - n};       // the position each direction comes from
+    // the output of block i (0: the input block, 1..Te: the transition blocks) of direction d:
+    // the final one lands where the next position reads the state from; intermediate ones
+    // alternate with it through tx, so a block never reads and writes the same buffer
+    struct Slot {
+      float *p;
+      int ld;
+    };
+    auto block_out = [&](int d, int i) -> Slot {
+      if ((Te - i) % 2 != 0) return {tx + (size_t)d * B * H, H};
+      if (bf) return {sst + ((size_t)(2 * d + (n & 1)) * B) * H, H};
+      return {c32 + (size_t)pos[d] * C + (size_t)d * H, (int)ldc};
+    };
     // recurrent products of both directions from the previous states (zero at n = 0)
     if (n > 0) {
       GemmProblem pr[2]{};
@@ -627,28 +682,67 @@ mt_status mt_encode(mt_model *model, int B, int S, const int32_t *src_tok, const
       }
       LAUNCH(MT_KERNEL_ENCODE, launch_gemm(bf, pr, 2, EPI_STORE, st));
     }
-    for (int d = 0; d < 2; ++d) {
-      const float *u = n > 0 ? (d == 0 ? uf : ub) : uz;
-      const size_t oc = (size_t)pos[d] * C + (size_t)d * H, op = (size_t)prv[d] * C + (size_t)d * H;
-      const float *hsrc;
-      int ldh;
+    // one launch runs both directions' cells (the second at element offsets from the first)
+    struct CellArgs {
+      const float *a, *u, *h;
       float *out;
-      int ldo;
-      if (bf) {
-        hsrc = n > 0 ? sst + ((size_t)(2 * d + ((n - 1) & 1)) * B) * H : nullptr;
-        ldh = H;
-        out = sst + ((size_t)(2 * d + (n & 1)) * B) * H;
-        ldo = H;
-      } else {
-        hsrc = n > 0 ? c32 + op : nullptr;
-        ldh = (int)ldc;
-        out = c32 + oc;
-        ldo = (int)ldc;
+      bf16 *o16;
+      const float *keep;
+    };
+    auto pair_of = [](const CellArgs &f, const CellArgs &b, long long dln) {
+      CellPair pr{};
+      pr.da = b.a - f.a; pr.du = b.u - f.u; pr.dh = f.h ? b.h - f.h : 0; pr.dout = b.out - f.out;
+      pr.d16 = f.o16 ? b.o16 - f.o16 : 0; pr.dkeep = b.keep - f.keep; pr.dln = dln;
+      return pr;
+    };
+    {
+      CellArgs ca[2];
+      int ldh = 0;
+      for (int d = 0; d < 2; ++d) {
+        const size_t oc = (size_t)pos[d] * C + (size_t)d * H, op = (size_t)prv[d] * C + (size_t)d * H;
+        const float *hsrc;
+        if (bf) {
+          hsrc = n > 0 ? sst + ((size_t)(2 * d + ((n - 1) & 1)) * B) * H : nullptr;
+          ldh = H;
+        } else {
+          hsrc = n > 0 ? c32 + op : nullptr;
+          ldh = (int)ldc;
+        }
+        ca[d] = {xe + (size_t)pos[d] * 6 * H + (size_t)d * 3 * H, n > 0 ? (d == 0 ? uf : ub) : uz, hsrc,
+                 block_out(d, 0).p, bf && Te == 0 ? c16 + oc : nullptr, mask + pos[d]};
       }
+      const CellPair pr = pair_of(ca[0], ca[1], 3 * H);
       LAUNCH(MT_KERNEL_ENCODE,
-             launch_gru_cell_ex(B, H, xe + (size_t)pos[d] * 6 * H + (size_t)d * 3 * H, S * 6 * H, nullptr, B, u,
-                                3 * H, hsrc, ldh, nullptr, B, model->err, nullptr, nullptr, nullptr, nullptr, 0.f,
-                                out, ldo, bf ? c16 + oc : nullptr, (int)ldc, nullptr, mask + pos[d], S, st));
+             launch_gru_cell_ex(B, H, ca[0].a, S * 6 * H, nullptr, B, ca[0].u, 3 * H, ca[0].h, ldh, nullptr, B,
+                                model->err, eln ? eln[0] : nullptr, eln ? eln[1] : nullptr, eln ? eln[2] : nullptr,
+                                eln ? eln[3] : nullptr, eps, ca[0].out, block_out(0, 0).ld, ca[0].o16, (int)ldc,
+                                nullptr, ca[0].keep, S, st, &pr));
+    }
+    // transition blocks: recurrent products of both directions, then both directions' cells
+    // with the bias as the whole input path (lda = 0); a padded position keeps its state
+    for (int j = 0; j < Te; ++j) {
+      GemmProblem pt[2]{};
+      for (int d = 0; d < 2; ++d) {
+        const Slot x = block_out(d, j);
+        pt[d].A = x.p; pt[d].a_rows = B; pt[d].lda = x.ld; pt[d].a_bf16 = 0;
+        const Packed &U = d == 0 ? model->wenc_tf[j] : model->wenc_tb[j];
+        pt[d].Bp = U.p; pt[d].ldb = U.ldb; pt[d].wblk = U.blk;
+        pt[d].out = d == 0 ? uf : ub; pt[d].ldc = 3 * H; pt[d].M = B; pt[d].N = 3 * H; pt[d].K = H;
+      }
+      LAUNCH(MT_KERNEL_ENCODE, launch_gemm(bf, pt, 2, EPI_STORE, st));
+      CellArgs ca[2];
+      for (int d = 0; d < 2; ++d) {
+        const size_t oc = (size_t)pos[d] * C + (size_t)d * H;
+        ca[d] = {model->bias_tenc + (size_t)(2 * j + d) * 3 * H, d == 0 ? uf : ub, block_out(d, j).p,
+                 block_out(d, j + 1).p, bf && j + 1 == Te ? c16 + oc : nullptr, mask + pos[d]};
+      }
+      const CellPair pr = pair_of(ca[0], ca[1], (long long)Te * 3 * H);
+      const size_t to = (size_t)j * 3 * H;  // forward direction's block j
+      LAUNCH(MT_KERNEL_ENCODE,
+             launch_gru_cell_ex(B, H, ca[0].a, 0, nullptr, B, ca[0].u, 3 * H, ca[0].h, block_out(0, j).ld, nullptr,
+                                B, model->err, nullptr, nullptr, eln ? eln[4] + to : nullptr,
+                                eln ? eln[5] + to : nullptr, eps, ca[0].out, block_out(0, j + 1).ld, ca[0].o16,
+                                (int)ldc, nullptr, ca[0].keep, S, st, &pr));
     }
   }
   return MT_OK;

@@ -430,14 +430,22 @@ hipError_t launch_gru_cell(int M, int H, const float *a, int lda, const int32_t 
                            int32_t *err, const float *ga, const float *ba, const float *gu, const float *bu,
                            float eps, float *out, int ldo, bf16 *out16, float *tap, hipStream_t st);
 
+// Element offsets from one cell's operands to a second cell of the same shape and options
+// run by the same launch (the two directions of an encoder position): a, u, previous state,
+// output, bf16 copy, keep and the layer-norm vectors (one offset for all four).
+struct CellPair {
+  long long da, du, dh, dout, d16, dkeep, dln;
+};
+
 // the same with row strides for the previous state (ldh; hsrc NULL: zero state) and the bf16
 // copy (ld16), and keep (if given): a row m whose keep[m * keep_ld] is 0 carries its previous
-// state over instead of updating
+// state over instead of updating.  pair (if given): a second cell at those offsets, run by
+// the same launch.
 hipError_t launch_gru_cell_ex(int M, int H, const float *a, int lda, const int32_t *aidx, int arows,
                               const float *u, int ldu, const float *hsrc, int ldh, const int32_t *hidx, int hrows,
                               int32_t *err, const float *ga, const float *ba, const float *gu, const float *bu,
                               float eps, float *out, int ldo, bf16 *out16, int ld16, float *tap,
-                              const float *keep, int keep_ld, hipStream_t st);
+                              const float *keep, int keep_ld, hipStream_t st, const CellPair *pair = nullptr);
 hipError_t launch_fill_zero(float *p, long long n, hipStream_t st);
 
 hipError_t launch_readout(int M, int E, const float *p1, int ld1, const float *p2, int ld2, const int32_t *idx2,

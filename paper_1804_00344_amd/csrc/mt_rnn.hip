@@ -67,12 +67,23 @@ __global__ __launch_bounds__(kT) void gru_cell_kernel(int M, int H, const float 
                                                       float *__restrict__ out, int ldo,
                                                       bf16 *__restrict__ out16,
                                                       float *__restrict__ tap, int ldh, int ld16,
-                                                      const float *__restrict__ keep, int keep_ld) {
+                                                      const float *__restrict__ keep, int keep_ld,
+                                                      CellPair pr) {
   constexpr bool LN = LNM != 0;
   constexpr int G0 = LNM == 2 ? 3 : 0;  // first normalised block
   __shared__ float red[4][12];
   const int m = blockIdx.x;
   const int t = threadIdx.x;
+  if (blockIdx.y) {  // the launch's second cell
+    a += pr.da;
+    u += pr.du;
+    if (hsrc) hsrc += pr.dh;
+    out += pr.dout;
+    if (out16) out16 += pr.d16;
+    if (keep) keep += pr.dkeep;
+    if (ga) ga += pr.dln, ba += pr.dln;
+    if (gu) gu += pr.dln, bu += pr.dln;
+  }
   const int ar = aidx ? clamp_row(aidx, m, arows, err, 0) : m;
   const int hr = hidx ? clamp_row(hidx, m, hrows, err, 1) : m;
   const float *arow = a + (size_t)ar * lda;
@@ -330,14 +341,17 @@ hipError_t launch_gru_cell_ex(int M, int H, const float *a, int lda, const int32
                               const float *u, int ldu, const float *hsrc, int ldh, const int32_t *hidx, int hrows,
                               int32_t *err, const float *ga, const float *ba, const float *gu, const float *bu,
                               float eps, float *out, int ldo, bf16 *out16, int ld16, float *tap,
-                              const float *keep, int keep_ld, hipStream_t st) {
+                              const float *keep, int keep_ld, hipStream_t st, const CellPair *pair) {
   if (M == 0) return hipSuccess;
+  if (pair && (tap || aidx || hidx)) return hipErrorInvalidValue;  // not offset by the pair
+  const CellPair pr = pair ? *pair : CellPair{};
+  const dim3 grid(M, pair ? 2 : 1);
   // layer norm on both paths (ga given), on the recurrent path only (gu alone), or none
   const int lnm = ga ? 1 : gu ? 2 : 0;
 #define MT_GRU_L(N, L)                                                                                  \
-  hipLaunchKernelGGL((gru_cell_kernel<N, L>), dim3(M), dim3(kT), 0, st, M, H, a, lda, aidx, arows, u,  \
+  hipLaunchKernelGGL((gru_cell_kernel<N, L>), grid, dim3(kT), 0, st, M, H, a, lda, aidx, arows, u,     \
                      ldu, hsrc, hidx, hrows, err, ga, ba, gu, bu, eps, out, ldo, out16, tap, ldh, ld16,    \
-                     keep, keep_ld)
+                     keep, keep_ld, pr)
 #define MT_GRU(N)              \
   if (lnm == 1)                \
     MT_GRU_L(N, 1);            \

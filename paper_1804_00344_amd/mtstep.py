@@ -35,13 +35,15 @@ class mt_config(C.Structure):
     _fields_ = [("E", C.c_int32), ("H", C.c_int32), ("A", C.c_int32), ("V", C.c_int32),
                 ("layer_norm", C.c_int32), ("tied_output", C.c_int32), ("k_max", C.c_int32),
                 ("gemm_dtype", C.c_int32), ("ln_eps", C.c_float), ("dec_transitions", C.c_int32),
-                ("src_V", C.c_int32), ("dual_source", C.c_int32)]
+                ("src_V", C.c_int32), ("dual_source", C.c_int32), ("enc_transitions", C.c_int32),
+                ("enc_layer_norm", C.c_int32)]
 
 
 WEIGHT_FIELDS = ["emb", "W1", "U1", "b1", "Ua", "ba", "Wa", "va", "W2", "U2", "b2", "Wt_s", "Wt_y",
                  "Wt_c", "bt", "Wo", "bo", "Wi", "bi", "g1a", "be1a", "g1u", "be1u", "g2a", "be2a",
                  "g2u", "be2u", "gt", "bet", "Ut", "btr", "gtu", "betu",
-                 "semb", "Wef", "Uef", "bef", "Web", "Ueb", "beb", "Ua2", "ba2", "Wa2", "va2"]
+                 "semb", "Wef", "Uef", "bef", "Web", "Ueb", "beb", "Ua2", "ba2", "Wa2", "va2",
+                 "Utef", "btef", "Uteb", "bteb", "gea", "bea", "geu", "beu", "gteu", "beteu"]
 
 _fp = C.POINTER(C.c_float)
 
@@ -122,9 +124,10 @@ def _stream(stream) -> Optional[int]:
 
 
 def make_config(E, H, A, V, *, layer_norm=False, tied_output=False, k_max=16, gemm="f32", ln_eps=1e-5,
-                transitions=0, src_V=0, dual_source=False):
+                transitions=0, src_V=0, dual_source=False, enc_transitions=0, enc_layer_norm=False):
     return mt_config(E, H, A, V, int(layer_norm), int(tied_output), k_max,
-                     MT_BF16 if gemm == "bf16" else MT_F32, ln_eps, transitions, src_V, int(dual_source))
+                     MT_BF16 if gemm == "bf16" else MT_F32, ln_eps, transitions, src_V, int(dual_source),
+                     enc_transitions, int(enc_layer_norm))
 
 
 class Model:

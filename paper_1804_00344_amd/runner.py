@@ -18,13 +18,15 @@ from . import mtstep as mt
 class Decoder:
     def __init__(self, E: int, H: int, A: int, V: int, weights: Dict[str, np.ndarray], *, gemm: str = "f32",
                  layer_norm: bool = False, tied_output: bool = False, k_max: int = 16, ln_eps: float = 1e-5,
-                 transitions: int = 0, src_V: int = 0, dual_source: bool = False, device: str = "cuda:0"):
+                 transitions: int = 0, src_V: int = 0, dual_source: bool = False, enc_transitions: int = 0,
+                 enc_layer_norm: bool = False, device: str = "cuda:0"):
         self.E, self.H, self.A, self.V, self.C = E, H, A, V, 2 * H
         self.gemm = gemm
         self.device = torch.device(device)
         self.cfg = mt.make_config(E, H, A, V, layer_norm=layer_norm, tied_output=tied_output, k_max=k_max,
                                   gemm=gemm, ln_eps=ln_eps, transitions=transitions, src_V=src_V,
-                                  dual_source=dual_source)
+                                  dual_source=dual_source, enc_transitions=enc_transitions,
+                                  enc_layer_norm=enc_layer_norm)
         self.dual = bool(dual_source)
         self.S2 = 0
         with torch.cuda.device(self.device):

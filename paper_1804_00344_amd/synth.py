@@ -270,19 +270,40 @@ def make_source2(p: Preset):
 
 
 ENCODER_NAMES = ("semb", "Wef", "Uef", "bef", "Web", "Ueb", "beb")
+ENCODER_TRANSITION_NAMES = ("Utef", "btef", "Uteb", "bteb")  # stacked over the transition blocks
+ENCODER_LN_NAMES = ("gea", "bea", "geu", "beu", "gteu", "beteu")  # forward, backward stacked
 
 
-def make_encoder_weights(p: Preset, src_V: int) -> Dict[str, np.ndarray]:
+def make_encoder_weights(p: Preset, src_V: int, transitions: int = 0, layer_norm: bool = False
+                         ) -> Dict[str, np.ndarray]:
     """Bi-directional GRU encoder over a source vocabulary of src_V: embeddings N(0, 0.1),
     gate matrices Glorot-uniform per gate block, zero biases (bf16 presets round the product
-    operands to bf16)."""
+    operands to bf16); with transitions = T > 0 also T recurrent-only blocks per direction
+    (Glorot-uniform gate matrices, biases N(0, 0.1)); with layer_norm gains 1 + N(0, 0.1) and
+    shifts N(0, 0.1) for the input blocks' two paths [2,3H] and the transition blocks'
+    recurrent path [2,T,3H]."""
     E, H = p.E, p.H
     w = {"semb": rng_for(p, "semb").normal(0.0, 0.1, size=(src_V, E)).astype(np.float32),
          "Wef": _gate_matrix(p, "Wef", E), "Uef": _gate_matrix(p, "Uef", H), "bef": np.zeros(3 * H, np.float32),
          "Web": _gate_matrix(p, "Web", E), "Ueb": _gate_matrix(p, "Ueb", H), "beb": np.zeros(3 * H, np.float32)}
+    if transitions:
+        T = transitions
+        w["Utef"] = np.stack([_gate_matrix(p, f"Utef{j}", H) for j in range(T)])
+        w["Uteb"] = np.stack([_gate_matrix(p, f"Uteb{j}", H) for j in range(T)])
+        w["btef"] = rng_for(p, "btef").normal(0.0, 0.1, size=(T, 3 * H)).astype(np.float32)
+        w["bteb"] = rng_for(p, "bteb").normal(0.0, 0.1, size=(T, 3 * H)).astype(np.float32)
+    if layer_norm:
+        r = rng_for(p, "enc_ln")
+        T = transitions
+        for g, b, shape in (("gea", "bea", (2, 3 * H)), ("geu", "beu", (2, 3 * H)), ("gteu", "beteu", (2, T, 3 * H))):
+            if shape[1] == 0:
+                continue
+            w[g] = (1.0 + r.normal(0.0, 0.1, size=shape)).astype(np.float32)
+            w[b] = r.normal(0.0, 0.1, size=shape).astype(np.float32)
     if p.gemm == "bf16":
-        for k in ("semb", "Wef", "Uef", "Web", "Ueb"):
-            w[k] = round_bf16(w[k])
+        for k in ("semb", "Wef", "Uef", "Web", "Ueb", "Utef", "Uteb"):
+            if k in w:
+                w[k] = round_bf16(w[k])
     return w
 
 

@@ -61,6 +61,10 @@ def _load_status(cfg, weights):
     (dict(V=8, k_max=9), mt.MT_ERR_SHAPE),
     (dict(transitions=-1), mt.MT_ERR_SHAPE),
     (dict(transitions=17), mt.MT_ERR_SHAPE),
+    (dict(src_V=100, enc_transitions=-1), mt.MT_ERR_SHAPE),
+    (dict(src_V=100, enc_transitions=17), mt.MT_ERR_SHAPE),
+    (dict(enc_transitions=3), mt.MT_ERR_ARG),  # encoder transition blocks without an encoder
+    (dict(enc_layer_norm=True), mt.MT_ERR_ARG),  # encoder layer norm without an encoder
 ])
 def test_load_weights_rejects_bad_config(kw, status):
     p = synth.PRESETS["tiny_f32"]
@@ -97,6 +101,19 @@ def test_load_weights_rejects_missing_tensors():
     del wd["gtu"]
     rc, _ = _load_status(_cfg(layer_norm=True, transitions=6), wd)
     assert rc == mt.MT_ERR_ARG and "gtu" in mt.lib().mt_last_error().decode()
+    # encoder transition blocks requested but their weights absent
+    p = synth.PRESETS["tiny_f32"]
+    we = {**w, **synth.make_encoder_weights(p, 100, transitions=3)}
+    del we["bteb"]
+    rc, _ = _load_status(_cfg(src_V=100, enc_transitions=3), we)
+    assert rc == mt.MT_ERR_ARG and "bteb" in mt.lib().mt_last_error().decode()
+    we = {**w, **synth.make_encoder_weights(p, 100, transitions=3, layer_norm=True)}
+    del we["beteu"]
+    rc, _ = _load_status(_cfg(src_V=100, enc_transitions=3, enc_layer_norm=True), we)
+    assert rc == mt.MT_ERR_ARG and "beteu" in mt.lib().mt_last_error().decode()
+    del we["geu"]
+    rc, _ = _load_status(_cfg(src_V=100, enc_layer_norm=True), we)
+    assert rc == mt.MT_ERR_ARG and "geu" in mt.lib().mt_last_error().decode()
     # NULL config / weights / out
     L = mt.lib()
     h = C.c_void_p()

@@ -560,18 +560,27 @@ def test_translate_nbest_parity(name, eos):
 # context
 # ------------------------------------------------------------------------------------------
 
-@pytest.mark.parametrize("name,src_V,n_sent", [("tiny_f32", 1000, 99), ("tiny_bf16_ln", 1000, 6),
-                                                ("nematus_f32", 30000, 3), ("nematus_bf16_ln", 30000, 3)])
-def test_encoder_parity(name, src_V, n_sent):
+@pytest.mark.parametrize("name,src_V,n_sent,enc_T,eln", [
+    ("tiny_f32", 1000, 99, 0, False), ("tiny_bf16_ln", 1000, 6, 0, False), ("nematus_f32", 30000, 3, 0, False),
+    ("nematus_bf16_ln", 30000, 3, 0, False), ("tiny_f32", 1000, 99, 3, False), ("tiny_bf16_ln", 1000, 6, 3, False),
+    ("nematus_f32", 30000, 3, 3, False), ("nematus_bf16_ln", 30000, 3, 3, False), ("tiny_f32", 1000, 20, 1, False),
+    ("tiny_f32", 1000, 99, 3, True), ("tiny_f32", 1000, 20, 0, True), ("tiny_bf16_ln", 1000, 6, 3, True),
+    ("nematus_f32", 30000, 3, 3, True), ("nematus_bf16_ln", 30000, 3, 3, True)])
+def test_encoder_parity(name, src_V, n_sent, enc_T, eln):
+    """Encoded context against the oracle's encoder; enc_T > 0: deep-transition cells (an input
+    block and enc_T recurrent-only blocks per direction; the deep model's cell has four); eln:
+    layer norm inside the encoder's blocks."""
     p = synth.PRESETS[name]
-    log(f"\n[encoder] {name} src_V={src_V}")
+    log(f"\n[encoder] {name} src_V={src_V} transitions={enc_T} layer_norm={eln}")
     w = synth.make_weights(p, peaked_bias=True)
-    ew = synth.make_encoder_weights(p, src_V)
+    ew = synth.make_encoder_weights(p, src_V, transitions=enc_T, layer_norm=eln)
     _, mask, lens = synth.make_source(p)
     S = mask.shape[1]
     src = synth.source_tokens(p, src_V, lens, S)
     dec = Decoder(p.E, p.H, p.A, p.V, {**w, **ew}, gemm=p.gemm, layer_norm=p.layer_norm, k_max=max(p.K, 1),
-                  src_V=src_V)
+                  src_V=src_V, enc_transitions=enc_T, enc_layer_norm=eln)
+    trans = tuple(ew[k] for k in synth.ENCODER_TRANSITION_NAMES) if enc_T else None
+    lnp = tuple(ew[k] for k in synth.ENCODER_LN_NAMES if k in ew) if eln else None
     dec.set_source(src, mask, p.K)
     dec.precompute()
     ctx_gpu = dec.ctx.float().cpu().numpy()
@@ -580,12 +589,13 @@ def test_encoder_parity(name, src_V, n_sent):
     tol = TOL[p.gemm]["state"]
     worst = 0.0
     for b in sents:
-        ref = mtref.encode(src[b:b + 1], mask[b:b + 1], *[ew[k] for k in synth.ENCODER_NAMES])
+        ref = mtref.encode(src[b:b + 1], mask[b:b + 1], *[ew[k] for k in synth.ENCODER_NAMES], transitions=trans,
+                           ln=lnp, eps=1e-5)
         L = int(lens[b])
         worst = max(worst, maxerr(ctx_gpu[b, :L], ref[0, :L]))
-    log(f"[encoder] {name}: context max error {worst:.3g} over sentences {sents[:6]}")
+    log(f"[encoder] {name} T={enc_T} LN={eln}: context max error {worst:.3g} over sentences {sents[:6]}")
     assert worst <= tol
-    if name == "tiny_f32":
+    if name == "tiny_f32" and enc_T == 0 and not eln:
         # the step on the encoded context against the oracle's encoder + step
         ctx_o = mtref.encode(src, mask, *[ew[k] for k in synth.ENCODER_NAMES])
         tok, srow, state, score = synth.mid_decode_inputs(p, salt=6)
