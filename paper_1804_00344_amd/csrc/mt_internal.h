@@ -107,11 +107,15 @@ struct List {
 };
 
 // Repeatedly extracts the block-wide best head of the per-thread sorted lists; the
-// winner pops its head.  Writes n results (key bits, idx) through `emit`.
+// winner pops its head.  Writes n <= KMAX results (key bits, idx) through `emit`, called by
+// threads 0..n-1 once the extraction is over: the results wait in LDS, since a global store
+// inside the loop would hold every round's barrier until the store completed.
 template <int KMAX, typename Emit>
 __device__ __forceinline__ void block_extract(List<KMAX> &L, int n, Emit emit) {
   __shared__ float wv[4];
   __shared__ int wi[4];
+  __shared__ float rv[KMAX];
+  __shared__ int ri[KMAX];
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   for (int r = 0; r < n; ++r) {
     float bv = L.v[0];
@@ -131,8 +135,13 @@ __device__ __forceinline__ void block_extract(List<KMAX> &L, int n, Emit emit) {
       if (better(wv[w], wi[w], bv, bi)) { bv = wv[w]; bi = wi[w]; }
     __syncthreads();
     if (L.i[0] == bi && L.v[0] == bv) L.pop();
-    if (t == 0) emit(r, bv, bi);
+    if (t == 0) {
+      rv[r] = bv;
+      ri[r] = bi;
+    }
   }
+  __syncthreads();
+  if (t < n) emit(t, rv[t], ri[t]);
 }
 
 // ---- exact selection by bisection over order-preserving key codes ----

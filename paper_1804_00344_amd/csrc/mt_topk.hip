@@ -290,9 +290,74 @@ __global__ __launch_bounds__(kTT) void topk_scan_logp_kernel(int M, int K, int V
   const float sc = prev_score[m];
   const float *row = logp + (size_t)m * V;
   const int v0 = ch * chunk, v1 = min(V, v0 + chunk);
+  // A wave's K-th largest lane maximum bounds its K best keys from below (K of its keys reach
+  // it), so a key under it is never among the chunk's K best: only keys at or above it enter
+  // the per-thread lists, whose insertions would otherwise dominate.  Both passes form the
+  // key the same way.  Each pass issues kU loads per thread before it uses any of them; a
+  // chunk of at most kU * kTT entries stays in registers between the passes, a longer one is
+  // read again (from cache).
+  constexpr int kU = 16;
+  const bool resident = v1 - v0 <= kU * kTT;
+  uint32_t mx[1] = {0u};
+  float x[kU];
+  for (int b0 = v0; b0 < v1; b0 += kU * kTT) {  // the same trip count for every lane
+    const int base = b0 + threadIdx.x;
+#pragma unroll
+    for (int q = 0; q < kU; ++q) x[q] = base + q * kTT < v1 ? row[base + q * kTT] : 0.f;
+#pragma unroll
+    for (int q = 0; q < kU; ++q)
+      if (base + q * kTT < v1) {
+        const uint32_t c = key_code(sc + x[q]);
+        mx[0] = c > mx[0] ? c : mx[0];
+      }
+  }
+  const uint32_t tau = wave_count_ge<1>(mx, 1, 1u) >= K ? wave_kth_code<1>(mx, 1, K) : 0u;
+  // The keys that pass are appended to a wave-private LDS list (ballot ranks), so each lane
+  // then inserts about one of them into its sorted list: the insertion is straight-line
+  // register code, which would otherwise run for every key.  More than kCap passing keys
+  // (ties at the bound) take the direct route instead.
+  constexpr int kCap = 256;
+  __shared__ float pk[4][kCap];
+  __shared__ int pi[4][kCap];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const uint64_t lt = (1ull << lane) - 1ull;
+  int npass = 0;  // wave-uniform
+  for (int b0 = v0; b0 < v1; b0 += kU * kTT) {  // the same trip count for every lane
+    const int base = b0 + threadIdx.x;
+    if (!resident)
+#pragma unroll
+      for (int q = 0; q < kU; ++q) x[q] = base + q * kTT < v1 ? row[base + q * kTT] : 0.f;
+#pragma unroll
+    for (int q = 0; q < kU; ++q) {
+      const float key = sc + x[q];
+      const bool pass = base + q * kTT < v1 && key_code(key) >= tau;
+      const uint64_t bal = __ballot(pass);
+      const int slot = npass + __popcll(bal & lt);
+      if (pass && slot < kCap) {
+        pk[wv][slot] = key;
+        pi[wv][slot] = base + q * kTT;
+      }
+      npass += __popcll(bal);
+    }
+  }
+  __syncthreads();  // the appended keys are read by other lanes of the wave
   List<KMAX> lst;
   lst.init();
-  for (int v = v0 + threadIdx.x; v < v1; v += kTT) lst.push(sc + row[v], v);
+  if (npass <= kCap) {
+    for (int j = lane; j < npass; j += 64) lst.push(pk[wv][j], pi[wv][j]);
+  } else {
+    for (int b0 = v0; b0 < v1; b0 += kU * kTT) {
+      const int base = b0 + threadIdx.x;
+      if (!resident)
+#pragma unroll
+        for (int q = 0; q < kU; ++q) x[q] = base + q * kTT < v1 ? row[base + q * kTT] : 0.f;
+#pragma unroll
+      for (int q = 0; q < kU; ++q) {
+        const float key = sc + x[q];
+        if (base + q * kTT < v1 && key_code(key) >= tau) lst.push(key, base + q * kTT);
+      }
+    }
+  }
   int2 *o = cand_out + (size_t)m * K * nch + ch;  // entry r at o[r * nch] (entry-major per row)
   block_extract<KMAX>(lst, K, [&](int r, float v, int i) { o[(size_t)r * nch] = make_int2(__float_as_int(v), i); });
 }

@@ -305,8 +305,10 @@ def test_tiny_trajectory(name, anchor):
 # top-K on given log-probabilities: bit-exact against the oracle's full sort
 # ------------------------------------------------------------------------------------------
 
-@pytest.mark.parametrize("K,V", [(1, 16), (2, 7), (3, 1000), (5, 85000), (12, 50000), (16, 50000), (16, 16), (4, 2049)])
+@pytest.mark.parametrize("K,V", [(1, 16), (2, 7), (3, 1000), (5, 85000), (12, 50000), (16, 50000), (16, 16), (4, 2049),
+                                 (2, 300000)])
 def test_topk_given_logp_bit_exact(K, V):
+    """V = 300000 makes the first level's chunks longer than its register-resident size."""
     log(f"\n[topk] K={K} V={V}")
     B = 6
     rng = np.random.default_rng(K * 1000 + V)
