@@ -108,8 +108,7 @@ struct List {
 
 // Repeatedly extracts the block-wide best head of the per-thread sorted lists; the
 // winner pops its head.  Writes n <= KMAX results (key bits, idx) through `emit`, called by
-// threads 0..n-1 once the extraction is over: the results wait in LDS, since a global store
-// inside the loop would hold every round's barrier until the store completed.
+// threads 0..n-1 once the extraction is over (the results wait in LDS meanwhile).
 template <int KMAX, typename Emit>
 __device__ __forceinline__ void block_extract(List<KMAX> &L, int n, Emit emit) {
   __shared__ float wv[4];
