@@ -606,6 +606,35 @@ def test_encoder_parity(name, src_V, n_sent, enc_T, eln):
         compare_rows(p, gpu, orc, sents, TOL[p.gemm], name + "_encoded")
 
 
+@pytest.mark.parametrize("S,lens,enc_T,eln", [(1, [1, 1, 1], 3, True), (7, [1, 7, 2, 5], 3, True),
+                                               (7, [1, 7, 2, 5], 0, False), (5, [5], 1, False),
+                                               (9, [3, 9, 1, 9, 4, 2], 2, True)])
+def test_encoder_edge_shapes(S, lens, enc_T, eln):
+    """Single-position sources, one-token sentences beside full ones, a single sentence:
+    every position of the context, padded ones included (the forward state carried, the
+    backward state zero), against the oracle's encoder."""
+    p = synth.PRESETS["tiny_f32"]
+    src_V = 50
+    log(f"\n[encoder edge] S={S} lens={lens} transitions={enc_T} layer_norm={eln}")
+    w = synth.make_weights(p, peaked_bias=True)
+    ew = synth.make_encoder_weights(p, src_V, transitions=enc_T, layer_norm=eln)
+    lens = np.asarray(lens)
+    mask = (np.arange(S)[None, :] < lens[:, None]).astype(np.float32)
+    src = synth.source_tokens(p, src_V, lens, S)
+    dec = Decoder(p.E, p.H, p.A, p.V, {**w, **ew}, gemm=p.gemm, layer_norm=p.layer_norm, k_max=max(p.K, 1),
+                  src_V=src_V, enc_transitions=enc_T, enc_layer_norm=eln)
+    dec.set_source(src, mask, p.K)
+    got = dec.ctx.float().cpu().numpy()
+    assert mt.mt_device_errors(dec.model) == 0
+    trans = tuple(ew[k] for k in synth.ENCODER_TRANSITION_NAMES) if enc_T else None
+    lnp = tuple(ew[k] for k in synth.ENCODER_LN_NAMES if k in ew) if eln else None
+    ref = mtref.encode(src, mask, *[ew[k] for k in synth.ENCODER_NAMES], transitions=trans, ln=lnp, eps=1e-5)
+    err = maxerr(got, ref)
+    log(f"[encoder edge] max error {err:.3g}")
+    assert err <= TOL["f32"]["state"]
+    assert np.all(got[:, :, p.H:][mask == 0] == 0)
+
+
 # ------------------------------------------------------------------------------------------
 # dual-source steps: a second source with its own attention; GRU 2 and the readout take both
 # contexts
