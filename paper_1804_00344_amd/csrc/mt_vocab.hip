@@ -76,6 +76,7 @@ struct VocabArgs {
   int cap;
   float *logits;        // [M][logits_ld] or NULL
   int logits_ld;
+  int logits_vec;       // 16-byte aligned rows (base aligned, logits_ld % 4 == 0): float4 stores
   int fixed_ref;        // logits proven bounded: log-sum-exp without a running maximum
 };
 
@@ -353,13 +354,22 @@ __global__ __launch_bounds__((VShape<CT, HB>::NT)) void vocab_kernel(VocabArgs a
           }
         }
         if (LOG && h < a.M) {
+          // a lane's four consecutive entries v..v+3 go out as one 16-byte store where the
+          // row layout allows it
           float *lrowp = a.logits + (size_t)h * a.logits_ld;
 #pragma unroll
           for (int i = 0; i < NB; ++i)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-              const int v = v0 + 32 * i + 8 * (r >> 2) + 4 * lhalf + (r & 3);
-              if (v < a.V && v < a.logits_ld) lrowp[v] = acc[i][j][r];
+            for (int q = 0; q < 4; ++q) {
+              const int vb = v0 + 32 * i + 8 * q + 4 * lhalf;
+              if (a.logits_vec && vb + 3 < a.V) {
+                *(float4 *)(lrowp + vb) =
+                    make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+              } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                  if (vb + e < a.V && vb + e < a.logits_ld) lrowp[vb + e] = acc[i][j][4 * q + e];
+              }
             }
         }
       }
@@ -590,6 +600,7 @@ hipError_t launch_vocab(int bf16_mma, const void *t, const void *wp, const float
   a.cap = cap;
   a.logits = logits;
   a.logits_ld = V;
+  a.logits_vec = logits && ((uintptr_t)logits & 15) == 0 && V % 4 == 0;
   a.fixed_ref = fixed_ref;
   return vgo_any(bf16_mma, a, st);
 }
