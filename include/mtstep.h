@@ -239,8 +239,6 @@ mt_status mt_beam_topk(mt_model *model, int B, int K, const float *prev_score, c
                        float *score_out, int32_t *tok_out, int32_t *bp_out, int32_t *row_out,
                        void *ws, size_t ws_bytes, void *stream);
 
-/* Reads and clears the device-side error bits (synchronises the device):
- * bit 0 = a prev_tok out of range, bit 1 = a src_row out of range. */
 /* Ensemble of n models decoding the same beams (Section 2.3: ensembling of models as a
  * meta-algorithm of batched beam search).  Each member runs its own mt_decoder_step on the
  * shared tokens and state rows (its own states) with logp_out given; this call combines
@@ -275,7 +273,17 @@ mt_status mt_beam_finish(mt_model *model, int B, int K, int step, int32_t eos, f
                          int32_t *fin_count, int32_t *hist_tok, int32_t *hist_bp, float *fin_score,
                          float *fin_norm, int32_t *fin_step, int32_t *fin_parent, int32_t *fin_tok, void *stream);
 
+/* Reads and clears the device-side error bits (synchronises the device):
+ * bit 0 = a prev_tok out of range, bit 1 = a src_row out of range, bit 3 = a source token of
+ * mt_encode out of range. */
 mt_status mt_device_errors(mt_model *model, int32_t *flags);
+
+/* Reads and clears (synchronises the device) the number of hypothesis rows that mt_beam_topk,
+ * selecting from the candidates its preceding mt_decoder_step left in the workspace (logp =
+ * NULL), recomputed exactly from the weights because their candidates did not fit the
+ * workspace lists (or fell short of K), since the last call.  A diagnostic of the fused
+ * selection (Section 2.3, batched beam search): the result is exact either way. */
+mt_status mt_recomputed_rows(mt_model *model, int64_t *rows);
 
 /* Kernel timing with HIP events recorded on the launch stream around each
  * launch of the selected kernel classes (bit k of kernel_mask selects
@@ -306,6 +314,12 @@ typedef enum {
 mt_status mt_profile_enable(mt_model *model, uint32_t kernel_mask);
 mt_status mt_profile_reset(mt_model *model);
 mt_status mt_profile_query(mt_model *model, int kernel, double *total_ms, int64_t *launches);
+
+/* The fp32 -> bf16 conversion that mt_load_weights applies to every matrix of a bf16 model
+ * (gemm_dtype = MT_BF16): dst[i] = the bf16 bit pattern nearest to src[i], ties to even; a NaN
+ * stays a quiet NaN, +-inf stay infinite, a value rounding past the largest finite bf16
+ * becomes +-inf.  HOST pointers; needs no device; n = 0 or a NULL pointer does nothing. */
+void mt_round_bf16(const float *src, uint16_t *dst, size_t n);
 
 /* Message of the last failed call on this thread ("" if none). */
 const char *mt_last_error(void);

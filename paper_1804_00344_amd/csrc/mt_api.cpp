@@ -88,6 +88,7 @@ struct mt_model {
   float *btr = nullptr;           // [T][3H] their biases
   float *gtu = nullptr, *betu = nullptr;  // [T][3H] layer norm of their recurrent products
   int32_t *err;
+  unsigned long long *nrecompute;  // rows whose fused candidates were recomputed exactly
   std::vector<void *> allocs;
   // call-order state for mt_beam_topk(logp = NULL)
   int last_B = -1, last_K = -1;
@@ -135,13 +136,7 @@ mt_status check_cfg(const mt_config *c) {
   return MT_OK;
 }
 
-uint16_t bf16_bits(float f) {  // round to nearest even, NaN stays a quiet NaN
-  uint32_t u;
-  std::memcpy(&u, &f, 4);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
-}
+uint16_t bf16_bits(float f) { return bf16_rne_bits(f); }
 
 struct Seg {
   const float *w;  // logical [K][ncols] row-major
@@ -364,6 +359,11 @@ extern "C" {
 
 const char *mt_last_error(void) { return g_err; }
 
+void mt_round_bf16(const float *src, uint16_t *dst, size_t n) {
+  if (!src || !dst) return;
+  for (size_t i = 0; i < n; ++i) dst[i] = bf16_rne_bits(src[i]);
+}
+
 mt_status mt_load_weights(const mt_config *cfg, const mt_weights *w, mt_model **out) {
   g_err[0] = 0;
   if (!out) return fail(MT_ERR_ARG, "out is NULL");
@@ -543,6 +543,8 @@ mt_status mt_load_weights(const mt_config *cfg, const mt_weights *w, mt_model **
     }
     int32_t zero = 0;
     CHECK(dev_upload(m, &zero, sizeof zero, (void **)&m->err));
+    unsigned long long zero64 = 0;
+    CHECK(dev_upload(m, &zero64, sizeof zero64, (void **)&m->nrecompute));
     {
       // The token side of GRU 1 and of the readout, x [W1 | Wt_y] + [b1 | 0], depends only on
       // the token: it is computed once here for the whole vocabulary (same products, same
@@ -1011,6 +1013,7 @@ mt_status mt_beam_topk(mt_model *model, int B, int K, const float *prev_score, c
   rs.row_cand = rowc;
   rs.scnt = (int *)(W + L.scnt);
   rs.score_out = score_out; rs.tok_out = tok_out; rs.bp_out = bp_out; rs.row_out = row_out;
+  rs.nrecompute = model->nrecompute;
   if (!logp) {
     rs.nl = L.ntiles * vocab_lists(); rs.cap = kVocabCap;
     rs.cnt = (const int *)(W + L.ccnt); rs.cbuf = (const int2 *)(W + L.cbuf);
@@ -1083,6 +1086,18 @@ mt_status mt_device_errors(mt_model *model, int32_t *flags) {
   HIP_TRY(hipDeviceSynchronize());
   HIP_TRY(hipMemcpy(flags, model->err, 4, hipMemcpyDeviceToHost));
   HIP_TRY(hipMemset(model->err, 0, 4));
+  return MT_OK;
+}
+
+mt_status mt_recomputed_rows(mt_model *model, int64_t *rows) {
+  g_err[0] = 0;
+  if (!valid_model(model)) return fail(MT_ERR_ARG, "invalid model handle");
+  if (!rows) return fail(MT_ERR_ARG, "rows is NULL");
+  unsigned long long n = 0;
+  HIP_TRY(hipDeviceSynchronize());
+  HIP_TRY(hipMemcpy(&n, model->nrecompute, sizeof n, hipMemcpyDeviceToHost));
+  HIP_TRY(hipMemset(model->nrecompute, 0, sizeof n));
+  *rows = (int64_t)n;
   return MT_OK;
 }
 

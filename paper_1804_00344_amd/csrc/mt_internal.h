@@ -52,6 +52,17 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
+// Host-side fp32 -> bf16 bits, round to nearest with ties to even (the weight packing of every
+// bf16 model uses it): a NaN stays a quiet NaN (its payload's top bits kept, the quiet bit set),
+// +-inf stay infinite, values that round past the largest finite bf16 become +-inf.
+inline uint16_t bf16_rne_bits(float f) {
+  uint32_t u;
+  __builtin_memcpy(&u, &f, 4);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
 // bf16 <-> fp32, round to nearest even (NaN kept quiet)
 __device__ __forceinline__ bf16 to_bf16(float f) { return (bf16)f; }
 __device__ __forceinline__ float to_f32(bf16 h) { return (float)h; }
@@ -519,6 +530,7 @@ struct RowSelect {
   int *scnt;
   float *score_out;
   int32_t *tok_out, *bp_out, *row_out;
+  unsigned long long *nrecompute;  // optional: counts the rows recomputed exactly
 };
 hipError_t launch_row_select(const RowSelect &a, hipStream_t st);
 // Block (0, 0) also clears the B sentence arrival counters scnt.

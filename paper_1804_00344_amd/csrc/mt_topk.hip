@@ -177,7 +177,10 @@ __global__ __launch_bounds__(kTT) void row_select_kernel(RowSelect a) {
     }
     if (any_over || N > kRowCap || (cr && N < K)) {
       // the candidates do not fit (or fall short of K): exact recomputation of the row
-      if (fused) row_recompute<CT, KMAX>(a.vv, m, K, L, sc, emit_row);
+      if (fused) {
+        if (t == 0 && a.nrecompute) atomicAdd(a.nrecompute, 1ull);
+        row_recompute<CT, KMAX>(a.vv, m, K, L, sc, emit_row);
+      }
     } else {
       // ---- stage the candidates as (key code, token) in LDS ----
       auto stage = [&](int pos, int2 v) {

@@ -480,14 +480,7 @@ void vocab_pack_host(int bf16_mma, int V, int E, const float *src, int src_is_em
           if (v < V) x = src_is_emb ? src[(size_t)v * E + k] : src[(size_t)k * V + v];
           const size_t o = (((size_t)vb * KS + ks) * 64 + l) * epv + j;
           if (bf16_mma) {
-            uint32_t u;
-            __builtin_memcpy(&u, &x, 4);
-            uint16_t hbits;
-            if ((u & 0x7fffffffu) > 0x7f800000u)
-              hbits = (uint16_t)((u >> 16) | 0x40u);
-            else
-              hbits = (uint16_t)((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
-            ((uint16_t *)out)[o] = hbits;
+            ((uint16_t *)out)[o] = bf16_rne_bits(x);
           } else {
             ((float *)out)[o] = x;
           }

@@ -90,12 +90,25 @@ def lib() -> C.CDLL:
         L.mt_profile_enable.argtypes = [_vp, C.c_uint32]
         L.mt_profile_reset.argtypes = [_vp]
         L.mt_profile_query.argtypes = [_vp, C.c_int, C.POINTER(C.c_double), C.POINTER(C.c_int64)]
+        L.mt_recomputed_rows.argtypes = [_vp, C.POINTER(C.c_int64)]
+        L.mt_recomputed_rows.restype = C.c_int
+        L.mt_round_bf16.argtypes = [_vp, _vp, C.c_size_t]
+        L.mt_round_bf16.restype = None
         for f in ("mt_load_weights", "mt_free", "mt_precompute_ctx", "mt_decoder_step", "mt_beam_topk",
                   "mt_ensemble_logp", "mt_beam_finish", "mt_encode", "mt_precompute_keys2", "mt_decoder_step_dual",
                   "mt_device_errors", "mt_profile_enable", "mt_profile_reset", "mt_profile_query"):
             getattr(L, f).restype = C.c_int
         _lib = L
     return _lib
+
+
+def mt_round_bf16(x: np.ndarray) -> np.ndarray:
+    """bf16 bit patterns (uint16) of fp32 values, as mt_load_weights converts a bf16 model's
+    matrices (host memory, no device)."""
+    src = np.ascontiguousarray(x, np.float32)
+    dst = np.empty(src.shape, np.uint16)
+    lib().mt_round_bf16(src.ctypes.data, dst.ctypes.data, src.size)
+    return dst
 
 
 def _check(rc: int):
@@ -246,6 +259,12 @@ def mt_device_errors(model: Model) -> int:
     f = C.c_int32(0)
     _check(lib().mt_device_errors(model.handle, C.byref(f)))
     return int(f.value)
+
+
+def mt_recomputed_rows(model: Model) -> int:
+    n = C.c_int64(0)
+    _check(lib().mt_recomputed_rows(model.handle, C.byref(n)))
+    return int(n.value)
 
 
 def mt_profile_enable(model: Model, kernels=("VOCAB_GEMM",)):

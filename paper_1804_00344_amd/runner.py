@@ -233,35 +233,23 @@ class Ensemble:
     def set_batch(self, ctx: np.ndarray, mask: np.ndarray, K: int):
         for d in self.members:
             d.set_batch(ctx, mask, K)
+        self._alloc_logp()
+
+    def _alloc_logp(self):
         lead = self.lead
         self.logp = [torch.empty((lead.M, lead.V), dtype=torch.float32, device=lead.device) for _ in self.members]
         self.comb = torch.empty((lead.M, lead.V), dtype=torch.float32, device=lead.device)
 
     def set_source(self, src_tok: np.ndarray, mask: np.ndarray, K: int, stream=None):
-        """Batch from source tokens: the context comes from the model's encoder (mt_encode)."""
-        B, S = src_tok.shape
-        self.set_batch(np.zeros((1, 1, self.C), np.float32), np.ones((1, 1), np.float32), K)  # buffers of the right kind
-        d = self.device
-        self.B, self.S, self.K, self.M = B, S, K, B * K
-        self.src_tok = torch.from_numpy(np.ascontiguousarray(src_tok, np.int32)).to(d)
-        self.mask = torch.from_numpy(np.ascontiguousarray(mask, np.float32)).to(d)
-        self.ctx = torch.empty((B, S, self.C), dtype=self.io_dtype, device=d)
-        self.pctx = torch.empty((B, S, self.A), dtype=self.io_dtype, device=d)
-        self.s0 = torch.empty((B, self.H), dtype=torch.float32, device=d)
-        nbytes = mt.mt_workspace_bytes(self.model, B, K, S)
-        self.ws = torch.empty(nbytes, dtype=torch.uint8, device=d)
-        self.ews = torch.empty(mt.mt_encode_workspace_bytes(self.model, B, S), dtype=torch.uint8, device=d)
-        M = self.M
-        self.state = [torch.empty((M, self.H), dtype=torch.float32, device=d) for _ in range(2)]
-        self.tok = torch.empty(M, dtype=torch.int32, device=d)
-        self.row = torch.empty(M, dtype=torch.int32, device=d)
-        self.bp = torch.empty(M, dtype=torch.int32, device=d)
-        self.score = torch.empty(M, dtype=torch.float32, device=d)
-        self.cur = 0
-        self.encode(stream=stream)
+        """Batch from source tokens: every member encodes them with its own encoder (mt_encode)
+        into its own context, as each member of an ensemble has its own encoder."""
+        for d in self.members:
+            d.set_source(src_tok, mask, K, stream=stream)
+        self._alloc_logp()
 
     def encode(self, stream=None):
-        mt.mt_encode(self.model, self.B, self.S, self.src_tok, self.mask, self.ctx, self.ews, stream=stream)
+        for d in self.members:
+            d.encode(stream=stream)
 
     def precompute(self, stream=None):
         for d in self.members:

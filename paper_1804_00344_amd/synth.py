@@ -126,8 +126,10 @@ GEMM_OPERANDS = ("emb", "W1", "U1", "Ua", "Wa", "W2", "U2", "Wt_s", "Wt_y", "Wt_
 TRANSITION_NAMES = ("Ut", "btr", "gtu", "betu")  # stacked over the transition blocks
 
 
-def make_weights(p: Preset, peaked_bias: bool = False) -> Dict[str, np.ndarray]:
-    """All model parameters, fp32, row-major logical [in x out]."""
+def make_weights(p: Preset, peaked_bias: bool = False, round_operands: bool = True) -> Dict[str, np.ndarray]:
+    """All model parameters, fp32, row-major logical [in x out].  round_operands=False keeps
+    a bf16 preset's matrices as drawn (fp32 masters), leaving the bf16 conversion to the
+    consumer."""
     E, H, C, A, V = p.E, p.H, p.C, p.A, p.V
     w: Dict[str, np.ndarray] = {}
     w["emb"] = rng_for(p, "emb").normal(0.0, 0.1, size=(V, E)).astype(np.float32)
@@ -171,7 +173,7 @@ def make_weights(p: Preset, peaked_bias: bool = False) -> Dict[str, np.ndarray]:
                                  for j in range(T)])
             w["betu"] = np.stack([rng_for(p, f"betu{j}").normal(0, 0.05, 3 * H).astype(np.float32)
                                   for j in range(T)])
-    if p.gemm == "bf16":
+    if p.gemm == "bf16" and round_operands:
         for k in GEMM_OPERANDS:
             if k in w:
                 w[k] = round_bf16(w[k])
@@ -191,14 +193,15 @@ def source_lengths(p: Preset, B: Optional[int] = None) -> np.ndarray:
     return L.astype(np.int32)
 
 
-def make_source(p: Preset, nan_padding: bool = False):
-    """Encoder output stand-in: (ctx [B,S,C] fp32, mask [B,S] fp32 0/1, lens [B])."""
+def make_source(p: Preset, nan_padding: bool = False, round_operands: bool = True):
+    """Encoder output stand-in: (ctx [B,S,C] fp32, mask [B,S] fp32 0/1, lens [B]);
+    round_operands=False keeps a bf16 preset's context as drawn."""
     lens = source_lengths(p)
     S = int(p.len_b) if p.len_dist == "uniform" else int(lens.max())
     S = max(S, int(lens.max()))
     ctx = rng_for(p, "ctx").normal(0.0, 1.0, size=(p.B, S, p.C)).astype(np.float32)
     mask = (np.arange(S)[None, :] < lens[:, None]).astype(np.float32)
-    if p.gemm == "bf16":
+    if p.gemm == "bf16" and round_operands:
         ctx = round_bf16(ctx)
     if nan_padding:
         ctx = ctx.copy()

@@ -41,15 +41,19 @@ def oracle_sentences(om: mtref.Model, K: int, sents: Sequence[int], ctx, mask, t
                      src2=None):
     """Runs the oracle's precompute + one step on each sampled sentence separately.
 
-    state_in rows for sentence b are the K rows b*K..b*K+K-1 (mid-decode), or with
-    start=True the oracle's own start state of the sentence (src_row = m // K)."""
+    state_in rows for sentence b are the K rows b*K..b*K+K-1 (mid-decode); with start=True
+    the oracle's own start state of the sentence (src_row = m // K); with start="given",
+    state_in holds one start state per sentence [B, H] (the GPU's, src_row = m // K)."""
 
     def one(b):
         c = ctx[b:b + 1]
         m = mask[b:b + 1]
         P, s0 = om.precompute(c, m)
         rows = slice(b * K, (b + 1) * K)
-        if start:
+        if isinstance(start, str) and start == "given":
+            st = state_in[b:b + 1]
+            sr = np.zeros(K, np.int32)
+        elif start:
             st = s0
             sr = np.zeros(K, np.int32)
         else:
@@ -70,26 +74,39 @@ def oracle_sentences(om: mtref.Model, K: int, sents: Sequence[int], ctx, mask, t
 def topk_gap_check(K: int, score: np.ndarray, logp_oracle: np.ndarray, g_score, g_tok, g_bp, tau: float):
     """Gap rule for one sentence: slot j is decided iff its oracle candidate is separated from
     both neighbours in the oracle's sorted order by more than 2*tau.  Decided slots must match
-    bit-exactly in token and backpointer; every slot's score within tau (+1 ulp).
-    Returns (n_decided, n_slots)."""
+    bit-exactly in token and backpointer; every slot's score within tau (+1 ulp) of the
+    oracle's j-th best.  Where several results are correct (undecided slots) the GPU's must be
+    valid: its K (backpointer, token) pairs are distinct, and the oracle's own candidate at each
+    of them is within tau (+1 ulp) of the GPU's score, so each pick is one of the oracle's
+    near-best candidates and carries its score.  Returns (n_decided, n_slots)."""
     V = logp_oracle.shape[1]
     cand = (score[:, None].astype(np.float32) + logp_oracle.astype(np.float32)).astype(np.float32).reshape(-1)
     n = min(K + 1, cand.size)
     part = np.argpartition(-cand, n - 1)[:n] if n < cand.size else np.arange(cand.size)
     order = part[np.lexsort((part, -cand[part]))]
     o = cand[order].astype(np.float64)
+    ulp = lambda x: abs(x) * 2.0 ** -23
     decided = 0
+    pairs = set()
     for j in range(K):
         prev_ok = j == 0 or (o[j - 1] - o[j] > 2 * tau)
         next_ok = (j + 1 >= len(o)) or (o[j] - o[j + 1] > 2 * tau)
+        gs = float(g_score[j])
         if math.isfinite(o[j]):
-            assert abs(float(g_score[j]) - o[j]) <= tau + abs(o[j]) * 2.0 ** -23, (j, g_score[j], o[j])
+            assert abs(gs - o[j]) <= tau + ulp(o[j]), (j, gs, o[j])
         else:
-            assert g_score[j] == o[j]
+            assert gs == o[j]
+        gt, gb = int(g_tok[j]), int(g_bp[j])
+        assert 0 <= gt < V and 0 <= gb < K, (j, gt, gb)
+        if math.isfinite(gs):
+            assert (gb, gt) not in pairs, ("repeated (bp, tok)", j, gb, gt)
+            pairs.add((gb, gt))
+            ok = float(cand[gb * V + gt])
+            assert abs(ok - gs) <= tau + ulp(ok), ("oracle key at the GPU's pick", j, gb, gt, ok, gs)
         if prev_ok and next_ok:
             decided += 1
-            assert int(g_tok[j]) == int(order[j] % V) and int(g_bp[j]) == int(order[j] // V), (
-                j, int(g_tok[j]), int(g_bp[j]), int(order[j] % V), int(order[j] // V))
+            assert gt == int(order[j] % V) and gb == int(order[j] // V), (
+                j, gt, gb, int(order[j] % V), int(order[j] // V))
     return decided, K
 
 

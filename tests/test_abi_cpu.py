@@ -1,6 +1,7 @@
 """C-ABI checks that need no GPU: the library loads, exports every declared entry
 point, and rejects bad arguments on the host before touching the device."""
 import ctypes as C
+import math
 import os
 import re
 
@@ -17,7 +18,7 @@ HEADER = os.path.join(ROOT, "include", "mtstep.h")
 def declared_functions():
     src = open(HEADER).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(mt_[a-z_]+)\s*\(", src)))
+    return sorted(set(re.findall(r"\b(mt_[a-z0-9_]+)\s*\(", src)))
 
 
 def test_header_declares_the_four_calls():
@@ -136,3 +137,70 @@ def test_calls_reject_invalid_handles():
     junk = (C.c_uint32 * 64)()
     assert L.mt_profile_enable(C.cast(junk, C.c_void_p), 1) == mt.MT_ERR_ARG
     assert "invalid model handle" in L.mt_last_error().decode()
+
+
+# ------------------------------------------------------------------------------------------
+# the fp32 -> bf16 conversion that mt_load_weights applies to a bf16 model's matrices
+# ------------------------------------------------------------------------------------------
+
+def _nearest_bf16_exact(x: float):
+    """Nearest bf16 value to a finite fp32 value by exact rational arithmetic over the two
+    bf16 neighbours (ties to the one with an even significand); None if it overflows."""
+    from fractions import Fraction
+    if x == 0.0:
+        return math.copysign(0.0, x)
+    sign = -1 if x < 0 else 1
+    a = Fraction(abs(x))
+    e = math.frexp(abs(x))[1] - 1          # 2^e <= |x| < 2^(e+1)
+    e = max(e, -126)                        # subnormal range shares the smallest exponent
+    ulp = Fraction(2) ** (e - 7)            # 8 significand bits (7 stored)
+    lo = (a // ulp) * ulp
+    hi = lo + ulp
+    if a - lo < hi - a:
+        r = lo
+    elif hi - a < a - lo:
+        r = hi
+    else:                                   # exact tie: the even multiple of ulp
+        r = lo if (lo / ulp) % 2 == 0 else hi
+    if r > Fraction(2) ** 127 * (2 - Fraction(2) ** -7):
+        return None
+    return sign * float(r)
+
+
+def _bf16_value(bits: int) -> float:
+    return float(np.array([bits << 16], np.uint32).view(np.float32)[0])
+
+
+def test_bf16_conversion_round_to_nearest_even():
+    one = 1.0
+    cases = [
+        one + 2.0 ** -8,                    # halfway between 1 and 1 + 2^-7: ties to even -> 1
+        one + 3 * 2.0 ** -8,                # halfway, odd neighbour below -> rounds up to 1 + 2^-6
+        one + 2.0 ** -8 + 2.0 ** -20,       # just above the tie -> up
+        -(one + 2.0 ** -8),                 # the sign does not change the rule
+        3.140625, 1e-40, -1e-42, 2.0 ** -133,  # exact, subnormals
+        float(np.float32(3.3895313892515355e38)),  # the largest finite bf16
+        0.0, -0.0, 65504.0, 1.0e-3, 123456.7,
+    ]
+    x = np.array(cases, np.float32)
+    got = mt.mt_round_bf16(x)
+    for xi, gi in zip(x.tolist(), got.tolist()):
+        want = _nearest_bf16_exact(float(np.float32(xi)))
+        assert want is not None
+        g = _bf16_value(gi)
+        assert g == want and math.copysign(1.0, g) == math.copysign(1.0, want), (xi, hex(gi), g, want)
+    rng = np.random.default_rng(12)
+    r = (rng.standard_normal(2000) * np.exp(rng.uniform(-30, 30, 2000))).astype(np.float32)
+    for xi, gi in zip(r.tolist(), mt.mt_round_bf16(r).tolist()):
+        assert _bf16_value(gi) == _nearest_bf16_exact(xi), xi
+
+
+def test_bf16_conversion_special_values():
+    bits = np.array([0x7F800000, 0xFF800000, 0x7FC00000, 0x7F800001, 0xFF800123, 0x7F7FFFFF, 0xFF7FFFFF],
+                    np.uint32)
+    got = mt.mt_round_bf16(bits.view(np.float32)).tolist()
+    assert got[0] == 0x7F80 and got[1] == 0xFF80            # +-inf stay infinite
+    for g in got[2:5]:                                      # NaNs stay NaN (quiet), never inf
+        assert (g & 0x7F80) == 0x7F80 and (g & 0x7F) != 0 and (g & 0x40)
+    assert got[4] & 0x8000                                  # a negative NaN keeps its sign
+    assert got[5] == 0x7F80 and got[6] == 0xFF80            # the largest floats round past bf16 -> inf

@@ -492,6 +492,95 @@ def test_full_step_equals_torch_reexpression():
         assert np.max(np.abs(out["logp"][m] - lp.numpy())) <= 1e-5
 
 
+# --------------------------------------------------------------------------------------
+# layer-norm wiring of the whole step (layer normalisation inside the GRU blocks and on the
+# readout, Section 3.1.1): each gate block of each path of both GRUs is normalised with its
+# own gain/shift set, and the summed readout pre-activation is normalised before the tanh
+# --------------------------------------------------------------------------------------
+
+
+def torch_ln_gru(x, h, W, U, b, ga, ba, gu, bu, eps=1e-5):
+    """GRU block with per-gate-block layer norm on both paths, written with F.layer_norm in
+    float64: a = LN_g(x W + b), u = LN_g(h U) per block g in (r, z, h), then the usual
+    r, z, candidate and convex update."""
+    T64 = lambda v: torch.from_numpy(np.asarray(v, np.float64))
+    H = h.size
+    a = T64(x) @ T64(W) + T64(b)
+    u = T64(h) @ T64(U)
+    an = [F.layer_norm(a[g * H:(g + 1) * H], (H,), T64(ga[g * H:(g + 1) * H]), T64(ba[g * H:(g + 1) * H]), eps)
+          for g in range(3)]
+    un = [F.layer_norm(u[g * H:(g + 1) * H], (H,), T64(gu[g * H:(g + 1) * H]), T64(bu[g * H:(g + 1) * H]), eps)
+          for g in range(3)]
+    r = torch.sigmoid(an[0] + un[0])
+    z = torch.sigmoid(an[1] + un[1])
+    n = torch.tanh(an[2] + r * un[2])
+    return ((1 - z) * n + z * T64(h)).numpy()
+
+
+def test_ln_step_equals_torch_reexpression():
+    """The layer-norm step against float64 torch: F.layer_norm on each of the three gate blocks
+    of the input and recurrent paths of GRU 1 (g1a/be1a, g1u/be1u) and GRU 2 (g2a/be2a,
+    g2u/be2u), and on the summed readout pre-activation (gt/bet) before the tanh.  A swapped
+    parameter set, a dropped readout norm or a norm after the tanh all fail it."""
+    model, w = tiny_model(seed=90, layer_norm=True)
+    ctx, mask, lens, tok, src, state = tiny_batch(seed=91)
+    P, _ = model.precompute(ctx, mask)
+    out = model.step(2, tok, src, state, ctx, P, mask, want_alpha=True, taps=True)
+    T64 = lambda a: torch.from_numpy(np.asarray(a, np.float64))
+    eps = 1e-5
+    for m in range(tok.size):
+        b = m // 2
+        x = w["emb"][tok[m]]
+        s1 = torch_ln_gru(x, state[src[m]], w["W1"], w["U1"], w["b1"], w["g1a"], w["be1a"], w["g1u"], w["be1u"])
+        assert np.max(np.abs(out["s1"][m] - s1)) <= 1e-6
+        q = T64(s1) @ T64(w["Wa"])
+        e = torch.tanh(T64(P[b]) + q) @ T64(w["va"])
+        e = e.masked_fill(T64(mask[b]) == 0, -math.inf)
+        c = torch.softmax(e, 0) @ T64(ctx[b])
+        s = torch_ln_gru(c.numpy(), s1, w["W2"], w["U2"], w["b2"], w["g2a"], w["be2a"], w["g2u"], w["be2u"])
+        assert np.max(np.abs(out["state"][m] - s)) <= 1e-6
+        pre = T64(s) @ T64(w["Wt_s"]) + T64(x) @ T64(w["Wt_y"]) + c @ T64(w["Wt_c"]) + T64(w["bt"])
+        t = torch.tanh(F.layer_norm(pre, (E_,), T64(w["gt"]), T64(w["bet"]), eps))
+        assert np.max(np.abs(out["t"][m] - t.numpy())) <= 1e-6
+        lp = torch.log_softmax(t @ T64(w["Wo"]) + T64(w["bo"]), 0)
+        assert np.max(np.abs(out["logp"][m] - lp.numpy())) <= 1e-5
+
+
+def test_ln_step_zero_readout_gain_gives_tanh_of_shift():
+    """gt = 0: the normalised readout pre-activation is exactly its shift, so every row's
+    readout is t = tanh(bet), whatever the state, context and token."""
+    _, w0 = tiny_model(seed=92, layer_norm=True)
+    bet = w0["bet"]
+    model, w = tiny_model(seed=92, layer_norm=True, gt=np.zeros(E_, np.float32))
+    ctx, mask, lens, tok, src, state = tiny_batch(seed=93)
+    P, _ = model.precompute(ctx, mask)
+    out = model.step(2, tok, src, state, ctx, P, mask, taps=True)
+    ref = np.tanh(bet.astype(np.float64)).astype(np.float32)
+    for m in range(tok.size):
+        assert np.max(np.abs(out["t"][m] - ref)) == 0.0
+    # and the log-probabilities are then the same for every row
+    assert np.max(np.abs(out["logp"] - out["logp"][0:1])) == 0.0
+
+
+def test_ln_step_parameter_sets_are_not_interchangeable():
+    """Exchanging GRU 1's layer-norm sets (g1a, be1a, g1u, be1u) with GRU 2's changes the new
+    state, and so does exchanging the input-path and recurrent-path sets of one GRU: each of
+    the four sets acts where the step says."""
+    model, w = tiny_model(seed=94, layer_norm=True)
+    ctx, mask, lens, tok, src, state = tiny_batch(seed=95)
+    P, _ = model.precompute(ctx, mask)
+    ref = model.step(2, tok, src, state, ctx, P, mask)["state"]
+    swaps = [{"g1a": "g2a", "be1a": "be2a", "g1u": "g2u", "be1u": "be2u"},
+             {"g1a": "g1u", "be1a": "be1u"}, {"g2a": "g2u", "be2a": "be2u"}]
+    for sw in swaps:
+        w2 = dict(w)
+        for a, b in sw.items():
+            w2[a], w2[b] = w[b], w[a]
+        m2 = mtref.Model(E_, H_, A_, V_, w2, layer_norm=True)
+        got = m2.step(2, tok, src, state, ctx, P, mask)["state"]
+        assert np.max(np.abs(got - ref)) > 1e-3, sw
+
+
 def test_beam_k1_equals_greedy_decoding():
     model, w = tiny_model(seed=20, layer_norm=True)
     ctx, mask, lens, *_ = tiny_batch(B=3, K=1, seed=21)
@@ -677,6 +766,27 @@ def test_ensemble_is_the_weighted_sum_with_torch():
     w = [0.5, 0.3, 0.2]
     ref = sum(torch.from_numpy(l.astype(np.float64)) * float(np.float32(x)) for l, x in zip(lps, w))
     assert np.max(np.abs(mtref.ensemble_logp(lps, w) - ref.numpy())) <= 1e-6
+
+
+
+def test_ensemble_is_log_linear_not_probability_averaging():
+    """Two members over V = 3 where the two usual ways of combining disagree on the best token.
+    Member 1 puts p = (0.9, 0.099, 0.001), member 2 p = (0.001, 0.5, 0.499); with weights 1/2
+    the average of the probabilities, (0.4505, 0.2995, 0.25), prefers token 0, while the
+    weighted sum of the log-probabilities, the log of the geometric mean (0.030, 0.222, 0.022)
+    up to a constant, prefers token 1.  The combination is the log-linear one: its values are
+    the closed forms (ln p1 + ln p2) / 2, and the beam step extends token 1."""
+    p1 = np.array([[0.9, 0.099, 0.001]])
+    p2 = np.array([[0.001, 0.5, 0.499]])
+    lps = [np.log(p1).astype(np.float32), np.log(p2).astype(np.float32)]
+    out = mtref.ensemble_logp(lps, [0.5, 0.5])
+    closed = [0.5 * (math.log(0.9) + math.log(0.001)), 0.5 * (math.log(0.099) + math.log(0.5)),
+              0.5 * (math.log(0.001) + math.log(0.499))]
+    assert np.max(np.abs(out[0] - np.array(closed))) <= 1e-6
+    averaged = np.log(0.5 * (p1 + p2))[0]
+    assert np.min(np.abs(out[0] - averaged)) > 0.2
+    tok, bp, sc = mtref.topk(1, np.zeros(1, np.float32), out)
+    assert int(tok[0]) == 1 and int(np.argmax(averaged)) == 0
 
 
 def test_ensemble_beam_of_two_copies_equals_single_model_beam():
