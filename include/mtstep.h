@@ -209,6 +209,19 @@ mt_status mt_decoder_step(mt_model *model, int B, int K, int S, const int32_t *p
                           float *logp_out, float *attn_out, const mt_taps *taps, void *ws,
                           size_t ws_bytes, void *stream);
 
+/* mt_precompute_ctx without a workspace argument, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that forbid it): the
+ * same kernels and results, with the workspace in a library-owned scratch array of 16 MiB
+ * per GPU (a file-scope device array, allocated when the library's code is loaded on a GPU
+ * and held until the process ends).  Calls no hipMalloc, hipFree or other allocating routine
+ * and records no profiling events.  Needs rup256(B*2H*4) + rup256(B*S*4) + 256 bytes <= 16 MiB
+ * (e.g. B <= 1900 at H = 1024, S = 80), else MT_ERR_WORKSPACE; the current device must be the
+ * one the model was loaded on (MT_ERR_STATE otherwise).  Every call on a GPU shares that GPU's
+ * scratch: calls that overlap on one GPU (other streams, other threads, other models) race.
+ * Nothing in the scratch has to start at zero: every byte a call reads it first writes. */
+mt_status mt_precompute_ctx_noalloc(mt_model *model, int B, int S, const void *ctx, const float *mask,
+                                    void *pctx_out, float *s0_out, void *stream);
+
 /* Dual-source models (the dual-attention post-editing models of Section 3.2: two encoders,
  * a decoder attending to both).  mt_precompute_keys2: the second source's attention keys
  * pctx2_out [B,S2,A] = ctx2 Ua2 + ba2 at its valid positions (ctx2 [B,S2,2H] and mask2

@@ -7,6 +7,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -87,6 +88,7 @@ struct mt_model {
   std::vector<Packed> wtr;        // transition blocks' recurrent matrices
   float *btr = nullptr;           // [T][3H] their biases
   float *gtu = nullptr, *betu = nullptr;  // [T][3H] layer norm of their recurrent products
+  int device;     // the HIP device the model was loaded on
   int32_t *err;
   unsigned long long *nrecompute;  // rows whose fused candidates were recomputed exactly
   std::vector<void *> allocs;
@@ -284,6 +286,31 @@ size_t precompute_ws_bytes(const mt_model *m, int B, int S) {
   return rup256((size_t)B * 2 * m->cfg.H * 4) + rup256((size_t)B * S * 4) + 256;
 }
 
+// Scratch of mt_precompute_ctx_noalloc: a file-scope device array, one copy per GPU, held
+// until the process ends.  In host code `scratch` only names the symbol; its device address
+// on each GPU comes from hipGetSymbolAddress with that GPU current, resolved once per device
+// (at model load, or at the entry point's first call on a device) and kept in g_scratch.
+constexpr size_t kNoAllocScratchBytes = size_t(16) << 20;
+constexpr int kMaxDevices = 64;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+std::mutex g_scratch_mu;
+void *g_scratch[kMaxDevices] = {};
+
+// device address of this device's scratch (dev must be the current device)
+mt_status scratch_for_device(int dev, void **out) {
+  if (dev < 0 || dev >= kMaxDevices) return fail(MT_ERR_HIP, "device %d out of range for the scratch table", dev);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void *ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress((void **)&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr)
+      return fail(MT_ERR_HIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev, hipGetErrorString(e));
+    g_scratch[dev] = ptr;
+  }
+  *out = g_scratch[dev];
+  return MT_OK;
+}
+
 // ---- profiling ----
 hipEvent_t get_event(mt_model *m) {
   if (!m->ev_pool.empty()) {
@@ -315,8 +342,8 @@ struct Timed {  // records events around one launch when profiling is on
   int k;
   hipStream_t st;
   hipEvent_t a = nullptr, b = nullptr;
-  Timed(mt_model *m_, int k_, hipStream_t st_) : m(m_), k(k_), st(st_) {
-    if (m->prof_mask & (1u << k)) {
+  Timed(mt_model *m_, int k_, hipStream_t st_, bool on = true) : m(m_), k(k_), st(st_) {
+    if (on && (m->prof_mask & (1u << k))) {
       a = get_event(m);
       b = get_event(m);
       if (a && b) hipEventRecord(a, st);
@@ -331,15 +358,17 @@ struct Timed {  // records events around one launch when profiling is on
   }
 };
 
-#define LAUNCH(kid, expr)                                                                   \
+// LAUNCH_IF: timing events (when profiling selects the kernel class) only if `on`
+#define LAUNCH_IF(kid, on, expr)                                                            \
   do {                                                                                      \
     hipError_t e_;                                                                          \
     {                                                                                       \
-      Timed tm_(model, kid, st);                                                            \
+      Timed tm_(model, kid, st, on);                                                        \
       e_ = (expr);                                                                          \
     }                                                                                       \
     if (e_ != hipSuccess) return fail(MT_ERR_HIP, "%s: %s", #expr, hipGetErrorString(e_)); \
   } while (0)
+#define LAUNCH(kid, expr) LAUNCH_IF(kid, true, expr)
 
 mt_status check_dev_ptr(const void *p, const char *name, size_t align = 16) {
   if (!p) return fail(MT_ERR_ARG, "%s is NULL", name);
@@ -424,6 +453,15 @@ mt_status mt_load_weights(const mt_config *cfg, const mt_weights *w, mt_model **
       return fail(MT_ERR_HIP, "cannot query the device's compute units");
     }
     m->num_cu = ncu;
+    m->device = dev;
+    void *sp = nullptr;  // this device's no-alloc scratch, resolved at set-up
+    if (scratch_for_device(dev, &sp) != MT_OK) {
+      char keep[sizeof g_err];
+      std::memcpy(keep, g_err, sizeof keep);
+      delete m;
+      std::memcpy(g_err, keep, sizeof keep);
+      return MT_ERR_HIP;
+    }
   }
   const int E = c.E, H = c.H, A = c.A, V = c.V, C = 2 * c.H;
   mt_status s = MT_OK;
@@ -750,20 +788,10 @@ mt_status mt_encode(mt_model *model, int B, int S, const int32_t *src_tok, const
   return MT_OK;
 }
 
-mt_status mt_precompute_ctx(mt_model *model, int B, int S, const void *ctx, const float *mask,
-                            void *pctx_out, float *s0_out, void *ws, size_t ws_bytes, void *stream) {
-  g_err[0] = 0;
-  if (!valid_model(model)) return fail(MT_ERR_ARG, "invalid model handle");
-  if (B < 1 || S < 1 || S > 1024) return fail(MT_ERR_SHAPE, "B=%d S=%d: need B >= 1, 1 <= S <= 1024", B, S);
-  if ((long long)B * S > (1 << 24)) return fail(MT_ERR_SHAPE, "B*S=%lld exceeds 2^24", (long long)B * S);
-  CHECK(check_dev_ptr(ctx, "ctx"));
-  CHECK(check_dev_ptr(mask, "mask", 4));
-  CHECK(check_dev_ptr(pctx_out, "pctx_out"));
-  CHECK(check_dev_ptr(s0_out, "s0_out"));
-  CHECK(check_dev_ptr(ws, "ws", 256));
-  const size_t need = precompute_ws_bytes(model, B, S);
-  if (ws_bytes < need) return fail(MT_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, need);
-  hipStream_t st = (hipStream_t)stream;
+// The precompute's launches on a workspace of at least precompute_ws_bytes (validated by the
+// caller).  timed = false launches without the profiling events (the no-alloc entry point).
+static mt_status precompute_impl(mt_model *model, int B, int S, const void *ctx, const float *mask, void *pctx_out,
+                                 float *s0_out, void *ws, hipStream_t st, bool timed) {
   const mt_config &c = model->cfg;
   const int H = c.H, A = c.A, C = model->C;
   float *cbar = (float *)ws;
@@ -771,21 +799,62 @@ mt_status mt_precompute_ctx(mt_model *model, int B, int S, const void *ctx, cons
   int *nvalid = (int *)((char *)vrows + rup256((size_t)B * S * 4));
   // keys only at valid positions (the others are never read): the product gathers the valid
   // context rows, counted on the device, and stores each key row at its own position
-  LAUNCH(MT_KERNEL_PRECOMPUTE, launch_valid_rows(B * S, mask, vrows, nvalid, st));
+  LAUNCH_IF(MT_KERNEL_PRECOMPUTE, timed, launch_valid_rows(B * S, mask, vrows, nvalid, st));
   GemmProblem p{};
   p.A = ctx; p.a_idx = vrows; p.a_rows = B * S; p.lda = C; p.a_bf16 = model->bf16;
   p.Bp = model->wp.p; p.ldb = model->wp.ldb; p.wblk = model->wp.blk; p.bias = model->ba;
   p.out = pctx_out; p.ldc = A; p.out_bf16 = model->bf16;
   p.M = B * S; p.N = A; p.K = C; p.err = nullptr; p.err_bit = 0; p.m_dev = nvalid;
-  LAUNCH(MT_KERNEL_PRECOMPUTE, launch_gemm(model->bf16, &p, 1, EPI_SCATTER, st));
-  LAUNCH(MT_KERNEL_PRECOMPUTE, launch_masked_mean(B, S, C, ctx, model->bf16, mask, cbar, st));
+  LAUNCH_IF(MT_KERNEL_PRECOMPUTE, timed, launch_gemm(model->bf16, &p, 1, EPI_SCATTER, st));
+  LAUNCH_IF(MT_KERNEL_PRECOMPUTE, timed, launch_masked_mean(B, S, C, ctx, model->bf16, mask, cbar, st));
   GemmProblem q{};
   q.A = cbar; q.a_rows = B; q.lda = C; q.a_bf16 = 0;
   q.Bp = model->ws0.p; q.ldb = model->ws0.ldb; q.wblk = model->ws0.blk; q.bias = model->bi;
   q.out = s0_out; q.ldc = H; q.out_bf16 = 0;
   q.M = B; q.N = H; q.K = C;
-  LAUNCH(MT_KERNEL_PRECOMPUTE, launch_gemm(model->bf16, &q, 1, EPI_TANH, st));
+  LAUNCH_IF(MT_KERNEL_PRECOMPUTE, timed, launch_gemm(model->bf16, &q, 1, EPI_TANH, st));
   return MT_OK;
+}
+
+static mt_status precompute_args(mt_model *model, int B, int S, const void *ctx, const float *mask,
+                                 const void *pctx_out, const float *s0_out) {
+  if (!valid_model(model)) return fail(MT_ERR_ARG, "invalid model handle");
+  if (B < 1 || S < 1 || S > 1024) return fail(MT_ERR_SHAPE, "B=%d S=%d: need B >= 1, 1 <= S <= 1024", B, S);
+  if ((long long)B * S > (1 << 24)) return fail(MT_ERR_SHAPE, "B*S=%lld exceeds 2^24", (long long)B * S);
+  CHECK(check_dev_ptr(ctx, "ctx"));
+  CHECK(check_dev_ptr(mask, "mask", 4));
+  CHECK(check_dev_ptr(pctx_out, "pctx_out"));
+  CHECK(check_dev_ptr(s0_out, "s0_out"));
+  return MT_OK;
+}
+
+mt_status mt_precompute_ctx(mt_model *model, int B, int S, const void *ctx, const float *mask,
+                            void *pctx_out, float *s0_out, void *ws, size_t ws_bytes, void *stream) {
+  g_err[0] = 0;
+  CHECK(precompute_args(model, B, S, ctx, mask, pctx_out, s0_out));
+  CHECK(check_dev_ptr(ws, "ws", 256));
+  const size_t need = precompute_ws_bytes(model, B, S);
+  if (ws_bytes < need) return fail(MT_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, need);
+  return precompute_impl(model, B, S, ctx, mask, pctx_out, s0_out, ws, (hipStream_t)stream, true);
+}
+
+mt_status mt_precompute_ctx_noalloc(mt_model *model, int B, int S, const void *ctx, const float *mask,
+                                    void *pctx_out, float *s0_out, void *stream) {
+  g_err[0] = 0;
+  CHECK(precompute_args(model, B, S, ctx, mask, pctx_out, s0_out));
+  const size_t need = precompute_ws_bytes(model, B, S);
+  if (need > kNoAllocScratchBytes)
+    return fail(MT_ERR_WORKSPACE, "B=%d S=%d needs %zu bytes of scratch, more than the %zu of the no-alloc entry point",
+                B, S, need, kNoAllocScratchBytes);
+  int dev = -1;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev != model->device)
+    return fail(MT_ERR_STATE, "current device %d is not the model's device %d", dev, model->device);
+  void *sp = nullptr;
+  CHECK(scratch_for_device(dev, &sp));
+  // every scratch byte the kernels read they first write (valid-row list and count, masked
+  // means), so nothing is cleared: what the previous call left is never read
+  return precompute_impl(model, B, S, ctx, mask, pctx_out, s0_out, sp, (hipStream_t)stream, false);
 }
 
 // The step, with an optional second source (S2 > 0: dual-source models)

@@ -74,6 +74,8 @@ def lib() -> C.CDLL:
         L.mt_workspace_bytes.argtypes = [_vp, C.c_int, C.c_int, C.c_int]
         L.mt_workspace_bytes.restype = C.c_size_t
         L.mt_precompute_ctx.argtypes = [_vp, C.c_int, C.c_int, _vp, _vp, _vp, _vp, _vp, C.c_size_t, _vp]
+        L.mt_precompute_ctx_noalloc.argtypes = [_vp, C.c_int, C.c_int, _vp, _vp, _vp, _vp, _vp]
+        L.mt_precompute_ctx_noalloc.restype = C.c_int
         L.mt_decoder_step.argtypes = [_vp, C.c_int, C.c_int, C.c_int, _vp, _vp, C.c_int, _vp, _vp, _vp,
                                       _vp, _vp, _vp, _vp, C.POINTER(mt_taps), _vp, C.c_size_t, _vp]
         L.mt_beam_topk.argtypes = [_vp, C.c_int, C.c_int, _vp, _vp, _vp, _vp, _vp, _vp, _vp, C.c_size_t, _vp]
@@ -215,6 +217,11 @@ def mt_precompute_ctx(model: Model, B, S, ctx, mask, pctx_out, s0_out, ws, ws_by
     ws_bytes = ws.numel() * ws.element_size() if ws_bytes is None else ws_bytes
     _check(lib().mt_precompute_ctx(model.handle, B, S, _ptr(ctx), _ptr(mask), _ptr(pctx_out), _ptr(s0_out),
                                    _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def mt_precompute_ctx_noalloc(model: Model, B, S, ctx, mask, pctx_out, s0_out, stream=None):
+    _check(lib().mt_precompute_ctx_noalloc(model.handle, B, S, _ptr(ctx), _ptr(mask), _ptr(pctx_out), _ptr(s0_out),
+                                           _stream(stream)))
 
 
 def mt_decoder_step(model: Model, B, K, S, prev_tok, src_row, n_state_rows, state_in, ctx, pctx, mask,
