@@ -3,10 +3,12 @@
 
 A bench step is one pass of the whole hot path over the batch: mt_decoder_step
 (cGRU 1, attention, cGRU 2, readout, vocabulary GEMM with fused log-sum-exp and
-per-tile top-K) followed by mt_beam_topk.  Every `preset.steps` steps a new
-decode starts: mt_precompute_ctx (attention keys and start state) runs inside
-the timed region at that rate, as it would when translating batch after batch.
-Inputs are synthetic and already resident in HBM when timing starts.
+per-tile top-K) followed by mt_beam_topk.  A new decode (mt_precompute_ctx: the
+attention keys and the start state, then the start beam) begins whenever the
+running step index, warmup steps included, reaches a multiple of preset.steps;
+the timed region contains such a restart only if it spans that index (the JSON
+line says how many it contained).  Inputs are synthetic and already resident in
+HBM when timing starts.
 
     python bench.py [--steps K] [--warmup W] [--preset nematus_f32]
 
@@ -31,6 +33,9 @@ sys.path.insert(0, ROOT)
 METRIC = "beam decoder steps/s (B×K hyp-rows/s) + % of HBM BW / bf16 MFMA peak"
 PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}
 HBM_GBS = 8000.0
+# transcendental issue rate (exp2, rcp): a quarter of the 16 lanes per SIMD per clock, 4 SIMDs
+# per CU, 256 CUs at 2.4 GHz
+TRANS_TOPS = 256 * 4 * 4 * 2.4e9 / 1e12
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
 
@@ -40,6 +45,68 @@ def log(msg):
 
 def source_hash(path):
     return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+
+
+def kernel_work(p, lens, S, nsrc=1):
+    """Algorithmic work of each kernel class in one step (summed over its launches): flops of
+    the matrix products, HBM bytes of the streaming kernels (every operand read once, every
+    result written once; weights of the products are not counted as bytes here), and the
+    transcendental operations of the attention (2 per tanh: exp2 and rcp).  Returns
+    {class: (bound, amount, unit)}."""
+    M, E, H, A, V, C, K = p.M, p.E, p.H, p.A, p.V, p.C, p.K
+    es = 4 if p.gemm == "f32" else 2                # operand bytes
+    bf_copy = 0 if p.gemm == "f32" else H * 2        # bf16 copy of a new state / s1
+    T = p.transitions
+    slen = float(sum(int(x) for x in lens))
+    w = {}
+    w["GEMM_GRU1"] = ("mfma", 2.0 * M * H * 3 * H)
+    cell = M * (3 * H * 4 + 3 * H * 4 + H * 4 + H * 4 + bf_copy)   # a, u, h read; state (+bf16) written
+    cell_t = M * (3 * H * 4 + H * 4 + H * 4 + bf_copy)            # transition block: u, h, state
+    w["GRU_CELL"] = ("hbm", 2.0 * cell + T * cell_t)
+    w["GEMM_S1"] = ("mfma", 2.0 * M * H * (nsrc * A + 3 * H))
+    attn_bytes = nsrc * slen * (A + C) * es + M * nsrc * A * 4 + M * nsrc * C * es
+    w["ATTENTION"] = ("hbm", attn_bytes)
+    w["ATTENTION_tanh"] = ("trans", 2.0 * K * slen * A * nsrc)
+    w["GEMM_CTX"] = ("mfma", 2.0 * M * nsrc * C * (3 * H + E))
+    w["GEMM_READOUT"] = ("mfma", 2.0 * M * H * E)
+    w["READOUT"] = ("hbm", M * (E * 4 * 3 + E * es))
+    w["VOCAB_GEMM"] = ("mfma", 2.0 * M * E * V)
+    w["VOCAB_THRESHOLD"] = ("mfma", 2.0 * M * E * min(V, 2048))
+    if T:
+        w["GEMM_TRANSITION"] = ("mfma", T * 2.0 * M * H * 3 * H)
+    return w
+
+
+def roof_of(bound, amount, us, gemm):
+    if not us:
+        return None
+    t = us * 1e-6
+    if bound == "mfma":
+        a = amount / t / 1e12
+        return {"bound": "mfma", "achieved": round(a, 2), "peak": PEAK_TFLOPS[gemm], "unit": "TFLOP/s",
+                "frac": round(a / PEAK_TFLOPS[gemm], 4)}
+    if bound == "hbm":
+        a = amount / t / 1e9
+        return {"bound": "hbm", "achieved": round(a, 1), "peak": HBM_GBS, "unit": "GB/s", "frac": round(a / HBM_GBS, 4)}
+    a = amount / t / 1e12
+    return {"bound": "alu", "achieved": round(a, 3), "peak": round(TRANS_TOPS, 3), "unit": "Ttrans/s",
+            "frac": round(a / TRANS_TOPS, 4)}
+
+
+def host_cpu():
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    try:
+        avail = len(os.sched_getaffinity(0))
+    except AttributeError:
+        avail = os.cpu_count()
+    return {"nproc": avail, "cpu_count": os.cpu_count(), "cpu_model": model}
 
 
 def cpu_baseline(members, ctx, mask, budget_s=15.0, src2=None):
@@ -84,6 +151,7 @@ def cpu_baseline(members, ctx, mask, budget_s=15.0, src2=None):
         "unit": "steps/s",
         "cores": 1,
         "kind": "oracle",
+        "host": host_cpu(),
         "sample": f"{n} of {p.B} sentences ({n * p.K} hyp rows), one step each + their start-state precompute "
                   f"amortised over {p.steps} steps; {t_pre + t_step:.1f} s of CPU; scaled linearly to the batch",
         "hyp_rows_per_s": steps_per_s * p.M,
@@ -160,7 +228,7 @@ def main():
         drive.set_batch(ctx, mask, p.K)
         cell = f"ensemble of {NE} {cell}"
 
-    tr = {"translations": 0, "steps": 0}
+    tr = {"translations": 0, "steps": 0, "restarts": 0}
 
     def run(n, first_index):
         """n steps (or, translating, whole translations until at least n steps); returns the steps run"""
@@ -177,6 +245,7 @@ def main():
             if i % p.steps == 0:
                 drive.precompute()
                 drive.start(tok0, score0)
+                tr["restarts"] += 1
             drive.advance()
         return n
 
@@ -188,10 +257,11 @@ def main():
     log(f"[bench] timing {args.steps} steps")
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    tr.update(translations=0, steps=0)
+    tr.update(translations=0, steps=0, restarts=0)
     timed_steps = run(args.steps, args.warmup)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+    restarts_timed = tr["restarts"]
     vocab_ms, vocab_n = mt.mt_profile_query(dec.model, "VOCAB_GEMM")
     mt.mt_profile_enable(dec.model, ())
     assert mt.mt_device_errors(dec.model) == 0
@@ -202,11 +272,46 @@ def main():
     bsteps = run(min(args.steps, 50), args.warmup + args.steps)
     torch.cuda.synchronize()
     breakdown = {}
+    work = kernel_work(p, lens, dec.S, nsrc=2 if args.dual else 1)
     for k in mt.KERNELS:
         ms, n = mt.mt_profile_query(dec.model, k)
         if n:
-            breakdown[k.lower()] = {"us_per_step": round(1e3 * ms / bsteps, 2), "launches": n}
+            us = 1e3 * ms / bsteps
+            ent = {"us_per_step": round(us, 2), "launches": n}
+            if k in work and NE == 1 and not args.translate:
+                r = roof_of(*work[k], us, p.gemm)
+                if r:
+                    ent["roof"] = r
+                if k == "ATTENTION":
+                    ent["roof_tanh"] = roof_of(*work["ATTENTION_tanh"], us, p.gemm)
+            breakdown[k.lower()] = ent
     mt.mt_profile_enable(dec.model, ())
+
+    # the materialised selection: mt_beam_topk reading a [M, V] fp32 log-probability matrix
+    # (ensembles, or callers that want the log-probabilities), an HBM-bound first level
+    topk_mat = None
+    if NE == 1 and not args.translate:
+        g = torch.Generator(device="cuda").manual_seed(5)
+        lp = torch.randn((p.M, p.V), device="cuda", generator=g) - math.log(p.V)
+        sc = torch.zeros(p.M, device="cuda")
+        so, to, bo_, ro = (torch.empty_like(dec.score), torch.empty_like(dec.tok), torch.empty_like(dec.bp),
+                           torch.empty_like(dec.row))
+        for _ in range(3):
+            dec.topk(sc, lp, score_out=so, tok_out=to, bp_out=bo_, row_out=ro)
+        torch.cuda.synchronize()
+        mt.mt_profile_enable(dec.model, ("TOPK",))
+        mt.mt_profile_reset(dec.model)
+        nrep = 20
+        for _ in range(nrep):
+            dec.topk(sc, lp, score_out=so, tok_out=to, bp_out=bo_, row_out=ro)
+        torch.cuda.synchronize()
+        ms, n = mt.mt_profile_query(dec.model, "TOPK")
+        mt.mt_profile_enable(dec.model, ())
+        us = 1e3 * ms / nrep
+        topk_mat = {"what": "mt_beam_topk on a materialised [M, V] fp32 log-probability matrix (both levels)",
+                    "us_per_call": round(us, 2), "bytes": p.M * p.V * 4,
+                    "roof": roof_of("hbm", p.M * p.V * 4, us, p.gemm)}
+        del lp
 
     if args.copy_calib_mib:
         # a plain elementwise kernel of known traffic: reads N MiB, writes N MiB
@@ -264,7 +369,10 @@ def main():
         "target_tok_per_s": round(steps_per_s * p.B, 1),
         "roofline": roofline,
         "kernels": breakdown,
+        "restarts_in_timed_region": restarts_timed,
     }
+    if topk_mat:
+        rec["topk_materialised"] = topk_mat
     if args.encode:
         # encoder of the same shapes over Zipf source tokens with the batch's lengths
         ew = synth.make_encoder_weights(p, args.encode, transitions=args.enc_transitions,

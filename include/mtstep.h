@@ -186,6 +186,9 @@ mt_status mt_encode(mt_model *model, int B, int S, const int32_t *src_tok, const
  *        written at valid positions only (masked rows are left as they were and
  *        never read);
  *   s0_out [B,H] fp32 — tanh(masked mean of ctx[b] times Wi + bi).
+ * It also records in the model the order of the B sentences by length, which later steps
+ * with the same B use to schedule their attention (the longest first); it decides
+ * scheduling only, never results.
  * 1 <= S <= 1024; B*S <= 2^24. */
 mt_status mt_precompute_ctx(mt_model *model, int B, int S, const void *ctx, const float *mask,
                             void *pctx_out, float *s0_out, void *ws, size_t ws_bytes,

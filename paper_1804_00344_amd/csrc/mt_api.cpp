@@ -89,6 +89,10 @@ struct mt_model {
   float *btr = nullptr;           // [T][3H] their biases
   float *gtu = nullptr, *betu = nullptr;  // [T][3H] layer norm of their recurrent products
   int device;     // the HIP device the model was loaded on
+  // sentence order (longest first) of each source's attention, written by the precompute of
+  // a batch of srank_B[i] sentences (-1: none yet); it only schedules the attention rows
+  int *srank[2] = {nullptr, nullptr};
+  int srank_B[2] = {-1, -1};
   int32_t *err;
   unsigned long long *nrecompute;  // rows whose fused candidates were recomputed exactly
   std::vector<void *> allocs;
@@ -583,6 +587,8 @@ mt_status mt_load_weights(const mt_config *cfg, const mt_weights *w, mt_model **
     CHECK(dev_upload(m, &zero, sizeof zero, (void **)&m->err));
     unsigned long long zero64 = 0;
     CHECK(dev_upload(m, &zero64, sizeof zero64, (void **)&m->nrecompute));
+    for (int i = 0; i < 2; ++i)
+      CHECK(dev_upload(m, nullptr, (size_t)attention_order_max_sentences() * sizeof(int), (void **)&m->srank[i]));
     {
       // The token side of GRU 1 and of the readout, x [W1 | Wt_y] + [b1 | 0], depends only on
       // the token: it is computed once here for the whole vocabulary (same products, same
@@ -813,6 +819,13 @@ static mt_status precompute_impl(mt_model *model, int B, int S, const void *ctx,
   q.out = s0_out; q.ldc = H; q.out_bf16 = 0;
   q.M = B; q.N = H; q.K = C;
   LAUNCH_IF(MT_KERNEL_PRECOMPUTE, timed, launch_gemm(model->bf16, &q, 1, EPI_TANH, st));
+  // the batch's sentence order for the steps' attention (into model memory)
+  if (B <= attention_order_max_sentences()) {
+    LAUNCH_IF(MT_KERNEL_PRECOMPUTE, timed, launch_attention_order(B, S, mask, model->srank[0], st));
+    model->srank_B[0] = B;
+  } else {
+    model->srank_B[0] = -1;
+  }
   return MT_OK;
 }
 
@@ -928,12 +941,16 @@ static mt_status decoder_step_impl(mt_model *model, int B, int K, int S, const i
   // context goes to the right half of the [M][2C] rows
   float *cc32 = (!bf || (taps && taps->c)) ? cc : nullptr;
   bf16 *ch = bf ? (bf16 *)(W + L.ch) : nullptr;
+  // rows are scheduled longest sentence first, by the order the batch's precompute left in the
+  // model (any permutation of the B sentences gives the same results: it only schedules)
+  const int *srank1 = model->srank_B[0] == B ? model->srank[0] : nullptr;
+  const int *srank2 = model->srank_B[1] == B ? model->srank[1] : nullptr;
   LAUNCH(MT_KERNEL_ATTENTION, launch_attention(B, K, S, A, C, pctx, ctx, bf, mask, g2, ldg2, model->va, cc32, Cc,
-                                               ch, Cc, attn_out, st));
+                                               ch, Cc, attn_out, srank1, st));
   if (S2 > 0)
     LAUNCH(MT_KERNEL_ATTENTION, launch_attention(B, K, S2, A, C, pctx2, ctx2, bf, mask2, g2 + A, ldg2, model->va2,
                                                  cc32 ? cc32 + C : nullptr, Cc, ch ? ch + C : nullptr, Cc, nullptr,
-                                                 st));
+                                                 srank2, st));
   if (taps && taps->c) HIP_TRY(hipMemcpyAsync(taps->c, cc, (size_t)M * Cc * 4, hipMemcpyDeviceToDevice, st));
   // c [W2 | Wt_c] + [b2 | 0]
   GemmProblem p3{};
@@ -1050,6 +1067,12 @@ mt_status mt_precompute_keys2(mt_model *model, int B, int S2, const void *ctx2, 
   p.out = pctx2_out; p.ldc = A; p.out_bf16 = model->bf16;
   p.M = B * S2; p.N = A; p.K = C; p.m_dev = nvalid;
   LAUNCH(MT_KERNEL_PRECOMPUTE, launch_gemm(model->bf16, &p, 1, EPI_SCATTER, st));
+  if (B <= attention_order_max_sentences()) {
+    LAUNCH(MT_KERNEL_PRECOMPUTE, launch_attention_order(B, S2, mask2, model->srank[1], st));
+    model->srank_B[1] = B;
+  } else {
+    model->srank_B[1] = -1;
+  }
   return MT_OK;
 }
 

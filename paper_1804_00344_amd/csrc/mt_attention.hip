@@ -22,8 +22,9 @@
 // loads in flight while the current group is accumulated; the first two groups are loaded
 // before the softmax.
 //
-// Workgroup ids are remapped so that the K rows of one sentence run on one XCD and share
-// its L2 copy of P[b] and Cx[b].
+// Scheduling: a small kernel orders the sentences by length, and the longest rows start
+// first on every XCD, with the K rows of one sentence on one XCD sharing its L2 copy of P[b]
+// and Cx[b] (row_of_block).
 #include "mt_internal.h"
 
 namespace mt {
@@ -63,9 +64,82 @@ struct Gran<bf16> {
   }
 };
 
+// Row of workgroup w.  With a sentence order (srank[s] = the sentence of rank s, longest
+// first), sentence rank s runs on XCD s % 8 (workgroups are dispatched round-robin over the 8
+// XCDs: w -> XCD w % 8), and within an XCD the sentences follow their rank, each one's K rows
+// in a row: the longest rows start first on every XCD, and the K rows of a sentence share its
+// XCD's L2 copy of the keys and the context.  The sentences past the last multiple of 8 (the
+// shortest) take the last workgroups in order.  Without an order: consecutive rows on one XCD.
+__device__ __forceinline__ int row_of_block(int w, int B, int K, const int *srank) {
+  if (!srank) return xcd_remap(w, B * K);
+  const int nfull = B & ~(kXcds - 1);
+  int s, k;
+  if (w < nfull * K) {
+    const int j = w / kXcds;
+    s = (j / K) * kXcds + w % kXcds;
+    k = j % K;
+  } else {
+    const int r = w - nfull * K;
+    s = nfull + r / K;
+    k = r % K;
+  }
+  return srank[s] * K + k;
+}
+
+// Sentences by decreasing number of valid positions (the order of equal lengths is
+// unspecified: it only schedules work), one 1024-thread workgroup: a histogram of the
+// lengths, its exclusive prefix sums from the longest length down, then each sentence takes
+// the next slot of its length.
+constexpr int kOrderMaxB = 8192;
+__global__ __launch_bounds__(1024) void attention_order_kernel(int B, int S, const float *__restrict__ mask,
+                                                               int *__restrict__ srank) {
+  __shared__ int hist[kMaxS + 1];
+  __shared__ int lens[kOrderMaxB];
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  for (int l = t; l <= S; l += 1024) hist[l] = 0;
+  __syncthreads();
+  for (int b = w; b < B; b += 16) {  // one wave per sentence: coalesced mask rows, ballot counts
+    const float *mr = mask + (size_t)b * S;
+    int n = 0;
+    for (int i0 = 0; i0 < S; i0 += 64) n += __popcll(__ballot(i0 + lane < S && mr[i0 + lane] != 0.f));
+    if (lane == 0) {
+      lens[b] = n;
+      atomicAdd(&hist[n], 1);
+    }
+  }
+  __syncthreads();
+  if (w == 0) {  // start[L] = sentences longer than L, for L = S .. 0 (reversed index r = S - L)
+    const int nb = S + 1, per = (nb + 63) / 64;
+    int sum = 0;
+    for (int i = 0; i < per; ++i) {
+      const int r = lane * per + i;
+      if (r < nb) sum += hist[S - r];
+    }
+    int incl = sum;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(incl, o, 64);
+      if (lane >= o) incl += y;
+    }
+    int run = incl - sum;
+    for (int i = 0; i < per; ++i) {
+      const int r = lane * per + i;
+      if (r < nb) {
+        const int h = hist[S - r];
+        hist[S - r] = run;
+        run += h;
+      }
+    }
+  }
+  __syncthreads();
+  for (int b = t; b < B; b += 1024) srank[atomicAdd(&hist[lens[b]], 1)] = b;
+}
+
 // NG: granules per lane of a score row (A <= 64 * NG * Gran<T>::N);
-// NC: granules per thread of a context row (2H <= 256 * NC * Gran<T>::N)
-template <typename T, int NG, int NC>
+// NC: granules per thread of a context row (2H <= 256 * NC * Gran<T>::N);
+// RD: key rows in flight per wave in the score loop (two cover the latency: deeper rings, 4 to
+// 8 rows at one beam row per sentence, measured no faster)
+template <typename T, int NG, int NC, int RD>
 __global__ __launch_bounds__(kAT) void attention_kernel(int B, int K, int S, int A, int Cd,
                                                         const T *__restrict__ P,
                                                         const T *__restrict__ Cx,
@@ -74,14 +148,15 @@ __global__ __launch_bounds__(kAT) void attention_kernel(int B, int K, int S, int
                                                         const float *__restrict__ va,
                                                         float *__restrict__ ctx_out, int ldc,
                                                         bf16 *__restrict__ ctx16, int ld16,
-                                                        float *__restrict__ alpha_out) {
+                                                        float *__restrict__ alpha_out,
+                                                        const int *__restrict__ srank) {
   constexpr int G = Gran<T>::N;
   constexpr int U = NC <= 2 ? 8 : NC == 4 ? 4 : 2;  // context positions in flight per thread
   __shared__ float es[kMaxS];
   __shared__ int vidx[kMaxS];
   __shared__ float stat[2];
   __shared__ int nvalid;
-  const int m = xcd_remap(blockIdx.x, gridDim.x);
+  const int m = row_of_block(blockIdx.x, B, K, srank);
   const int b = m / K;
   const int t = threadIdx.x, lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
@@ -154,21 +229,22 @@ __global__ __launch_bounds__(kAT) void attention_kernel(int B, int K, int S, int
     return wave_sum(acc);
   };
   if (wave < n) {  // wave-uniform
-    v4u32 ra[NG], rb[NG];
-    load_raw(wave, ra);
-    load_raw(wave + 4, rb);
+    v4u32 ring[RD][NG];
+#pragma unroll
+    for (int d = 0; d < RD; ++d) load_raw(wave + 4 * d, ring[d]);
     int j = wave;
-    for (;;) {
-      const float s0 = score_raw(ra);
-      if (lane == 0) es[j] = vsum + s0;
-      load_raw(j + 8, ra);
-      j += 4;
-      if (j >= n) break;
-      const float s1 = score_raw(rb);
-      if (lane == 0) es[j] = vsum + s1;
-      load_raw(j + 8, rb);
-      j += 4;
-      if (j >= n) break;
+    bool go = true;
+    while (go) {
+#pragma unroll
+      for (int d = 0; d < RD; ++d) {
+        if (go) {
+          const float sc = score_raw(ring[d]);
+          if (lane == 0) es[j] = vsum + sc;
+          load_raw(j + 4 * RD, ring[d]);
+          j += 4;
+          go = j < n;
+        }
+      }
     }
   }
   __syncthreads();
@@ -269,31 +345,44 @@ __global__ __launch_bounds__(kAT) void attention_kernel(int B, int K, int S, int
   }
 }
 
+#ifndef MT_ATTN_RING_K1
+#define MT_ATTN_RING_K1 2
+#endif
+constexpr int kAttnRingK1 = MT_ATTN_RING_K1;
+
 static int bucket(int n) { return n <= 1 ? 1 : n <= 2 ? 2 : n <= 4 ? 4 : n <= 8 ? 8 : 16; }
 
 template <typename T, int NG>
 static void attn_go_c(int nc, int B, int K, int S, int A, int Cd, const T *P, const T *Cx, const float *mask,
                       const float *q, int ldq, const float *va, float *ctx_out, int ldc, bf16 *ctx16,
-                      int ld16, float *alpha_out, hipStream_t st) {
+                      int ld16, float *alpha_out, const int *srank, hipStream_t st) {
   const int M = B * K;
-#define MT_AT(NC)                                                                                    \
-  hipLaunchKernelGGL((attention_kernel<T, NG, NC>), dim3(M), dim3(kAT), 0, st, B, K, S, A, Cd, P, Cx, \
-                     mask, q, ldq, va, ctx_out, ldc, ctx16, ld16, alpha_out)
+#define MT_AT1(NC, RD)                                                                                   \
+  hipLaunchKernelGGL((attention_kernel<T, NG, NC, RD>), dim3(M), dim3(kAT), 0, st, B, K, S, A, Cd, P, Cx, \
+                     mask, q, ldq, va, ctx_out, ldc, ctx16, ld16, alpha_out, srank)
+#define MT_AT(NC)                       \
+  do {                                  \
+    if (K == 1)                         \
+      MT_AT1(NC, kAttnRingK1);          \
+    else                                \
+      MT_AT1(NC, 2);                    \
+  } while (0)
   if (nc <= 1) MT_AT(1);
   else if (nc <= 2) MT_AT(2);
   else if (nc <= 4) MT_AT(4);
   else MT_AT(8);
 #undef MT_AT
+#undef MT_AT1
 }
 
 template <typename T>
 static void attn_go(int B, int K, int S, int A, int Cd, const T *P, const T *Cx, const float *mask,
                     const float *q, int ldq, const float *va, float *ctx_out, int ldc, bf16 *ctx16,
-                    int ld16, float *alpha_out, hipStream_t st) {
+                    int ld16, float *alpha_out, const int *srank, hipStream_t st) {
   constexpr int G = Gran<T>::N;
   const int ng = bucket((A / G + 63) / 64);
   const int nc = bucket((Cd / G + kAT - 1) / kAT);
-#define MT_AG(NG) attn_go_c<T, NG>(nc, B, K, S, A, Cd, P, Cx, mask, q, ldq, va, ctx_out, ldc, ctx16, ld16, alpha_out, st)
+#define MT_AG(NG) attn_go_c<T, NG>(nc, B, K, S, A, Cd, P, Cx, mask, q, ldq, va, ctx_out, ldc, ctx16, ld16, alpha_out, srank, st)
   switch (ng) {
     case 1: MT_AG(1); break;
     case 2: MT_AG(2); break;
@@ -304,17 +393,25 @@ static void attn_go(int B, int K, int S, int A, int Cd, const T *P, const T *Cx,
 #undef MT_AG
 }
 
+hipError_t launch_attention_order(int B, int S, const float *mask, int *srank, hipStream_t st) {
+  if (B < 1 || B > kOrderMaxB || S < 1 || S > kMaxS) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(attention_order_kernel, dim3(1), dim3(1024), 0, st, B, S, mask, srank);
+  return hipGetLastError();
+}
+
+int attention_order_max_sentences() { return kOrderMaxB; }
+
 hipError_t launch_attention(int B, int K, int S, int A, int Cd, const void *P, const void *Cx,
                             int bf16_io, const float *mask, const float *q, int ldq,
                             const float *va, float *ctx_out, int ldc, bf16 *ctx16, int ld16, float *alpha_out,
-                            hipStream_t st) {
+                            const int *srank, hipStream_t st) {
   if (B * K == 0) return hipSuccess;
   if (bf16_io)
     attn_go<bf16>(B, K, S, A, Cd, (const bf16 *)P, (const bf16 *)Cx, mask, q, ldq, va, ctx_out, ldc, ctx16,
-                  ld16, alpha_out, st);
+                  ld16, alpha_out, srank, st);
   else
     attn_go<float>(B, K, S, A, Cd, (const float *)P, (const float *)Cx, mask, q, ldq, va, ctx_out, ldc, ctx16,
-                   ld16, alpha_out, st);
+                   ld16, alpha_out, srank, st);
   return hipGetLastError();
 }
 

@@ -477,11 +477,17 @@ hipError_t launch_masked_mean(int B, int S, int Cd, const void *ctx, int ctx_bf1
 // rows of a [n] 0/1 mask that are valid (nonzero), in increasing order: idx[0..*count)
 hipError_t launch_valid_rows(int n, const float *mask, int32_t *idx, int *count, hipStream_t st);
 
-// context rows go to ctx_out [M][ldc] fp32 and/or ctx16 [M][ld16] bf16 (either may be NULL)
+// context rows go to ctx_out [M][ldc] fp32 and/or ctx16 [M][ld16] bf16 (either may be NULL);
+// srank (or NULL): the sentences by decreasing length, from launch_attention_order, which only
+// decides the order in which rows are scheduled
 hipError_t launch_attention(int B, int K, int S, int A, int Cd, const void *P, const void *Cx,
                             int bf16_io, const float *mask, const float *q, int ldq,
                             const float *va, float *ctx_out, int ldc, bf16 *ctx16, int ld16, float *alpha_out,
-                            hipStream_t st);
+                            const int *srank, hipStream_t st);
+// srank[0..B) = the sentences of mask [B][S] by decreasing number of valid positions
+// (B <= attention_order_max_sentences())
+hipError_t launch_attention_order(int B, int S, const float *mask, int *srank, hipStream_t st);
+int attention_order_max_sentences();
 
 // translation bookkeeping for B sentences of K ranked results each (see mt_beam_finish)
 struct BeamFinish {

@@ -63,6 +63,12 @@ _vp = C.c_void_p
 def lib() -> C.CDLL:
     global _lib
     if _lib is None:
+        # The library must run on torch's HIP runtime: its device pointers and streams are
+        # torch's.  torch's runtime carries the soname libamdhip64.so.7 but torch names it
+        # libamdhip64.so, so loading libmtstep first would bring in a second runtime (the one
+        # libmtstep was linked against), which then fails to initialise beside torch's.  With
+        # torch loaded first, libmtstep's dependency resolves to the runtime already there.
+        import torch  # noqa: F401
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
                                "(python -m paper_1804_00344_amd.build)")
