@@ -287,6 +287,22 @@ def main():
             breakdown[k.lower()] = ent
     mt.mt_profile_enable(dec.model, ())
 
+    # HBM traffic per launch from the counter passes (profiles/traffic.json), for the classes
+    # whose kernels the counters were taken on (the source file's hash still matches)
+    if os.path.exists(TRAFFIC_FILE):
+        tf = json.load(open(TRAFFIC_FILE)).get(p.name, {})
+        cls_of = {"GRU_CELL": "gru_cell", "ATTENTION": "attention", "READOUT": "readout", "VOCAB_GEMM": "vocab_gemm",
+                  "TOPK": "topk_row_select", "VOCAB_THRESHOLD": "vocab_threshold", "LSE": "lse"}
+        for k, cls in cls_of.items():
+            ent = breakdown.get(k.lower())
+            hits = [e for key, e in tf.items() if key.startswith(cls + "@")]
+            if not ent or not hits:
+                continue
+            e = hits[0]
+            src = os.path.join(ROOT, "paper_1804_00344_amd", "csrc", e["source"])
+            if os.path.exists(src) and source_hash(src) == e["source_hash"]:
+                ent["counter_MB_per_launch"] = round(e["bytes_per_launch"] / 1e6, 3)
+
     # the materialised selection: mt_beam_topk reading a [M, V] fp32 log-probability matrix
     # (ensembles, or callers that want the log-probabilities), an HBM-bound first level
     topk_mat = None

@@ -42,10 +42,11 @@ def _one(d: str, pattern: str) -> str:
     return hits[0]
 
 
-def trace(d, steps, title, cmd):
+def trace(d, steps, title, cmd, note=""):
     rows = list(csv.DictReader(open(_one(d, "*kernel_stats.csv"))))
     out = [f"# {title}", "", f"Command: `{cmd}`", "",
-           f"Per-step column: total duration / {steps} launches of the step (bench warmup + timed + breakdown).", "",
+           f"Per-step column: total duration / {steps} launches of the step (bench warmup + timed + breakdown)."
+           + (f"  {note}" if note else ""), "",
            "| kernel | calls | avg us | per step us | % |", "|---|---:|---:|---:|---:|"]
     tot = 0.0
     for r in rows:
@@ -100,6 +101,108 @@ def traffic(fetch_dir, write_dir, preset, calib_mib, kernel, cmd, json_path=None
     return "\n".join(md) + "\n"
 
 
+# kernel name substring -> (class, source file): the counters of a class are valid while its
+# source file hashes as recorded
+KERNEL_CLASSES = [
+    ("vocab_threshold_kernel", "vocab_threshold", "mt_vocab.hip"),
+    ("vocab_kernel", "vocab_gemm", "mt_vocab.hip"),
+    ("attention_order_kernel", "attention_order", "mt_attention.hip"),
+    ("attention_kernel", "attention", "mt_attention.hip"),
+    ("gru_cell_kernel", "gru_cell", "mt_rnn.hip"),
+    ("readout_kernel", "readout", "mt_rnn.hip"),
+    ("lse_kernel", "lse", "mt_rnn.hip"),
+    ("row_select_kernel", "topk_row_select", "mt_topk.hip"),
+    ("topk_scan_logp_kernel", "topk_scan_logp", "mt_topk.hip"),
+    ("gemm_wd_kernel", "gemm_bf16", "mt_gemm.hip"),
+    ("gemm_f32_kernel", "gemm_f32", "mt_gemm.hip"),
+]
+
+
+def _classify(name):
+    for sub, cls, src in KERNEL_CLASSES:
+        if sub in name:
+            return cls, src
+    return None, None
+
+
+def _by_dispatch_shape(d, counters):
+    """{(kernel name, grid size): {counter: [values per dispatch]}} of one pass."""
+    agg = collections.defaultdict(lambda: collections.defaultdict(list))
+    for r in csv.DictReader(open(_one(d, "*counter_collection.csv"))):
+        if r["Counter_Name"] in counters:
+            agg[(r["Kernel_Name"], int(r["Grid_Size"]))][r["Counter_Name"]].append(float(r["Counter_Value"]))
+    return agg
+
+
+def counters(fetch_dir, write_dir, mfma_dir, preset, calib_mib, cmd, json_path=None, num_simd=1024, xcds=8):
+    """HBM traffic (calibrated FETCH_SIZE / WRITE_SIZE, KiB per dispatch) and matrix-core busy
+    fraction (SQ_VALU_MFMA_BUSY_CYCLES over the kernel's cycles times the SIMDs; the kernel's
+    cycles are GRBM_GUI_ACTIVE / number of XCDs, which count it once each) of every kernel of
+    the decoder step, per (kernel, grid) shape."""
+    f = _by_dispatch_shape(fetch_dir, {"FETCH_SIZE"})
+    w = _by_dispatch_shape(write_dir, {"WRITE_SIZE"})
+    mf = _by_dispatch_shape(mfma_dir, {"SQ_VALU_MFMA_BUSY_CYCLES", "GRBM_GUI_ACTIVE"}) if mfma_dir else {}
+    calib_bytes = calib_mib * (1 << 20)
+
+    def calib(agg, c):
+        best = max((max(v[c]), n) for n, v in agg.items() if "elementwise" in n[0] and c in v)
+        return calib_bytes / (best[0] * 1024.0), best[1][0]
+
+    ff, fname = calib(f, "FETCH_SIZE")
+    wf, wname = calib(w, "WRITE_SIZE")
+    root_src = os.path.join(ROOT, "paper_1804_00344_amd", "csrc")
+    rows = []
+    for key in sorted(set(f) | set(w), key=lambda k: (k[0], k[1])):
+        cls, src = _classify(key[0])
+        if cls is None:
+            continue
+        fv = f.get(key, {}).get("FETCH_SIZE", [])
+        wv = w.get(key, {}).get("WRITE_SIZE", [])
+        if not fv or not wv:
+            continue
+        fb = sum(fv) / len(fv) * 1024.0 * ff
+        wb = sum(wv) / len(wv) * 1024.0 * wf
+        busy = None
+        m = mf.get(key)
+        if m and m.get("SQ_VALU_MFMA_BUSY_CYCLES") and m.get("GRBM_GUI_ACTIVE"):
+            b = sum(m["SQ_VALU_MFMA_BUSY_CYCLES"]) / len(m["SQ_VALU_MFMA_BUSY_CYCLES"])
+            g = sum(m["GRBM_GUI_ACTIVE"]) / len(m["GRBM_GUI_ACTIVE"])
+            busy = b / (g / xcds * num_simd) if g > 0 else None
+        rows.append(dict(cls=cls, src=src, name=short(key[0]), grid=key[1], n=len(fv), fetch=fb, write=wb, busy=busy,
+                         src_hash=source_hash(os.path.join(root_src, src))))
+    md = [f"# HBM traffic and matrix-core busy fraction per kernel ({preset})", "",
+          f"Command: `{cmd}`", "",
+          f"Calibration: elementwise kernel over {calib_mib} MiB (`{short(fname)}`, reads and writes {calib_mib} MiB) "
+          f"counted {calib_bytes / ff / 2**20:.1f} MiB fetched and {calib_bytes / wf / 2**20:.1f} MiB written: fetch "
+          f"counts are scaled by {ff:.3f}, write counts by {wf:.3f}.  MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / "
+          f"(GRBM_GUI_ACTIVE / {xcds} XCDs x {num_simd} SIMDs).", "",
+          "FETCH_SIZE and WRITE_SIZE count the L2's traffic to the memory fabric.  Data that the 256 MB "
+          "Infinity Cache still holds from the previous step (the attention keys and context, the step's "
+          "own intermediates) can be served without being counted, so small working sets may count below "
+          "their algorithmic bytes; counts above them mean the kernel re-reads.",
+          "",
+          "| kernel | grid | dispatches | fetched MB | written MB | HBM MB per dispatch | MFMA busy |",
+          "|---|---:|---:|---:|---:|---:|---:|"]
+    for r in rows:
+        md.append(f"| `{r['name']}` | {r['grid']} | {r['n']} | {r['fetch'] / 1e6:.2f} | {r['write'] / 1e6:.2f} | "
+                  f"{(r['fetch'] + r['write']) / 1e6:.2f} | {'' if r['busy'] is None else format(r['busy'], '.3f')} |")
+    md += ["", "Source hashes: " + ", ".join(sorted({f"{r['src']} {r['src_hash']}" for r in rows})) + "."]
+    if json_path:
+        data = json.load(open(json_path)) if os.path.exists(json_path) else {}
+        ent = data.setdefault(preset, {})
+        for r in rows:
+            k = f"{r['cls']}@{r['grid']}"
+            ent[k] = {"kernel": r["name"], "grid": r["grid"], "bytes_per_launch": round(r["fetch"] + r["write"]),
+                      "fetch_bytes": round(r["fetch"]), "write_bytes": round(r["write"]),
+                      "mfma_busy": None if r["busy"] is None else round(r["busy"], 4),
+                      "fetch_scale": round(ff, 4), "write_scale": round(wf, 4), "source": r["src"],
+                      "source_hash": r["src_hash"], "command": cmd}
+            if r["cls"] == "vocab_gemm":
+                ent["vocab_gemm"] = dict(ent[k])
+        json.dump(data, open(json_path, "w"), indent=1, sort_keys=True)
+    return "\n".join(md) + "\n"
+
+
 def main():
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd_name", required=True)
@@ -108,6 +211,7 @@ def main():
     t.add_argument("--steps", type=float, required=True)
     t.add_argument("--title", default="Kernel trace")
     t.add_argument("--cmd", default="")
+    t.add_argument("--note", default="")
     r = sub.add_parser("traffic")
     r.add_argument("fetch_dir")
     r.add_argument("write_dir")
@@ -116,9 +220,20 @@ def main():
     r.add_argument("--kernel", required=True)
     r.add_argument("--cmd", default="")
     r.add_argument("--json")
+    c = sub.add_parser("counters")
+    c.add_argument("fetch_dir")
+    c.add_argument("write_dir")
+    c.add_argument("--mfma-dir")
+    c.add_argument("--preset", required=True)
+    c.add_argument("--calib-mib", type=int, required=True)
+    c.add_argument("--cmd", default="")
+    c.add_argument("--json")
     a = ap.parse_args()
+    if a.cmd_name == "counters":
+        sys.stdout.write(counters(a.fetch_dir, a.write_dir, a.mfma_dir, a.preset, a.calib_mib, a.cmd, a.json))
+        return
     if a.cmd_name == "trace":
-        sys.stdout.write(trace(a.dir, a.steps, a.title, a.cmd))
+        sys.stdout.write(trace(a.dir, a.steps, a.title, a.cmd, a.note))
     else:
         sys.stdout.write(traffic(a.fetch_dir, a.write_dir, a.preset, a.calib_mib, a.kernel, a.cmd, a.json))
 
