@@ -263,13 +263,10 @@ WsLayout ws_layout(const mt_model *m, int B, int K) {
   L.ccnt = take(M * L.ntiles * vocab_lists() * sizeof(int));
   L.lse = take(M * 4);
   L.rowc = take(M * K * sizeof(int2));
-  // chunks of a materialised row for the first selection level: about 3072 workgroups in all
-  // (each then runs K block-wide extraction rounds over its per-thread lists, so fewer,
-  // longer chunks cost less), at least 256 entries (one per thread) each
+  // chunks of a materialised row for the first selection level
   {
-    const long want = (3072 + (long)M - 1) / (long)M;
-    const long most = std::max(1L, std::min(64L, (long)c.V / 256));
-    L.nchunks = (int)std::max(1L, std::min(want, most));
+    int chunk = 0;
+    topk_scan_shape((int)M, c.V, &chunk, &L.nchunks);
   }
   L.scand = take(M * L.nchunks * K * sizeof(int2));
   L.scnt = take((size_t)B * sizeof(int));

@@ -539,6 +539,9 @@ struct RowSelect {
   unsigned long long *nrecompute;  // optional: counts the rows recomputed exactly
 };
 hipError_t launch_row_select(const RowSelect &a, hipStream_t st);
+// Chunks of one row of a materialised logp for the first selection level (both the workspace
+// layout and the launch take them from here).
+void topk_scan_shape(int M, int V, int *chunk, int *nchunks);
 // Block (0, 0) also clears the B sentence arrival counters scnt.
 hipError_t launch_topk_scan_logp(int M, int K, int V, int nchunks, const float *prev_score,
                                  const float *logp, int2 *cand_out, int *scnt, int B, hipStream_t st);

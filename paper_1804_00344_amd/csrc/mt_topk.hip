@@ -17,6 +17,7 @@
 // chain longer than one min/max reduction.
 #include "mt_internal.h"
 
+#include <algorithm>
 #include <type_traits>
 
 namespace mt {
@@ -281,88 +282,180 @@ __global__ __launch_bounds__(kTT) void row_select_kernel(RowSelect a) {
   if (t == 0) __hip_atomic_store(a.scnt + b, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Level 1 for a materialised logp: the best K keys score + logp[v] of one chunk of a row.
-template <int KMAX>
+// Level 1 for a materialised logp: the best K keys score + logp[v] of one chunk of a row (at
+// most kScanKU * kTT entries, so the whole chunk is read once and stays in registers, as
+// order-preserving key codes; VEC: 16-byte loads, the chunk start and the row 16-byte
+// aligned).  A wave's K-th largest lane maximum bounds its K best keys from below (K of its
+// keys reach it), so only keys at or above it are appended to a wave-private LDS list (ballot
+// ranks); each wave then selects its K best exactly by bisection over the codes (wave_topk),
+// and the first wave merges the four waves' selections the same way.  More than kCap keys at
+// or above the bound (ties) are selected from the registers directly.  A chunk with fewer
+// than K entries fills the rest of its K slots with no-token entries.
+constexpr int kScanKU = 32;  // entries per thread of a chunk
+
+// Rank of this lane's entry (code mu, index mi) among the n entries held by lanes 0..n-1 (n
+// wave-uniform, at most 64): the number of entries that come before it in the order (larger
+// code, then smaller index).  With distinct indices the ranks of the n entries are 0..n-1.
+__device__ __forceinline__ int wave_rank_small(uint32_t mu, int mi, int n) {
+  int rank = 0;
+  for (int j = 0; j < n; ++j) {
+    const uint32_t ou = __builtin_amdgcn_readlane(mu, j);
+    const int oi = __builtin_amdgcn_readlane(mi, j);
+    rank += (ou > mu || (ou == mu && oi < mi)) ? 1 : 0;
+  }
+  return rank;
+}
+template <int KMAX, bool VEC>
 __global__ __launch_bounds__(kTT) void topk_scan_logp_kernel(int M, int K, int V, int chunk,
                                                              const float *__restrict__ prev_score,
                                                              const float *__restrict__ logp,
                                                              int2 *__restrict__ cand_out, int *scnt, int B) {
+  constexpr int kCap = 256;
+  __shared__ uint32_t pk[4][kCap];
+  __shared__ int pi[4][kCap];
+  __shared__ uint32_t wsu[4][KMAX];
+  __shared__ int wsi[4][KMAX];
+  __shared__ uint32_t qu[4][KMAX];
+  __shared__ int qi[4][KMAX];
+  __shared__ int qn[4];
   const int m = blockIdx.y, ch = blockIdx.x, nch = gridDim.x;
+  const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
   if (m == 0 && ch == 0)
-    for (int i = threadIdx.x; i < B; i += kTT) __hip_atomic_store(scnt + i, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    for (int i = t; i < B; i += kTT) __hip_atomic_store(scnt + i, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   const float sc = prev_score[m];
   const float *row = logp + (size_t)m * V;
   const int v0 = ch * chunk, v1 = min(V, v0 + chunk);
-  // A wave's K-th largest lane maximum bounds its K best keys from below (K of its keys reach
-  // it), so a key under it is never among the chunk's K best: only keys at or above it enter
-  // the per-thread lists, whose insertions would otherwise dominate.  Both passes form the
-  // key the same way.  Each pass issues kU loads per thread before it uses any of them; a
-  // chunk of at most kU * kTT entries stays in registers between the passes, a longer one is
-  // read again (from cache).
-  constexpr int kU = 16;
-  const bool resident = v1 - v0 <= kU * kTT;
-  uint32_t mx[1] = {0u};
-  float x[kU];
-  for (int b0 = v0; b0 < v1; b0 += kU * kTT) {  // the same trip count for every lane
-    const int base = b0 + threadIdx.x;
+  // entry q of this thread: VEC, vector g = q / 4 of 4 consecutive entries; else one entry
+  auto idx_of = [&](int q) { return VEC ? v0 + 4 * (t + (q >> 2) * kTT) + (q & 3) : v0 + t + q * kTT; };
+  // keys sc + logp in registers; entries past the chunk end are -inf and never taken (an
+  // entry is taken only when its key is at least the wave's bound, which is a real key)
+  float key[kScanKU];
+  if constexpr (VEC) {
 #pragma unroll
-    for (int q = 0; q < kU; ++q) x[q] = base + q * kTT < v1 ? row[base + q * kTT] : 0.f;
-#pragma unroll
-    for (int q = 0; q < kU; ++q)
-      if (base + q * kTT < v1) {
-        const uint32_t c = key_code(sc + x[q]);
-        mx[0] = c > mx[0] ? c : mx[0];
+    for (int g = 0; g < kScanKU / 4; ++g) {
+      const int i0 = v0 + 4 * (t + g * kTT);
+      float4 xv = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (i0 + 3 < v1) {
+        xv = *(const float4 *)(row + i0);
+      } else if (i0 < v1) {  // the chunk's ragged end
+        xv.x = row[i0];
+        if (i0 + 1 < v1) xv.y = row[i0 + 1];
+        if (i0 + 2 < v1) xv.z = row[i0 + 2];
       }
+      key[4 * g + 0] = i0 + 0 < v1 ? sc + xv.x : -INFINITY;
+      key[4 * g + 1] = i0 + 1 < v1 ? sc + xv.y : -INFINITY;
+      key[4 * g + 2] = i0 + 2 < v1 ? sc + xv.z : -INFINITY;
+      key[4 * g + 3] = i0 + 3 < v1 ? sc + xv.w : -INFINITY;
+    }
+  } else {
+#pragma unroll
+    for (int q = 0; q < kScanKU; ++q) key[q] = idx_of(q) < v1 ? sc + row[idx_of(q)] : -INFINITY;
   }
-  const uint32_t tau = wave_count_ge<1>(mx, 1, 1u) >= K ? wave_kth_code<1>(mx, 1, K) : 0u;
-  // The keys that pass are appended to a wave-private LDS list (ballot ranks), so each lane
-  // then inserts about one of them into its sorted list: the insertion is straight-line
-  // register code, which would otherwise run for every key.  More than kCap passing keys
-  // (ties at the bound) take the direct route instead.
-  constexpr int kCap = 256;
-  __shared__ float pk[4][kCap];
-  __shared__ int pi[4][kCap];
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  // lane maximum over the lane's real entries, as a code (0: none)
+  float lm = -INFINITY;
+  bool any = false;
+#pragma unroll
+  for (int q = 0; q < kScanKU; ++q) {
+    lm = fmaxf(lm, key[q]);
+    any |= idx_of(q) < v1;
+  }
+  uint32_t mx[1] = {any ? key_code(lm) : 0u};
+  // the bound: the K-th largest lane maximum (with fewer than K lanes holding entries, the
+  // smallest real key: every entry is then taken)
+  const bool enough = wave_count_ge<1>(mx, 1, 1u) >= K;
+  uint32_t tau = enough ? wave_kth_code<1>(mx, 1, K) : 1u;
+  const float tauf = key_from_code(tau < 1u ? 1u : tau);
   const uint64_t lt = (1ull << lane) - 1ull;
   int npass = 0;  // wave-uniform
-  for (int b0 = v0; b0 < v1; b0 += kU * kTT) {  // the same trip count for every lane
-    const int base = b0 + threadIdx.x;
-    if (!resident)
 #pragma unroll
-      for (int q = 0; q < kU; ++q) x[q] = base + q * kTT < v1 ? row[base + q * kTT] : 0.f;
-#pragma unroll
-    for (int q = 0; q < kU; ++q) {
-      const float key = sc + x[q];
-      const bool pass = base + q * kTT < v1 && key_code(key) >= tau;
-      const uint64_t bal = __ballot(pass);
+  for (int q = 0; q < kScanKU; ++q) {
+    const bool pass = idx_of(q) < v1 && (enough ? key[q] >= tauf : true);
+    const uint64_t bal = __ballot(pass);
+    if (bal) {  // uniform: most entries of most waves stay under the bound
       const int slot = npass + __popcll(bal & lt);
       if (pass && slot < kCap) {
-        pk[wv][slot] = key;
-        pi[wv][slot] = base + q * kTT;
+        pk[wv][slot] = key_code(key[q]);
+        pi[wv][slot] = idx_of(q);
       }
       npass += __popcll(bal);
     }
   }
-  __syncthreads();  // the appended keys are read by other lanes of the wave
-  List<KMAX> lst;
-  lst.init();
-  if (npass <= kCap) {
-    for (int j = lane; j < npass; j += 64) lst.push(pk[wv][j], pi[wv][j]);
-  } else {
-    for (int b0 = v0; b0 < v1; b0 += kU * kTT) {
-      const int base = b0 + threadIdx.x;
-      if (!resident)
-#pragma unroll
-        for (int q = 0; q < kU; ++q) x[q] = base + q * kTT < v1 ? row[base + q * kTT] : 0.f;
-#pragma unroll
-      for (int q = 0; q < kU; ++q) {
-        const float key = sc + x[q];
-        if (base + q * kTT < v1 && key_code(key) >= tau) lst.push(key, base + q * kTT);
-      }
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  // this wave's K best, by rank, into qu/qi
+  auto keep = [&](int rank, float key, int idx) {
+    qu[wv][rank] = key_code(key);
+    qi[wv][rank] = idx;
+  };
+  int ns;
+  if (npass <= 64) {  // the usual case: one appended key per lane, ranked directly
+    const bool has = lane < npass;
+    const uint32_t mu = has ? pk[wv][lane] : 0u;
+    const int mi = has ? pi[wv][lane] : 0x7fffffff;
+    const int rank = wave_rank_small(mu, mi, npass);
+    if (has && rank < K) {
+      qu[wv][rank] = mu;
+      qi[wv][rank] = mi;
     }
+    ns = npass < K ? npass : K;
+  } else if (npass <= kCap) {
+    constexpr int R = kCap / 64;
+    uint32_t cu[R];
+    int ci[R];
+    const int rs = (npass + 63) / 64;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const int j = r * 64 + lane;
+      const bool ok = j < npass;
+      cu[r] = ok ? pk[wv][j] : 0u;
+      ci[r] = ok ? pi[wv][j] : 0x7fffffff;
+    }
+    ns = wave_topk<R>(cu, ci, rs, K, wsu[wv], wsi[wv], keep);
+  } else {  // more than kCap keys at or above the bound (ties): select from the registers
+    uint32_t u[kScanKU];
+    int ix[kScanKU];
+#pragma unroll
+    for (int q = 0; q < kScanKU; ++q) {
+      ix[q] = idx_of(q);
+      u[q] = ix[q] < v1 ? key_code(key[q]) : 0u;
+    }
+    ns = wave_topk<kScanKU>(u, ix, kScanKU, K, wsu[wv], wsi[wv], keep);
   }
+  if (lane == 0) qn[wv] = ns;
+  __syncthreads();
+  if (wv != 0) return;
+  // the first wave merges the four selections (at most 4 K <= 64 entries, one per lane)
+  int base = 0, src = -1, r = 0;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    if (src < 0 && lane < base + qn[w]) {
+      src = w;
+      r = lane - base;
+    }
+    base += qn[w];
+  }
+  const uint32_t mu = src >= 0 ? qu[src][r] : 0u;
+  const int mi = src >= 0 ? qi[src][r] : 0x7fffffff;
   int2 *o = cand_out + (size_t)m * K * nch + ch;  // entry r at o[r * nch] (entry-major per row)
-  block_extract<KMAX>(lst, K, [&](int r, float v, int i) { o[(size_t)r * nch] = make_int2(__float_as_int(v), i); });
+  const int rank = wave_rank_small(mu, mi, base);  // base = the four selections' entries (<= 4 K)
+  if (src >= 0 && rank < K) o[(size_t)rank * nch] = make_int2(__float_as_int(key_from_code(mu)), mi);
+  const int nsel = base < K ? base : K;
+  if (lane >= nsel && lane < K) o[(size_t)lane * nch] = make_int2(0, -1);  // no entry
+}
+
+// chunks of a materialised row: at most kScanKU * kTT entries each (register-resident), a
+// multiple of 1024 (16-byte aligned starts), and for few rows enough chunks for about 3072
+// workgroups in all
+void topk_scan_shape(int M, int V, int *chunk, int *nchunks) {
+  const long nmin = ((long)V + kScanKU * kTT - 1) / (kScanKU * kTT);
+  const long want = (3072 + (long)M - 1) / (M > 0 ? M : 1);
+  const long most = ((long)V + 1023) / 1024;
+  const long n = std::max(nmin, std::min(want, most));
+  long c = ((long)V + n - 1) / n;
+  c = (c + 1023) / 1024 * 1024;
+  *chunk = (int)c;
+  *nchunks = (int)(((long)V + c - 1) / c);
 }
 
 static int kbucket(int K) { return K <= 1 ? 1 : K <= 2 ? 2 : K <= 4 ? 4 : K <= 8 ? 8 : 16; }
@@ -392,8 +485,17 @@ hipError_t launch_row_select(const RowSelect &a, hipStream_t st) {
 hipError_t launch_topk_scan_logp(int M, int K, int V, int nchunks, const float *prev_score,
                                  const float *logp, int2 *cand_out, int *scnt, int B, hipStream_t st) {
   if (M == 0) return hipSuccess;
-  const int chunk = (V + nchunks - 1) / nchunks;
-#define MT_TS(N) hipLaunchKernelGGL((topk_scan_logp_kernel<N>), dim3(nchunks, M), dim3(kTT), 0, st, M, K, V, chunk, prev_score, logp, cand_out, scnt, B)
+  int chunk = 0, nch = 0;
+  topk_scan_shape(M, V, &chunk, &nch);
+  if (nch != nchunks) return hipErrorInvalidValue;  // the workspace holds nchunks lists per row
+  const bool vec = V % 4 == 0 && ((uintptr_t)logp & 15) == 0;
+#define MT_TS(N)                                                                                               \
+  if (vec)                                                                                                     \
+    hipLaunchKernelGGL((topk_scan_logp_kernel<N, true>), dim3(nch, M), dim3(kTT), 0, st, M, K, V, chunk,        \
+                       prev_score, logp, cand_out, scnt, B);                                                   \
+  else                                                                                                         \
+    hipLaunchKernelGGL((topk_scan_logp_kernel<N, false>), dim3(nch, M), dim3(kTT), 0, st, M, K, V, chunk,       \
+                       prev_score, logp, cand_out, scnt, B);
   MT_KSWITCH(K, MT_TS)
 #undef MT_TS
   return hipGetLastError();
