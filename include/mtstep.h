@@ -267,6 +267,34 @@ mt_status mt_beam_topk(mt_model *model, int B, int K, const float *prev_score, c
 mt_status mt_ensemble_logp(mt_model *model, int n, const float *const *logp, const float *weights, int M,
                            float *out, void *stream);
 
+/* Fused ensemble step (Section 2.3: ensembling inside batched beam search).  The combined
+ * log-probability sum_i w_i logp_i(v) = sum_i w_i logit_i(v) - C, with C = sum_i w_i LSE_i a
+ * per-row constant, so the members never materialise their log-probabilities:
+ *   mt_ensemble_step: member `member` of n_members (called for 0, 1, ... in order) runs its
+ *     decoder step (mt_decoder_step's arguments and state outputs) and writes weight * its
+ *     logits (t Wo + bo) into comb_logits [B*K, V] fp32 device memory (member 0 stores, later
+ *     members add, fp32, in member order); its log-sum-exp partials stay in its workspace ws.
+ *     The last member (member = n_members - 1) also collects the beam candidates, on the
+ *     combined values it stores; the others skip the candidate threshold.  weight finite and
+ *     nonzero; 1 <= n_members <= 8; not for dual-source models (MT_ERR_STATE).
+ *   mt_ensemble_topk: C[m] = sum_i weights[i] * LSE_i[m] (from the partials each member's
+ *     mt_ensemble_step left in ws[i], which must be that call's workspace, of ws_bytes[i], and
+ *     weights[i] that call's weight), then the beam selection of mt_beam_topk on the keys
+ *     (prev_score - C) + comb_logits, from the last member's candidates (a row whose
+ *     candidates overflow is selected from comb_logits): score_out = prev_score + sum_i w_i
+ *     logp_i up to rounding.  models, weights, ws, ws_bytes: HOST arrays of the n members
+ *     (same V, k_max >= K); row_const_out [B*K] or NULL receives C.  The selection's scratch
+ *     lives in ws[n-1].  MT_ERR_STATE unless the members' last calls were exactly these
+ *     ensemble steps.  1 <= n <= 8.  Asynchronous. */
+mt_status mt_ensemble_step(mt_model *model, int member, int n_members, float weight, int B, int K, int S,
+                           const int32_t *prev_tok, const int32_t *src_row, int n_state_rows, const float *state_in,
+                           const void *ctx, const void *pctx, const float *mask, float *state_out,
+                           float *comb_logits, void *ws, size_t ws_bytes, void *stream);
+mt_status mt_ensemble_topk(int n, mt_model *const *models, const float *weights, void *const *ws,
+                           const size_t *ws_bytes, int B, int K, const float *prev_score, const float *comb_logits,
+                           float *score_out, int32_t *tok_out, int32_t *bp_out, int32_t *row_out, float *row_const_out,
+                           void *stream);
+
 /* Translation bookkeeping after mt_beam_topk of step `step` (batched beam search decoding
  * to an n-best list as large as the beam, Sections 2.3 and 3.1.3).  Per sentence b:
  *   beam[b] (device int32 [B], in/out): K minus the hypotheses b has finished (start: K);
@@ -321,7 +349,7 @@ typedef enum {
   MT_KERNEL_PRECOMPUTE = 10,
   MT_KERNEL_VOCAB_THRESHOLD = 11, /* logits of the first vocabulary entries -> candidate threshold */
   MT_KERNEL_GEMM_TRANSITION = 12, /* s Ut_j of the transition blocks (dec_transitions > 0) */
-  MT_KERNEL_ENSEMBLE = 13,  /* mt_ensemble_logp */
+  MT_KERNEL_ENSEMBLE = 13,  /* mt_ensemble_logp; the row constant of mt_ensemble_topk */
   MT_KERNEL_BEAM_FINISH = 14, /* mt_beam_finish */
   MT_KERNEL_ENCODE = 15,    /* every kernel of mt_encode */
   MT_KERNEL_COUNT = 16

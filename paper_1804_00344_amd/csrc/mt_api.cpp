@@ -99,6 +99,8 @@ struct mt_model {
   // call-order state for mt_beam_topk(logp = NULL)
   int last_B = -1, last_K = -1;
   const void *last_ws = nullptr;
+  int last_ens_n = 0;      // the last step ran as the last of this many fused-ensemble members (0: not)
+  float last_ens_w = 0.f;  // and with this weight
   // profiling
   uint32_t prof_mask = 0;
   ProfSlot prof[MT_KERNEL_COUNT];
@@ -868,11 +870,16 @@ mt_status mt_precompute_ctx_noalloc(mt_model *model, int B, int S, const void *c
 }
 
 // The step, with an optional second source (S2 > 0: dual-source models)
+// ens_w != 0: a fused-ensemble member: logp_out receives ens_w * logits, added to what it holds
+// when ens_acc, and is not turned into log-probabilities.  Only the last member (ens_last: the
+// ensemble's size) collects beam candidates, on the combined values it stores; the others
+// skip the threshold pass and write only their log-sum-exp partials.
 static mt_status decoder_step_impl(mt_model *model, int B, int K, int S, const int32_t *prev_tok,
                                    const int32_t *src_row, int n_state_rows, const float *state_in,
                                    const void *ctx, const void *pctx, const float *mask, int S2, const void *ctx2,
                                    const void *pctx2, const float *mask2, float *state_out, float *logp_out,
-                                   float *attn_out, const mt_taps *taps, void *ws, size_t ws_bytes, void *stream) {
+                                   float *attn_out, const mt_taps *taps, void *ws, size_t ws_bytes, void *stream,
+                                   float ens_w = 0.f, int ens_acc = 0, int ens_last = 0) {
   const mt_config &c = model->cfg;
   if (B < 1 || K < 1 || K > c.k_max || K > c.V || S < 1 || S > 1024)
     return fail(MT_ERR_SHAPE, "B=%d K=%d S=%d: need B >= 1, 1 <= K <= k_max=%d, 1 <= S <= 1024", B, K, S, c.k_max);
@@ -989,25 +996,32 @@ static mt_status decoder_step_impl(mt_model *model, int B, int K, int S, const i
   // vocabulary projection: threshold pass, then the full pass with fused log-sum-exp partials
   // and threshold-filtered beam candidates
   float2 *part = (float2 *)(W + L.part);
-  {
+  const bool ens = ens_w != 0.f;
+  const bool want_cand = !ens || ens_last > 0;
+  if (want_cand) {
     const int S = vocab_sample_size(V);
     GemmProblem ps{};
     ps.A = t; ps.a_rows = M; ps.lda = E; ps.a_bf16 = bf;
     ps.Bp = model->wsamp.p; ps.ldb = model->wsamp.ldb; ps.wblk = model->wsamp.blk; ps.bias = model->bo_pad;
     ps.out = W + L.sample; ps.ldc = S; ps.M = M; ps.N = S; ps.K = E;
     LAUNCH(MT_KERNEL_VOCAB_THRESHOLD, launch_gemm(bf, &ps, 1, EPI_STORE, st));
-    LAUNCH(MT_KERNEL_VOCAB_THRESHOLD, launch_vocab_threshold(M, V, K, (const float *)(W + L.sample),
-                                                             (float *)(W + L.thr), (int *)(W + L.scnt), B, st));
+    LAUNCH(MT_KERNEL_VOCAB_THRESHOLD,
+           launch_vocab_threshold(M, V, K, (const float *)(W + L.sample), (float *)(W + L.thr), (int *)(W + L.scnt),
+                                  B, st, ens && ens_acc ? logp_out : nullptr, ens ? ens_w : 1.f));
   }
   LAUNCH(MT_KERNEL_VOCAB_GEMM, launch_vocab(bf, t, model->wo_frag, model->bo_pad, M, V, E, L.ntiles,
-                                            (const float *)(W + L.thr), part, (int2 *)(W + L.cbuf),
-                                            (int *)(W + L.ccnt), kVocabCap, logp_out, model->logit_bounded, st));
+                                            want_cand ? (const float *)(W + L.thr) : nullptr, part,
+                                            (int2 *)(W + L.cbuf), (int *)(W + L.ccnt), kVocabCap, logp_out,
+                                            model->logit_bounded, st, ens ? ens_w : 1.f, ens_acc, ens ? 1 : 0));
   // the row log-sum-exp is merged by the beam selection itself; this pass only turns the
   // written logits into log-probabilities
-  if (logp_out) LAUNCH(MT_KERNEL_LSE, launch_lse(M, L.ntiles, part, (float *)(W + L.lse), logp_out, V, st));
+  if (logp_out && !ens)
+    LAUNCH(MT_KERNEL_LSE, launch_lse(M, L.ntiles, part, (float *)(W + L.lse), logp_out, V, st));
   model->last_B = B;
   model->last_K = K;
   model->last_ws = ws;
+  model->last_ens_n = ens ? ens_last : 0;
+  model->last_ens_w = ens_w;
   return MT_OK;
 }
 
@@ -1038,6 +1052,89 @@ mt_status mt_decoder_step_dual(mt_model *model, int B, int K, int S, const int32
   CHECK(check_dev_ptr(mask2, "mask2", 4));
   return decoder_step_impl(model, B, K, S, prev_tok, src_row, n_state_rows, state_in, ctx, pctx, mask, S2, ctx2,
                            pctx2, mask2, state_out, logp_out, attn_out, taps, ws, ws_bytes, stream);
+}
+
+mt_status mt_ensemble_step(mt_model *model, int member, int n_members, float weight, int B, int K, int S,
+                           const int32_t *prev_tok,
+                           const int32_t *src_row, int n_state_rows, const float *state_in, const void *ctx,
+                           const void *pctx, const float *mask, float *state_out, float *comb_logits, void *ws,
+                           size_t ws_bytes, void *stream) {
+  g_err[0] = 0;
+  if (!valid_model(model)) return fail(MT_ERR_ARG, "invalid model handle");
+  if (model->cfg.dual_source) return fail(MT_ERR_STATE, "dual-source model: not supported in a fused ensemble");
+  if (n_members < 1 || n_members > kMaxEnsemble)
+    return fail(MT_ERR_ARG, "n_members=%d: need 1..%d", n_members, kMaxEnsemble);
+  if (member < 0 || member >= n_members) return fail(MT_ERR_ARG, "member=%d: need 0..%d", member, n_members - 1);
+  if (!(weight != 0.f && std::isfinite(weight))) return fail(MT_ERR_ARG, "weight must be finite and nonzero");
+  CHECK(check_dev_ptr(comb_logits, "comb_logits", 4));
+  return decoder_step_impl(model, B, K, S, prev_tok, src_row, n_state_rows, state_in, ctx, pctx, mask, 0, nullptr,
+                           nullptr, nullptr, state_out, comb_logits, nullptr, nullptr, ws, ws_bytes, stream, weight,
+                           member > 0 ? 1 : 0, member == n_members - 1 ? n_members : 0);
+}
+
+mt_status mt_ensemble_topk(int n, mt_model *const *models, const float *weights, void *const *ws,
+                           const size_t *ws_bytes, int B, int K, const float *prev_score, const float *comb_logits,
+                           float *score_out, int32_t *tok_out, int32_t *bp_out, int32_t *row_out, float *row_const_out,
+                           void *stream) {
+  g_err[0] = 0;
+  if (n < 1 || n > kMaxEnsemble) return fail(MT_ERR_SHAPE, "n=%d: need 1..%d members", n, kMaxEnsemble);
+  if (!models || !weights || !ws || !ws_bytes) return fail(MT_ERR_ARG, "models, weights, ws or ws_bytes is NULL");
+  mt_model *lead = models[0];
+  if (!valid_model(lead)) return fail(MT_ERR_ARG, "invalid model handle (member 0)");
+  const mt_config &c = lead->cfg;
+  if (B < 1 || K < 1 || K > c.k_max || K > c.V) return fail(MT_ERR_SHAPE, "B=%d K=%d: need B >= 1, 1 <= K <= k_max", B, K);
+  if ((long long)B * K > (1 << 20)) return fail(MT_ERR_SHAPE, "B*K exceeds 2^20");
+  CHECK(check_dev_ptr(prev_score, "prev_score", 4));
+  CHECK(check_dev_ptr(comb_logits, "comb_logits"));
+  CHECK(check_dev_ptr(score_out, "score_out", 4));
+  CHECK(check_dev_ptr(tok_out, "tok_out", 4));
+  CHECK(check_dev_ptr(bp_out, "bp_out", 4));
+  if (row_out) CHECK(check_dev_ptr(row_out, "row_out", 4));
+  if (row_const_out) CHECK(check_dev_ptr(row_const_out, "row_const_out", 4));
+  EnsembleConst ec{};
+  ec.n = n;
+  for (int i = 0; i < n; ++i) {
+    mt_model *mi = models[i];
+    if (!valid_model(mi)) return fail(MT_ERR_ARG, "invalid model handle (member %d)", i);
+    if (mi->cfg.V != c.V || mi->cfg.k_max < K) return fail(MT_ERR_SHAPE, "member %d: V or k_max differs", i);
+    if (!std::isfinite(weights[i]) || weights[i] == 0.f) return fail(MT_ERR_ARG, "weights[%d] must be finite and nonzero", i);
+    CHECK(check_dev_ptr(ws[i], "ws[i]", 256));
+    const WsLayout Li = ws_layout(mi, B, K);
+    if (ws_bytes[i] < Li.total) return fail(MT_ERR_WORKSPACE, "ws[%d]: %zu bytes < %zu needed", i, ws_bytes[i], Li.total);
+    if (mi->last_B != B || mi->last_K != K || mi->last_ws != ws[i] || mi->last_ens_w != weights[i])
+      return fail(MT_ERR_STATE, "member %d: no preceding mt_ensemble_step with this B, K, weight and workspace", i);
+    if ((mi->last_ens_n != 0) != (i == n - 1) || (i == n - 1 && mi->last_ens_n != n))
+      return fail(MT_ERR_STATE, "member %d: its mt_ensemble_step was not called as member %d of %d", i, i, n);
+    ec.part[i] = (const float2 *)((const char *)ws[i] + Li.part);
+    ec.ntiles[i] = Li.ntiles;
+    ec.w[i] = weights[i];
+  }
+  // the candidates are the last member's (collected on the combined values), and so is the
+  // selection's scratch
+  mt_model *model = models[n - 1];  // profiling slot
+  hipStream_t st = (hipStream_t)stream;
+  const WsLayout L = ws_layout(model, B, K);
+  char *W = (char *)ws[n - 1];
+  const int M = B * K, V = c.V;
+  float *prev_adj = (float *)(W + L.lse);  // prev_score - C, in the row log-sum-exp slot
+  ec.prev = prev_score;
+  ec.prev_adj = prev_adj;
+  ec.row_const = row_const_out;
+  LAUNCH(MT_KERNEL_ENSEMBLE, launch_ensemble_const(ec, M, st));
+  RowSelect rs{};
+  rs.B = B; rs.K = K; rs.V = V;
+  rs.nl = L.ntiles * vocab_lists(); rs.cap = kVocabCap;
+  rs.cnt = (const int *)(W + L.ccnt);
+  rs.cbuf = (const int2 *)(W + L.cbuf);
+  rs.prev_score = prev_adj;
+  rs.comb = comb_logits;
+  rs.bf16_mma = model->bf16;
+  rs.row_cand = (int2 *)(W + L.rowc);
+  rs.scnt = (int *)(W + L.scnt);
+  rs.score_out = score_out; rs.tok_out = tok_out; rs.bp_out = bp_out; rs.row_out = row_out;
+  rs.nrecompute = model->nrecompute;
+  LAUNCH(MT_KERNEL_TOPK, launch_row_select(rs, st));
+  return MT_OK;
 }
 
 mt_status mt_precompute_keys2(mt_model *model, int B, int S2, const void *ctx2, const float *mask2,
@@ -1092,6 +1189,8 @@ mt_status mt_beam_topk(mt_model *model, int B, int K, const float *prev_score, c
   if (ws_bytes < L.total) return fail(MT_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, L.total);
   if (!logp && (model->last_B != B || model->last_K != K || model->last_ws != ws))
     return fail(MT_ERR_STATE, "no preceding mt_decoder_step with this B, K and workspace (pass logp instead)");
+  if (!logp && model->last_ens_w != 0.f)
+    return fail(MT_ERR_STATE, "the preceding step was a fused-ensemble member's (select with mt_ensemble_topk)");
   hipStream_t st = (hipStream_t)stream;
   char *W = (char *)ws;
   const int M = B * K, V = c.V;

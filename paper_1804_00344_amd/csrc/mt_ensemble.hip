@@ -3,7 +3,9 @@
 // before one beam selection,
 //   out[i] = sum_j w_j * logp_j[i],  i < M * V, members in order j = 0, 1, ...
 // A pure stream: each element is read once from every member and written once, so the kernel
-// is bound by HBM bandwidth ((n + 1) * 4 bytes per element).  Every thread takes 16-byte
+// is bound by HBM bandwidth ((n + 1) * 4 bytes per element).  (The fused ensemble path instead
+// adds each member's weighted logits in its vocabulary kernel and subtracts the per-row
+// constant sum_i w_i LSE_i at selection: ensemble_const_kernel below.)  Every thread takes 16-byte
 // granules in a grid-stride loop and issues the loads of all members before the sums.
 #include "mt_internal.h"
 
@@ -75,6 +77,28 @@ hipError_t launch_ensemble(int n, const float *const *in, const float *w, long l
     default: MT_EN(8); break;
   }
 #undef MT_EN
+  return hipGetLastError();
+}
+
+// Row constant of a fused ensemble (see EnsembleConst): one 256-thread workgroup per row; each
+// member's log-sum-exp is merged by the same routine, in the same order, as the beam selection
+// merges a row's partials.
+__global__ __launch_bounds__(256) void ensemble_const_kernel(EnsembleConst a) {
+  const int m = blockIdx.x;
+  float c = 0.f;
+  for (int i = 0; i < a.n; ++i) {
+    const float L = block_row_lse(a.part[i] + (size_t)m * a.ntiles[i], a.ntiles[i]);
+    c = __builtin_fmaf(a.w[i], L, c);
+  }
+  if (threadIdx.x == 0) {
+    a.prev_adj[m] = a.prev[m] - c;
+    if (a.row_const) a.row_const[m] = c;
+  }
+}
+
+hipError_t launch_ensemble_const(const EnsembleConst &a, int M, hipStream_t st) {
+  if (M == 0) return hipSuccess;
+  hipLaunchKernelGGL(ensemble_const_kernel, dim3(M), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 

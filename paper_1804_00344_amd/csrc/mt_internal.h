@@ -16,6 +16,7 @@ typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
 constexpr int kWave = 64;
 constexpr int kXcds = 8;
 constexpr int kKMax = 16;  // largest supported beam
+constexpr int kMaxEnsemble = 8;  // members of an ensemble
 
 // ---------------------------------------------------------------------------------------
 // device helpers
@@ -427,15 +428,36 @@ void vocab_pack_host(int bf16_mma, int V, int E, const float *src, int src_is_em
 // minus a rounding margin, S = vocab_sample_size(V);
 // sample [M][S] holds the logits of the first S vocabulary entries (computed by launch_gemm)
 // Block 0 also clears the B sentence arrival counters scnt of the following beam selection.
+// A fused ensemble's last member takes it over its combined values instead: w * sample[m][v],
+// plus comb[m][v] (comb [M][V], the earlier members' weighted logits) if comb is not NULL.
 hipError_t launch_vocab_threshold(int M, int V, int K, const float *sample, float *thr, int *scnt, int B,
-                                  hipStream_t st);
+                                  hipStream_t st, const float *comb = nullptr, float w = 1.f);
 // part [M][n_chunks] (reference m, sum exp(l - m)); every logit >= thr[m] goes to cbuf
 // [M][cap][n_chunks * lists] (entry-major per row) with counts in ccnt [M][n_chunks][lists] (a count above cap marks
 // an overflowed list); logits [M][V] or NULL.  fixed_ref: the caller has proven every logit
 // lies in [-40, 40], so the reference is 0 and no running maximum is kept.
+// logits_w, logits_acc: the logits are stored multiplied by logits_w, and added to the values
+// already in logits when logits_acc (the members of a fused ensemble).  cap_stored (with
+// logits): the candidates are the stored values rather than the logits (the last member).
+// thr NULL: no candidates (the partials are still written).
 hipError_t launch_vocab(int bf16_mma, const void *t, const void *wp, const float *bias_pad, int M, int V,
                         int E, int n_chunks, const float *thr, float2 *part, int2 *cbuf, int *ccnt, int cap,
-                        float *logits, int fixed_ref, hipStream_t st);
+                        float *logits, int fixed_ref, hipStream_t st, float logits_w = 1.f, int logits_acc = 0,
+                        int cap_stored = 0);
+
+// Fused ensemble: per row m, C[m] = sum_i w[i] * LSE_i[m] (LSE_i merged from member i's partials
+// part[i] [M][ntiles[i]] exactly as the beam selection merges a row's), prev_adj[m] =
+// prev[m] - C[m], and row_const[m] = C[m] if given.
+struct EnsembleConst {
+  int n;
+  const float2 *part[kMaxEnsemble];
+  int ntiles[kMaxEnsemble];
+  float w[kMaxEnsemble];
+  const float *prev;
+  float *prev_adj;
+  float *row_const;
+};
+hipError_t launch_ensemble_const(const EnsembleConst &a, int M, hipStream_t st);
 constexpr int kVocabCap = 32;  // candidate buffer entries per (row, chunk, list)
 constexpr int kVocabPad = 64;  // vocabulary rows are padded to a multiple of this
 
@@ -504,7 +526,6 @@ hipError_t launch_beam_finish(const BeamFinish &a, int B, hipStream_t st);
 
 // ensemble combination out[i] = sum_j w[j] * in[j][i] over count elements (16-byte aligned
 // buffers; out may be one of the inputs); 1 <= n <= kMaxEnsemble
-constexpr int kMaxEnsemble = 8;
 hipError_t launch_ensemble(int n, const float *const *in, const float *w, long long count, float *out,
                            int num_cu, hipStream_t st);
 
@@ -537,6 +558,10 @@ struct RowSelect {
   float *score_out;
   int32_t *tok_out, *bp_out, *row_out;
   unsigned long long *nrecompute;  // optional: counts the rows recomputed exactly
+  // A fused ensemble's combined values [M][V] (or NULL).  With it the candidates are combined
+  // values c, their keys prev_score + c (no log-sum-exp: part is NULL and prev_score already
+  // holds the row constant), and a row whose lists overflow is selected from its stored row.
+  const float *comb;
 };
 hipError_t launch_row_select(const RowSelect &a, hipStream_t st);
 // Chunks of one row of a materialised logp for the first selection level (both the workspace

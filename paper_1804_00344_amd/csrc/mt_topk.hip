@@ -94,6 +94,16 @@ __device__ __forceinline__ void sentence_merge(const RowSelect &a, int b, uint32
   }
 }
 
+// The K best keys prev + x[v] of one stored row x [V] (a fused ensemble's combined values),
+// read by a 256-thread workgroup; emit(rank, key, token) for ranks 0..K-1.
+template <int KMAX, typename Emit>
+__device__ __forceinline__ void row_rescan(const float *x, int V, int K, float prev, Emit emit) {
+  List<KMAX> lst;
+  lst.init();
+  for (int v = threadIdx.x; v < V; v += kTT) lst.push(prev + x[v], v);
+  block_extract<KMAX>(lst, K, emit);
+}
+
 // Levels 2 and 3: one workgroup per row (see RowSelect).  A row's K best are staged as (key
 // code, token) in LDS, four waves each select from a quarter and wave 0 merges the quarters.
 // Every workgroup then counts itself in for its sentence; the last of the sentence's K rows
@@ -110,15 +120,16 @@ __global__ __launch_bounds__(kTT) void row_select_kernel(RowSelect a) {
   const int m = blockIdx.x, t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int K = a.K, V = a.V, nl = a.nl, cap = a.cap;
   const int b = m / K;
-  const bool fused = a.part != nullptr;
+  const bool has_lse = a.part != nullptr;
+  const bool fused = has_lse || a.comb != nullptr;  // lists from the vocabulary pass, keys formed here
   const int *cr = a.cnt ? a.cnt + (size_t)m * nl : nullptr;
 
   // ---- one round trip for the usual shape (at most one partial and two lists per thread):
   // the row's log-sum-exp partial, its list fill counts and the first kSpec entries of this
   // thread's lists are all requested before any of them is needed (lists hold about one entry
   // each; entries past a list's count are loaded and ignored) ----
-  const bool pre = nl <= 2 * kTT && (!fused || a.ntiles <= kTT);  // uniform
-  const bool has_p = fused && t < a.ntiles;
+  const bool pre = nl <= 2 * kTT && (!has_lse || a.ntiles <= kTT);  // uniform
+  const bool has_p = has_lse && t < a.ntiles;
   float2 pq = make_float2(0.f, 0.f);
   int pc[2] = {0, 0};
   int2 pe[2][kSpec];
@@ -135,9 +146,9 @@ __global__ __launch_bounds__(kTT) void row_select_kernel(RowSelect a) {
       }
     }
   }
-  const float L = !fused ? 0.f
-                  : pre  ? block_row_lse_one(pq, has_p)
-                         : block_row_lse(a.part + (size_t)m * a.ntiles, a.ntiles);
+  const float L = !has_lse ? 0.f
+                  : pre    ? block_row_lse_one(pq, has_p)
+                           : block_row_lse(a.part + (size_t)m * a.ntiles, a.ntiles);
   const float sc = fused ? a.prev_score[m] : 0.f;
   int2 *out = a.row_cand + (size_t)m * K;
   auto emit_row = [&](int rank, float key, int tok) { put_row(out + rank, key, tok); };
@@ -180,7 +191,10 @@ __global__ __launch_bounds__(kTT) void row_select_kernel(RowSelect a) {
       // the candidates do not fit (or fall short of K): exact recomputation of the row
       if (fused) {
         if (t == 0 && a.nrecompute) atomicAdd(a.nrecompute, 1ull);
-        row_recompute<CT, KMAX>(a.vv, m, K, L, sc, emit_row);
+        if (a.comb)
+          row_rescan<KMAX>(a.comb + (size_t)m * V, V, K, sc, emit_row);
+        else
+          row_recompute<CT, KMAX>(a.vv, m, K, L, sc, emit_row);
       }
     } else {
       // ---- stage the candidates as (key code, token) in LDS ----

@@ -77,6 +77,10 @@ struct VocabArgs {
   float *logits;        // [M][logits_ld] or NULL
   int logits_ld;
   int logits_vec;       // 16-byte aligned rows (base aligned, logits_ld % 4 == 0): float4 stores
+  float logits_w;       // the logits are stored multiplied by this weight (1: as they are)
+  int logits_acc;       // 1: added to the values already stored (ensemble members after the first)
+  int cap_stored;       // 1: candidates are the stored (weighted, accumulated) values, not the logits
+                        // (a fused ensemble's last member: the combined values of all members)
   int fixed_ref;        // logits proven bounded: log-sum-exp without a running maximum
 };
 
@@ -150,7 +154,7 @@ __global__ __launch_bounds__((VShape<CT, HB>::NT)) void vocab_kernel(VocabArgs a
     const int h = h0 + hc0 + j * 32 + lrow;
     lm[j] = FIX ? 0.f : -INFINITY;
     ls[j] = 0.f;
-    th[j] = (collect && h < a.M) ? a.thr[h] : INFINITY;
+    th[j] = (collect && a.thr && h < a.M) ? a.thr[h] : INFINITY;
     loff[j] = (uint32_t)(((size_t)(h < a.M ? h : 0) * a.cap * nlr + chunk * kLists + src) * sizeof(int2));
     lend[j] = loff[j] + (uint32_t)(a.cap - 1) * lstep;
   }
@@ -310,15 +314,15 @@ __global__ __launch_bounds__((VShape<CT, HB>::NT)) void vocab_kernel(VocabArgs a
 #pragma unroll
       for (int j = 0; j < HBB; ++j) {
         const int h = h0 + hc0 + j * 32 + lrow;
+        // candidate capture: store the (logit, token) pair at the lane's next slot and advance;
+        // the offset sticks at the list's last slot, and a list that reaches it is reported as
+        // overflowed (its row is recomputed exactly)
+        auto capture = [&](float x, int i, int r) {
+          *(int2 *)(cbase + loff[j]) = make_int2(__float_as_int(x), v0 + 32 * i + 8 * (r >> 2) + 4 * lhalf + (r & 3));
+          const uint32_t nx = loff[j] + lstep;
+          loff[j] = nx < lend[j] ? nx : lend[j];
+        };
         if (collect) {
-          // candidate capture: store the (logit, token) pair at the lane's next slot and
-          // advance; the offset sticks at the list's last slot, and a list that reaches it is
-          // reported as overflowed (its row is recomputed exactly)
-          auto capture = [&](float x, int i, int r) {
-            *(int2 *)(cbase + loff[j]) = make_int2(__float_as_int(x), v0 + 32 * i + 8 * (r >> 2) + 4 * lhalf + (r & 3));
-            const uint32_t nx = loff[j] + lstep;
-            loff[j] = nx < lend[j] ? nx : lend[j];
-          };
           if constexpr (FIX) {
             float se = 0.f;
 #pragma unroll
@@ -327,7 +331,7 @@ __global__ __launch_bounds__((VShape<CT, HB>::NT)) void vocab_kernel(VocabArgs a
               for (int r = 0; r < 16; ++r) {
                 const float x = acc[i][j][r];
                 se += __builtin_amdgcn_exp2f(x * kLog2e);
-                if (x >= th[j]) capture(x, i, r);
+                if (!(LOG && a.cap_stored) && x >= th[j]) capture(x, i, r);
               }
             ls[j] += se;
           } else {
@@ -345,7 +349,7 @@ __global__ __launch_bounds__((VShape<CT, HB>::NT)) void vocab_kernel(VocabArgs a
                 for (int r = 0; r < 16; ++r) {
                   const float x = acc[i][j][r];
                   se += __builtin_amdgcn_exp2f(__builtin_fmaf(x, kLog2e, -mts));
-                  if (x >= th[j]) capture(x, i, r);
+                  if (!(LOG && a.cap_stored) && x >= th[j]) capture(x, i, r);
                 }
               const float mn = fmaxf(lm[j], mt);
               ls[j] = ls[j] * exp_fast(lm[j] - mn) + se * exp_fast(mt - mn);
@@ -363,12 +367,28 @@ __global__ __launch_bounds__((VShape<CT, HB>::NT)) void vocab_kernel(VocabArgs a
             for (int q = 0; q < 4; ++q) {
               const int vb = v0 + 32 * i + 8 * q + 4 * lhalf;
               if (a.logits_vec && vb + 3 < a.V) {
-                *(float4 *)(lrowp + vb) =
-                    make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+                float4 val = make_float4(a.logits_w * acc[i][j][4 * q], a.logits_w * acc[i][j][4 * q + 1],
+                                         a.logits_w * acc[i][j][4 * q + 2], a.logits_w * acc[i][j][4 * q + 3]);
+                if (a.logits_acc) {
+                  const float4 o = *(const float4 *)(lrowp + vb);
+                  val.x += o.x; val.y += o.y; val.z += o.z; val.w += o.w;
+                }
+                if (a.cap_stored) {
+                  if (val.x >= th[j]) capture(val.x, i, 4 * q + 0);
+                  if (val.y >= th[j]) capture(val.y, i, 4 * q + 1);
+                  if (val.z >= th[j]) capture(val.z, i, 4 * q + 2);
+                  if (val.w >= th[j]) capture(val.w, i, 4 * q + 3);
+                }
+                *(float4 *)(lrowp + vb) = val;
               } else {
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
-                  if (vb + e < a.V && vb + e < a.logits_ld) lrowp[vb + e] = acc[i][j][4 * q + e];
+                  if (vb + e < a.V && vb + e < a.logits_ld) {
+                    float val = a.logits_w * acc[i][j][4 * q + e];
+                    if (a.logits_acc) val += lrowp[vb + e];
+                    if (a.cap_stored && val >= th[j]) capture(val, i, 4 * q + e);
+                    lrowp[vb + e] = val;
+                  }
               }
             }
         }
@@ -417,9 +437,12 @@ __global__ __launch_bounds__((VShape<CT, HB>::NT)) void vocab_kernel(VocabArgs a
 // bisection over order-preserving codes): K different lanes reach it, so K sampled logits do.
 // Against the K-th best of the whole sample it is lower only when two of the sample's best
 // share a lane, at a small fraction of the cost.
+// A fused ensemble's last member thresholds the combined values instead: cw * sample[m][v],
+// plus comb[m][v] (the earlier members' weighted logits, row stride V) when there are any.
 template <int R>
 __global__ __launch_bounds__(256) void vocab_threshold_kernel(int M, int S, int K, const float *__restrict__ sample,
-                                                              int ld, float *__restrict__ thr, int *scnt, int B) {
+                                                              int ld, float *__restrict__ thr, int *scnt, int B,
+                                                              const float *__restrict__ comb, int V, float cw) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   if (blockIdx.x == 0)
     for (int i = threadIdx.x; i < B; i += 256) __hip_atomic_store(scnt + i, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -430,7 +453,7 @@ __global__ __launch_bounds__(256) void vocab_threshold_kernel(int M, int S, int 
 #pragma unroll
   for (int s = 0; s < R; ++s) {
     const int v = s * 64 + lane;
-    x[s] = v < S ? row[v] : -INFINITY;
+    x[s] = v < S ? (comb ? cw * row[v] + comb[(size_t)m * V + v] : cw * row[v]) : -INFINITY;
   }
   uint32_t um[1] = {0u};
 #pragma unroll
@@ -570,18 +593,19 @@ static VocabArgs base_args(int bf16_mma, const void *t, const void *wp, const fl
 }
 
 hipError_t launch_vocab_threshold(int M, int V, int K, const float *sample, float *thr, int *scnt, int B,
-                                  hipStream_t st) {
+                                  hipStream_t st, const float *comb, float w) {
   if (M == 0) return hipSuccess;
   const int S = vocab_sample_size(V);
   const int Sv = V < S ? V : S;  // entries >= V of the sample are padding
   hipLaunchKernelGGL((vocab_threshold_kernel<kSampleMax / 64>), dim3((M + 3) / 4), dim3(256), 0, st, M, Sv, K,
-                     sample, S, thr, scnt, B);
+                     sample, S, thr, scnt, B, comb, V, w);
   return hipGetLastError();
 }
 
 hipError_t launch_vocab(int bf16_mma, const void *t, const void *wp, const float *bias_pad, int M, int V,
                         int E, int n_chunks, const float *thr, float2 *part, int2 *cbuf, int *ccnt, int cap,
-                        float *logits, int fixed_ref, hipStream_t st) {
+                        float *logits, int fixed_ref, hipStream_t st, float logits_w, int logits_acc,
+                        int cap_stored) {
   if (M == 0) return hipSuccess;
   VocabArgs a = base_args(bf16_mma, t, wp, bias_pad, M, V, E);
   a.tiles_total = (V + kVRows - 1) / kVRows;
@@ -594,6 +618,9 @@ hipError_t launch_vocab(int bf16_mma, const void *t, const void *wp, const float
   a.logits = logits;
   a.logits_ld = V;
   a.logits_vec = logits && ((uintptr_t)logits & 15) == 0 && V % 4 == 0;
+  a.logits_w = logits_w;
+  a.logits_acc = logits_acc;
+  a.cap_stored = logits && cap_stored;
   a.fixed_ref = fixed_ref;
   return vgo_any(bf16_mma, a, st);
 }

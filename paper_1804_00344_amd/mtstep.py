@@ -98,6 +98,12 @@ def lib() -> C.CDLL:
         L.mt_profile_enable.argtypes = [_vp, C.c_uint32]
         L.mt_profile_reset.argtypes = [_vp]
         L.mt_profile_query.argtypes = [_vp, C.c_int, C.POINTER(C.c_double), C.POINTER(C.c_int64)]
+        L.mt_ensemble_step.argtypes = [_vp, C.c_int, C.c_int, C.c_float, C.c_int, C.c_int, C.c_int, _vp, _vp, C.c_int, _vp,
+                                       _vp, _vp, _vp, _vp, _vp, _vp, C.c_size_t, _vp]
+        L.mt_ensemble_step.restype = C.c_int
+        L.mt_ensemble_topk.argtypes = [C.c_int, C.POINTER(_vp), C.POINTER(C.c_float), C.POINTER(_vp),
+                                       C.POINTER(C.c_size_t), C.c_int, C.c_int, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]
+        L.mt_ensemble_topk.restype = C.c_int
         L.mt_recomputed_rows.argtypes = [_vp, C.POINTER(C.c_int64)]
         L.mt_recomputed_rows.restype = C.c_int
         L.mt_round_bf16.argtypes = [_vp, _vp, C.c_size_t]
@@ -272,6 +278,25 @@ def mt_device_errors(model: Model) -> int:
     f = C.c_int32(0)
     _check(lib().mt_device_errors(model.handle, C.byref(f)))
     return int(f.value)
+
+
+def mt_ensemble_step(model: Model, member, n_members, weight, B, K, S, prev_tok, src_row, n_state_rows, state_in, ctx,
+                     pctx, mask, state_out, comb_logits, ws, ws_bytes=None, stream=None):
+    ws_bytes = ws.numel() * ws.element_size() if ws_bytes is None else ws_bytes
+    _check(lib().mt_ensemble_step(model.handle, member, n_members, float(weight), B, K, S, _ptr(prev_tok), _ptr(src_row),
+                                  n_state_rows, _ptr(state_in), _ptr(ctx), _ptr(pctx), _ptr(mask), _ptr(state_out),
+                                  _ptr(comb_logits), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def mt_ensemble_topk(models, weights, wss, B, K, prev_score, comb_logits, score_out, tok_out, bp_out, row_out=None,
+                     row_const_out=None, stream=None):
+    n = len(models)
+    hs = (_vp * n)(*[m.handle for m in models])
+    ws_ = (C.c_float * n)(*[float(x) for x in weights])
+    wp = (_vp * n)(*[_ptr(w) for w in wss])
+    wb = (C.c_size_t * n)(*[w.numel() * w.element_size() for w in wss])
+    _check(lib().mt_ensemble_topk(n, hs, ws_, wp, wb, B, K, _ptr(prev_score), _ptr(comb_logits), _ptr(score_out),
+                                  _ptr(tok_out), _ptr(bp_out), _ptr(row_out), _ptr(row_const_out), _stream(stream)))
 
 
 def mt_recomputed_rows(model: Model) -> int:

@@ -220,15 +220,19 @@ def translate(dec: "Decoder", tok0, score0, max_steps: int, eos: int, alpha: flo
 
 
 class Ensemble:
-    """Members decoding one beam (ensembling, a meta-algorithm of batched beam search): every
-    member runs its step on the shared beam with its own states and materialised
-    log-probabilities, mt_ensemble_logp combines them, and the first member's selection
-    extends the beam that all members read next."""
+    """Members decoding one beam (ensembling, a meta-algorithm of batched beam search), each
+    with its own states.  Fused (the default): every member's step adds its weighted logits
+    into one buffer (mt_ensemble_step) and one selection subtracts the per-row constant
+    sum_i w_i LSE_i (mt_ensemble_topk), selecting from the beam candidates the last member
+    collected on the combined values.  Materialised (fused=False): every member writes its
+    log-probabilities, mt_ensemble_logp combines them and mt_beam_topk selects.  Either way the
+    first member's beam buffers hold the beam that all members read next."""
 
-    def __init__(self, members, weights):
+    def __init__(self, members, weights, fused=True):
         assert len(members) == len(weights) >= 1
         self.members, self.weights = list(members), [float(x) for x in weights]
         self.lead = self.members[0]
+        self.fused = fused
 
     def set_batch(self, ctx: np.ndarray, mask: np.ndarray, K: int):
         for d in self.members:
@@ -237,7 +241,9 @@ class Ensemble:
 
     def _alloc_logp(self):
         lead = self.lead
-        self.logp = [torch.empty((lead.M, lead.V), dtype=torch.float32, device=lead.device) for _ in self.members]
+        # the fused path needs only the combined buffer
+        self.logp = [None if self.fused else torch.empty((lead.M, lead.V), dtype=torch.float32, device=lead.device)
+                     for _ in self.members]
         self.comb = torch.empty((lead.M, lead.V), dtype=torch.float32, device=lead.device)
 
     def set_source(self, src_tok: np.ndarray, mask: np.ndarray, K: int, stream=None):
@@ -259,17 +265,26 @@ class Ensemble:
         for d in self.members:
             d.start(tok0, score0)
 
-    def advance(self, stream=None):
+    def advance(self, stream=None, row_const=None):
         lead = self.lead
-        for d, lp in zip(self.members, self.logp):
+        for i, (d, lp) in enumerate(zip(self.members, self.logp)):
             if d.first:
                 state_in, nrows = d.s0, d.B
             else:
                 state_in, nrows = d.state[d.cur], d.M
             out = d.state[1 - d.cur] if not d.first else d.state[d.cur]
-            d.step(lead.tok, lead.row, state_in, nrows, out, logp=lp, stream=stream)
-        mt.mt_ensemble_logp(lead.model, self.logp, self.weights, lead.M, self.comb, stream=stream)
-        lead.topk(lead.score, self.comb, stream=stream)
+            if self.fused:
+                mt.mt_ensemble_step(d.model, i, len(self.members), self.weights[i], d.B, d.K, d.S, lead.tok, lead.row,
+                                    nrows, state_in, d.ctx, d.pctx, d.mask, out, self.comb, d.ws, stream=stream)
+            else:
+                d.step(lead.tok, lead.row, state_in, nrows, out, logp=lp, stream=stream)
+        if self.fused:
+            mt.mt_ensemble_topk([d.model for d in self.members], self.weights, [d.ws for d in self.members], lead.B,
+                                lead.K, lead.score, self.comb, lead.score, lead.tok, lead.bp, lead.row,
+                                row_const_out=row_const, stream=stream)
+        else:
+            mt.mt_ensemble_logp(lead.model, self.logp, self.weights, lead.M, self.comb, stream=stream)
+            lead.topk(lead.score, self.comb, stream=stream)
         for d in self.members:
             if not d.first:
                 d.cur = 1 - d.cur

@@ -435,6 +435,20 @@ def test_candidate_buffer_overflow_falls_back_exactly():
 # states; their log-probabilities are combined on the GPU and one selection extends the beam
 # ------------------------------------------------------------------------------------------
 
+def exact_topk_check(B, K, keys, sc, tk, bp):
+    """sc/tk/bp [B*K] are, per sentence, the K best of keys [B*K, V] (flattened k*V + v),
+    larger key first, equal keys by smaller flat index; bit-exact."""
+    V = keys.shape[1]
+    for b in range(B):
+        f = keys[b * K:(b + 1) * K].reshape(-1)
+        kth = np.partition(f, f.size - K)[f.size - K]
+        idx = np.nonzero(f >= kth)[0]
+        order = idx[np.lexsort((idx, -f[idx].astype(np.float64)))][:K]
+        rows = slice(b * K, (b + 1) * K)
+        assert np.array_equal(sc[rows], f[order]), (b, sc[rows], f[order])
+        assert np.array_equal(tk[rows], order % V) and np.array_equal(bp[rows], order // V), b
+
+
 @pytest.mark.parametrize("name,weights", [("tiny_f32", (0.6, 0.4)), ("nematus_f32", (0.5, 0.5)),
                                           ("nematus_bf16_ln", (0.7, 0.3))])
 def test_ensemble_step_parity(name, weights):
@@ -478,6 +492,99 @@ def test_ensemble_step_parity(name, weights):
     mt.mt_ensemble_logp(decs[0].model, logps, weights, base.M, logps[0])
     torch.cuda.synchronize()
     assert torch.max(torch.abs(logps[0].double() - ref)).item() <= 1e-4
+
+
+def exact_topk_check(B, K, keys, sc, tk, bp):
+    """sc/tk/bp [B*K] are, per sentence, the K best of keys [B*K, V] (flattened k*V + v),
+    larger key first, equal keys by smaller flat index; bit-exact."""
+    V = keys.shape[1]
+    for b in range(B):
+        f = keys[b * K:(b + 1) * K].reshape(-1)
+        kth = np.partition(f, f.size - K)[f.size - K]
+        idx = np.nonzero(f >= kth)[0]
+        order = idx[np.lexsort((idx, -f[idx].astype(np.float64)))][:K]
+        rows = slice(b * K, (b + 1) * K)
+        assert np.array_equal(sc[rows], f[order]), (b, sc[rows], f[order])
+        assert np.array_equal(tk[rows], order % V) and np.array_equal(bp[rows], order // V), b
+
+
+@pytest.mark.parametrize("name,weights", [("tiny_f32", (0.6, 0.4)), ("nematus_f32", (0.5, 0.5)),
+                                          ("nematus_bf16_ln", (0.7, 0.3)), ("tiny_bf16_ln", (0.2, 0.5, 0.3))])
+def test_fused_ensemble_step_parity(name, weights):
+    """Fused ensemble: each member adds its weighted logits into one buffer and the selection
+    subtracts the per-row constant sum_i w_i LSE_i; the combined log-probabilities (buffer minus
+    the constant), the members' states and the beam against the oracle's ensemble."""
+    base = synth.PRESETS[name]
+    members = [base] + [dataclasses.replace(base, name=f"{name}_m{i}", index=base.index + 100 * i)
+                        for i in range(1, len(weights))]
+    log(f"\n[fused ensemble] {name} weights={weights}")
+    ctx, mask, lens = synth.make_source(base)
+    tok, src, state, score = synth.mid_decode_inputs(base, salt=5)
+    decs, ws = [], []
+    comb = torch.empty((base.M, base.V), device=DEV)
+    states = []
+    for i, p in enumerate(members):
+        w = synth.make_weights(p, peaked_bias=True)
+        dec = Decoder.from_preset(p, w)
+        dec.set_batch(ctx, mask, p.K)
+        dec.precompute()
+        out = torch.empty((p.M, p.H), device=DEV)
+        mt.mt_ensemble_step(dec.model, i, len(weights), weights[i], p.B, p.K, dec.S, T(tok), T(src), p.M, T(state),
+                            dec.ctx, dec.pctx, dec.mask, out, comb, dec.ws)
+        decs.append(dec)
+        ws.append(w)
+        states.append(out)
+    cst = torch.empty(base.M, device=DEV)
+    sc_t, tk_t, bp_t, rw_t = (torch.empty(base.M, device=DEV), torch.empty(base.M, dtype=torch.int32, device=DEV),
+                              torch.empty(base.M, dtype=torch.int32, device=DEV),
+                              torch.empty(base.M, dtype=torch.int32, device=DEV))
+    mt.mt_ensemble_topk([d.model for d in decs], weights, [d.ws for d in decs], base.B, base.K, T(score), comb, sc_t,
+                        tk_t, bp_t, rw_t, row_const_out=cst)
+    torch.cuda.synchronize()
+    for d in decs:
+        assert mt.mt_device_errors(d.model) == 0
+    g = (comb - cst[:, None]).cpu().numpy()
+    sc, tk, bp, rw = [x.cpu().numpy() for x in (sc_t, tk_t, bp_t, rw_t)]
+    # the selection from the last member's candidates is exactly the best K of the keys
+    # (prev - C) + stored combined value over each sentence's whole K x V block (fp32, the
+    # same two roundings), ties to the smaller flat index
+    keys = (score.astype(np.float32) - cst.cpu().numpy())[:, None] + comb.cpu().numpy()
+    exact_topk_check(base.B, base.K, keys, sc, tk, bp)
+    sents = sample_sentences(lens, N_SAMPLE[name] if name in N_SAMPLE else 99)
+    orcs = [oracle_sentences(oracle_model(p, w), base.K, sents, ctx, mask, tok, src, state, want_alpha=False,
+                             taps=False) for p, w in zip(members, ws)]
+    tol = TOL[base.gemm]
+    worst = worst_s = 0.0
+    dec_n = tot = 0
+    for b in sents:
+        rows = slice(b * base.K, (b + 1) * base.K)
+        ens = mtref.ensemble_logp([o[b]["logp"] for o in orcs], weights)
+        worst = max(worst, maxerr(g[rows], ens))
+        for o, st in zip(orcs, states):
+            worst_s = max(worst_s, maxerr(st[rows].cpu().numpy(), o[b]["state"]))
+        d, n = topk_gap_check(base.K, score[rows], ens, sc[rows], tk[rows], bp[rows], tol["logp"])
+        dec_n += d
+        tot += n
+        assert np.array_equal(rw[rows], b * base.K + bp[rows])
+    log(f"[fused ensemble] {name}: combined logp max error {worst:.3g}, member state error {worst_s:.3g}, "
+        f"decided slots {dec_n}/{tot}")
+    assert worst <= tol["logp"] and worst_s <= tol["state"]
+    # the same beam through the runner's fused and materialised ensembles agrees within the
+    # rounding of the two forms
+    from paper_1804_00344_amd.runner import Ensemble
+    sel = {}
+    for fused in (True, False):
+        ens = Ensemble(decs, weights, fused=fused)
+        ens.set_batch(ctx, mask, base.K)
+        ens.precompute()
+        tok0, _, score0 = synth.start_beam(base)
+        ens.start(tok0, score0)
+        ens.advance()
+        torch.cuda.synchronize()
+        sel[fused] = [x.cpu().numpy().copy() for x in (decs[0].score, decs[0].tok, decs[0].bp)]
+    assert np.all(np.abs(sel[True][0] - sel[False][0]) <= 2 * tol["logp"])
+    agree = np.mean((sel[True][1] == sel[False][1]) & (sel[True][2] == sel[False][2]))
+    log(f"[fused ensemble] {name}: step-0 beam agreement fused vs materialised {agree:.4f}")
 
 
 # ------------------------------------------------------------------------------------------

@@ -229,9 +229,11 @@ def test_ensemble_from_source_tokens():
     ens.precompute()
     tok0, _, score0 = synth.start_beam(p)
     ens.start(tok0, score0)
-    ens.advance()
+    row_const = torch.empty(p.M, dtype=torch.float32, device="cuda")
+    ens.advance(row_const=row_const)
     torch.cuda.synchronize()
-    g = ens.comb.cpu().numpy()
+    # the fused step leaves sum_i w_i logit_i; the combined logp is that minus the row constant
+    g = ens.comb.cpu().numpy().astype(np.float64) - row_const.cpu().numpy()[:, None]
     sc, tk, bp = ens.lead.score.cpu().numpy(), ens.lead.tok.cpu().numpy(), ens.lead.bp.cpu().numpy()
     lps = []
     for (q, w), d in zip(members, decs):
