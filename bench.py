@@ -338,7 +338,9 @@ def main():
 
     steps_per_s = timed_steps / elapsed
     avg_vocab_s = vocab_ms / 1e3 / max(vocab_n, 1)
-    flops = 2.0 * p.M * p.E * p.V
+    # a joint ensemble pass computes every member's logits in one launch
+    vocab_members = NE if NE > 1 and getattr(drive, "joint", False) else 1
+    flops = 2.0 * p.M * p.E * p.V * vocab_members
     achieved = flops / avg_vocab_s / 1e12
     peak = PEAK_TFLOPS[p.gemm]
     traffic = None
@@ -346,12 +348,14 @@ def main():
         # HBM bytes per launch from the FETCH_SIZE / WRITE_SIZE passes, valid only while the
         # vocabulary kernel's source is the one the counters were taken on
         tf = json.load(open(TRAFFIC_FILE))
-        ent = tf.get(p.name, {}).get("vocab_gemm")
+        ent = tf.get(p.name, {}).get("vocab_gemm") if vocab_members == 1 else None
         src_h = source_hash(os.path.join(ROOT, "paper_1804_00344_amd", "csrc", "mt_vocab.hip"))
         if ent and ent.get("source_hash") == src_h:
             traffic = ent["bytes_per_launch"]
     roofline = {
-        "kernel": "vocab_gemm (t Wo + bo, fused log-sum-exp partials + per-tile top-K)",
+        "kernel": ("vocab_joint (every member's t Wo + bo in one pass, per-member log-sum-exp partials + "
+                   "candidates of the combined value)" if vocab_members > 1 else
+                   "vocab_gemm (t Wo + bo, fused log-sum-exp partials + per-tile top-K)"),
         "bound": "mfma",
         "achieved": round(achieved, 2),
         "peak": peak,

@@ -286,6 +286,13 @@ mt_status mt_ensemble_logp(mt_model *model, int n, const float *const *logp, con
  *     (same V, k_max >= K); row_const_out [B*K] or NULL receives C.  The selection's scratch
  *     lives in ws[n-1].  MT_ERR_STATE unless the members' last calls were exactly these
  *     ensemble steps.  1 <= n <= 8.  Asynchronous. */
+/* Joint vocabulary pass (comb_logits = NULL in both calls): the members' steps stop after the
+ * readout and the threshold sample, and mt_ensemble_topk runs one vocabulary kernel for all
+ * members, which keeps every member's readout activations resident, forms the combined value
+ * sum_i w_i logit_i(v) of each entry in registers and collects the beam candidates on it (a
+ * row whose candidates overflow is recomputed from the members' weights); no [B*K, V] buffer
+ * is written.  mt_ensemble_step fails with MT_ERR_SHAPE where the pass does not support the
+ * member (see mt_ensemble_joint_ok). */
 mt_status mt_ensemble_step(mt_model *model, int member, int n_members, float weight, int B, int K, int S,
                            const int32_t *prev_tok, const int32_t *src_row, int n_state_rows, const float *state_in,
                            const void *ctx, const void *pctx, const float *mask, float *state_out,
@@ -294,6 +301,10 @@ mt_status mt_ensemble_topk(int n, mt_model *const *models, const float *weights,
                            const size_t *ws_bytes, int B, int K, const float *prev_score, const float *comb_logits,
                            float *score_out, int32_t *tok_out, int32_t *bp_out, int32_t *row_out, float *row_const_out,
                            void *stream);
+/* 1 if the joint vocabulary pass supports these n members (2 <= n <= 4, single-source, equal V,
+ * E and gemm dtype, the members' readout activations of one row block fitting one workgroup's
+ * LDS together), else 0.  models: HOST array. */
+int mt_ensemble_joint_ok(int n, mt_model *const *models);
 
 /* Translation bookkeeping after mt_beam_topk of step `step` (batched beam search decoding
  * to an n-best list as large as the beam, Sections 2.3 and 3.1.3).  Per sentence b:

@@ -101,6 +101,7 @@ struct mt_model {
   const void *last_ws = nullptr;
   int last_ens_n = 0;      // the last step ran as the last of this many fused-ensemble members (0: not)
   float last_ens_w = 0.f;  // and with this weight
+  int last_ens_joint = 0;  // the last step was a member of this many for the joint vocabulary pass
   // profiling
   uint32_t prof_mask = 0;
   ProfSlot prof[MT_KERNEL_COUNT];
@@ -873,7 +874,8 @@ mt_status mt_precompute_ctx_noalloc(mt_model *model, int B, int S, const void *c
 // ens_w != 0: a fused-ensemble member: logp_out receives ens_w * logits, added to what it holds
 // when ens_acc, and is not turned into log-probabilities.  Only the last member (ens_last: the
 // ensemble's size) collects beam candidates, on the combined values it stores; the others
-// skip the threshold pass and write only their log-sum-exp partials.
+// skip the threshold pass and write only their log-sum-exp partials.  With logp_out NULL the
+// member stops after the threshold sample: the joint pass of mt_ensemble_topk does the rest.
 static mt_status decoder_step_impl(mt_model *model, int B, int K, int S, const int32_t *prev_tok,
                                    const int32_t *src_row, int n_state_rows, const float *state_in,
                                    const void *ctx, const void *pctx, const float *mask, int S2, const void *ctx2,
@@ -997,22 +999,26 @@ static mt_status decoder_step_impl(mt_model *model, int B, int K, int S, const i
   // and threshold-filtered beam candidates
   float2 *part = (float2 *)(W + L.part);
   const bool ens = ens_w != 0.f;
+  const bool joint = ens && !logp_out;
   const bool want_cand = !ens || ens_last > 0;
-  if (want_cand) {
+  if (want_cand || joint) {
     const int S = vocab_sample_size(V);
     GemmProblem ps{};
     ps.A = t; ps.a_rows = M; ps.lda = E; ps.a_bf16 = bf;
     ps.Bp = model->wsamp.p; ps.ldb = model->wsamp.ldb; ps.wblk = model->wsamp.blk; ps.bias = model->bo_pad;
     ps.out = W + L.sample; ps.ldc = S; ps.M = M; ps.N = S; ps.K = E;
     LAUNCH(MT_KERNEL_VOCAB_THRESHOLD, launch_gemm(bf, &ps, 1, EPI_STORE, st));
-    LAUNCH(MT_KERNEL_VOCAB_THRESHOLD,
-           launch_vocab_threshold(M, V, K, (const float *)(W + L.sample), (float *)(W + L.thr), (int *)(W + L.scnt),
-                                  B, st, ens && ens_acc ? logp_out : nullptr, ens ? ens_w : 1.f));
+    if (!joint)
+      LAUNCH(MT_KERNEL_VOCAB_THRESHOLD,
+             launch_vocab_threshold(M, V, K, (const float *)(W + L.sample), (float *)(W + L.thr),
+                                    (int *)(W + L.scnt), B, st, ens && ens_acc ? logp_out : nullptr,
+                                    ens ? ens_w : 1.f));
   }
-  LAUNCH(MT_KERNEL_VOCAB_GEMM, launch_vocab(bf, t, model->wo_frag, model->bo_pad, M, V, E, L.ntiles,
-                                            want_cand ? (const float *)(W + L.thr) : nullptr, part,
-                                            (int2 *)(W + L.cbuf), (int *)(W + L.ccnt), kVocabCap, logp_out,
-                                            model->logit_bounded, st, ens ? ens_w : 1.f, ens_acc, ens ? 1 : 0));
+  if (!joint)
+    LAUNCH(MT_KERNEL_VOCAB_GEMM, launch_vocab(bf, t, model->wo_frag, model->bo_pad, M, V, E, L.ntiles,
+                                              want_cand ? (const float *)(W + L.thr) : nullptr, part,
+                                              (int2 *)(W + L.cbuf), (int *)(W + L.ccnt), kVocabCap, logp_out,
+                                              model->logit_bounded, st, ens ? ens_w : 1.f, ens_acc, ens ? 1 : 0));
   // the row log-sum-exp is merged by the beam selection itself; this pass only turns the
   // written logits into log-probabilities
   if (logp_out && !ens)
@@ -1022,6 +1028,7 @@ static mt_status decoder_step_impl(mt_model *model, int B, int K, int S, const i
   model->last_ws = ws;
   model->last_ens_n = ens ? ens_last : 0;
   model->last_ens_w = ens_w;
+  model->last_ens_joint = 0;  // set by mt_ensemble_step
   return MT_OK;
 }
 
@@ -1054,6 +1061,88 @@ mt_status mt_decoder_step_dual(mt_model *model, int B, int K, int S, const int32
                            pctx2, mask2, state_out, logp_out, attn_out, taps, ws, ws_bytes, stream);
 }
 
+// The joint vocabulary pass of a fused ensemble and its selection: the combined threshold, one
+// vocabulary kernel for all members (their readout activations and threshold samples are in
+// their workspaces), the row constant, then the selection from the combined candidates.
+// Candidates, threshold and the selection's scratch live in ws[0].  Arguments checked.
+static mt_status ensemble_topk_joint(int n, mt_model *const *models, const float *weights, void *const *ws, int B,
+                                     int K, const float *prev_score, float *score_out, int32_t *tok_out,
+                                     int32_t *bp_out, int32_t *row_out, float *row_const_out, hipStream_t st) {
+  mt_model *model = models[0];  // profiling slot
+  const mt_config &c = model->cfg;
+  const int M = B * K, V = c.V, E = c.E, bf = model->bf16;
+  if (n < 2 || n > kJointMax || vocab_joint_rows(bf, E, n) == 0)
+    return fail(MT_ERR_SHAPE, "the joint vocabulary pass does not support %d members at E=%d", n, E);
+  const int nj = vocab_joint_chunks(bf, M, V, E, n, model->num_cu);
+  const WsLayout L0 = ws_layout(model, B, K);
+  char *W0 = (char *)ws[0];
+  VocabJointSample smp{};
+  smp.n = n;
+  smp.ld = vocab_sample_size(V);
+  VocabJoint vj{};
+  vj.n = n; vj.bf16_mma = bf; vj.M = M; vj.V = V; vj.E = E; vj.n_chunks = nj; vj.cap = kVocabCap;
+  vj.fixed_ref = 1;
+  EnsembleConst ec{};
+  ec.n = n;
+  RowSelect rs{};
+  rs.nens = n;
+  for (int i = 0; i < n; ++i) {
+    mt_model *mi = models[i];
+    const WsLayout Li = ws_layout(mi, B, K);
+    if (nj > Li.ntiles) return fail(MT_ERR_STATE, "member %d: workspace holds %d chunks < %d", i, Li.ntiles, nj);
+    char *Wi = (char *)ws[i];
+    smp.sample[i] = (const float *)(Wi + Li.sample);
+    smp.w[i] = weights[i];
+    vj.t[i] = Wi + Li.t;
+    vj.wp[i] = mi->wo_frag;
+    vj.bias[i] = mi->bo_pad;
+    vj.w[i] = weights[i];
+    vj.part[i] = (float2 *)(Wi + Li.part);
+    vj.fixed_ref &= mi->logit_bounded ? 1 : 0;
+    ec.part[i] = vj.part[i];
+    ec.ntiles[i] = nj;
+    ec.w[i] = weights[i];
+    rs.evv[i].t = vj.t[i]; rs.evv[i].wp = mi->wo_frag; rs.evv[i].bias = mi->bo_pad;
+    rs.evv[i].V = V; rs.evv[i].E = E; rs.evv[i].KS = E / (bf ? 16 : 8);
+    rs.ew[i] = weights[i];
+  }
+  float *thr = (float *)(W0 + L0.thr);
+  int *scnt = (int *)(W0 + L0.scnt);
+  LAUNCH(MT_KERNEL_VOCAB_THRESHOLD, launch_vocab_joint_threshold(M, V, K, smp, thr, scnt, B, st));
+  vj.thr = thr;
+  vj.cbuf = (int2 *)(W0 + L0.cbuf);
+  vj.ccnt = (int *)(W0 + L0.ccnt);
+  LAUNCH(MT_KERNEL_VOCAB_GEMM, launch_vocab_joint(vj, st));
+  float *prev_adj = (float *)(W0 + L0.lse);  // prev_score - C, in the row log-sum-exp slot
+  ec.prev = prev_score;
+  ec.prev_adj = prev_adj;
+  ec.row_const = row_const_out;
+  LAUNCH(MT_KERNEL_ENSEMBLE, launch_ensemble_const(ec, M, st));
+  rs.B = B; rs.K = K; rs.V = V;
+  rs.nl = nj * vocab_lists(); rs.cap = kVocabCap;
+  rs.cnt = vj.ccnt;
+  rs.cbuf = vj.cbuf;
+  rs.prev_score = prev_adj;
+  rs.bf16_mma = bf;
+  rs.row_cand = (int2 *)(W0 + L0.rowc);
+  rs.scnt = scnt;
+  rs.score_out = score_out; rs.tok_out = tok_out; rs.bp_out = bp_out; rs.row_out = row_out;
+  rs.nrecompute = model->nrecompute;
+  LAUNCH(MT_KERNEL_TOPK, launch_row_select(rs, st));
+  return MT_OK;
+}
+
+int mt_ensemble_joint_ok(int n, mt_model *const *models) {
+  if (n < 2 || n > kJointMax || !models) return 0;
+  for (int i = 0; i < n; ++i) {
+    if (!valid_model(models[i]) || models[i]->cfg.dual_source) return 0;
+    if (models[i]->cfg.V != models[0]->cfg.V || models[i]->cfg.E != models[0]->cfg.E ||
+        models[i]->bf16 != models[0]->bf16)
+      return 0;
+  }
+  return vocab_joint_rows(models[0]->bf16, models[0]->cfg.E, n) > 0 ? 1 : 0;
+}
+
 mt_status mt_ensemble_step(mt_model *model, int member, int n_members, float weight, int B, int K, int S,
                            const int32_t *prev_tok,
                            const int32_t *src_row, int n_state_rows, const float *state_in, const void *ctx,
@@ -1066,10 +1155,17 @@ mt_status mt_ensemble_step(mt_model *model, int member, int n_members, float wei
     return fail(MT_ERR_ARG, "n_members=%d: need 1..%d", n_members, kMaxEnsemble);
   if (member < 0 || member >= n_members) return fail(MT_ERR_ARG, "member=%d: need 0..%d", member, n_members - 1);
   if (!(weight != 0.f && std::isfinite(weight))) return fail(MT_ERR_ARG, "weight must be finite and nonzero");
-  CHECK(check_dev_ptr(comb_logits, "comb_logits", 4));
-  return decoder_step_impl(model, B, K, S, prev_tok, src_row, n_state_rows, state_in, ctx, pctx, mask, 0, nullptr,
-                           nullptr, nullptr, state_out, comb_logits, nullptr, nullptr, ws, ws_bytes, stream, weight,
-                           member > 0 ? 1 : 0, member == n_members - 1 ? n_members : 0);
+  if (comb_logits) {
+    CHECK(check_dev_ptr(comb_logits, "comb_logits", 4));
+  } else if (vocab_joint_rows(model->bf16, model->cfg.E, n_members) == 0) {
+    return fail(MT_ERR_SHAPE, "the joint vocabulary pass does not support %d members at E=%d (%s): pass comb_logits",
+                n_members, model->cfg.E, model->bf16 ? "bf16" : "fp32");
+  }
+  CHECK(decoder_step_impl(model, B, K, S, prev_tok, src_row, n_state_rows, state_in, ctx, pctx, mask, 0, nullptr,
+                          nullptr, nullptr, state_out, comb_logits, nullptr, nullptr, ws, ws_bytes, stream, weight,
+                          member > 0 ? 1 : 0, member == n_members - 1 ? n_members : 0));
+  model->last_ens_joint = comb_logits ? 0 : n_members;
+  return MT_OK;
 }
 
 mt_status mt_ensemble_topk(int n, mt_model *const *models, const float *weights, void *const *ws,
@@ -1085,7 +1181,8 @@ mt_status mt_ensemble_topk(int n, mt_model *const *models, const float *weights,
   if (B < 1 || K < 1 || K > c.k_max || K > c.V) return fail(MT_ERR_SHAPE, "B=%d K=%d: need B >= 1, 1 <= K <= k_max", B, K);
   if ((long long)B * K > (1 << 20)) return fail(MT_ERR_SHAPE, "B*K exceeds 2^20");
   CHECK(check_dev_ptr(prev_score, "prev_score", 4));
-  CHECK(check_dev_ptr(comb_logits, "comb_logits"));
+  const bool joint = comb_logits == nullptr;
+  if (!joint) CHECK(check_dev_ptr(comb_logits, "comb_logits", 4));
   CHECK(check_dev_ptr(score_out, "score_out", 4));
   CHECK(check_dev_ptr(tok_out, "tok_out", 4));
   CHECK(check_dev_ptr(bp_out, "bp_out", 4));
@@ -1103,12 +1200,21 @@ mt_status mt_ensemble_topk(int n, mt_model *const *models, const float *weights,
     if (ws_bytes[i] < Li.total) return fail(MT_ERR_WORKSPACE, "ws[%d]: %zu bytes < %zu needed", i, ws_bytes[i], Li.total);
     if (mi->last_B != B || mi->last_K != K || mi->last_ws != ws[i] || mi->last_ens_w != weights[i])
       return fail(MT_ERR_STATE, "member %d: no preceding mt_ensemble_step with this B, K, weight and workspace", i);
-    if ((mi->last_ens_n != 0) != (i == n - 1) || (i == n - 1 && mi->last_ens_n != n))
+    if (joint) {
+      if (mi->last_ens_joint != n)
+        return fail(MT_ERR_STATE, "member %d: its mt_ensemble_step was not a joint-pass step of %d members", i, n);
+      if (mi->cfg.E != c.E || mi->bf16 != lead->bf16)
+        return fail(MT_ERR_SHAPE, "member %d: E or gemm dtype differs (the joint pass needs them equal)", i);
+    } else if (mi->last_ens_joint != 0 || (mi->last_ens_n != 0) != (i == n - 1) ||
+               (i == n - 1 && mi->last_ens_n != n)) {
       return fail(MT_ERR_STATE, "member %d: its mt_ensemble_step was not called as member %d of %d", i, i, n);
+    }
     ec.part[i] = (const float2 *)((const char *)ws[i] + Li.part);
     ec.ntiles[i] = Li.ntiles;
     ec.w[i] = weights[i];
   }
+  if (joint) return ensemble_topk_joint(n, models, weights, ws, B, K, prev_score, score_out, tok_out, bp_out, row_out,
+                                         row_const_out, (hipStream_t)stream);
   // the candidates are the last member's (collected on the combined values), and so is the
   // selection's scratch
   mt_model *model = models[n - 1];  // profiling slot

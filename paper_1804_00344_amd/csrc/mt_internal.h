@@ -17,6 +17,7 @@ constexpr int kWave = 64;
 constexpr int kXcds = 8;
 constexpr int kKMax = 16;  // largest supported beam
 constexpr int kMaxEnsemble = 8;  // members of an ensemble
+constexpr int kJointMax = 4;     // members of an ensemble whose vocabulary pass runs as one kernel
 
 // ---------------------------------------------------------------------------------------
 // device helpers
@@ -380,6 +381,39 @@ __device__ __forceinline__ void row_recompute(const VocabView &vv, int m, int K,
   block_extract<KMAX>(lst, K, emit);
 }
 
+// Exact K best keys prev + sum_m w[m] * logit_m(v) of row m over the whole vocabulary (a joint
+// ensemble's row), recomputed from the n members' weights by a 256-thread workgroup.
+template <typename CT, int KMAX, typename Emit>
+__device__ __forceinline__ void row_recompute_ens(const VocabView *vvs, const float *w, int n, int m, int K,
+                                                  float prev, Emit emit) {
+  constexpr int epv = 16 / (int)sizeof(CT);
+  constexpr int KV = 2 * epv;
+  const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
+  const int V = vvs[0].V;
+  const int nvb = (V + 31) / 32;
+  List<KMAX> lst;
+  lst.init();
+  for (int vb = wv; vb < nvb; vb += 4) {
+    const int v = vb * 32 + (lane & 31);
+    float c = 0.f;
+    for (int mm = 0; mm < n; ++mm) {
+      const VocabView &vv = vvs[mm];
+      const CT *trow = (const CT *)vv.t + (size_t)m * vv.E;
+      float acc = 0.f;
+      for (int ks = 0; ks < vv.KS; ++ks) {
+        const CT *wq = (const CT *)((const char *)vv.wp + (((size_t)vb * vv.KS + ks) * 64 + lane) * 16);
+        const int k0 = ks * KV + (lane >> 5) * epv;
+#pragma unroll
+        for (int j = 0; j < epv; ++j) acc += to_f32(wq[j]) * to_f32(trow[k0 + j]);
+      }
+      acc += __shfl_xor(acc, 32, 64);
+      if (v < V) c += w[mm] * (acc + vv.bias[v]);
+    }
+    if (lane < 32 && v < V) lst.push(prev + c, v);
+  }
+  block_extract<KMAX>(lst, K, emit);
+}
+
 // ---------------------------------------------------------------------------------------
 // launchers (host side).  All return hipSuccess or the launch error.
 // ---------------------------------------------------------------------------------------
@@ -458,6 +492,32 @@ struct EnsembleConst {
   float *row_const;
 };
 hipError_t launch_ensemble_const(const EnsembleConst &a, int M, hipStream_t st);
+
+// ---- fused ensemble: one vocabulary pass for 2..kJointMax members (same V, E and type) ----
+// hypothesis rows per workgroup of the joint pass (0: not supported for this E, type and n)
+int vocab_joint_rows(int bf16_mma, int E, int n);
+// vocabulary chunks of the joint pass (<= vocab_chunks of the same model: its workspace holds them)
+int vocab_joint_chunks(int bf16_mma, int M, int V, int E, int n, int num_cu);
+struct VocabJoint {
+  int n, bf16_mma, M, V, E, n_chunks, cap, fixed_ref;
+  const void *t[kJointMax];      // [M][E] readout activations per member
+  const void *wp[kJointMax];     // packed Wo^T per member (vocab_pack_host layout)
+  const float *bias[kJointMax];  // padded output bias per member
+  float w[kJointMax];
+  float2 *part[kJointMax];       // [M][n_chunks] per member
+  const float *thr;              // [M] threshold on the combined value
+  int2 *cbuf;                    // [M][cap][n_chunks * lists]: combined values >= thr
+  int *ccnt;                     // [M][n_chunks][lists]
+};
+hipError_t launch_vocab_joint(const VocabJoint &j, hipStream_t st);
+// combined sample values sum_m w[m] * sample[m][row * ld + v] for the joint threshold
+struct VocabJointSample {
+  int n, ld;
+  const float *sample[kJointMax];
+  float w[kJointMax];
+};
+hipError_t launch_vocab_joint_threshold(int M, int V, int K, const VocabJointSample &smp, float *thr, int *scnt,
+                                        int B, hipStream_t st);
 constexpr int kVocabCap = 32;  // candidate buffer entries per (row, chunk, list)
 constexpr int kVocabPad = 64;  // vocabulary rows are padded to a multiple of this
 
@@ -562,6 +622,12 @@ struct RowSelect {
   // values c, their keys prev_score + c (no log-sum-exp: part is NULL and prev_score already
   // holds the row constant), and a row whose lists overflow is selected from its stored row.
   const float *comb;
+  // A joint ensemble pass (nens > 0, comb NULL): the same keys, and a row whose lists overflow
+  // is recomputed from the members' weights, sum_m ew[m] * (logit_m), with evv[m] each
+  // member's view (all of type CT)
+  int nens;
+  VocabView evv[kJointMax];
+  float ew[kJointMax];
 };
 hipError_t launch_row_select(const RowSelect &a, hipStream_t st);
 // Chunks of one row of a materialised logp for the first selection level (both the workspace

@@ -121,7 +121,7 @@ __global__ __launch_bounds__(kTT) void row_select_kernel(RowSelect a) {
   const int K = a.K, V = a.V, nl = a.nl, cap = a.cap;
   const int b = m / K;
   const bool has_lse = a.part != nullptr;
-  const bool fused = has_lse || a.comb != nullptr;  // lists from the vocabulary pass, keys formed here
+  const bool fused = has_lse || a.comb != nullptr || a.nens > 0;  // lists from the vocabulary pass
   const int *cr = a.cnt ? a.cnt + (size_t)m * nl : nullptr;
 
   // ---- one round trip for the usual shape (at most one partial and two lists per thread):
@@ -193,6 +193,8 @@ __global__ __launch_bounds__(kTT) void row_select_kernel(RowSelect a) {
         if (t == 0 && a.nrecompute) atomicAdd(a.nrecompute, 1ull);
         if (a.comb)
           row_rescan<KMAX>(a.comb + (size_t)m * V, V, K, sc, emit_row);
+        else if (a.nens > 0)
+          row_recompute_ens<CT, KMAX>(a.evv, a.ew, a.nens, m, K, sc, emit_row);
         else
           row_recompute<CT, KMAX>(a.vv, m, K, L, sc, emit_row);
       }

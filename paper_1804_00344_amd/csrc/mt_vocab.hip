@@ -27,40 +27,11 @@
 // Wo^T[vb*32 + l%32][ks*KV + (l/32)*KV/2 + j], j < 16/sizeof(CT).  fp32 uses the 32x32x2
 // MFMA with each 16-byte vector feeding 4 successive MFMAs (lane half g supplies k = 4g + s
 // to MFMA s); bf16 uses 32x32x16 with one vector per MFMA.
-#include "mt_internal.h"
+#include "mt_vocab_common.h"
 
 #include <type_traits>
 
 namespace mt {
-
-typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
-typedef uint32_t v4u __attribute__((ext_vector_type(4)));
-
-constexpr int kVRows = 64;       // vocabulary rows per wave tile (2 MFMA blocks)
-constexpr int kLists = 8;        // candidate buffers per (hypothesis, chunk): 2 lane halves x 4 runs
-constexpr int kSampleMax = 2048;  // vocabulary entries of the threshold pass
-constexpr float kLog2e = 1.4426950408889634f;
-
-// Hypothesis columns per wave: at most 64 (two 32-column MFMA blocks); a workgroup of HB
-// columns runs HB/64 waves per vocabulary run on the same tiles.
-template <typename CT, int HB>
-struct VShape {
-  static constexpr int WH = HB >= 64 ? 64 : HB;  // columns per wave
-  static constexpr int HBW = WH / 32;            // 32-column MFMA blocks per wave
-  static constexpr int NW = 4 * (HB / WH);       // waves per workgroup
-  static constexpr int NT = 64 * NW;             // threads per workgroup
-};
-
-template <typename CT>
-struct VCfg;
-template <>
-struct VCfg<bf16> {
-  static constexpr int KV = 16;  // k per 16-byte vector step
-};
-template <>
-struct VCfg<float> {
-  static constexpr int KV = 8;
-};
 
 struct VocabArgs {
   const void *t;        // [M][E] activations in CT
@@ -188,16 +159,18 @@ __global__ __launch_bounds__((VShape<CT, HB>::NT)) void vocab_kernel(VocabArgs a
     };
     v4u ring[D][2];
     // buffer view of the packed weights (KSC > 0): fixed per-lane offset, scalar fragment
-    // offsets; reads past the end return zero
+    // offsets.  A tile's second fragment is the next block's; a single-block tile reads its
+    // own block again, so no read leaves the run.
     const __amdgpu_buffer_rsrc_t wrs =
         __builtin_amdgcn_make_buffer_rsrc((void *)a.wp, 0, a.tiles_total * kVRows * a.E * es, 0x00020000);
     const int wvo = lane * 16;
     if constexpr (KSC > 0) {
+      const int sec0 = 0 < npair ? KSC * 1024 : 0;
 #pragma unroll
       for (int d = 0; d < D; ++d) {
         const int so = (b_begin * KSC + d) * 1024;
         ring[d][0] = __builtin_amdgcn_raw_buffer_load_b128(wrs, wvo, so, 0);
-        ring[d][1] = __builtin_amdgcn_raw_buffer_load_b128(wrs, wvo, so + KSC * 1024, 0);
+        ring[d][1] = __builtin_amdgcn_raw_buffer_load_b128(wrs, wvo, so + sec0, 0);
       }
     } else {
 #pragma unroll
@@ -279,16 +252,17 @@ __global__ __launch_bounds__((VShape<CT, HB>::NT)) void vocab_kernel(VocabArgs a
       };
       if constexpr (KSC > 0) {
         // byte offsets of this tile's and the next tile's first fragment (the last tile
-        // prefetches itself again, in bounds; a single block's second fragment reads the
-        // following block, or zero past the end)
+        // prefetches itself again) and of their second blocks
         const int tb = (b_begin + 2 * ti) * KSC * 1024;
-        const int tn = ti + 1 < ntile ? tb + 2 * KSC * 1024 : tb;
+        const int tnx = ti + 1 < ntile ? ti + 1 : ti;
+        const int tn = (b_begin + 2 * tnx) * KSC * 1024;
+        const int sec_cur = ti < npair ? KSC * 1024 : 0, sec_nxt = tnx < npair ? KSC * 1024 : 0;
 #pragma unroll
         for (int ks = 0; ks < KSC; ++ks)
           kstep(ks, ring[ks % D], [&](v4u(&r)[2]) {
             const int so = ks + D < KSC ? tb + (ks + D) * 1024 : tn + (ks + D - KSC) * 1024;
             r[0] = __builtin_amdgcn_raw_buffer_load_b128(wrs, wvo, so, 0);
-            r[1] = __builtin_amdgcn_raw_buffer_load_b128(wrs, wvo, so + KSC * 1024, 0);
+            r[1] = __builtin_amdgcn_raw_buffer_load_b128(wrs, wvo, so + (ks + D < KSC ? sec_cur : sec_nxt), 0);
           });
       } else {
         for (int ks0 = 0; ks0 < KS; ks0 += D) {

@@ -104,6 +104,8 @@ def lib() -> C.CDLL:
         L.mt_ensemble_topk.argtypes = [C.c_int, C.POINTER(_vp), C.POINTER(C.c_float), C.POINTER(_vp),
                                        C.POINTER(C.c_size_t), C.c_int, C.c_int, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]
         L.mt_ensemble_topk.restype = C.c_int
+        L.mt_ensemble_joint_ok.argtypes = [C.c_int, C.POINTER(_vp)]
+        L.mt_ensemble_joint_ok.restype = C.c_int
         L.mt_recomputed_rows.argtypes = [_vp, C.POINTER(C.c_int64)]
         L.mt_recomputed_rows.restype = C.c_int
         L.mt_round_bf16.argtypes = [_vp, _vp, C.c_size_t]
@@ -286,6 +288,12 @@ def mt_ensemble_step(model: Model, member, n_members, weight, B, K, S, prev_tok,
     _check(lib().mt_ensemble_step(model.handle, member, n_members, float(weight), B, K, S, _ptr(prev_tok), _ptr(src_row),
                                   n_state_rows, _ptr(state_in), _ptr(ctx), _ptr(pctx), _ptr(mask), _ptr(state_out),
                                   _ptr(comb_logits), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def mt_ensemble_joint_ok(models) -> bool:
+    n = len(models)
+    hs = (_vp * n)(*[m.handle for m in models])
+    return bool(lib().mt_ensemble_joint_ok(n, hs))
 
 
 def mt_ensemble_topk(models, weights, wss, B, K, prev_score, comb_logits, score_out, tok_out, bp_out, row_out=None,

@@ -224,15 +224,22 @@ class Ensemble:
     with its own states.  Fused (the default): every member's step adds its weighted logits
     into one buffer (mt_ensemble_step) and one selection subtracts the per-row constant
     sum_i w_i LSE_i (mt_ensemble_topk), selecting from the beam candidates the last member
-    collected on the combined values.  Materialised (fused=False): every member writes its
+    collected on the combined values; where the library supports it (joint) the members' steps
+    stop after the readout and one vocabulary pass serves them all.  Materialised (fused=False): every member writes its
     log-probabilities, mt_ensemble_logp combines them and mt_beam_topk selects.  Either way the
     first member's beam buffers hold the beam that all members read next."""
 
-    def __init__(self, members, weights, fused=True):
+    def __init__(self, members, weights, fused=True, joint=None):
         assert len(members) == len(weights) >= 1
         self.members, self.weights = list(members), [float(x) for x in weights]
         self.lead = self.members[0]
         self.fused = fused
+        # fused: one vocabulary pass for all members where the library supports it (no combined
+        # buffer), else each member adds its weighted logits into the combined buffer
+        ok = fused and mt.mt_ensemble_joint_ok([d.model for d in self.members])
+        self.joint = ok if joint is None else bool(joint)
+        if self.joint and not ok:
+            raise ValueError("the joint vocabulary pass does not support these members")
 
     def set_batch(self, ctx: np.ndarray, mask: np.ndarray, K: int):
         for d in self.members:
@@ -241,10 +248,10 @@ class Ensemble:
 
     def _alloc_logp(self):
         lead = self.lead
-        # the fused path needs only the combined buffer
+        # the fused path needs only the combined buffer, the joint pass not even that
         self.logp = [None if self.fused else torch.empty((lead.M, lead.V), dtype=torch.float32, device=lead.device)
                      for _ in self.members]
-        self.comb = torch.empty((lead.M, lead.V), dtype=torch.float32, device=lead.device)
+        self.comb = None if self.joint else torch.empty((lead.M, lead.V), dtype=torch.float32, device=lead.device)
 
     def set_source(self, src_tok: np.ndarray, mask: np.ndarray, K: int, stream=None):
         """Batch from source tokens: every member encodes them with its own encoder (mt_encode)

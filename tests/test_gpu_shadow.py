@@ -224,7 +224,7 @@ def test_ensemble_from_source_tokens():
         w = {**synth.make_weights(q, peaked_bias=True), **synth.make_encoder_weights(q, src_V)}
         members.append((q, w))
         decs.append(Decoder(q.E, q.H, q.A, q.V, w, k_max=q.K, src_V=src_V))
-    ens = Ensemble(decs, [0.6, 0.4])
+    ens = Ensemble(decs, [0.6, 0.4], joint=False)   # the per-member pass keeps the combined buffer
     ens.set_source(src, mask, p.K)
     ens.precompute()
     tok0, _, score0 = synth.start_beam(p)
