@@ -515,10 +515,11 @@ static hipError_t vgo_k(const VocabArgs &a, hipStream_t st) {
   return a.fixed_ref ? vgo<CT, HB, D, true, false, KSC>(a, st) : vgo<CT, HB, D, false, false, KSC>(a, st);
 }
 
-// bf16 at E = 512 (32 k-steps) takes the unrolled form
+// E = 512 (bf16: 32 k-steps, fp32: 64) takes the unrolled form
 template <typename CT, int HB, int D>
 static hipError_t vgo_f(const VocabArgs &a, hipStream_t st) {
   if (sizeof(CT) == 2 && a.KS == 32 && 32 % D == 0) return vgo_k<CT, HB, D, 32>(a, st);
+  if (sizeof(CT) == 4 && a.KS == 64 && 64 % D == 0) return vgo_k<CT, HB, D, 64>(a, st);
   return vgo_k<CT, HB, D, 0>(a, st);
 }
 
