@@ -301,6 +301,17 @@ mt_status mt_ensemble_topk(int n, mt_model *const *models, const float *weights,
                            const size_t *ws_bytes, int B, int K, const float *prev_score, const float *comb_logits,
                            float *score_out, int32_t *tok_out, int32_t *bp_out, int32_t *row_out, float *row_const_out,
                            void *stream);
+/* Recurrent-product operand reuse (bf16 models; Section 2.1: the step's fused kernels).  Every
+ * step of a bf16 model leaves in its workspace the bf16 copy of state_out that the next
+ * products read.  With on != 0, a step whose state_in is the state_out pointer of the
+ * previous step on this model, with the same workspace and n_state_rows = that step's B*K,
+ * gathers that copy for h U1 instead of rounding state_in again: the results are
+ * bit-identical, PROVIDED the caller has not written to that state buffer since; a caller
+ * that edits states between steps must leave this off (the default) for the step after the
+ * edit.  Switching it does not forget the copy; any other call on the model (precompute,
+ * encode, second-source keys) does.  fp32 models: no effect. */
+mt_status mt_set_state_reuse(mt_model *model, int on);
+
 /* 1 if the joint vocabulary pass supports these n members (2 <= n <= 4, single-source, equal V,
  * E and gemm dtype, the members' readout activations of one row block fitting one workgroup's
  * LDS together), else 0.  models: HOST array. */

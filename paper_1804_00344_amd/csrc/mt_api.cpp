@@ -102,6 +102,11 @@ struct mt_model {
   int last_ens_n = 0;      // the last step ran as the last of this many fused-ensemble members (0: not)
   float last_ens_w = 0.f;  // and with this weight
   int last_ens_joint = 0;  // the last step was a member of this many for the joint vocabulary pass
+  // bf16 copy of a state the step wrote (mt_set_state_reuse): state_out, workspace and rows of
+  // the last step, whose workspace holds the copy (cleared by every other call on the model)
+  int reuse_state = 0;
+  const void *shadow_of = nullptr, *shadow_ws = nullptr;
+  int shadow_rows = 0;
   // profiling
   uint32_t prof_mask = 0;
   ProfSlot prof[MT_KERNEL_COUNT];
@@ -672,6 +677,7 @@ mt_status mt_encode(mt_model *model, int B, int S, const int32_t *src_tok, const
                     void *ws, size_t ws_bytes, void *stream) {
   g_err[0] = 0;
   if (!valid_model(model)) return fail(MT_ERR_ARG, "invalid model handle");
+  model->shadow_of = nullptr;
   if (model->cfg.src_V <= 0) return fail(MT_ERR_STATE, "the model has no encoder (src_V = 0)");
   if (B < 1 || S < 1 || S > 1024) return fail(MT_ERR_SHAPE, "B=%d S=%d: need B >= 1, 1 <= S <= 1024", B, S);
   if ((long long)B * S > (1 << 24)) return fail(MT_ERR_SHAPE, "B*S exceeds 2^24");
@@ -798,6 +804,7 @@ mt_status mt_encode(mt_model *model, int B, int S, const int32_t *src_tok, const
 // caller).  timed = false launches without the profiling events (the no-alloc entry point).
 static mt_status precompute_impl(mt_model *model, int B, int S, const void *ctx, const float *mask, void *pctx_out,
                                  float *s0_out, void *ws, hipStream_t st, bool timed) {
+  model->shadow_of = nullptr;
   const mt_config &c = model->cfg;
   const int H = c.H, A = c.A, C = model->C;
   float *cbar = (float *)ws;
@@ -927,7 +934,14 @@ static mt_status decoder_step_impl(mt_model *model, int B, int K, int S, const i
   // GRU 1: h U1 (the gathered previous state), then the cell with the token side gathered
   // from the precomputed x [W1 | Wt_y] + [b1 | 0] table
   GemmProblem p1{};
-  p1.A = state_in; p1.a_idx = src_row; p1.a_rows = n_state_rows; p1.lda = H; p1.a_bf16 = 0;
+  // bf16 models under mt_set_state_reuse: when state_in is the previous step's state_out on
+  // this workspace, the product gathers the bf16 copy of it that step left there (the very
+  // values it would round state_in to)
+  const bool shadow = bf && model->reuse_state && state_in == model->shadow_of && ws == model->shadow_ws &&
+                      n_state_rows == model->shadow_rows;
+  model->shadow_of = nullptr;  // valid again only once this step has completed its launches
+  p1.A = shadow ? (const void *)(W + L.sth) : (const void *)state_in;
+  p1.a_idx = src_row; p1.a_rows = n_state_rows; p1.lda = H; p1.a_bf16 = shadow ? 1 : 0;
   p1.Bp = model->w1h.p; p1.ldb = model->w1h.ldb; p1.wblk = model->w1h.blk; p1.bias = nullptr;
   p1.out = gh; p1.ldc = 3 * H; p1.M = M; p1.N = 3 * H; p1.K = H;
   p1.err = model->err; p1.err_bit = 1;
@@ -1026,6 +1040,9 @@ static mt_status decoder_step_impl(mt_model *model, int B, int K, int S, const i
   model->last_B = B;
   model->last_K = K;
   model->last_ws = ws;
+  model->shadow_of = bf ? state_out : nullptr;  // the step's bf16 copy of state_out is in L.sth
+  model->shadow_ws = ws;
+  model->shadow_rows = M;
   model->last_ens_n = ens ? ens_last : 0;
   model->last_ens_w = ens_w;
   model->last_ens_joint = 0;  // set by mt_ensemble_step
@@ -1129,6 +1146,13 @@ static mt_status ensemble_topk_joint(int n, mt_model *const *models, const float
   rs.score_out = score_out; rs.tok_out = tok_out; rs.bp_out = bp_out; rs.row_out = row_out;
   rs.nrecompute = model->nrecompute;
   LAUNCH(MT_KERNEL_TOPK, launch_row_select(rs, st));
+  return MT_OK;
+}
+
+mt_status mt_set_state_reuse(mt_model *model, int on) {
+  g_err[0] = 0;
+  if (!valid_model(model)) return fail(MT_ERR_ARG, "invalid model handle");
+  model->reuse_state = on ? 1 : 0;
   return MT_OK;
 }
 
@@ -1247,6 +1271,7 @@ mt_status mt_precompute_keys2(mt_model *model, int B, int S2, const void *ctx2, 
                               void *pctx2_out, void *ws, size_t ws_bytes, void *stream) {
   g_err[0] = 0;
   if (!valid_model(model)) return fail(MT_ERR_ARG, "invalid model handle");
+  model->shadow_of = nullptr;
   if (!model->cfg.dual_source) return fail(MT_ERR_STATE, "not a dual-source model (dual_source = 0)");
   if (B < 1 || S2 < 1 || S2 > 1024) return fail(MT_ERR_SHAPE, "B=%d S2=%d: need B >= 1, 1 <= S2 <= 1024", B, S2);
   if ((long long)B * S2 > (1 << 24)) return fail(MT_ERR_SHAPE, "B*S2 exceeds 2^24");

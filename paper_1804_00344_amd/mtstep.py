@@ -104,6 +104,8 @@ def lib() -> C.CDLL:
         L.mt_ensemble_topk.argtypes = [C.c_int, C.POINTER(_vp), C.POINTER(C.c_float), C.POINTER(_vp),
                                        C.POINTER(C.c_size_t), C.c_int, C.c_int, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]
         L.mt_ensemble_topk.restype = C.c_int
+        L.mt_set_state_reuse.argtypes = [_vp, C.c_int]
+        L.mt_set_state_reuse.restype = C.c_int
         L.mt_ensemble_joint_ok.argtypes = [C.c_int, C.POINTER(_vp)]
         L.mt_ensemble_joint_ok.restype = C.c_int
         L.mt_recomputed_rows.argtypes = [_vp, C.POINTER(C.c_int64)]
@@ -288,6 +290,10 @@ def mt_ensemble_step(model: Model, member, n_members, weight, B, K, S, prev_tok,
     _check(lib().mt_ensemble_step(model.handle, member, n_members, float(weight), B, K, S, _ptr(prev_tok), _ptr(src_row),
                                   n_state_rows, _ptr(state_in), _ptr(ctx), _ptr(pctx), _ptr(mask), _ptr(state_out),
                                   _ptr(comb_logits), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def mt_set_state_reuse(model: Model, on: bool):
+    _check(lib().mt_set_state_reuse(model.handle, 1 if on else 0))
 
 
 def mt_ensemble_joint_ok(models) -> bool:

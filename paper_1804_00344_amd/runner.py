@@ -7,6 +7,7 @@ provides device memory and the stream; all arithmetic runs in libmtstep.
 """
 from __future__ import annotations
 
+import contextlib
 from typing import Dict, Optional
 
 import numpy as np
@@ -32,6 +33,7 @@ class Decoder:
         with torch.cuda.device(self.device):
             self.model = mt.mt_load_weights(self.cfg, weights)
         self.io_dtype = torch.bfloat16 if gemm == "bf16" else torch.float32
+        self.reuse_state = True  # the decode loop's steps reuse the previous step's bf16 state copy
 
     @classmethod
     def from_preset(cls, p, weights, **kw):
@@ -146,6 +148,20 @@ class Decoder:
         self.score.copy_(self._start_score)
         self.first = True
 
+    @contextlib.contextmanager
+    def _reuse(self):
+        """Within the decode loop the state a step reads is the previous step's output, which
+        nothing else writes: a bf16 model's step may take the copy of it the previous step
+        left in the workspace (mt_set_state_reuse), for that call only."""
+        on = self.reuse_state and self.gemm == "bf16" and not self.first
+        if on:
+            mt.mt_set_state_reuse(self.model, True)
+        try:
+            yield
+        finally:
+            if on:
+                mt.mt_set_state_reuse(self.model, False)
+
     def advance(self, *, logp=None, attn=None, stream=None):
         """One beam-search step: decoder step on the current beam, then top-K in place."""
         if self.first:
@@ -153,7 +169,8 @@ class Decoder:
         else:
             state_in, nrows = self.state[self.cur], self.M
         out = self.state[1 - self.cur] if not self.first else self.state[self.cur]
-        self.step(self.tok, self.row, state_in, nrows, out, logp=logp, attn=attn, stream=stream)
+        with self._reuse():
+            self.step(self.tok, self.row, state_in, nrows, out, logp=logp, attn=attn, stream=stream)
         self.topk(self.score, None, stream=stream)
         if not self.first:
             self.cur = 1 - self.cur
@@ -280,11 +297,13 @@ class Ensemble:
             else:
                 state_in, nrows = d.state[d.cur], d.M
             out = d.state[1 - d.cur] if not d.first else d.state[d.cur]
-            if self.fused:
-                mt.mt_ensemble_step(d.model, i, len(self.members), self.weights[i], d.B, d.K, d.S, lead.tok, lead.row,
-                                    nrows, state_in, d.ctx, d.pctx, d.mask, out, self.comb, d.ws, stream=stream)
-            else:
-                d.step(lead.tok, lead.row, state_in, nrows, out, logp=lp, stream=stream)
+            with d._reuse():
+                if self.fused:
+                    mt.mt_ensemble_step(d.model, i, len(self.members), self.weights[i], d.B, d.K, d.S, lead.tok,
+                                        lead.row, nrows, state_in, d.ctx, d.pctx, d.mask, out, self.comb, d.ws,
+                                        stream=stream)
+                else:
+                    d.step(lead.tok, lead.row, state_in, nrows, out, logp=lp, stream=stream)
         if self.fused:
             mt.mt_ensemble_topk([d.model for d in self.members], self.weights, [d.ws for d in self.members], lead.B,
                                 lead.K, lead.score, self.comb, lead.score, lead.tok, lead.bp, lead.row,

@@ -435,6 +435,39 @@ def test_candidate_buffer_overflow_falls_back_exactly():
 # states; their log-probabilities are combined on the GPU and one selection extends the beam
 # ------------------------------------------------------------------------------------------
 
+@pytest.mark.parametrize("name", ["tiny_bf16_ln", "nematus_bf16_ln", "deep_bf16_ln"])
+def test_state_reuse_is_bit_identical(name):
+    """bf16 models: steps that gather the bf16 copy of the previous state from the workspace
+    (mt_set_state_reuse, as the decode loop runs them) give bit-identical states, scores and
+    beams to steps that round the fp32 state again, over several steps and a restart."""
+    p = synth.PRESETS[name]
+    w = synth.make_weights(p, peaked_bias=True)
+    ctx, mask, _ = synth.make_source(p)
+    dec = Decoder.from_preset(p, w)
+    dec.set_batch(ctx, mask, p.K)
+    tok0, _, score0 = synth.start_beam(p)
+    runs = []
+    for reuse in (True, False, True):
+        dec.reuse_state = reuse
+        rec = []
+        for restart in range(2):
+            dec.precompute()
+            dec.start(tok0, score0)
+            for _ in range(4):
+                st = dec.advance()
+                rec.append([x.clone() for x in (st, dec.score, dec.tok, dec.bp)])
+        torch.cuda.synchronize()
+        runs.append(rec)
+    assert mt.mt_device_errors(dec.model) == 0
+    for a, b in zip(runs[0], runs[1]):
+        for x, y in zip(a, b):
+            assert torch.equal(x, y)
+    for a, b in zip(runs[0], runs[2]):
+        for x, y in zip(a, b):
+            assert torch.equal(x, y)
+    log(f"[state reuse] {name}: 8 steps bit-identical with and without the bf16 state copy")
+
+
 def exact_topk_check(B, K, keys, sc, tk, bp):
     """sc/tk/bp [B*K] are, per sentence, the K best of keys [B*K, V] (flattened k*V + v),
     larger key first, equal keys by smaller flat index; bit-exact."""
@@ -492,6 +525,39 @@ def test_ensemble_step_parity(name, weights):
     mt.mt_ensemble_logp(decs[0].model, logps, weights, base.M, logps[0])
     torch.cuda.synchronize()
     assert torch.max(torch.abs(logps[0].double() - ref)).item() <= 1e-4
+
+
+@pytest.mark.parametrize("name", ["tiny_bf16_ln", "nematus_bf16_ln", "deep_bf16_ln"])
+def test_state_reuse_is_bit_identical(name):
+    """bf16 models: steps that gather the bf16 copy of the previous state from the workspace
+    (mt_set_state_reuse, as the decode loop runs them) give bit-identical states, scores and
+    beams to steps that round the fp32 state again, over several steps and a restart."""
+    p = synth.PRESETS[name]
+    w = synth.make_weights(p, peaked_bias=True)
+    ctx, mask, _ = synth.make_source(p)
+    dec = Decoder.from_preset(p, w)
+    dec.set_batch(ctx, mask, p.K)
+    tok0, _, score0 = synth.start_beam(p)
+    runs = []
+    for reuse in (True, False, True):
+        dec.reuse_state = reuse
+        rec = []
+        for restart in range(2):
+            dec.precompute()
+            dec.start(tok0, score0)
+            for _ in range(4):
+                st = dec.advance()
+                rec.append([x.clone() for x in (st, dec.score, dec.tok, dec.bp)])
+        torch.cuda.synchronize()
+        runs.append(rec)
+    assert mt.mt_device_errors(dec.model) == 0
+    for a, b in zip(runs[0], runs[1]):
+        for x, y in zip(a, b):
+            assert torch.equal(x, y)
+    for a, b in zip(runs[0], runs[2]):
+        for x, y in zip(a, b):
+            assert torch.equal(x, y)
+    log(f"[state reuse] {name}: 8 steps bit-identical with and without the bf16 state copy")
 
 
 def exact_topk_check(B, K, keys, sc, tk, bp):
