@@ -339,6 +339,23 @@ mt_status mt_beam_finish(mt_model *model, int B, int K, int step, int32_t eos, f
                          int32_t *fin_count, int32_t *hist_tok, int32_t *hist_bp, float *fin_score,
                          float *fin_norm, int32_t *fin_step, int32_t *fin_parent, int32_t *fin_tok, void *stream);
 
+/* The n-best lists of a finished translation batch from mt_beam_finish's records (decoding to
+ * an n-best list as large as the beam, Sections 2.3 and 3.1.3), on the device.  Per sentence b
+ * with fc = min(fin_count[b], K) finished entries (b*K + e, e < fc, as mt_beam_finish wrote
+ * them):
+ *   order[b*K + r] = the entry e of rank r (fin_norm descending, equal values by smaller e),
+ *     -1 for r >= fc;
+ *   seq[(b*K + r) * ld_seq + s] = token s of that hypothesis for s <= its fin_step (the last is
+ *     its fin_tok, the earlier ones read back through hist_tok / hist_bp of steps fin_step-1 ..
+ *     0, starting from fin_parent), -1 after it and in rows of unused ranks.
+ * hist_tok, hist_bp: device int32 [steps][B*K], the records of steps 0 .. steps-1; fin_*: as
+ * mt_beam_finish left them; order [B*K], seq [B*K][ld_seq] device int32, ld_seq >= steps.
+ * 1 <= K <= 16.  Asynchronous on the stream. */
+mt_status mt_beam_nbest(mt_model *model, int B, int K, int steps, const int32_t *hist_tok, const int32_t *hist_bp,
+                        const int32_t *fin_count, const float *fin_norm, const int32_t *fin_step,
+                        const int32_t *fin_parent, const int32_t *fin_tok, int32_t *order, int32_t *seq, int ld_seq,
+                        void *stream);
+
 /* Reads and clears the device-side error bits (synchronises the device):
  * bit 0 = a prev_tok out of range, bit 1 = a src_row out of range, bit 3 = a source token of
  * mt_encode out of range. */

@@ -1398,6 +1398,34 @@ mt_status mt_beam_finish(mt_model *model, int B, int K, int step, int32_t eos, f
   return MT_OK;
 }
 
+mt_status mt_beam_nbest(mt_model *model, int B, int K, int steps, const int32_t *hist_tok, const int32_t *hist_bp,
+                        const int32_t *fin_count, const float *fin_norm, const int32_t *fin_step,
+                        const int32_t *fin_parent, const int32_t *fin_tok, int32_t *order, int32_t *seq, int ld_seq,
+                        void *stream) {
+  g_err[0] = 0;
+  if (!valid_model(model)) return fail(MT_ERR_ARG, "invalid model handle");
+  if (B < 1 || K < 1 || K > kKMax) return fail(MT_ERR_SHAPE, "B=%d K=%d: need B >= 1, 1 <= K <= %d", B, K, kKMax);
+  if ((long long)B * K > (1 << 20)) return fail(MT_ERR_SHAPE, "B*K exceeds 2^20");
+  if (steps < 1) return fail(MT_ERR_SHAPE, "steps=%d must be >= 1", steps);
+  if (ld_seq < steps) return fail(MT_ERR_SHAPE, "ld_seq=%d < steps=%d", ld_seq, steps);
+  if ((long long)B * K * ld_seq > (1ll << 31) || (long long)steps * B * K > (1ll << 31))
+    return fail(MT_ERR_SHAPE, "records or sequences exceed 2^31 entries");
+  struct {
+    const void *p;
+    const char *n;
+  } ptrs[] = {{hist_tok, "hist_tok"}, {hist_bp, "hist_bp"}, {fin_count, "fin_count"}, {fin_norm, "fin_norm"},
+              {fin_step, "fin_step"}, {fin_parent, "fin_parent"}, {fin_tok, "fin_tok"}, {order, "order"},
+              {seq, "seq"}};
+  for (auto &q : ptrs) CHECK(check_dev_ptr(q.p, q.n, 4));
+  hipStream_t st = (hipStream_t)stream;
+  BeamNbest a{};
+  a.K = K; a.steps = steps; a.ld_hist = B * K; a.ld_seq = ld_seq;
+  a.hist_tok = hist_tok; a.hist_bp = hist_bp; a.fin_count = fin_count; a.fin_norm = fin_norm;
+  a.fin_step = fin_step; a.fin_parent = fin_parent; a.fin_tok = fin_tok; a.order = order; a.seq = seq;
+  LAUNCH(MT_KERNEL_BEAM_FINISH, launch_beam_nbest(a, B, st));
+  return MT_OK;
+}
+
 mt_status mt_device_errors(mt_model *model, int32_t *flags) {
   g_err[0] = 0;
   if (!valid_model(model)) return fail(MT_ERR_ARG, "invalid model handle");

@@ -583,6 +583,16 @@ struct BeamFinish {
   int32_t *fin_step, *fin_parent, *fin_tok;
 };
 hipError_t launch_beam_finish(const BeamFinish &a, int B, hipStream_t st);
+struct BeamNbest {
+  int K, steps, ld_hist, ld_seq;
+  const int32_t *hist_tok, *hist_bp;  // [steps][ld_hist]
+  const int32_t *fin_count;           // [B]
+  const float *fin_norm;              // [B][K]
+  const int32_t *fin_step, *fin_parent, *fin_tok;
+  int32_t *order;                     // [B][K]
+  int32_t *seq;                       // [B*K][ld_seq]
+};
+hipError_t launch_beam_nbest(const BeamNbest &a, int B, hipStream_t st);
 
 // ensemble combination out[i] = sum_j w[j] * in[j][i] over count elements (16-byte aligned
 // buffers; out may be one of the inputs); 1 <= n <= kMaxEnsemble

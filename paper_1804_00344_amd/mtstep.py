@@ -104,6 +104,8 @@ def lib() -> C.CDLL:
         L.mt_ensemble_topk.argtypes = [C.c_int, C.POINTER(_vp), C.POINTER(C.c_float), C.POINTER(_vp),
                                        C.POINTER(C.c_size_t), C.c_int, C.c_int, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]
         L.mt_ensemble_topk.restype = C.c_int
+        L.mt_beam_nbest.argtypes = [_vp, C.c_int, C.c_int, C.c_int] + [_vp] * 9 + [C.c_int, _vp]
+        L.mt_beam_nbest.restype = C.c_int
         L.mt_set_state_reuse.argtypes = [_vp, C.c_int]
         L.mt_set_state_reuse.restype = C.c_int
         L.mt_ensemble_joint_ok.argtypes = [C.c_int, C.POINTER(_vp)]
@@ -290,6 +292,14 @@ def mt_ensemble_step(model: Model, member, n_members, weight, B, K, S, prev_tok,
     _check(lib().mt_ensemble_step(model.handle, member, n_members, float(weight), B, K, S, _ptr(prev_tok), _ptr(src_row),
                                   n_state_rows, _ptr(state_in), _ptr(ctx), _ptr(pctx), _ptr(mask), _ptr(state_out),
                                   _ptr(comb_logits), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def mt_beam_nbest(model: Model, B, K, steps, hist_tok, hist_bp, fin_count, fin_norm, fin_step, fin_parent, fin_tok,
+                  order, seq, stream=None):
+    ld_seq = seq.shape[1]
+    _check(lib().mt_beam_nbest(model.handle, B, K, steps, _ptr(hist_tok), _ptr(hist_bp), _ptr(fin_count),
+                               _ptr(fin_norm), _ptr(fin_step), _ptr(fin_parent), _ptr(fin_tok), _ptr(order), _ptr(seq),
+                               ld_seq, _stream(stream)))
 
 
 def mt_set_state_reuse(model: Model, on: bool):

@@ -178,16 +178,6 @@ class Decoder:
         return self.state[self.cur]
 
 
-def backtrack(K, hist_tok, hist_bp, b, step, parent, token):
-    """Token sequence of a finished hypothesis through the recorded beams (host arrays)."""
-    seq = [int(token)]
-    p = int(parent)
-    for s in range(step - 1, -1, -1):
-        seq.append(int(hist_tok[s, b * K + p]))
-        p = int(hist_bp[s, b * K + p])
-    return seq[::-1]
-
-
 def translate(dec: "Decoder", tok0, score0, max_steps: int, eos: int, alpha: float, check_every: int = 4,
               stream=None):
     """Batched beam search to finished translations: steps, selections and the device-side
@@ -213,26 +203,20 @@ def translate(dec: "Decoder", tok0, score0, max_steps: int, eos: int, alpha: flo
         steps = t + 1
         if (t + 1) % check_every == 0 and int(beam.sum().item()) == 0:
             break
-    ht, hb = hist_tok[:steps].cpu().numpy(), hist_bp[:steps].cpu().numpy()
-    fc = fcount.cpu().numpy()
-    fs, fn, fst, fpa, fto = [x.cpu().numpy() for x in (fs, fn, fst, fpa, fto)]
-    # every finished hypothesis at once: walk the recorded beams back one step at a time
-    sel = np.concatenate([b * K + np.arange(int(fc[b])) for b in range(B)]).astype(np.int64)
-    fb = sel // K
-    step_of, parent = fst[sel].astype(np.int64), fpa[sel].astype(np.int64)
-    seqs = np.full((sel.size, max(steps, 1)), -1, np.int64)
-    seqs[np.arange(sel.size), step_of] = fto[sel]
-    for s in range(steps - 2, -1, -1):
-        act = step_of > s
-        idx = fb[act] * K + parent[act]
-        seqs[act, s] = ht[s, idx]
-        parent[act] = hb[s, idx]
-    nbest = [[] for _ in range(B)]
-    for e in range(sel.size):
-        f = sel[e]
-        nbest[fb[e]].append((float(fn[f]), float(fs[f]), seqs[e, :step_of[e] + 1].tolist()))
-    for lst in nbest:
-        lst.sort(key=lambda x: -x[0])
+    # the n-best lists ranked and backtracked on the device (mt_beam_nbest); the host only
+    # unpacks them
+    order = torch.empty(M, dtype=torch.int32, device=d)
+    seq = torch.empty((M, max(steps, 1)), dtype=torch.int32, device=d)
+    mt.mt_beam_nbest(dec.model, B, K, steps, hist_tok, hist_bp, fcount, fn, fst, fpa, fto, order, seq, stream=stream)
+    fc, od, sq = fcount.cpu().numpy(), order.cpu().numpy(), seq.cpu().numpy()
+    fs, fn, fst = fs.cpu().numpy(), fn.cpu().numpy(), fst.cpu().numpy()
+    nbest = []
+    for b in range(B):
+        lst = []
+        for r in range(min(int(fc[b]), K)):
+            f = b * K + int(od[b * K + r])
+            lst.append((float(fn[f]), float(fs[f]), sq[b * K + r, :int(fst[f]) + 1].tolist()))
+        nbest.append(lst)
     return nbest, steps
 
 

@@ -700,6 +700,53 @@ def test_fused_ensemble_step_parity(name, weights, peaked):
 # translation bookkeeping (mt_beam_finish) and whole translations
 # ------------------------------------------------------------------------------------------
 
+@pytest.mark.parametrize("B,K,steps", [(7, 12, 9), (3, 16, 1), (5, 1, 6), (64, 12, 40)])
+def test_beam_nbest_bit_exact(B, K, steps):
+    """mt_beam_nbest on random records (ties in the normalised scores, empty and full lists,
+    hypotheses finished at every step) against a plain CPU ranking and walk back through the
+    records: order and token rows equal."""
+    p = synth.PRESETS["tiny_f32"]
+    dec = Decoder(p.E, p.H, p.A, p.V, synth.make_weights(p), k_max=16)
+    rng = np.random.default_rng(7 + B * K + steps)
+    M = B * K
+    ht = rng.integers(0, 1000, (steps, M)).astype(np.int32)
+    hb = rng.integers(0, K, (steps, M)).astype(np.int32)
+    fc = rng.integers(0, K + 1, B).astype(np.int32)
+    fc[0], fc[-1] = K, 0
+    fn = rng.choice(np.array([-1.5, -2.0, -0.25, -3.0], np.float32), M) + \
+        (rng.random(M) < 0.5) * rng.standard_normal(M).astype(np.float32)
+    fn = fn.astype(np.float32)
+    fst = rng.integers(0, steps, M).astype(np.int32)
+    fpa = rng.integers(0, K, M).astype(np.int32)
+    fto = rng.integers(0, 1000, M).astype(np.int32)
+    ld = steps + 3
+    order = torch.full((M,), 77, dtype=torch.int32, device=DEV)
+    seq = torch.full((M, ld), 77, dtype=torch.int32, device=DEV)
+    mt.mt_beam_nbest(dec.model, B, K, steps, T(ht), T(hb), T(fc), T(fn), T(fst), T(fpa), T(fto), order, seq)
+    torch.cuda.synchronize()
+    g_order, g_seq = order.cpu().numpy(), seq.cpu().numpy()
+    for b in range(B):
+        ents = list(range(int(fc[b])))
+        ents.sort(key=lambda e: (-float(fn[b * K + e]), e))
+        for r in range(K):
+            row = g_seq[b * K + r]
+            if r >= len(ents):
+                assert g_order[b * K + r] == -1 and np.all(row == -1), (b, r)
+                continue
+            e = ents[r]
+            f = b * K + e
+            assert g_order[b * K + r] == e, (b, r, g_order[b * K + r], e)
+            toks = [int(fto[f])]
+            par = int(fpa[f])
+            for st in range(int(fst[f]) - 1, -1, -1):
+                toks.append(int(ht[st, b * K + par]))
+                par = int(hb[st, b * K + par])
+            toks = toks[::-1]
+            n = len(toks)
+            assert row[:n].tolist() == toks, (b, r)
+            assert np.all(row[n:] == -1), (b, r)
+
+
 @pytest.mark.parametrize("B,K,final", [(5, 4, False), (7, 12, False), (3, 16, True), (4, 1, False)])
 def test_beam_finish_bit_exact(B, K, final):
     """Random ranked beams (some EOS tokens, some -inf scores, beams already shrunk) through
