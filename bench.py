@@ -348,8 +348,12 @@ def main():
         # HBM bytes per launch from the FETCH_SIZE / WRITE_SIZE passes, valid only while the
         # vocabulary kernel's source is the one the counters were taken on
         tf = json.load(open(TRAFFIC_FILE))
-        ent = tf.get(p.name, {}).get("vocab_gemm") if vocab_members == 1 else None
-        src_h = source_hash(os.path.join(ROOT, "paper_1804_00344_amd", "csrc", "mt_vocab.hip"))
+        if vocab_members == 1:
+            ent = tf.get(p.name, {}).get("vocab_gemm")
+            src_h = source_hash(os.path.join(ROOT, "paper_1804_00344_amd", "csrc", "mt_vocab.hip"))
+        else:
+            ent = tf.get(f"{p.name}_ens{NE}", {}).get("vocab_joint")
+            src_h = source_hash(os.path.join(ROOT, "paper_1804_00344_amd", "csrc", "mt_vocab_joint.hip"))
         if ent and ent.get("source_hash") == src_h:
             traffic = ent["bytes_per_launch"]
     roofline = {

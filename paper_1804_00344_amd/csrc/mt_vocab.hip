@@ -413,7 +413,7 @@ __global__ __launch_bounds__((VShape<CT, HB>::NT)) void vocab_kernel(VocabArgs a
 // share a lane, at a small fraction of the cost.
 // A fused ensemble's last member thresholds the combined values instead: cw * sample[m][v],
 // plus comb[m][v] (the earlier members' weighted logits, row stride V) when there are any.
-template <int R>
+template <int R, bool COMB>
 __global__ __launch_bounds__(256) void vocab_threshold_kernel(int M, int S, int K, const float *__restrict__ sample,
                                                               int ld, float *__restrict__ thr, int *scnt, int B,
                                                               const float *__restrict__ comb, int V, float cw) {
@@ -427,7 +427,10 @@ __global__ __launch_bounds__(256) void vocab_threshold_kernel(int M, int S, int 
 #pragma unroll
   for (int s = 0; s < R; ++s) {
     const int v = s * 64 + lane;
-    x[s] = v < S ? (comb ? cw * row[v] + comb[(size_t)m * V + v] : cw * row[v]) : -INFINITY;
+    if constexpr (COMB)
+      x[s] = v < S ? cw * row[v] + (comb ? comb[(size_t)m * V + v] : 0.f) : -INFINITY;
+    else
+      x[s] = v < S ? row[v] : -INFINITY;
   }
   uint32_t um[1] = {0u};
 #pragma unroll
@@ -572,8 +575,14 @@ hipError_t launch_vocab_threshold(int M, int V, int K, const float *sample, floa
   if (M == 0) return hipSuccess;
   const int S = vocab_sample_size(V);
   const int Sv = V < S ? V : S;  // entries >= V of the sample are padding
-  hipLaunchKernelGGL((vocab_threshold_kernel<kSampleMax / 64>), dim3((M + 3) / 4), dim3(256), 0, st, M, Sv, K,
-                     sample, S, thr, scnt, B, comb, V, w);
+  // a fused ensemble's last member (weight w, earlier members' values comb) takes the combined
+  // form; a single model's the plain one
+  if (comb || w != 1.f)
+    hipLaunchKernelGGL((vocab_threshold_kernel<kSampleMax / 64, true>), dim3((M + 3) / 4), dim3(256), 0, st, M, Sv,
+                       K, sample, S, thr, scnt, B, comb, V, w);
+  else
+    hipLaunchKernelGGL((vocab_threshold_kernel<kSampleMax / 64, false>), dim3((M + 3) / 4), dim3(256), 0, st, M, Sv,
+                       K, sample, S, thr, scnt, B, comb, V, w);
   return hipGetLastError();
 }
 

@@ -104,6 +104,11 @@ def traffic(fetch_dir, write_dir, preset, calib_mib, kernel, cmd, json_path=None
 # kernel name substring -> (class, source file): the counters of a class are valid while its
 # source file hashes as recorded
 KERNEL_CLASSES = [
+    ("vocab_joint_threshold_kernel", "vocab_joint_threshold", "mt_vocab_joint.hip"),
+    ("vocab_joint_kernel", "vocab_joint", "mt_vocab_joint.hip"),
+    ("ensemble_const_kernel", "ensemble_const", "mt_ensemble.hip"),
+    ("beam_finish_kernel", "beam_finish", "mt_beam.hip"),
+    ("beam_nbest_kernel", "beam_nbest", "mt_beam.hip"),
     ("vocab_threshold_kernel", "vocab_threshold", "mt_vocab.hip"),
     ("vocab_kernel", "vocab_gemm", "mt_vocab.hip"),
     ("attention_order_kernel", "attention_order", "mt_attention.hip"),
@@ -197,8 +202,8 @@ def counters(fetch_dir, write_dir, mfma_dir, preset, calib_mib, cmd, json_path=N
                       "mfma_busy": None if r["busy"] is None else round(r["busy"], 4),
                       "fetch_scale": round(ff, 4), "write_scale": round(wf, 4), "source": r["src"],
                       "source_hash": r["src_hash"], "command": cmd}
-            if r["cls"] == "vocab_gemm":
-                ent["vocab_gemm"] = dict(ent[k])
+            if r["cls"] in ("vocab_gemm", "vocab_joint"):
+                ent[r["cls"]] = dict(ent[k])
         json.dump(data, open(json_path, "w"), indent=1, sort_keys=True)
     return "\n".join(md) + "\n"
 
