@@ -578,7 +578,8 @@ def exact_topk_check(B, K, keys, sc, tk, bp):
                                                  ("nematus_bf16_ln", (0.7, 0.3), True),
                                                  ("tiny_bf16_ln", (0.2, 0.5, 0.3), True),
                                                  ("nematus_bf16_ln", (0.5, 0.5), False),
-                                                 ("tiny_f32", (0.1, 0.2, 0.3, 0.4), False)])
+                                                 ("tiny_f32", (0.1, 0.2, 0.3, 0.4), False),
+                                                 ("nematus_bf16_ln", (0.3, 0.3, 0.4), False)])
 def test_fused_ensemble_step_parity(name, weights, peaked):
     """Fused ensemble: each member adds its weighted logits into one buffer and the selection
     subtracts the per-row constant sum_i w_i LSE_i; the combined log-probabilities (buffer minus
