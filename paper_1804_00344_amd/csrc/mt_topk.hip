@@ -117,6 +117,8 @@ __global__ __launch_bounds__(kTT) void row_select_kernel(RowSelect a) {
   __shared__ int qi[4][KMAX];
   __shared__ int qn[4];
   __shared__ int last;
+  __shared__ float res_key;  // K = 1: the row's result is the sentence's
+  __shared__ int res_tok;
   const int m = blockIdx.x, t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int K = a.K, V = a.V, nl = a.nl, cap = a.cap;
   const int b = m / K;
@@ -151,10 +153,19 @@ __global__ __launch_bounds__(kTT) void row_select_kernel(RowSelect a) {
                            : block_row_lse(a.part + (size_t)m * a.ntiles, a.ntiles);
   const float sc = fused ? a.prev_score[m] : 0.f;
   int2 *out = a.row_cand + (size_t)m * K;
-  auto emit_row = [&](int rank, float key, int tok) { put_row(out + rank, key, tok); };
+  // A row result goes to the row-candidate buffer for the sentence merge; with K = 1 the row
+  // is the sentence, and its result is kept in LDS for the outputs (no merge, no hand-off).
+  auto emit_row = [&](int rank, float key, int tok) {
+    if (K == 1) {
+      res_key = key;
+      res_tok = tok;
+    } else {
+      put_row(out + rank, key, tok);
+    }
+  };
 
   if (fused && sc == -INFINITY) {  // every key of the row is -inf: the K smallest tokens win
-    if (t < K) put_row(out + t, -INFINITY, t);
+    if (t < K) emit_row(t, -INFINITY, t);
   } else {
     // ---- list fill counts and the block-wide offsets of this thread's entries ----
     int mine = 0;
@@ -283,11 +294,23 @@ __global__ __launch_bounds__(kTT) void row_select_kernel(RowSelect a) {
         uint32_t u[1] = {src >= 0 ? qu[src][r] : 0u};
         int ix[1] = {src >= 0 ? qi[src][r] : 0x7fffffff};
         const int ns = wave_topk<1>(u, ix, 1, K, su, si, emit_row);
-        if (lane >= ns && lane < K) put_row(out + lane, -INFINITY, 0x7fffffff);
+        if (lane >= ns && lane < K) emit_row(lane, -INFINITY, 0x7fffffff);
       }
     }
   }
 
+  if (K == 1) {  // the sentence's result, as the merge would write it
+    __syncthreads();
+    if (t == 0) {
+      const bool real = res_tok >= 0 && res_tok < V;
+      const uint32_t mu = real ? key_code(res_key) : 0u;
+      a.score_out[m] = mu != 0u ? key_from_code(mu) : -INFINITY;
+      a.tok_out[m] = mu != 0u ? res_tok : 0;
+      a.bp_out[m] = 0;
+      if (a.row_out) a.row_out[m] = m;
+    }
+    return;
+  }
   // ---- the last row of the sentence to finish merges the sentence ----
   __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): this thread's row stores have completed
   __syncthreads();
