@@ -230,7 +230,7 @@ class Ensemble:
     log-probabilities, mt_ensemble_logp combines them and mt_beam_topk selects.  Either way the
     first member's beam buffers hold the beam that all members read next."""
 
-    def __init__(self, members, weights, fused=True, joint=None):
+    def __init__(self, members, weights, fused=True, joint=None, concurrent=True):
         assert len(members) == len(weights) >= 1
         self.members, self.weights = list(members), [float(x) for x in weights]
         self.lead = self.members[0]
@@ -241,6 +241,14 @@ class Ensemble:
         self.joint = ok if joint is None else bool(joint)
         if self.joint and not ok:
             raise ValueError("the joint vocabulary pass does not support these members")
+        # Members whose steps are independent (the joint pass, or materialised log-probabilities)
+        # run on streams of their own, so that one member's latency-bound kernels overlap the
+        # other's; the per-member fused pass adds into one buffer in member order and stays on
+        # the caller's stream.  The streams keep the default priority.
+        self.concurrent = concurrent and len(self.members) > 1 and (self.joint or not self.fused)
+        dev = self.lead.device
+        self.streams = [torch.cuda.Stream(device=dev) for _ in self.members] if self.concurrent else None
+        self._ev = [torch.cuda.Event() for _ in range(len(self.members) + 1)] if self.concurrent else None
 
     def set_batch(self, ctx: np.ndarray, mask: np.ndarray, K: int):
         for d in self.members:
@@ -275,19 +283,32 @@ class Ensemble:
 
     def advance(self, stream=None, row_const=None):
         lead = self.lead
+        base = stream if stream is not None else torch.cuda.current_stream(lead.device)
+        if self.concurrent:  # the members' streams start after what the caller queued
+            self._ev[-1].record(base)
         for i, (d, lp) in enumerate(zip(self.members, self.logp)):
             if d.first:
                 state_in, nrows = d.s0, d.B
             else:
                 state_in, nrows = d.state[d.cur], d.M
             out = d.state[1 - d.cur] if not d.first else d.state[d.cur]
+            st = base
+            if self.concurrent:
+                st = self.streams[i]
+                st.wait_event(self._ev[-1])
             with d._reuse():
                 if self.fused:
                     mt.mt_ensemble_step(d.model, i, len(self.members), self.weights[i], d.B, d.K, d.S, lead.tok,
                                         lead.row, nrows, state_in, d.ctx, d.pctx, d.mask, out, self.comb, d.ws,
-                                        stream=stream)
+                                        stream=st)
                 else:
-                    d.step(lead.tok, lead.row, state_in, nrows, out, logp=lp, stream=stream)
+                    d.step(lead.tok, lead.row, state_in, nrows, out, logp=lp, stream=st)
+            if self.concurrent:
+                self._ev[i].record(st)
+        if self.concurrent:  # the selection waits for every member
+            for i in range(len(self.members)):
+                base.wait_event(self._ev[i])
+        stream = base
         if self.fused:
             mt.mt_ensemble_topk([d.model for d in self.members], self.weights, [d.ws for d in self.members], lead.B,
                                 lead.K, lead.score, self.comb, lead.score, lead.tok, lead.bp, lead.row,

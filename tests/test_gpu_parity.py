@@ -468,6 +468,40 @@ def test_state_reuse_is_bit_identical(name):
     log(f"[state reuse] {name}: 8 steps bit-identical with and without the bf16 state copy")
 
 
+@pytest.mark.parametrize("name,fused", [("nematus_bf16_ln", True), ("tiny_f32", False)])
+def test_ensemble_member_streams_identical(name, fused):
+    """Members stepping on streams of their own (the joint pass, or materialised
+    log-probabilities) give bit-identical beams and states to the same members stepping one
+    after another on one stream, over a restart and several steps."""
+    from paper_1804_00344_amd.runner import Ensemble
+    base = synth.PRESETS[name]
+    ctx, mask, _ = synth.make_source(base)
+    tok0, _, score0 = synth.start_beam(base)
+    decs = []
+    for i in range(2):
+        p = dataclasses.replace(base, name=f"{name}_m{i}", index=base.index + 100 * i)
+        decs.append(Decoder.from_preset(p, synth.make_weights(p, peaked_bias=True)))
+    runs = []
+    for conc in (True, False):
+        ens = Ensemble(decs, (0.6, 0.4), fused=fused, concurrent=conc)
+        assert ens.concurrent == conc
+        ens.set_batch(ctx, mask, base.K)
+        rec = []
+        for _ in range(2):
+            ens.precompute()
+            ens.start(tok0, score0)
+            for _ in range(3):
+                states = ens.advance()
+                rec.append([x.clone() for x in states] + [decs[0].score.clone(), decs[0].tok.clone(),
+                                                         decs[0].bp.clone()])
+        torch.cuda.synchronize()
+        runs.append(rec)
+    for a, b in zip(*runs):
+        for x, y in zip(a, b):
+            assert torch.equal(x, y)
+    log(f"[ensemble streams] {name} fused={fused}: 6 steps bit-identical on member streams and on one stream")
+
+
 def exact_topk_check(B, K, keys, sc, tk, bp):
     """sc/tk/bp [B*K] are, per sentence, the K best of keys [B*K, V] (flattened k*V + v),
     larger key first, equal keys by smaller flat index; bit-exact."""
@@ -558,6 +592,40 @@ def test_state_reuse_is_bit_identical(name):
         for x, y in zip(a, b):
             assert torch.equal(x, y)
     log(f"[state reuse] {name}: 8 steps bit-identical with and without the bf16 state copy")
+
+
+@pytest.mark.parametrize("name,fused", [("nematus_bf16_ln", True), ("tiny_f32", False)])
+def test_ensemble_member_streams_identical(name, fused):
+    """Members stepping on streams of their own (the joint pass, or materialised
+    log-probabilities) give bit-identical beams and states to the same members stepping one
+    after another on one stream, over a restart and several steps."""
+    from paper_1804_00344_amd.runner import Ensemble
+    base = synth.PRESETS[name]
+    ctx, mask, _ = synth.make_source(base)
+    tok0, _, score0 = synth.start_beam(base)
+    decs = []
+    for i in range(2):
+        p = dataclasses.replace(base, name=f"{name}_m{i}", index=base.index + 100 * i)
+        decs.append(Decoder.from_preset(p, synth.make_weights(p, peaked_bias=True)))
+    runs = []
+    for conc in (True, False):
+        ens = Ensemble(decs, (0.6, 0.4), fused=fused, concurrent=conc)
+        assert ens.concurrent == conc
+        ens.set_batch(ctx, mask, base.K)
+        rec = []
+        for _ in range(2):
+            ens.precompute()
+            ens.start(tok0, score0)
+            for _ in range(3):
+                states = ens.advance()
+                rec.append([x.clone() for x in states] + [decs[0].score.clone(), decs[0].tok.clone(),
+                                                         decs[0].bp.clone()])
+        torch.cuda.synchronize()
+        runs.append(rec)
+    for a, b in zip(*runs):
+        for x, y in zip(a, b):
+            assert torch.equal(x, y)
+    log(f"[ensemble streams] {name} fused={fused}: 6 steps bit-identical on member streams and on one stream")
 
 
 def exact_topk_check(B, K, keys, sc, tk, bp):
