@@ -395,6 +395,11 @@ typedef enum {
 } mt_kernel_id;
 
 mt_status mt_profile_enable(mt_model *model, uint32_t kernel_mask);
+/* Times one launch in `every` (>= 1, default 1) of each selected class, the first after a
+ * reset included: an event record makes the stream wait for the work before it, which adds
+ * a few microseconds around a timed launch, so sampling keeps a timed run's step time
+ * representative while the average over the timed launches stays the class's. */
+mt_status mt_profile_sample(mt_model *model, uint32_t every);
 mt_status mt_profile_reset(mt_model *model);
 mt_status mt_profile_query(mt_model *model, int kernel, double *total_ms, int64_t *launches);
 

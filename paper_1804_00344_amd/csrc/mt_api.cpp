@@ -55,6 +55,7 @@ struct ProfSlot {
   std::vector<std::pair<hipEvent_t, hipEvent_t>> pending;
   double ms = 0.0;
   int64_t n = 0;
+  uint64_t seen = 0;  // launches of the class since the last reset (timed or not)
 };
 
 }  // namespace
@@ -109,6 +110,7 @@ struct mt_model {
   int shadow_rows = 0;
   // profiling
   uint32_t prof_mask = 0;
+  uint32_t prof_every = 1;  // time one launch in this many of each selected class
   ProfSlot prof[MT_KERNEL_COUNT];
   std::vector<hipEvent_t> ev_pool;
 };
@@ -352,7 +354,7 @@ struct Timed {  // records events around one launch when profiling is on
   hipStream_t st;
   hipEvent_t a = nullptr, b = nullptr;
   Timed(mt_model *m_, int k_, hipStream_t st_, bool on = true) : m(m_), k(k_), st(st_) {
-    if (on && (m->prof_mask & (1u << k))) {
+    if (on && (m->prof_mask & (1u << k)) && m->prof[k].seen++ % m->prof_every == 0) {
       a = get_event(m);
       b = get_event(m);
       if (a && b) hipEventRecord(a, st);
@@ -1456,6 +1458,14 @@ mt_status mt_profile_enable(mt_model *model, uint32_t kernel_mask) {
   return MT_OK;
 }
 
+mt_status mt_profile_sample(mt_model *model, uint32_t every) {
+  g_err[0] = 0;
+  if (!valid_model(model)) return fail(MT_ERR_ARG, "invalid model handle");
+  if (every < 1) return fail(MT_ERR_ARG, "every=%u must be >= 1", every);
+  model->prof_every = every;
+  return MT_OK;
+}
+
 mt_status mt_profile_reset(mt_model *model) {
   g_err[0] = 0;
   if (!valid_model(model)) return fail(MT_ERR_ARG, "invalid model handle");
@@ -1463,6 +1473,7 @@ mt_status mt_profile_reset(mt_model *model) {
     fold_profile(model, k);
     model->prof[k].ms = 0.0;
     model->prof[k].n = 0;
+    model->prof[k].seen = 0;
   }
   return MT_OK;
 }

@@ -97,6 +97,8 @@ def lib() -> C.CDLL:
         L.mt_beam_finish.argtypes = [_vp, C.c_int, C.c_int, C.c_int, C.c_int32, C.c_float, C.c_int] + [_vp] * 14
         L.mt_profile_enable.argtypes = [_vp, C.c_uint32]
         L.mt_profile_reset.argtypes = [_vp]
+        L.mt_profile_sample.argtypes = [_vp, C.c_uint32]
+        L.mt_profile_sample.restype = C.c_int
         L.mt_profile_query.argtypes = [_vp, C.c_int, C.POINTER(C.c_double), C.POINTER(C.c_int64)]
         L.mt_ensemble_step.argtypes = [_vp, C.c_int, C.c_int, C.c_float, C.c_int, C.c_int, C.c_int, _vp, _vp, C.c_int, _vp,
                                        _vp, _vp, _vp, _vp, _vp, _vp, C.c_size_t, _vp]
@@ -335,6 +337,11 @@ def mt_profile_enable(model: Model, kernels=("VOCAB_GEMM",)):
     for k in kernels:
         mask |= 1 << (KERNEL_ID[k] if isinstance(k, str) else int(k))
     _check(lib().mt_profile_enable(model.handle, mask))
+
+
+def mt_profile_sample(model: Model, every: int):
+    """Times one launch in `every` of each selected class."""
+    _check(lib().mt_profile_sample(model.handle, int(every)))
 
 
 def mt_profile_reset(model: Model):
