@@ -251,12 +251,16 @@ class Ensemble:
         self._ev = [torch.cuda.Event() for _ in range(len(self.members) + 1)] if self.concurrent else None
 
     def set_batch(self, ctx: np.ndarray, mask: np.ndarray, K: int):
+        if self.concurrent:  # the members' old buffers may still be in use on their streams
+            torch.cuda.synchronize(self.lead.device)
         for d in self.members:
             d.set_batch(ctx, mask, K)
         self._alloc_logp()
 
     def _alloc_logp(self):
         lead = self.lead
+        if self.concurrent:  # no member stream may still use buffers that are about to be replaced
+            torch.cuda.synchronize(lead.device)
         # the fused path needs only the combined buffer, the joint pass not even that
         self.logp = [None if self.fused else torch.empty((lead.M, lead.V), dtype=torch.float32, device=lead.device)
                      for _ in self.members]
@@ -265,6 +269,8 @@ class Ensemble:
     def set_source(self, src_tok: np.ndarray, mask: np.ndarray, K: int, stream=None):
         """Batch from source tokens: every member encodes them with its own encoder (mt_encode)
         into its own context, as each member of an ensemble has its own encoder."""
+        if self.concurrent:
+            torch.cuda.synchronize(self.lead.device)
         for d in self.members:
             d.set_source(src_tok, mask, K, stream=stream)
         self._alloc_logp()
