@@ -43,15 +43,35 @@ __device__ __forceinline__ float tanh_fast(float x) {
 }
 __device__ __forceinline__ float sigmoid_fast(float x) { return rcp_fast(1.0f + exp_fast(-x)); }
 
+// Wave-wide sum and maximum, the result in every lane; every lane of the wave must be active.
+// Within each 16-lane row, DPP moves (quad exchanges, then row rotations by 4 and 8) leave
+// lanes 0, 16, 32 and 48 with their row totals (a fixed order of operations); the four are
+// read into scalars and combined as (r0 + r1) + (r2 + r3).  Lane exchanges through LDS
+// permutes, as a shuffle butterfly compiles to, cost a round trip of the LDS unit per step.
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float lane_f(float v, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+constexpr int kDppQuadSwap1 = 0xB1;  // quad_perm [1,0,3,2]
+constexpr int kDppQuadSwap2 = 0x4E;  // quad_perm [2,3,0,1]
+constexpr int kDppRowRor4 = 0x124;
+constexpr int kDppRowRor8 = 0x128;
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
+  v += dpp_mov<kDppQuadSwap1>(v);
+  v += dpp_mov<kDppQuadSwap2>(v);
+  v += dpp_mov<kDppRowRor4>(v);
+  v += dpp_mov<kDppRowRor8>(v);
+  return (lane_f(v, 0) + lane_f(v, 16)) + (lane_f(v, 32) + lane_f(v, 48));
 }
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
+  v = fmaxf(v, dpp_mov<kDppQuadSwap1>(v));
+  v = fmaxf(v, dpp_mov<kDppQuadSwap2>(v));
+  v = fmaxf(v, dpp_mov<kDppRowRor4>(v));
+  v = fmaxf(v, dpp_mov<kDppRowRor8>(v));
+  return fmaxf(fmaxf(lane_f(v, 0), lane_f(v, 16)), fmaxf(lane_f(v, 32), lane_f(v, 48)));
 }
 
 // Host-side fp32 -> bf16 bits, round to nearest with ties to even (the weight packing of every

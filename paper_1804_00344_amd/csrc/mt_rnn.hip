@@ -5,31 +5,99 @@
 //
 // GRU cell and readout: one 256-thread workgroup per row; thread t holds 16-byte granules
 // 4t + 1024p of each H-block in registers, and every operand (products, previous state,
-// layer-norm gains and shifts) is loaded up front so the row costs one memory round trip.
-// Layer-norm statistics are taken in one pass over shifted values d = x - x_0 (x_0 = the
-// block's first element): mean = x_0 + sum(d)/n and var = sum(d^2)/n - (sum(d)/n)^2, which
-// keeps the cancellation of the one-pass formula small; all blocks' sums are reduced
-// together (wave shuffles, then 4 partials through LDS).
+// layer-norm gains and shifts) is loaded up front so the row costs one memory round trip
+// (the row indices of gathered operands are read together before it).  Layer-norm
+// statistics need one workgroup barrier: each wave takes the mean of its own values and the
+// sum of their squared deviations from it (two DPP reductions over registers, no
+// cancellation), and the four waves' (count, mean, squared deviations) are combined through
+// LDS with the pairwise update of Chan, Golub and LeVeque:
+//   mean = sum_w n_w m_w / n,   M2 = sum_w (M2_w + n_w (m_w - mean)^2).
 #include "mt_internal.h"
 
 namespace mt {
 
 constexpr int kT = 256;
 
-// sum of NV values over the 256-thread block; every thread receives the totals
-template <int NV>
-__device__ __forceinline__ void block_sum(float (&v)[NV], float (*red)[NV]) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+// Layer-norm statistics of NB blocks of n values each, thread t holding elements 4t + 1024p
+// (p < G) of every block as x(g, p, e): on return mean[g] and inv[g] = 1/sqrt(var + eps)
+// (population variance), in every thread.  One barrier; `red` is used once.
+template <int NB, int G, typename X>
+__device__ __forceinline__ void ln_stats(X x, int n, float eps, float (*red)[2][NB], float (&mean)[NB],
+                                         float (&inv)[NB]) {
+  const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
+  auto wave_count = [&](int w) {  // values held by wave w
+    int c = 0;
 #pragma unroll
-  for (int i = 0; i < NV; ++i) v[i] = wave_sum(v[i]);
+    for (int p = 0; p < G; ++p) {
+      const int r = n - 4 * kT * p - 256 * w;
+      c += r <= 0 ? 0 : r < 256 ? r : 256;
+    }
+    return c;
+  };
+  const int nw = wave_count(wv);
+  const float rn = nw ? 1.0f / (float)nw : 0.f;
+  float wm[NB], wq[NB];
+#pragma unroll
+  for (int g = 0; g < NB; ++g) {
+    float s1 = 0.f;
+#pragma unroll
+    for (int p = 0; p < G; ++p) {
+      const bool ok = 4 * t + 4 * kT * p < n;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) s1 += ok ? x(g, p, e) : 0.f;
+    }
+    wm[g] = wave_sum(s1) * rn;
+  }
+#pragma unroll
+  for (int g = 0; g < NB; ++g) {
+    float s2 = 0.f;
+#pragma unroll
+    for (int p = 0; p < G; ++p) {
+      const bool ok = 4 * t + 4 * kT * p < n;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float d = x(g, p, e) - wm[g];
+        s2 += ok ? d * d : 0.f;
+      }
+    }
+    wq[g] = wave_sum(s2);
+  }
   if (lane == 0) {
 #pragma unroll
-    for (int i = 0; i < NV; ++i) red[wave][i] = v[i];
+    for (int g = 0; g < NB; ++g) {
+      red[wv][0][g] = wm[g];
+      red[wv][1][g] = wq[g];
+    }
   }
   __syncthreads();
+  float cn[4];
 #pragma unroll
-  for (int i = 0; i < NV; ++i) v[i] = red[0][i] + red[1][i] + red[2][i] + red[3][i];
-  __syncthreads();
+  for (int w = 0; w < 4; ++w) cn[w] = (float)wave_count(w);
+  const float invn = 1.0f / (float)n;
+#pragma unroll
+  for (int g = 0; g < NB; ++g) {
+    float mu = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) mu += cn[w] * red[w][0][g];
+    mu *= invn;
+    float m2 = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float d = red[w][0][g] - mu;
+      m2 += red[w][1][g] + cn[w] * d * d;
+    }
+    mean[g] = mu;
+    inv[g] = 1.0f / sqrtf(m2 * invn + eps);
+  }
+}
+
+// Row index idx[m] clamped to [0, rows); an out-of-range index sets error bit `bit`
+__device__ __forceinline__ int clamp_idx(int r, int rows, int32_t *err, int bit) {
+  if (r < 0 || r >= rows) {
+    if (threadIdx.x == 0 && err) atomicOr(err, 1 << bit);
+    r = r < 0 ? 0 : rows - 1;
+  }
+  return r;
 }
 
 __device__ __forceinline__ float4 ld4(const float *p) { return *(const float4 *)p; }
@@ -71,7 +139,8 @@ __global__ __launch_bounds__(kT) void gru_cell_kernel(int M, int H, const float 
                                                       CellPair pr) {
   constexpr bool LN = LNM != 0;
   constexpr int G0 = LNM == 2 ? 3 : 0;  // first normalised block
-  __shared__ float red[4][12];
+  constexpr int NB = 6 - G0;            // normalised blocks
+  __shared__ float red[4][2][NB];
   const int m = blockIdx.x;
   const int t = threadIdx.x;
   if (blockIdx.y) {  // the launch's second cell
@@ -84,23 +153,18 @@ __global__ __launch_bounds__(kT) void gru_cell_kernel(int M, int H, const float 
     if (ga) ga += pr.dln, ba += pr.dln;
     if (gu) gu += pr.dln, bu += pr.dln;
   }
-  const int ar = aidx ? clamp_row(aidx, m, arows, err, 0) : m;
-  const int hr = hidx ? clamp_row(hidx, m, hrows, err, 1) : m;
-  const float *arow = a + (size_t)ar * lda;
-  const float *urow = u + (size_t)m * ldu;
-  const float *hp = hsrc ? hsrc + (size_t)hr * ldh : nullptr;  // no previous state: zero
-  // keep (if given): a row whose keep value is 0 carries its previous state over
-  const bool upd = keep == nullptr || keep[(size_t)m * keep_ld] != 0.f;
   float x[6][G][4], h[G][4];
   float lg[6][G][4], lb[6][G][4];
+  // the operands that do not depend on a row index are requested first, so that the index
+  // loads' round trip runs under them
+  const float *urow = u + (size_t)m * ldu;
 #pragma unroll
   for (int p = 0; p < G; ++p) {
     const int j = 4 * t + 4 * kT * p;
     const int jc = j < H ? j : 0;  // lanes past H read element 0 and take no part
 #pragma unroll
     for (int g = 0; g < 3; ++g) {
-      const float4 va = ld4(arow + g * H + jc), vu = ld4(urow + g * H + jc);
-      x[g][p][0] = va.x; x[g][p][1] = va.y; x[g][p][2] = va.z; x[g][p][3] = va.w;
+      const float4 vu = ld4(urow + g * H + jc);
       x[3 + g][p][0] = vu.x; x[3 + g][p][1] = vu.y; x[3 + g][p][2] = vu.z; x[3 + g][p][3] = vu.w;
       if (LNM == 1) {
         const float4 g0 = ld4(ga + g * H + jc), b0 = ld4(ba + g * H + jc);
@@ -113,46 +177,39 @@ __global__ __launch_bounds__(kT) void gru_cell_kernel(int M, int H, const float 
         lb[3 + g][p][0] = b1.x; lb[3 + g][p][1] = b1.y; lb[3 + g][p][2] = b1.z; lb[3 + g][p][3] = b1.w;
       }
     }
+  }
+  // both row indices and the keep flag are requested before any of them is used
+  int ar = m, hr = m;
+  if (aidx) ar = aidx[m];
+  if (hidx) hr = hidx[m];
+  // keep (if given): a row whose keep value is 0 carries its previous state over
+  const bool upd = keep == nullptr || keep[(size_t)m * keep_ld] != 0.f;
+  if (aidx) ar = clamp_idx(ar, arows, err, 0);
+  if (hidx) hr = clamp_idx(hr, hrows, err, 1);
+  const float *arow = a + (size_t)ar * lda;
+  const float *hp = hsrc ? hsrc + (size_t)hr * ldh : nullptr;  // no previous state: zero
+#pragma unroll
+  for (int p = 0; p < G; ++p) {
+    const int j = 4 * t + 4 * kT * p;
+    const int jc = j < H ? j : 0;
+#pragma unroll
+    for (int g = 0; g < 3; ++g) {
+      const float4 va = ld4(arow + g * H + jc);
+      x[g][p][0] = va.x; x[g][p][1] = va.y; x[g][p][2] = va.z; x[g][p][3] = va.w;
+    }
     const float4 vh = hp ? ld4(hp + jc) : make_float4(0.f, 0.f, 0.f, 0.f);
     h[p][0] = vh.x; h[p][1] = vh.y; h[p][2] = vh.z; h[p][3] = vh.w;
   }
   if (LN) {
-    float sh[6];
+    float mean[NB], inv[NB];
+    ln_stats<NB, G>([&](int g, int p, int e) { return x[G0 + g][p][e]; }, H, eps, red, mean, inv);
 #pragma unroll
-    for (int g = 0; g < 3; ++g) {
-      sh[g] = arow[g * H];
-      sh[3 + g] = urow[g * H];
-    }
-    float st[12];
-#pragma unroll
-    for (int g = 0; g < 6; ++g) {
-      float s1 = 0.f, s2 = 0.f;
-#pragma unroll
-      for (int p = 0; p < G; ++p) {
-        if (4 * t + 4 * kT * p >= H) continue;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float d = x[g][p][e] - sh[g];
-          s1 += d;
-          s2 += d * d;
-        }
-      }
-      st[2 * g] = s1;
-      st[2 * g + 1] = s2;
-    }
-    block_sum<12>(st, red);
-    const float invn = 1.0f / (float)H;
-#pragma unroll
-    for (int g = G0; g < 6; ++g) {
-      const float md = st[2 * g] * invn;
-      const float var = fmaxf(st[2 * g + 1] * invn - md * md, 0.f);
-      const float mean = sh[g] + md;
-      const float inv = 1.0f / sqrtf(var + eps);
+    for (int g = 0; g < NB; ++g)
 #pragma unroll
       for (int p = 0; p < G; ++p)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) x[g][p][e] = lg[g][p][e] * (x[g][p][e] - mean) * inv + lb[g][p][e];
-    }
+        for (int e = 0; e < 4; ++e)
+          x[G0 + g][p][e] = lg[G0 + g][p][e] * (x[G0 + g][p][e] - mean[g]) * inv[g] + lb[G0 + g][p][e];
   }
   float *o = out + (size_t)m * ldo;
 #pragma unroll
@@ -189,7 +246,7 @@ __global__ __launch_bounds__(kT) void readout_kernel(int M, int E, const float *
                                                      const float *__restrict__ g,
                                                      const float *__restrict__ be, float eps,
                                                      TO *__restrict__ tout, float *__restrict__ tap) {
-  __shared__ float red[4][2];
+  __shared__ float red[4][2][1];
   const int m = blockIdx.x, t = threadIdx.x;
   const int r2 = idx2 ? clamp_row(idx2, m, rows2, nullptr, 0) : m;
   const float *q1 = p1 + (size_t)m * ld1, *q2 = p2 + (size_t)r2 * ld2, *q3 = p3 + (size_t)m * ld3;
@@ -210,27 +267,12 @@ __global__ __launch_bounds__(kT) void readout_kernel(int M, int E, const float *
     }
   }
   if (LN) {
-    const float sh = q1[0] + q2[0] + q3[0] + bt[0];
-    float st[2] = {0.f, 0.f};
-#pragma unroll
-    for (int p = 0; p < G; ++p) {
-      if (4 * t + 4 * kT * p >= E) continue;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float d = x[p][e] - sh;
-        st[0] += d;
-        st[1] += d * d;
-      }
-    }
-    block_sum<2>(st, red);
-    const float md = st[0] / (float)E;
-    const float var = fmaxf(st[1] / (float)E - md * md, 0.f);
-    const float mean = sh + md;
-    const float inv = 1.0f / sqrtf(var + eps);
+    float mean[1], inv[1];
+    ln_stats<1, G>([&](int, int p, int e) { return x[p][e]; }, E, eps, red, mean, inv);
 #pragma unroll
     for (int p = 0; p < G; ++p)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) x[p][e] = lg[p][e] * (x[p][e] - mean) * inv + lb[p][e];
+      for (int e = 0; e < 4; ++e) x[p][e] = lg[p][e] * (x[p][e] - mean[0]) * inv[0] + lb[p][e];
   }
 #pragma unroll
   for (int p = 0; p < G; ++p) {
