@@ -80,17 +80,18 @@ hipError_t launch_ensemble(int n, const float *const *in, const float *w, long l
   return hipGetLastError();
 }
 
-// Row constant of a fused ensemble (see EnsembleConst): one 256-thread workgroup per row; each
-// member's log-sum-exp is merged by the same routine, in the same order, as the beam selection
-// merges a row's partials.
-__global__ __launch_bounds__(256) void ensemble_const_kernel(EnsembleConst a) {
-  const int m = blockIdx.x;
+// Row constant of a fused ensemble (see EnsembleConst): one wave per row (four rows per
+// workgroup); each member's log-sum-exp is merged by the same routine, in the same order, as the
+// beam selection merges a row's partials (wave_row_lse).
+__global__ __launch_bounds__(256) void ensemble_const_kernel(EnsembleConst a, int M) {
+  const int m = blockIdx.x * 4 + (int)(threadIdx.x >> 6);
+  if (m >= M) return;  // wave-uniform
   float c = 0.f;
   for (int i = 0; i < a.n; ++i) {
-    const float L = block_row_lse(a.part[i] + (size_t)m * a.ntiles[i], a.ntiles[i]);
+    const float L = wave_row_lse(a.part[i] + (size_t)m * a.ntiles[i], a.ntiles[i]);
     c = __builtin_fmaf(a.w[i], L, c);
   }
-  if (threadIdx.x == 0) {
+  if ((threadIdx.x & 63) == 0) {
     a.prev_adj[m] = a.prev[m] - c;
     if (a.row_const) a.row_const[m] = c;
   }
@@ -98,7 +99,7 @@ __global__ __launch_bounds__(256) void ensemble_const_kernel(EnsembleConst a) {
 
 hipError_t launch_ensemble_const(const EnsembleConst &a, int M, hipStream_t st) {
   if (M == 0) return hipSuccess;
-  hipLaunchKernelGGL(ensemble_const_kernel, dim3(M), dim3(256), 0, st, a);
+  hipLaunchKernelGGL(ensemble_const_kernel, dim3((M + 3) / 4), dim3(256), 0, st, a, M);
   return hipGetLastError();
 }
 

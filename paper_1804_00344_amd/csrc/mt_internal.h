@@ -66,6 +66,18 @@ __device__ __forceinline__ float wave_sum(float v) {
   v += dpp_mov<kDppRowRor8>(v);
   return (lane_f(v, 0) + lane_f(v, 16)) + (lane_f(v, 32) + lane_f(v, 48));
 }
+// Inclusive prefix sum over the 64 lanes of a wave (every lane active): within each 16-lane
+// row by DPP row shifts of 1, 2, 4 and 8 (lanes shifted in from outside the row add 0), then
+// across rows by the row broadcasts of lane 15 (to rows 1 and 3) and lane 31 (to rows 2 and 3).
+__device__ __forceinline__ int wave_incl_scan(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, false);  // row_shr:1
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, false);  // row_shr:2
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, false);  // row_shr:4
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, false);  // row_shr:8
+  v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xA, 0xF, false);  // row_bcast:15 -> rows 1, 3
+  v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xC, 0xF, false);  // row_bcast:31 -> rows 2, 3
+  return v;
+}
 __device__ __forceinline__ float wave_max(float v) {
   v = fmaxf(v, dpp_mov<kDppQuadSwap1>(v));
   v = fmaxf(v, dpp_mov<kDppQuadSwap2>(v));
@@ -174,6 +186,28 @@ __device__ __forceinline__ void block_extract(List<KMAX> &L, int n, Emit emit) {
   }
   __syncthreads();
   if (t < n) emit(t, rv[t], ri[t]);
+}
+
+// The same extraction by one wave: result r is kept by lane r, which calls emit(r, key, idx)
+// once the n results are known.  Indices must be distinct.
+template <int KMAX, typename Emit>
+__device__ __forceinline__ void wave_extract(List<KMAX> &L, int n, Emit emit) {
+  const int lane = threadIdx.x & 63;
+  float mv = -INFINITY;
+  int mi = 0x7fffffff;
+  for (int r = 0; r < n; ++r) {
+    float bv = L.v[0];
+    int bi = L.i[0];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float ov = __shfl_xor(bv, o, 64);
+      const int oi = __shfl_xor(bi, o, 64);
+      if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
+    }
+    if (L.i[0] == bi && L.v[0] == bv) L.pop();
+    if (lane == r) { mv = bv; mi = bi; }
+  }
+  if (lane < n) emit(lane, mv, mi);
 }
 
 // ---- exact selection by bisection over order-preserving key codes ----
@@ -297,70 +331,71 @@ __device__ __forceinline__ int wave_topk(const uint32_t (&u)[R], const int (&ix)
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
   const int ns = base < K ? base : K;
+  // lane j < ns holds selected entry j; each counts the entries that beat it, read from the
+  // other lanes' registers (one LDS read per lane, then lane reads)
+  uint32_t mu = 0u;
+  int mi = 0;
   if (lane < ns) {
-    const uint32_t mu = su[lane];
-    const int mi = si[lane];
-    int rank = 0;
-    for (int j = 0; j < ns; ++j) {
-      const uint32_t ou = su[j];
-      const int oi = si[j];
-      rank += (ou > mu || (ou == mu && oi < mi)) ? 1 : 0;
-    }
-    emit(rank, key_from_code(mu), mi);
+    mu = su[lane];
+    mi = si[lane];
   }
+  int rank = 0;
+  for (int j = 0; j < ns; ++j) {
+    const uint32_t ou = (uint32_t)__builtin_amdgcn_readlane((int)mu, j);
+    const int oi = __builtin_amdgcn_readlane(mi, j);
+    rank += (ou > mu || (ou == mu && oi < mi)) ? 1 : 0;
+  }
+  if (lane < ns) emit(rank, key_from_code(mu), mi);
   return ns;
 }
 
 // ---- row-level pieces shared by the log-sum-exp pass and the beam selection ----
 
 // Log-sum-exp of one row from its per-chunk partials (m_c, s_c), s_c = sum of exp(logit - m_c)
-// over chunk c: L = M + ln sum_c s_c exp(m_c - M), M = max_c m_c.  Called by a whole
-// 256-thread workgroup (every thread gets L) with a fixed order of operations, so every
-// caller obtains the same bits from the same partials.
-// The same reduction when each thread holds at most one partial (thread t holds partial t,
-// has = t < ntiles): the identical operations in the identical order, so the same bits.
-__device__ __forceinline__ float block_row_lse_one(float2 q, bool has) {
-  __shared__ float wmx1[4], wsm1[4];
-  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+// over chunk c: L = M + ln sum_c s_c exp(m_c - M), M = max_c m_c.  Computed by one wave with a
+// fixed order of operations: lane l folds partials l, l + 64, l + 128, ... in that order, then
+// the lanes are combined by wave_max and wave_sum.  Every caller obtains the same bits from the
+// same partials, whether it reads them through a pointer or holds them in registers (partial
+// lane + 64 j in pq[j]).  Every lane of the wave must be active.
+template <int NP>
+__device__ __forceinline__ float wave_row_lse_regs(const float2 (&pq)[NP], int ntiles) {
+  const int lane = threadIdx.x & 63;
   float mx = -INFINITY;
-  if (has) mx = fmaxf(mx, q.x);
+#pragma unroll
+  for (int j = 0; j < NP; ++j)
+    if (lane + 64 * j < ntiles) mx = fmaxf(mx, pq[j].x);
   mx = wave_max(mx);
-  if (lane == 0) wmx1[w] = mx;
-  __syncthreads();
-  mx = fmaxf(fmaxf(wmx1[0], wmx1[1]), fmaxf(wmx1[2], wmx1[3]));
   float s = 0.f;
-  if (has) s += q.y * exp_fast(q.x - mx);
+#pragma unroll
+  for (int j = 0; j < NP; ++j)
+    if (lane + 64 * j < ntiles) s += pq[j].y * exp_fast(pq[j].x - mx);
   s = wave_sum(s);
-  if (lane == 0) wsm1[w] = s;
-  __syncthreads();
-  s = wsm1[0] + wsm1[1] + wsm1[2] + wsm1[3];
-  __syncthreads();  // the scratch may be reused by the caller's next call
   return mx + __builtin_amdgcn_logf(s) * 0.6931471805599453f;
 }
-__device__ __forceinline__ float block_row_lse(const float2 *pr, int ntiles) {
-  if (ntiles <= 256) {
-    const bool has = (int)threadIdx.x < ntiles;
-    return block_row_lse_one(has ? pr[threadIdx.x] : make_float2(0.f, 0.f), has);
-  }
-  __shared__ float wmx[4], wsm[4];
-  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+__device__ __forceinline__ float wave_row_lse(const float2 *pr, int ntiles) {
+  const int lane = threadIdx.x & 63;
   float mx = -INFINITY;
-  for (int i = t; i < ntiles; i += 256) mx = fmaxf(mx, pr[i].x);
+  for (int i = lane; i < ntiles; i += 64) mx = fmaxf(mx, pr[i].x);
   mx = wave_max(mx);
-  if (lane == 0) wmx[w] = mx;
-  __syncthreads();
-  mx = fmaxf(fmaxf(wmx[0], wmx[1]), fmaxf(wmx[2], wmx[3]));
   float s = 0.f;
-  for (int i = t; i < ntiles; i += 256) {
+  for (int i = lane; i < ntiles; i += 64) {
     const float2 q = pr[i];
     s += q.y * exp_fast(q.x - mx);
   }
   s = wave_sum(s);
-  if (lane == 0) wsm[w] = s;
-  __syncthreads();
-  s = wsm[0] + wsm[1] + wsm[2] + wsm[3];
-  __syncthreads();  // the scratch may be reused by the caller's next call
   return mx + __builtin_amdgcn_logf(s) * 0.6931471805599453f;
+}
+// The same value in every thread of a workgroup (its first wave computes it)
+__device__ __forceinline__ float block_row_lse(const float2 *pr, int ntiles) {
+  __shared__ float sl;
+  if (threadIdx.x < 64) {
+    const float L = wave_row_lse(pr, ntiles);
+    if (threadIdx.x == 0) sl = L;
+  }
+  __syncthreads();
+  const float L = sl;
+  __syncthreads();  // sl may be rewritten by the caller's next call
+  return L;
 }
 
 // The output projection as the exact recomputation reads it: packed Wo^T in MFMA fragment
@@ -374,19 +409,18 @@ struct VocabView {
   int V, E, KS;
 };
 
-// Exact K best keys prev + (logit - L) of row m over the whole vocabulary, recomputed from the
-// weights by a 256-thread workgroup; emit(rank, key, token) for ranks 0..K-1.
-template <typename CT, int KMAX, typename Emit>
-__device__ __forceinline__ void row_recompute(const VocabView &vv, int m, int K, float L, float prev, Emit emit) {
+// Exact keys prev + (logit - L) of row m over the whole vocabulary, recomputed from the weights
+// into each lane's list: the waves w0, w0 + nw, ... of the caller take every nw-th 32-entry
+// vocabulary block (lane pairs (l, l+32) of a wave share one vocabulary entry).
+template <typename CT, int KMAX>
+__device__ __forceinline__ void row_recompute_fill(const VocabView &vv, int m, float L, float prev, int w0, int nw,
+                                                   List<KMAX> &lst) {
   constexpr int epv = 16 / (int)sizeof(CT);  // k-values per lane vector
   constexpr int KV = 2 * epv;
-  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int lane = threadIdx.x & 63;
   const CT *trow = (const CT *)vv.t + (size_t)m * vv.E;
   const int nvb = (vv.V + 31) / 32;
-  List<KMAX> lst;
-  lst.init();
-  // lane pairs (l, l+32) of a wave share one vocabulary entry
-  for (int vb = w; vb < nvb; vb += 4) {
+  for (int vb = w0; vb < nvb; vb += nw) {
     float acc = 0.f;
     for (int ks = 0; ks < vv.KS; ++ks) {
       const CT *wv = (const CT *)((const char *)vv.wp + (((size_t)vb * vv.KS + ks) * 64 + lane) * 16);
@@ -398,22 +432,27 @@ __device__ __forceinline__ void row_recompute(const VocabView &vv, int m, int K,
     const int v = vb * 32 + (lane & 31);
     if (lane < 32 && v < vv.V) lst.push(prev + ((acc + vv.bias[v]) - L), v);
   }
+}
+// The K best of them by a 256-thread workgroup; emit(rank, key, token) for ranks 0..K-1
+template <typename CT, int KMAX, typename Emit>
+__device__ __forceinline__ void row_recompute(const VocabView &vv, int m, int K, float L, float prev, Emit emit) {
+  List<KMAX> lst;
+  lst.init();
+  row_recompute_fill<CT, KMAX>(vv, m, L, prev, threadIdx.x >> 6, 4, lst);
   block_extract<KMAX>(lst, K, emit);
 }
 
-// Exact K best keys prev + sum_m w[m] * logit_m(v) of row m over the whole vocabulary (a joint
-// ensemble's row), recomputed from the n members' weights by a 256-thread workgroup.
-template <typename CT, int KMAX, typename Emit>
-__device__ __forceinline__ void row_recompute_ens(const VocabView *vvs, const float *w, int n, int m, int K,
-                                                  float prev, Emit emit) {
+// Exact keys prev + sum_m w[m] * logit_m(v) of row m over the whole vocabulary (a joint
+// ensemble's row), recomputed from the n members' weights, split over waves as above.
+template <typename CT, int KMAX>
+__device__ __forceinline__ void row_recompute_ens_fill(const VocabView *vvs, const float *w, int n, int m,
+                                                       float prev, int w0, int nw, List<KMAX> &lst) {
   constexpr int epv = 16 / (int)sizeof(CT);
   constexpr int KV = 2 * epv;
-  const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
+  const int lane = threadIdx.x & 63;
   const int V = vvs[0].V;
   const int nvb = (V + 31) / 32;
-  List<KMAX> lst;
-  lst.init();
-  for (int vb = wv; vb < nvb; vb += 4) {
+  for (int vb = w0; vb < nvb; vb += nw) {
     const int v = vb * 32 + (lane & 31);
     float c = 0.f;
     for (int mm = 0; mm < n; ++mm) {
@@ -431,6 +470,13 @@ __device__ __forceinline__ void row_recompute_ens(const VocabView *vvs, const fl
     }
     if (lane < 32 && v < V) lst.push(prev + c, v);
   }
+}
+template <typename CT, int KMAX, typename Emit>
+__device__ __forceinline__ void row_recompute_ens(const VocabView *vvs, const float *w, int n, int m, int K,
+                                                  float prev, Emit emit) {
+  List<KMAX> lst;
+  lst.init();
+  row_recompute_ens_fill<CT, KMAX>(vvs, w, n, m, prev, threadIdx.x >> 6, 4, lst);
   block_extract<KMAX>(lst, K, emit);
 }
 

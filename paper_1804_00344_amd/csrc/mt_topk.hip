@@ -42,28 +42,18 @@ __device__ __forceinline__ int2 get_row(const int2 *p) {
   return make_int2((int)(uint32_t)v, (int)(uint32_t)(v >> 32));
 }
 
-// Level 3 for one sentence, by the whole workgroup: the K best of the K x K row results
-// (row_cand [M][K] of (key bits, token)); candidate (k, j) has flat index k*V + token.  Every
-// candidate counts the candidates that beat it (larger key code, or equal code and smaller
-// index); entries without a token get distinct indices above every real one, so the counts
-// are a permutation of 0..K*K-1 and the K candidates with counts below K write themselves to
-// their rank.  Entries without a token that rank below K are dead slots (fewer than K real
-// candidates): they continue hypothesis 0 with score -inf.
-__device__ __forceinline__ void sentence_merge(const RowSelect &a, int b, uint32_t *su, int *si) {
+// Level 3 for one sentence: the K best of the K x K row results, held as a table of (key code,
+// flat index) with candidate (k, j) at k*K + j and flat index k*V + token.  Every candidate
+// counts the candidates that beat it (larger key code, or equal code and smaller index);
+// entries without a token get distinct indices above every real one, so the counts are a
+// permutation of 0..K*K-1 and the K candidates with counts below K write themselves to their
+// rank.  Entries without a token that rank below K are dead slots (fewer than K real
+// candidates): they continue hypothesis 0 with score -inf.  The table is padded to whole
+// groups of four with entries that beat nothing; threads 0..K*K-1 rank.
+__device__ __forceinline__ void sentence_rank(const RowSelect &a, int b, const uint32_t *su, const int *si) {
   const int t = threadIdx.x, K = a.K, V = a.V;
-  const int n = K * K;  // <= 256: K <= 16
+  const int n = K * K;
   const int n4 = (n + 3) / 4;
-  if (t < n) {
-    const int k = t / K;
-    const int2 e = get_row(a.row_cand + (size_t)(b * K + k) * K + (t - k * K));
-    const bool real = e.y >= 0 && e.y < V;
-    su[t] = real ? key_code(__int_as_float(e.x)) : 0u;
-    si[t] = real ? k * V + e.y : K * V + t;
-  } else if (t < 4 * n4) {  // padding to whole 16-byte groups: beats nothing
-    su[t] = 0u;
-    si[t] = 0x7fffffff;
-  }
-  __syncthreads();
   if (t >= n) return;
   const uint32_t mu = su[t];
   const int mi = si[t];
@@ -93,6 +83,27 @@ __device__ __forceinline__ void sentence_merge(const RowSelect &a, int b, uint32
     if (a.row_out) a.row_out[o] = b * K;
   }
 }
+// Entry t of the table from the row candidates (key bits, token) of row k = t / K
+__device__ __forceinline__ void table_entry(int t, int K, int V, float key, int tok, uint32_t *su, int *si) {
+  const bool real = tok >= 0 && tok < V;
+  su[t] = real ? key_code(key) : 0u;
+  si[t] = real ? (t / K) * V + tok : K * V + t;
+}
+// The table from the row results of row_cand [M][K] (key bits, token), by the whole workgroup
+__device__ __forceinline__ void sentence_merge(const RowSelect &a, int b, uint32_t *su, int *si) {
+  const int t = threadIdx.x, K = a.K, V = a.V;
+  const int n = K * K;  // <= 256: K <= 16
+  const int n4 = (n + 3) / 4;
+  if (t < n) {
+    const int2 e = get_row(a.row_cand + (size_t)b * K * K + t);
+    table_entry(t, K, V, __int_as_float(e.x), e.y, su, si);
+  } else if (t < 4 * n4) {  // padding to whole 16-byte groups: beats nothing
+    su[t] = 0u;
+    si[t] = 0x7fffffff;
+  }
+  __syncthreads();
+  sentence_rank(a, b, su, si);
+}
 
 // The K best keys prev + x[v] of one stored row x [V] (a fused ensemble's combined values),
 // read by a 256-thread workgroup; emit(rank, key, token) for ranks 0..K-1.
@@ -119,6 +130,7 @@ __global__ __launch_bounds__(kTT) void row_select_kernel(RowSelect a) {
   __shared__ int last;
   __shared__ float res_key;  // K = 1: the row's result is the sentence's
   __shared__ int res_tok;
+  __shared__ float row_lse;
   const int m = blockIdx.x, t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int K = a.K, V = a.V, nl = a.nl, cap = a.cap;
   const int b = m / K;
@@ -131,12 +143,17 @@ __global__ __launch_bounds__(kTT) void row_select_kernel(RowSelect a) {
   // thread's lists are all requested before any of them is needed (lists hold about one entry
   // each; entries past a list's count are loaded and ignored) ----
   const bool pre = nl <= 2 * kTT && (!has_lse || a.ntiles <= kTT);  // uniform
-  const bool has_p = has_lse && t < a.ntiles;
-  float2 pq = make_float2(0.f, 0.f);
+  float2 pq[4];  // wave 0: partials lane + 64 j
   int pc[2] = {0, 0};
   int2 pe[2][kSpec];
   if (pre) {
-    if (has_p) pq = a.part[(size_t)m * a.ntiles + t];
+    if (has_lse && w == 0) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int i = lane + 64 * j;
+        pq[j] = i < a.ntiles ? a.part[(size_t)m * a.ntiles + i] : make_float2(0.f, 0.f);
+      }
+    }
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       const int l = t + j * kTT;
@@ -148,9 +165,14 @@ __global__ __launch_bounds__(kTT) void row_select_kernel(RowSelect a) {
       }
     }
   }
-  const float L = !has_lse ? 0.f
-                  : pre    ? block_row_lse_one(pq, has_p)
-                           : block_row_lse(a.part + (size_t)m * a.ntiles, a.ntiles);
+  // the row's log-sum-exp by wave 0 (wave_row_lse: the same bits as every other merge of these
+  // partials), read by all after the next barrier
+  if (w == 0) {
+    const float Lw = !has_lse ? 0.f
+                     : pre    ? wave_row_lse_regs<4>(pq, a.ntiles)
+                              : wave_row_lse(a.part + (size_t)m * a.ntiles, a.ntiles);
+    if (lane == 0) row_lse = Lw;
+  }
   const float sc = fused ? a.prev_score[m] : 0.f;
   int2 *out = a.row_cand + (size_t)m * K;
   // A row result goes to the row-candidate buffer for the sentence merge; with K = 1 the row
@@ -184,14 +206,10 @@ __global__ __launch_bounds__(kTT) void row_select_kernel(RowSelect a) {
         mine += c < cap ? c : cap;
       }
     }
-    int incl = mine;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int y = __shfl_up(incl, o, 64);
-      if (lane >= o) incl += y;
-    }
+    const int incl = wave_incl_scan(mine);
     if (lane == 63) wtot[w] = incl;
     const bool any_over = __syncthreads_or(over);
+    const float L = row_lse;
     int off = incl - mine, N = 0;
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
@@ -319,6 +337,204 @@ __global__ __launch_bounds__(kTT) void row_select_kernel(RowSelect a) {
   if (!last) return;
   sentence_merge(a, b, su, si);
   if (t == 0) __hip_atomic_store(a.scnt + b, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Levels 2 and 3 for beams of K >= 2 rows whose candidate lists fit one round trip: one
+// workgroup per sentence, one wave per row, so no row result leaves the workgroup (the per-row
+// form hands its results to the sentence's last row through device-scope stores, an arrival
+// count and loads, three round trips past the L2).  Wave k takes row b*K + k: it requests the
+// row's log-sum-exp partials, list fill counts and first kSpec entries of its lists together,
+// merges the log-sum-exp (wave_row_lse), stages the row's candidates in its own LDS region
+// (ballot-free offsets from a wave prefix sum), selects the K best exactly (wave_topk) into the
+// sentence table, and after one barrier the table is ranked (sentence_rank).  A row whose lists
+// overflow, or whose candidates exceed its region, is recomputed exactly by its own wave.
+constexpr int kWaveCap = 1024;    // candidates one row's wave can stage
+constexpr int kSentLists = 8;     // lists per lane: nl <= 512
+constexpr int kSentParts = 4;     // partials per lane: ntiles <= 256
+
+template <int KMAX, typename CT>
+__global__ __launch_bounds__(64 * KMAX) void sentence_select_kernel(RowSelect a) {
+  __shared__ __attribute__((aligned(16))) uint32_t su[KMAX][kWaveCap];
+  __shared__ __attribute__((aligned(16))) int si[KMAX][kWaveCap];
+  __shared__ uint32_t qu[KMAX][KMAX];
+  __shared__ int qi[KMAX][KMAX];
+  __shared__ uint32_t tu[KMAX * KMAX];
+  __shared__ int ti[KMAX * KMAX];
+  const int b = blockIdx.x, lane = threadIdx.x & 63;
+  const int k = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int K = a.K, V = a.V, nl = a.nl, cap = a.cap;
+  const int m = b * K + k;
+  const bool has_lse = a.part != nullptr;
+  const bool fused = has_lse || a.comb != nullptr || a.nens > 0;  // lists from the vocabulary pass
+  const int *cr = a.cnt ? a.cnt + (size_t)m * nl : nullptr;
+  const int2 *e0 = a.cbuf + (size_t)m * cap * nl;  // entry q of list l at e0[l + q * nl]
+
+  // ---- one round trip: partials, list counts and the first kSpec entries of every list ----
+  float2 pq[kSentParts];
+#pragma unroll
+  for (int j = 0; j < kSentParts; ++j) {
+    const int i = lane + 64 * j;
+    pq[j] = has_lse && i < a.ntiles ? a.part[(size_t)m * a.ntiles + i] : make_float2(0.f, 0.f);
+  }
+  int pc[kSentLists];
+  int2 pe[kSentLists][kSpec];
+#pragma unroll
+  for (int j = 0; j < kSentLists; ++j) {
+    const int l = lane + 64 * j;
+    pc[j] = 0;
+    if (l < nl) {
+      pc[j] = cr ? cr[l] : cap;
+#pragma unroll
+      for (int q = 0; q < kSpec; ++q) pe[j][q] = q < cap ? e0[l + (size_t)q * nl] : make_int2(0, -1);
+    }
+  }
+  const float sc = fused ? a.prev_score[m] : 0.f;
+  const float L = has_lse ? wave_row_lse_regs<kSentParts>(pq, a.ntiles) : 0.f;
+
+  // row results go straight into the sentence table
+  uint32_t *tab_u = tu;
+  int *tab_i = ti;
+  auto emit_tab = [&](int rank, float key, int tok) { table_entry(k * K + rank, K, V, key, tok, tab_u, tab_i); };
+
+  if (fused && sc == -INFINITY) {  // every key of the row is -inf: the K smallest tokens win
+    if (lane < K) emit_tab(lane, -INFINITY, lane);
+  } else {
+    int mine = 0;
+    bool over = false;
+#pragma unroll
+    for (int j = 0; j < kSentLists; ++j)
+      if (lane + 64 * j < nl) {
+        over |= pc[j] > cap;
+        mine += pc[j] < cap ? pc[j] : cap;
+      }
+    const int incl = wave_incl_scan(mine);
+    const int N = __builtin_amdgcn_readlane(incl, 63);
+    const bool any_over = __ballot(over) != 0ull;
+    if (any_over || N > kWaveCap || (cr && N < K)) {
+      // the candidates do not fit (or fall short of K): exact recomputation of the row
+      if (fused) {
+        if (lane == 0 && a.nrecompute) atomicAdd(a.nrecompute, 1ull);
+        List<KMAX> lst;
+        lst.init();
+        if (a.comb) {
+          const float *x = a.comb + (size_t)m * V;
+          for (int v = lane; v < V; v += 64) lst.push(sc + x[v], v);
+        } else if (a.nens > 0) {
+          row_recompute_ens_fill<CT, KMAX>(a.evv, a.ew, a.nens, m, sc, 0, 1, lst);
+        } else {
+          row_recompute_fill<CT, KMAX>(a.vv, m, L, sc, 0, 1, lst);
+        }
+        wave_extract<KMAX>(lst, K, emit_tab);
+      } else if (lane < K) {  // (materialised lists always fit: the launch checks nl * cap)
+        emit_tab(lane, -INFINITY, 0x7fffffff);
+      }
+    } else {
+      // ---- stage the row's candidates as (key code, token) in the wave's region ----
+      uint32_t *wu = su[k];
+      int *wi = si[k];
+      auto stage = [&](int pos, int2 v) {
+        const int tok = v.y;
+        uint32_t code = 0u;
+        if (tok >= 0 && tok < V) {
+          float key = __int_as_float(v.x);
+          if (fused) key = sc + (key - L);
+          code = key_code(key);
+        }
+        wu[pos] = code;
+        wi[pos] = tok;
+      };
+      int off = incl - mine;
+      int lo[kSentLists], lc[kSentLists];  // each list's first position and entry count
+      bool longl = false;
+#pragma unroll
+      for (int j = 0; j < kSentLists; ++j) {
+        const int l = lane + 64 * j;
+        const int c = l < nl ? (pc[j] < cap ? pc[j] : cap) : 0;
+        lo[j] = off;
+        lc[j] = c;
+#pragma unroll
+        for (int q = 0; q < kSpec; ++q)
+          if (q < c) stage(off + q, pe[j][q]);
+        longl |= c > kSpec;
+        off += c;
+      }
+      if (__ballot(longl) != 0ull) {
+        // entries past the first kSpec: the next two of every list requested together, the
+        // rest (rarer still) one by one
+        int2 ex[kSentLists][2];
+#pragma unroll
+        for (int j = 0; j < kSentLists; ++j)
+#pragma unroll
+          for (int q2 = 0; q2 < 2; ++q2) {
+            const int q = kSpec + q2;
+            ex[j][q2] = q < lc[j] ? e0[lane + 64 * j + (size_t)q * nl] : make_int2(0, -1);
+          }
+#pragma unroll
+        for (int j = 0; j < kSentLists; ++j) {
+#pragma unroll
+          for (int q2 = 0; q2 < 2; ++q2)
+            if (kSpec + q2 < lc[j]) stage(lo[j] + kSpec + q2, ex[j][q2]);
+          for (int q = kSpec + 2; q < lc[j]; ++q) stage(lo[j] + q, e0[lane + 64 * j + (size_t)q * nl]);
+        }
+      }
+      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+      // ---- exact K best of the row (register slots sized to its candidate count) ----
+      const int rs = (N + 63) / 64;
+      auto select = [&](auto slots) {
+        constexpr int R = decltype(slots)::value;
+        uint32_t u[R];
+        int ix[R];
+#pragma unroll
+        for (int s2 = 0; s2 < R; ++s2) {
+          const int j = s2 * 64 + lane;
+          const bool ok = s2 < rs && j < N;
+          u[s2] = ok ? wu[j] : 0u;
+          ix[s2] = ok ? wi[j] : 0x7fffffff;
+        }
+        return wave_topk<R>(u, ix, rs, K, qu[k], qi[k], emit_tab);
+      };
+      int ns;
+      if (rs <= 2)
+        ns = select(std::integral_constant<int, 2>());
+      else if (rs <= 4)
+        ns = select(std::integral_constant<int, 4>());
+      else if (rs <= 8)
+        ns = select(std::integral_constant<int, 8>());
+      else
+        ns = select(std::integral_constant<int, kWaveCap / 64>());
+      if (lane >= ns && lane < K) emit_tab(lane, -INFINITY, 0x7fffffff);
+    }
+  }
+  __syncthreads();
+  // ---- level 3 by wave 0: the K best of the K x K table (the order of sentence_rank: key code,
+  // then flat index; entries without a token are empty slots and rank below every real one) ----
+  if (k != 0) return;
+  const int n = K * K;  // <= 256
+  uint32_t u[4];
+  int ix[4];
+#pragma unroll
+  for (int s2 = 0; s2 < 4; ++s2) {
+    const int j = s2 * 64 + lane;
+    u[s2] = j < n ? tu[j] : 0u;
+    ix[s2] = j < n ? ti[j] : 0x7fffffff;
+  }
+  auto emit_out = [&](int rank, float key, int idx) {
+    const int o = b * K + rank;
+    a.score_out[o] = key;
+    a.tok_out[o] = idx % V;
+    a.bp_out[o] = idx / V;
+    if (a.row_out) a.row_out[o] = b * K + idx / V;
+  };
+  const int ns = wave_topk<4>(u, ix, (n + 63) / 64, K, qu[0], qi[0], emit_out);
+  if (lane >= ns && lane < K) {  // dead slots: hypothesis 0 continued with score -inf
+    const int o = b * K + lane;
+    a.score_out[o] = -INFINITY;
+    a.tok_out[o] = 0;
+    a.bp_out[o] = 0;
+    if (a.row_out) a.row_out[o] = b * K;
+  }
 }
 
 // Level 1 for a materialised logp: the best K keys score + logp[v] of one chunk of a row (at
@@ -511,6 +727,25 @@ static int kbucket(int K) { return K <= 1 ? 1 : K <= 2 ? 2 : K <= 4 ? 4 : K <= 8
 hipError_t launch_row_select(const RowSelect &a, hipStream_t st) {
   const int M = a.B * a.K;
   if (M == 0) return hipSuccess;
+  const bool fused = a.part != nullptr || a.comb != nullptr || a.nens > 0;
+  // One workgroup per sentence when a row's work is light: a materialised row's candidates
+  // (nl * cap of them) fit a wave's region, or a fused row has at most one list per lane.  The
+  // workgroups then occupy only B compute units, and with the vocabulary pass's lists of a
+  // large vocabulary (a few hundred per row, about one candidate each) the per-row form, over
+  // every unit, is faster despite its hand-off (17 against 23 us at B = 64, K = 12, V = 50k).
+  const bool light = fused ? a.nl <= 64 : (long)a.nl * a.cap <= kWaveCap;
+  const bool by_sentence = a.K >= 2 && a.K <= 16 && a.nl <= 64 * kSentLists &&
+                           (a.part == nullptr || a.ntiles <= 64 * kSentParts) && light;
+  if (by_sentence) {
+#define MT_SS(N)                                                                                        \
+  if (a.bf16_mma)                                                                                       \
+    hipLaunchKernelGGL((sentence_select_kernel<N, bf16>), dim3(a.B), dim3(64 * a.K), 0, st, a);         \
+  else                                                                                                  \
+    hipLaunchKernelGGL((sentence_select_kernel<N, float>), dim3(a.B), dim3(64 * a.K), 0, st, a);
+    MT_KSWITCH(a.K, MT_SS)
+#undef MT_SS
+    return hipGetLastError();
+  }
 #define MT_RS(N)                                                                          \
   if (a.bf16_mma)                                                                         \
     hipLaunchKernelGGL((row_select_kernel<N, bf16>), dim3(M), dim3(kTT), 0, st, a);       \
