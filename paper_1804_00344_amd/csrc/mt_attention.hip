@@ -162,6 +162,34 @@ __global__ __launch_bounds__(kAT) void attention_kernel(int B, int K, int S, int
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int ng = A / G;  // granules per P row
 
+  // ---- this lane's slice of q (scaled by 2/ln2) and va (scaled by -2): requested before the
+  // mask is read and used after it, so the two round trips overlap ----
+  float qr[NG][G], vr[NG][G];
+  int goff[NG];  // element offset of the lane's granule j in a P row (clamped)
+  float4 qraw[NG][G / 4], vraw[NG][G / 4];
+#pragma unroll
+  for (int j = 0; j < NG; ++j) {
+    const int g = j * 64 + lane;
+    goff[j] = (g < ng ? g : ng - 1) * G;
+#pragma unroll
+    for (int e = 0; e < G; e += 4) {
+      qraw[j][e / 4] = *(const float4 *)(q + (size_t)m * ldq + goff[j] + e);
+      vraw[j][e / 4] = *(const float4 *)(va + goff[j] + e);
+    }
+  }
+  // ---- the wave's first key rows, requested before the valid positions are known on the
+  // guess that they form a prefix (as padding does): rows wave + 4 d, clamped to the padded
+  // length; a row that is not the compacted position it stands for is loaded again below ----
+  typedef uint32_t v4u32 __attribute__((ext_vector_type(4)));
+  v4u32 ring[RD][NG];
+#pragma unroll
+  for (int d = 0; d < RD; ++d) {
+    const int i = wave + 4 * d < S ? wave + 4 * d : S - 1;
+    const char *row = (const char *)(P + ((size_t)b * S + i) * A);
+#pragma unroll
+    for (int jj = 0; jj < NG; ++jj) ring[d][jj] = *(const v4u32 *)(row + (size_t)goff[jj] * sizeof(T));
+  }
+
   // ---- compact the valid positions ----
   if (wave == 0) {
     const float *msk = mask + (size_t)b * S;
@@ -177,22 +205,15 @@ __global__ __launch_bounds__(kAT) void attention_kernel(int B, int K, int S, int
     if (lane == 0) nvalid = n;
   }
 
-  // ---- this lane's slice of q (scaled by 2/ln2) and va (scaled by -2) ----
-  float qr[NG][G], vr[NG][G];
-  int goff[NG];  // element offset of the lane's granule j in a P row (clamped)
   float vsum = 0.f;
 #pragma unroll
   for (int j = 0; j < NG; ++j) {
-    const int g = j * 64 + lane;
-    const bool ok = g < ng;
-    goff[j] = (ok ? g : ng - 1) * G;
+    const bool ok = j * 64 + lane < ng;
     float qv[G], vv[G];
 #pragma unroll
     for (int e = 0; e < G; e += 4) {
-      const float4 a = *(const float4 *)(q + (size_t)m * ldq + goff[j] + e);
-      const float4 w = *(const float4 *)(va + goff[j] + e);
-      qv[e] = a.x; qv[e + 1] = a.y; qv[e + 2] = a.z; qv[e + 3] = a.w;
-      vv[e] = w.x; vv[e + 1] = w.y; vv[e + 2] = w.z; vv[e + 3] = w.w;
+      __builtin_memcpy(qv + e, &qraw[j][e / 4], 16);
+      __builtin_memcpy(vv + e, &vraw[j][e / 4], 16);
     }
 #pragma unroll
     for (int e = 0; e < G; ++e) {
@@ -207,7 +228,6 @@ __global__ __launch_bounds__(kAT) void attention_kernel(int B, int K, int S, int
 
   // ---- scores: wave w takes positions w, w + 4, w + 8, ... through a two-deep ring of
   // raw P rows, so the next row's loads are in flight while the current one is scored ----
-  typedef uint32_t v4u32 __attribute__((ext_vector_type(4)));
   auto load_raw = [&](int jp, v4u32(&r)[NG]) {
     const int i = vidx[jp < n ? jp : 0];  // past the end: an in-range row, never scored
     const char *row = (const char *)(P + ((size_t)b * S + i) * A);
@@ -229,9 +249,9 @@ __global__ __launch_bounds__(kAT) void attention_kernel(int B, int K, int S, int
     return wave_sum(acc);
   };
   if (wave < n) {  // wave-uniform
-    v4u32 ring[RD][NG];
 #pragma unroll
-    for (int d = 0; d < RD; ++d) load_raw(wave + 4 * d, ring[d]);
+    for (int d = 0; d < RD; ++d)
+      if (wave + 4 * d < n && vidx[wave + 4 * d] != wave + 4 * d) load_raw(wave + 4 * d, ring[d]);
     int j = wave;
     bool go = true;
     while (go) {
