@@ -430,6 +430,38 @@ def test_candidate_buffer_overflow_falls_back_exactly():
         assert maxerr(lp[rows], orc[b]["logp"]) <= 1e-3
 
 
+@pytest.mark.parametrize("name", ["tiny_f32", "tiny_bf16_ln"])
+def test_equal_logits_overflow_in_sentence_selection(name):
+    """A zero output layer makes every logit of a row equal, so every vocabulary entry is a
+    candidate: the row's candidates exceed what one wave stages and the selection must fall back
+    to the exact recomputation.  At V = 2000 a row has at most 64 candidate lists, so the
+    selection runs one workgroup per sentence, whose fallback is the row's own wave.  Equal keys
+    rank by flat index: the K best of a sentence are the smallest tokens of its best previous
+    hypotheses, checked against the oracle's brute-force top-K of the GPU's log-probabilities."""
+    log(f"\n[equal-logit overflow] {name}")
+    p = synth.with_sizes(synth.PRESETS[name], V=2000, K=4, B=2)
+    w = synth.make_weights(p)
+    w["Wo"] = np.zeros_like(w["Wo"])
+    w["bo"] = np.zeros(p.V, np.float32)
+    dec = Decoder.from_preset(p, w)
+    ctx, mask, lens = synth.make_source(p)
+    dec.set_batch(ctx, mask, p.K)
+    dec.precompute()
+    tok, src, state, score = synth.mid_decode_inputs(p, salt=7)
+    n0 = mt.mt_recomputed_rows(dec.model)
+    gpu = run_step(dec, p, tok, src, T(state), p.M, attn=False, taps=False)
+    sc, tk, bp, _ = [x.cpu().numpy() for x in dec.topk(T(score), None)]
+    assert mt.mt_recomputed_rows(dec.model) - n0 == p.M  # every row fell back
+    lp = gpu["logp"].cpu().numpy()
+    assert np.all(lp == lp[:, :1])
+    t2, b2, s2 = mtref.topk(p.K, score, lp)
+    assert np.array_equal(tk, t2) and np.array_equal(bp, b2)
+    assert np.all(np.abs(sc.astype(np.float64) - s2) <= 1e-5 * (1.0 + np.abs(s2)))
+    # materialised keys through the same selection (its lists never overflow)
+    sc2, tk2, bp2, _ = [x.cpu().numpy() for x in dec.topk(T(score), gpu["logp"])]
+    assert np.array_equal(tk2, t2) and np.array_equal(bp2, b2) and np.array_equal(sc2, sc)
+
+
 # ------------------------------------------------------------------------------------------
 # ensembles: two members (different seeded weights) decode the same beam, each with its own
 # states; their log-probabilities are combined on the GPU and one selection extends the beam
