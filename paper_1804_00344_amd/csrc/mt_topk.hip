@@ -733,8 +733,11 @@ hipError_t launch_row_select(const RowSelect &a, hipStream_t st) {
   // workgroups then occupy only B compute units, and with the vocabulary pass's lists of a
   // large vocabulary (a few hundred per row, about one candidate each) the per-row form, over
   // every unit, is faster despite its hand-off (17 against 23 us at B = 64, K = 12, V = 50k).
-  const bool light = fused ? a.nl <= 64 : (long)a.nl * a.cap <= kWaveCap;
-  const bool by_sentence = a.K >= 2 && a.K <= 16 && a.nl <= 64 * kSentLists &&
+  // Materialised lists go by sentence at any K (K = 1: one wave per row, 6.0 against 7.8 us
+  // at B = 1024); fused lists of a large vocabulary keep the per-row form at K = 1 too (one
+  // wave per row, 11.9 against 9.8 us).
+  const bool light = fused ? a.K >= 2 && a.nl <= 64 : (long)a.nl * a.cap <= kWaveCap;
+  const bool by_sentence = a.K >= 1 && a.K <= 16 && a.nl <= 64 * kSentLists &&
                            (a.part == nullptr || a.ntiles <= 64 * kSentParts) && light;
   if (by_sentence) {
 #define MT_SS(N)                                                                                        \
