@@ -345,9 +345,10 @@ __global__ __launch_bounds__(kTT) void row_select_kernel(RowSelect a) {
 // count and loads, three round trips past the L2).  Wave k takes row b*K + k: it requests the
 // row's log-sum-exp partials, list fill counts and first kSpec entries of its lists together,
 // merges the log-sum-exp (wave_row_lse), stages the row's candidates in its own LDS region
-// (ballot-free offsets from a wave prefix sum), selects the K best exactly (wave_topk) into the
-// sentence table, and after one barrier the table is ranked (sentence_rank).  A row whose lists
-// overflow, or whose candidates exceed its region, is recomputed exactly by its own wave.
+// (offsets from a DPP prefix sum), selects the K best exactly (wave_topk) into the sentence's
+// K x K table in LDS, and after one barrier wave 0 selects the sentence's K best of the table
+// (wave_topk again, in sentence_rank's order).  A row whose lists overflow, or whose candidates
+// exceed its region, is recomputed exactly by its own wave.
 constexpr int kWaveCap = 1024;    // candidates one row's wave can stage
 constexpr int kSentLists = 8;     // lists per lane: nl <= 512
 constexpr int kSentParts = 4;     // partials per lane: ntiles <= 256
