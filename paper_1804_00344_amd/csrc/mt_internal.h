@@ -5,6 +5,8 @@
 #include <stdint.h>
 #include <stddef.h>
 
+#include <type_traits>
+
 #include "../../include/mtstep.h"
 
 namespace mt {
@@ -77,6 +79,21 @@ __device__ __forceinline__ int wave_incl_scan(int v) {
   v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xA, 0xF, false);  // row_bcast:15 -> rows 1, 3
   v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xC, 0xF, false);  // row_bcast:31 -> rows 2, 3
   return v;
+}
+// Integer minimum / maximum over the wave (every lane active), the same DPP pattern
+template <typename I, bool MAX>
+__device__ __forceinline__ I wave_ext(I v) {
+  auto pick = [](I x, I y) { return MAX ? (x > y ? x : y) : (x < y ? x : y); };
+  auto mov = [](I x, auto ctrl) {
+    return (I)__builtin_amdgcn_mov_dpp((int)x, decltype(ctrl)::value, 0xF, 0xF, false);
+  };
+  v = pick(v, mov(v, std::integral_constant<int, kDppQuadSwap1>()));
+  v = pick(v, mov(v, std::integral_constant<int, kDppQuadSwap2>()));
+  v = pick(v, mov(v, std::integral_constant<int, kDppRowRor4>()));
+  v = pick(v, mov(v, std::integral_constant<int, kDppRowRor8>()));
+  const I r0 = (I)__builtin_amdgcn_readlane((int)v, 0), r1 = (I)__builtin_amdgcn_readlane((int)v, 16);
+  const I r2 = (I)__builtin_amdgcn_readlane((int)v, 32), r3 = (I)__builtin_amdgcn_readlane((int)v, 48);
+  return pick(pick(r0, r1), pick(r2, r3));
 }
 __device__ __forceinline__ float wave_max(float v) {
   v = fmaxf(v, dpp_mov<kDppQuadSwap1>(v));
@@ -252,14 +269,8 @@ __device__ __forceinline__ uint32_t wave_kth_code(const uint32_t (&u)[R], int rs
       lo = u[s] < lo ? u[s] : lo;
       hi = u[s] > hi ? u[s] : hi;
     }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const uint32_t a = __shfl_xor(lo, o, 64), b = __shfl_xor(hi, o, 64);
-    lo = a < lo ? a : lo;
-    hi = b > hi ? b : hi;
-  }
-  lo = __builtin_amdgcn_readfirstlane(lo);
-  hi = __builtin_amdgcn_readfirstlane(hi);
+  lo = wave_ext<uint32_t, false>(lo);
+  hi = wave_ext<uint32_t, true>(hi);
   while (lo < hi) {  // invariant: count(>= lo) >= K, count(>= hi + 1) < K
     const uint32_t mid = lo + (uint32_t)(((uint64_t)hi - lo + 1u) >> 1);
     if (wave_count_ge<R>(u, rs, mid) >= K)
@@ -295,14 +306,8 @@ __device__ __forceinline__ int wave_topk(const uint32_t (&u)[R], const int (&ix)
           lo = ix[s] < lo ? ix[s] : lo;
           hi = ix[s] > hi ? ix[s] : hi;
         }
-#pragma unroll
-      for (int o = 32; o > 0; o >>= 1) {
-        const int a = __shfl_xor(lo, o, 64), b = __shfl_xor(hi, o, 64);
-        lo = a < lo ? a : lo;
-        hi = b > hi ? b : hi;
-      }
-      lo = __builtin_amdgcn_readfirstlane(lo);
-      hi = __builtin_amdgcn_readfirstlane(hi);
+      lo = wave_ext<int, false>(lo);
+      hi = wave_ext<int, true>(hi);
       while (lo < hi) {  // smallest i with count(code == tau, idx <= i) >= need
         const int mid = (int)(((int64_t)lo + hi) >> 1);
         if (wave_count_eq_le<R>(u, ix, rs, tau, mid) >= need)

@@ -43,13 +43,16 @@ __device__ __forceinline__ int2 get_row(const int2 *p) {
 }
 
 // Level 3 for one sentence: the K best of the K x K row results, held as a table of (key code,
-// flat index) with candidate (k, j) at k*K + j and flat index k*V + token.  Every candidate
-// counts the candidates that beat it (larger key code, or equal code and smaller index);
-// entries without a token get distinct indices above every real one, so the counts are a
-// permutation of 0..K*K-1 and the K candidates with counts below K write themselves to their
-// rank.  Entries without a token that rank below K are dead slots (fewer than K real
-// candidates): they continue hypothesis 0 with score -inf.  The table is padded to whole
-// groups of four with entries that beat nothing; threads 0..K*K-1 rank.
+// flat index) with candidate (k, j) at k*K + j and flat index k*V + token; entries without a
+// token have code 0 and distinct indices above every real one.  The order: larger key code
+// first, equal codes by smaller flat index; ranks past the real entries (fewer than K) are dead
+// slots: hypothesis 0 continued with score -inf.  Two forms, chosen by the table's size:
+// sentence_rank (K*K <= 64), in which every entry counts the entries that beat it (16-byte LDS
+// reads of a table padded to whole groups of four with entries that beat nothing), so the
+// counts are a permutation and the K entries below K write themselves to their rank; and
+// sentence_select_wave (larger tables), one wave's exact selection by bisection (wave_topk),
+// whose cost grows with the slots per lane, not with the table's square.
+constexpr int kRankMax = 64;  // tables up to this size are ranked by counting
 __device__ __forceinline__ void sentence_rank(const RowSelect &a, int b, const uint32_t *su, const int *si) {
   const int t = threadIdx.x, K = a.K, V = a.V;
   const int n = K * K;
@@ -83,14 +86,47 @@ __device__ __forceinline__ void sentence_rank(const RowSelect &a, int b, const u
     if (a.row_out) a.row_out[o] = b * K;
   }
 }
+
+// One wave (every lane active): the table's K*K <= 256 entries in four register slots, entries
+// without a token empty; qu/qi: K entries of wave-private LDS scratch.
+__device__ __forceinline__ void sentence_select_wave(const RowSelect &a, int b, const uint32_t *su, const int *si,
+                                                     uint32_t *qu, int *qi) {
+  const int lane = threadIdx.x & 63, K = a.K, V = a.V;
+  const int n = K * K;
+  uint32_t u[4];
+  int ix[4];
+#pragma unroll
+  for (int s2 = 0; s2 < 4; ++s2) {
+    const int j = s2 * 64 + lane;
+    u[s2] = j < n ? su[j] : 0u;
+    ix[s2] = j < n ? si[j] : 0x7fffffff;
+  }
+  auto emit_out = [&](int rank, float key, int idx) {
+    const int o = b * K + rank;
+    a.score_out[o] = key;
+    a.tok_out[o] = idx % V;
+    a.bp_out[o] = idx / V;
+    if (a.row_out) a.row_out[o] = b * K + idx / V;
+  };
+  const int ns = wave_topk<4>(u, ix, (n + 63) / 64, K, qu, qi, emit_out);
+  if (lane >= ns && lane < K) {  // dead slots: hypothesis 0 continued with score -inf
+    const int o = b * K + lane;
+    a.score_out[o] = -INFINITY;
+    a.tok_out[o] = 0;
+    a.bp_out[o] = 0;
+    if (a.row_out) a.row_out[o] = b * K;
+  }
+}
 // Entry t of the table from the row candidates (key bits, token) of row k = t / K
 __device__ __forceinline__ void table_entry(int t, int K, int V, float key, int tok, uint32_t *su, int *si) {
   const bool real = tok >= 0 && tok < V;
   su[t] = real ? key_code(key) : 0u;
   si[t] = real ? (t / K) * V + tok : K * V + t;
 }
-// The table from the row results of row_cand [M][K] (key bits, token), by the whole workgroup
-__device__ __forceinline__ void sentence_merge(const RowSelect &a, int b, uint32_t *su, int *si) {
+// The table from the row results of row_cand [M][K] (key bits, token), read by the whole
+// workgroup; its first wave selects
+__device__ __forceinline__ void sentence_merge(const RowSelect &a, int b, uint32_t *su, int *si, uint32_t *qu,
+                                               int *qi) {
   const int t = threadIdx.x, K = a.K, V = a.V;
   const int n = K * K;  // <= 256: K <= 16
   const int n4 = (n + 3) / 4;
@@ -102,7 +138,10 @@ __device__ __forceinline__ void sentence_merge(const RowSelect &a, int b, uint32
     si[t] = 0x7fffffff;
   }
   __syncthreads();
-  sentence_rank(a, b, su, si);
+  if (n <= kRankMax)
+    sentence_rank(a, b, su, si);
+  else if (t < 64)
+    sentence_select_wave(a, b, su, si, qu, qi);
 }
 
 // The K best keys prev + x[v] of one stored row x [V] (a fused ensemble's combined values),
@@ -335,7 +374,7 @@ __global__ __launch_bounds__(kTT) void row_select_kernel(RowSelect a) {
   if (t == 0) last = __hip_atomic_fetch_add(a.scnt + b, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == K - 1;
   __syncthreads();
   if (!last) return;
-  sentence_merge(a, b, su, si);
+  sentence_merge(a, b, su, si, qu[0], qi[0]);
   if (t == 0) __hip_atomic_store(a.scnt + b, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
@@ -347,7 +386,7 @@ __global__ __launch_bounds__(kTT) void row_select_kernel(RowSelect a) {
 // merges the log-sum-exp (wave_row_lse), stages the row's candidates in its own LDS region
 // (offsets from a DPP prefix sum), selects the K best exactly (wave_topk) into the sentence's
 // K x K table in LDS, and after one barrier wave 0 selects the sentence's K best of the table
-// (wave_topk again, in sentence_rank's order).  A row whose lists overflow, or whose candidates
+// (sentence_select_wave).  A row whose lists overflow, or whose candidates
 // exceed its region, is recomputed exactly by its own wave.
 constexpr int kWaveCap = 1024;    // candidates one row's wave can stage
 constexpr int kSentLists = 8;     // lists per lane: nl <= 512
@@ -359,8 +398,8 @@ __global__ __launch_bounds__(64 * KMAX) void sentence_select_kernel(RowSelect a)
   __shared__ __attribute__((aligned(16))) int si[KMAX][kWaveCap];
   __shared__ uint32_t qu[KMAX][KMAX];
   __shared__ int qi[KMAX][KMAX];
-  __shared__ uint32_t tu[KMAX * KMAX];
-  __shared__ int ti[KMAX * KMAX];
+  __shared__ __attribute__((aligned(16))) uint32_t tu[KMAX * KMAX + 4];
+  __shared__ __attribute__((aligned(16))) int ti[KMAX * KMAX + 4];
   const int b = blockIdx.x, lane = threadIdx.x & 63;
   const int k = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int K = a.K, V = a.V, nl = a.nl, cap = a.cap;
@@ -508,33 +547,19 @@ __global__ __launch_bounds__(64 * KMAX) void sentence_select_kernel(RowSelect a)
       if (lane >= ns && lane < K) emit_tab(lane, -INFINITY, 0x7fffffff);
     }
   }
-  __syncthreads();
-  // ---- level 3 by wave 0: the K best of the K x K table (the order of sentence_rank: key code,
-  // then flat index; entries without a token are empty slots and rank below every real one) ----
-  if (k != 0) return;
-  const int n = K * K;  // <= 256
-  uint32_t u[4];
-  int ix[4];
-#pragma unroll
-  for (int s2 = 0; s2 < 4; ++s2) {
-    const int j = s2 * 64 + lane;
-    u[s2] = j < n ? tu[j] : 0u;
-    ix[s2] = j < n ? ti[j] : 0x7fffffff;
+  {  // padding of the table to whole groups of four (entries that beat nothing)
+    const int t = threadIdx.x, n = K * K;
+    if (t >= n && t < 4 * ((n + 3) / 4)) {
+      tu[t] = 0u;
+      ti[t] = 0x7fffffff;
+    }
   }
-  auto emit_out = [&](int rank, float key, int idx) {
-    const int o = b * K + rank;
-    a.score_out[o] = key;
-    a.tok_out[o] = idx % V;
-    a.bp_out[o] = idx / V;
-    if (a.row_out) a.row_out[o] = b * K + idx / V;
-  };
-  const int ns = wave_topk<4>(u, ix, (n + 63) / 64, K, qu[0], qi[0], emit_out);
-  if (lane >= ns && lane < K) {  // dead slots: hypothesis 0 continued with score -inf
-    const int o = b * K + lane;
-    a.score_out[o] = -INFINITY;
-    a.tok_out[o] = 0;
-    a.bp_out[o] = 0;
-    if (a.row_out) a.row_out[o] = b * K;
+  __syncthreads();
+  // ---- level 3: the K best of the K x K table ----
+  if (K * K <= kRankMax) {
+    sentence_rank(a, b, tu, ti);
+  } else if (k == 0) {
+    sentence_select_wave(a, b, tu, ti, qu[0], qi[0]);
   }
 }
 
