@@ -324,6 +324,23 @@ __global__ __launch_bounds__(kTT) void row_select_kernel(RowSelect a) {
             u[s] = ok ? su[j] : 0u;
             ix[s] = ok ? si[j] : 0x7fffffff;
           }
+          if (K == 1) {  // the best entry only: a DPP maximum of the codes, then of the indices
+            uint32_t bu = 0u;
+            int bi = 0x7fffffff;
+#pragma unroll
+            for (int s = 0; s < R; ++s)
+              if (u[s] > bu || (u[s] == bu && ix[s] < bi)) {
+                bu = u[s];
+                bi = ix[s];
+              }
+            const uint32_t mu = wave_ext<uint32_t, true>(bu);
+            const int mi = wave_ext<int, false>(bu == mu ? bi : 0x7fffffff);
+            if (lane == 0) {
+              qu[w][0] = mu;
+              qi[w][0] = mi;
+            }
+            return mu != 0u ? 1 : 0;
+          }
           return wave_topk<R>(u, ix, rs, K, qu[w], qi[w], [](int, float, int) {});
         };
         int ns;
@@ -350,8 +367,19 @@ __global__ __launch_bounds__(kTT) void row_select_kernel(RowSelect a) {
         }
         uint32_t u[1] = {src >= 0 ? qu[src][r] : 0u};
         int ix[1] = {src >= 0 ? qi[src][r] : 0x7fffffff};
-        const int ns = wave_topk<1>(u, ix, 1, K, su, si, emit_row);
-        if (lane >= ns && lane < K) emit_row(lane, -INFINITY, 0x7fffffff);
+        if (K == 1) {  // the best of the four quarters' best
+          const uint32_t mu = wave_ext<uint32_t, true>(u[0]);
+          const int mi = wave_ext<int, false>(u[0] == mu ? ix[0] : 0x7fffffff);
+          if (lane == 0) {
+            if (mu != 0u)
+              emit_row(0, key_from_code(mu), mi);
+            else
+              emit_row(0, -INFINITY, 0x7fffffff);
+          }
+        } else {
+          const int ns = wave_topk<1>(u, ix, 1, K, su, si, emit_row);
+          if (lane >= ns && lane < K) emit_row(lane, -INFINITY, 0x7fffffff);
+        }
       }
     }
   }
