@@ -354,6 +354,58 @@ __device__ __forceinline__ int wave_topk(const uint32_t (&u)[R], const int (&ix)
   return ns;
 }
 
+// The same selection by K rounds of a wave maximum (for small K): each round takes the best
+// remaining entry (DPP maxima of the lanes' best codes, then of their indices among equal
+// codes) and its owner clears it, so the entries come out in rank order and nothing is
+// counted.  Lane j < n_sel writes entry j to scratch (su, si) and calls emit(j, key, idx).
+// Returns n_sel = min(K, entries) (wave-uniform).  Indices must be distinct.
+template <int R, typename Emit>
+__device__ __forceinline__ int wave_topk_rounds(uint32_t (&u)[R], const int (&ix)[R], int rs, int K,
+                                                uint32_t *su, int *si, Emit emit) {
+  const int lane = threadIdx.x & 63;
+  uint32_t my_u = 0u;
+  int my_i = 0x7fffffff;
+  int ns = 0;
+  for (int r = 0; r < K; ++r) {
+    uint32_t bu = 0u;
+    int bi = 0x7fffffff;
+#pragma unroll
+    for (int s = 0; s < R; ++s)
+      if (s < rs && (u[s] > bu || (u[s] == bu && ix[s] < bi))) {
+        bu = u[s];
+        bi = ix[s];
+      }
+    const uint32_t mu = wave_ext<uint32_t, true>(bu);
+    if (mu == 0u) break;  // no entries left (wave-uniform)
+    const int mi = wave_ext<int, false>(bu == mu ? bi : 0x7fffffff);
+#pragma unroll
+    for (int s = 0; s < R; ++s)
+      if (u[s] == mu && ix[s] == mi) u[s] = 0u;
+    if (lane == r) {
+      my_u = mu;
+      my_i = mi;
+    }
+    ns = r + 1;
+  }
+  if (lane < ns) {
+    su[lane] = my_u;
+    si[lane] = my_i;
+    emit(lane, key_from_code(my_u), my_i);
+  }
+  return ns;
+}
+
+// K best of a wave's entries by whichever form is cheaper: K rounds of a wave maximum for
+// K <= 6, the bisection above that (at K = 12 the rounds cost 3 us more per selection, at
+// K = 5 they save 1 us; kernel traces of the beam selection).
+constexpr int kRoundsMaxK = 6;
+template <int R, typename Emit>
+__device__ __forceinline__ int wave_select(uint32_t (&u)[R], const int (&ix)[R], int rs, int K, uint32_t *su,
+                                           int *si, Emit emit) {
+  if (K <= kRoundsMaxK) return wave_topk_rounds<R>(u, ix, rs, K, su, si, emit);
+  return wave_topk<R>(u, ix, rs, K, su, si, emit);
+}
+
 // ---- row-level pieces shared by the log-sum-exp pass and the beam selection ----
 
 // Log-sum-exp of one row from its per-chunk partials (m_c, s_c), s_c = sum of exp(logit - m_c)

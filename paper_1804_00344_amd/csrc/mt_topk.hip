@@ -108,7 +108,7 @@ __device__ __forceinline__ void sentence_select_wave(const RowSelect &a, int b, 
     a.bp_out[o] = idx / V;
     if (a.row_out) a.row_out[o] = b * K + idx / V;
   };
-  const int ns = wave_topk<4>(u, ix, (n + 63) / 64, K, qu, qi, emit_out);
+  const int ns = wave_select<4>(u, ix, (n + 63) / 64, K, qu, qi, emit_out);
   if (lane >= ns && lane < K) {  // dead slots: hypothesis 0 continued with score -inf
     const int o = b * K + lane;
     a.score_out[o] = -INFINITY;
@@ -341,7 +341,7 @@ __global__ __launch_bounds__(kTT) void row_select_kernel(RowSelect a) {
             }
             return mu != 0u ? 1 : 0;
           }
-          return wave_topk<R>(u, ix, rs, K, qu[w], qi[w], [](int, float, int) {});
+          return wave_select<R>(u, ix, rs, K, qu[w], qi[w], [](int, float, int) {});
         };
         int ns;
         if (rs <= 2)
@@ -377,7 +377,7 @@ __global__ __launch_bounds__(kTT) void row_select_kernel(RowSelect a) {
               emit_row(0, -INFINITY, 0x7fffffff);
           }
         } else {
-          const int ns = wave_topk<1>(u, ix, 1, K, su, si, emit_row);
+          const int ns = wave_select<1>(u, ix, 1, K, su, si, emit_row);
           if (lane >= ns && lane < K) emit_row(lane, -INFINITY, 0x7fffffff);
         }
       }
@@ -561,7 +561,7 @@ __global__ __launch_bounds__(64 * KMAX) void sentence_select_kernel(RowSelect a)
           u[s2] = ok ? wu[j] : 0u;
           ix[s2] = ok ? wi[j] : 0x7fffffff;
         }
-        return wave_topk<R>(u, ix, rs, K, qu[k], qi[k], emit_tab);
+        return wave_select<R>(u, ix, rs, K, qu[k], qi[k], emit_tab);
       };
       int ns;
       if (rs <= 2)
