@@ -188,8 +188,8 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(decoding shards by sentence with no exchange; see the design notes)", file=sys.stderr)
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
+              "(decoding would shard by sentence, with no exchange between GPUs)", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
