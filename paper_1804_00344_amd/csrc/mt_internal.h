@@ -294,10 +294,37 @@ __device__ __forceinline__ int wave_topk(const uint32_t (&u)[R], const int (&ix)
   uint32_t tau = 1u;
   int iota = 0x7fffffff;
   if (n > K) {
-    tau = wave_kth_code<R>(u, rs, K);
-    const int gt = tau == 0xffffffffu ? 0 : wave_count_ge<R>(u, rs, tau + 1u);
+    // The cut: the bisection of wave_kth_code, stopped as soon as a midpoint has exactly K
+    // entries at or above it (then those K are the selection; with distinct keys that takes
+    // about log2 of the entry count steps instead of one per bit of the codes' spread).
+    // Otherwise it runs to the K-th largest code and the ties there are resolved below.
+    uint32_t lo = 0xffffffffu, hi = 0u;
+#pragma unroll
+    for (int s = 0; s < R; ++s)
+      if (s < rs && u[s] != 0u) {
+        lo = u[s] < lo ? u[s] : lo;
+        hi = u[s] > hi ? u[s] : hi;
+      }
+    lo = wave_ext<uint32_t, false>(lo);
+    hi = wave_ext<uint32_t, true>(hi);
+    bool exact = false;
+    while (lo < hi) {  // invariant: count(>= lo) >= K, count(>= hi + 1) < K
+      const uint32_t mid = lo + (uint32_t)(((uint64_t)hi - lo + 1u) >> 1);
+      const int c = wave_count_ge<R>(u, rs, mid);
+      if (c == K) {
+        lo = mid;
+        exact = true;
+        break;
+      }
+      if (c > K)
+        lo = mid;
+      else
+        hi = mid - 1u;
+    }
+    tau = lo;
+    const int gt = exact ? K : tau == 0xffffffffu ? 0 : wave_count_ge<R>(u, rs, tau + 1u);
     const int need = K - gt;
-    const int eq = wave_count_eq_le<R>(u, ix, rs, tau, 0x7fffffff);
+    const int eq = exact ? 0 : wave_count_eq_le<R>(u, ix, rs, tau, 0x7fffffff);
     if (eq > need) {  // ties at the cut: keep the `need` smallest indices among them
       int lo = 0x7fffffff, hi = (int)0x80000000;
 #pragma unroll
