@@ -283,17 +283,33 @@ __global__ __launch_bounds__(kTT) void row_select_kernel(RowSelect a) {
         si[pos] = tok;
       };
       if (pre) {
+        // the first kSpec entries were loaded with the counts; of a longer list the next four
+        // are requested together (one more round trip, not one per entry), the rest one by one
+        int lo[2], lc[2];
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
           const int l = t + j * kTT;
-          if (l >= nl) continue;
-          const int c = pc[j] < cap ? pc[j] : cap;
-          const int2 *e = a.cbuf + (size_t)m * cap * nl + l;
+          const int c = l < nl ? (pc[j] < cap ? pc[j] : cap) : 0;
+          lo[j] = off;
+          lc[j] = c;
 #pragma unroll
           for (int q = 0; q < kSpec; ++q)
             if (q < c) stage(off + q, pe[j][q]);
-          for (int q = kSpec; q < c; ++q) stage(off + q, e[(size_t)q * nl]);  // long lists (rare)
           off += c;
+        }
+        int2 ex[2][4];
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int q2 = 0; q2 < 4; ++q2)
+            if (kSpec + q2 < lc[j]) ex[j][q2] = a.cbuf[(size_t)m * cap * nl + t + j * kTT + (size_t)(kSpec + q2) * nl];
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+#pragma unroll
+          for (int q2 = 0; q2 < 4; ++q2)
+            if (kSpec + q2 < lc[j]) stage(lo[j] + kSpec + q2, ex[j][q2]);
+          for (int q = kSpec + 4; q < lc[j]; ++q)  // (rarer still)
+            stage(lo[j] + q, a.cbuf[(size_t)m * cap * nl + t + j * kTT + (size_t)q * nl]);
         }
       } else {
         for (int l = t; l < nl; l += kTT) {
